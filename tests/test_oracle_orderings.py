@@ -1,0 +1,161 @@
+"""Pins for the oracle's orderings (Alg. 2, Alg. 3) against the eager definition.
+
+The paper states that forward- and backward-fusion only reorder the same
+updates and leave the optimizer algorithm and the training result unchanged.
+In float64 with identical per-element arithmetic that means bit-identical
+parameters, histories, losses and counters.
+"""
+import numpy as np
+import pytest
+
+from oracle import run, new_model
+from oracle import layers as L
+from workloads import get_config, reduced_config
+
+CASES = ["mlp3", "mlp8x1024", "linear4x8192", "tblock12", "vgg11"]
+
+
+def _same(a, b):
+    for k in ("params", "m", "v"):
+        assert a[k].keys() == b[k].keys()
+        for n in a[k]:
+            np.testing.assert_array_equal(a[k][n], b[k][n], err_msg=f"{k}[{n}]")
+    np.testing.assert_array_equal(a["losses"], b["losses"])
+    assert a["eval_loss"] == b["eval_loss"]
+    assert a["step"] == b["step"]
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_orderings_bit_identical(name):
+    cfg = reduced_config(name)
+    e = run(cfg, "eager")
+    f = run(cfg, "ff")
+    b = run(cfg, "bf")
+    _same(e, f)
+    _same(e, b)
+    K = cfg["steps"]
+    assert all(s == K for s in e["step"].values())
+    assert all(c == 0 for c in b["count"].values())
+    # FF: every node that ran backward holds a pending update until the flush.
+    assert not any(f["updated_before_flush"])
+    assert all(f["updated"])
+    # Training moved the parameters and the loss is finite.
+    assert np.all(np.isfinite(e["losses"]))
+    init = new_model(cfg).params
+    assert any(np.any(e["params"][k] != init[k].value) for k in init)
+
+
+def test_full_size_mlp3_orderings():
+    cfg = get_config("mlp3")
+    e, f, b = run(cfg, "eager"), run(cfg, "ff"), run(cfg, "bf")
+    _same(e, f)
+    _same(e, b)
+    assert len(e["losses"]) == 5
+
+
+@pytest.mark.parametrize("name", ["mlp3", "vgg11", "tblock12"])
+def test_planted_dependency_violation_is_caught(name):
+    """Updating theta before the input gradient is computed (against the rule after
+    Alg. 3) must change the result: the invariant test can see the race."""
+    cfg = reduced_config(name)
+    e = run(cfg, "eager")
+    bad = run(cfg, "bf", race_bug=True)
+    # NaN (a diverged wrong run) counts as a difference too.
+    assert any(np.any(~(np.abs(e["params"][k] - bad["params"][k]) <= 1e-6)) for k in e["params"])
+
+
+def _shared_model(cfg):
+    """x -> A -> relu -> B -> relu -> A (same operator again) -> relu -> C: A is used twice."""
+    rng = np.random.default_rng(11)
+    d = 12
+    A = L.Linear(L.Param("A.w", rng.uniform(-0.5, 0.5, (d, d))), L.Param("A.b", np.zeros(d)))
+    B = L.Linear(L.Param("B.w", rng.uniform(-0.5, 0.5, (d, d))), L.Param("B.b", np.zeros(d)))
+    C = L.Linear(L.Param("C.w", rng.uniform(-0.5, 0.5, (4, d))), None)
+    nodes = [(A, ["input"], "a1"), (L.ReLU(), ["a1"], "r1"), (B, ["r1"], "b"),
+             (L.ReLU(), ["b"], "r2"), (A, ["r2"], "a2"), (L.ReLU(), ["a2"], "r3"),
+             (C, ["r3"], "output")]
+    params = {p.name: p for op in (A, B, C) for p in op.params}
+    from oracle.run import Model
+    return Model(nodes, params, "xent", cfg["opt"]), A
+
+
+@pytest.mark.parametrize("opt", ["sgd", "adam"])
+def test_shared_operator_updated_once_per_step(opt):
+    cfg = get_config("mlp3" if opt == "sgd" else "mlp8x1024")
+    rng = np.random.default_rng(12)
+    batches = [(rng.standard_normal((6, 12)), rng.integers(0, 4, 6)) for _ in range(4)]
+    results = {}
+    for ordering in ("eager", "ff", "bf"):
+        model, A = _shared_model(cfg)
+        losses = []
+        for x, y in batches:
+            if ordering == "eager":
+                losses.append(model.step_eager(x, y))
+            elif ordering == "ff":
+                losses.append(model.step_ff(x, y))
+                assert A.updated is False
+            else:
+                losses.append(model.step_bf(x, y))
+                assert all(p.count == 0 for p in model.params.values())
+        if ordering == "ff":
+            model.flush()
+        assert all(p.step == len(batches) for p in model.params.values())
+        results[ordering] = (losses, {k: p.value.copy() for k, p in model.params.items()})
+    for ordering in ("ff", "bf"):
+        assert results[ordering][0] == results["eager"][0]
+        for k, v in results["eager"][1].items():
+            np.testing.assert_array_equal(results[ordering][1][k], v)
+
+
+def test_bf_counts_forward_uses():
+    cfg = get_config("mlp3")
+    model, A = _shared_model(cfg)
+    x, y = np.ones((2, 12)), np.array([0, 1])
+    out, _ = model.forward(x, before_node=lambda op: [setattr(p, "count", p.count + 1)
+                                                      for p in op.params])
+    assert A.w.count == 2 and model.params["B.w"].count == 1
+
+
+def test_ff_first_iteration_applies_nothing():
+    cfg = reduced_config("mlp3")
+    model = new_model(cfg)
+    before = {k: p.value.copy() for k, p in model.params.items()}
+    x = np.random.default_rng(0).standard_normal((32, 64))
+    y = np.zeros(32, dtype=np.int64)
+    model.step_ff(x, y)
+    for k, p in model.params.items():
+        np.testing.assert_array_equal(p.value, before[k])
+        assert p.step == 0 and p.grad is not None
+
+
+@pytest.mark.parametrize("name,over", [
+    ("mlp3", dict(dims=[5, 7, 6, 4], batch=3, classes=4)),
+    ("linear4x8192", dict(dims=[6] * 5, batch=3)),
+    ("tblock12", dict(blocks=2, hidden=6, ffn=10, batch=4, dtype="f32")),
+    ("vgg11", dict(channels=[3, 4, 4, 4, 5, 5, 5, 5], batch=2)),
+])
+def test_whole_model_gradient_finite_differences(name, over):
+    """Backward through the whole graph (wiring, residuals, pooling, loss) vs float64
+    central differences of the training loss, for every parameter element."""
+    cfg = reduced_config(name, **over)
+    from workloads import make_batch
+    model = new_model(cfg)
+    x, y = make_batch(cfg, 1)
+    x = x.astype(np.float64)
+    y = y if y.dtype == np.int64 else y.astype(np.float64)
+    out, tape = model.forward(x)
+    _, dout = model.loss_and_grad(out, y)
+    model.backward(tape, dout)
+    h = 1e-6
+    rng = np.random.default_rng(0)
+    for p in model.params.values():
+        flat = p.value.reshape(-1)
+        for i in rng.choice(flat.size, size=min(flat.size, 6), replace=False):
+            old = flat[i]
+            flat[i] = old + h
+            lp = model.loss_and_grad(model.forward(x)[0], y)[0]
+            flat[i] = old - h
+            lm = model.loss_and_grad(model.forward(x)[0], y)[0]
+            flat[i] = old
+            num = (lp - lm) / (2 * h)
+            assert p.grad.reshape(-1)[i] == pytest.approx(num, rel=1e-5, abs=1e-8), p.name
