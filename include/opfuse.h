@@ -1,0 +1,276 @@
+/*
+ * opfuse.h -- optimizer fusion on AMD Instinct MI355X (gfx950), C ABI.
+ *
+ * Implements the hot path of "Optimizer Fusion: Efficient Training with Better
+ * Locality and Parallelism" (Jiang et al., arXiv 2104.00237):
+ *
+ *   - backward-fusion (Section 3 "Backward-Fusion", Appendix B.2, Alg. 3): the
+ *     weight-gradient contraction dW = dZ^T X applies the optimizer to W and
+ *     its history in its epilogue; dW is never written to memory;
+ *   - forward-fusion (Section 3 "Forward-Fusion", Appendix B.1, Alg. 2): the
+ *     pending update is applied while the next forward contraction loads its
+ *     W tiles; the updated tile is written back and fed to the matrix cores;
+ *   - the eager three-stage path (Section 1, Fig. 1(b)): forward, backward
+ *     writing every gradient, then one multi-tensor optimizer launch.
+ *
+ * Conventions for every entry point:
+ *   - Pointers named x, y, w, ... are DEVICE pointers owned by the caller.
+ *     The library never allocates, frees or retains them after returning.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t passed as
+ *     void*; NULL is the null stream).  Device faults surface at the caller's
+ *     next synchronisation.
+ *   - Arguments are validated synchronously before any HIP call; on failure
+ *     nothing is enqueued and a status other than OF_OK is returned, with a
+ *     message in of_last_error() (thread-local).
+ *   - Layouts are row-major.  A linear layer has X [M,K] (row stride ldx),
+ *     W [N,K], bias [N], Z/Y [M,N] (row stride ldy).  A convolution has NHWC
+ *     activations and [Cout,3,3,Cin] filters.
+ *   - Any size is accepted (ragged tails are masked); 128-bit memory paths are
+ *     used when a pointer is 16-byte aligned and its row stride is a multiple
+ *     of 4 elements.  fp32 pointers must be 4-byte aligned (else OF_EALIGN).
+ *   - Entry points that take a workspace need at least the bytes the matching
+ *     *_workspace_size query returns (else OF_EWORKSPACE).  The workspace holds
+ *     split-reduction partials only; it needs no initialisation and may be
+ *     reused by later calls on the same stream.
+ *   - Calls that touch the same parameter on different streams race unless the
+ *     caller orders them (except inside of_linear_bwd_fused, see there).
+ */
+#ifndef OPFUSE_H
+#define OPFUSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OF_VERSION 1
+
+typedef enum of_status {
+  OF_OK = 0,
+  OF_EINVAL = 1,        /* null required pointer, non-positive size, bad enum, step < 1 */
+  OF_EUNSUPPORTED = 2,  /* valid but unsupported combination (dtype / activation / shape) */
+  OF_EALIGN = 3,        /* pointer not aligned to its element size */
+  OF_EWORKSPACE = 4,    /* workspace smaller than the query returns */
+  OF_EHIP = 5           /* a HIP launch failed; of_last_error() has the HIP error text */
+} of_status;
+
+typedef enum of_dtype { OF_F32 = 0, OF_BF16 = 1 } of_dtype;
+
+/* Activation applied to Z in a forward epilogue; its derivative is applied
+ * in the dgrad epilogue of the NEXT layer (see of_linear_bwd_data). */
+typedef enum of_act { OF_ACT_NONE = 0, OF_ACT_RELU = 1, OF_ACT_GELU = 2 } of_act;
+
+/*
+ * Optimizer policy pi (Appendix A, Alg. 1).  `step` is the 1-based index t of
+ * the update being applied; the caller owns and increments it.  Bias
+ * corrections 1 - beta^t are computed by the library on the host in float64.
+ *
+ *   OF_OPT_SGD    momentum (Appendix A, Eq. for pi_2) with coupled weight decay:
+ *                   g' = g + wd*w;  m = momentum*m + g';  w -= lr*m
+ *                 (m starts at 0, dampening 0, no Nesterov; momentum 0 is pi_1)
+ *   OF_OPT_ADAM   Adam with coupled L2 weight decay g' = g + wd*w:
+ *                   m = b1 m + (1-b1) g';  v = b2 v + (1-b2) g'^2
+ *                   w -= (lr/(1-b1^t)) * m / (sqrt(v)/sqrt(1-b2^t) + eps)
+ *   OF_OPT_ADAMW  w *= (1 - lr*wd), then the Adam step on the raw g.
+ *
+ * Every kernel that updates a parameter uses one shared per-element update
+ * with explicitly rounded operations, so all orderings compute bit-identical
+ * values from identical gradients.
+ */
+typedef enum of_opt_kind { OF_OPT_SGD = 0, OF_OPT_ADAM = 1, OF_OPT_ADAMW = 2 } of_opt_kind;
+
+typedef struct of_opt {
+  int32_t kind;
+  float lr;
+  float weight_decay;
+  float momentum;   /* SGD only */
+  float beta1;      /* Adam / AdamW */
+  float beta2;
+  float eps;
+  int64_t step;     /* >= 1 */
+} of_opt;
+
+/*
+ * A trainable tensor theta with its history (Fig. 2, "History").
+ *   w       fp32 master values [numel]
+ *   m       SGD momentum buffer or Adam first moment [numel] (required)
+ *   v       Adam second moment [numel] (required for Adam/AdamW, ignored for SGD)
+ *   w_bf16  optional bf16 copy of w (round to nearest even), rewritten by every
+ *           update when not NULL; it is the matmul operand when dtype is OF_BF16
+ */
+typedef struct of_param {
+  float* w;
+  float* m;
+  float* v;
+  uint16_t* w_bf16;
+  int64_t numel;
+} of_param;
+
+typedef struct of_linear_desc {
+  int64_t M, N, K;   /* rows, output features, input features (all >= 1) */
+  int64_t ldx;       /* row stride of X in elements; 0 means K */
+  int64_t ldy;       /* row stride of Y, Z, dZ in elements; 0 means N */
+  int32_t dtype;     /* matmul operand type: OF_F32, or OF_BF16 (operands rounded to bf16, fp32 accumulate) */
+  int32_t act;       /* of_act applied in the forward epilogue */
+  int32_t has_bias;  /* 1: bias [N] added in the forward */
+} of_linear_desc;
+
+typedef struct of_conv_desc {
+  int64_t N, H, W, C;  /* input batch, height, width, channels (NHWC) */
+  int64_t Cout;        /* output channels; filter is [Cout,3,3,C], stride 1, zero pad 1 */
+  int32_t act;         /* of_act applied in the forward epilogue (NONE or RELU) */
+  int32_t has_bias;
+} of_conv_desc;
+
+/* Which call a workspace query is for. */
+typedef enum of_linear_op {
+  OF_LINEAR_FWD = 0,        /* of_linear_fwd, of_linear_fwd_fused */
+  OF_LINEAR_BWD_DATA = 1,   /* of_linear_bwd_data, the dgrad half of of_linear_bwd_fused */
+  OF_LINEAR_BWD_WEIGHT = 2  /* of_linear_bwd_weight, the wgrad half of of_linear_bwd_fused */
+} of_linear_op;
+
+typedef enum of_conv_op {
+  OF_CONV_FWD = 0, OF_CONV_BWD_DATA = 1, OF_CONV_BWD_WEIGHT = 2
+} of_conv_op;
+
+/* ---------------------------------------------------------------- basics */
+
+/* OF_VERSION of the built library. */
+int of_version(void);
+
+/* Message for the last non-OF_OK status returned on this thread ("" if none). */
+const char* of_last_error(void);
+
+/* Bytes of workspace `op` needs for `d` (0 if none); 0 and OF_EINVAL in
+ * of_last_error() for an invalid descriptor. */
+size_t of_linear_workspace_size(const of_linear_desc* d, int32_t op);
+
+/* ------------------------------------------------------- linear layers */
+
+/*
+ * Plain forward (Fig. 1(a), the forward node of a linear layer):
+ *   Z = X W^T + b,  Y = act(Z).
+ * x: [M, ldx] fp32 (OF_F32) or fp32 rounded to bf16 on load (OF_BF16).
+ * W: W->w is read for OF_F32, W->w_bf16 for OF_BF16.  b: [N] or NULL when
+ * !has_bias.  z: [M, ldy] fp32, optional (needed by GELU's derivative);
+ * y: [M, ldy] fp32, required.  Workspace: OF_LINEAR_FWD.
+ */
+of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param* W,
+                        const float* b, float* z, float* y, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/*
+ * Forward-fusion forward (Section 3 "Forward-Fusion"; Appendix B.1, Alg. 2):
+ * the optimizer of W (and b) runs on the pending gradients gW [N,K] (gb [N])
+ * with `opt`, writes back W, m, v (and w_bf16), and Y = act(X W'^T + b') is
+ * computed from the updated values.  Each element is updated exactly once.
+ * The update is applied while the W tiles are loaded for the contraction when
+ * M fits one row tile of the forward (M <= 256); for larger M the same update
+ * runs as a separate pass just before the contraction, with identical results.
+ * opt == NULL means nothing is pending (the first iteration): identical to
+ * of_linear_fwd.  b/gb: both NULL when !has_bias.  Workspace: OF_LINEAR_FWD.
+ */
+of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_param* W,
+                              const float* gW, const of_param* b, const float* gb,
+                              const of_opt* opt, float* z, float* y, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
+ * Data gradient with the OLD weights (the dependency rule after Alg. 3):
+ *   dX = (dZ W) * act_prev'(prev)
+ * dz: [M, ldy].  prev: the previous layer's saved tensor, [M, ldx]: its Y for
+ * OF_ACT_RELU (the mask is Y > 0, equal to Z > 0), its Z for OF_ACT_GELU,
+ * NULL for OF_ACT_NONE.  dx: [M, ldx] fp32.  Workspace: OF_LINEAR_BWD_DATA.
+ */
+of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_param* W,
+                             const float* prev, int32_t act_prev, float* dx, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/*
+ * Eager weight gradient (Fig. 1(b); the gradient is materialised and later
+ * read and reset by the optimizer, Section 3 "Baseline"):
+ *   dW = dZ^T X [N,K],  db = sum over rows of dZ [N] (db may be NULL).
+ * accumulate = 1 adds into dw/db (a parameter used more than once).
+ * Workspace: OF_LINEAR_BWD_WEIGHT.
+ */
+of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const float* x,
+                               float* dw, float* db, int32_t accumulate, void* ws,
+                               size_t ws_bytes, void* stream);
+
+/*
+ * Backward-fusion for one linear layer (Section 3 "Backward-Fusion";
+ * Appendix B.2, Alg. 3 and the dependency rule after it):
+ *   1. if dx_prev != NULL: dX = (dZ W_old) * act_prev'(prev) on `stream`
+ *      (exactly of_linear_bwd_data);
+ *   2. the weight-gradient contraction dZ^T X, whose epilogue adds gW_partial
+ *      (gradient of earlier uses of a shared W, or NULL), applies `opt` to W
+ *      and its history and writes W, m, v (and w_bf16); dW is never stored.
+ *      With b != NULL the bias gradient sum(dZ) (+ gb_partial) updates b the
+ *      same way inside the same kernel.
+ * Step 2 runs after step 1 in stream order, so step 1 always reads the old W.
+ * If update_stream != NULL, step 2 is enqueued on update_stream after an
+ * event recorded on `stream` behind step 1, and `stream` continues at once
+ * (the overlap of updating with back-propagation, Section 3); the caller must
+ * then order later reads of W and b after update_stream.  The two halves use
+ * workspaces ws (OF_LINEAR_BWD_DATA) and ws_update (OF_LINEAR_BWD_WEIGHT),
+ * which must not overlap when update_stream != NULL.
+ */
+of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const float* x,
+                              const of_param* W, const of_param* b, const float* gW_partial,
+                              const float* gb_partial, const of_opt* opt, const float* prev,
+                              int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
+                              void* ws_update, size_t ws_update_bytes, void* stream,
+                              void* update_stream);
+
+/* ------------------------------------------------ elementwise optimizer */
+
+/*
+ * Fused elementwise update of one tensor (bias / norm parameters, and the
+ * forward-fusion flush; Section 3, the optimizer reads and resets the
+ * accumulated gradient):
+ *   g_rows == 1: gradient g[numel];
+ *   g_rows  > 1: g is [g_rows, numel] with row stride g_ld (0 means numel),
+ *                and the gradient is the sum of the rows, taken in row order
+ *                inside the kernel; it is never stored.
+ */
+of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t g_rows,
+                                      int64_t g_ld, const of_opt* opt, void* stream);
+
+/*
+ * Eager optimizer stage (Fig. 1(b) stage 3; one launch for the element-wise
+ * work of many tensors, in the manner of fused multi-tensor optimizers,
+ * Appendix A): for i < n, params[i] is updated with grads[i] [params[i].numel].
+ * params and grads are HOST arrays of n entries holding device pointers.
+ */
+of_status of_optimizer_step(int32_t n, const of_param* params, const float* const* grads,
+                            const of_opt* opt, void* stream);
+
+/* ------------------------------------------------------------- losses */
+
+/*
+ * Softmax cross-entropy, forward and backward in one launch:
+ *   loss = mean_b (logsumexp(z_b) - z_{b,label_b});  dz = (softmax(z) - onehot)/B.
+ * logits: [B, C] row stride ld (0 means C); labels: int64 [B] in [0, C)
+ * (out-of-range labels give loss NaN); loss: one fp32 on the device; dlogits:
+ * [B, ld].
+ */
+of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B, int64_t C,
+                          int64_t ld, float* loss, float* dlogits, void* stream);
+
+/*
+ * Mean squared error, forward and backward:
+ *   loss = mean over all M*D elements of (y - t)^2;  dy = 2 (y - t) / (M*D).
+ * y: [M, ld], t: [M, D] contiguous, dy: [M, ld]; loss: one fp32 on the device.
+ * ws: at least of_mse_workspace_size(M, D) bytes.
+ */
+size_t of_mse_workspace_size(int64_t M, int64_t D);
+of_status of_mse_fwd_bwd(const float* y, const float* t, int64_t M, int64_t D, int64_t ld,
+                         float* loss, float* dy, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OPFUSE_H */

@@ -50,7 +50,7 @@ class Op:
 
     def __init__(self):
         # Nothing is pending before the first iteration (see the FF reading in
-        # the oracle's run module), so the flag starts True.
+        # the oracle's train module), so the flag starts True.
         self.updated = True
 
 
@@ -70,6 +70,11 @@ class Linear(Op):
             z = z + self.b.value
         return z, x
 
+    def abs_bound(self, x):
+        """sum_k |x_mk w_nk| + |b_n|: the scale of the rounding error of z."""
+        s = np.abs(_maybe_bf16(x, self.bf16)) @ np.abs(_maybe_bf16(self.w.value, self.bf16)).T
+        return s + np.abs(self.b.value) if self.b is not None else s
+
     def backward(self, x, dz):
         dzq = _maybe_bf16(dz, self.bf16)
         dx = dzq @ _maybe_bf16(self.w.value, self.bf16)
@@ -79,11 +84,19 @@ class Linear(Op):
 
 
 class ReLU(Op):
+    """flip: optional boolean array; where True the backward mask decision is
+    inverted (used to enumerate the decisions float32 rounding can change)."""
+
+    flip = None
+
     def forward(self, z):
         return np.maximum(z, 0.0), z
 
     def backward(self, z, dy):
-        return (np.where(z > 0.0, dy, 0.0),), ()
+        mask = z > 0.0
+        if self.flip is not None:
+            mask = mask ^ self.flip
+        return (np.where(mask, dy, 0.0),), ()
 
 
 def gelu_cdf(z):

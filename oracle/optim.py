@@ -53,5 +53,6 @@ def apply(param, hyper):
     policy = POLICIES[hyper["kind"]]
     step = param.step + 1
     param.value, param.m, param.v = policy(param.value, param.grad, param.m, param.v, step, **hyper)
+    param.last_grad = param.grad   # kept for state snapshots only
     param.grad = None
     param.step = step

@@ -27,12 +27,23 @@ Returned by run(): per-step losses (loss t uses theta^(t-1)), the evaluation
 loss at theta^(K), final values / histories / step counters of every
 parameter, the flags and counts, and the max-pool argmax of step 1.
 
+For Adam-family optimizers run() also reports, per parameter element, the
+smallest positive bias-corrected second-moment root sqrt(v_t / (1 - beta2^t))
+seen over the steps (inf if the gradient was exactly 0 at every step: such an
+element never moves under Adam); this is instrumentation only.  Where it is
+comparable to eps, the update
+m_hat / (sqrt(v_hat) + eps) is ill-conditioned in the gradient (its derivative
+reaches 1/eps), so any float32 rounding of the gradient moves that element by
+up to a whole step; the GPU parity tests use this to tell such elements apart.
+
 Pinned by: the ordering invariant eager == ff(flushed) == bf bit for bit, a
 planted dependency violation that breaks it, a shared-parameter toy with
 step == K (tests/test_oracle_orderings.py).  Whole K-step trajectories have no
 printed reference values in the paper: beyond the component pins and the
 invariant they are parity unpinned.
 """
+import itertools
+
 import numpy as np
 
 from workloads import make_params, make_batch, make_eval_batch
@@ -141,6 +152,72 @@ class Model:
         return loss
 
 
+def ambiguous_relu_decisions(model, x, c=1.0):
+    """Backward ReLU decisions a float32 run may take differently.
+
+    A decision z > 0 is ambiguous when |z| < c * 2^-24 * sum_k |x_mk w_nk| (+|b|),
+    i.e. within the rounding scale of the float32 sum that produces z.  Returns
+    [(node index, row, column, |z| / scale)] sorted from most to least
+    ambiguous.  Only ReLUs fed directly by a Linear are examined.
+    """
+    u = 2.0 ** -24
+    env = {"input": x}
+    producer = {}
+    out = []
+    for i, (op, ins, name) in enumerate(model.nodes):
+        vals = [env[n] for n in ins]
+        y, _ = op.forward(*vals)
+        if isinstance(op, L.ReLU) and ins[0] in producer:
+            lin, lin_in = producer[ins[0]]
+            scale = u * lin.abs_bound(lin_in)
+            ratio = np.abs(vals[0]) / np.maximum(scale, 1e-300)
+            for r, col in zip(*np.nonzero(ratio < c)):
+                out.append((i, int(r), int(col), float(ratio[r, col])))
+        if isinstance(op, L.Linear):
+            producer[name] = (op, vals[0])
+        env[name] = y
+    out.sort(key=lambda d: d[3])
+    return out
+
+
+def candidate_steps(cfg, state, t, max_decisions=8, seed=0):
+    """Every valid float32 outcome of eager step t from `state` (a snapshot).
+
+    Enumerates the subsets of the ambiguous ReLU decisions of the step (at most
+    `max_decisions`, the most ambiguous ones), fewest flips first, and yields
+    (flipped decisions, loss, state after the step) for each; for Adam-family
+    optimizers the state also holds min_sqrt_vhat, the positive bias-corrected
+    sqrt(v_hat) after the step (inf where v is 0), as run() reports it.
+    """
+    x, y = make_batch(cfg, t, seed)
+    x = np.asarray(x, np.float64)
+    y = y if y.dtype == np.int64 else np.asarray(y, np.float64)
+    probe = new_model(cfg, init=state["params"])
+    dec = ambiguous_relu_decisions(probe, x)[:max_decisions]
+    for nflip in range(len(dec) + 1):
+        for subset in itertools.combinations(dec, nflip):
+            model = new_model(cfg, init=state["params"])
+            for k, p in model.params.items():
+                p.m, p.v, p.step = state["m"][k].copy(), state["v"][k].copy(), state["step"][k]
+            for i, r, col, _ in subset:
+                op = model.nodes[i][0]
+                if op.flip is None:
+                    op.flip = np.zeros((x.shape[0], model.nodes[i - 1][0].w.value.shape[0]), bool)
+                op.flip[r, col] = True
+            loss = model.step_eager(x, y)
+            ps = model.params
+            vh = {}
+            if cfg["opt"]["kind"] != "sgd":
+                for k, p in ps.items():
+                    r = np.sqrt(p.v / (1.0 - cfg["opt"]["beta2"] ** p.step))
+                    vh[k] = np.where(r > 0.0, r, np.inf)
+            yield subset, loss, dict(params={k: p.value for k, p in ps.items()},
+                                     m={k: p.m for k, p in ps.items()},
+                                     v={k: p.v for k, p in ps.items()},
+                                     step={k: p.step for k, p in ps.items()},
+                                     min_sqrt_vhat=vh)
+
+
 def _accumulate(op, grads):
     for p, g in zip(op.params, grads):
         p.grad = g.copy() if p.grad is None else p.grad + g
@@ -200,17 +277,36 @@ def new_model(cfg, init=None, seed=0):
     return Model(nodes, params, cfg["loss"], cfg["opt"])
 
 
-def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=None):
+def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=None,
+        snapshots=()):
     """Train workload `cfg` for `steps` steps under `ordering` in float64.
 
     Returns a dict: losses, eval_loss, params / m / v (float64 arrays by name),
     step (int by name), updated (per node, after the run), count (by name),
-    argmax (max-pool window positions of step 1, by node index).
+    argmax (max-pool window positions of step 1, by node index),
+    snapshots {t: state after step t (t = 0: the initial state)} for t in
+    `snapshots` -- params / m / v copies, step counters, the gradient the
+    update of step t consumed and min_sqrt_vhat up to step t (eager ordering).
     """
     steps = cfg["steps"] if steps is None else steps
     model = new_model(cfg, init, seed)
     losses = []
     argmax = {}
+    hyper = cfg["opt"]
+    min_vhat = {}
+    snaps = {}
+
+    def snap():
+        ps = model.params
+        return dict(params={k: p.value.copy() for k, p in ps.items()},
+                    m={k: p.m.copy() for k, p in ps.items()},
+                    v={k: p.v.copy() for k, p in ps.items()},
+                    step={k: p.step for k, p in ps.items()},
+                    grad={k: getattr(p, "last_grad", None) for k, p in ps.items()},
+                    min_sqrt_vhat={k: v.copy() for k, v in min_vhat.items()})
+
+    if 0 in snapshots:
+        snaps[0] = snap()
     for t in range(1, steps + 1):
         x, y = batches[t - 1] if batches is not None else make_batch(cfg, t, seed)
         x = np.asarray(x, np.float64)
@@ -225,6 +321,14 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
             raise ValueError(ordering)
         if t == 1:
             argmax = dict(model.last_argmax)
+        if hyper["kind"] != "sgd":
+            for k, p in model.params.items():
+                if p.step > 0:
+                    r = np.sqrt(p.v / (1.0 - hyper["beta2"] ** p.step))
+                    r = np.where(r > 0.0, r, np.inf)
+                    min_vhat[k] = np.minimum(min_vhat[k], r) if k in min_vhat else r
+        if t in snapshots:
+            snaps[t] = snap()
     updated_before_flush = [op.updated for op, _, _ in model.nodes]
     if ordering == "ff":
         model.flush()
@@ -243,4 +347,6 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
         updated_before_flush=updated_before_flush,
         updated=[op.updated for op, _, _ in model.nodes],
         argmax=argmax,
+        min_sqrt_vhat=min_vhat,
+        snapshots=snaps,
     )

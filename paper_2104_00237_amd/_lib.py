@@ -1,0 +1,151 @@
+"""ctypes binding of libopfuse.so: argument marshalling only.
+
+Each function has the C name and signature of include/opfuse.h; device
+pointers are passed as Python ints, stream handles as ints (0 = null stream),
+structs as the ctypes mirrors below.  A status other than OF_OK raises
+OpfuseError with the library's message.  There is no fallback: if the
+library is not built, loading fails loudly.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("OPFUSE_LIB", os.path.join(_HERE, "libopfuse.so"))
+
+OF_OK, OF_EINVAL, OF_EUNSUPPORTED, OF_EALIGN, OF_EWORKSPACE, OF_EHIP = range(6)
+STATUS_NAMES = {0: "OF_OK", 1: "OF_EINVAL", 2: "OF_EUNSUPPORTED", 3: "OF_EALIGN",
+                4: "OF_EWORKSPACE", 5: "OF_EHIP"}
+OF_F32, OF_BF16 = 0, 1
+OF_ACT_NONE, OF_ACT_RELU, OF_ACT_GELU = 0, 1, 2
+OF_OPT_SGD, OF_OPT_ADAM, OF_OPT_ADAMW = 0, 1, 2
+OF_LINEAR_FWD, OF_LINEAR_BWD_DATA, OF_LINEAR_BWD_WEIGHT = 0, 1, 2
+ACTS = {"none": OF_ACT_NONE, "relu": OF_ACT_RELU, "gelu": OF_ACT_GELU}
+OPT_KINDS = {"sgd": OF_OPT_SGD, "adam": OF_OPT_ADAM, "adamw": OF_OPT_ADAMW}
+
+c_int32, c_int64, c_float, c_void_p, c_size_t = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                                  ctypes.c_void_p, ctypes.c_size_t)
+
+
+class OfOpt(ctypes.Structure):
+    _fields_ = [("kind", c_int32), ("lr", c_float), ("weight_decay", c_float),
+                ("momentum", c_float), ("beta1", c_float), ("beta2", c_float),
+                ("eps", c_float), ("step", c_int64)]
+
+
+class OfParam(ctypes.Structure):
+    _fields_ = [("w", c_void_p), ("m", c_void_p), ("v", c_void_p), ("w_bf16", c_void_p),
+                ("numel", c_int64)]
+
+
+class OfLinearDesc(ctypes.Structure):
+    _fields_ = [("M", c_int64), ("N", c_int64), ("K", c_int64), ("ldx", c_int64),
+                ("ldy", c_int64), ("dtype", c_int32), ("act", c_int32), ("has_bias", c_int32)]
+
+
+class OfConvDesc(ctypes.Structure):
+    _fields_ = [("N", c_int64), ("H", c_int64), ("W", c_int64), ("C", c_int64),
+                ("Cout", c_int64), ("act", c_int32), ("has_bias", c_int32)]
+
+
+class OpfuseError(RuntimeError):
+    def __init__(self, status, fn, msg):
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+P = ctypes.POINTER
+_SIGS = {
+    "of_version": (ctypes.c_int, []),
+    "of_last_error": (ctypes.c_char_p, []),
+    "of_linear_workspace_size": (c_size_t, [P(OfLinearDesc), c_int32]),
+    "of_linear_fwd": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_void_p,
+                                c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_linear_fwd_fused": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p,
+                                      P(OfParam), c_void_p, P(OfOpt), c_void_p, c_void_p,
+                                      c_void_p, c_size_t, c_void_p]),
+    "of_linear_bwd_data": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_int32,
+                                     c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_linear_bwd_weight": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_int32, c_void_p, c_size_t, c_void_p]),
+    "of_linear_bwd_fused": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, P(OfParam),
+                                      P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
+                                      c_int32, c_void_p, c_void_p, c_size_t, c_void_p, c_size_t,
+                                      c_void_p, c_void_p]),
+    "of_elementwise_fused_update": (c_int32, [P(OfParam), c_void_p, c_int64, c_int64,
+                                              P(OfOpt), c_void_p]),
+    "of_optimizer_step": (c_int32, [c_int32, P(OfParam), P(c_void_p), P(OfOpt), c_void_p]),
+    "of_xent_fwd_bwd": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_int64, c_void_p,
+                                  c_void_p, c_void_p]),
+    "of_mse_workspace_size": (c_size_t, [c_int64, c_int64]),
+    "of_mse_fwd_bwd": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_int64, c_void_p,
+                                 c_void_p, c_void_p, c_size_t, c_void_p]),
+}
+
+_lib = None
+
+
+def load():
+    """Load libopfuse.so (once).  Raises if it is missing: there is no fallback path."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"opfuse HIP library not found at {LIB_PATH}; build it with "
+                               "`python -m paper_2104_00237_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def exported_names():
+    return list(_SIGS)
+
+
+def _wrap(name):
+    def call(*args):
+        lib = load()
+        st = getattr(lib, name)(*args)
+        if st != OF_OK:
+            raise OpfuseError(st, name, lib.of_last_error().decode())
+        return st
+    call.__name__ = name
+    return call
+
+
+def of_version():
+    return load().of_version()
+
+
+def of_last_error():
+    return load().of_last_error().decode()
+
+
+def of_linear_workspace_size(desc, op):
+    return load().of_linear_workspace_size(ctypes.byref(desc), op)
+
+
+def of_mse_workspace_size(M, D):
+    return load().of_mse_workspace_size(M, D)
+
+
+for _n in ("of_linear_fwd", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
+           "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
+           "of_xent_fwd_bwd", "of_mse_fwd_bwd"):
+    globals()[_n] = _wrap(_n)
+del _n
+
+
+def make_opt(hyper, step):
+    """of_opt from a workload's optimizer dict and the 1-based update index."""
+    return OfOpt(OPT_KINDS[hyper["kind"]], hyper["lr"], hyper.get("weight_decay", 0.0),
+                 hyper.get("momentum", 0.0), hyper.get("beta1", 0.0), hyper.get("beta2", 0.0),
+                 hyper.get("eps", 0.0), step)
+
+
+def param_of(w, m, v=None, w_bf16=None):
+    """OfParam over torch tensors (device pointers taken once)."""
+    return OfParam(w.data_ptr(), m.data_ptr(), v.data_ptr() if v is not None else None,
+                   w_bf16.data_ptr() if w_bf16 is not None else None, w.numel())

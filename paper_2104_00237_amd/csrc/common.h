@@ -1,0 +1,172 @@
+// Internal declarations shared by the opfuse HIP sources (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/opfuse.h"
+
+namespace opfuse {
+
+// Optimizer hyperparameters as the kernels consume them.  Everything that
+// depends on the step (bias corrections) is folded on the host in float64.
+struct OptK {
+  int kind;          // of_opt_kind
+  float lr, wd, mom;
+  float b1, b2, eps;
+  float omb1, omb2;  // 1 - beta1, 1 - beta2
+  float step_size;   // lr / (1 - beta1^t)
+  float rsqrt_bc2;   // 1 / sqrt(1 - beta2^t)
+  float decay;       // 1 - lr * wd  (AdamW)
+};
+
+OptK make_optk(const of_opt& o);
+
+// The one per-element update used by every kernel that changes a parameter
+// (Appendix A, Alg. 1: theta_t = theta_{t-1} + pi(...)).  All operations are
+// explicitly rounded (the sources are also built with -ffp-contract=off), so
+// the same gradient gives the same bits in every ordering and kernel.
+__device__ __forceinline__ void opt_update(const OptK& o, float& w, float g, float& m, float& v) {
+  if (o.kind == OF_OPT_SGD) {
+    // Momentum policy pi_2 with coupled weight decay.
+    const float gp = __fmaf_rn(o.wd, w, g);
+    m = __fmaf_rn(o.mom, m, gp);
+    w = __fmaf_rn(-o.lr, m, w);
+  } else {
+    float gp = g;
+    if (o.kind == OF_OPT_ADAMW) {
+      w = __fmul_rn(w, o.decay);
+    } else {
+      gp = __fmaf_rn(o.wd, w, g);
+    }
+    m = __fmaf_rn(o.b1, m, __fmul_rn(o.omb1, gp));
+    v = __fmaf_rn(o.b2, v, __fmul_rn(__fmul_rn(o.omb2, gp), gp));
+    const float denom = __fadd_rn(__fmul_rn(__fsqrt_rn(v), o.rsqrt_bc2), o.eps);
+    w = __fsub_rn(w, __fdiv_rn(__fmul_rn(o.step_size, m), denom));
+  }
+}
+
+// float -> bfloat16 bits, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_round(float f) {
+  return __uint_as_float(((uint32_t)f32_to_bf16(f)) << 16);
+}
+
+// Derivative of the forward activation, evaluated from the saved tensor the
+// dgrad epilogue receives: Y for ReLU (Y > 0 exactly when Z > 0), Z for GELU.
+__device__ __forceinline__ float act_grad(int act, float saved) {
+  if (act == OF_ACT_RELU) return saved > 0.f ? 1.f : 0.f;
+  if (act == OF_ACT_GELU) {
+    const float cdf = 0.5f * (1.f + erff(saved * 0.70710678118654752f));
+    const float pdf = 0.39894228040143268f * expf(-0.5f * saved * saved);
+    return cdf + saved * pdf;
+  }
+  return 1.f;
+}
+
+__device__ __forceinline__ float act_fwd(int act, float z) {
+  if (act == OF_ACT_RELU) return z > 0.f ? z : 0.f;
+  if (act == OF_ACT_GELU) return z * (0.5f * (1.f + erff(z * 0.70710678118654752f)));
+  return z;
+}
+
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+
+__device__ __forceinline__ void st_bf16x4(uint16_t* p, float4 w) {
+  const uint32_t lo = (uint32_t)f32_to_bf16(w.x) | ((uint32_t)f32_to_bf16(w.y) << 16);
+  const uint32_t hi = (uint32_t)f32_to_bf16(w.z) | ((uint32_t)f32_to_bf16(w.w) << 16);
+  *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+}
+
+// Update 4 consecutive parameter elements at `off` (all valid, 16B aligned).
+__device__ __forceinline__ float4 update4(const OptK& o, const of_param& P, float4 g, int64_t off) {
+  float4 w = ld4(P.w + off), m = ld4(P.m + off);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  const bool adam = o.kind != OF_OPT_SGD;
+  if (adam) v = ld4(P.v + off);
+  opt_update(o, w.x, g.x, m.x, v.x);
+  opt_update(o, w.y, g.y, m.y, v.y);
+  opt_update(o, w.z, g.z, m.z, v.z);
+  opt_update(o, w.w, g.w, m.w, v.w);
+  st4(P.w + off, w);
+  st4(P.m + off, m);
+  if (adam) st4(P.v + off, v);
+  if (P.w_bf16) st_bf16x4(P.w_bf16 + off, w);
+  return w;
+}
+
+__device__ __forceinline__ float update1(const OptK& o, const of_param& P, float g, int64_t off) {
+  float w = P.w[off], m = P.m[off], v = 0.f;
+  const bool adam = o.kind != OF_OPT_SGD;
+  if (adam) v = P.v[off];
+  opt_update(o, w, g, m, v);
+  P.w[off] = w;
+  P.m[off] = m;
+  if (adam) P.v[off] = v;
+  if (P.w_bf16) P.w_bf16[off] = f32_to_bf16(w);
+  return w;
+}
+
+inline bool aligned16(const void* p) { return (((uintptr_t)p) & 15u) == 0; }
+
+// ---------------------------------------------------------------- GEMM API
+// C[P,Q] = sum_r A(p,r) B(q,r) with
+//   A(p,r) = A[p*a_sp + r*a_sr], one of a_sp / a_sr equal to 1,
+//   B(q,r) = B[q*b_sq + r*b_sr], one of b_sq / b_sr equal to 1.
+
+enum EpiKind {
+  EPI_FWD = 0,        // y = act(c + bias), z = c + bias
+  EPI_FWD_FF = 1,     // forward-fusion: B tiles (W) are updated while loaded
+  EPI_DGRAD = 2,      // dx = c * act'(prev)
+  EPI_WGRAD = 3,      // dw = c (or +=), db = column sums of A (or +=)
+  EPI_WGRAD_BF = 4,   // backward-fusion: update W (and b) from c (and sums)
+};
+
+struct GemmProblem {
+  const float* A; int64_t a_sp, a_sr;
+  const float* B; int64_t b_sq, b_sr;
+  int P, Q, R;
+};
+
+struct EpiArgs {
+  // outputs
+  float* out; int64_t ldo;      // y (FWD), dx (DGRAD), dw (WGRAD)
+  float* z; int64_t ldz;        // FWD: pre-activation (optional)
+  const float* prev; int64_t ldp;  // DGRAD: saved tensor of the previous layer
+  int act;                      // FWD: activation; DGRAD: previous layer's activation
+  int accumulate;               // WGRAD
+  // bias
+  const float* bias;            // FWD: bias to add (may be NULL)
+  float* db;                    // WGRAD: bias gradient out (may be NULL)
+  // parameters being updated (FWD_FF: W is the B operand; WGRAD_BF: W is the output)
+  of_param W;                   // W.w etc.
+  const float* gW;              // FWD_FF: pending gradient; WGRAD_BF: extra gradient (shared use)
+  of_param b;                   // FF / BF bias parameter (b.w NULL if none)
+  const float* gb;              // FF: pending bias gradient; BF: extra bias gradient
+  int with_db;                  // WGRAD: db != NULL; WGRAD_BF: b.w != NULL
+  OptK opt;
+};
+
+size_t gemm_workspace_bytes(int kind, int P, int Q, int R);
+hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                       hipStream_t stream);
+
+// ------------------------------------------------------ elementwise / losses
+hipError_t launch_multi_update(int n, const of_param* params, const float* const* grads,
+                               const OptK& o, hipStream_t stream);
+hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, int64_t ld,
+                              const OptK& o, hipStream_t stream);
+hipError_t launch_xent(const float* z, const int64_t* labels, int64_t B, int64_t C, int64_t ld,
+                       float* loss, float* dz, hipStream_t stream);
+size_t mse_ws_bytes(int64_t M, int64_t D);
+hipError_t launch_mse(const float* y, const float* t, int64_t M, int64_t D, int64_t ld,
+                      float* loss, float* dy, void* ws, hipStream_t stream);
+
+}  // namespace opfuse

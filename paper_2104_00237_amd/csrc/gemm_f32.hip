@@ -1,0 +1,643 @@
+// fp32 MFMA contractions of a linear layer, with the optimizer fused into
+// their prologue (forward-fusion) or epilogue (backward-fusion).
+//
+// One tiled kernel computes C[P,Q] = sum_r A(p,r) B(q,r) on the CDNA matrix
+// cores (v_mfma_f32_32x32x2_f32).  A workgroup of 4 wavefronts owns a BP x BQ
+// output tile; wavefronts split it WP x WQ and, when WR > 1, also split each
+// reduction chunk (their partial tiles are summed in wave order).  Operand
+// tiles go global -> registers -> LDS ([r][x] layout, double buffered); the
+// next chunk's global loads are issued before the current chunk's MFMAs.
+// A grid-level split of the reduction (gridDim.z > 1) writes partial tiles to
+// the workspace and a second kernel sums them in split order and runs the
+// epilogue, so every result is deterministic and the same shape always uses
+// the same tiling whatever the epilogue is.
+//
+// The three contractions of a linear layer (X [M,K], W [N,K], dZ [M,N]):
+//   forward  C[m,n] = sum_k X[m,k] W[n,k]    P=M Q=N R=K  A,B reduction-contiguous
+//   dgrad    C[m,k] = sum_n dZ[m,n] W[n,k]   P=M Q=K R=N  A red.-contig., B output-contig.
+//   wgrad    C[n,k] = sum_m dZ[m,n] X[m,k]   P=N Q=K R=M  A,B output-contiguous
+//
+// Forward-fusion (Appendix B.1, Alg. 2): the B operand of the forward is W.
+// When M fits one row tile (gridDim.x == 1) each W element is loaded by
+// exactly one workgroup; that workgroup loads W, the pending gradient and the
+// history, applies the update, writes them back, and puts the updated value
+// into LDS for the MFMAs (Fig. 2: the update's write is merged with the next
+// forward's read).  The bias update is done once per column tile by the
+// split-0 workgroup.
+//
+// Backward-fusion (Appendix B.2, Alg. 3): the output of the wgrad is dW; its
+// epilogue loads W and the history, applies the update with the accumulated
+// tile as the gradient and writes them back; dW is never stored (Fig. 2: the
+// gradient accumulation is merged with the optimizer's read).  The bias
+// gradient is the column sum of the A tiles (dZ) the workgroups of column
+// tile 0 already stage in LDS.
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace opfuse {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_>
+struct Tile {
+  static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_, WR = WR_;
+  static_assert(WP * WQ * WR == 4, "a workgroup is 4 wavefronts");
+  static constexpr int WTP = BP / WP, WTQ = BQ / WQ;   // wavefront tile
+  static constexpr int TP = WTP / 32, TQ = WTQ / 32;   // 32x32 MFMA blocks per wavefront
+  static_assert(TP >= 1 && TQ >= 1 && WTP % 32 == 0 && WTQ % 32 == 0, "32x32 blocks");
+  static constexpr int RW = BR / WR;                    // chunk rows per wavefront
+  static_assert(RW % 2 == 0 && BR % 4 == 0, "k pairs");
+  static constexpr int LDA = BP + 4, LDB = BQ + 4;
+  static constexpr int LDC = (WR * BP * (BQ + 4) * 4 <= 60 * 1024) ? BQ + 4 : BQ;
+  static constexpr int SM_MAIN = 2 * BR * (LDA + LDB);
+  static constexpr int SM_C = WR * BP * LDC;
+  static constexpr int SMX = SM_MAIN > SM_C ? SM_MAIN : SM_C;  // floats
+  static_assert(SMX * 4 <= 64 * 1024, "LDS per workgroup");
+};
+
+// Tile menu (P x Q per workgroup, reduction chunk, wavefront split).
+using T32x32 = Tile<32, 32, 32, 1, 1, 4>;
+using T64x32 = Tile<64, 32, 32, 2, 1, 2>;
+using T64x64 = Tile<64, 64, 16, 2, 2, 1>;
+using T128x64 = Tile<128, 64, 16, 2, 2, 1>;
+using T128x128 = Tile<128, 128, 16, 2, 2, 1>;
+using T256x32 = Tile<256, 32, 16, 4, 1, 1>;
+
+enum TileId { TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32, TI_COUNT };
+static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256};
+static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32};
+static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16};
+
+// ------------------------------------------------------------ operand tiles
+// A BX (output dim) x BR (reduction) tile of one operand, held in registers as
+// float4s between its global load and its LDS store.  RC: the reduction index
+// is contiguous in memory (else the output index is).
+template <int BX, int BR, bool RC>
+struct TileLoad {
+  static constexpr int NV = BX * BR / 4;
+  static constexpr int PER = (NV + 255) / 256;
+  float4 v[PER];
+
+  __device__ __forceinline__ void load(const float* __restrict__ base, int64_t s_x, int64_t s_r,
+                                       int x0, int X, int r0, int rend, bool vec, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = tid + i * 256;
+      float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (idx < NV) {
+        if (RC) {
+          const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
+          const int gx = x0 + x, gr = r0 + r;
+          if (gx < X) {
+            const float* p = base + (int64_t)gx * s_x + gr;
+            if (vec && gr + 3 < rend) {
+              val = *reinterpret_cast<const float4*>(p);
+            } else {
+              if (gr + 0 < rend) val.x = p[0];
+              if (gr + 1 < rend) val.y = p[1];
+              if (gr + 2 < rend) val.z = p[2];
+              if (gr + 3 < rend) val.w = p[3];
+            }
+          }
+        } else {
+          const int r = idx / (BX / 4), x = (idx % (BX / 4)) * 4;
+          const int gx = x0 + x, gr = r0 + r;
+          if (gr < rend) {
+            const float* p = base + (int64_t)gr * s_r + gx;
+            if (vec && gx + 3 < X) {
+              val = *reinterpret_cast<const float4*>(p);
+            } else {
+              if (gx + 0 < X) val.x = p[0];
+              if (gx + 1 < X) val.y = p[1];
+              if (gx + 2 < X) val.z = p[2];
+              if (gx + 3 < X) val.w = p[3];
+            }
+          }
+        }
+      }
+      v[i] = val;
+    }
+  }
+
+  __device__ __forceinline__ void store(float* lds, int tid) const {
+    constexpr int LD = BX + 4;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = tid + i * 256;
+      if (idx < NV) {
+        if (RC) {
+          const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
+          lds[(r + 0) * LD + x] = v[i].x;
+          lds[(r + 1) * LD + x] = v[i].y;
+          lds[(r + 2) * LD + x] = v[i].z;
+          lds[(r + 3) * LD + x] = v[i].w;
+        } else {
+          const int r = idx / (BX / 4), x = (idx % (BX / 4)) * 4;
+          *reinterpret_cast<float4*>(&lds[r * LD + x]) = v[i];
+        }
+      }
+    }
+  }
+};
+
+// Forward-fusion B operand: W tile (reduction-contiguous) with its pending
+// update.  load() issues the loads of W, g, m, v; apply() runs after the
+// current chunk's MFMAs, updates, writes back and stages the new W in LDS.
+template <int BX, int BR>
+struct FFTileLoad {
+  static constexpr int NV = BX * BR / 4;
+  static constexpr int PER = (NV + 255) / 256;
+  float4 w[PER], g[PER], m[PER], v[PER];
+  int valid[PER];  // bit e set: element e of the float4 is inside the matrix
+  int64_t off[PER];
+
+  __device__ __forceinline__ void load(const EpiArgs& ea, int64_t ldw, int x0, int X, int r0,
+                                       int rend, bool vec, int tid) {
+    const bool adam = ea.opt.kind != OF_OPT_SGD;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = tid + i * 256;
+      valid[i] = 0;
+      w[i] = g[i] = m[i] = v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (idx < NV) {
+        const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
+        const int gx = x0 + x, gr = r0 + r;
+        if (gx < X) {
+          const int64_t o = (int64_t)gx * ldw + gr;
+          off[i] = o;
+          if (vec && gr + 3 < rend) {
+            valid[i] = 0xf;
+            w[i] = ld4(ea.W.w + o);
+            g[i] = ld4(ea.gW + o);
+            m[i] = ld4(ea.W.m + o);
+            if (adam) v[i] = ld4(ea.W.v + o);
+          } else {
+            float* pw = reinterpret_cast<float*>(&w[i]);
+            float* pg = reinterpret_cast<float*>(&g[i]);
+            float* pm = reinterpret_cast<float*>(&m[i]);
+            float* pv = reinterpret_cast<float*>(&v[i]);
+            for (int e = 0; e < 4; ++e) {
+              if (gr + e < rend) {
+                valid[i] |= 1 << e;
+                pw[e] = ea.W.w[o + e];
+                pg[e] = ea.gW[o + e];
+                pm[e] = ea.W.m[o + e];
+                if (adam) pv[e] = ea.W.v[o + e];
+              }
+            }
+          }
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void apply(const EpiArgs& ea, float* lds, int tid) {
+    constexpr int LD = BX + 4;
+    const bool adam = ea.opt.kind != OF_OPT_SGD;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = tid + i * 256;
+      if (idx >= NV) continue;
+      const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
+      float* pw = reinterpret_cast<float*>(&w[i]);
+      float* pg = reinterpret_cast<float*>(&g[i]);
+      float* pm = reinterpret_cast<float*>(&m[i]);
+      float* pv = reinterpret_cast<float*>(&v[i]);
+      if (valid[i] == 0xf) {
+        for (int e = 0; e < 4; ++e) opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
+        if (((uintptr_t)(ea.W.w + off[i]) & 15u) == 0) {
+          st4(ea.W.w + off[i], w[i]);
+          st4(ea.W.m + off[i], m[i]);
+          if (adam) st4(ea.W.v + off[i], v[i]);
+          if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + off[i], w[i]);
+        } else {
+          for (int e = 0; e < 4; ++e) {
+            ea.W.w[off[i] + e] = pw[e];
+            ea.W.m[off[i] + e] = pm[e];
+            if (adam) ea.W.v[off[i] + e] = pv[e];
+            if (ea.W.w_bf16) ea.W.w_bf16[off[i] + e] = f32_to_bf16(pw[e]);
+          }
+        }
+      } else if (valid[i]) {
+        for (int e = 0; e < 4; ++e) {
+          if (valid[i] & (1 << e)) {
+            opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
+            ea.W.w[off[i] + e] = pw[e];
+            ea.W.m[off[i] + e] = pm[e];
+            if (adam) ea.W.v[off[i] + e] = pv[e];
+            if (ea.W.w_bf16) ea.W.w_bf16[off[i] + e] = f32_to_bf16(pw[e]);
+          }
+        }
+      }
+      lds[(r + 0) * LD + x] = w[i].x;
+      lds[(r + 1) * LD + x] = w[i].y;
+      lds[(r + 2) * LD + x] = w[i].z;
+      lds[(r + 3) * LD + x] = w[i].w;
+    }
+  }
+};
+
+// ----------------------------------------------------------------- epilogues
+// c[0..n) are the results for (p, q..q+n-1).  vec: 128-bit memory paths allowed
+// (bit 0: out/z/prev, bit 1: parameter arrays); only used when n == 4.
+template <int EPI>
+__device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const float (&c)[4],
+                                         int n, const float* bias, int vec) {
+  if (EPI == EPI_FWD || EPI == EPI_FWD_FF) {
+    float zv[4];
+    for (int e = 0; e < 4; ++e) zv[e] = (bias && e < n) ? __fadd_rn(c[e], bias[e]) : c[e];
+    const int64_t oy = (int64_t)p * ea.ldo + q, oz = (int64_t)p * ea.ldz + q;
+    if (n == 4 && (vec & 1)) {
+      if (ea.z) st4(ea.z + oz, make_float4(zv[0], zv[1], zv[2], zv[3]));
+      st4(ea.out + oy, make_float4(act_fwd(ea.act, zv[0]), act_fwd(ea.act, zv[1]),
+                                   act_fwd(ea.act, zv[2]), act_fwd(ea.act, zv[3])));
+    } else {
+      for (int e = 0; e < n; ++e) {
+        if (ea.z) ea.z[oz + e] = zv[e];
+        ea.out[oy + e] = act_fwd(ea.act, zv[e]);
+      }
+    }
+  } else if (EPI == EPI_DGRAD) {
+    const int64_t oo = (int64_t)p * ea.ldo + q, op = (int64_t)p * ea.ldp + q;
+    if (n == 4 && (vec & 1)) {
+      float4 r = make_float4(c[0], c[1], c[2], c[3]);
+      if (ea.act != OF_ACT_NONE) {
+        const float4 s = ld4(ea.prev + op);
+        r.x = __fmul_rn(r.x, act_grad(ea.act, s.x));
+        r.y = __fmul_rn(r.y, act_grad(ea.act, s.y));
+        r.z = __fmul_rn(r.z, act_grad(ea.act, s.z));
+        r.w = __fmul_rn(r.w, act_grad(ea.act, s.w));
+      }
+      st4(ea.out + oo, r);
+    } else {
+      for (int e = 0; e < n; ++e) {
+        float r = c[e];
+        if (ea.act != OF_ACT_NONE) r = __fmul_rn(r, act_grad(ea.act, ea.prev[op + e]));
+        ea.out[oo + e] = r;
+      }
+    }
+  } else if (EPI == EPI_WGRAD) {
+    const int64_t oo = (int64_t)p * ea.ldo + q;
+    if (n == 4 && (vec & 1)) {
+      float4 r = make_float4(c[0], c[1], c[2], c[3]);
+      if (ea.accumulate) {
+        const float4 o = ld4(ea.out + oo);
+        r.x = __fadd_rn(o.x, r.x); r.y = __fadd_rn(o.y, r.y);
+        r.z = __fadd_rn(o.z, r.z); r.w = __fadd_rn(o.w, r.w);
+      }
+      st4(ea.out + oo, r);
+    } else {
+      for (int e = 0; e < n; ++e)
+        ea.out[oo + e] = ea.accumulate ? __fadd_rn(ea.out[oo + e], c[e]) : c[e];
+    }
+  } else if (EPI == EPI_WGRAD_BF) {
+    const int64_t oo = (int64_t)p * ea.ldo + q;
+    if (n == 4 && (vec & 2)) {
+      float4 g = make_float4(c[0], c[1], c[2], c[3]);
+      if (ea.gW) {
+        const float4 e = ld4(ea.gW + oo);
+        g.x = __fadd_rn(e.x, g.x); g.y = __fadd_rn(e.y, g.y);
+        g.z = __fadd_rn(e.z, g.z); g.w = __fadd_rn(e.w, g.w);
+      }
+      update4(ea.opt, ea.W, g, oo);
+    } else {
+      for (int e = 0; e < n; ++e) {
+        const float g = ea.gW ? __fadd_rn(ea.gW[oo + e], c[e]) : c[e];
+        update1(ea.opt, ea.W, g, oo + e);
+      }
+    }
+  }
+}
+
+// Bias gradient of output row p (wgrad): store / accumulate, or update the bias.
+template <int EPI>
+__device__ __forceinline__ void bias_epilogue(const EpiArgs& ea, int p, float g) {
+  if (EPI == EPI_WGRAD) {
+    ea.db[p] = ea.accumulate ? __fadd_rn(ea.db[p], g) : g;
+  } else if (EPI == EPI_WGRAD_BF) {
+    update1(ea.opt, ea.b, ea.gb ? __fadd_rn(ea.gb[p], g) : g, p);
+  }
+}
+
+// -------------------------------------------------------------------- kernel
+template <class T, int EPI>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, int r_split,
+                                                   float* partial, int vec_ops, int vec_epi) {
+  constexpr bool A_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF || EPI == EPI_DGRAD);
+  constexpr bool B_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF);
+  constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
+  // Forward-fusion also keeps the updated bias slice of its column tile.
+  constexpr int SMEM = T::SMX + (EPI == EPI_FWD_FF ? T::BQ : 0);
+  static_assert(SMEM * 4 <= 64 * 1024, "LDS per workgroup");
+  __shared__ __attribute__((aligned(16))) float smem[SMEM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wp = wave % T::WP, wq = (wave / T::WP) % T::WQ, wr = wave / (T::WP * T::WQ);
+  const int p0 = blockIdx.x * T::BP, q0 = blockIdx.y * T::BQ;
+  const int split = blockIdx.z, S = gridDim.z;
+  const int rbeg = split * r_split;
+  const int rend = min(pr.R, rbeg + r_split);
+  const int nch = (rend - rbeg + T::BR - 1) / T::BR;
+  const bool vecA = vec_ops & 1, vecB = vec_ops & 2;
+  const bool do_db = WG && ea.with_db && blockIdx.y == 0;
+
+  // Buffer b (0/1) of the A and B tiles: A at b*STAGE, B at b*STAGE + BR*LDA.
+  constexpr int STAGE = T::BR * (T::LDA + T::LDB);
+  constexpr int BOFF = T::BR * T::LDA;
+  float* bias_s = smem + T::SMX;  // valid for forward-fusion only
+
+  floatx16 acc[T::TP][T::TQ];
+#pragma unroll
+  for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TQ; ++j)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) acc[i][j][k] = 0.f;
+
+  TileLoad<T::BP, T::BR, A_RC> la;
+  TileLoad<T::BQ, T::BR, B_RC> lb;
+  FFTileLoad<T::BQ, T::BR> lf;
+  const int64_t ldw = pr.b_sq;  // FF: W row stride (= K)
+
+  float dbsum = 0.f;
+
+  la.load(pr.A, pr.a_sp, pr.a_sr, p0, pr.P, rbeg, rend, vecA, tid);
+  if (EPI == EPI_FWD_FF) {
+    lf.load(ea, ldw, q0, pr.Q, rbeg, rend, vecB, tid);
+    lf.apply(ea, smem + BOFF, tid);
+  } else {
+    lb.load(pr.B, pr.b_sq, pr.b_sr, q0, pr.Q, rbeg, rend, vecB, tid);
+    lb.store(smem + BOFF, tid);
+  }
+  la.store(smem, tid);
+  __syncthreads();
+
+  for (int c = 0; c < nch; ++c) {
+    const int cur = c & 1;
+    const bool more = c + 1 < nch;
+    if (more) {
+      const int rn = rbeg + (c + 1) * T::BR;
+      la.load(pr.A, pr.a_sp, pr.a_sr, p0, pr.P, rn, rend, vecA, tid);
+      if (EPI == EPI_FWD_FF) lf.load(ea, ldw, q0, pr.Q, rn, rend, vecB, tid);
+      else lb.load(pr.B, pr.b_sq, pr.b_sr, q0, pr.Q, rn, rend, vecB, tid);
+    }
+    const float* a_s = smem + cur * STAGE;
+    const float* b_s = smem + cur * STAGE + BOFF;
+#pragma unroll
+    for (int kk = 0; kk < T::RW; kk += 2) {
+      const int r = wr * T::RW + kk + (lane >> 5);
+      float a[T::TP], b[T::TQ];
+#pragma unroll
+      for (int i = 0; i < T::TP; ++i) a[i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
+#pragma unroll
+      for (int j = 0; j < T::TQ; ++j) b[j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
+#pragma unroll
+      for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TQ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (do_db && tid < T::BP) {
+      // Column sums of dZ for this tile's output rows, in reduction order.
+#pragma unroll 4
+      for (int r = 0; r < T::BR; ++r) dbsum = __fadd_rn(dbsum, a_s[r * T::LDA + tid]);
+    }
+    if (more) {
+      float* nxt = smem + (cur ^ 1) * STAGE;
+      la.store(nxt, tid);
+      if (EPI == EPI_FWD_FF) lf.apply(ea, nxt + BOFF, tid);
+      else lb.store(nxt + BOFF, tid);
+    }
+    __syncthreads();
+  }
+
+  // Stage the accumulators (MFMA 32x32 layout: lane holds column lane%32 and
+  // rows 8*(k/4) + 4*(lane/32) + k%4) through LDS in row-major order.
+  float* Cs = smem;
+#pragma unroll
+  for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TQ; ++j)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int p = wp * T::WTP + i * 32 + (k >> 2) * 8 + (lane >> 5) * 4 + (k & 3);
+        const int q = wq * T::WTQ + j * 32 + (lane & 31);
+        Cs[(wr * T::BP + p) * T::LDC + q] = acc[i][j][k];
+      }
+
+  // Forward-fusion bias: updated once per column tile, by the split-0 workgroup.
+  const bool ff_bias = (EPI == EPI_FWD_FF) && ea.b.w != nullptr;
+  if (ff_bias && split == 0 && tid < T::BQ && q0 + tid < pr.Q)
+    bias_s[tid] = update1(ea.opt, ea.b, ea.gb[q0 + tid], q0 + tid);
+  __syncthreads();
+
+  const float* bias_base = nullptr;
+  if (EPI == EPI_FWD) bias_base = ea.bias;
+  constexpr int NQ4 = T::BQ / 4;
+  for (int idx = tid; idx < T::BP * NQ4; idx += 256) {
+    const int p = idx / NQ4, q = (idx % NQ4) * 4;
+    const int gp = p0 + p, gq = q0 + q;
+    if (gp >= pr.P || gq >= pr.Q) continue;
+    float c[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float s = Cs[p * T::LDC + q + e];
+#pragma unroll
+      for (int w2 = 1; w2 < T::WR; ++w2) s = __fadd_rn(s, Cs[(w2 * T::BP + p) * T::LDC + q + e]);
+      c[e] = s;
+    }
+    const int n = min(4, pr.Q - gq);
+    if (S > 1) {
+      float* dst = partial + ((int64_t)split * pr.P + gp) * pr.Q + gq;
+      if (n == 4 && (pr.Q & 3) == 0) st4(dst, make_float4(c[0], c[1], c[2], c[3]));
+      else for (int e = 0; e < n; ++e) dst[e] = c[e];
+    } else {
+      const float* bias = nullptr;
+      if (EPI == EPI_FWD && bias_base) bias = bias_base + gq;
+      if (EPI == EPI_FWD_FF && ff_bias) bias = bias_s + q;
+      epilogue<EPI>(ea, gp, gq, c, n, bias, vec_epi);
+    }
+  }
+  if (do_db && tid < T::BP && p0 + tid < pr.P) {
+    if (S > 1) partial[(int64_t)S * pr.P * pr.Q + (int64_t)split * pr.P + p0 + tid] = dbsum;
+    else bias_epilogue<EPI>(ea, p0 + tid, dbsum);
+  }
+}
+
+// Sum the split partials in split order, then run the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void split_reduce_kernel(int P, int Q, int S, EpiArgs ea,
+                                                           const float* __restrict__ partial,
+                                                           int vec_epi, int with_db) {
+  const int nq4 = (Q + 3) / 4;
+  const int64_t total = (int64_t)P * nq4;
+  const int64_t PQ = (int64_t)P * Q;
+  for (int64_t idx = blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
+    const int p = (int)(idx / nq4), q = (int)(idx % nq4) * 4;
+    const int n = min(4, Q - q);
+    float c[4] = {0.f, 0.f, 0.f, 0.f};
+    const float* src = partial + (int64_t)p * Q + q;
+    if (n == 4 && (Q & 3) == 0) {
+      float4 s = ld4(src);
+      for (int k = 1; k < S; ++k) {
+        const float4 t = ld4(src + k * PQ);
+        s.x = __fadd_rn(s.x, t.x); s.y = __fadd_rn(s.y, t.y);
+        s.z = __fadd_rn(s.z, t.z); s.w = __fadd_rn(s.w, t.w);
+      }
+      c[0] = s.x; c[1] = s.y; c[2] = s.z; c[3] = s.w;
+    } else {
+      for (int e = 0; e < n; ++e) {
+        float s = src[e];
+        for (int k = 1; k < S; ++k) s = __fadd_rn(s, src[k * PQ + e]);
+        c[e] = s;
+      }
+    }
+    const float* bias = nullptr;
+    if ((EPI == EPI_FWD || EPI == EPI_FWD_FF) && ea.bias) bias = ea.bias + q;
+    epilogue<EPI == EPI_FWD_FF ? EPI_FWD : EPI>(ea, p, q, c, n, bias, vec_epi);
+  }
+  if (with_db) {
+    const float* dbp = partial + (int64_t)S * PQ;
+    for (int p = blockIdx.x * 256 + threadIdx.x; p < P; p += gridDim.x * 256) {
+      float s = dbp[p];
+      for (int k = 1; k < S; ++k) s = __fadd_rn(s, dbp[(int64_t)k * P + p]);
+      bias_epilogue<EPI>(ea, p, s);
+    }
+  }
+}
+
+// --------------------------------------------------------------- host side
+struct GemmCfg {
+  int tile;
+  int S;        // grid-level reduction splits
+  int r_split;  // reduction elements per split (multiple of the tile's BR)
+};
+
+static int64_t ntiles(int t, int P, int Q) {
+  return (int64_t)((P + kTileBP[t] - 1) / kTileBP[t]) * ((Q + kTileBQ[t] - 1) / kTileBQ[t]);
+}
+
+// The tiling depends only on (kind class, P, Q, R): the fused and unfused
+// variants of a contraction always share it, so their sums are identical.
+static GemmCfg select_cfg(int kind, int P, int Q, int R) {
+  const bool fwd = (kind == EPI_FWD || kind == EPI_FWD_FF);
+  const bool wg = (kind == EPI_WGRAD || kind == EPI_WGRAD_BF);
+  int t;
+  if ((fwd && P <= 256) || (kind == EPI_DGRAD && P <= 64)) {
+    // Forward: one row tile covers all of M, so forward-fusion has one owner per W element.
+    t = P <= 32 ? TI_32x32 : P <= 64 ? TI_64x32 : P <= 128 ? TI_128x64 : TI_256x32;
+  } else if (wg && R <= 512) {
+    // Short reductions: the epilogue's parameter traffic dominates; small tiles, many workgroups.
+    t = ntiles(TI_64x64, P, Q) >= 256 ? TI_64x64 : TI_32x32;
+  } else {
+    const int order[4] = {TI_128x128, TI_128x64, TI_64x64, TI_32x32};
+    t = TI_32x32;
+    for (int i = 0; i < 4; ++i)
+      if (ntiles(order[i], P, Q) >= 256) { t = order[i]; break; }
+  }
+  const int BR = kTileBR[t];
+  const int64_t nt = ntiles(t, P, Q);
+  const int64_t target = 1024;
+  int S = (int)std::max<int64_t>(1, (target + nt - 1) / nt);
+  const int maxS = std::max(1, R / (4 * BR));  // at least 4 chunks per split
+  S = std::min(S, std::min(maxS, 256));
+  int r_split = (((R + S - 1) / S) + BR - 1) / BR * BR;
+  S = (R + r_split - 1) / r_split;
+  return GemmCfg{t, S, r_split};
+}
+
+size_t gemm_workspace_bytes(int kind, int P, int Q, int R) {
+  const GemmCfg c = select_cfg(kind, P, Q, R);
+  if (c.S <= 1) return 0;
+  return (size_t)c.S * ((size_t)P * Q + P) * sizeof(float);
+}
+
+template <class T, int EPI>
+static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                           int vec_ops, int vec_epi, hipStream_t stream) {
+  dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
+  hipLaunchKernelGGL((gemm_kernel<T, EPI>), grid, dim3(256), 0, stream, pr, ea, c.r_split,
+                     (float*)ws, vec_ops, vec_epi);
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                              int vec_ops, int vec_epi, hipStream_t s) {
+  switch (c.tile) {
+    case TI_32x32: return launch_t<T32x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_64x32: return launch_t<T64x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_64x64: return launch_t<T64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_128x64: return launch_t<T128x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_128x128:
+      // Never chosen for a forward with M <= 256, the only forward-fusion case.
+      if constexpr (EPI == EPI_FWD_FF) return hipErrorInvalidValue;
+      else return launch_t<T128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_256x32: return launch_t<T256x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int EPI>
+static hipError_t launch_reduce(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea,
+                                void* ws, int vec_epi, int with_db, hipStream_t s) {
+  const int64_t work = (int64_t)pr.P * ((pr.Q + 3) / 4);
+  const int blocks = (int)std::min<int64_t>(2048, std::max<int64_t>(1, (work + 255) / 256));
+  hipLaunchKernelGGL((split_reduce_kernel<EPI>), dim3(blocks), dim3(256), 0, s, pr.P, pr.Q, c.S,
+                     ea, (const float*)ws, vec_epi, with_db);
+  return hipGetLastError();
+}
+
+static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* vec_epi) {
+  // Operand tiles: 128-bit loads need a 16B-aligned base and a row stride that
+  // keeps every row 16B aligned.
+  const bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0);
+  bool vb = aligned16(pr.B) && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % 4 == 0);
+  if (kind == EPI_FWD_FF)
+    vb = vb && aligned16(ea.W.w) && aligned16(ea.W.m) && aligned16(ea.gW) &&
+         (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) &&
+         (ea.W.w_bf16 == nullptr || ((uintptr_t)ea.W.w_bf16 & 7u) == 0);
+  int ve = 0;
+  if (aligned16(ea.out) && ea.ldo % 4 == 0 && (ea.z == nullptr || (aligned16(ea.z) && ea.ldz % 4 == 0)) &&
+      (ea.prev == nullptr || (aligned16(ea.prev) && ea.ldp % 4 == 0)))
+    ve |= 1;
+  if (kind == EPI_WGRAD_BF && aligned16(ea.W.w) && aligned16(ea.W.m) && ea.ldo % 4 == 0 &&
+      (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) && (ea.gW == nullptr || aligned16(ea.gW)) &&
+      (ea.W.w_bf16 == nullptr || ((uintptr_t)ea.W.w_bf16 & 7u) == 0))
+    ve |= 2;
+  *vec_epi = ve;
+  return (va ? 1 : 0) | (vb ? 2 : 0);
+}
+
+hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                       hipStream_t stream) {
+  const GemmCfg c = select_cfg(kind, pr.P, pr.Q, pr.R);
+  int vec_epi = 0;
+  const int vec_ops = vec_flags(pr, kind, ea, &vec_epi);
+  const bool wg = (kind == EPI_WGRAD || kind == EPI_WGRAD_BF);
+  const int with_db = wg && ea.with_db;
+  hipError_t e;
+  switch (kind) {
+    case EPI_FWD: e = launch_kind<EPI_FWD>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_FWD_FF: e = launch_kind<EPI_FWD_FF>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_DGRAD: e = launch_kind<EPI_DGRAD>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_WGRAD: e = launch_kind<EPI_WGRAD>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_WGRAD_BF: e = launch_kind<EPI_WGRAD_BF>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (e != hipSuccess || c.S <= 1) return e;
+  EpiArgs er = ea;
+  if (kind == EPI_FWD_FF) er.bias = ea.b.w;  // already updated by the split-0 workgroups
+  switch (kind) {
+    case EPI_FWD: return launch_reduce<EPI_FWD>(c, pr, er, ws, vec_epi, 0, stream);
+    case EPI_FWD_FF: return launch_reduce<EPI_FWD_FF>(c, pr, er, ws, vec_epi, 0, stream);
+    case EPI_DGRAD: return launch_reduce<EPI_DGRAD>(c, pr, er, ws, vec_epi, 0, stream);
+    case EPI_WGRAD: return launch_reduce<EPI_WGRAD>(c, pr, er, ws, vec_epi, with_db, stream);
+    case EPI_WGRAD_BF: return launch_reduce<EPI_WGRAD_BF>(c, pr, er, ws, vec_epi, with_db, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace opfuse

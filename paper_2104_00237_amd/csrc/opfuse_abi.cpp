@@ -1,0 +1,401 @@
+// C ABI of the opfuse library: argument validation (before any HIP call),
+// dispatch to the kernel launchers, thread-local error text.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <unordered_map>
+
+#include "common.h"
+
+using namespace opfuse;
+
+namespace {
+
+thread_local std::string g_err;
+
+of_status fail(of_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+of_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return OF_OK;
+  return fail(OF_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool al4(const void* p) { return (((uintptr_t)p) & 3u) == 0; }
+
+#define REQUIRE(cond, st, ...)                   \
+  do {                                           \
+    if (!(cond)) return fail(st, __VA_ARGS__);   \
+  } while (0)
+
+of_status check_opt(const of_opt* o) {
+  REQUIRE(o != nullptr, OF_EINVAL, "opt is NULL");
+  REQUIRE(o->kind == OF_OPT_SGD || o->kind == OF_OPT_ADAM || o->kind == OF_OPT_ADAMW, OF_EINVAL,
+          "opt->kind %d is not an of_opt_kind", (int)o->kind);
+  REQUIRE(o->step >= 1, OF_EINVAL, "opt->step must be >= 1 (got %lld)", (long long)o->step);
+  REQUIRE(std::isfinite(o->lr) && std::isfinite(o->weight_decay), OF_EINVAL,
+          "opt->lr / weight_decay must be finite");
+  if (o->kind != OF_OPT_SGD) {
+    REQUIRE(o->beta1 >= 0.f && o->beta1 < 1.f && o->beta2 >= 0.f && o->beta2 < 1.f, OF_EINVAL,
+            "opt->beta1 / beta2 must be in [0, 1)");
+  }
+  return OF_OK;
+}
+
+of_status check_param(const of_param* p, const char* name, int64_t numel, int kind, bool need_w) {
+  REQUIRE(p != nullptr, OF_EINVAL, "%s is NULL", name);
+  REQUIRE(p->numel == numel, OF_EINVAL, "%s->numel is %lld, expected %lld", name,
+          (long long)p->numel, (long long)numel);
+  if (need_w) REQUIRE(p->w != nullptr, OF_EINVAL, "%s->w is NULL", name);
+  REQUIRE(p->m != nullptr, OF_EINVAL, "%s->m is NULL", name);
+  if (kind != OF_OPT_SGD) REQUIRE(p->v != nullptr, OF_EINVAL, "%s->v is NULL (Adam needs v)", name);
+  REQUIRE(al4(p->w) && al4(p->m) && al4(p->v), OF_EALIGN, "%s arrays must be 4-byte aligned", name);
+  REQUIRE((((uintptr_t)p->w_bf16) & 1u) == 0, OF_EALIGN, "%s->w_bf16 must be 2-byte aligned", name);
+  return OF_OK;
+}
+
+of_status check_linear(const of_linear_desc* d) {
+  REQUIRE(d != nullptr, OF_EINVAL, "desc is NULL");
+  REQUIRE(d->M >= 1 && d->N >= 1 && d->K >= 1, OF_EINVAL, "M, N, K must be >= 1 (got %lld %lld %lld)",
+          (long long)d->M, (long long)d->N, (long long)d->K);
+  REQUIRE(d->M < (1LL << 31) && d->N < (1LL << 31) && d->K < (1LL << 31), OF_EUNSUPPORTED,
+          "M, N, K must be < 2^31");
+  REQUIRE(d->ldx == 0 || d->ldx >= d->K, OF_EINVAL, "ldx must be 0 or >= K");
+  REQUIRE(d->ldy == 0 || d->ldy >= d->N, OF_EINVAL, "ldy must be 0 or >= N");
+  REQUIRE(d->act == OF_ACT_NONE || d->act == OF_ACT_RELU || d->act == OF_ACT_GELU, OF_EINVAL,
+          "act %d is not an of_act", (int)d->act);
+  REQUIRE(d->dtype == OF_F32 || d->dtype == OF_BF16, OF_EINVAL, "dtype %d is not an of_dtype",
+          (int)d->dtype);
+  REQUIRE(d->dtype == OF_F32, OF_EUNSUPPORTED, "bf16 operands are not supported by this build");
+  return OF_OK;
+}
+
+int64_t ldx_of(const of_linear_desc* d) { return d->ldx ? d->ldx : d->K; }
+int64_t ldy_of(const of_linear_desc* d) { return d->ldy ? d->ldy : d->N; }
+
+int kind_of(int32_t op) {
+  return op == OF_LINEAR_FWD ? EPI_FWD : op == OF_LINEAR_BWD_DATA ? EPI_DGRAD : EPI_WGRAD;
+}
+
+size_t ws_needed(const of_linear_desc* d, int kind) {
+  const int M = (int)d->M, N = (int)d->N, K = (int)d->K;
+  switch (kind) {
+    case EPI_FWD: case EPI_FWD_FF: return gemm_workspace_bytes(kind, M, N, K);
+    case EPI_DGRAD: return gemm_workspace_bytes(kind, M, K, N);
+    default: return gemm_workspace_bytes(kind, N, K, M);
+  }
+}
+
+of_status check_ws(const of_linear_desc* d, int kind, const void* ws, size_t ws_bytes) {
+  const size_t need = ws_needed(d, kind);
+  REQUIRE(ws_bytes >= need, OF_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed",
+          ws_bytes, need);
+  REQUIRE(need == 0 || ws != nullptr, OF_EWORKSPACE, "workspace is NULL");
+  REQUIRE(ws == nullptr || (((uintptr_t)ws) & 15u) == 0, OF_EALIGN, "workspace must be 16-byte aligned");
+  return OF_OK;
+}
+
+EpiArgs empty_epi() {
+  EpiArgs e;
+  memset(&e, 0, sizeof(e));
+  return e;
+}
+
+hipEvent_t side_event() {
+  // One event per thread and device: a wait enqueued by hipStreamWaitEvent is
+  // bound to the record made before it, so re-recording later is safe.
+  thread_local std::unordered_map<int, hipEvent_t> events;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  auto it = events.find(dev);
+  if (it != events.end()) return it->second;
+  hipEvent_t ev = nullptr;
+  if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return nullptr;
+  events[dev] = ev;
+  return ev;
+}
+
+// Launch helpers shared by the entry points (arguments already validated).
+of_status run_fwd(const of_linear_desc* d, const float* x, const float* w, const float* b, float* z,
+                  float* y, void* ws, hipStream_t s) {
+  GemmProblem pr{x, ldx_of(d), 1, w, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
+  EpiArgs ea = empty_epi();
+  ea.out = y; ea.ldo = ldy_of(d);
+  ea.z = z; ea.ldz = ldy_of(d);
+  ea.act = d->act;
+  ea.bias = d->has_bias ? b : nullptr;
+  return hip_status(gemm_launch(EPI_FWD, pr, ea, ws, s), "of_linear_fwd launch");
+}
+
+of_status run_dgrad(const of_linear_desc* d, const float* dz, const float* w, const float* prev,
+                    int32_t act_prev, float* dx, void* ws, hipStream_t s) {
+  // dX[m,k] = sum_n dZ[m,n] W[n,k]: A = dZ (reduction-contiguous), B(k, n) = W[n*K + k].
+  GemmProblem pr{dz, ldy_of(d), 1, w, 1, d->K, (int)d->M, (int)d->K, (int)d->N};
+  EpiArgs ea = empty_epi();
+  ea.out = dx; ea.ldo = ldx_of(d);
+  ea.prev = prev; ea.ldp = ldx_of(d);
+  ea.act = act_prev;
+  return hip_status(gemm_launch(EPI_DGRAD, pr, ea, ws, s), "dgrad launch");
+}
+
+GemmProblem wgrad_problem(const of_linear_desc* d, const float* dz, const float* x) {
+  // dW[n,k] = sum_m dZ[m,n] X[m,k]: A(n, m) = dZ[m*ldy + n], B(k, m) = X[m*ldx + k].
+  return GemmProblem{dz, 1, ldy_of(d), x, 1, ldx_of(d), (int)d->N, (int)d->K, (int)d->M};
+}
+
+of_status check_act_prev(int32_t act_prev, const float* prev) {
+  REQUIRE(act_prev == OF_ACT_NONE || act_prev == OF_ACT_RELU || act_prev == OF_ACT_GELU, OF_EINVAL,
+          "act_prev %d is not an of_act", (int)act_prev);
+  REQUIRE(act_prev == OF_ACT_NONE || prev != nullptr, OF_EINVAL,
+          "prev is NULL but act_prev needs the previous layer's saved tensor");
+  REQUIRE(al4(prev), OF_EALIGN, "prev must be 4-byte aligned");
+  return OF_OK;
+}
+
+}  // namespace
+
+namespace opfuse {
+OptK make_optk(const of_opt& o) {
+  OptK k;
+  k.kind = o.kind;
+  k.lr = o.lr;
+  k.wd = o.weight_decay;
+  k.mom = o.momentum;
+  k.b1 = o.beta1;
+  k.b2 = o.beta2;
+  k.eps = o.eps;
+  k.omb1 = (float)(1.0 - (double)o.beta1);
+  k.omb2 = (float)(1.0 - (double)o.beta2);
+  const double t = (double)o.step;
+  const double bc1 = 1.0 - std::pow((double)o.beta1, t);
+  const double bc2 = 1.0 - std::pow((double)o.beta2, t);
+  k.step_size = o.kind == OF_OPT_SGD ? 0.f : (float)((double)o.lr / bc1);
+  k.rsqrt_bc2 = o.kind == OF_OPT_SGD ? 0.f : (float)(1.0 / std::sqrt(bc2));
+  k.decay = (float)(1.0 - (double)o.lr * (double)o.weight_decay);
+  return k;
+}
+}  // namespace opfuse
+
+extern "C" {
+
+int of_version(void) { return OF_VERSION; }
+
+const char* of_last_error(void) { return g_err.c_str(); }
+
+size_t of_linear_workspace_size(const of_linear_desc* d, int32_t op) {
+  if (check_linear(d) != OF_OK) return 0;
+  if (op < OF_LINEAR_FWD || op > OF_LINEAR_BWD_WEIGHT) {
+    fail(OF_EINVAL, "op %d is not an of_linear_op", (int)op);
+    return 0;
+  }
+  return ws_needed(d, kind_of(op));
+}
+
+of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
+                        float* z, float* y, void* ws, size_t ws_bytes, void* stream) {
+  of_status st = check_linear(d);
+  if (st != OF_OK) return st;
+  REQUIRE(x && W && W->w && y, OF_EINVAL, "x, W, W->w and y are required");
+  REQUIRE(W->numel == d->N * d->K, OF_EINVAL, "W->numel must be N*K");
+  REQUIRE(!d->has_bias || b, OF_EINVAL, "has_bias is set but b is NULL");
+  REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z (its derivative reads Z)");
+  REQUIRE(al4(x) && al4(W->w) && al4(b) && al4(z) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
+  return run_fwd(d, x, W->w, b, z, y, ws, (hipStream_t)stream);
+}
+
+of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_param* W,
+                              const float* gW, const of_param* b, const float* gb,
+                              const of_opt* opt, float* z, float* y, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (opt == nullptr) return of_linear_fwd(d, x, W, b ? b->w : nullptr, z, y, ws, ws_bytes, stream);
+  of_status st = check_linear(d);
+  if (st != OF_OK) return st;
+  if ((st = check_opt(opt)) != OF_OK) return st;
+  REQUIRE(x && y && gW, OF_EINVAL, "x, y and gW are required");
+  if ((st = check_param(W, "W", d->N * d->K, opt->kind, true)) != OF_OK) return st;
+  if (d->has_bias) {
+    if ((st = check_param(b, "b", d->N, opt->kind, true)) != OF_OK) return st;
+    REQUIRE(gb != nullptr, OF_EINVAL, "has_bias is set but gb is NULL");
+  }
+  REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z");
+  REQUIRE(al4(x) && al4(gW) && al4(gb) && al4(z) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_ws(d, EPI_FWD_FF, ws, ws_bytes)) != OF_OK) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  const OptK ok = make_optk(*opt);
+  if (d->M > 256) {
+    // The forward's row tiles cannot cover M: several workgroups read each W
+    // tile.  Apply the identical update as one pass right before the contraction.
+    of_param ps[2] = {*W, d->has_bias ? *b : of_param{}};
+    const float* gs[2] = {gW, gb};
+    hipError_t e = launch_multi_update(d->has_bias ? 2 : 1, ps, gs, ok, s);
+    if (e != hipSuccess) return hip_status(e, "forward-fusion update");
+    return run_fwd(d, x, W->w, d->has_bias ? b->w : nullptr, z, y, ws, s);
+  }
+  GemmProblem pr{x, ldx_of(d), 1, W->w, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
+  EpiArgs ea = empty_epi();
+  ea.out = y; ea.ldo = ldy_of(d);
+  ea.z = z; ea.ldz = ldy_of(d);
+  ea.act = d->act;
+  ea.W = *W;
+  ea.gW = gW;
+  if (d->has_bias) { ea.b = *b; ea.gb = gb; }
+  ea.opt = ok;
+  return hip_status(gemm_launch(EPI_FWD_FF, pr, ea, ws, s), "of_linear_fwd_fused launch");
+}
+
+of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_param* W,
+                             const float* prev, int32_t act_prev, float* dx, void* ws,
+                             size_t ws_bytes, void* stream) {
+  of_status st = check_linear(d);
+  if (st != OF_OK) return st;
+  REQUIRE(dz && W && W->w && dx, OF_EINVAL, "dz, W, W->w and dx are required");
+  REQUIRE(W->numel == d->N * d->K, OF_EINVAL, "W->numel must be N*K");
+  if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
+  REQUIRE(al4(dz) && al4(W->w) && al4(dx), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
+  return run_dgrad(d, dz, W->w, prev, act_prev, dx, ws, (hipStream_t)stream);
+}
+
+of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const float* x, float* dw,
+                               float* db, int32_t accumulate, void* ws, size_t ws_bytes,
+                               void* stream) {
+  of_status st = check_linear(d);
+  if (st != OF_OK) return st;
+  REQUIRE(dz && x && dw, OF_EINVAL, "dz, x and dw are required");
+  REQUIRE(al4(dz) && al4(x) && al4(dw) && al4(db), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_ws(d, EPI_WGRAD, ws, ws_bytes)) != OF_OK) return st;
+  EpiArgs ea = empty_epi();
+  ea.out = dw; ea.ldo = d->K;
+  ea.db = db;
+  ea.with_db = db != nullptr;
+  ea.accumulate = accumulate ? 1 : 0;
+  return hip_status(gemm_launch(EPI_WGRAD, wgrad_problem(d, dz, x), ea, ws, (hipStream_t)stream),
+                    "of_linear_bwd_weight launch");
+}
+
+of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const float* x,
+                              const of_param* W, const of_param* b, const float* gW_partial,
+                              const float* gb_partial, const of_opt* opt, const float* prev,
+                              int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
+                              void* ws_update, size_t ws_update_bytes, void* stream,
+                              void* update_stream) {
+  of_status st = check_linear(d);
+  if (st != OF_OK) return st;
+  if ((st = check_opt(opt)) != OF_OK) return st;
+  REQUIRE(dz && x, OF_EINVAL, "dz and x are required");
+  if ((st = check_param(W, "W", d->N * d->K, opt->kind, true)) != OF_OK) return st;
+  if (b) {
+    if ((st = check_param(b, "b", d->N, opt->kind, true)) != OF_OK) return st;
+  }
+  REQUIRE(al4(dz) && al4(x) && al4(gW_partial) && al4(gb_partial) && al4(dx_prev), OF_EALIGN,
+          "fp32 pointers must be 4-byte aligned");
+  if (dx_prev) {
+    if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
+    if ((st = check_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
+  }
+  if ((st = check_ws(d, EPI_WGRAD_BF, ws_update, ws_update_bytes)) != OF_OK) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  hipStream_t su = s;
+  hipEvent_t ev = nullptr;
+  if (update_stream != nullptr && update_stream != stream) {
+    ev = side_event();
+    REQUIRE(ev != nullptr, OF_EHIP, "could not create the side-stream event");
+    su = (hipStream_t)update_stream;
+  }
+  if (dx_prev) {
+    // Data gradient first, with the old W (the dependency rule after Alg. 3).
+    if ((st = run_dgrad(d, dz, W->w, prev, act_prev, dx_prev, ws, s)) != OF_OK) return st;
+  }
+  if (ev) {
+    if ((st = hip_status(hipEventRecord(ev, s), "hipEventRecord")) != OF_OK) return st;
+    if ((st = hip_status(hipStreamWaitEvent(su, ev, 0), "hipStreamWaitEvent")) != OF_OK) return st;
+  }
+  EpiArgs ea = empty_epi();
+  ea.ldo = d->K;
+  ea.W = *W;
+  ea.gW = gW_partial;
+  if (b) { ea.b = *b; ea.gb = gb_partial; }
+  ea.with_db = b != nullptr;
+  ea.opt = make_optk(*opt);
+  return hip_status(gemm_launch(EPI_WGRAD_BF, wgrad_problem(d, dz, x), ea, ws_update, su),
+                    "of_linear_bwd_fused launch");
+}
+
+of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t g_rows,
+                                      int64_t g_ld, const of_opt* opt, void* stream) {
+  of_status st = check_opt(opt);
+  if (st != OF_OK) return st;
+  REQUIRE(p != nullptr && p->numel >= 1, OF_EINVAL, "p is NULL or p->numel < 1");
+  if ((st = check_param(p, "p", p->numel, opt->kind, true)) != OF_OK) return st;
+  REQUIRE(g != nullptr, OF_EINVAL, "g is NULL");
+  REQUIRE(al4(g), OF_EALIGN, "g must be 4-byte aligned");
+  REQUIRE(g_rows >= 1, OF_EINVAL, "g_rows must be >= 1");
+  REQUIRE(g_ld == 0 || g_ld >= p->numel, OF_EINVAL, "g_ld must be 0 or >= numel");
+  const OptK ok = make_optk(*opt);
+  const hipStream_t s = (hipStream_t)stream;
+  if (g_rows == 1) {
+    const float* gs[1] = {g};
+    return hip_status(launch_multi_update(1, p, gs, ok, s), "of_elementwise_fused_update launch");
+  }
+  return hip_status(launch_rows_update(*p, g, g_rows, g_ld ? g_ld : p->numel, ok, s),
+                    "of_elementwise_fused_update launch");
+}
+
+of_status of_optimizer_step(int32_t n, const of_param* params, const float* const* grads,
+                            const of_opt* opt, void* stream) {
+  of_status st = check_opt(opt);
+  if (st != OF_OK) return st;
+  REQUIRE(n >= 1 && params && grads, OF_EINVAL, "n >= 1, params and grads are required");
+  for (int32_t i = 0; i < n; ++i) {
+    char name[32];
+    snprintf(name, sizeof(name), "params[%d]", (int)i);
+    REQUIRE(params[i].numel >= 1, OF_EINVAL, "%s.numel < 1", name);
+    if ((st = check_param(&params[i], name, params[i].numel, opt->kind, true)) != OF_OK) return st;
+    REQUIRE(grads[i] != nullptr, OF_EINVAL, "grads[%d] is NULL", (int)i);
+    REQUIRE(al4(grads[i]), OF_EALIGN, "grads[%d] must be 4-byte aligned", (int)i);
+  }
+  return hip_status(launch_multi_update(n, params, grads, make_optk(*opt), (hipStream_t)stream),
+                    "of_optimizer_step launch");
+}
+
+of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B, int64_t C,
+                          int64_t ld, float* loss, float* dlogits, void* stream) {
+  REQUIRE(logits && labels && loss && dlogits, OF_EINVAL, "logits, labels, loss, dlogits are required");
+  REQUIRE(B >= 1 && C >= 1, OF_EINVAL, "B and C must be >= 1");
+  REQUIRE(ld == 0 || ld >= C, OF_EINVAL, "ld must be 0 or >= C");
+  REQUIRE(al4(logits) && al4(loss) && al4(dlogits) && (((uintptr_t)labels) & 7u) == 0, OF_EALIGN,
+          "misaligned pointer");
+  return hip_status(launch_xent(logits, labels, B, C, ld ? ld : C, loss, dlogits, (hipStream_t)stream),
+                    "of_xent_fwd_bwd launch");
+}
+
+size_t of_mse_workspace_size(int64_t M, int64_t D) { return mse_ws_bytes(M, D); }
+
+of_status of_mse_fwd_bwd(const float* y, const float* t, int64_t M, int64_t D, int64_t ld,
+                         float* loss, float* dy, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(y && t && loss && dy, OF_EINVAL, "y, t, loss and dy are required");
+  REQUIRE(M >= 1 && D >= 1, OF_EINVAL, "M and D must be >= 1");
+  REQUIRE(ld == 0 || ld >= D, OF_EINVAL, "ld must be 0 or >= D");
+  REQUIRE(al4(y) && al4(t) && al4(loss) && al4(dy), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  const size_t need = mse_ws_bytes(M, D);
+  REQUIRE(ws_bytes >= need && ws != nullptr, OF_EWORKSPACE, "workspace of %zu bytes is smaller than %zu",
+          ws_bytes, need);
+  REQUIRE((((uintptr_t)ws) & 7u) == 0, OF_EALIGN, "workspace must be 8-byte aligned");
+  return hip_status(launch_mse(y, t, M, D, ld ? ld : D, loss, dy, ws, (hipStream_t)stream),
+                    "of_mse_fwd_bwd launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,129 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared
+entry point, and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2104_00237_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "opfuse.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(of_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        pytest.skip("libopfuse.so not built")
+    return L.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in L.exported_names(), f"binding lacks {n}"
+    assert L.of_version() == 1
+
+
+def _desc(M=8, N=16, K=12, **kw):
+    d = L.OfLinearDesc(M, N, K, 0, 0, L.OF_F32, L.OF_ACT_NONE, 0)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+FAKE = 0x10000  # never dereferenced: validation fails before any HIP call
+
+
+def _status(fn, *args):
+    with pytest.raises(L.OpfuseError) as e:
+        fn(*args)
+    return e.value.status
+
+
+def _param(numel, w=FAKE, m=FAKE, v=FAKE):
+    return L.OfParam(w, m, v, None, numel)
+
+
+def test_linear_fwd_validation(lib):
+    W = _param(16 * 12)
+    assert _status(L.of_linear_fwd, None, FAKE, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(M=0), FAKE, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(), None, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(), FAKE, _param(5), None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(act=7), FAKE, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(has_bias=1), FAKE, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(act=L.OF_ACT_GELU), FAKE, W, None, None, FAKE, None, 0,
+                   None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(), FAKE + 2, W, None, None, FAKE, None, 0, None) == L.OF_EALIGN
+    assert _status(L.of_linear_fwd, _desc(ldx=3), FAKE, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd, _desc(dtype=5), FAKE, W, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert "ldx" in L.of_last_error() or "dtype" in L.of_last_error()
+
+
+def test_workspace_query_and_check(lib):
+    d = _desc(M=64, N=8192, K=8192)
+    need = L.of_linear_workspace_size(d, L.OF_LINEAR_FWD)
+    assert need > 0  # a reduction split is used for this shape
+    W = _param(8192 * 8192)
+    assert _status(L.of_linear_fwd, d, FAKE, W, None, None, FAKE, FAKE, need - 4, None) == L.OF_EWORKSPACE
+    assert L.of_linear_workspace_size(_desc(M=0), 0) == 0
+    assert L.of_linear_workspace_size(_desc(), 9) == 0
+
+
+def test_optimizer_validation(lib):
+    opt = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 0)
+    p = _param(100)
+    g = FAKE
+    assert _status(L.of_elementwise_fused_update, p, g, 1, 0, opt, None) == L.OF_EINVAL  # step 0
+    opt.step = 1
+    assert _status(L.of_elementwise_fused_update, _param(100, v=None), g, 1, 0, opt, None) == L.OF_EINVAL
+    assert _status(L.of_elementwise_fused_update, p, None, 1, 0, opt, None) == L.OF_EINVAL
+    assert _status(L.of_elementwise_fused_update, p, g, 0, 0, opt, None) == L.OF_EINVAL
+    assert _status(L.of_elementwise_fused_update, p, g, 2, 50, opt, None) == L.OF_EINVAL
+    bad = L.make_opt(dict(kind="adam", lr=1e-3, beta1=1.5, beta2=0.999, eps=1e-8), 1)
+    assert _status(L.of_elementwise_fused_update, p, g, 1, 0, bad, None) == L.OF_EINVAL
+    bad.kind = 9
+    assert _status(L.of_elementwise_fused_update, p, g, 1, 0, bad, None) == L.OF_EINVAL
+    arr = (L.OfParam * 2)(p, _param(0))
+    grads = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    assert _status(L.of_optimizer_step, 2, arr, grads, opt, None) == L.OF_EINVAL
+    assert _status(L.of_optimizer_step, 0, arr, grads, opt, None) == L.OF_EINVAL
+    sgd = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1)
+    # SGD needs no v; a NULL m is still an error.
+    assert _status(L.of_elementwise_fused_update, _param(10, m=None, v=None), g, 1, 0, sgd,
+                   None) == L.OF_EINVAL
+
+
+def test_fused_entry_validation(lib):
+    d = _desc()
+    W = _param(16 * 12)
+    opt = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1)
+    # forward-fusion needs the pending gradient
+    assert _status(L.of_linear_fwd_fused, d, FAKE, W, None, None, None, opt, None, FAKE, None, 0,
+                   None) == L.OF_EINVAL
+    # backward-fusion: bad act_prev, and a dgrad that needs the saved tensor
+    assert _status(L.of_linear_bwd_fused, d, FAKE, FAKE, W, None, None, None, opt, None, 4, FAKE,
+                   None, 0, None, 0, None, None) == L.OF_EINVAL
+    assert _status(L.of_linear_bwd_fused, d, FAKE, FAKE, W, None, None, None, opt, None,
+                   L.OF_ACT_RELU, FAKE, None, 0, None, 0, None, None) == L.OF_EINVAL
+    opt.step = -1
+    assert _status(L.of_linear_bwd_fused, d, FAKE, FAKE, W, None, None, None, opt, None, 0, None,
+                   None, 0, None, 0, None, None) == L.OF_EINVAL
+    assert "step" in L.of_last_error()
+
+
+def test_loss_validation(lib):
+    assert _status(L.of_xent_fwd_bwd, FAKE, FAKE, 0, 10, 0, FAKE, FAKE, None) == L.OF_EINVAL
+    assert _status(L.of_xent_fwd_bwd, FAKE, FAKE + 4, 4, 10, 0, FAKE, FAKE, None) == L.OF_EALIGN
+    assert _status(L.of_mse_fwd_bwd, FAKE, FAKE, 4, 8, 0, FAKE, FAKE, FAKE, 0, None) == L.OF_EWORKSPACE
+    assert L.of_mse_workspace_size(4, 8) > 0

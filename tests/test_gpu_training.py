@@ -1,0 +1,158 @@
+"""K-step training parity on the GPU: every ordering against the oracle's eager
+run on the same seeded inputs, and the three GPU orderings bit for bit against
+each other.  Steps and counters are compared exactly."""
+import numpy as np
+import pytest
+
+import oracle
+from parity import rel, check_param, check_param_decisions
+from workloads import get_config, reduced_config, make_params, make_batch, make_eval_batch
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _gpu_run(torch, cfg, ordering, steps, dev):
+    from paper_2104_00237_amd.trainer import Trainer
+    tr = Trainer(cfg, make_params(cfg), dev)
+    for t in range(1, steps + 1):
+        x, y = make_batch(cfg, t)
+        tr.step(torch.as_tensor(x).to(dev), torch.as_tensor(y).to(dev), ordering)
+    pending = [op.updated for op in tr.ops]
+    losses = tr.loss_history()
+    if ordering == "ff":
+        tr.flush()
+    xe, ye = make_eval_batch(cfg)
+    ev = tr.eval_loss(torch.as_tensor(xe).to(dev), torch.as_tensor(ye).to(dev))
+    st = tr.state()
+    st.update(losses=losses, eval_loss=ev, pending=pending)
+    return st
+
+
+CASES = [
+    ("mlp3", "full"),
+    ("mlp8x1024", "reduced"),
+    ("linear4x8192", "reduced"),
+]
+
+
+def _cfg(name, how):
+    return reduced_config(name) if how == "reduced" else get_config(name)
+
+
+@pytest.mark.parametrize("name,how", CASES)
+def test_training_parity(gpu, name, how):
+    import torch
+    cfg = _cfg(name, how)
+    K = cfg["steps"]
+    ref = oracle.run(cfg, "eager", steps=K)
+    runs = {o: _gpu_run(torch, cfg, o, K, gpu) for o in ("eager", "ff", "bf")}
+    for o, st in runs.items():
+        assert rel(st["losses"], ref["losses"]) <= TOL, (o, st["losses"], ref["losses"])
+        assert abs(st["eval_loss"] - ref["eval_loss"]) <= TOL * abs(ref["eval_loss"])
+        for k in ref["params"]:
+            check_param(st["params"][k], ref["params"][k], cfg["opt"], K, TOL,
+                        ref["min_sqrt_vhat"].get(k), what=f"{o} {k}")
+            assert rel(st["m"][k], ref["m"][k]) <= TOL, (o, k)
+            if cfg["opt"]["kind"] != "sgd":
+                assert rel(st["v"][k], ref["v"][k]) <= TOL, (o, k)
+            assert st["step"][k] == ref["step"][k] == K
+            assert st["count"][k] == 0
+        assert all(st["updated"])
+    assert not any(runs["ff"]["pending"])   # Alg. 2: every layer pending before the flush
+    # The orderings only move the same updates in time: identical bits on the GPU.
+    for o in ("ff", "bf"):
+        np.testing.assert_array_equal(runs[o]["losses"], runs["eager"]["losses"])
+        for k in ref["params"]:
+            np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
+            np.testing.assert_array_equal(runs[o]["m"][k], runs["eager"]["m"][k])
+            np.testing.assert_array_equal(runs[o]["v"][k], runs["eager"]["v"][k])
+
+
+WINDOWS = [  # full-size workloads: one-step windows starting from the oracle's own state
+    ("mlp8x1024", (0, 1, 9, 19)),
+    ("linear4x8192", (0, 1)),
+]
+
+
+def _mismatch(st, loss, cand_loss, cand, cfg, steps):
+    """None if a GPU state equals one oracle candidate within the parity rules,
+    else the first violated rule."""
+    try:
+        assert rel(loss, [cand_loss]) <= TOL, f"loss {loss} vs {cand_loss}"
+        for k in cand["params"]:
+            check_param(st["params"][k], cand["params"][k], cfg["opt"], steps, TOL,
+                        cand["min_sqrt_vhat"].get(k), what=k)
+            r = rel(st["m"][k], cand["m"][k])
+            assert r <= TOL, f"m {k}: rel {r:.2e}"
+            r = rel(st["v"][k], cand["v"][k])
+            assert r <= TOL, f"v {k}: rel {r:.2e}"
+        return None
+    except AssertionError as e:
+        return str(e)
+
+
+@pytest.mark.parametrize("name,starts", WINDOWS)
+def test_windowed_parity_full_size(gpu, name, starts):
+    """Full-size workloads, whose K-step trajectory is chaotic in float32 (Adam's
+    first steps move eps-dominated elements by O(lr), which shifts later ReLU
+    decisions).  The GPU restarts from the oracle's state after step s (rounded to
+    fp32) and computes step s+1; forward-fusion restarts one update earlier,
+    holding the oracle's gradient of step s as its pending update, so its fused
+    forward applies update s and its flush applies update s+1.
+
+    A backward ReLU decision on a pre-activation within float32 rounding of 0 can
+    go either way, so the oracle enumerates the step's outcomes over its ambiguous
+    decisions (fewest flips first) and each ordering must equal one of them under
+    the parity rules; which one is reported."""
+    import torch
+    from paper_2104_00237_amd.trainer import Trainer
+    cfg = get_config(name)
+    last = max(starts) + 1
+    want = set(starts) | {s - 1 for s in starts if s > 0}
+    ref = oracle.run(cfg, "eager", steps=last, snapshots=want)
+    for s in starts:
+        results = {}
+        for o in ("eager", "ff", "bf"):
+            tr = Trainer(cfg, make_params(cfg), gpu)
+            if o == "ff" and s > 0:
+                a = ref["snapshots"][s - 1]
+                tr.load_state(a["params"], a["m"], a["v"], a["step"],
+                              pending=ref["snapshots"][s]["grad"])
+            else:
+                a = ref["snapshots"][s]
+                tr.load_state(a["params"], a["m"], a["v"], a["step"])
+            x, y = make_batch(cfg, s + 1)
+            tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
+            loss = tr.loss_history()
+            if o == "ff":
+                tr.flush()
+            st = tr.state()
+            assert all(v == s + 1 for v in st["step"].values())
+            results[o] = (st, loss)
+            del tr
+            torch.cuda.empty_cache()
+        np.testing.assert_array_equal(results["bf"][0]["params"]["fc1.weight"],
+                                      results["eager"][0]["params"]["fc1.weight"])
+        matched = {}
+        why = {}
+        for flips, cand_loss, cand in oracle.candidate_steps(cfg, ref["snapshots"][s], s + 1):
+            # One step from the oracle's own state: the sensitivity of this step's
+            # update is set by this outcome's sqrt(v_hat) alone (cand["min_sqrt_vhat"]).
+            for o, (st, loss) in results.items():
+                if o in matched:
+                    continue
+                msg = _mismatch(st, loss, cand_loss, cand, cfg, 1)
+                if msg is None:
+                    matched[o] = flips
+                else:
+                    why.setdefault(o, []).append((len(flips), msg))
+            if len(matched) == len(results):
+                break
+        print(f"{name} step {s + 1}: matched candidates", {o: len(f) for o, f in matched.items()})
+        for o in set(results) - set(matched):
+            for n, msg in why[o][:12]:
+                print(f"  {o}: candidate with {n} flips rejected: {msg}")
+        assert set(matched) == set(results), f"step {s + 1}: no oracle outcome for " \
+            f"{sorted(set(results) - set(matched))}"

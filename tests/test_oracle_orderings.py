@@ -75,7 +75,7 @@ def _shared_model(cfg):
              (L.ReLU(), ["b"], "r2"), (A, ["r2"], "a2"), (L.ReLU(), ["a2"], "r3"),
              (C, ["r3"], "output")]
     params = {p.name: p for op in (A, B, C) for p in op.params}
-    from oracle.run import Model
+    from oracle.train import Model
     return Model(nodes, params, "xent", cfg["opt"]), A
 
 
@@ -159,3 +159,31 @@ def test_whole_model_gradient_finite_differences(name, over):
             flat[i] = old
             num = (lp - lm) / (2 * h)
             assert p.grad.reshape(-1)[i] == pytest.approx(num, rel=1e-5, abs=1e-8), p.name
+
+
+def test_ambiguous_decisions_and_candidates():
+    """A pre-activation placed within float32 rounding of 0 is reported, and the
+    candidate steps are the plain step (no flip) and the flipped one."""
+    from oracle.train import ambiguous_relu_decisions, candidate_steps, Model
+    cfg = reduced_config("mlp3", dims=[4, 3, 2], batch=2, classes=2, steps=1)
+    from workloads import make_batch, make_params
+    init = make_params(cfg)
+    x, _ = make_batch(cfg, 1)
+    # Make z[0, 1] of the first layer tiny: shift its bias so the value is ~1e-12.
+    z = x.astype(np.float64) @ init["fc1.weight"].astype(np.float64).T
+    init["fc1.bias"] = init["fc1.bias"].astype(np.float64)
+    init["fc1.bias"][1] = -z[0, 1] + 1e-12
+    model = new_model(cfg, init=init)
+    dec = ambiguous_relu_decisions(model, x.astype(np.float64))
+    assert [(d[1], d[2]) for d in dec] == [(0, 1)]
+    state = dict(params=init, m={k: np.zeros(np.shape(v)) for k, v in init.items()},
+                 v={k: np.zeros(np.shape(v)) for k, v in init.items()},
+                 step={k: 0 for k in init})
+    cands = list(candidate_steps(cfg, state, 1))
+    assert len(cands) == 2 and cands[0][0] == () and len(cands[1][0]) == 1
+    plain = run(cfg, "eager", steps=1, init=init)
+    for k in plain["params"]:
+        np.testing.assert_array_equal(cands[0][2]["params"][k], plain["params"][k])
+    # the flip moves the first layer's gradient row of unit 1 only
+    d = np.abs(cands[1][2]["params"]["fc1.weight"] - cands[0][2]["params"]["fc1.weight"])
+    assert d[1].max() > 0 and d[0].max() == 0 and d[2].max() == 0
