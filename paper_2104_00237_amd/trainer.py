@@ -111,6 +111,7 @@ class Trainer:
         self.side_done = torch.cuda.Event()
         self._opts = {}
         self.pending_ordering = None
+        self.timer = None   # optional KernelTimer: HIP events around chosen launch classes
 
     # ------------------------------------------------------------ helpers
     def _opt(self, step):
@@ -123,6 +124,11 @@ class Trainer:
         return self.stream.cuda_stream
 
     def _loss(self, y):
+        self._t0("loss", self.stream)
+        self._loss_launch(y)
+        self._t1("loss", self.stream)
+
+    def _loss_launch(self, y):
         out = self.a[-1]
         M, C = out.shape
         loss_ptr = self.losses.data_ptr() + 4 * (self.t % self.losses.numel())
@@ -140,21 +146,35 @@ class Trainer:
     def _bias_ptr(self, op):
         return op.b.w.data_ptr() if op.b is not None else None
 
+    def _t0(self, cls, stream, op=None):
+        if self.timer is not None:
+            self.timer.start(cls, stream, op)
+
+    def _t1(self, cls, stream):
+        if self.timer is not None:
+            self.timer.stop(cls, stream)
+
     def _fwd_plain(self, i, op, x):
+        self._t0("fwd", self.stream, op)
         L.of_linear_fwd(op.desc, self._x(i, x), op.W.p, self._bias_ptr(op), None,
                         self.a[i + 1].data_ptr(), self.ws_main.data_ptr(), self.ws_main_bytes,
                         self._s())
+        self._t1("fwd", self.stream)
 
     def _bwd_data(self, i, op):
         prev = self.a[i].data_ptr() if op.act_prev != "none" else None
+        self._t0("dgrad", self.stream, op)
         L.of_linear_bwd_data(op.desc, self.d[i + 1].data_ptr(), op.W.p, prev,
                              L.ACTS[op.act_prev], self.d[i].data_ptr(), self.ws_main.data_ptr(),
                              self.ws_main_bytes, self._s())
+        self._t1("dgrad", self.stream)
 
     def _bwd_weight(self, i, op, x):
+        self._t0("wgrad", self.stream, op)
         L.of_linear_bwd_weight(op.desc, self.d[i + 1].data_ptr(), self._x(i, x),
                                op.W.g.data_ptr(), op.b.g.data_ptr() if op.b is not None else None,
                                0, self.ws_main.data_ptr(), self.ws_main_bytes, self._s())
+        self._t1("wgrad", self.stream)
 
     # ---------------------------------------------------------- orderings
     def step(self, x, y, ordering):
@@ -186,7 +206,9 @@ class Trainer:
         assert all(p.step + 1 == step for p in ps)
         arr = (L.OfParam * len(ps))(*[p.p for p in ps])
         grads = (L.c_void_p * len(ps))(*[p.g.data_ptr() for p in ps])
+        self._t0("opt", self.stream)
         L.of_optimizer_step(len(ps), arr, grads, self._opt(step), self._s())
+        self._t1("opt", self.stream)
         for p in ps:
             p.step = step
 
@@ -195,11 +217,13 @@ class Trainer:
             if not op.updated:
                 step = op.W.step + 1
                 b = op.b
+                self._t0("fwd_ff", self.stream, op)
                 L.of_linear_fwd_fused(op.desc, self._x(i, x), op.W.p, op.W.g.data_ptr(),
                                       b.p if b is not None else None,
                                       b.g.data_ptr() if b is not None else None,
                                       self._opt(step), None, self.a[i + 1].data_ptr(),
                                       self.ws_main.data_ptr(), self.ws_main_bytes, self._s())
+                self._t1("fwd_ff", self.stream)
                 for p in op.params:
                     p.step = step
                 op.updated = True
@@ -244,11 +268,27 @@ class Trainer:
             b = op.b
             dx = self.d[i].data_ptr() if i > 0 else None
             prev = self.a[i].data_ptr() if (i > 0 and op.act_prev != "none") else None
-            L.of_linear_bwd_fused(op.desc, self.d[i + 1].data_ptr(), self._x(i, x), op.W.p,
-                                  b.p if b is not None else None, None, None, self._opt(step),
-                                  prev, L.ACTS[op.act_prev] if i > 0 else 0, dx,
-                                  self.ws_main.data_ptr(), self.ws_main_bytes,
-                                  self.ws_side.data_ptr(), self.ws_side_bytes, self._s(), side)
+            if self.timer is not None and self.timer.wants("wgrad_bf"):
+                # Same launches, split so that events can bracket the fused kernel on
+                # the update stream: dgrad on S, event, wait, fused wgrad on U.
+                if i > 0:
+                    self._bwd_data(i, op)
+                ev = torch.cuda.Event()
+                ev.record(self.stream)
+                self.side.wait_event(ev)
+                self._t0("wgrad_bf", self.side, op)
+                L.of_linear_bwd_fused(op.desc, self.d[i + 1].data_ptr(), self._x(i, x), op.W.p,
+                                      b.p if b is not None else None, None, None,
+                                      self._opt(step), None, 0, None, None, 0,
+                                      self.ws_side.data_ptr(), self.ws_side_bytes, side, None)
+                self._t1("wgrad_bf", self.side)
+            else:
+                L.of_linear_bwd_fused(op.desc, self.d[i + 1].data_ptr(), self._x(i, x), op.W.p,
+                                      b.p if b is not None else None, None, None,
+                                      self._opt(step), prev, L.ACTS[op.act_prev] if i > 0 else 0,
+                                      dx, self.ws_main.data_ptr(), self.ws_main_bytes,
+                                      self.ws_side.data_ptr(), self.ws_side_bytes, self._s(),
+                                      side)
             for p in op.params:
                 p.step = step
         self.side_done.record(self.side)
@@ -307,3 +347,36 @@ class Trainer:
         self._loss(y)
         torch.cuda.synchronize(self.device)
         return float(self.losses[saved % self.losses.numel()].item())
+
+
+class KernelTimer:
+    """HIP events around chosen launch classes, recorded on the launch's stream."""
+
+    def __init__(self, classes):
+        self.classes = set(classes)
+        self.records = {c: [] for c in self.classes}
+        self._open = {}
+
+    def wants(self, cls):
+        return cls in self.classes
+
+    def start(self, cls, stream, op=None):
+        if cls in self.classes:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            self._open[cls] = (e, op)
+
+    def stop(self, cls, stream):
+        if cls in self.classes:
+            e0, op = self._open.pop(cls)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e1.record(stream)
+            self.records[cls].append((e0, e1, op))
+
+    def clear(self):
+        self.records = {c: [] for c in self.classes}
+
+    def durations(self, cls):
+        """[(milliseconds, op)] of every recorded launch of `cls` (synchronises)."""
+        torch.cuda.synchronize()
+        return [(e0.elapsed_time(e1), op) for e0, e1, op in self.records[cls]]
