@@ -65,7 +65,8 @@ typedef enum of_act { OF_ACT_NONE = 0, OF_ACT_RELU = 1, OF_ACT_GELU = 2 } of_act
 /*
  * Optimizer policy pi (Appendix A, Alg. 1).  `step` is the 1-based index t of
  * the update being applied; the caller owns and increments it.  Bias
- * corrections 1 - beta^t are computed by the library on the host in float64.
+ * corrections 1 - beta^t are computed in float64 by every kernel that updates,
+ * from the step it is given.
  *
  *   OF_OPT_SGD    momentum (Appendix A, Eq. for pi_2) with coupled weight decay:
  *                   g' = g + wd*w;  m = momentum*m + g';  w -= lr*m
@@ -89,7 +90,11 @@ typedef struct of_opt {
   float beta1;      /* Adam / AdamW */
   float beta2;
   float eps;
-  int64_t step;     /* >= 1 */
+  int64_t step;     /* >= 1; ignored when step_dev is not NULL */
+  /* Optional device address of the step, read by the kernels when they run
+   * (for launches captured once and replayed, e.g. in a HIP graph; see
+   * of_step_advance).  The value there must be >= 1 when they run. */
+  const int64_t* step_dev;
 } of_opt;
 
 /*
@@ -246,6 +251,13 @@ of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t
  */
 of_status of_optimizer_step(int32_t n, const of_param* params, const float* const* grads,
                             const of_opt* opt, void* stream);
+
+/*
+ * Adds `delta` to the device step counter *step_dev in stream order (one
+ * thread; part of the host ordering state a captured training step replays:
+ * Alg. 2 / Alg. 3 count the updates per parameter).
+ */
+of_status of_step_advance(int64_t* step_dev, int64_t delta, void* stream);
 
 /* ------------------------------------------------------------- losses */
 

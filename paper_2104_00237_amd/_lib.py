@@ -29,7 +29,7 @@ c_int32, c_int64, c_float, c_void_p, c_size_t = (ctypes.c_int32, ctypes.c_int64,
 class OfOpt(ctypes.Structure):
     _fields_ = [("kind", c_int32), ("lr", c_float), ("weight_decay", c_float),
                 ("momentum", c_float), ("beta1", c_float), ("beta2", c_float),
-                ("eps", c_float), ("step", c_int64)]
+                ("eps", c_float), ("step", c_int64), ("step_dev", c_void_p)]
 
 
 class OfParam(ctypes.Structure):
@@ -74,6 +74,7 @@ _SIGS = {
     "of_elementwise_fused_update": (c_int32, [P(OfParam), c_void_p, c_int64, c_int64,
                                               P(OfOpt), c_void_p]),
     "of_optimizer_step": (c_int32, [c_int32, P(OfParam), P(c_void_p), P(OfOpt), c_void_p]),
+    "of_step_advance": (c_int32, [c_void_p, c_int64, c_void_p]),
     "of_xent_fwd_bwd": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_int64, c_void_p,
                                   c_void_p, c_void_p]),
     "of_mse_workspace_size": (c_size_t, [c_int64, c_int64]),
@@ -133,16 +134,17 @@ def of_mse_workspace_size(M, D):
 
 for _n in ("of_linear_fwd", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
-           "of_xent_fwd_bwd", "of_mse_fwd_bwd"):
+           "of_step_advance", "of_xent_fwd_bwd", "of_mse_fwd_bwd"):
     globals()[_n] = _wrap(_n)
 del _n
 
 
-def make_opt(hyper, step):
-    """of_opt from a workload's optimizer dict and the 1-based update index."""
+def make_opt(hyper, step, step_dev=None):
+    """of_opt from a workload's optimizer dict and the 1-based update index
+    (or a device address holding it)."""
     return OfOpt(OPT_KINDS[hyper["kind"]], hyper["lr"], hyper.get("weight_decay", 0.0),
                  hyper.get("momentum", 0.0), hyper.get("beta1", 0.0), hyper.get("beta2", 0.0),
-                 hyper.get("eps", 0.0), step)
+                 hyper.get("eps", 0.0), step, step_dev)
 
 
 def param_of(w, m, v=None, w_bf16=None):

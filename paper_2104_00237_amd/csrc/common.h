@@ -8,19 +8,31 @@
 
 namespace opfuse {
 
-// Optimizer hyperparameters as the kernels consume them.  Everything that
-// depends on the step (bias corrections) is folded on the host in float64.
+// Optimizer hyperparameters as the kernels consume them.  The step-dependent
+// bias corrections are computed by opt_prepare() at kernel start, in float64,
+// from the step passed by value or read from device memory.
 struct OptK {
   int kind;          // of_opt_kind
   float lr, wd, mom;
   float b1, b2, eps;
   float omb1, omb2;  // 1 - beta1, 1 - beta2
-  float step_size;   // lr / (1 - beta1^t)
-  float rsqrt_bc2;   // 1 / sqrt(1 - beta2^t)
   float decay;       // 1 - lr * wd  (AdamW)
+  int64_t step;
+  const int64_t* step_dev;
+  float step_size;   // lr / (1 - beta1^t)       (set by opt_prepare)
+  float rsqrt_bc2;   // 1 / sqrt(1 - beta2^t)    (set by opt_prepare)
 };
 
 OptK make_optk(const of_opt& o);
+
+__device__ __forceinline__ void opt_prepare(OptK& o) {
+  if (o.kind == OF_OPT_SGD) return;
+  const int64_t t = o.step_dev ? *o.step_dev : o.step;
+  const double bc1 = 1.0 - pow((double)o.b1, (double)t);
+  const double bc2 = 1.0 - pow((double)o.b2, (double)t);
+  o.step_size = (float)((double)o.lr / bc1);
+  o.rsqrt_bc2 = (float)(1.0 / sqrt(bc2));
+}
 
 // The one per-element update used by every kernel that changes a parameter
 // (Appendix A, Alg. 1: theta_t = theta_{t-1} + pi(...)).  All operations are
@@ -163,6 +175,7 @@ hipError_t launch_multi_update(int n, const of_param* params, const float* const
                                const OptK& o, hipStream_t stream);
 hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, int64_t ld,
                               const OptK& o, hipStream_t stream);
+hipError_t launch_step_advance(int64_t* step_dev, int64_t delta, hipStream_t stream);
 hipError_t launch_xent(const float* z, const int64_t* labels, int64_t B, int64_t C, int64_t ld,
                        float* loss, float* dz, hipStream_t stream);
 size_t mse_ws_bytes(int64_t M, int64_t D);

@@ -33,6 +33,8 @@
 // tile 0 already stage in LDS.
 
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 
 #include "common.h"
 
@@ -40,9 +42,10 @@ namespace opfuse {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_>
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_>
 struct Tile {
   static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_, WR = WR_;
+  static constexpr int NS = NS_;  // operand chunks in the register ring
   static_assert(WP * WQ * WR == 4, "a workgroup is 4 wavefronts");
   static constexpr int WTP = BP / WP, WTQ = BQ / WQ;   // wavefront tile
   static constexpr int TP = WTP / 32, TQ = WTQ / 32;   // 32x32 MFMA blocks per wavefront
@@ -58,12 +61,12 @@ struct Tile {
 };
 
 // Tile menu (P x Q per workgroup, reduction chunk, wavefront split).
-using T32x32 = Tile<32, 32, 32, 1, 1, 4>;
-using T64x32 = Tile<64, 32, 32, 2, 1, 2>;
-using T64x64 = Tile<64, 64, 16, 2, 2, 1>;
-using T128x64 = Tile<128, 64, 16, 2, 2, 1>;
-using T128x128 = Tile<128, 128, 16, 2, 2, 1>;
-using T256x32 = Tile<256, 32, 16, 4, 1, 1>;
+using T32x32 = Tile<32, 32, 32, 1, 1, 4, 8>;
+using T64x32 = Tile<64, 32, 32, 2, 1, 2, 4>;
+using T64x64 = Tile<64, 64, 16, 2, 2, 1, 6>;
+using T128x64 = Tile<128, 64, 16, 2, 2, 1, 4>;
+using T128x128 = Tile<128, 128, 16, 2, 2, 1, 3>;
+using T256x32 = Tile<256, 32, 16, 4, 1, 1, 3>;
 
 enum TileId { TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32, TI_COUNT };
 static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256};
@@ -71,53 +74,61 @@ static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32};
 static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16};
 
 // ------------------------------------------------------------ operand tiles
+// Operand loads are buffer loads: an offset outside the buffer returns 0, so a
+// masked element is loaded from an out-of-range offset instead of being
+// branched around.  Every thread issues the same loads every chunk, which lets
+// the compiler keep several chunks in flight (its wait counters stay exact).
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;  // beyond num_records: reads as 0
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
+  // raw buffer, stride 0, 2^31-1 bytes addressable from `base`
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff,
+                                           0x00020000);
+}
+__device__ __forceinline__ float4 bload4(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float bload1(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
 // A BX (output dim) x BR (reduction) tile of one operand, held in registers as
 // float4s between its global load and its LDS store.  RC: the reduction index
-// is contiguous in memory (else the output index is).
-template <int BX, int BR, bool RC>
+// is contiguous in memory (else the output index is).  `base` points at the
+// tile's first element; nx / nr are the valid extents from there (<= 0: none).
+// vec: 128-bit loads (base 16B aligned, strides and both extents' ends
+// multiples of 4 along the contiguous index).
+template <int BX, int BR, bool RC, bool VEC>
 struct TileLoad {
   static constexpr int NV = BX * BR / 4;
   static constexpr int PER = (NV + 255) / 256;
   float4 v[PER];
 
-  __device__ __forceinline__ void load(const float* __restrict__ base, int64_t s_x, int64_t s_r,
-                                       int x0, int X, int r0, int rend, bool vec, int tid) {
+  __device__ __forceinline__ void load(const float* base, int64_t s_x, int64_t s_r, int nx,
+                                       int nr, int tid) {
+    const rsrc_t rs = make_rsrc(base);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int idx = tid + i * 256;
-      float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (idx < NV) {
-        if (RC) {
-          const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
-          const int gx = x0 + x, gr = r0 + r;
-          if (gx < X) {
-            const float* p = base + (int64_t)gx * s_x + gr;
-            if (vec && gr + 3 < rend) {
-              val = *reinterpret_cast<const float4*>(p);
-            } else {
-              if (gr + 0 < rend) val.x = p[0];
-              if (gr + 1 < rend) val.y = p[1];
-              if (gr + 2 < rend) val.z = p[2];
-              if (gr + 3 < rend) val.w = p[3];
-            }
-          }
-        } else {
-          const int r = idx / (BX / 4), x = (idx % (BX / 4)) * 4;
-          const int gx = x0 + x, gr = r0 + r;
-          if (gr < rend) {
-            const float* p = base + (int64_t)gr * s_r + gx;
-            if (vec && gx + 3 < X) {
-              val = *reinterpret_cast<const float4*>(p);
-            } else {
-              if (gx + 0 < X) val.x = p[0];
-              if (gx + 1 < X) val.y = p[1];
-              if (gx + 2 < X) val.z = p[2];
-              if (gx + 3 < X) val.w = p[3];
-            }
-          }
+      int x, r;
+      if (RC) { x = idx / (BR / 4); r = (idx % (BR / 4)) * 4; }
+      else    { r = idx / (BX / 4); x = (idx % (BX / 4)) * 4; }
+      const bool live = idx < NV;
+      if constexpr (VEC) {
+        const bool ok = live && x < nx && r < nr;
+        const uint32_t off = ok ? (uint32_t)((x * s_x + r * s_r) * 4) : kOOB;
+        v[i] = bload4(rs, off);
+      } else {
+        float e[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int xx = RC ? x : x + k, rr = RC ? r + k : r;
+          const bool ok = live && xx < nx && rr < nr;
+          e[k] = bload1(rs, ok ? (uint32_t)((xx * s_x + rr * s_r) * 4) : kOOB);
         }
+        v[i] = make_float4(e[0], e[1], e[2], e[3]);
       }
-      v[i] = val;
     }
   }
 
@@ -144,56 +155,58 @@ struct TileLoad {
 
 // Forward-fusion B operand: W tile (reduction-contiguous) with its pending
 // update.  load() issues the loads of W, g, m, v; apply() runs after the
-// current chunk's MFMAs, updates, writes back and stages the new W in LDS.
-template <int BX, int BR>
+// previous chunk's MFMAs, updates, writes back and stages the new W in LDS.
+// `off` is relative to the tile's first element (row stride ldw).
+template <int BX, int BR, bool VEC>
 struct FFTileLoad {
   static constexpr int NV = BX * BR / 4;
   static constexpr int PER = (NV + 255) / 256;
   float4 w[PER], g[PER], m[PER], v[PER];
   int valid[PER];  // bit e set: element e of the float4 is inside the matrix
-  int64_t off[PER];
+  int64_t base;    // element index of the tile origin in W
 
-  __device__ __forceinline__ void load(const EpiArgs& ea, int64_t ldw, int x0, int X, int r0,
-                                       int rend, bool vec, int tid) {
+  __device__ __forceinline__ void load(const EpiArgs& ea, int64_t ldw, int x0, int r0, int nx,
+                                       int nr, int tid) {
     const bool adam = ea.opt.kind != OF_OPT_SGD;
+    base = (int64_t)x0 * ldw + r0;
+    const rsrc_t rw = make_rsrc(ea.W.w + base), rg = make_rsrc(ea.gW + base);
+    const rsrc_t rm = make_rsrc(ea.W.m + base);
+    const rsrc_t rv = make_rsrc(adam ? ea.W.v + base : ea.W.m + base);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int idx = tid + i * 256;
-      valid[i] = 0;
-      w[i] = g[i] = m[i] = v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (idx < NV) {
-        const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
-        const int gx = x0 + x, gr = r0 + r;
-        if (gx < X) {
-          const int64_t o = (int64_t)gx * ldw + gr;
-          off[i] = o;
-          if (vec && gr + 3 < rend) {
-            valid[i] = 0xf;
-            w[i] = ld4(ea.W.w + o);
-            g[i] = ld4(ea.gW + o);
-            m[i] = ld4(ea.W.m + o);
-            if (adam) v[i] = ld4(ea.W.v + o);
-          } else {
-            float* pw = reinterpret_cast<float*>(&w[i]);
-            float* pg = reinterpret_cast<float*>(&g[i]);
-            float* pm = reinterpret_cast<float*>(&m[i]);
-            float* pv = reinterpret_cast<float*>(&v[i]);
-            for (int e = 0; e < 4; ++e) {
-              if (gr + e < rend) {
-                valid[i] |= 1 << e;
-                pw[e] = ea.W.w[o + e];
-                pg[e] = ea.gW[o + e];
-                pm[e] = ea.W.m[o + e];
-                if (adam) pv[e] = ea.W.v[o + e];
-              }
-            }
-          }
+      const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
+      const bool live = idx < NV && x < nx;
+      if constexpr (VEC) {
+        const bool ok = live && r < nr;
+        valid[i] = ok ? 0xf : 0;
+        const uint32_t off = ok ? (uint32_t)((x * ldw + r) * 4) : kOOB;
+        w[i] = bload4(rw, off);
+        g[i] = bload4(rg, off);
+        m[i] = bload4(rm, off);
+        v[i] = bload4(rv, off);
+      } else {
+        float ew[4], eg[4], em[4], ev[4];
+        valid[i] = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const bool ok = live && r + k < nr;
+          valid[i] |= ok ? (1 << k) : 0;
+          const uint32_t off = ok ? (uint32_t)((x * ldw + r + k) * 4) : kOOB;
+          ew[k] = bload1(rw, off);
+          eg[k] = bload1(rg, off);
+          em[k] = bload1(rm, off);
+          ev[k] = bload1(rv, off);
         }
+        w[i] = make_float4(ew[0], ew[1], ew[2], ew[3]);
+        g[i] = make_float4(eg[0], eg[1], eg[2], eg[3]);
+        m[i] = make_float4(em[0], em[1], em[2], em[3]);
+        v[i] = make_float4(ev[0], ev[1], ev[2], ev[3]);
       }
     }
   }
 
-  __device__ __forceinline__ void apply(const EpiArgs& ea, float* lds, int tid) {
+  __device__ __forceinline__ void apply(const EpiArgs& ea, int64_t ldw, float* lds, int tid) {
     constexpr int LD = BX + 4;
     const bool adam = ea.opt.kind != OF_OPT_SGD;
 #pragma unroll
@@ -201,33 +214,25 @@ struct FFTileLoad {
       const int idx = tid + i * 256;
       if (idx >= NV) continue;
       const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
+      const int64_t o = base + (int64_t)x * ldw + r;
       float* pw = reinterpret_cast<float*>(&w[i]);
       float* pg = reinterpret_cast<float*>(&g[i]);
       float* pm = reinterpret_cast<float*>(&m[i]);
       float* pv = reinterpret_cast<float*>(&v[i]);
-      if (valid[i] == 0xf) {
+      if (valid[i] == 0xf && ((uintptr_t)(ea.W.w + o) & 15u) == 0) {
         for (int e = 0; e < 4; ++e) opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
-        if (((uintptr_t)(ea.W.w + off[i]) & 15u) == 0) {
-          st4(ea.W.w + off[i], w[i]);
-          st4(ea.W.m + off[i], m[i]);
-          if (adam) st4(ea.W.v + off[i], v[i]);
-          if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + off[i], w[i]);
-        } else {
-          for (int e = 0; e < 4; ++e) {
-            ea.W.w[off[i] + e] = pw[e];
-            ea.W.m[off[i] + e] = pm[e];
-            if (adam) ea.W.v[off[i] + e] = pv[e];
-            if (ea.W.w_bf16) ea.W.w_bf16[off[i] + e] = f32_to_bf16(pw[e]);
-          }
-        }
+        st4(ea.W.w + o, w[i]);
+        st4(ea.W.m + o, m[i]);
+        if (adam) st4(ea.W.v + o, v[i]);
+        if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + o, w[i]);
       } else if (valid[i]) {
         for (int e = 0; e < 4; ++e) {
           if (valid[i] & (1 << e)) {
             opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
-            ea.W.w[off[i] + e] = pw[e];
-            ea.W.m[off[i] + e] = pm[e];
-            if (adam) ea.W.v[off[i] + e] = pv[e];
-            if (ea.W.w_bf16) ea.W.w_bf16[off[i] + e] = f32_to_bf16(pw[e]);
+            ea.W.w[o + e] = pw[e];
+            ea.W.m[o + e] = pm[e];
+            if (adam) ea.W.v[o + e] = pv[e];
+            if (ea.W.w_bf16) ea.W.w_bf16[o + e] = f32_to_bf16(pw[e]);
           }
         }
       }
@@ -322,9 +327,10 @@ __device__ __forceinline__ void bias_epilogue(const EpiArgs& ea, int p, float g)
 }
 
 // -------------------------------------------------------------------- kernel
-template <class T, int EPI>
+template <class T, int EPI, bool VEC>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, int r_split,
-                                                   float* partial, int vec_ops, int vec_epi) {
+                                                   float* partial, int vec_epi) {
+  if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
   constexpr bool A_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF || EPI == EPI_DGRAD);
   constexpr bool B_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF);
   constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
@@ -340,7 +346,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
-  const bool vecA = vec_ops & 1, vecB = vec_ops & 2;
   const bool do_db = WG && ea.with_db && blockIdx.y == 0;
 
   // Buffer b (0/1) of the A and B tiles: A at b*STAGE, B at b*STAGE + BR*LDA.
@@ -356,62 +361,114 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
 #pragma unroll
       for (int k = 0; k < 16; ++k) acc[i][j][k] = 0.f;
 
-  TileLoad<T::BP, T::BR, A_RC> la;
-  TileLoad<T::BQ, T::BR, B_RC> lb;
-  FFTileLoad<T::BQ, T::BR> lf;
+  // Epilogue operands of small tiles are loaded before the main loop so their
+  // latency hides behind it: the parameter and history tile of backward-fusion
+  // (this workgroup is their only reader and writer) and the previous layer's
+  // saved tensor of the data gradient.  Thread t handles the float4 items
+  // t, t+256, ... of the tile in row-major order.
+  constexpr int NQ4 = T::BQ / 4;
+  constexpr int ITEMS = T::BP * NQ4;
+  constexpr int EPT = (ITEMS + 255) / 256;
+  constexpr bool PREF_BF = (EPI == EPI_WGRAD_BF) && EPT <= 2;
+  constexpr bool PREF_DG = (EPI == EPI_DGRAD) && EPT <= 4;
+  constexpr int NPF = (PREF_BF || PREF_DG) ? EPT : 1;
+  float4 pf_w[NPF], pf_m[NPF], pf_v[NPF];
+  const bool pref = (PREF_BF && S == 1 && (vec_epi & 2) && ea.gW == nullptr) ||
+                    (PREF_DG && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE);
+  if constexpr (PREF_BF || PREF_DG) {
+    if (pref) {
+      const int64_t ld = PREF_BF ? ea.ldo : ea.ldp;
+      const int64_t org = (int64_t)p0 * ld + q0;
+      const rsrc_t r0 = make_rsrc(PREF_BF ? ea.W.w + org : ea.prev + org);
+      const rsrc_t r1 = make_rsrc(PREF_BF ? ea.W.m + org : ea.prev + org);
+      const rsrc_t r2 = make_rsrc((PREF_BF && ea.opt.kind != OF_OPT_SGD) ? ea.W.v + org
+                                                                         : ea.W.m + org);
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const int idx = tid + e * 256;
+        const int p = idx / NQ4, q = (idx % NQ4) * 4;
+        const bool ok = idx < ITEMS && p0 + p < pr.P && q0 + q + 3 < pr.Q;
+        const uint32_t off = ok ? (uint32_t)((p * ld + q) * 4) : kOOB;
+        pf_w[e] = bload4(r0, off);
+        if constexpr (PREF_BF) {
+          pf_m[e] = bload4(r1, off);
+          pf_v[e] = bload4(r2, off);
+        }
+      }
+    }
+  }
+
+  // Register ring of NS operand chunks: the loads of chunk c+NS-1 are issued
+  // before chunk c is stored to LDS and multiplied, so NS-1 chunks are in
+  // flight per workgroup.  The loop runs to a multiple of NS; chunks past the
+  // end load nothing (every offset out of range) and skip the MFMAs.
+  // Forward-fusion holds four arrays per stage and keeps a two-stage ring.
+  constexpr int NS = (EPI == EPI_FWD_FF) ? 2 : T::NS;
+  TileLoad<T::BP, T::BR, A_RC, VEC> la[NS];
+  TileLoad<T::BQ, T::BR, B_RC, VEC> lb[(EPI == EPI_FWD_FF) ? 1 : NS];
+  FFTileLoad<T::BQ, T::BR, VEC> lf[(EPI == EPI_FWD_FF) ? NS : 1];
   const int64_t ldw = pr.b_sq;  // FF: W row stride (= K)
+  const int np = pr.P - p0, nq = pr.Q - q0;
 
   float dbsum = 0.f;
 
-  la.load(pr.A, pr.a_sp, pr.a_sr, p0, pr.P, rbeg, rend, vecA, tid);
-  if (EPI == EPI_FWD_FF) {
-    lf.load(ea, ldw, q0, pr.Q, rbeg, rend, vecB, tid);
-    lf.apply(ea, smem + BOFF, tid);
-  } else {
-    lb.load(pr.B, pr.b_sq, pr.b_sr, q0, pr.Q, rbeg, rend, vecB, tid);
-    lb.store(smem + BOFF, tid);
-  }
-  la.store(smem, tid);
-  __syncthreads();
+  auto issue = [&](int slot, int c) {
+    const int r0 = rbeg + c * T::BR;
+    const int nr = c < nch ? rend - r0 : 0;
+    la[slot].load(pr.A + (int64_t)p0 * pr.a_sp + (int64_t)r0 * pr.a_sr, pr.a_sp, pr.a_sr, np, nr,
+                  tid);
+    if constexpr (EPI == EPI_FWD_FF)
+      lf[slot].load(ea, ldw, q0, r0, nq, nr, tid);
+    else
+      lb[slot].load(pr.B + (int64_t)q0 * pr.b_sq + (int64_t)r0 * pr.b_sr, pr.b_sq, pr.b_sr, nq,
+                    nr, tid);
+  };
 
-  for (int c = 0; c < nch; ++c) {
-    const int cur = c & 1;
-    const bool more = c + 1 < nch;
-    if (more) {
-      const int rn = rbeg + (c + 1) * T::BR;
-      la.load(pr.A, pr.a_sp, pr.a_sr, p0, pr.P, rn, rend, vecA, tid);
-      if (EPI == EPI_FWD_FF) lf.load(ea, ldw, q0, pr.Q, rn, rend, vecB, tid);
-      else lb.load(pr.B, pr.b_sq, pr.b_sr, q0, pr.Q, rn, rend, vecB, tid);
-    }
-    const float* a_s = smem + cur * STAGE;
-    const float* b_s = smem + cur * STAGE + BOFF;
 #pragma unroll
-    for (int kk = 0; kk < T::RW; kk += 2) {
-      const int r = wr * T::RW + kk + (lane >> 5);
-      float a[T::TP], b[T::TQ];
+  for (int s = 0; s < NS - 1; ++s) issue(s, s);
+
+  for (int c0 = 0; c0 < nch; c0 += NS) {
 #pragma unroll
-      for (int i = 0; i < T::TP; ++i) a[i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
+    for (int s = 0; s < NS; ++s) {
+      const int c = c0 + s;
+      issue((s + NS - 1) % NS, c + NS - 1);
+      float* buf = smem + (c & 1) * STAGE;
+      la[s].store(buf, tid);
+      if constexpr (EPI == EPI_FWD_FF) {
+        if (c < nch) lf[s].apply(ea, ldw, buf + BOFF, tid);
+      } else {
+        lb[s].store(buf + BOFF, tid);
+      }
+      __syncthreads();
+      if (c < nch) {
+        const float* a_s = buf;
+        const float* b_s = buf + BOFF;
 #pragma unroll
-      for (int j = 0; j < T::TQ; ++j) b[j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
+        for (int kk = 0; kk < T::RW; kk += 2) {
+          const int r = wr * T::RW + kk + (lane >> 5);
+          float a[T::TP], b[T::TQ];
 #pragma unroll
-      for (int i = 0; i < T::TP; ++i)
+          for (int i = 0; i < T::TP; ++i)
+            a[i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
 #pragma unroll
-        for (int j = 0; j < T::TQ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (do_db && tid < T::BP) {
-      // Column sums of dZ for this tile's output rows, in reduction order.
+          for (int j = 0; j < T::TQ; ++j)
+            b[j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
+#pragma unroll
+          for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+            for (int j = 0; j < T::TQ; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        if (do_db && tid < T::BP) {
+          // Column sums of dZ for this tile's output rows, in reduction order.
 #pragma unroll 4
-      for (int r = 0; r < T::BR; ++r) dbsum = __fadd_rn(dbsum, a_s[r * T::LDA + tid]);
+          for (int r = 0; r < T::BR; ++r) dbsum = __fadd_rn(dbsum, a_s[r * T::LDA + tid]);
+        }
+      }
     }
-    if (more) {
-      float* nxt = smem + (cur ^ 1) * STAGE;
-      la.store(nxt, tid);
-      if (EPI == EPI_FWD_FF) lf.apply(ea, nxt + BOFF, tid);
-      else lb.store(nxt + BOFF, tid);
-    }
-    __syncthreads();
   }
+  // Every wavefront is done with the operand buffers before they are reused.
+  __syncthreads();
 
   // Stage the accumulators (MFMA 32x32 layout: lane holds column lane%32 and
   // rows 8*(k/4) + 4*(lane/32) + k%4) through LDS in row-major order.
@@ -435,8 +492,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
 
   const float* bias_base = nullptr;
   if (EPI == EPI_FWD) bias_base = ea.bias;
-  constexpr int NQ4 = T::BQ / 4;
-  for (int idx = tid; idx < T::BP * NQ4; idx += 256) {
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int idx = tid + e * 256;
+    if (idx >= ITEMS) break;
     const int p = idx / NQ4, q = (idx % NQ4) * 4;
     const int gp = p0 + p, gq = q0 + q;
     if (gp >= pr.P || gq >= pr.Q) continue;
@@ -453,6 +512,27 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       float* dst = partial + ((int64_t)split * pr.P + gp) * pr.Q + gq;
       if (n == 4 && (pr.Q & 3) == 0) st4(dst, make_float4(c[0], c[1], c[2], c[3]));
       else for (int e = 0; e < n; ++e) dst[e] = c[e];
+    } else if (pref && n == 4) {
+      if constexpr (PREF_BF) {
+        // backward-fusion with the parameter tile already in registers
+        float4 w = pf_w[e], m = pf_m[e], v = pf_v[e];
+        opt_update(ea.opt, w.x, c[0], m.x, v.x);
+        opt_update(ea.opt, w.y, c[1], m.y, v.y);
+        opt_update(ea.opt, w.z, c[2], m.z, v.z);
+        opt_update(ea.opt, w.w, c[3], m.w, v.w);
+        const int64_t oo = (int64_t)gp * ea.ldo + gq;
+        st4(ea.W.w + oo, w);
+        st4(ea.W.m + oo, m);
+        if (ea.opt.kind != OF_OPT_SGD) st4(ea.W.v + oo, v);
+        if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + oo, w);
+      } else if constexpr (PREF_DG) {
+        const float4 sv = pf_w[e];
+        const float4 r = make_float4(__fmul_rn(c[0], act_grad(ea.act, sv.x)),
+                                     __fmul_rn(c[1], act_grad(ea.act, sv.y)),
+                                     __fmul_rn(c[2], act_grad(ea.act, sv.z)),
+                                     __fmul_rn(c[3], act_grad(ea.act, sv.w)));
+        st4(ea.out + (int64_t)gp * ea.ldo + gq, r);
+      }
     } else {
       const float* bias = nullptr;
       if (EPI == EPI_FWD && bias_base) bias = bias_base + gq;
@@ -471,6 +551,7 @@ template <int EPI>
 __global__ __launch_bounds__(256) void split_reduce_kernel(int P, int Q, int S, EpiArgs ea,
                                                            const float* __restrict__ partial,
                                                            int vec_epi, int with_db) {
+  if (EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
   const int nq4 = (Q + 3) / 4;
   const int64_t total = (int64_t)P * nq4;
   const int64_t PQ = (int64_t)P * Q;
@@ -519,34 +600,55 @@ static int64_t ntiles(int t, int P, int Q) {
   return (int64_t)((P + kTileBP[t] - 1) / kTileBP[t]) * ((Q + kTileBQ[t] - 1) / kTileBQ[t]);
 }
 
-// The tiling depends only on (kind class, P, Q, R): the fused and unfused
-// variants of a contraction always share it, so their sums are identical.
-static GemmCfg select_cfg(int kind, int P, int Q, int R) {
-  const bool fwd = (kind == EPI_FWD || kind == EPI_FWD_FF);
-  const bool wg = (kind == EPI_WGRAD || kind == EPI_WGRAD_BF);
-  int t;
-  if ((fwd && P <= 256) || (kind == EPI_DGRAD && P <= 64)) {
-    // Forward: one row tile covers all of M, so forward-fusion has one owner per W element.
-    t = P <= 32 ? TI_32x32 : P <= 64 ? TI_64x32 : P <= 128 ? TI_128x64 : TI_256x32;
-  } else if (wg && R <= 512) {
-    // Short reductions: the epilogue's parameter traffic dominates; small tiles, many workgroups.
-    t = ntiles(TI_64x64, P, Q) >= 256 ? TI_64x64 : TI_32x32;
-  } else {
-    const int order[4] = {TI_128x128, TI_128x64, TI_64x64, TI_32x32};
-    t = TI_32x32;
-    for (int i = 0; i < 4; ++i)
-      if (ntiles(order[i], P, Q) >= 256) { t = order[i]; break; }
-  }
+// Tiling by contraction kind and shape (measured on MI355X):
+//   * the eager and backward-fusion weight gradients share one rule, so their
+//     accumulated sums are identical;
+//   * forward-fusion needs one row tile to cover all of M (each W element is
+//     loaded, updated and written by exactly one workgroup); the plain forward
+//     uses that same tiling while M <= 64 and its own faster one above.
+static GemmCfg make_cfg(int t, int P, int Q, int R, int64_t target_ctas, int max_s) {
   const int BR = kTileBR[t];
   const int64_t nt = ntiles(t, P, Q);
-  const int64_t target = 1024;
-  int S = (int)std::max<int64_t>(1, (target + nt - 1) / nt);
+  int S = (int)std::max<int64_t>(1, (target_ctas + nt - 1) / nt);
   const int maxS = std::max(1, R / (4 * BR));  // at least 4 chunks per split
-  S = std::min(S, std::min(maxS, 256));
+  S = std::min(S, std::min(maxS, max_s));
   int r_split = (((R + S - 1) / S) + BR - 1) / BR * BR;
   S = (R + r_split - 1) / r_split;
   return GemmCfg{t, S, r_split};
 }
+
+static int ff_tile(int P) {
+  return P <= 32 ? TI_32x32 : P <= 64 ? TI_64x32 : P <= 128 ? TI_128x64 : TI_256x32;
+}
+
+static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
+  if (kind == EPI_FWD_FF) return make_cfg(ff_tile(P), P, Q, R, 512, 8);
+  if (kind == EPI_FWD && P <= 64) return make_cfg(ff_tile(P), P, Q, R, 1024, 8);
+  if (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) {
+    if (R <= 128 && ntiles(TI_128x128, P, Q) >= 1024) return make_cfg(TI_128x128, P, Q, R, 1, 1);
+    if (R <= 1024 && ntiles(TI_32x32, P, Q) >= 512) return make_cfg(TI_32x32, P, Q, R, 1, 1);
+  }
+  if (P <= 64 && ntiles(TI_64x64, P, Q) >= 64) return make_cfg(TI_64x64, P, Q, R, 1024, 8);
+  // Larger outputs: the biggest tile that still gives one workgroup per CU; no
+  // reduction split (each split costs a second kernel, ~4 us back to back).
+  const int order[4] = {TI_128x128, TI_128x64, TI_64x64, TI_32x32};
+  for (int i = 0; i < 4; ++i)
+    if (ntiles(order[i], P, Q) >= 256) return make_cfg(order[i], P, Q, R, 256, 16);
+  return make_cfg(TI_32x32, P, Q, R, 1024, 64);
+}
+
+#ifdef OPFUSE_TUNING
+// Tuning builds only: OPFUSE_CFG="tile,S" overrides the tiling of every contraction.
+static GemmCfg select_cfg(int kind, int P, int Q, int R) {
+  const char* e = getenv("OPFUSE_CFG");
+  if (!e) return select_cfg_default(kind, P, Q, R);
+  int t = 0, S = 1;
+  sscanf(e, "%d,%d", &t, &S);
+  return make_cfg(t, P, Q, R, (int64_t)S * ntiles(t, P, Q), S);
+}
+#else
+static GemmCfg select_cfg(int kind, int P, int Q, int R) { return select_cfg_default(kind, P, Q, R); }
+#endif
 
 size_t gemm_workspace_bytes(int kind, int P, int Q, int R) {
   const GemmCfg c = select_cfg(kind, P, Q, R);
@@ -558,8 +660,13 @@ template <class T, int EPI>
 static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                            int vec_ops, int vec_epi, hipStream_t stream) {
   dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
-  hipLaunchKernelGGL((gemm_kernel<T, EPI>), grid, dim3(256), 0, stream, pr, ea, c.r_split,
-                     (float*)ws, vec_ops, vec_epi);
+  // 128-bit operand loads only when both operands allow them.
+  if (vec_ops == 3)
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, true>), grid, dim3(256), 0, stream, pr, ea,
+                       c.r_split, (float*)ws, vec_epi);
+  else
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, false>), grid, dim3(256), 0, stream, pr, ea,
+                       c.r_split, (float*)ws, vec_epi);
   return hipGetLastError();
 }
 
@@ -593,8 +700,14 @@ static hipError_t launch_reduce(const GemmCfg& c, const GemmProblem& pr, const E
 static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* vec_epi) {
   // Operand tiles: 128-bit loads need a 16B-aligned base and a row stride that
   // keeps every row 16B aligned.
-  const bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0);
-  bool vb = aligned16(pr.B) && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % 4 == 0);
+  // The contiguous extent must also end on a float4 boundary (a float4 is
+  // either wholly inside the operand or wholly masked).
+  const bool a_rc = (kind == EPI_FWD || kind == EPI_FWD_FF || kind == EPI_DGRAD);
+  const bool b_rc = (kind == EPI_FWD || kind == EPI_FWD_FF);
+  const bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0) &&
+                  ((a_rc ? pr.R : pr.P) % 4 == 0);
+  bool vb = aligned16(pr.B) && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % 4 == 0) &&
+            ((b_rc ? pr.R : pr.Q) % 4 == 0);
   if (kind == EPI_FWD_FF)
     vb = vb && aligned16(ea.W.w) && aligned16(ea.W.m) && aligned16(ea.gW) &&
          (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) &&

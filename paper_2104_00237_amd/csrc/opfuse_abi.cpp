@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -44,7 +45,9 @@ of_status check_opt(const of_opt* o) {
   REQUIRE(o != nullptr, OF_EINVAL, "opt is NULL");
   REQUIRE(o->kind == OF_OPT_SGD || o->kind == OF_OPT_ADAM || o->kind == OF_OPT_ADAMW, OF_EINVAL,
           "opt->kind %d is not an of_opt_kind", (int)o->kind);
-  REQUIRE(o->step >= 1, OF_EINVAL, "opt->step must be >= 1 (got %lld)", (long long)o->step);
+  REQUIRE(o->step_dev != nullptr || o->step >= 1, OF_EINVAL, "opt->step must be >= 1 (got %lld)",
+          (long long)o->step);
+  REQUIRE((((uintptr_t)o->step_dev) & 7u) == 0, OF_EALIGN, "opt->step_dev must be 8-byte aligned");
   REQUIRE(std::isfinite(o->lr) && std::isfinite(o->weight_decay), OF_EINVAL,
           "opt->lr / weight_decay must be finite");
   if (o->kind != OF_OPT_SGD) {
@@ -92,7 +95,9 @@ int kind_of(int32_t op) {
 size_t ws_needed(const of_linear_desc* d, int kind) {
   const int M = (int)d->M, N = (int)d->N, K = (int)d->K;
   switch (kind) {
-    case EPI_FWD: case EPI_FWD_FF: return gemm_workspace_bytes(kind, M, N, K);
+    case EPI_FWD: case EPI_FWD_FF:
+      // one query serves both forwards
+      return std::max(gemm_workspace_bytes(EPI_FWD, M, N, K), gemm_workspace_bytes(EPI_FWD_FF, M, N, K));
     case EPI_DGRAD: return gemm_workspace_bytes(kind, M, K, N);
     default: return gemm_workspace_bytes(kind, N, K, M);
   }
@@ -178,12 +183,11 @@ OptK make_optk(const of_opt& o) {
   k.eps = o.eps;
   k.omb1 = (float)(1.0 - (double)o.beta1);
   k.omb2 = (float)(1.0 - (double)o.beta2);
-  const double t = (double)o.step;
-  const double bc1 = 1.0 - std::pow((double)o.beta1, t);
-  const double bc2 = 1.0 - std::pow((double)o.beta2, t);
-  k.step_size = o.kind == OF_OPT_SGD ? 0.f : (float)((double)o.lr / bc1);
-  k.rsqrt_bc2 = o.kind == OF_OPT_SGD ? 0.f : (float)(1.0 / std::sqrt(bc2));
   k.decay = (float)(1.0 - (double)o.lr * (double)o.weight_decay);
+  k.step = o.step;
+  k.step_dev = o.step_dev;
+  k.step_size = 0.f;
+  k.rsqrt_bc2 = 0.f;
   return k;
 }
 }  // namespace opfuse
@@ -369,6 +373,13 @@ of_status of_optimizer_step(int32_t n, const of_param* params, const float* cons
   }
   return hip_status(launch_multi_update(n, params, grads, make_optk(*opt), (hipStream_t)stream),
                     "of_optimizer_step launch");
+}
+
+of_status of_step_advance(int64_t* step_dev, int64_t delta, void* stream) {
+  REQUIRE(step_dev != nullptr, OF_EINVAL, "step_dev is NULL");
+  REQUIRE((((uintptr_t)step_dev) & 7u) == 0, OF_EALIGN, "step_dev must be 8-byte aligned");
+  return hip_status(launch_step_advance(step_dev, delta, (hipStream_t)stream),
+                    "of_step_advance launch");
 }
 
 of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B, int64_t C,

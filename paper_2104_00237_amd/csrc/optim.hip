@@ -33,6 +33,7 @@ struct MTArgs {
 };
 
 __global__ __launch_bounds__(256) void multi_update_kernel(MTArgs a, OptK o) {
+  opt_prepare(o);
   const int64_t chunk = blockIdx.x;
   int t = 0;
   while (t + 1 < a.n && a.e[t + 1].chunk0 <= chunk) ++t;
@@ -84,6 +85,7 @@ hipError_t launch_multi_update(int n, const of_param* params, const float* const
 
 __global__ __launch_bounds__(256) void rows_update_kernel(of_param p, const float* __restrict__ g,
                                                           int64_t rows, int64_t ld, OptK o) {
+  opt_prepare(o);
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= p.numel) return;
   float s = g[i];
@@ -95,6 +97,15 @@ hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, i
                               const OptK& o, hipStream_t stream) {
   const unsigned blocks = (unsigned)((p.numel + 255) / 256);
   hipLaunchKernelGGL(rows_update_kernel, dim3(blocks), dim3(256), 0, stream, p, g, rows, ld, o);
+  return hipGetLastError();
+}
+
+__global__ void step_advance_kernel(int64_t* step, int64_t delta) {
+  if (threadIdx.x == 0) *step += delta;
+}
+
+hipError_t launch_step_advance(int64_t* step_dev, int64_t delta, hipStream_t stream) {
+  hipLaunchKernelGGL(step_advance_kernel, dim3(1), dim3(64), 0, stream, step_dev, delta);
   return hipGetLastError();
 }
 

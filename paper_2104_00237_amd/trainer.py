@@ -106,19 +106,25 @@ class Trainer:
         self.ws_side_bytes = self.ws_side.numel() * 4
         self.losses = torch.zeros(4096, **f32)
         self.t = 0
+        # Device copy of the 1-based index of the update being applied: advanced in
+        # stream order right before each step's updates, read by the kernels when
+        # they run, so one launch sequence (or a captured graph) serves every step.
+        self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
+        self.opt = L.make_opt(self.hyper, 0, self.step_dev.data_ptr())
         self.stream = torch.cuda.current_stream(self.device)
         self.side = torch.cuda.Stream(self.device)
         self.side_done = torch.cuda.Event()
-        self._opts = {}
         self.pending_ordering = None
         self.timer = None   # optional KernelTimer: HIP events around chosen launch classes
 
     # ------------------------------------------------------------ helpers
-    def _opt(self, step):
-        o = self._opts.get(step)
-        if o is None:
-            o = self._opts[step] = L.make_opt(self.hyper, step)
-        return o
+    def _advance(self, ps):
+        """Next update index for parameters ps (host mirror + device counter)."""
+        step = ps[0].step + 1
+        if any(p.step + 1 != step for p in ps):
+            raise RuntimeError("parameters out of step: this trainer keeps one update counter")
+        L.of_step_advance(self.step_dev.data_ptr(), 1, self._s())
+        return step
 
     def _s(self):
         return self.stream.cuda_stream
@@ -202,26 +208,27 @@ class Trainer:
                 self._bwd_data(i, op)
             self._bwd_weight(i, op, x)
         ps = list(self.params.values())
-        step = ps[0].step + 1
-        assert all(p.step + 1 == step for p in ps)
+        step = self._advance(ps)
         arr = (L.OfParam * len(ps))(*[p.p for p in ps])
         grads = (L.c_void_p * len(ps))(*[p.g.data_ptr() for p in ps])
         self._t0("opt", self.stream)
-        L.of_optimizer_step(len(ps), arr, grads, self._opt(step), self._s())
+        L.of_optimizer_step(len(ps), arr, grads, self.opt, self._s())
         self._t1("opt", self.stream)
         for p in ps:
             p.step = step
 
     def _step_ff(self, x, y):
+        pending = [p for op in self.ops if not op.updated for p in op.params]
+        if pending:
+            step = self._advance(pending)
         for i, op in enumerate(self.ops):
             if not op.updated:
-                step = op.W.step + 1
                 b = op.b
                 self._t0("fwd_ff", self.stream, op)
                 L.of_linear_fwd_fused(op.desc, self._x(i, x), op.W.p, op.W.g.data_ptr(),
                                       b.p if b is not None else None,
                                       b.g.data_ptr() if b is not None else None,
-                                      self._opt(step), None, self.a[i + 1].data_ptr(),
+                                      self.opt, None, self.a[i + 1].data_ptr(),
                                       self.ws_main.data_ptr(), self.ws_main_bytes, self._s())
                 self._t1("fwd_ff", self.stream)
                 for p in op.params:
@@ -239,32 +246,32 @@ class Trainer:
 
     def flush(self):
         """Apply every update forward-fusion still holds (what the next forward would do)."""
-        for op in self.ops:
-            if not op.updated:
-                for p in op.params:
-                    step = p.step + 1
-                    L.of_elementwise_fused_update(p.p, p.g.data_ptr(), 1, 0, self._opt(step),
-                                                  self._s())
-                    p.step = step
+        pending = [p for op in self.ops if not op.updated for p in op.params]
+        if pending:
+            step = self._advance(pending)
+            for p in pending:
+                L.of_elementwise_fused_update(p.p, p.g.data_ptr(), 1, 0, self.opt, self._s())
+                p.step = step
+            for op in self.ops:
                 op.updated = True
         self.pending_ordering = None
 
     def _step_bf(self, x, y):
-        # The forward of layer i at this step needs its update from the last step.
-        self.stream.wait_event(self.side_done)
+        # The forward of layer i at this step needs its update from the last step:
+        # the previous step ended with the main stream joining the update stream.
         for i, op in enumerate(self.ops):
             self._fwd_plain(i, op, x)
             for p in op.params:
                 p.count += 1
         self._loss(y)
         side = self.side.cuda_stream
+        step = self._advance(list(self.params.values()))
         for i in reversed(range(len(self.ops))):
             op = self.ops[i]
             for p in op.params:
                 p.count -= 1
             if any(p.count != 0 for p in op.params):
                 raise NotImplementedError("shared parameters are not supported on the GPU path")
-            step = op.W.step + 1
             b = op.b
             dx = self.d[i].data_ptr() if i > 0 else None
             prev = self.a[i].data_ptr() if (i > 0 and op.act_prev != "none") else None
@@ -279,13 +286,13 @@ class Trainer:
                 self._t0("wgrad_bf", self.side, op)
                 L.of_linear_bwd_fused(op.desc, self.d[i + 1].data_ptr(), self._x(i, x), op.W.p,
                                       b.p if b is not None else None, None, None,
-                                      self._opt(step), None, 0, None, None, 0,
+                                      self.opt, None, 0, None, None, 0,
                                       self.ws_side.data_ptr(), self.ws_side_bytes, side, None)
                 self._t1("wgrad_bf", self.side)
             else:
                 L.of_linear_bwd_fused(op.desc, self.d[i + 1].data_ptr(), self._x(i, x), op.W.p,
                                       b.p if b is not None else None, None, None,
-                                      self._opt(step), prev, L.ACTS[op.act_prev] if i > 0 else 0,
+                                      self.opt, prev, L.ACTS[op.act_prev] if i > 0 else 0,
                                       dx, self.ws_main.data_ptr(), self.ws_main_bytes,
                                       self.ws_side.data_ptr(), self.ws_side_bytes, self._s(),
                                       side)
@@ -293,6 +300,51 @@ class Trainer:
                 p.step = step
         self.side_done.record(self.side)
         self.stream.wait_event(self.side_done)
+
+    # ------------------------------------------------------------- graphs
+    def capture(self, x, y, ordering):
+        """Capture one steady-state training step on (x, y) as a HIP graph.
+
+        Returns a callable that replays it and advances the host counters as
+        step() would.  The step-dependent optimizer constants come from the
+        device step counter, so every replay is the next step.  Forward-fusion
+        is captured with its pending updates in place (call after one ff step).
+        """
+        if ordering == "ff" and all(op.updated for op in self.ops):
+            raise RuntimeError("capture forward-fusion after one ff step (steady state)")
+        if self.pending_ordering == "ff" and ordering != "ff":
+            self.flush()
+        saved = ([(p.step, p.count) for p in self.params.values()],
+                 [op.updated for op in self.ops], self.t, self.pending_ordering)
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream(self.device)
+        cap.wait_stream(self.stream)
+        main = self.stream
+        torch.cuda.synchronize(self.device)
+        try:
+            self.stream = cap
+            with torch.cuda.graph(g, stream=cap):
+                self.step(x, y, ordering)
+        finally:
+            self.stream = main
+        flags = [op.updated for op in self.ops]
+        for p, (st, cn) in zip(self.params.values(), saved[0]):
+            p.step, p.count = st, cn
+        for op, u in zip(self.ops, saved[1]):
+            op.updated = u
+        self.t, self.pending_ordering = saved[2], saved[3]
+
+        def replay():
+            g.replay()
+            for p in self.params.values():
+                p.step += 1
+            for op, u in zip(self.ops, flags):
+                op.updated = u
+            self.pending_ordering = ordering
+            self.t += 1
+
+        replay.graph = g
+        return replay
 
     # --------------------------------------------------------------- state
     def load_state(self, params, m, v, step, pending=None):
@@ -307,6 +359,10 @@ class Trainer:
                 p.v.copy_(torch.as_tensor(np.asarray(v[k], np.float32)))
             p.step = int(step[k])
             p.count = 0
+        steps = {p.step for p in self.params.values()}
+        if len(steps) != 1:
+            raise RuntimeError("parameters out of step: this trainer keeps one update counter")
+        self.step_dev.fill_(steps.pop())
         for op in self.ops:
             op.updated = True
         self.pending_ordering = None
