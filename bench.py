@@ -190,7 +190,19 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy << 18  # floats
+        src = torch.ones(n, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -238,10 +250,17 @@ def main():
     shape = max(by_shape, key=lambda s: s[0] * s[1])
     durs = by_shape[shape]
     per = next(d for d in launches if (d["N"], d["K"]) == shape)[dom]
-    avg_s = float(np.mean(durs)) / 1e3
+    # Each launch is bracketed by an event pair on its own stream; the pair's own
+    # cost (an empty pair on the same stream) is taken off.
+    from paper_2104_00237_amd.trainer import KernelTimer
+    dom_stream = torch.cuda.Stream() if dom == "wgrad_bf" else torch.cuda.current_stream()
+    marker_ms = KernelTimer.marker_overhead_ms(dom_stream)
+    avg_s = (float(np.mean(durs)) - marker_ms) / 1e3
     roof = kernel_roofline(per[0], per[1], avg_s)
     roof.update(kernel=dom, shape=f"M={cfg['batch']} N={shape[0]} K={shape[1]}",
                 avg_us=round(avg_s * 1e6, 3), launches=len(durs),
+                bracketed_avg_us=round(float(np.mean(durs)) * 1e3, 3),
+                marker_us=round(marker_ms * 1e3, 3),
                 algorithmic_bytes=per[1], algorithmic_flops=per[0],
                 traffic=traffic_for(dom, args.workload))
 

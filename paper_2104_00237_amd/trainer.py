@@ -436,3 +436,17 @@ class KernelTimer:
         """[(milliseconds, op)] of every recorded launch of `cls` (synchronises)."""
         torch.cuda.synchronize()
         return [(e0.elapsed_time(e1), op) for e0, e1, op in self.records[cls]]
+
+    @staticmethod
+    def marker_overhead_ms(stream, samples=50):
+        """Mean elapsed time of an event pair with nothing between it on `stream`:
+        the cost of the markers themselves, which bracketing a kernel adds."""
+        pairs = []
+        for _ in range(samples):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            e1.record(stream)
+            pairs.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in pairs]))
