@@ -229,6 +229,64 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
                               void* ws_update, size_t ws_update_bytes, void* stream,
                               void* update_stream);
 
+/* ------------------------------------------------- convolution layers */
+/*
+ * 3x3 convolutions (cross-correlation, stride 1, zero padding 1) as implicit
+ * GEMMs: x [N,H,W,C] NHWC, filter W [Cout,3,3,C] (KRSC), bias [Cout],
+ * y / dy [N,H,W,Cout].  Workspace: of_conv_workspace_size(d, op).
+ */
+size_t of_conv_workspace_size(const of_conv_desc* d, int32_t op);
+
+/* Forward node of a convolution layer (Fig. 1(a)): y = act(conv(x, W) + b). */
+of_status of_conv_fwd(const of_conv_desc* d, const float* x, const of_param* W, const float* b,
+                      float* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Data gradient with the OLD filter (the dependency rule after Alg. 3):
+ *   dx = conv_transpose(dy, W) * act_prev'(prev),  dx [N,H,W,C];
+ * prev: the previous layer's saved output [N,H,W,C] (ReLU: mask prev > 0), or
+ * NULL with OF_ACT_NONE.
+ */
+of_status of_conv_bwd_data(const of_conv_desc* d, const float* dy, const of_param* W,
+                           const float* prev, int32_t act_prev, float* dx, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* Eager filter gradient: dw [Cout,3,3,C] = sum over n,h,w of dy (x) im2col(x);
+ * db [Cout] = sum of dy (db may be NULL); accumulate = 1 adds. */
+of_status of_conv_bwd_weight(const of_conv_desc* d, const float* dy, const float* x, float* dw,
+                             float* db, int32_t accumulate, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * Backward-fusion for a convolution layer (Section 3 "Backward-Fusion";
+ * Appendix B.2, Alg. 3): the implicit-GEMM filter-gradient contraction whose
+ * epilogue adds gW_partial (may be NULL), applies `opt` (e.g. SGD with
+ * momentum, Appendix A) to W and its history and writes them; the filter
+ * gradient is never stored.  With b != NULL the bias gradient sum(dy)
+ * (+ gb_partial) updates b in the same kernel.  The caller runs the data
+ * gradient (of_conv_bwd_data) first: it needs the old W.
+ */
+of_status of_conv_wgrad_fused(const of_conv_desc* d, const float* dy, const float* x,
+                              const of_param* W, const of_param* b, const float* gW_partial,
+                              const float* gb_partial, const of_opt* opt, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
+ * 2x2 max-pool, stride 2 (H, W even): y [N,H/2,W/2,C]; argmax [N,H/2,W/2,C]
+ * holds the window position 0..3 of the first maximum in row-major window
+ * order (ties keep the earlier position).
+ */
+of_status of_maxpool2x2_fwd(const float* x, int64_t N, int64_t H, int64_t W, int64_t C, float* y,
+                            uint8_t* argmax, void* stream);
+
+/*
+ * Backward of the max-pool: dx [N,H,W,C] gets dy at each window's argmax and 0
+ * elsewhere; with mask_src != NULL (the pool input, a ReLU output) the value
+ * at the argmax is kept only where mask_src > 0 (the ReLU derivative).
+ */
+of_status of_maxpool2x2_bwd(const float* dy, const uint8_t* argmax, const float* mask_src,
+                            int64_t N, int64_t H, int64_t W, int64_t C, float* dx, void* stream);
+
 /* ------------------------------------------------ elementwise optimizer */
 
 /*

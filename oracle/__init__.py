@@ -20,4 +20,5 @@ Parity status per function is stated in each module's header; whole K-step
 trajectories are pinned transitively (component pins + the ordering
 invariant), since the paper prints no worked numeric example.
 """
-from .train import run, new_model, ambiguous_relu_decisions, candidate_steps  # noqa: F401
+from .train import (run, new_model, ambiguous_relu_decisions, candidate_steps,  # noqa: F401
+                    DecisionSearch)

@@ -180,6 +180,17 @@ class Conv3x3(Op):
             y += self.b.value
         return y, xp
 
+    def abs_bound(self, x):
+        """sum over taps and channels of |x||w| + |b|: the scale of the rounding error of y."""
+        n, h, wd, _ = x.shape
+        xp = np.pad(np.abs(x), ((0, 0), (1, 1), (1, 1), (0, 0)))
+        w = np.abs(self.w.value)
+        s = np.zeros((n, h, wd, w.shape[0]))
+        for r in range(3):
+            for c in range(3):
+                s += xp[:, r:r + h, c:c + wd, :] @ w[:, r, c, :].T
+        return s + np.abs(self.b.value) if self.b is not None else s
+
     def backward(self, xp, dy):
         n, h, wd, cout = dy.shape
         w = self.w.value

@@ -350,3 +350,180 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
         min_sqrt_vhat=min_vhat,
         snapshots=snaps,
     )
+
+
+class DecisionSearch:
+    """Eager step t from a snapshot on a chain model, with the backward pass's
+    rounding-sensitive decisions left open and settled node by node.
+
+    A float32 run takes each ReLU mask (z > 0) and each max-pool window choice
+    from values whose rounding error is of the order of u * S, with u = 2^-24
+    and S = sum |x||w| + |b| over the contraction that produced them.  With a
+    factor c for error carried in from earlier layers, a decision is ambiguous
+    when
+      ReLU      |z| < c u S(z);
+      max-pool  an entry q of the window lies within c u (S_p + S_q) of the
+                window's first maximum p and one of the two is positive; the
+                flipped decision routes the gradient to q.
+    Any set of flipped ambiguous decisions is a valid float32 outcome of the
+    step.  At full size there are far too many sets to enumerate, but in a
+    chain the gradient of a parametrised node depends only on the decisions
+    above it.  So the search visits the parametrised nodes from the output
+    down: candidates() yields, for each subset of the open decisions between
+    the node and the one above it (the most ambiguous `max_decisions`, at most
+    `max_flips` flipped, fewest flips first), the node's parameters after the
+    update; accept() settles one subset and moves down; finish() returns the
+    whole state after the step.  The forward pass takes the oracle's own
+    decisions (a flipped one changes a forward value only at rounding level).
+    """
+
+    def __init__(self, cfg, state, t, c=8.0, max_decisions=6, seed=0):
+        x, y = make_batch(cfg, t, seed)
+        x = np.asarray(x, np.float64)
+        y = y if y.dtype == np.int64 else np.asarray(y, np.float64)
+        self.model = model = new_model(cfg, init=state["params"])
+        for k, p in model.params.items():
+            p.m, p.v, p.step = state["m"][k].copy(), state["v"][k].copy(), state["step"][k]
+        self.hyper = cfg["opt"]
+        self.max_decisions = max_decisions
+        nodes = model.nodes
+        prev = "input"
+        for op, ins, out in nodes:
+            if ins != [prev]:
+                raise ValueError("the decision search needs a chain model")
+            prev = out
+        u = 2.0 ** -24
+        self.tape, self.decisions = [], {}
+        h, scale = x, None
+        for i, (op, _, _) in enumerate(nodes):
+            out, ctx = op.forward(h)
+            self.tape.append(ctx)
+            dec = []
+            next_scale = None
+            if isinstance(op, (L.Linear, L.Conv3x3)):
+                next_scale = op.abs_bound(h)
+            elif isinstance(op, L.ReLU) and scale is not None:
+                ratio = np.abs(h) / np.maximum(c * u * scale, 1e-300)
+                for idx in zip(*np.nonzero(ratio < 1.0)):
+                    dec.append((float(ratio[idx]), ("relu", i, tuple(int(a) for a in idx), None)))
+                next_scale = scale
+            elif isinstance(op, L.MaxPool2x2) and scale is not None:
+                arg = ctx[1]
+                win = [h[:, a::2, b::2, :] for a in (0, 1) for b in (0, 1)]
+                sc = [scale[:, a::2, b::2, :] for a in (0, 1) for b in (0, 1)]
+                best = np.choose(arg, win)
+                sbest = np.choose(arg, sc)
+                for q in range(4):
+                    den = np.maximum(c * u * (sbest + sc[q]), 1e-300)
+                    ratio = np.abs(best - win[q]) / den
+                    amb = (ratio < 1.0) & (arg != q) & (np.maximum(best, win[q]) > 0.0)
+                    for idx in zip(*np.nonzero(amb)):
+                        dec.append((float(ratio[idx]),
+                                    ("pool", i, tuple(int(a) for a in idx), q)))
+            if dec:
+                self.decisions[i] = dec
+            h, scale = out, next_scale
+        self.loss, self.g = model.loss_and_grad(h, y)
+        self.pos = len(nodes) - 1      # next node to back-propagate
+        self.grads = {}
+        self.flipped = []
+        self._cache = None
+        self._advance_to_param()
+
+    # -- walking ----------------------------------------------------------
+    def _advance_to_param(self):
+        """Find the next parametrised node at or below self.pos."""
+        k = self.pos
+        while k >= 0 and not self.model.nodes[k][0].params:
+            k -= 1
+        self.node = k if k >= 0 else None
+
+    @property
+    def done(self):
+        return self.node is None
+
+    def current(self):
+        """(node index, parameter names) of the node being settled."""
+        op = self.model.nodes[self.node][0]
+        return self.node, [p.name for p in op.params]
+
+    def open_decisions(self):
+        """The ambiguous decisions between the current node and the one above,
+        most ambiguous first, at most max_decisions of them."""
+        dec = []
+        for j in range(self.node + 1, self.pos + 1):
+            dec += self.decisions.get(j, [])
+        dec.sort(key=lambda d: d[0])
+        return [d[1] for d in dec[: self.max_decisions]]
+
+    def _through(self, subset):
+        """Gradient w.r.t. the current node's output with `subset` flipped, then
+        the node's own backward: (dxs, grads)."""
+        g = self.g
+        for j in range(self.pos, self.node, -1):
+            op = self.model.nodes[j][0]
+            ctx = self.tape[j]
+            mine = [d for d in subset if d[1] == j]
+            if mine and isinstance(op, L.ReLU):
+                op.flip = np.zeros(ctx.shape, bool)
+                for d in mine:
+                    op.flip[d[2]] = True
+                try:
+                    (g,), _ = op.backward(ctx, g)
+                finally:
+                    op.flip = None
+            elif mine:
+                shape, arg = ctx
+                arg = arg.copy()
+                for d in mine:
+                    arg[d[2]] = d[3]
+                (g,), _ = op.backward((shape, arg), g)
+            else:
+                (g,), _ = op.backward(ctx, g)
+        return self.model.nodes[self.node][0].backward(self.tape[self.node], g)
+
+    def candidates(self, max_flips=2):
+        """Yield (flipped decisions, {name: (value, m, v)} after the update) for
+        the current node, fewest flips first."""
+        op = self.model.nodes[self.node][0]
+        dec = self.open_decisions()
+        for n in range(min(max_flips, len(dec)) + 1):
+            for subset in itertools.combinations(dec, n):
+                dxs, grads = self._through(subset)
+                self._cache = (subset, dxs, grads)
+                upd = {}
+                for p, g in zip(op.params, grads):
+                    q = L.Param(p.name, p.value)
+                    q.m, q.v, q.step, q.grad = p.m.copy(), p.v.copy(), p.step, g
+                    apply_optimizer(q, self.hyper)
+                    upd[p.name] = (q.value, q.m, q.v)
+                yield subset, upd
+
+    def accept(self, subset):
+        """Settle the current node's decisions to `subset` and move down."""
+        subset = tuple(subset)
+        if self._cache is not None and self._cache[0] == subset:
+            _, dxs, grads = self._cache
+        else:
+            dxs, grads = self._through(subset)
+        op = self.model.nodes[self.node][0]
+        for p, g in zip(op.params, grads):
+            self.grads[p.name] = g
+        self.flipped += list(subset)
+        self.g = dxs[0]
+        self.pos = self.node - 1
+        self._cache = None
+        self._advance_to_param()
+
+    def finish(self):
+        """State after the step (every node settled): params, m, v, step by name."""
+        if not self.done:
+            raise RuntimeError("nodes left to settle")
+        ps = self.model.params
+        for k, p in ps.items():
+            p.grad = self.grads[k]
+            apply_optimizer(p, self.hyper)
+        return dict(params={k: p.value for k, p in ps.items()},
+                    m={k: p.m for k, p in ps.items()},
+                    v={k: p.v for k, p in ps.items()},
+                    step={k: p.step for k, p in ps.items()})

@@ -19,6 +19,7 @@ OF_F32, OF_BF16 = 0, 1
 OF_ACT_NONE, OF_ACT_RELU, OF_ACT_GELU = 0, 1, 2
 OF_OPT_SGD, OF_OPT_ADAM, OF_OPT_ADAMW = 0, 1, 2
 OF_LINEAR_FWD, OF_LINEAR_BWD_DATA, OF_LINEAR_BWD_WEIGHT = 0, 1, 2
+OF_CONV_FWD, OF_CONV_BWD_DATA, OF_CONV_BWD_WEIGHT = 0, 1, 2
 ACTS = {"none": OF_ACT_NONE, "relu": OF_ACT_RELU, "gelu": OF_ACT_GELU}
 OPT_KINDS = {"sgd": OF_OPT_SGD, "adam": OF_OPT_ADAM, "adamw": OF_OPT_ADAMW}
 
@@ -75,6 +76,20 @@ _SIGS = {
                                               P(OfOpt), c_void_p]),
     "of_optimizer_step": (c_int32, [c_int32, P(OfParam), P(c_void_p), P(OfOpt), c_void_p]),
     "of_step_advance": (c_int32, [c_void_p, c_int64, c_void_p]),
+    "of_conv_workspace_size": (c_size_t, [P(OfConvDesc), c_int32]),
+    "of_conv_fwd": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_void_p, c_void_p,
+                              c_size_t, c_void_p]),
+    "of_conv_bwd_data": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_int32,
+                                   c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_conv_bwd_weight": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_int32, c_void_p, c_size_t, c_void_p]),
+    "of_conv_wgrad_fused": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, P(OfParam), P(OfParam),
+                                      c_void_p, c_void_p, P(OfOpt), c_void_p, c_size_t,
+                                      c_void_p]),
+    "of_maxpool2x2_fwd": (c_int32, [c_void_p, c_int64, c_int64, c_int64, c_int64, c_void_p,
+                                    c_void_p, c_void_p]),
+    "of_maxpool2x2_bwd": (c_int32, [c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64,
+                                    c_int64, c_void_p, c_void_p]),
     "of_xent_fwd_bwd": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_int64, c_void_p,
                                   c_void_p, c_void_p]),
     "of_mse_workspace_size": (c_size_t, [c_int64, c_int64]),
@@ -132,9 +147,15 @@ def of_mse_workspace_size(M, D):
     return load().of_mse_workspace_size(M, D)
 
 
+def of_conv_workspace_size(desc, op):
+    return load().of_conv_workspace_size(ctypes.byref(desc), op)
+
+
 for _n in ("of_linear_fwd", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
-           "of_step_advance", "of_xent_fwd_bwd", "of_mse_fwd_bwd"):
+           "of_step_advance", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
+           "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
+           "of_maxpool2x2_fwd", "of_maxpool2x2_bwd"):
     globals()[_n] = _wrap(_n)
 del _n
 

@@ -141,10 +141,18 @@ enum EpiKind {
   EPI_WGRAD_BF = 4,   // backward-fusion: update W (and b) from c (and sums)
 };
 
+// Convolutions (3x3, stride 1, zero padding 1, NHWC activations, [Cout,3,3,C]
+// filters) run as implicit GEMMs: conv != 0 selects gathered operand addressing
+// instead of the strides above.
+//   forward  C[m, co]   = sum_k X~(m, k) W[co, k]     m=(n,h,w), k=(r,s,c)
+//   dgrad    C[m, c]    = sum_k dY~(m, k) W~(c, k)    k=(r,s,co): dY at (h+1-r, w+1-s)
+//   wgrad    C[co, k]   = sum_m dY[m, co] X~(k, m)
 struct GemmProblem {
   const float* A; int64_t a_sp, a_sr;
   const float* B; int64_t b_sq, b_sr;
   int P, Q, R;
+  int conv;                     // 0: strided operands; 1: convolution gathers
+  int cN, cH, cW, cC, cCout;    // convolution geometry (input N, H, W, C; Cout)
 };
 
 struct EpiArgs {
@@ -176,6 +184,11 @@ hipError_t launch_multi_update(int n, const of_param* params, const float* const
 hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, int64_t ld,
                               const OptK& o, hipStream_t stream);
 hipError_t launch_step_advance(int64_t* step_dev, int64_t delta, hipStream_t stream);
+hipError_t launch_maxpool_fwd(const float* x, int64_t N, int64_t H, int64_t W, int64_t C,
+                              float* y, uint8_t* arg, hipStream_t s);
+hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, const float* mask_src,
+                              int64_t N, int64_t H, int64_t W, int64_t C, float* dx,
+                              hipStream_t s);
 hipError_t launch_xent(const float* z, const int64_t* labels, int64_t B, int64_t C, int64_t ld,
                        float* loss, float* dz, hipStream_t stream);
 size_t mse_ws_bytes(int64_t M, int64_t D);

@@ -33,6 +33,7 @@
 // tile 0 already stage in LDS.
 
 #include <algorithm>
+#include <type_traits>
 #include <cstdio>
 #include <cstdlib>
 
@@ -105,9 +106,9 @@ struct TileLoad {
   static constexpr int PER = (NV + 255) / 256;
   float4 v[PER];
 
-  __device__ __forceinline__ void load(const float* base, int64_t s_x, int64_t s_r, int nx,
-                                       int nr, int tid) {
-    const rsrc_t rs = make_rsrc(base);
+  __device__ __forceinline__ void load(const float* tensor, const GemmProblem&, int64_t s_x,
+                                       int64_t s_r, int x0, int r0, int nx, int nr, int tid) {
+    const rsrc_t rs = make_rsrc(tensor + (int64_t)x0 * s_x + (int64_t)r0 * s_r);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int idx = tid + i * 256;
@@ -148,6 +149,67 @@ struct TileLoad {
           const int r = idx / (BX / 4), x = (idx % (BX / 4)) * 4;
           *reinterpret_cast<float4*>(&lds[r * LD + x]) = v[i];
         }
+      }
+    }
+  }
+};
+
+// Convolution operands gathered from NHWC tensors / KRSC filters.  Element
+// (x, r) of the tile is tensor element (x0 + x, r0 + r) of the implicit GEMM
+// operand; its offset is formed from the convolution geometry, and elements in
+// the zero padding (or past the operand) read from an out-of-range offset.
+// VEC: the channel count along the contiguous index is a multiple of 4, so a
+// float4 never straddles two filter taps.
+enum GatherKind { G_FWD_A = 1, G_DGRAD_A = 2, G_WGRAD_B = 3, G_DGRAD_B = 4 };
+
+template <int KIND>
+__device__ __forceinline__ int64_t gather_off(const GemmProblem& g, int x, int r, bool& ok) {
+  // FWD_A: x = m, r = k = (tap, c).  DGRAD_A: x = m, r = k = (tap, co).
+  // WGRAD_B: x = k = (tap, c), r = m.  DGRAD_B: x = c, r = k = (tap, co).
+  if constexpr (KIND == G_DGRAD_B) {
+    const int co = r % g.cCout, tap = r / g.cCout;
+    return ((int64_t)co * 9 + tap) * g.cC + x;
+  } else {
+    const int m = (KIND == G_WGRAD_B) ? r : x;
+    const int k = (KIND == G_WGRAD_B) ? x : r;
+    const int ch = (KIND == G_DGRAD_A) ? g.cCout : g.cC;
+    const int w = m % g.cW, t = m / g.cW, h = t % g.cH, n = t / g.cH;
+    const int c = k % ch, tap = k / ch, rr = tap / 3, ss = tap % 3;
+    const int hi = (KIND == G_DGRAD_A) ? h + 1 - rr : h + rr - 1;
+    const int wi = (KIND == G_DGRAD_A) ? w + 1 - ss : w + ss - 1;
+    ok = ok && hi >= 0 && hi < g.cH && wi >= 0 && wi < g.cW;
+    return (((int64_t)n * g.cH + hi) * g.cW + wi) * ch + c;
+  }
+}
+
+template <int BX, int BR, bool RC, bool VEC, int KIND>
+struct GatherLoad : TileLoad<BX, BR, RC, VEC> {
+  using Base = TileLoad<BX, BR, RC, VEC>;
+  using Base::v;
+  __device__ __forceinline__ void load(const float* tensor, const GemmProblem& g, int64_t, int64_t,
+                                       int x0, int r0, int nx, int nr, int tid) {
+    const rsrc_t rs = make_rsrc(tensor);
+#pragma unroll
+    for (int i = 0; i < Base::PER; ++i) {
+      const int idx = tid + i * 256;
+      int x, r;
+      if (RC) { x = idx / (BR / 4); r = (idx % (BR / 4)) * 4; }
+      else    { r = idx / (BX / 4); x = (idx % (BX / 4)) * 4; }
+      const bool live = idx < Base::NV;
+      if constexpr (VEC) {
+        bool ok = live && x < nx && r < nr;
+        const int64_t o = gather_off<KIND>(g, x0 + x, r0 + r, ok);
+        v[i] = bload4(rs, ok ? (uint32_t)(o * 4) : kOOB);
+      } else {
+        float e[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int xx = RC ? x : x + k, rr = RC ? r + k : r;
+          bool ok = live && xx < nx && rr < nr;
+          const int64_t o = gather_off<KIND>(g, x0 + xx, r0 + rr, ok);
+          e[k] = bload1(rs, ok ? (uint32_t)(o * 4) : kOOB);
+        }
+        v[i] = make_float4(e[0], e[1], e[2], e[3]);
       }
     }
   }
@@ -327,7 +389,7 @@ __device__ __forceinline__ void bias_epilogue(const EpiArgs& ea, int p, float g)
 }
 
 // -------------------------------------------------------------------- kernel
-template <class T, int EPI, bool VEC>
+template <class T, int EPI, bool VEC, bool CONV>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, int r_split,
                                                    float* partial, int vec_epi) {
   if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
@@ -404,8 +466,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   // end load nothing (every offset out of range) and skip the MFMAs.
   // Forward-fusion holds four arrays per stage and keeps a two-stage ring.
   constexpr int NS = (EPI == EPI_FWD_FF) ? 2 : T::NS;
-  TileLoad<T::BP, T::BR, A_RC, VEC> la[NS];
-  TileLoad<T::BQ, T::BR, B_RC, VEC> lb[(EPI == EPI_FWD_FF) ? 1 : NS];
+  using ALoad = std::conditional_t<
+      CONV && (EPI == EPI_FWD || EPI == EPI_DGRAD),
+      GatherLoad<T::BP, T::BR, true, VEC, EPI == EPI_FWD ? G_FWD_A : G_DGRAD_A>,
+      TileLoad<T::BP, T::BR, A_RC, VEC>>;
+  using BLoad = std::conditional_t<
+      CONV && EPI == EPI_DGRAD, GatherLoad<T::BQ, T::BR, false, VEC, G_DGRAD_B>,
+      std::conditional_t<CONV && WG, GatherLoad<T::BQ, T::BR, false, VEC, G_WGRAD_B>,
+                         TileLoad<T::BQ, T::BR, B_RC, VEC>>>;
+  ALoad la[NS];
+  BLoad lb[(EPI == EPI_FWD_FF) ? 1 : NS];
   FFTileLoad<T::BQ, T::BR, VEC> lf[(EPI == EPI_FWD_FF) ? NS : 1];
   const int64_t ldw = pr.b_sq;  // FF: W row stride (= K)
   const int np = pr.P - p0, nq = pr.Q - q0;
@@ -415,13 +485,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   auto issue = [&](int slot, int c) {
     const int r0 = rbeg + c * T::BR;
     const int nr = c < nch ? rend - r0 : 0;
-    la[slot].load(pr.A + (int64_t)p0 * pr.a_sp + (int64_t)r0 * pr.a_sr, pr.a_sp, pr.a_sr, np, nr,
-                  tid);
+    la[slot].load(pr.A, pr, pr.a_sp, pr.a_sr, p0, r0, np, nr, tid);
     if constexpr (EPI == EPI_FWD_FF)
       lf[slot].load(ea, ldw, q0, r0, nq, nr, tid);
     else
-      lb[slot].load(pr.B + (int64_t)q0 * pr.b_sq + (int64_t)r0 * pr.b_sr, pr.b_sq, pr.b_sr, nq,
-                    nr, tid);
+      lb[slot].load(pr.B, pr, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
   };
 
 #pragma unroll
@@ -661,11 +729,22 @@ static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArg
                            int vec_ops, int vec_epi, hipStream_t stream) {
   dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
   // 128-bit operand loads only when both operands allow them.
+  if constexpr (EPI != EPI_FWD_FF) {
+    if (pr.conv) {
+      if (vec_ops == 3)
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, true, true>), grid, dim3(256), 0, stream, pr, ea,
+                           c.r_split, (float*)ws, vec_epi);
+      else
+        hipLaunchKernelGGL((gemm_kernel<T, EPI, false, true>), grid, dim3(256), 0, stream, pr,
+                           ea, c.r_split, (float*)ws, vec_epi);
+      return hipGetLastError();
+    }
+  }
   if (vec_ops == 3)
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, true>), grid, dim3(256), 0, stream, pr, ea,
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, true, false>), grid, dim3(256), 0, stream, pr, ea,
                        c.r_split, (float*)ws, vec_epi);
   else
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, false>), grid, dim3(256), 0, stream, pr, ea,
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, false, false>), grid, dim3(256), 0, stream, pr, ea,
                        c.r_split, (float*)ws, vec_epi);
   return hipGetLastError();
 }
@@ -704,10 +783,21 @@ static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* ve
   // either wholly inside the operand or wholly masked).
   const bool a_rc = (kind == EPI_FWD || kind == EPI_FWD_FF || kind == EPI_DGRAD);
   const bool b_rc = (kind == EPI_FWD || kind == EPI_FWD_FF);
-  const bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0) &&
-                  ((a_rc ? pr.R : pr.P) % 4 == 0);
+  bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0) &&
+            ((a_rc ? pr.R : pr.P) % 4 == 0);
   bool vb = aligned16(pr.B) && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % 4 == 0) &&
             ((b_rc ? pr.R : pr.Q) % 4 == 0);
+  if (pr.conv) {
+    // gathers: a float4 stays within one filter tap when the channel count along
+    // the contiguous index is a multiple of 4
+    const bool cin4 = pr.cC % 4 == 0, cout4 = pr.cCout % 4 == 0;
+    if (kind == EPI_FWD) { va = aligned16(pr.A) && cin4; vb = aligned16(pr.B) && cin4; }
+    if (kind == EPI_DGRAD) { va = aligned16(pr.A) && cout4; vb = aligned16(pr.B) && cin4; }
+    if (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) {
+      va = aligned16(pr.A) && cout4;
+      vb = aligned16(pr.B) && cin4;
+    }
+  }
   if (kind == EPI_FWD_FF)
     vb = vb && aligned16(ea.W.w) && aligned16(ea.W.m) && aligned16(ea.gW) &&
          (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) &&

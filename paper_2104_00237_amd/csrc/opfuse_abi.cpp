@@ -169,6 +169,49 @@ of_status check_act_prev(int32_t act_prev, const float* prev) {
   return OF_OK;
 }
 
+of_status check_conv(const of_conv_desc* d) {
+  REQUIRE(d != nullptr, OF_EINVAL, "desc is NULL");
+  REQUIRE(d->N >= 1 && d->H >= 1 && d->W >= 1 && d->C >= 1 && d->Cout >= 1, OF_EINVAL,
+          "N, H, W, C, Cout must be >= 1");
+  REQUIRE(d->N * d->H * d->W < (1LL << 31) && 9 * d->C * d->Cout < (1LL << 31), OF_EUNSUPPORTED,
+          "convolution too large for 32-bit indexing");
+  REQUIRE(d->N * d->H * d->W * std::max(d->C, d->Cout) * 4 < (1LL << 31), OF_EUNSUPPORTED,
+          "activation tensors must be < 2 GiB");
+  REQUIRE(d->act == OF_ACT_NONE || d->act == OF_ACT_RELU, OF_EUNSUPPORTED,
+          "convolutions support OF_ACT_NONE and OF_ACT_RELU");
+  return OF_OK;
+}
+
+GemmProblem conv_problem(const of_conv_desc* d, int kind, const float* a, const float* b) {
+  const int NHW = (int)(d->N * d->H * d->W), C = (int)d->C, Co = (int)d->Cout;
+  GemmProblem pr{};
+  pr.conv = 1;
+  pr.cN = (int)d->N; pr.cH = (int)d->H; pr.cW = (int)d->W; pr.cC = C; pr.cCout = Co;
+  pr.A = a; pr.B = b;
+  if (kind == EPI_FWD) {          // A = x gathered, B = W [Cout, 9C]
+    pr.P = NHW; pr.Q = Co; pr.R = 9 * C; pr.b_sq = 9 * C; pr.b_sr = 1;
+  } else if (kind == EPI_DGRAD) { // A = dy gathered, B = W gathered
+    pr.P = NHW; pr.Q = C; pr.R = 9 * Co;
+  } else {                        // A = dy [NHW, Cout], B = x gathered
+    pr.P = Co; pr.Q = 9 * C; pr.R = NHW; pr.a_sp = 1; pr.a_sr = Co;
+  }
+  return pr;
+}
+
+size_t conv_ws(const of_conv_desc* d, int kind) {
+  const GemmProblem pr = conv_problem(d, kind, nullptr, nullptr);
+  return gemm_workspace_bytes(kind, pr.P, pr.Q, pr.R);
+}
+
+of_status check_conv_ws(const of_conv_desc* d, int kind, const void* ws, size_t ws_bytes) {
+  const size_t need = conv_ws(d, kind);
+  REQUIRE(ws_bytes >= need, OF_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed",
+          ws_bytes, need);
+  REQUIRE(need == 0 || ws != nullptr, OF_EWORKSPACE, "workspace is NULL");
+  REQUIRE(ws == nullptr || (((uintptr_t)ws) & 15u) == 0, OF_EALIGN, "workspace must be 16-byte aligned");
+  return OF_OK;
+}
+
 }  // namespace
 
 namespace opfuse {
@@ -336,6 +379,115 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
   ea.opt = make_optk(*opt);
   return hip_status(gemm_launch(EPI_WGRAD_BF, wgrad_problem(d, dz, x), ea, ws_update, su),
                     "of_linear_bwd_fused launch");
+}
+
+size_t of_conv_workspace_size(const of_conv_desc* d, int32_t op) {
+  if (check_conv(d) != OF_OK) return 0;
+  if (op < OF_CONV_FWD || op > OF_CONV_BWD_WEIGHT) {
+    fail(OF_EINVAL, "op %d is not an of_conv_op", (int)op);
+    return 0;
+  }
+  const int kind = op == OF_CONV_FWD ? EPI_FWD : op == OF_CONV_BWD_DATA ? EPI_DGRAD : EPI_WGRAD;
+  return conv_ws(d, kind);
+}
+
+of_status of_conv_fwd(const of_conv_desc* d, const float* x, const of_param* W, const float* b,
+                      float* y, void* ws, size_t ws_bytes, void* stream) {
+  of_status st = check_conv(d);
+  if (st != OF_OK) return st;
+  REQUIRE(x && W && W->w && y, OF_EINVAL, "x, W, W->w and y are required");
+  REQUIRE(W->numel == 9 * d->C * d->Cout, OF_EINVAL, "W->numel must be Cout*9*C");
+  REQUIRE(!d->has_bias || b, OF_EINVAL, "has_bias is set but b is NULL");
+  REQUIRE(al4(x) && al4(W->w) && al4(b) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_conv_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
+  EpiArgs ea = empty_epi();
+  ea.out = y; ea.ldo = d->Cout;
+  ea.act = d->act;
+  ea.bias = d->has_bias ? b : nullptr;
+  return hip_status(gemm_launch(EPI_FWD, conv_problem(d, EPI_FWD, x, W->w), ea, ws,
+                                (hipStream_t)stream), "of_conv_fwd launch");
+}
+
+of_status of_conv_bwd_data(const of_conv_desc* d, const float* dy, const of_param* W,
+                           const float* prev, int32_t act_prev, float* dx, void* ws,
+                           size_t ws_bytes, void* stream) {
+  of_status st = check_conv(d);
+  if (st != OF_OK) return st;
+  REQUIRE(dy && W && W->w && dx, OF_EINVAL, "dy, W, W->w and dx are required");
+  REQUIRE(W->numel == 9 * d->C * d->Cout, OF_EINVAL, "W->numel must be Cout*9*C");
+  if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
+  REQUIRE(act_prev != OF_ACT_GELU, OF_EUNSUPPORTED, "convolutions support ReLU only");
+  REQUIRE(al4(dy) && al4(W->w) && al4(dx), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_conv_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
+  EpiArgs ea = empty_epi();
+  ea.out = dx; ea.ldo = d->C;
+  ea.prev = prev; ea.ldp = d->C;
+  ea.act = act_prev;
+  return hip_status(gemm_launch(EPI_DGRAD, conv_problem(d, EPI_DGRAD, dy, W->w), ea, ws,
+                                (hipStream_t)stream), "of_conv_bwd_data launch");
+}
+
+of_status of_conv_bwd_weight(const of_conv_desc* d, const float* dy, const float* x, float* dw,
+                             float* db, int32_t accumulate, void* ws, size_t ws_bytes,
+                             void* stream) {
+  of_status st = check_conv(d);
+  if (st != OF_OK) return st;
+  REQUIRE(dy && x && dw, OF_EINVAL, "dy, x and dw are required");
+  REQUIRE(al4(dy) && al4(x) && al4(dw) && al4(db), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_conv_ws(d, EPI_WGRAD, ws, ws_bytes)) != OF_OK) return st;
+  EpiArgs ea = empty_epi();
+  ea.out = dw; ea.ldo = 9 * d->C;
+  ea.db = db;
+  ea.with_db = db != nullptr;
+  ea.accumulate = accumulate ? 1 : 0;
+  return hip_status(gemm_launch(EPI_WGRAD, conv_problem(d, EPI_WGRAD, dy, x), ea, ws,
+                                (hipStream_t)stream), "of_conv_bwd_weight launch");
+}
+
+of_status of_conv_wgrad_fused(const of_conv_desc* d, const float* dy, const float* x,
+                              const of_param* W, const of_param* b, const float* gW_partial,
+                              const float* gb_partial, const of_opt* opt, void* ws,
+                              size_t ws_bytes, void* stream) {
+  of_status st = check_conv(d);
+  if (st != OF_OK) return st;
+  if ((st = check_opt(opt)) != OF_OK) return st;
+  REQUIRE(dy && x, OF_EINVAL, "dy and x are required");
+  if ((st = check_param(W, "W", 9 * d->C * d->Cout, opt->kind, true)) != OF_OK) return st;
+  if (b) {
+    if ((st = check_param(b, "b", d->Cout, opt->kind, true)) != OF_OK) return st;
+  }
+  REQUIRE(al4(dy) && al4(x) && al4(gW_partial) && al4(gb_partial), OF_EALIGN,
+          "fp32 pointers must be 4-byte aligned");
+  if ((st = check_conv_ws(d, EPI_WGRAD_BF, ws, ws_bytes)) != OF_OK) return st;
+  EpiArgs ea = empty_epi();
+  ea.ldo = 9 * d->C;
+  ea.W = *W;
+  ea.gW = gW_partial;
+  if (b) { ea.b = *b; ea.gb = gb_partial; }
+  ea.with_db = b != nullptr;
+  ea.opt = make_optk(*opt);
+  return hip_status(gemm_launch(EPI_WGRAD_BF, conv_problem(d, EPI_WGRAD_BF, dy, x), ea, ws,
+                                (hipStream_t)stream), "of_conv_wgrad_fused launch");
+}
+
+of_status of_maxpool2x2_fwd(const float* x, int64_t N, int64_t H, int64_t W, int64_t C, float* y,
+                            uint8_t* argmax, void* stream) {
+  REQUIRE(x && y && argmax, OF_EINVAL, "x, y and argmax are required");
+  REQUIRE(N >= 1 && H >= 2 && W >= 2 && C >= 1 && H % 2 == 0 && W % 2 == 0, OF_EINVAL,
+          "N, C >= 1 and H, W even and >= 2 are required");
+  REQUIRE(al4(x) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_maxpool_fwd(x, N, H, W, C, y, argmax, (hipStream_t)stream),
+                    "of_maxpool2x2_fwd launch");
+}
+
+of_status of_maxpool2x2_bwd(const float* dy, const uint8_t* argmax, const float* mask_src,
+                            int64_t N, int64_t H, int64_t W, int64_t C, float* dx, void* stream) {
+  REQUIRE(dy && argmax && dx, OF_EINVAL, "dy, argmax and dx are required");
+  REQUIRE(N >= 1 && H >= 2 && W >= 2 && C >= 1 && H % 2 == 0 && W % 2 == 0, OF_EINVAL,
+          "N, C >= 1 and H, W even and >= 2 are required");
+  REQUIRE(al4(dy) && al4(dx) && al4(mask_src), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_maxpool_bwd(dy, argmax, mask_src, N, H, W, C, dx, (hipStream_t)stream),
+                    "of_maxpool2x2_bwd launch");
 }
 
 of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t g_rows,

@@ -187,3 +187,106 @@ def test_ambiguous_decisions_and_candidates():
     # the flip moves the first layer's gradient row of unit 1 only
     d = np.abs(cands[1][2]["params"]["fc1.weight"] - cands[0][2]["params"]["fc1.weight"])
     assert d[1].max() > 0 and d[0].max() == 0 and d[2].max() == 0
+
+
+def _zero_state(init):
+    z = {k: np.zeros(np.shape(v)) for k, v in init.items()}
+    return dict(params=init, m=z, v=dict(z), step={k: 0 for k in init})
+
+
+@pytest.mark.parametrize("name", ["mlp3", "vgg11"])
+def test_decision_search_without_flips_is_the_eager_step(name):
+    """Settling every node with no flipped decision reproduces the eager step."""
+    from oracle.train import DecisionSearch
+    from workloads import make_params
+    cfg = reduced_config(name, steps=1)
+    init = make_params(cfg)
+    plain = run(cfg, "eager", steps=1, init=init)
+    s = DecisionSearch(cfg, _zero_state(init), 1)
+    assert s.loss == plain["losses"][0]
+    while not s.done:
+        s.accept(())
+    st = s.finish()
+    for k in plain["params"]:
+        np.testing.assert_array_equal(st["params"][k], plain["params"][k])
+        np.testing.assert_array_equal(st["m"][k], plain["m"][k])
+        assert st["step"][k] == 1
+
+
+def _settle_with(s, kind):
+    """Walk the search, flipping the first open decision of `kind` met; return it.
+    ReLU decisions are taken where no max-pool follows (there the incoming
+    gradient is dense, so the flip changes the step)."""
+    from oracle import layers as OLY
+    chosen = None
+    nodes = s.model.nodes
+    while not s.done:
+        pick = ()
+        if chosen is None:
+            for d in s.open_decisions():
+                if d[0] == kind and not (kind == "relu" and
+                                         isinstance(nodes[d[1] + 1][0], OLY.MaxPool2x2)):
+                    pick = (d,)
+                    chosen = d
+                    break
+        s.accept(pick)
+    return chosen, s.finish()
+
+
+def test_decision_search_relu_flip_is_a_flipped_mask():
+    """A flipped ReLU decision equals the step of a model whose backward mask is
+    inverted at that element (the oracle's own flip mechanism)."""
+    from oracle.train import DecisionSearch, new_model
+    from workloads import make_params, make_batch
+    cfg = reduced_config("vgg11", steps=1)
+    init = make_params(cfg)
+    # a huge c makes every decision "ambiguous", so the walk has choices
+    d, st = _settle_with(DecisionSearch(cfg, _zero_state(init), 1, c=1e12), "relu")
+    assert d is not None
+    model = new_model(cfg, init=init)
+    _, i, idx, _ = d
+    op = model.nodes[i][0]
+    x, y = make_batch(cfg, 1)
+    out, tape = model.forward(np.asarray(x, np.float64))
+    op.flip = np.zeros(tape[i].shape, bool)
+    op.flip[idx] = True
+    loss, dout = model.loss_and_grad(out, y)
+    model.backward(tape, dout)
+    from oracle.optim import apply
+    for p in model.params.values():
+        apply(p, cfg["opt"])
+    changed = 0
+    for k, p in model.params.items():
+        np.testing.assert_array_equal(st["params"][k], p.value)
+        changed += int(np.any(st["params"][k] != run(cfg, "eager", steps=1, init=init)["params"][k]))
+    assert changed > 0
+
+
+def test_decision_search_pool_flip_routes_the_gradient():
+    """A flipped max-pool decision equals the step of a model whose pool picks
+    that window entry in the backward pass."""
+    from oracle.train import DecisionSearch, new_model
+    from oracle import layers as OLY
+    from oracle.optim import apply
+    from workloads import make_params, make_batch
+    cfg = reduced_config("vgg11", steps=1)
+    init = make_params(cfg)
+    d, st = _settle_with(DecisionSearch(cfg, _zero_state(init), 1, c=1e12), "pool")
+    assert d is not None
+    _, i, idx, q = d
+    model = new_model(cfg, init=init)
+    op = model.nodes[i][0]
+    assert isinstance(op, OLY.MaxPool2x2)
+    x, y = make_batch(cfg, 1)
+    out, tape = model.forward(np.asarray(x, np.float64))
+    shape, arg = tape[i]
+    assert arg[idx] != q
+    arg = arg.copy()
+    arg[idx] = q
+    tape[i] = (shape, arg)
+    loss, dout = model.loss_and_grad(out, y)
+    model.backward(tape, dout)
+    for p in model.params.values():
+        apply(p, cfg["opt"])
+    for k, p in model.params.items():
+        np.testing.assert_array_equal(st["params"][k], p.value)
