@@ -57,35 +57,70 @@ def state_bytes_per_param(kind, ordering):
     return 4 + 4 + upd
 
 
-def linear_launches(cfg):
-    """Per-launch algorithmic (flops, bytes) of each kernel class, by layer."""
-    M = cfg["batch"]
-    dims = cfg["dims"]
+def layer_launches(cfg):
+    """Per-launch algorithmic (flops, bytes) of each kernel class, by layer.
+
+    Linear [M,K] -> [M,N]: 2MNK flops; bytes = operands read + results written
+    once.  A 3x3 convolution counts as its implicit GEMM (M = N*H*W pixels,
+    N = Cout, K = 9*Cin) for flops, with the activation tensors (not the
+    gathered im2col matrix) for bytes.  Convolutions apply forward-fusion's
+    pending update in an element-wise pass before the forward, counted in
+    fwd_ff.  `extra` holds the max-pool bytes (forward, backward) after a layer.
+    """
     kind = cfg["opt"]["kind"]
     h = 2 if kind != "sgd" else 1
+
+    def upd(n):                      # R theta,hist + W theta,hist
+        return 4 * n * (2 + 2 * h)
+
+    layers = []                      # (name, kind, M, N, K, in_elems, out_elems, bias, act_prev, pool)
+    if cfg["kind"] == "mlp":
+        M, dims = cfg["batch"], cfg["dims"]
+        for i in range(1, len(dims)):
+            layers.append((f"fc{i}", "linear", M, dims[i], dims[i - 1], M * dims[i - 1],
+                           M * dims[i], cfg["bias"], i > 1 and cfg["act"] != "none", None))
+    elif cfg["kind"] == "vgg":
+        B, s, c = cfg["batch"], cfg["image"], cfg["in_channels"]
+        pooled = False
+        for i, co in enumerate(cfg["channels"], start=1):
+            pool = i in cfg["pool_after"]
+            layers.append((f"conv{i}", "conv", B * s * s, co, 9 * c, B * s * s * c, B * s * s * co,
+                           True, i > 1 and not pooled, B * s * s * co if pool else None))
+            pooled = pool
+            if pool:
+                s //= 2
+            c = co
+        layers.append(("fc", "linear", B, cfg["classes"], c, B * c, B * cfg["classes"], True,
+                       False, None))
     out = []
-    for i in range(1, len(dims)):
-        K, N = dims[i - 1], dims[i]
-        act_prev = i > 1 and cfg["act"] != "none"
-        w, xb, yb = 4 * N * K, 4 * M * K, 4 * M * N
-        bias = 4 * N if cfg["bias"] else 0
-        upd_w = 4 * N * K * (2 + 2 * h)          # R W,hist + W W,hist
-        upd_b = 4 * N * (2 + 2 * h) if cfg["bias"] else 0
+    for j, (name, lk, M, N, K, nin, nout, bias, act_prev, pool) in enumerate(layers):
+        w, xb, yb = 4 * N * K, 4 * nin, 4 * nout
+        bb = 4 * N if bias else 0
         f = 2 * M * N * K
+        if lk == "linear":
+            fwd_ff = (f, xb + yb + w * 2 + upd(N * K) + bb * 2 + (upd(N) if bias else 0))
+        else:
+            el = upd(N * K) + w + (upd(N) + bb if bias else 0)      # + R g
+            fwd_ff = (f, xb + w + yb + bb + el)
+        extra = 0
+        if pool:                                           # fwd R y W p,arg; bwd R gp,arg,y W gz
+            q = pool // 4
+            extra = (4 * pool + 5 * q) + (4 * q + q + 4 * pool + 4 * pool)
         out.append(dict(
-            layer=i, N=N, K=K,
-            fwd=(f, xb + w + yb + bias),
-            fwd_ff=(f, xb + yb + w * 2 + upd_w + bias * 2 + upd_b),   # + R g_W, g_b
-            dgrad=(f, yb + w + xb + (xb if act_prev else 0)) if i > 1 else None,
-            wgrad=(f, yb + xb + w + bias),
-            wgrad_bf=(f, yb + xb + upd_w + upd_b),
+            name=name, kind=lk, M=M, N=N, K=K, nparams=N * K + (N if bias else 0),
+            fwd=(f, xb + w + yb + bb),
+            fwd_ff=fwd_ff,
+            dgrad=(f, yb + w + xb + (xb if act_prev else 0)) if j > 0 else None,
+            wgrad=(f, yb + xb + w + bb),
+            wgrad_bf=(f, yb + xb + upd(N * K) + (upd(N) if bias else 0)),
+            extra=extra,
         ))
     return out
 
 
 def step_cost(cfg, ordering):
     """Whole-step algorithmic flops and bytes (kernels as implemented)."""
-    L = linear_launches(cfg)
+    L = layer_launches(cfg)
     F = B = 0
     for d in L:
         fk = "fwd_ff" if ordering == "ff" else "fwd"
@@ -94,13 +129,20 @@ def step_cost(cfg, ordering):
             if d[k] is not None:
                 F += d[k][0]
                 B += d[k][1]
-    n = sum(d["N"] * d["K"] + (d["N"] if cfg["bias"] else 0) for d in L)
+        B += d["extra"]
+    n = sum(d["nparams"] for d in L)
     h = 2 if cfg["opt"]["kind"] != "sgd" else 1
     if ordering == "eager":
         B += n * 4 * (3 + 2 * h)           # R w, g, hist; W w, hist
-    M, C = cfg["batch"], cfg["dims"][-1]
-    B += 4 * M * C * 2
+    B += 4 * L[-1]["M"] * L[-1]["N"] * 2   # loss: R logits, W their gradient
     return F, B
+
+
+def describe_layers(cfg):
+    if cfg["kind"] == "mlp":
+        return f"{len(cfg['dims']) - 1} linear, width {cfg['dims'][1]}"
+    return (f"{len(cfg['channels'])} conv3x3 ({','.join(map(str, cfg['channels']))}), "
+            f"max-pool after {cfg['pool_after']}, linear classifier, {cfg['image']}x{cfg['image']}")
 
 
 def kernel_roofline(flops, nbytes, seconds):
@@ -210,7 +252,7 @@ def main():
 
     import torch
     cfg = get_config(args.workload)
-    if cfg["kind"] != "mlp" or cfg["dtype"] != "f32":
+    if cfg["kind"] not in ("mlp", "vgg") or cfg["dtype"] != "f32":
         print(f"workload {args.workload} has no GPU path in this build", file=sys.stderr)
         sys.exit(2)
     dev = torch.device("cuda:0")
@@ -241,15 +283,16 @@ def main():
     dom = max(totals, key=totals.get)
     ms_dom_step, _, timer, _ = time_ordering(torch, cfg, "bf", batches, args.warmup, args.steps,
                                              (dom,))
-    launches = linear_launches(cfg)
+    launches = {d["name"]: d for d in layer_launches(cfg)}
     recs = timer.durations(dom)
-    # Group by layer shape: report the largest shape's launches (the repeated hidden layer).
+    # Group launches by layer shape (the repeated hidden layers of an MLP share
+    # one) and report the group with the largest total time.
     by_shape = {}
     for d_ms, op in recs:
-        by_shape.setdefault((op.N, op.K), []).append(d_ms)
-    shape = max(by_shape, key=lambda s: s[0] * s[1])
-    durs = by_shape[shape]
-    per = next(d for d in launches if (d["N"], d["K"]) == shape)[dom]
+        by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name))
+    shape = max(by_shape, key=lambda s: sum(d for d, _ in by_shape[s]))
+    durs = [d for d, _ in by_shape[shape]]
+    per = launches[by_shape[shape][0][1]][dom]
     # Each launch is bracketed by an event pair on its own stream; the pair's own
     # cost (an empty pair on the same stream) is taken off.
     from paper_2104_00237_amd.trainer import KernelTimer
@@ -257,14 +300,15 @@ def main():
     marker_ms = KernelTimer.marker_overhead_ms(dom_stream)
     avg_s = (float(np.mean(durs)) - marker_ms) / 1e3
     roof = kernel_roofline(per[0], per[1], avg_s)
-    roof.update(kernel=dom, shape=f"M={cfg['batch']} N={shape[0]} K={shape[1]}",
+    roof.update(kernel=dom, layers=sorted({n for _, n in by_shape[shape]}),
+                shape=f"{shape[0]} GEMM M={shape[1]} N={shape[2]} K={shape[3]}",
                 avg_us=round(avg_s * 1e6, 3), launches=len(durs),
                 bracketed_avg_us=round(float(np.mean(durs)) * 1e3, 3),
                 marker_us=round(marker_ms * 1e3, 3),
                 algorithmic_bytes=per[1], algorithmic_flops=per[0],
                 traffic=traffic_for(dom, args.workload))
 
-    n_params = sum(d["N"] * d["K"] + (d["N"] if cfg["bias"] else 0) for d in launches)
+    n_params = sum(d["nparams"] for d in launches.values())
     kind = cfg["opt"]["kind"]
     upd_bytes = n_params * state_bytes_per_param(kind, "bf")
     bf_s = res["bf"]["ms"] / 1e3
@@ -286,7 +330,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "global_batch": cfg["batch"],
-                   "layers": f"{len(cfg['dims']) - 1}x{cfg['dims'][1]}",
+                   "layers": describe_layers(cfg),
                    "optimizer": kind, "ordering": "backward-fusion",
                    "parallelism": "single-gpu"},
         "eager_ms_per_step": round(res["eager"]["ms"], 4),
