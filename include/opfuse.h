@@ -329,6 +329,49 @@ of_status of_step_advance(int64_t* step_dev, int64_t delta, void* stream);
 of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B, int64_t C,
                           int64_t ld, float* loss, float* dlogits, void* stream);
 
+/* ------------------------------------------------------ LayerNorm, add */
+
+/*
+ * LayerNorm over the last dimension (the normalisation of the Transformer
+ * blocks the paper trains, Appendix C): biased variance over D, eps inside
+ * the square root,
+ *   y = (x - mean) / sqrt(var + eps) * gamma + beta.
+ * x, y: [M, D] contiguous fp32; gamma, beta: [D]; mean, rstd: [M] outputs
+ * (1 / sqrt(var + eps)), kept for the backward.
+ */
+of_status of_layernorm_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
+                           const float* beta, float eps, float* y, float* mean, float* rstd,
+                           void* stream);
+
+/* Number of row groups G of the parameter-gradient partials of
+ * of_layernorm_bwd for M rows (1 <= G <= 64). */
+int64_t of_layernorm_partial_rows(int64_t M);
+
+/*
+ * LayerNorm backward.  With xh = (x - mean) * rstd and g = dy * gamma:
+ *   dx = dres + rstd * (g - mean_D(g) - xh * mean_D(g * xh))
+ * (dres: optional [M, D] gradient added in, e.g. the residual branch; NULL
+ * for none; it may alias dx).  The parameter gradients are written as per
+ * row-group partial sums dgamma_rows, dbeta_rows: [G, D] with
+ * G = of_layernorm_partial_rows(M), row g holding the sums over rows
+ * [g*ceil(M/G), (g+1)*ceil(M/G)) of dy * xh and dy.  Pass them to
+ * of_elementwise_fused_update with g_rows = G (backward- or forward-fusion:
+ * the gradient vector is never stored) or to of_reduce_rows (eager).
+ * dx must not alias dy or x.
+ */
+of_status of_layernorm_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
+                           const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
+                           float* dgamma_rows, float* dbeta_rows, void* stream);
+
+/* dst[i] = sum over r = 0 .. rows-1, in order, of src[r*ld + i], i < n
+ * (ld = 0 means n): materialises a gradient given as row partials. */
+of_status of_reduce_rows(const float* src, int64_t rows, int64_t ld, int64_t n, float* dst,
+                         void* stream);
+
+/* out = a + b element-wise over n fp32 values (the residual connections of
+ * a Transformer block); out may alias a or b. */
+of_status of_add(const float* a, const float* b, int64_t n, float* out, void* stream);
+
 /*
  * Mean squared error, forward and backward:
  *   loss = mean over all M*D elements of (y - t)^2;  dy = 2 (y - t) / (M*D).

@@ -90,6 +90,13 @@ _SIGS = {
                                     c_void_p, c_void_p]),
     "of_maxpool2x2_bwd": (c_int32, [c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64,
                                     c_int64, c_void_p, c_void_p]),
+    "of_layernorm_fwd": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, c_void_p, c_float,
+                                   c_void_p, c_void_p, c_void_p, c_void_p]),
+    "of_layernorm_partial_rows": (c_int64, [c_int64]),
+    "of_layernorm_bwd": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                   c_int64, c_int64, c_void_p, c_void_p, c_void_p, c_void_p]),
+    "of_reduce_rows": (c_int32, [c_void_p, c_int64, c_int64, c_int64, c_void_p, c_void_p]),
+    "of_add": (c_int32, [c_void_p, c_void_p, c_int64, c_void_p, c_void_p]),
     "of_xent_fwd_bwd": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_int64, c_void_p,
                                   c_void_p, c_void_p]),
     "of_mse_workspace_size": (c_size_t, [c_int64, c_int64]),
@@ -151,11 +158,16 @@ def of_conv_workspace_size(desc, op):
     return load().of_conv_workspace_size(ctypes.byref(desc), op)
 
 
+def of_layernorm_partial_rows(M):
+    return load().of_layernorm_partial_rows(M)
+
+
 for _n in ("of_linear_fwd", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
-           "of_maxpool2x2_fwd", "of_maxpool2x2_bwd"):
+           "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_layernorm_fwd", "of_layernorm_bwd",
+           "of_reduce_rows", "of_add"):
     globals()[_n] = _wrap(_n)
 del _n
 

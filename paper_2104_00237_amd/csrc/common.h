@@ -153,6 +153,7 @@ struct GemmProblem {
   int P, Q, R;
   int conv;                     // 0: strided operands; 1: convolution gathers
   int cN, cH, cW, cC, cCout;    // convolution geometry (input N, H, W, C; Cout)
+  int a_bf16, b_bf16;           // bf16 kernels: the operand is stored as bf16 (else fp32)
 };
 
 struct EpiArgs {
@@ -177,6 +178,11 @@ struct EpiArgs {
 size_t gemm_workspace_bytes(int kind, int P, int Q, int R);
 hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                        hipStream_t stream);
+// bf16-operand contractions (operands rounded to bf16, fp32 accumulation);
+// kinds EPI_FWD, EPI_DGRAD, EPI_WGRAD, EPI_WGRAD_BF; strided operands only.
+size_t gemm_bf16_workspace_bytes(int kind, int P, int Q, int R);
+hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                            hipStream_t stream);
 
 // ------------------------------------------------------ elementwise / losses
 hipError_t launch_multi_update(int n, const of_param* params, const float* const* grads,
@@ -189,6 +195,16 @@ hipError_t launch_maxpool_fwd(const float* x, int64_t N, int64_t H, int64_t W, i
 hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, const float* mask_src,
                               int64_t N, int64_t H, int64_t W, int64_t C, float* dx,
                               hipStream_t s);
+int64_t ln_partial_rows(int64_t M);
+hipError_t launch_ln_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
+                         const float* beta, float eps, float* y, float* mean, float* rstd,
+                         hipStream_t s);
+hipError_t launch_ln_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
+                         const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
+                         float* dgamma_rows, float* dbeta_rows, hipStream_t s);
+hipError_t launch_reduce_rows(const float* src, int64_t rows, int64_t ld, int64_t n, float* dst,
+                              hipStream_t s);
+hipError_t launch_add(const float* a, const float* b, int64_t n, float* out, hipStream_t s);
 hipError_t launch_xent(const float* z, const int64_t* labels, int64_t B, int64_t C, int64_t ld,
                        float* loss, float* dz, hipStream_t stream);
 size_t mse_ws_bytes(int64_t M, int64_t D);

@@ -1,0 +1,451 @@
+// bf16-operand contractions of a linear layer on the CDNA4 matrix cores
+// (v_mfma_f32_32x32x16_bf16), with the same epilogues as the fp32 kernels:
+// plain forward, data gradient, weight gradient, and the weight gradient with
+// the optimizer applied in its epilogue (backward-fusion).
+//
+// Operands stay in their storage type in HBM: activations and gradients are
+// fp32 and are rounded to bf16 (round to nearest even) as they are staged into
+// LDS, which is the same value as rounding them just before the product; a
+// weight operand is read from its bf16 shadow when one is given (half the
+// bytes), else rounded from the fp32 master.  Products of bf16 values are exact
+// in fp32 and the sums accumulate in fp32.
+//
+// LDS layout: each operand tile is stored as BR/8 planes of [BX][8] bf16, so
+// the 8 consecutive reduction elements a lane feeds one MFMA are one 16-byte
+// read.  A tile element (x, r) lives at plane r/8, row x, slot r%8.  Loads are
+// grouped in quads along the contiguous index (4 reduction elements of one
+// row, or 4 rows by 4 output columns when the output index is contiguous), so
+// every LDS store writes 4 bf16 (8 bytes) along the reduction index.
+//
+// The reduction runs in chunks of BR with double-buffered LDS and one barrier
+// per chunk; the next chunk's global loads are issued before the current
+// chunk's MFMAs.  A grid-level split of the reduction writes fp32 partials that
+// a second kernel sums in split order before the epilogue (deterministic; the
+// eager and backward-fusion weight gradients share the tiling rule).
+
+#include <algorithm>
+
+#include "gemm_common.h"
+
+namespace opfuse {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx16_t __attribute__((ext_vector_type(16)));
+
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_>
+struct BTile {
+  static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_;
+  static_assert(WP * WQ == 4, "a workgroup is 4 wavefronts");
+  static_assert(BR % 16 == 0, "whole MFMA reduction steps");
+  static constexpr int WTP = BP / WP, WTQ = BQ / WQ;
+  static constexpr int TP = WTP / 32, TQ = WTQ / 32;
+  static_assert(TP >= 1 && TQ >= 1 && WTP % 32 == 0 && WTQ % 32 == 0, "32x32 blocks");
+  // Plane strides in bf16 elements, padded by 8 (16 bytes) against bank conflicts.
+  static constexpr int PLA = BP * 8 + 8, PLB = BQ * 8 + 8;
+  static constexpr int STAGE = (BR / 8) * (PLA + PLB);          // bf16 elements per stage
+  static constexpr int SM_MAIN = 2 * STAGE * 2;                  // bytes, two stages
+  static constexpr int LDC = (BP * (BQ + 4) * 4 <= 60 * 1024) ? BQ + 4 : BQ;
+  static constexpr int SM_C = BP * LDC * 4;                      // bytes
+  static constexpr int SMX = SM_MAIN > SM_C ? SM_MAIN : SM_C;
+  static_assert(SMX <= 64 * 1024, "LDS per workgroup");
+};
+
+using BT128x128 = BTile<128, 128, 32, 2, 2>;
+using BT64x64 = BTile<64, 64, 32, 2, 2>;
+
+enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_COUNT };
+static const int kBTileBP[BTI_COUNT] = {64, 128};
+static const int kBTileBQ[BTI_COUNT] = {64, 128};
+static const int kBTileBR[BTI_COUNT] = {32, 32};
+
+__device__ __forceinline__ uint2 pack_bf16x4(float a, float b, float c, float d) {
+  return make_uint2((uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16),
+                    (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16));
+}
+
+__device__ __forceinline__ uint2 bload8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+__device__ __forceinline__ uint32_t bload_u16(rsrc_t r, uint32_t off) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+
+// One operand tile (BX output rows x BR reduction elements) in flight between
+// its global loads and its LDS store.  RC: the reduction index is contiguous
+// in memory.  BF: the source holds bf16 (else fp32).  VEC: 128-bit (fp32) or
+// 64-bit (bf16) loads are allowed: aligned base, strides a multiple of 4
+// elements and the contiguous extent ending on a quad boundary.
+// An item is a quad along r (RC) or a 4 x 4 block (r, x) (not RC).
+template <int BX, int BR, bool RC, bool BF, bool VEC>
+struct BLoad {
+  static constexpr int NQ = RC ? BX * (BR / 4) : (BR / 4) * (BX / 4);  // items
+  static constexpr int PER = (NQ + 255) / 256;
+  static constexpr int NV = RC ? 1 : 4;          // vectors per item
+  static constexpr int PL = BX * 8 + 8;          // plane stride (bf16 elements)
+  // raw data: fp32 float4 or bf16 quads (as uint2), NV per item
+  float4 f[BF ? 1 : PER][BF ? 1 : NV];
+  uint2 h[BF ? PER : 1][BF ? NV : 1];
+
+  __device__ __forceinline__ static void coords(int idx, int& x, int& r) {
+    if (RC) { x = idx / (BR / 4); r = (idx % (BR / 4)) * 4; }
+    else    { r = (idx / (BX / 4)) * 4; x = (idx % (BX / 4)) * 4; }
+  }
+
+  __device__ __forceinline__ void load(const void* tensor, int64_t s_x, int64_t s_r, int x0,
+                                       int r0, int nx, int nr, int tid) {
+    constexpr int ES = BF ? 2 : 4;
+    const rsrc_t rs = make_rsrc((const char*)tensor + ((int64_t)x0 * s_x + (int64_t)r0 * s_r) * ES);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = tid + i * 256;
+      int x, r;
+      coords(idx, x, r);
+      const bool live = idx < NQ;
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        // vector j: RC -> the quad (x, r..r+3); else the quad (x..x+3, r+j)
+        const int vx = x, vr = RC ? r : r + j;
+        if constexpr (VEC) {
+          const bool ok = live && vx < nx && vr < nr;
+          const uint32_t off = ok ? (uint32_t)((vx * s_x + vr * s_r) * ES) : kOOB;
+          if constexpr (BF) h[i][j] = bload8(rs, off);
+          else f[i][j] = bload4(rs, off);
+        } else {
+          float e[4];
+          uint32_t u[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int xx = RC ? vx : vx + k, rr = RC ? vr + k : vr;
+            const bool ok = live && xx < nx && rr < nr;
+            const uint32_t off = ok ? (uint32_t)((xx * s_x + rr * s_r) * ES) : kOOB;
+            if constexpr (BF) u[k] = bload_u16(rs, off);
+            else e[k] = bload1(rs, off);
+          }
+          if constexpr (BF) h[i][j] = make_uint2(u[0] | (u[1] << 16), u[2] | (u[3] << 16));
+          else f[i][j] = make_float4(e[0], e[1], e[2], e[3]);
+        }
+      }
+    }
+  }
+
+  // Element k (0..3) of vector j of item i, as bf16 bits.
+  __device__ __forceinline__ uint32_t bits(int i, int j, int k) const {
+    if constexpr (BF) {
+      const uint32_t w = (k < 2) ? h[i][j].x : h[i][j].y;
+      return (k & 1) ? (w >> 16) : (w & 0xffffu);
+    } else {
+      const float v = k == 0 ? f[i][j].x : k == 1 ? f[i][j].y : k == 2 ? f[i][j].z : f[i][j].w;
+      return f32_to_bf16(v);
+    }
+  }
+
+  __device__ __forceinline__ void store(uint16_t* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int idx = tid + i * 256;
+      if (idx >= NQ) continue;
+      int x, r;
+      coords(idx, x, r);
+      const int plane = r >> 3, slot = r & 7;   // slot is 0 or 4
+      if (RC) {
+        uint2 q;
+        if constexpr (BF) q = h[i][0];
+        else q = pack_bf16x4(f[i][0].x, f[i][0].y, f[i][0].z, f[i][0].w);
+        *reinterpret_cast<uint2*>(&lds[plane * PL + x * 8 + slot]) = q;
+      } else {
+        // transpose the 4 x 4 block: row x+k gets elements k of vectors 0..3
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint2 q = make_uint2(bits(i, 0, k) | (bits(i, 1, k) << 16),
+                                     bits(i, 2, k) | (bits(i, 3, k) << 16));
+          *reinterpret_cast<uint2*>(&lds[plane * PL + (x + k) * 8 + slot]) = q;
+        }
+      }
+    }
+  }
+
+  // Column sums of the fp32 values (the A operand of a weight gradient is dZ:
+  // its sums over the reduction are the bias gradient).  Not RC only.
+  __device__ __forceinline__ void colsum(float (&acc)[PER][4]) const {
+    if constexpr (!BF && !RC) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        acc[i][0] = __fadd_rn(acc[i][0], __fadd_rn(__fadd_rn(__fadd_rn(f[i][0].x, f[i][1].x), f[i][2].x), f[i][3].x));
+        acc[i][1] = __fadd_rn(acc[i][1], __fadd_rn(__fadd_rn(__fadd_rn(f[i][0].y, f[i][1].y), f[i][2].y), f[i][3].y));
+        acc[i][2] = __fadd_rn(acc[i][2], __fadd_rn(__fadd_rn(__fadd_rn(f[i][0].z, f[i][1].z), f[i][2].z), f[i][3].z));
+        acc[i][3] = __fadd_rn(acc[i][3], __fadd_rn(__fadd_rn(__fadd_rn(f[i][0].w, f[i][1].w), f[i][2].w), f[i][3].w));
+      }
+    }
+  }
+};
+
+// Operand roles per contraction (see the fp32 kernels): forward A = X (RC),
+// B = W (RC); data gradient A = dZ (RC), B = W (output-contiguous); weight
+// gradient A = dZ, B = X (both output-contiguous).
+template <class T, int EPI, bool VA, bool VB, bool BBF>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs ea, int r_split,
+                                                        float* partial, int vec_epi) {
+  if (EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+  constexpr bool A_RC = (EPI == EPI_FWD || EPI == EPI_DGRAD);
+  constexpr bool B_RC = (EPI == EPI_FWD);
+  constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
+  __shared__ __attribute__((aligned(16))) unsigned char smem_raw[T::SMX];
+  uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wp = wave % T::WP, wq = wave / T::WP;
+  const int p0 = blockIdx.x * T::BP, q0 = blockIdx.y * T::BQ;
+  const int split = blockIdx.z, S = gridDim.z;
+  const int rbeg = split * r_split;
+  const int rend = min(pr.R, rbeg + r_split);
+  const int nch = (rend - rbeg + T::BR - 1) / T::BR;
+  const bool do_db = WG && ea.with_db && blockIdx.y == 0;
+
+  using LA = BLoad<T::BP, T::BR, A_RC, false, VA>;
+  using LB = BLoad<T::BQ, T::BR, B_RC, BBF, VB>;
+  LA la;
+  LB lb;
+  float dbs[LA::PER][4];
+#pragma unroll
+  for (int i = 0; i < LA::PER; ++i) dbs[i][0] = dbs[i][1] = dbs[i][2] = dbs[i][3] = 0.f;
+
+  floatx16_t acc[T::TP][T::TQ];
+#pragma unroll
+  for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TQ; ++j)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) acc[i][j][k] = 0.f;
+
+  const int np = pr.P - p0, nq = pr.Q - q0;
+  auto issue = [&](int c) {
+    const int r0 = rbeg + c * T::BR;
+    const int nr = c < nch ? rend - r0 : 0;
+    la.load(pr.A, pr.a_sp, pr.a_sr, p0, r0, np, nr, tid);
+    lb.load(pr.B, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
+  };
+
+  constexpr int SA = (T::BR / 8) * T::PLA;   // A part of a stage
+  issue(0);
+  for (int c = 0; c < nch; ++c) {
+    uint16_t* buf = smem + (c & 1) * T::STAGE;
+    la.store(buf, tid);
+    lb.store(buf + SA, tid);
+    if (do_db) la.colsum(dbs);
+    issue(c + 1);
+    __syncthreads();
+    const uint16_t* a_s = buf;
+    const uint16_t* b_s = buf + SA;
+#pragma unroll
+    for (int ks = 0; ks < T::BR / 16; ++ks) {
+      const int plane = 2 * ks + (lane >> 5);
+      bf16x8_t a[T::TP], b[T::TQ];
+#pragma unroll
+      for (int i = 0; i < T::TP; ++i)
+        a[i] = *reinterpret_cast<const bf16x8_t*>(
+            &a_s[plane * T::PLA + (wp * T::WTP + i * 32 + (lane & 31)) * 8]);
+#pragma unroll
+      for (int j = 0; j < T::TQ; ++j)
+        b[j] = *reinterpret_cast<const bf16x8_t*>(
+            &b_s[plane * T::PLB + (wq * T::WTQ + j * 32 + (lane & 31)) * 8]);
+#pragma unroll
+      for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TQ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  __syncthreads();
+
+  // Stage the accumulators through LDS in row-major order (MFMA 32x32 layout:
+  // lane holds column lane%32 and rows 8*(k/4) + 4*(lane/32) + k%4).
+  float* Cs = reinterpret_cast<float*>(smem_raw);
+#pragma unroll
+  for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TQ; ++j)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int p = wp * T::WTP + i * 32 + (k >> 2) * 8 + (lane >> 5) * 4 + (k & 3);
+        const int q = wq * T::WTQ + j * 32 + (lane & 31);
+        Cs[p * T::LDC + q] = acc[i][j][k];
+      }
+  __syncthreads();
+
+  constexpr int NQ4 = T::BQ / 4;
+  constexpr int ITEMS = T::BP * NQ4;
+  constexpr int EPT = (ITEMS + 255) / 256;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int idx = tid + e * 256;
+    if (idx >= ITEMS) break;
+    const int p = idx / NQ4, q = (idx % NQ4) * 4;
+    const int gp = p0 + p, gq = q0 + q;
+    if (gp >= pr.P || gq >= pr.Q) continue;
+    const float4 cv = *reinterpret_cast<const float4*>(&Cs[p * T::LDC + q]);
+    const float c[4] = {cv.x, cv.y, cv.z, cv.w};
+    const int n = min(4, pr.Q - gq);
+    if (S > 1) {
+      float* dst = partial + ((int64_t)split * pr.P + gp) * pr.Q + gq;
+      if (n == 4 && (pr.Q & 3) == 0) st4(dst, cv);
+      else for (int k = 0; k < n; ++k) dst[k] = c[k];
+    } else {
+      const float* bias = (EPI == EPI_FWD && ea.bias) ? ea.bias + gq : nullptr;
+      epilogue<EPI>(ea, gp, gq, c, n, bias, vec_epi);
+    }
+  }
+
+  if (do_db) {
+    // Bias gradient: per-thread column sums, then summed over the threads that
+    // hold the same columns, in thread order.
+    __syncthreads();
+    constexpr int RQ = T::BR / 4;           // threads per column quad
+    float* red = reinterpret_cast<float*>(smem_raw);  // [RQ][BP]
+#pragma unroll
+    for (int i = 0; i < LA::PER; ++i) {
+      const int idx = tid + i * 256;
+      if (idx < LA::NQ) {
+        const int rq = idx / (T::BP / 4), x = (idx % (T::BP / 4)) * 4;
+        for (int k = 0; k < 4; ++k) red[rq * T::BP + x + k] = dbs[i][k];
+      }
+    }
+    __syncthreads();
+    if (tid < T::BP && p0 + tid < pr.P) {
+      float s = red[tid];
+      for (int rq = 1; rq < RQ; ++rq) s = __fadd_rn(s, red[rq * T::BP + tid]);
+      if (S > 1) partial[(int64_t)S * pr.P * pr.Q + (int64_t)split * pr.P + p0 + tid] = s;
+      else bias_epilogue<EPI>(ea, p0 + tid, s);
+    }
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void split_reduce_bf16_kernel(int P, int Q, int S, EpiArgs ea,
+                                                                const float* __restrict__ partial,
+                                                                int vec_epi, int with_db) {
+  split_reduce_body<EPI>(P, Q, S, ea, partial, vec_epi, with_db);
+}
+
+// --------------------------------------------------------------- host side
+struct BCfg {
+  int tile, S, r_split;
+};
+
+static int64_t bntiles(int t, int P, int Q) {
+  return (int64_t)((P + kBTileBP[t] - 1) / kBTileBP[t]) * ((Q + kBTileBQ[t] - 1) / kBTileBQ[t]);
+}
+
+// 128x128 tiles when the output has enough of them, else 64x64; the reduction
+// is split until there are about 256 workgroups (at least 4 chunks per split).
+// The eager and backward-fusion weight gradients share this rule.
+static BCfg bselect(int kind, int P, int Q, int R) {
+  (void)kind;
+  const int t = bntiles(BTI_128x128, P, Q) >= 64 ? BTI_128x128 : BTI_64x64;
+  const int BR = kBTileBR[t];
+  const int64_t nt = bntiles(t, P, Q);
+  int S = (int)std::max<int64_t>(1, (256 + nt - 1) / nt);
+  S = std::min(S, std::min(8, std::max(1, R / (4 * BR))));
+  int r_split = (((R + S - 1) / S) + BR - 1) / BR * BR;
+  S = (R + r_split - 1) / r_split;
+  return BCfg{t, S, r_split};
+}
+
+size_t gemm_bf16_workspace_bytes(int kind, int P, int Q, int R) {
+  const BCfg c = bselect(kind, P, Q, R);
+  if (c.S <= 1) return 0;
+  return (size_t)c.S * ((size_t)P * Q + P) * sizeof(float);
+}
+
+template <class T, int EPI, bool VA, bool VB>
+static hipError_t blaunch_v(const BCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                            int vec_epi, hipStream_t s) {
+  dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
+  if (pr.b_bf16)
+    hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, true>), grid, dim3(256), 0, s, pr, ea,
+                       c.r_split, (float*)ws, vec_epi);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, false>), grid, dim3(256), 0, s, pr, ea,
+                       c.r_split, (float*)ws, vec_epi);
+  return hipGetLastError();
+}
+
+template <class T, int EPI>
+static hipError_t blaunch_t(const BCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                            int vec_ops, int vec_epi, hipStream_t s) {
+  switch (vec_ops) {
+    case 3: return blaunch_v<T, EPI, true, true>(c, pr, ea, ws, vec_epi, s);
+    case 1: return blaunch_v<T, EPI, true, false>(c, pr, ea, ws, vec_epi, s);
+    case 2: return blaunch_v<T, EPI, false, true>(c, pr, ea, ws, vec_epi, s);
+    default: return blaunch_v<T, EPI, false, false>(c, pr, ea, ws, vec_epi, s);
+  }
+}
+
+template <int EPI>
+static hipError_t blaunch_kind(const BCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                               int vec_ops, int vec_epi, hipStream_t s) {
+  if (c.tile == BTI_128x128) return blaunch_t<BT128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+  return blaunch_t<BT64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+}
+
+static int bvec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* vec_epi) {
+  const bool a_rc = (kind == EPI_FWD || kind == EPI_DGRAD);
+  const bool b_rc = (kind == EPI_FWD);
+  // fp32 quads: 16-byte aligned rows; bf16 quads: 8-byte aligned rows
+  const bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0) &&
+                  ((a_rc ? pr.R : pr.P) % 4 == 0);
+  const bool b_al = pr.b_bf16 ? (((uintptr_t)pr.B & 7u) == 0) : aligned16(pr.B);
+  const bool vb = b_al && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % 4 == 0) &&
+                  ((b_rc ? pr.R : pr.Q) % 4 == 0);
+  int ve = 0;
+  if (aligned16(ea.out) && ea.ldo % 4 == 0 && (ea.z == nullptr || (aligned16(ea.z) && ea.ldz % 4 == 0)) &&
+      (ea.prev == nullptr || (aligned16(ea.prev) && ea.ldp % 4 == 0)))
+    ve |= 1;
+  if (kind == EPI_WGRAD_BF && aligned16(ea.W.w) && aligned16(ea.W.m) && ea.ldo % 4 == 0 &&
+      (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) && (ea.gW == nullptr || aligned16(ea.gW)) &&
+      (ea.W.w_bf16 == nullptr || ((uintptr_t)ea.W.w_bf16 & 7u) == 0))
+    ve |= 2;
+  *vec_epi = ve;
+  return (va ? 1 : 0) | (vb ? 2 : 0);
+}
+
+hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+                            hipStream_t stream) {
+  if (pr.a_bf16 || pr.conv) return hipErrorInvalidValue;
+  const BCfg c = bselect(kind, pr.P, pr.Q, pr.R);
+  int vec_epi = 0;
+  const int vec_ops = bvec_flags(pr, kind, ea, &vec_epi);
+  const int with_db = (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) && ea.with_db;
+  hipError_t e;
+  switch (kind) {
+    case EPI_FWD: e = blaunch_kind<EPI_FWD>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_DGRAD: e = blaunch_kind<EPI_DGRAD>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_WGRAD: e = blaunch_kind<EPI_WGRAD>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    case EPI_WGRAD_BF: e = blaunch_kind<EPI_WGRAD_BF>(c, pr, ea, ws, vec_ops, vec_epi, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (e != hipSuccess || c.S <= 1) return e;
+  const int64_t work = (int64_t)pr.P * ((pr.Q + 3) / 4);
+  const int blocks = (int)std::min<int64_t>(2048, std::max<int64_t>(1, (work + 255) / 256));
+  const dim3 g(blocks);
+  switch (kind) {
+    case EPI_FWD:
+      hipLaunchKernelGGL(split_reduce_bf16_kernel<EPI_FWD>, g, dim3(256), 0, stream, pr.P, pr.Q,
+                         c.S, ea, (const float*)ws, vec_epi, 0);
+      break;
+    case EPI_DGRAD:
+      hipLaunchKernelGGL(split_reduce_bf16_kernel<EPI_DGRAD>, g, dim3(256), 0, stream, pr.P, pr.Q,
+                         c.S, ea, (const float*)ws, vec_epi, 0);
+      break;
+    case EPI_WGRAD:
+      hipLaunchKernelGGL(split_reduce_bf16_kernel<EPI_WGRAD>, g, dim3(256), 0, stream, pr.P, pr.Q,
+                         c.S, ea, (const float*)ws, vec_epi, with_db);
+      break;
+    case EPI_WGRAD_BF:
+      hipLaunchKernelGGL(split_reduce_bf16_kernel<EPI_WGRAD_BF>, g, dim3(256), 0, stream, pr.P,
+                         pr.Q, c.S, ea, (const float*)ws, vec_epi, with_db);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace opfuse

@@ -1,0 +1,155 @@
+// Device helpers shared by the fp32 and bf16 contraction kernels: buffer
+// loads with out-of-range masking, the epilogues (plain, data gradient,
+// weight gradient, backward-fusion update) and the split-reduction pass.
+#pragma once
+
+#include "common.h"
+
+namespace opfuse {
+
+// ------------------------------------------------------------ operand tiles
+// Operand loads are buffer loads: an offset outside the buffer returns 0, so a
+// masked element is loaded from an out-of-range offset instead of being
+// branched around.  Every thread issues the same loads every chunk, which lets
+// the compiler keep several chunks in flight (its wait counters stay exact).
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;  // beyond num_records: reads as 0
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
+  // raw buffer, stride 0, 2^31-1 bytes addressable from `base`
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff,
+                                           0x00020000);
+}
+__device__ __forceinline__ float4 bload4(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float bload1(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+// ----------------------------------------------------------------- epilogues
+// c[0..n) are the results for (p, q..q+n-1).  vec: 128-bit memory paths allowed
+// (bit 0: out/z/prev, bit 1: parameter arrays); only used when n == 4.
+template <int EPI>
+__device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const float (&c)[4],
+                                         int n, const float* bias, int vec) {
+  if (EPI == EPI_FWD || EPI == EPI_FWD_FF) {
+    float zv[4];
+    for (int e = 0; e < 4; ++e) zv[e] = (bias && e < n) ? __fadd_rn(c[e], bias[e]) : c[e];
+    const int64_t oy = (int64_t)p * ea.ldo + q, oz = (int64_t)p * ea.ldz + q;
+    if (n == 4 && (vec & 1)) {
+      if (ea.z) st4(ea.z + oz, make_float4(zv[0], zv[1], zv[2], zv[3]));
+      st4(ea.out + oy, make_float4(act_fwd(ea.act, zv[0]), act_fwd(ea.act, zv[1]),
+                                   act_fwd(ea.act, zv[2]), act_fwd(ea.act, zv[3])));
+    } else {
+      for (int e = 0; e < n; ++e) {
+        if (ea.z) ea.z[oz + e] = zv[e];
+        ea.out[oy + e] = act_fwd(ea.act, zv[e]);
+      }
+    }
+  } else if (EPI == EPI_DGRAD) {
+    const int64_t oo = (int64_t)p * ea.ldo + q, op = (int64_t)p * ea.ldp + q;
+    if (n == 4 && (vec & 1)) {
+      float4 r = make_float4(c[0], c[1], c[2], c[3]);
+      if (ea.act != OF_ACT_NONE) {
+        const float4 s = ld4(ea.prev + op);
+        r.x = __fmul_rn(r.x, act_grad(ea.act, s.x));
+        r.y = __fmul_rn(r.y, act_grad(ea.act, s.y));
+        r.z = __fmul_rn(r.z, act_grad(ea.act, s.z));
+        r.w = __fmul_rn(r.w, act_grad(ea.act, s.w));
+      }
+      st4(ea.out + oo, r);
+    } else {
+      for (int e = 0; e < n; ++e) {
+        float r = c[e];
+        if (ea.act != OF_ACT_NONE) r = __fmul_rn(r, act_grad(ea.act, ea.prev[op + e]));
+        ea.out[oo + e] = r;
+      }
+    }
+  } else if (EPI == EPI_WGRAD) {
+    const int64_t oo = (int64_t)p * ea.ldo + q;
+    if (n == 4 && (vec & 1)) {
+      float4 r = make_float4(c[0], c[1], c[2], c[3]);
+      if (ea.accumulate) {
+        const float4 o = ld4(ea.out + oo);
+        r.x = __fadd_rn(o.x, r.x); r.y = __fadd_rn(o.y, r.y);
+        r.z = __fadd_rn(o.z, r.z); r.w = __fadd_rn(o.w, r.w);
+      }
+      st4(ea.out + oo, r);
+    } else {
+      for (int e = 0; e < n; ++e)
+        ea.out[oo + e] = ea.accumulate ? __fadd_rn(ea.out[oo + e], c[e]) : c[e];
+    }
+  } else if (EPI == EPI_WGRAD_BF) {
+    const int64_t oo = (int64_t)p * ea.ldo + q;
+    if (n == 4 && (vec & 2)) {
+      float4 g = make_float4(c[0], c[1], c[2], c[3]);
+      if (ea.gW) {
+        const float4 e = ld4(ea.gW + oo);
+        g.x = __fadd_rn(e.x, g.x); g.y = __fadd_rn(e.y, g.y);
+        g.z = __fadd_rn(e.z, g.z); g.w = __fadd_rn(e.w, g.w);
+      }
+      update4(ea.opt, ea.W, g, oo);
+    } else {
+      for (int e = 0; e < n; ++e) {
+        const float g = ea.gW ? __fadd_rn(ea.gW[oo + e], c[e]) : c[e];
+        update1(ea.opt, ea.W, g, oo + e);
+      }
+    }
+  }
+}
+
+// Bias gradient of output row p (wgrad): store / accumulate, or update the bias.
+template <int EPI>
+__device__ __forceinline__ void bias_epilogue(const EpiArgs& ea, int p, float g) {
+  if (EPI == EPI_WGRAD) {
+    ea.db[p] = ea.accumulate ? __fadd_rn(ea.db[p], g) : g;
+  } else if (EPI == EPI_WGRAD_BF) {
+    update1(ea.opt, ea.b, ea.gb ? __fadd_rn(ea.gb[p], g) : g, p);
+  }
+}
+
+// Sum the split partials in split order, then run the epilogue.
+template <int EPI>
+__device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& ea,
+                                                  const float* __restrict__ partial, int vec_epi,
+                                                  int with_db) {
+  if (EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+  const int nq4 = (Q + 3) / 4;
+  const int64_t total = (int64_t)P * nq4;
+  const int64_t PQ = (int64_t)P * Q;
+  for (int64_t idx = blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
+    const int p = (int)(idx / nq4), q = (int)(idx % nq4) * 4;
+    const int n = min(4, Q - q);
+    float c[4] = {0.f, 0.f, 0.f, 0.f};
+    const float* src = partial + (int64_t)p * Q + q;
+    if (n == 4 && (Q & 3) == 0) {
+      float4 s = ld4(src);
+      for (int k = 1; k < S; ++k) {
+        const float4 t = ld4(src + k * PQ);
+        s.x = __fadd_rn(s.x, t.x); s.y = __fadd_rn(s.y, t.y);
+        s.z = __fadd_rn(s.z, t.z); s.w = __fadd_rn(s.w, t.w);
+      }
+      c[0] = s.x; c[1] = s.y; c[2] = s.z; c[3] = s.w;
+    } else {
+      for (int e = 0; e < n; ++e) {
+        float s = src[e];
+        for (int k = 1; k < S; ++k) s = __fadd_rn(s, src[k * PQ + e]);
+        c[e] = s;
+      }
+    }
+    const float* bias = nullptr;
+    if ((EPI == EPI_FWD || EPI == EPI_FWD_FF) && ea.bias) bias = ea.bias + q;
+    epilogue<EPI == EPI_FWD_FF ? EPI_FWD : EPI>(ea, p, q, c, n, bias, vec_epi);
+  }
+  if (with_db) {
+    const float* dbp = partial + (int64_t)S * PQ;
+    for (int p = blockIdx.x * 256 + threadIdx.x; p < P; p += gridDim.x * 256) {
+      float s = dbp[p];
+      for (int k = 1; k < S; ++k) s = __fadd_rn(s, dbp[(int64_t)k * P + p]);
+      bias_epilogue<EPI>(ea, p, s);
+    }
+  }
+}
+
+}  // namespace opfuse

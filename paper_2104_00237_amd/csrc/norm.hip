@@ -1,0 +1,174 @@
+// LayerNorm over the last dimension (biased variance, eps inside the square
+// root), its backward, and two small element-wise helpers (sum of rows, add).
+//
+// Forward: one wavefront per row; mean, then the variance of the centred
+// values, then y = (x - mean) * rstd * gamma + beta; mean and rstd are kept
+// for the backward.
+// Backward, per row: with xh = (x - mean) * rstd and g = dy * gamma,
+//   dx = rstd * (g - mean(g) - xh * mean(g * xh))  (+ the residual gradient);
+// the parameter gradients sum dy * xh and dy over the rows.  They are written
+// as per-row-group partials [G, D], which the element-wise fused update sums
+// in group order while it applies the optimizer, so the gradient vector of
+// gamma and beta is never stored (or of_reduce_rows materialises it).
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace opfuse {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = __fadd_rn(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x, int64_t M,
+                                                     int64_t D, const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta, float eps,
+                                                     float* __restrict__ y,
+                                                     float* __restrict__ mean,
+                                                     float* __restrict__ rstd) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const float* xr = x + row * D;
+  float s = 0.f;
+  for (int64_t j = lane; j < D; j += 64) s = __fadd_rn(s, xr[j]);
+  const float mu = __fdiv_rn(wave_sum(s), (float)D);
+  float q = 0.f;
+  for (int64_t j = lane; j < D; j += 64) {
+    const float d = __fsub_rn(xr[j], mu);
+    q = __fmaf_rn(d, d, q);
+  }
+  const float var = __fdiv_rn(wave_sum(q), (float)D);
+  const float rs = __fdiv_rn(1.f, __fsqrt_rn(__fadd_rn(var, eps)));
+  float* yr = y + row * D;
+  for (int64_t j = lane; j < D; j += 64)
+    yr[j] = __fmaf_rn(__fmul_rn(__fsub_rn(xr[j], mu), rs), gamma[j], beta[j]);
+  if (lane == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
+__global__ __launch_bounds__(256) void ln_bwd_dx_kernel(
+    const float* __restrict__ dy, const float* __restrict__ x, const float* __restrict__ mean,
+    const float* __restrict__ rstd, const float* __restrict__ gamma, const float* __restrict__ dres,
+    int64_t M, int64_t D, float* __restrict__ dx) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const float* xr = x + row * D;
+  const float* dr = dy + row * D;
+  const float mu = mean[row], rs = rstd[row];
+  float s1 = 0.f, s2 = 0.f;
+  for (int64_t j = lane; j < D; j += 64) {
+    const float xh = __fmul_rn(__fsub_rn(xr[j], mu), rs);
+    const float g = __fmul_rn(dr[j], gamma[j]);
+    s1 = __fadd_rn(s1, g);
+    s2 = __fmaf_rn(g, xh, s2);
+  }
+  const float c1 = __fdiv_rn(wave_sum(s1), (float)D);
+  const float c2 = __fdiv_rn(wave_sum(s2), (float)D);
+  float* o = dx + row * D;
+  const float* rr = dres ? dres + row * D : nullptr;
+  for (int64_t j = lane; j < D; j += 64) {
+    const float xh = __fmul_rn(__fsub_rn(xr[j], mu), rs);
+    const float g = __fmul_rn(dr[j], gamma[j]);
+    float v = __fmul_rn(rs, __fsub_rn(__fsub_rn(g, c1), __fmul_rn(xh, c2)));
+    if (rr) v = __fadd_rn(rr[j], v);
+    o[j] = v;
+  }
+}
+
+// Parameter-gradient partials: workgroup (column block, row group) sums its
+// rows in order for 256 columns.
+__global__ __launch_bounds__(256) void ln_bwd_param_kernel(
+    const float* __restrict__ dy, const float* __restrict__ x, const float* __restrict__ mean,
+    const float* __restrict__ rstd, int64_t M, int64_t D, int64_t rows_per_group,
+    float* __restrict__ dgamma_rows, float* __restrict__ dbeta_rows) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t grp = blockIdx.y;
+  if (j >= D) return;
+  const int64_t r0 = grp * rows_per_group, r1 = std::min(M, r0 + rows_per_group);
+  float sg = 0.f, sb = 0.f;
+  for (int64_t r = r0; r < r1; ++r) {
+    const float d = dy[r * D + j];
+    const float xh = __fmul_rn(__fsub_rn(x[r * D + j], mean[r]), rstd[r]);
+    sg = __fmaf_rn(d, xh, sg);
+    sb = __fadd_rn(sb, d);
+  }
+  dgamma_rows[grp * D + j] = sg;
+  dbeta_rows[grp * D + j] = sb;
+}
+
+int64_t ln_partial_rows(int64_t M) { return std::min<int64_t>(64, std::max<int64_t>(1, (M + 63) / 64)); }
+
+hipError_t launch_ln_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
+                         const float* beta, float eps, float* y, float* mean, float* rstd,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(ln_fwd_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, x, M, D, gamma,
+                     beta, eps, y, mean, rstd);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
+                         const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
+                         float* dgamma_rows, float* dbeta_rows, hipStream_t s) {
+  hipLaunchKernelGGL(ln_bwd_dx_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, dy, x, mean,
+                     rstd, gamma, dres, M, D, dx);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t G = ln_partial_rows(M);
+  const int64_t rpg = (M + G - 1) / G;
+  hipLaunchKernelGGL(ln_bwd_param_kernel, dim3((unsigned)((D + 255) / 256), (unsigned)G), dim3(256),
+                     0, s, dy, x, mean, rstd, M, D, rpg, dgamma_rows, dbeta_rows);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void reduce_rows_kernel(const float* __restrict__ src,
+                                                          int64_t rows, int64_t ld, int64_t n,
+                                                          float* __restrict__ dst) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = src[i];
+  for (int64_t r = 1; r < rows; ++r) s = __fadd_rn(s, src[r * ld + i]);
+  dst[i] = s;
+}
+
+hipError_t launch_reduce_rows(const float* src, int64_t rows, int64_t ld, int64_t n, float* dst,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(reduce_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
+                     rows, ld, n, dst);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void add_kernel(const float* __restrict__ a,
+                                                  const float* __restrict__ b, int64_t n, int vec,
+                                                  float* __restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride) {
+      const float4 x = ld4(a + 4 * i), y = ld4(b + 4 * i);
+      st4(out + 4 * i, make_float4(__fadd_rn(x.x, y.x), __fadd_rn(x.y, y.y), __fadd_rn(x.z, y.z),
+                                   __fadd_rn(x.w, y.w)));
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride)
+      out[i] = __fadd_rn(a[i], b[i]);
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride)
+      out[i] = __fadd_rn(a[i], b[i]);
+  }
+}
+
+hipError_t launch_add(const float* a, const float* b, int64_t n, float* out, hipStream_t s) {
+  const int vec = aligned16(a) && aligned16(b) && aligned16(out);
+  const int64_t work = vec ? (n + 3) / 4 : n;
+  const unsigned blocks = (unsigned)std::min<int64_t>(4096, std::max<int64_t>(1, (work + 255) / 256));
+  hipLaunchKernelGGL(add_kernel, dim3(blocks), dim3(256), 0, s, a, b, n, vec, out);
+  return hipGetLastError();
+}
+
+}  // namespace opfuse

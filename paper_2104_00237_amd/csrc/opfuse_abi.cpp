@@ -81,7 +81,13 @@ of_status check_linear(const of_linear_desc* d) {
           "act %d is not an of_act", (int)d->act);
   REQUIRE(d->dtype == OF_F32 || d->dtype == OF_BF16, OF_EINVAL, "dtype %d is not an of_dtype",
           (int)d->dtype);
-  REQUIRE(d->dtype == OF_F32, OF_EUNSUPPORTED, "bf16 operands are not supported by this build");
+  return OF_OK;
+}
+
+// A bf16 shadow of W is only meaningful when the contraction takes bf16 operands.
+of_status check_shadow(const of_linear_desc* d, const of_param* W) {
+  REQUIRE(d->dtype == OF_BF16 || W == nullptr || W->w_bf16 == nullptr, OF_EINVAL,
+          "W->w_bf16 is set but the descriptor's dtype is OF_F32");
   return OF_OK;
 }
 
@@ -94,6 +100,14 @@ int kind_of(int32_t op) {
 
 size_t ws_needed(const of_linear_desc* d, int kind) {
   const int M = (int)d->M, N = (int)d->N, K = (int)d->K;
+  if (d->dtype == OF_BF16) {
+    // bf16 forward-fusion runs its update as a pre-pass, then the plain forward
+    switch (kind) {
+      case EPI_FWD: case EPI_FWD_FF: return gemm_bf16_workspace_bytes(EPI_FWD, M, N, K);
+      case EPI_DGRAD: return gemm_bf16_workspace_bytes(kind, M, K, N);
+      default: return gemm_bf16_workspace_bytes(kind, N, K, M);
+    }
+  }
   switch (kind) {
     case EPI_FWD: case EPI_FWD_FF:
       // one query serves both forwards
@@ -132,27 +146,46 @@ hipEvent_t side_event() {
   return ev;
 }
 
+// Contraction on the fp32 or the bf16 matrix-core path, by the descriptor's dtype.
+hipError_t gemm_dispatch(const of_linear_desc* d, int kind, const GemmProblem& pr,
+                         const EpiArgs& ea, void* ws, hipStream_t s) {
+  return d->dtype == OF_BF16 ? gemm_bf16_launch(kind, pr, ea, ws, s)
+                             : gemm_launch(kind, pr, ea, ws, s);
+}
+
+// The weight operand: the bf16 shadow when the operands are bf16 and it exists.
+void set_weight_operand(const of_linear_desc* d, const of_param* W, GemmProblem& pr) {
+  if (d->dtype == OF_BF16 && W->w_bf16) {
+    pr.B = reinterpret_cast<const float*>(W->w_bf16);
+    pr.b_bf16 = 1;
+  } else {
+    pr.B = W->w;
+  }
+}
+
 // Launch helpers shared by the entry points (arguments already validated).
-of_status run_fwd(const of_linear_desc* d, const float* x, const float* w, const float* b, float* z,
-                  float* y, void* ws, hipStream_t s) {
-  GemmProblem pr{x, ldx_of(d), 1, w, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
+of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
+                  float* z, float* y, void* ws, hipStream_t s) {
+  GemmProblem pr{x, ldx_of(d), 1, nullptr, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
+  set_weight_operand(d, W, pr);
   EpiArgs ea = empty_epi();
   ea.out = y; ea.ldo = ldy_of(d);
   ea.z = z; ea.ldz = ldy_of(d);
   ea.act = d->act;
   ea.bias = d->has_bias ? b : nullptr;
-  return hip_status(gemm_launch(EPI_FWD, pr, ea, ws, s), "of_linear_fwd launch");
+  return hip_status(gemm_dispatch(d, EPI_FWD, pr, ea, ws, s), "of_linear_fwd launch");
 }
 
-of_status run_dgrad(const of_linear_desc* d, const float* dz, const float* w, const float* prev,
+of_status run_dgrad(const of_linear_desc* d, const float* dz, const of_param* W, const float* prev,
                     int32_t act_prev, float* dx, void* ws, hipStream_t s) {
   // dX[m,k] = sum_n dZ[m,n] W[n,k]: A = dZ (reduction-contiguous), B(k, n) = W[n*K + k].
-  GemmProblem pr{dz, ldy_of(d), 1, w, 1, d->K, (int)d->M, (int)d->K, (int)d->N};
+  GemmProblem pr{dz, ldy_of(d), 1, nullptr, 1, d->K, (int)d->M, (int)d->K, (int)d->N};
+  set_weight_operand(d, W, pr);
   EpiArgs ea = empty_epi();
   ea.out = dx; ea.ldo = ldx_of(d);
   ea.prev = prev; ea.ldp = ldx_of(d);
   ea.act = act_prev;
-  return hip_status(gemm_launch(EPI_DGRAD, pr, ea, ws, s), "dgrad launch");
+  return hip_status(gemm_dispatch(d, EPI_DGRAD, pr, ea, ws, s), "dgrad launch");
 }
 
 GemmProblem wgrad_problem(const of_linear_desc* d, const float* dz, const float* x) {
@@ -259,8 +292,10 @@ of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param*
   REQUIRE(!d->has_bias || b, OF_EINVAL, "has_bias is set but b is NULL");
   REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z (its derivative reads Z)");
   REQUIRE(al4(x) && al4(W->w) && al4(b) && al4(z) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  REQUIRE((((uintptr_t)W->w_bf16) & 1u) == 0, OF_EALIGN, "W->w_bf16 must be 2-byte aligned");
+  if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
-  return run_fwd(d, x, W->w, b, z, y, ws, (hipStream_t)stream);
+  return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream);
 }
 
 of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_param* W,
@@ -279,17 +314,19 @@ of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_
   }
   REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z");
   REQUIRE(al4(x) && al4(gW) && al4(gb) && al4(z) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_FWD_FF, ws, ws_bytes)) != OF_OK) return st;
   const hipStream_t s = (hipStream_t)stream;
   const OptK ok = make_optk(*opt);
-  if (d->M > 256) {
-    // The forward's row tiles cannot cover M: several workgroups read each W
-    // tile.  Apply the identical update as one pass right before the contraction.
+  if (d->M > 256 || d->dtype == OF_BF16) {
+    // The forward's row tiles cannot cover M (several workgroups read each W
+    // tile), or the operands are bf16 (whose kernel has no update prologue):
+    // the identical update runs as one pass right before the contraction.
     of_param ps[2] = {*W, d->has_bias ? *b : of_param{}};
     const float* gs[2] = {gW, gb};
     hipError_t e = launch_multi_update(d->has_bias ? 2 : 1, ps, gs, ok, s);
     if (e != hipSuccess) return hip_status(e, "forward-fusion update");
-    return run_fwd(d, x, W->w, d->has_bias ? b->w : nullptr, z, y, ws, s);
+    return run_fwd(d, x, W, d->has_bias ? b->w : nullptr, z, y, ws, s);
   }
   GemmProblem pr{x, ldx_of(d), 1, W->w, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
   EpiArgs ea = empty_epi();
@@ -312,8 +349,10 @@ of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_
   REQUIRE(W->numel == d->N * d->K, OF_EINVAL, "W->numel must be N*K");
   if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
   REQUIRE(al4(dz) && al4(W->w) && al4(dx), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  REQUIRE((((uintptr_t)W->w_bf16) & 1u) == 0, OF_EALIGN, "W->w_bf16 must be 2-byte aligned");
+  if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
-  return run_dgrad(d, dz, W->w, prev, act_prev, dx, ws, (hipStream_t)stream);
+  return run_dgrad(d, dz, W, prev, act_prev, dx, ws, (hipStream_t)stream);
 }
 
 of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const float* x, float* dw,
@@ -329,7 +368,7 @@ of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const f
   ea.db = db;
   ea.with_db = db != nullptr;
   ea.accumulate = accumulate ? 1 : 0;
-  return hip_status(gemm_launch(EPI_WGRAD, wgrad_problem(d, dz, x), ea, ws, (hipStream_t)stream),
+  return hip_status(gemm_dispatch(d, EPI_WGRAD, wgrad_problem(d, dz, x), ea, ws, (hipStream_t)stream),
                     "of_linear_bwd_weight launch");
 }
 
@@ -353,6 +392,7 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
     if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
     if ((st = check_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
   }
+  if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_WGRAD_BF, ws_update, ws_update_bytes)) != OF_OK) return st;
   const hipStream_t s = (hipStream_t)stream;
   hipStream_t su = s;
@@ -364,7 +404,7 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
   }
   if (dx_prev) {
     // Data gradient first, with the old W (the dependency rule after Alg. 3).
-    if ((st = run_dgrad(d, dz, W->w, prev, act_prev, dx_prev, ws, s)) != OF_OK) return st;
+    if ((st = run_dgrad(d, dz, W, prev, act_prev, dx_prev, ws, s)) != OF_OK) return st;
   }
   if (ev) {
     if ((st = hip_status(hipEventRecord(ev, s), "hipEventRecord")) != OF_OK) return st;
@@ -377,7 +417,7 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
   if (b) { ea.b = *b; ea.gb = gb_partial; }
   ea.with_db = b != nullptr;
   ea.opt = make_optk(*opt);
-  return hip_status(gemm_launch(EPI_WGRAD_BF, wgrad_problem(d, dz, x), ea, ws_update, su),
+  return hip_status(gemm_dispatch(d, EPI_WGRAD_BF, wgrad_problem(d, dz, x), ea, ws_update, su),
                     "of_linear_bwd_fused launch");
 }
 
@@ -543,6 +583,54 @@ of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B,
           "misaligned pointer");
   return hip_status(launch_xent(logits, labels, B, C, ld ? ld : C, loss, dlogits, (hipStream_t)stream),
                     "of_xent_fwd_bwd launch");
+}
+
+of_status of_layernorm_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
+                           const float* beta, float eps, float* y, float* mean, float* rstd,
+                           void* stream) {
+  REQUIRE(x && gamma && beta && y && mean && rstd, OF_EINVAL,
+          "x, gamma, beta, y, mean and rstd are required");
+  REQUIRE(M >= 1 && D >= 1, OF_EINVAL, "M and D must be >= 1");
+  REQUIRE(std::isfinite(eps) && eps > 0.f, OF_EINVAL, "eps must be finite and > 0");
+  REQUIRE(al4(x) && al4(gamma) && al4(beta) && al4(y) && al4(mean) && al4(rstd), OF_EALIGN,
+          "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_ln_fwd(x, M, D, gamma, beta, eps, y, mean, rstd, (hipStream_t)stream),
+                    "of_layernorm_fwd launch");
+}
+
+int64_t of_layernorm_partial_rows(int64_t M) { return M >= 1 ? ln_partial_rows(M) : 0; }
+
+of_status of_layernorm_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
+                           const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
+                           float* dgamma_rows, float* dbeta_rows, void* stream) {
+  REQUIRE(dy && x && mean && rstd && gamma && dx && dgamma_rows && dbeta_rows, OF_EINVAL,
+          "dy, x, mean, rstd, gamma, dx, dgamma_rows and dbeta_rows are required");
+  REQUIRE(M >= 1 && D >= 1, OF_EINVAL, "M and D must be >= 1");
+  REQUIRE(dx != dy && dx != x, OF_EINVAL, "dx must not alias dy or x (both are read again)");
+  REQUIRE(al4(dy) && al4(x) && al4(mean) && al4(rstd) && al4(gamma) && al4(dres) && al4(dx) &&
+              al4(dgamma_rows) && al4(dbeta_rows),
+          OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_ln_bwd(dy, x, mean, rstd, gamma, dres, M, D, dx, dgamma_rows,
+                                  dbeta_rows, (hipStream_t)stream),
+                    "of_layernorm_bwd launch");
+}
+
+of_status of_reduce_rows(const float* src, int64_t rows, int64_t ld, int64_t n, float* dst,
+                         void* stream) {
+  REQUIRE(src && dst, OF_EINVAL, "src and dst are required");
+  REQUIRE(rows >= 1 && n >= 1, OF_EINVAL, "rows and n must be >= 1");
+  if (ld == 0) ld = n;
+  REQUIRE(ld >= n, OF_EINVAL, "ld must be 0 or >= n");
+  REQUIRE(al4(src) && al4(dst), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_reduce_rows(src, rows, ld, n, dst, (hipStream_t)stream),
+                    "of_reduce_rows launch");
+}
+
+of_status of_add(const float* a, const float* b, int64_t n, float* out, void* stream) {
+  REQUIRE(a && b && out, OF_EINVAL, "a, b and out are required");
+  REQUIRE(n >= 1, OF_EINVAL, "n must be >= 1");
+  REQUIRE(al4(a) && al4(b) && al4(out), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_add(a, b, n, out, (hipStream_t)stream), "of_add launch");
 }
 
 size_t of_mse_workspace_size(int64_t M, int64_t D) { return mse_ws_bytes(M, D); }

@@ -127,3 +127,27 @@ def test_loss_validation(lib):
     assert _status(L.of_xent_fwd_bwd, FAKE, FAKE + 4, 4, 10, 0, FAKE, FAKE, None) == L.OF_EALIGN
     assert _status(L.of_mse_fwd_bwd, FAKE, FAKE, 4, 8, 0, FAKE, FAKE, FAKE, 0, None) == L.OF_EWORKSPACE
     assert L.of_mse_workspace_size(4, 8) > 0
+
+
+def test_bf16_shadow_and_norm_validation(lib):
+    # a bf16 shadow with fp32 operands is a caller error
+    Ws = L.OfParam(FAKE, FAKE, FAKE, FAKE, 16 * 12)
+    assert _status(L.of_linear_fwd, _desc(), FAKE, Ws, None, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert "w_bf16" in L.of_last_error()
+    assert _status(L.of_linear_bwd_data, _desc(), FAKE, Ws, None, 0, FAKE, None, 0, None) == L.OF_EINVAL
+    # odd shadow address
+    Wo = L.OfParam(FAKE, FAKE, FAKE, FAKE + 1, 16 * 12)
+    assert _status(L.of_linear_fwd, _desc(dtype=L.OF_BF16), FAKE, Wo, None, None, FAKE, None, 0,
+                   None) == L.OF_EALIGN
+    # bf16 workspace queries answer for the bf16 kernels (a split for a tall wgrad)
+    assert L.of_linear_workspace_size(_desc(M=4096, N=1024, K=1024, dtype=L.OF_BF16),
+                                      L.OF_LINEAR_BWD_WEIGHT) > 0
+    assert _status(L.of_layernorm_fwd, FAKE, 0, 8, FAKE, FAKE, 1e-5, FAKE, FAKE, FAKE, None) == L.OF_EINVAL
+    assert _status(L.of_layernorm_fwd, FAKE, 4, 8, FAKE, FAKE, 0.0, FAKE, FAKE, FAKE, None) == L.OF_EINVAL
+    assert _status(L.of_layernorm_fwd, FAKE + 2, 4, 8, FAKE, FAKE, 1e-5, FAKE, FAKE, FAKE,
+                   None) == L.OF_EALIGN
+    assert _status(L.of_layernorm_bwd, FAKE, FAKE + 64, FAKE, FAKE, FAKE, None, 4, 8, FAKE, FAKE,
+                   FAKE, None) == L.OF_EINVAL   # dx aliases dy
+    assert L.of_layernorm_partial_rows(4096) == 64 and L.of_layernorm_partial_rows(1) == 1
+    assert _status(L.of_reduce_rows, FAKE, 2, 3, 8, FAKE, None) == L.OF_EINVAL   # ld < n
+    assert _status(L.of_add, FAKE, None, 8, FAKE, None) == L.OF_EINVAL
