@@ -34,6 +34,7 @@ from workloads import get_config, make_params, make_batch  # noqa: E402
 
 PEAK_HBM = 8.0e12          # bytes/s
 PEAK_FP32_MFMA = 157.3e12  # flop/s
+PEAK_BF16_MFMA = 2.5e15    # flop/s, dense
 
 METRIC = "fused train-step time & update GB/s vs unfused eager; % of HBM/MFMA roofline"
 
@@ -74,6 +75,8 @@ def layer_launches(cfg):
         return 4 * n * (2 + 2 * h)
 
     layers = []                      # (name, kind, M, N, K, in_elems, out_elems, bias, act_prev, pool)
+    if cfg["kind"] == "tblock":
+        return tblock_launches(cfg)
     if cfg["kind"] == "mlp":
         M, dims = cfg["batch"], cfg["dims"]
         for i in range(1, len(dims)):
@@ -118,6 +121,45 @@ def layer_launches(cfg):
     return out
 
 
+def tblock_launches(cfg):
+    """Per-launch costs of the bf16 Transformer blocks.  Contractions take bf16
+    operands: the weight is read as its 2-byte shadow, activations and
+    gradients as fp32; the fused update also rewrites the shadow.  LayerNorm
+    and the residual adds count as `extra` bytes of their block."""
+    M, d, f, nb = cfg["batch"], cfg["hidden"], cfg["ffn"], cfg["blocks"]
+    h = 2 if cfg["opt"]["kind"] != "sgd" else 1
+    G = min(64, max(1, (M + 63) // 64))
+    out = []
+    for b in range(1, nb + 1):
+        p = f"blk{b}."
+        for name, N, K, act_prev, gelu in (("qkv", 3 * d, d, False, False),
+                                           ("proj", d, d, False, False),
+                                           ("fc1", f, d, False, True),
+                                           ("fc2", d, f, True, False)):
+            wb, xb, yb = 2 * N * K, 4 * M * K, 4 * M * N
+            upd_w = 4 * N * K * (2 + 2 * h) + 2 * N * K
+            upd_b = 4 * N * (2 + 2 * h)
+            fl = 2 * M * N * K
+            out.append(dict(
+                name=p + name, kind="linear", M=M, N=N, K=K, nparams=N * K + N, dtype="bf16",
+                fwd=(fl, xb + wb + yb * (2 if gelu else 1) + 4 * N),
+                fwd_ff=(fl, xb + wb + yb * (2 if gelu else 1) + 4 * N + upd_w + 4 * N * K + upd_b),
+                dgrad=(fl, yb + wb + xb + (xb if act_prev else 0)),
+                wgrad=(fl, yb + xb + 4 * N * K + 4 * N),
+                wgrad_bf=(fl, yb + xb + upd_w + upd_b),
+                extra=0,
+            ))
+        for name in ("ln1", "ln2"):
+            md = 4 * M * d
+            # fwd R x W y, mean, rstd; bwd R dy, x, dres W dx (+ the parameter pass
+            # R dy, x W 2 G d); residual add R 2 W 1
+            extra = (2 * md + 8 * M) + (4 * md + 8 * M) + (2 * md + 8 * G * d) + 3 * md
+            out.append(dict(name=p + name, kind="ln", M=M, N=d, K=0, nparams=2 * d, dtype="f32",
+                            fwd=None, fwd_ff=None, dgrad=None, wgrad=None, wgrad_bf=None,
+                            extra=extra))
+    return out
+
+
 def step_cost(cfg, ordering):
     """Whole-step algorithmic flops and bytes (kernels as implemented)."""
     L = layer_launches(cfg)
@@ -126,7 +168,7 @@ def step_cost(cfg, ordering):
         fk = "fwd_ff" if ordering == "ff" else "fwd"
         wk = "wgrad_bf" if ordering == "bf" else "wgrad"
         for k in (fk, "dgrad", wk):
-            if d[k] is not None:
+            if d.get(k) is not None:
                 F += d[k][0]
                 B += d[k][1]
         B += d["extra"]
@@ -139,21 +181,28 @@ def step_cost(cfg, ordering):
 
 
 def describe_layers(cfg):
+    if cfg["kind"] == "tblock":
+        return (f"{cfg['blocks']} pre-LN blocks, hidden {cfg['hidden']}, FFN {cfg['ffn']}, "
+                f"bf16 operands")
     if cfg["kind"] == "mlp":
         return f"{len(cfg['dims']) - 1} linear, width {cfg['dims'][1]}"
     return (f"{len(cfg['channels'])} conv3x3 ({','.join(map(str, cfg['channels']))}), "
             f"max-pool after {cfg['pool_after']}, linear classifier, {cfg['image']}x{cfg['image']}")
 
 
-def kernel_roofline(flops, nbytes, seconds):
-    t_hbm, t_mfma = nbytes / PEAK_HBM, flops / PEAK_FP32_MFMA
+def mfma_peak(cfg):
+    return PEAK_BF16_MFMA if cfg["dtype"] == "bf16" else PEAK_FP32_MFMA
+
+
+def kernel_roofline(flops, nbytes, seconds, peak_mfma=PEAK_FP32_MFMA):
+    t_hbm, t_mfma = nbytes / PEAK_HBM, flops / peak_mfma
     if t_hbm >= t_mfma:
         ach = nbytes / seconds / 1e9
         return dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM / 1e9, unit="GB/s",
                     frac=round(ach / (PEAK_HBM / 1e9), 4))
     ach = flops / seconds / 1e12
-    return dict(bound="mfma", achieved=round(ach, 2), peak=PEAK_FP32_MFMA / 1e12,
-                unit="TFLOP/s", frac=round(ach / (PEAK_FP32_MFMA / 1e12), 4))
+    return dict(bound="mfma", achieved=round(ach, 2), peak=peak_mfma / 1e12,
+                unit="TFLOP/s", frac=round(ach / (peak_mfma / 1e12), 4))
 
 
 def traffic_for(kernel_class, workload):
@@ -206,8 +255,15 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
 
 
 def cpu_baseline(cfg, budget_s=15.0):
+    """Oracle eager steps on this host, seconds per step of `cfg`.  The 12-block
+    Transformer stack is sampled as one block (same width and tokens) and its
+    time scaled by the block count."""
     import oracle
     from oracle.train import new_model
+    scale = 1
+    if cfg["kind"] == "tblock":
+        scale = cfg["blocks"]
+        cfg = dict(cfg, blocks=1)
     model = new_model(cfg)
     t0 = time.perf_counter()
     n = 0
@@ -218,7 +274,7 @@ def cpu_baseline(cfg, budget_s=15.0):
         n += 1
         if time.perf_counter() - t0 >= budget_s or n >= cfg["steps"]:
             break
-    dt = (time.perf_counter() - t0) / n
+    dt = (time.perf_counter() - t0) / n * scale
     del oracle
     return dt, n
 
@@ -252,7 +308,7 @@ def main():
 
     import torch
     cfg = get_config(args.workload)
-    if cfg["kind"] not in ("mlp", "vgg") or cfg["dtype"] != "f32":
+    if cfg["kind"] not in ("mlp", "vgg", "tblock"):
         print(f"workload {args.workload} has no GPU path in this build", file=sys.stderr)
         sys.exit(2)
     dev = torch.device("cuda:0")
@@ -290,7 +346,8 @@ def main():
     by_shape = {}
     for d_ms, op in recs:
         by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name))
-    shape = max(by_shape, key=lambda s: sum(d for d, _ in by_shape[s]))
+    costed = [k for k in by_shape if launches[by_shape[k][0][1]].get(dom)]
+    shape = max(costed, key=lambda s: sum(d for d, _ in by_shape[s]))
     durs = [d for d, _ in by_shape[shape]]
     per = launches[by_shape[shape][0][1]][dom]
     # Each launch is bracketed by an event pair on its own stream; the pair's own
@@ -299,7 +356,7 @@ def main():
     dom_stream = torch.cuda.Stream() if dom == "wgrad_bf" else torch.cuda.current_stream()
     marker_ms = KernelTimer.marker_overhead_ms(dom_stream)
     avg_s = (float(np.mean(durs)) - marker_ms) / 1e3
-    roof = kernel_roofline(per[0], per[1], avg_s)
+    roof = kernel_roofline(per[0], per[1], avg_s, mfma_peak(cfg))
     roof.update(kernel=dom, layers=sorted({n for _, n in by_shape[shape]}),
                 shape=f"{shape[0]} GEMM M={shape[1]} N={shape[2]} K={shape[3]}",
                 avg_us=round(avg_s * 1e6, 3), launches=len(durs),
@@ -314,7 +371,7 @@ def main():
     bf_s = res["bf"]["ms"] / 1e3
     value = upd_bytes / bf_s / 1e9
     F, B = step_cost(cfg, "bf")
-    step_roof_s = max(B / PEAK_HBM, F / PEAK_FP32_MFMA)
+    step_roof_s = max(B / PEAK_HBM, F / mfma_peak(cfg))
 
     out = {
         "metric": METRIC,
@@ -327,7 +384,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16" if cfg["dtype"] == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "global_batch": cfg["batch"],
                    "layers": describe_layers(cfg),
@@ -361,8 +418,10 @@ def main():
         out["cpu_baseline"] = {"value": round(eager_bytes / dt / 1e9, 4), "unit": "GB/s",
                                "cores": cores, "kind": "oracle",
                                "ms_per_step": round(dt * 1e3, 2),
-                               "sample": f"{n} eager float64 steps of {args.workload} "
-                                         f"(oracle, numpy, {cores} host threads)"}
+                               "sample": f"{n} eager float64 steps of {args.workload}"
+                                         + (" (one of its blocks, time x blocks)"
+                                            if cfg["kind"] == "tblock" else "")
+                                         + f" (oracle, numpy, {cores} host threads)"}
     print(json.dumps(out))
 
 

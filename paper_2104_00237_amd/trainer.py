@@ -1,11 +1,11 @@
 """Host scheduler: the three training orderings over the opfuse C ABI.
 
 The model is a topologically sorted array of operators (the input of Alg. 2
-and Alg. 3): linear or 3x3-convolution layers, each followed by its
-activation (fused into the kernel's epilogue) and optionally by a 2x2
-max-pool.  Every kernel runs in libopfuse.so; this module only decides which
-entry point runs where and keeps the per-parameter state the paper's
-algorithms need:
+and Alg. 3): a chain of linear or 3x3-convolution layers, each followed by
+its activation (fused into the kernel's epilogue) and optionally by a 2x2
+max-pool, or pre-LN residual blocks of LayerNorm and bf16-operand linears.
+Every kernel runs in libopfuse.so; this module only decides which entry point
+runs where and keeps the per-parameter state the paper's algorithms need:
 
   step[theta]   1-based index of the update applied last (mirrored on the device)
   updated[f]    Alg. 2 flag: False while f holds a pending update
@@ -15,10 +15,10 @@ Orderings (Section 3, Fig. 1(b)-(d)):
   eager  forward; backward writing every gradient; one multi-tensor optimizer
          launch over every parameter.
   ff     forward-fusion: a layer whose `updated` flag is False applies its
-         pending update in its forward (linear layers: of_linear_fwd_fused,
-         while the W tiles load; convolutions: an element-wise pass right
-         before the forward); backward writes the gradients, which stay
-         pending; flush() applies what is still pending.
+         pending update in its forward (fp32 linear layers: of_linear_fwd_fused,
+         while the W tiles load; convolutions, LayerNorms and bf16 linears: an
+         element-wise pass right before the forward); backward writes the
+         gradients, which stay pending; flush() applies what is still pending.
   bf     backward-fusion: each layer's data gradient runs with the old weights
          on the main stream, then its weight-gradient kernel with the
          optimizer in the epilogue runs on a second stream, so the update of
@@ -33,16 +33,34 @@ import torch
 from . import _lib as L
 
 
-class ParamBuf:
-    """A trainable tensor on the device with its history and host counters."""
+def _bf16_bits(a):
+    """bf16 bits (round to nearest even) of fp32 values, as int16 for torch."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    nan = np.isnan(np.asarray(a, np.float32))
+    r[nan] = ((u[nan] >> 16) | 0x40).astype(np.uint16)
+    return r.view(np.int16)
 
-    def __init__(self, name, value, kind, device, with_grad=True):
+
+class ParamBuf:
+    """A trainable tensor on the device with its history and host counters.
+
+    g holds the gradient as one vector (eager, and forward-fusion's pending
+    gradient); a LayerNorm parameter also has `rows`, its gradient as row-group
+    partials [G, numel] (summed by the fused update, or reduced into g).
+    A bf16-operand weight also keeps its bf16 shadow `wb`.
+    """
+
+    def __init__(self, name, value, kind, device, shadow=False, rows=0):
         self.name = name
         self.w = torch.as_tensor(np.ascontiguousarray(value, dtype=np.float32)).to(device)
         self.m = torch.zeros_like(self.w)
         self.v = torch.zeros_like(self.w) if kind != "sgd" else None
-        self.g = torch.zeros_like(self.w) if with_grad else None
-        self.p = L.param_of(self.w, self.m, self.v)
+        self.g = torch.zeros_like(self.w)
+        self.wb = torch.as_tensor(_bf16_bits(value)).to(device) if shadow else None
+        self.rows = (torch.zeros((rows,) + tuple(self.w.shape), dtype=torch.float32, device=device)
+                     if rows else None)
+        self.p = L.param_of(self.w, self.m, self.v, self.wb)
         self.step = 0
         self.count = 0
 
@@ -50,22 +68,47 @@ class ParamBuf:
     def numel(self):
         return self.w.numel()
 
+    def pending(self):
+        """(device pointer, rows, row stride) of the gradient an update consumes."""
+        if self.rows is not None:
+            return self.rows.data_ptr(), self.rows.shape[0], self.numel
+        return self.g.data_ptr(), 1, 0
+
+    def set(self, value):
+        self.w.copy_(torch.as_tensor(np.asarray(value, np.float32)))
+        if self.wb is not None:
+            self.wb.copy_(torch.as_tensor(_bf16_bits(np.asarray(value, np.float32))))
+
+    def set_pending(self, g):
+        g = torch.as_tensor(np.asarray(g, np.float32))
+        if self.rows is not None:
+            self.rows.zero_()
+            self.rows[0].copy_(g)
+        else:
+            self.g.copy_(g)
+
 
 def _ptr(t):
     return t.data_ptr() if t is not None else None
 
 
+def _update(tr, p, stream):
+    """Element-wise fused update of p from its pending gradient (a7)."""
+    ptr, rows, ld = p.pending()
+    L.of_elementwise_fused_update(p.p, ptr, rows, ld, tr.opt, stream)
+
+
 class LinearOp:
-    """f = act(X W^T + b) on a [M, K] input."""
+    """f = act(X W^T + b) on a [M, K] input (row stride ldx)."""
 
     kind = "linear"
 
-    def __init__(self, name, W, b, M, act):
+    def __init__(self, name, W, b, M, act, dtype=L.OF_F32, ldx=0):
         N, K = W.w.shape
         self.name, self.W, self.b = name, W, b
         self.M, self.N, self.K = M, N, K
         self.act = act
-        self.desc = L.OfLinearDesc(M, N, K, 0, 0, L.OF_F32, L.ACTS[act], int(b is not None))
+        self.desc = L.OfLinearDesc(M, N, K, ldx, 0, dtype, L.ACTS[act], int(b is not None))
         self.updated = True
         self.params = [W] if b is None else [W, b]
         self.out_shape = (M, N)
@@ -73,14 +116,14 @@ class LinearOp:
     def ws(self, which):
         return L.of_linear_workspace_size(self.desc, which)
 
-    def fwd(self, tr, x, y):
-        L.of_linear_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, None, y,
+    def fwd(self, tr, x, y, z=None):
+        L.of_linear_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z, y,
                         *tr.ws_main_args(), tr._s())
 
-    def fwd_ff(self, tr, x, y):
+    def fwd_ff(self, tr, x, y, z=None):
         b = self.b
         L.of_linear_fwd_fused(self.desc, x, self.W.p, self.W.g.data_ptr(),
-                              b.p if b else None, b.g.data_ptr() if b else None, tr.opt, None, y,
+                              b.p if b else None, b.g.data_ptr() if b else None, tr.opt, z, y,
                               *tr.ws_main_args(), tr._s())
 
     def dgrad(self, tr, g, prev, act_prev, dx):
@@ -132,7 +175,7 @@ class ConvOp:
         # The pending update runs element-wise right before the forward; the
         # filter-tile prologue of the convolution is not fused.
         for p in self.params:
-            L.of_elementwise_fused_update(p.p, p.g.data_ptr(), 1, 0, tr.opt, tr._s())
+            _update(tr, p, tr._s())
         self.fwd(tr, x, y)
 
     def dgrad(self, tr, g, prev, act_prev, dx):
@@ -150,24 +193,56 @@ class ConvOp:
                               *tr.ws_side_args(), stream)
 
 
-class Trainer:
-    """Trains one workload on one GPU under a chosen ordering."""
+class LayerNormOp:
+    """f = LayerNorm(X) * gamma + beta over the last dimension of [M, D]."""
 
-    def __init__(self, cfg, init, device="cuda:0"):
-        if cfg["dtype"] != "f32":
-            raise NotImplementedError("only fp32 operands in this build")
-        L.load()
-        self.cfg, self.hyper = cfg, cfg["opt"]
-        self.device = torch.device(device)
-        kind = self.hyper["kind"]
-        self.params = {}
+    kind = "ln"
+
+    def __init__(self, name, g, b, M, D, eps):
+        self.name, self.g, self.b = name, g, b
+        self.M, self.D, self.eps = M, D, eps
+        self.N, self.K = D, 0
+        self.updated = True
+        self.params = [g, b]
+
+    def ws(self, which):
+        return 0
+
+    def fwd(self, tr, x, y, mu, rs):
+        L.of_layernorm_fwd(x, self.M, self.D, self.g.w.data_ptr(), self.b.w.data_ptr(), self.eps,
+                           y, mu, rs, tr._s())
+
+    def fwd_ff(self, tr, x, y, mu, rs):
+        for p in self.params:
+            _update(tr, p, tr._s())
+        self.fwd(tr, x, y, mu, rs)
+
+    def bwd(self, tr, dy, x, mu, rs, dres, dx):
+        """dx (+ dres) and the parameter-gradient row partials."""
+        L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx,
+                           self.g.rows.data_ptr(), self.b.rows.data_ptr(), tr._s())
+
+    def reduce(self, tr):
+        """Eager: materialise the gradient vectors from the row partials."""
+        for p in self.params:
+            L.of_reduce_rows(p.rows.data_ptr(), p.rows.shape[0], 0, p.numel, p.g.data_ptr(),
+                             tr._s())
+
+
+def _side_after_main(tr):
+    """Order the side stream after everything enqueued so far on the main stream."""
+    ev = torch.cuda.Event()
+    ev.record(tr.stream)
+    tr.side.wait_event(ev)
+
+
+class ChainNet:
+    """Linear / conv layers in a chain, each with its activation and an
+    optional 2x2 max-pool after it (the MLP and VGG workloads)."""
+
+    def __init__(self, tr, cfg, pb):
+        self.tr = tr
         self.ops, self.pool = [], []
-
-        def pb(name):
-            p = ParamBuf(name, init[name], kind, self.device)
-            self.params[name] = p
-            return p
-
         if cfg["kind"] == "mlp":
             M, dims = cfg["batch"], cfg["dims"]
             nl = len(dims) - 1
@@ -176,8 +251,8 @@ class Trainer:
                 b = pb(f"fc{i}.bias") if cfg["bias"] else None
                 self.ops.append(LinearOp(f"fc{i}", W, b, M, cfg["act"] if i < nl else "none"))
                 self.pool.append(False)
-        elif cfg["kind"] == "vgg":
-            N, s, c = cfg["batch"], cfg["image"], cfg["in_channels"]
+        else:
+            N, s = cfg["batch"], cfg["image"]
             for i, cout in enumerate(cfg["channels"], start=1):
                 W, b = pb(f"conv{i}.weight"), pb(f"conv{i}.bias")
                 self.ops.append(ConvOp(f"conv{i}", W, b, N, s, s, "relu"))
@@ -185,15 +260,12 @@ class Trainer:
                 self.pool.append(pool)
                 if pool:
                     s //= 2
-                c = cout
             if s != 1:
                 raise NotImplementedError("the classifier expects a 1x1 feature map")
             self.ops.append(LinearOp("fc", pb("fc.weight"), pb("fc.bias"), N, "none"))
             self.pool.append(False)
-        else:
-            raise NotImplementedError(f"model kind {cfg['kind']!r} has no GPU path in this build")
-
-        f32 = dict(dtype=torch.float32, device=self.device)
+        dev = tr.device
+        f32 = dict(dtype=torch.float32, device=dev)
         n = len(self.ops)
         # y[i]: layer i's output after its activation; gz[i]: gradient w.r.t. its
         # pre-activation; p/arg/gp: pooled output, position of each window's
@@ -206,12 +278,282 @@ class Trainer:
                 N_, H_, W_, C_ = op.out_shape
                 ps = (N_, H_ // 2, W_ // 2, C_)
                 self.p[i] = torch.empty(ps, **f32)
-                self.arg[i] = torch.empty(ps, dtype=torch.uint8, device=self.device)
+                self.arg[i] = torch.empty(ps, dtype=torch.uint8, device=dev)
                 self.gp[i] = torch.empty(ps, **f32)
+        self.out, self.gout = self.y[-1], self.gz[-1]
+
+    def _in(self, i, x):
+        """Device pointer of layer i's input."""
+        if i == 0:
+            return x.data_ptr()
+        return (self.p[i - 1] if self.pool[i - 1] else self.y[i - 1]).data_ptr()
+
+    def forward(self, x, fused):
+        tr = self.tr
+        for i, op in enumerate(self.ops):
+            if fused and not op.updated:
+                tr._t0("fwd_ff", tr.stream, op)
+                op.fwd_ff(tr, self._in(i, x), self.y[i].data_ptr())
+                tr._t1("fwd_ff", tr.stream)
+                op.updated = True
+            else:
+                tr._t0("fwd", tr.stream, op)
+                op.fwd(tr, self._in(i, x), self.y[i].data_ptr())
+                tr._t1("fwd", tr.stream)
+            if self.pool[i]:
+                N, H, W, C = op.out_shape
+                L.of_maxpool2x2_fwd(self.y[i].data_ptr(), N, H, W, C, self.p[i].data_ptr(),
+                                    self.arg[i].data_ptr(), tr._s())
+
+    def _dgrad_target(self, i):
+        """Where layer i's data gradient goes: (dx, prev, act_prev).  Through a
+        max-pool the ReLU mask is applied by the pool's backward instead."""
+        if self.pool[i - 1]:
+            return self.gp[i - 1].data_ptr(), None, L.OF_ACT_NONE
+        prev_act = self.ops[i - 1].act
+        prev = self.y[i - 1].data_ptr() if prev_act != "none" else None
+        return self.gz[i - 1].data_ptr(), prev, L.ACTS[prev_act]
+
+    def _pool_bwd(self, i):
+        """After layer i's data gradient: back through layer i-1's max-pool and ReLU."""
+        if i > 0 and self.pool[i - 1]:
+            N, H, W, C = self.ops[i - 1].out_shape
+            L.of_maxpool2x2_bwd(self.gp[i - 1].data_ptr(), self.arg[i - 1].data_ptr(),
+                                self.y[i - 1].data_ptr(), N, H, W, C,
+                                self.gz[i - 1].data_ptr(), self.tr._s())
+
+    def _dgrad(self, i, op):
+        tr = self.tr
+        dx, prev, act_prev = self._dgrad_target(i)
+        tr._t0("dgrad", tr.stream, op)
+        op.dgrad(tr, self.gz[i].data_ptr(), prev, act_prev, dx)
+        tr._t1("dgrad", tr.stream)
+
+    def backward_plain(self, x):
+        tr = self.tr
+        for i in reversed(range(len(self.ops))):
+            op = self.ops[i]
+            if i > 0:
+                self._dgrad(i, op)
+            tr._t0("wgrad", tr.stream, op)
+            op.wgrad(tr, self.gz[i].data_ptr(), self._in(i, x))
+            tr._t1("wgrad", tr.stream)
+            self._pool_bwd(i)
+
+    def backward_fused(self, x, done):
+        """Backward-fusion: `done(op)` is called after each layer's update is enqueued."""
+        tr = self.tr
+        timed = tr.timer is not None and tr.timer.wants("wgrad_bf")
+        for i in reversed(range(len(self.ops))):
+            op = self.ops[i]
+            if op.kind == "linear" and not timed:
+                # one library call: dgrad with the old W on the main stream, then
+                # the fused update on the side stream behind an event
+                dx, prev, act_prev = self._dgrad_target(i) if i > 0 else (None, None, 0)
+                op.bwd_fused(tr, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx)
+            else:
+                # the same order by hand (events can then bracket the fused kernel):
+                # dgrad on the main stream, event, fused wgrad + update on the side
+                if i > 0:
+                    self._dgrad(i, op)
+                _side_after_main(tr)
+                tr._t0("wgrad_bf", tr.side, op)
+                op.wgrad_fused(tr, self.gz[i].data_ptr(), self._in(i, x), tr.side.cuda_stream)
+                tr._t1("wgrad_bf", tr.side)
+            self._pool_bwd(i)
+            done(op)
+
+    def argmax(self):
+        return {i: a for i, a in enumerate(self.arg) if a is not None}
+
+
+class TBlockNet:
+    """Pre-LN residual blocks with bf16-operand linears (the tblock workload):
+
+        a = LN1(x); qkv = a Wqkv^T + b; v = qkv[:, 2d:3d]   (identity attention)
+        h = x + v Wproj^T + b
+        c = LN2(h); u = c W1^T + b; g = GELU(u); y = h + g W2^T + b
+
+    Every tensor a later kernel reads is kept per block, and so is every
+    gradient buffer, so the side stream's fused updates of block b never race
+    with the main stream's back-propagation through the blocks below.
+    """
+
+    def __init__(self, tr, cfg, pb):
+        self.tr = tr
+        M, d, f, nb = cfg["batch"], cfg["hidden"], cfg["ffn"], cfg["blocks"]
+        self.M, self.d, self.f = M, d, f
+        dt = L.OF_BF16 if cfg["dtype"] == "bf16" else L.OF_F32
+        eps = cfg["ln_eps"]
+        G = L.of_layernorm_partial_rows(M)
+        shadow = dt == L.OF_BF16
+        self.blocks = []
+        self.ops = []
+        for b in range(1, nb + 1):
+            p = f"blk{b}."
+            blk = dict(
+                ln1=LayerNormOp(p + "ln1", pb(p + "ln1.weight", rows=G), pb(p + "ln1.bias", rows=G),
+                                M, d, eps),
+                qkv=LinearOp(p + "qkv", pb(p + "qkv.weight", shadow), pb(p + "qkv.bias"), M, "none",
+                             dt),
+                proj=LinearOp(p + "proj", pb(p + "proj.weight", shadow), pb(p + "proj.bias"), M,
+                              "none", dt, ldx=3 * d),
+                ln2=LayerNormOp(p + "ln2", pb(p + "ln2.weight", rows=G), pb(p + "ln2.bias", rows=G),
+                                M, d, eps),
+                fc1=LinearOp(p + "fc1", pb(p + "fc1.weight", shadow), pb(p + "fc1.bias"), M, "gelu",
+                             dt),
+                fc2=LinearOp(p + "fc2", pb(p + "fc2.weight", shadow), pb(p + "fc2.bias"), M, "none",
+                             dt),
+            )
+            self.ops += [blk[k] for k in ("ln1", "qkv", "proj", "ln2", "fc1", "fc2")]
+            self.blocks.append(blk)
+        f32 = dict(dtype=torch.float32, device=tr.device)
+
+        def t(*shape):
+            return torch.empty(shape, **f32)
+
+        for blk in self.blocks:
+            blk.update(a=t(M, d), mu1=t(M), rs1=t(M), qkv_out=t(M, 3 * d), o=t(M, d), h=t(M, d),
+                       c=t(M, d), mu2=t(M), rs2=t(M), u=t(M, f), g=t(M, f), w=t(M, d), y=t(M, d),
+                       gy=t(M, d), gu=t(M, f), gc=t(M, d), gh=t(M, d), ga=t(M, d),
+                       # the Q and K thirds of the QKV gradient stay zero
+                       gqkv=torch.zeros((M, 3 * d), **f32))
+        self.gx = t(M, d)   # gradient w.r.t. the network input (not used further)
+        self.out = self.blocks[-1]["y"]
+        self.gout = self.blocks[-1]["gy"]
+
+    def forward(self, x, fused):
+        tr = self.tr
+        d, n = self.d, self.M * self.d
+        xin = x.data_ptr()
+        for blk in self.blocks:
+            for name in ("ln1", "qkv", "proj", "ln2", "fc1", "fc2"):
+                op = blk[name]
+                ff = fused and not op.updated
+                cls = "fwd_ff" if ff else "fwd"
+                tr._t0(cls, tr.stream, op)
+                if name == "ln1":
+                    (op.fwd_ff if ff else op.fwd)(tr, xin, blk["a"].data_ptr(),
+                                                  blk["mu1"].data_ptr(), blk["rs1"].data_ptr())
+                elif name == "qkv":
+                    (op.fwd_ff if ff else op.fwd)(tr, blk["a"].data_ptr(), blk["qkv_out"].data_ptr())
+                elif name == "proj":
+                    (op.fwd_ff if ff else op.fwd)(tr, blk["qkv_out"].data_ptr() + 8 * d,
+                                                  blk["o"].data_ptr())
+                elif name == "ln2":
+                    (op.fwd_ff if ff else op.fwd)(tr, blk["h"].data_ptr(), blk["c"].data_ptr(),
+                                                  blk["mu2"].data_ptr(), blk["rs2"].data_ptr())
+                elif name == "fc1":
+                    (op.fwd_ff if ff else op.fwd)(tr, blk["c"].data_ptr(), blk["g"].data_ptr(),
+                                                  blk["u"].data_ptr())
+                else:
+                    (op.fwd_ff if ff else op.fwd)(tr, blk["g"].data_ptr(), blk["w"].data_ptr())
+                tr._t1(cls, tr.stream)
+                if ff:
+                    op.updated = True
+                if name == "proj":
+                    L.of_add(xin, blk["o"].data_ptr(), n, blk["h"].data_ptr(), tr._s())
+            L.of_add(blk["h"].data_ptr(), blk["w"].data_ptr(), n, blk["y"].data_ptr(), tr._s())
+            xin = blk["y"].data_ptr()
+
+    def _block_in(self, k, x):
+        return x.data_ptr() if k == 0 else self.blocks[k - 1]["y"].data_ptr()
+
+    def _gx_of(self, k):
+        return self.gx.data_ptr() if k == 0 else self.blocks[k - 1]["gy"].data_ptr()
+
+    def _linear_bwd(self, op, dz, x, prev, act_prev, dx, fused, done):
+        tr = self.tr
+        if not fused:
+            tr._t0("dgrad", tr.stream, op)
+            op.dgrad(tr, dz, prev, act_prev, dx)
+            tr._t1("dgrad", tr.stream)
+            tr._t0("wgrad", tr.stream, op)
+            op.wgrad(tr, dz, x)
+            tr._t1("wgrad", tr.stream)
+        elif tr.timer is not None and tr.timer.wants("wgrad_bf"):
+            tr._t0("dgrad", tr.stream, op)
+            op.dgrad(tr, dz, prev, act_prev, dx)
+            tr._t1("dgrad", tr.stream)
+            _side_after_main(tr)
+            tr._t0("wgrad_bf", tr.side, op)
+            op.wgrad_fused(tr, dz, x, tr.side.cuda_stream)
+            tr._t1("wgrad_bf", tr.side)
+            done(op)
+        else:
+            op.bwd_fused(tr, dz, x, prev, act_prev, dx)
+            done(op)
+
+    def _ln_bwd(self, op, dy, x, mu, rs, dres, dx, fused, done):
+        tr = self.tr
+        op.bwd(tr, dy, x, mu, rs, dres, dx)
+        if fused:
+            # the row partials are complete: update gamma and beta on the side stream
+            _side_after_main(tr)
+            for p in op.params:
+                _update(tr, p, tr.side.cuda_stream)
+            done(op)
+        elif tr.eager_reduce:
+            op.reduce(tr)
+
+    def _backward(self, x, fused, done):
+        d = self.d
+        for k in reversed(range(len(self.blocks))):
+            blk = self.blocks[k]
+            P = {n: blk[n].data_ptr() for n in blk if isinstance(blk[n], torch.Tensor)}
+            self._linear_bwd(blk["fc2"], P["gy"], P["g"], P["u"], L.OF_ACT_GELU, P["gu"], fused,
+                             done)
+            self._linear_bwd(blk["fc1"], P["gu"], P["c"], None, L.OF_ACT_NONE, P["gc"], fused,
+                             done)
+            self._ln_bwd(blk["ln2"], P["gc"], P["h"], P["mu2"], P["rs2"], P["gy"], P["gh"], fused,
+                         done)
+            self._linear_bwd(blk["proj"], P["gh"], P["qkv_out"] + 8 * d, None, L.OF_ACT_NONE,
+                             P["gqkv"] + 8 * d, fused, done)
+            self._linear_bwd(blk["qkv"], P["gqkv"], P["a"], None, L.OF_ACT_NONE, P["ga"], fused,
+                             done)
+            self._ln_bwd(blk["ln1"], P["ga"], self._block_in(k, x), P["mu1"], P["rs1"], P["gh"],
+                         self._gx_of(k), fused, done)
+
+    def backward_plain(self, x):
+        self._backward(x, False, None)
+
+    def backward_fused(self, x, done):
+        self._backward(x, True, done)
+
+    def argmax(self):
+        return {}
+
+
+class Trainer:
+    """Trains one workload on one GPU under a chosen ordering."""
+
+    def __init__(self, cfg, init, device="cuda:0"):
+        L.load()
+        self.cfg, self.hyper = cfg, cfg["opt"]
+        self.device = torch.device(device)
+        kind = self.hyper["kind"]
+        self.params = {}
+
+        def pb(name, shadow=False, rows=0):
+            p = ParamBuf(name, init[name], kind, self.device, shadow, rows)
+            self.params[name] = p
+            return p
+
+        if cfg["kind"] in ("mlp", "vgg"):
+            if cfg["dtype"] != "f32":
+                raise NotImplementedError("linear / conv chains run with fp32 operands")
+            self.net = ChainNet(self, cfg, pb)
+        elif cfg["kind"] == "tblock":
+            self.net = TBlockNet(self, cfg, pb)
+        else:
+            raise NotImplementedError(f"model kind {cfg['kind']!r} has no GPU path in this build")
+        self.ops = self.net.ops
+        self.eager_reduce = True
+        f32 = dict(dtype=torch.float32, device=self.device)
         wsm = max([op.ws(w) for op in self.ops for w in (0, 1, 2)] + [16])
         wss = max([op.ws(2) for op in self.ops] + [16])
         if cfg["loss"] == "mse":
-            wsm = max(wsm, L.of_mse_workspace_size(*self.ops[-1].out_shape))
+            wsm = max(wsm, L.of_mse_workspace_size(*self.net.out.shape))
         self.ws_main = torch.empty((wsm + 15) // 16 * 4, **f32)
         self.ws_side = torch.empty((wss + 15) // 16 * 4, **f32)
         self.losses = torch.zeros(4096, **f32)
@@ -253,73 +595,18 @@ class Trainer:
         if self.timer is not None:
             self.timer.stop(cls, stream)
 
-    def _in(self, i, x):
-        """Device pointer of layer i's input."""
-        if i == 0:
-            return x.data_ptr()
-        return (self.p[i - 1] if self.pool[i - 1] else self.y[i - 1]).data_ptr()
-
     def _loss(self, y):
         self._t0("loss", self.stream)
-        out = self.y[-1]
+        out, gout = self.net.out, self.net.gout
         M, C = out.shape
         loss_ptr = self.losses.data_ptr() + 4 * (self.t % self.losses.numel())
         if self.cfg["loss"] == "xent":
-            L.of_xent_fwd_bwd(out.data_ptr(), y.data_ptr(), M, C, 0, loss_ptr,
-                              self.gz[-1].data_ptr(), self._s())
+            L.of_xent_fwd_bwd(out.data_ptr(), y.data_ptr(), M, C, 0, loss_ptr, gout.data_ptr(),
+                              self._s())
         else:
-            L.of_mse_fwd_bwd(out.data_ptr(), y.data_ptr(), M, C, 0, loss_ptr,
-                             self.gz[-1].data_ptr(), *self.ws_main_args(), self._s())
+            L.of_mse_fwd_bwd(out.data_ptr(), y.data_ptr(), M, C, 0, loss_ptr, gout.data_ptr(),
+                             *self.ws_main_args(), self._s())
         self._t1("loss", self.stream)
-
-    def _forward(self, x, fused):
-        for i, op in enumerate(self.ops):
-            if fused and not op.updated:
-                self._t0("fwd_ff", self.stream, op)
-                op.fwd_ff(self, self._in(i, x), self.y[i].data_ptr())
-                self._t1("fwd_ff", self.stream)
-                op.updated = True
-            else:
-                self._t0("fwd", self.stream, op)
-                op.fwd(self, self._in(i, x), self.y[i].data_ptr())
-                self._t1("fwd", self.stream)
-            if self.pool[i]:
-                N, H, W, C = op.out_shape
-                L.of_maxpool2x2_fwd(self.y[i].data_ptr(), N, H, W, C, self.p[i].data_ptr(),
-                                    self.arg[i].data_ptr(), self._s())
-
-    def _dgrad_target(self, i):
-        """Where layer i's data gradient goes: (dx, prev, act_prev).  Through a
-        max-pool the ReLU mask is applied by the pool's backward instead."""
-        if self.pool[i - 1]:
-            return self.gp[i - 1].data_ptr(), None, L.OF_ACT_NONE
-        prev_act = self.ops[i - 1].act
-        prev = self.y[i - 1].data_ptr() if prev_act != "none" else None
-        return self.gz[i - 1].data_ptr(), prev, L.ACTS[prev_act]
-
-    def _pool_bwd(self, i):
-        """After layer i's data gradient: back through layer i-1's max-pool and ReLU."""
-        if i > 0 and self.pool[i - 1]:
-            N, H, W, C = self.ops[i - 1].out_shape
-            L.of_maxpool2x2_bwd(self.gp[i - 1].data_ptr(), self.arg[i - 1].data_ptr(),
-                                self.y[i - 1].data_ptr(), N, H, W, C,
-                                self.gz[i - 1].data_ptr(), self._s())
-
-    def _dgrad(self, i, op):
-        dx, prev, act_prev = self._dgrad_target(i)
-        self._t0("dgrad", self.stream, op)
-        op.dgrad(self, self.gz[i].data_ptr(), prev, act_prev, dx)
-        self._t1("dgrad", self.stream)
-
-    def _backward_plain(self, x):
-        for i in reversed(range(len(self.ops))):
-            op = self.ops[i]
-            if i > 0:
-                self._dgrad(i, op)
-            self._t0("wgrad", self.stream, op)
-            op.wgrad(self, self.gz[i].data_ptr(), self._in(i, x))
-            self._t1("wgrad", self.stream)
-            self._pool_bwd(i)
 
     # ---------------------------------------------------------- orderings
     def step(self, x, y, ordering):
@@ -338,9 +625,10 @@ class Trainer:
         self.t += 1
 
     def _step_eager(self, x, y):
-        self._forward(x, fused=False)
+        self.net.forward(x, fused=False)
         self._loss(y)
-        self._backward_plain(x)
+        self.eager_reduce = True
+        self.net.backward_plain(x)
         ps = list(self.params.values())
         step = self._advance(ps)
         arr = (L.OfParam * len(ps))(*[p.p for p in ps])
@@ -357,9 +645,11 @@ class Trainer:
             step = self._advance(pending)
             for p in pending:
                 p.step = step
-        self._forward(x, fused=True)
+        self.net.forward(x, fused=True)
         self._loss(y)
-        self._backward_plain(x)
+        # gradients stay pending (LayerNorm's as row partials)
+        self.eager_reduce = False
+        self.net.backward_plain(x)
         for op in self.ops:
             op.updated = False
 
@@ -369,47 +659,30 @@ class Trainer:
         if pending:
             step = self._advance(pending)
             for p in pending:
-                L.of_elementwise_fused_update(p.p, p.g.data_ptr(), 1, 0, self.opt, self._s())
+                _update(self, p, self._s())
                 p.step = step
             for op in self.ops:
                 op.updated = True
         self.pending_ordering = None
 
     def _step_bf(self, x, y):
-        # The forward of layer i at this step needs its update from the last step:
-        # the previous step ended with the main stream joining the update stream.
+        # The forward of each layer at this step needs its update from the last
+        # step: the previous step ended with the main stream joining the side one.
         for op in self.ops:
             for p in op.params:
                 p.count += 1
-        self._forward(x, fused=False)
+        self.net.forward(x, fused=False)
         self._loss(y)
         step = self._advance(list(self.params.values()))
-        timed = self.timer is not None and self.timer.wants("wgrad_bf")
-        for i in reversed(range(len(self.ops))):
-            op = self.ops[i]
+
+        def done(op):
             for p in op.params:
                 p.count -= 1
-            if any(p.count != 0 for p in op.params):
-                raise NotImplementedError("shared parameters are not supported on the GPU path")
-            if op.kind == "linear" and not timed:
-                # one library call: dgrad with the old W on the main stream, then
-                # the fused update on the side stream behind an event
-                dx, prev, act_prev = self._dgrad_target(i) if i > 0 else (None, None, 0)
-                op.bwd_fused(self, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx)
-            else:
-                # the same order by hand (events can then bracket the fused kernel):
-                # dgrad on the main stream, event, fused wgrad + update on the side
-                if i > 0:
-                    self._dgrad(i, op)
-                ev = torch.cuda.Event()
-                ev.record(self.stream)
-                self.side.wait_event(ev)
-                self._t0("wgrad_bf", self.side, op)
-                op.wgrad_fused(self, self.gz[i].data_ptr(), self._in(i, x), self.side.cuda_stream)
-                self._t1("wgrad_bf", self.side)
-            self._pool_bwd(i)
-            for p in op.params:
+                if p.count != 0:
+                    raise NotImplementedError("shared parameters are not supported on the GPU path")
                 p.step = step
+
+        self.net.backward_fused(x, done)
         self.side_done.record(self.side)
         self.stream.wait_event(self.side_done)
 
@@ -465,7 +738,7 @@ class Trainer:
         update (their layers' `updated` flags become False)."""
         torch.cuda.synchronize(self.device)
         for k, p in self.params.items():
-            p.w.copy_(torch.as_tensor(np.asarray(params[k], np.float32)))
+            p.set(params[k])
             p.m.copy_(torch.as_tensor(np.asarray(m[k], np.float32)))
             if p.v is not None:
                 p.v.copy_(torch.as_tensor(np.asarray(v[k], np.float32)))
@@ -482,7 +755,7 @@ class Trainer:
             for op in self.ops:
                 if all(p.name in pending for p in op.params):
                     for p in op.params:
-                        p.g.copy_(torch.as_tensor(np.asarray(pending[p.name], np.float32)))
+                        p.set_pending(pending[p.name])
                     op.updated = False
             self.pending_ordering = "ff"
         torch.cuda.synchronize(self.device)
@@ -494,8 +767,7 @@ class Trainer:
     def argmax(self):
         """Max-pool window positions of the last forward by layer index (synchronises)."""
         torch.cuda.synchronize(self.device)
-        return {i: a.cpu().numpy().astype(np.int32) for i, a in enumerate(self.arg)
-                if a is not None}
+        return {i: a.cpu().numpy().astype(np.int32) for i, a in self.net.argmax().items()}
 
     def state(self):
         """Parameters, histories and counters as host arrays (synchronises)."""
@@ -515,7 +787,7 @@ class Trainer:
         if self.pending_ordering == "ff":
             self.flush()
         self.stream.wait_event(self.side_done)
-        self._forward(x, fused=False)
+        self.net.forward(x, fused=False)
         saved = self.t
         self._loss(y)
         torch.cuda.synchronize(self.device)

@@ -17,6 +17,7 @@ import numpy as np
 
 EPS_FACTOR = 100.0
 MAX_SENSITIVE_FRACTION = 1e-2
+MAX_UNDETERMINED_FRACTION = 0.75
 
 
 def rel(a, b):
@@ -26,8 +27,21 @@ def rel(a, b):
     return float(np.max(np.abs(a - b)) / (den if den > 0 else 1.0)) if b.size else 0.0
 
 
-def check_param(gpu, ref, hyper, steps, tol, min_sqrt_vhat=None, what=""):
-    """Assert parity of one trained parameter tensor; returns (rel error, #eps-dominated)."""
+def check_param(gpu, ref, hyper, steps, tol, min_sqrt_vhat=None, what="", ref_m=None,
+                grad_tol=None):
+    """Assert parity of one trained parameter tensor; returns (rel error, #sensitive).
+
+    ref_m, grad_tol (one Adam step, optional): the oracle's first moment and the
+    tolerance the test holds the moment itself to.  After one step Adam moves
+    an element by lr * g / (|g| + eps), about lr * sign(g).  Where the oracle's
+    |g| is within grad_tol * max|g| of zero, a run that meets the gradient
+    tolerance may hold a gradient of either sign or of a size comparable with
+    eps, and every move within Adam's bound is then a valid outcome; those
+    elements (decided by the oracle) are held to that bound, at most
+    MAX_UNDETERMINED_FRACTION of the tensor, and every other element to the
+    tolerance.  This matters for bf16 operands, whose gradients carry ~1e-3
+    relative noise.
+    """
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     den = max(float(np.max(np.abs(ref))), 1e-30)
@@ -39,13 +53,21 @@ def check_param(gpu, ref, hyper, steps, tol, min_sqrt_vhat=None, what=""):
     sens = np.asarray(min_sqrt_vhat) < EPS_FACTOR * hyper["eps"]
     frac = float(sens.mean())
     assert frac <= MAX_SENSITIVE_FRACTION, f"{what}: eps-dominated fraction {frac:.2e}"
+    if ref_m is not None and grad_tol is not None:
+        am = np.abs(np.asarray(ref_m, np.float64))
+        # exact zeros (a structurally zero gradient, e.g. the unused Q and K
+        # thirds of a fused QKV weight) are exact on both sides
+        und = (am <= grad_tol * am.max()) & (am > 0)
+        uf = float(und.mean())
+        assert uf <= MAX_UNDETERMINED_FRACTION, f"{what}: undetermined fraction {uf:.2e}"
+        sens = sens | und
     r = float(err[~sens].max() / den) if (~sens).any() else 0.0
     assert r <= tol, f"{what}: rel {r:.3e} > {tol} on well-conditioned elements"
     if sens.any():
         step_bound = hyper["lr"] * (1 - hyper["beta1"]) / np.sqrt(1 - hyper["beta2"])
         bound = 2.0 * steps * step_bound + tol * den
         worst = float(err[sens].max())
-        assert worst <= bound, f"{what}: eps-dominated element moved {worst:.3e} > {bound:.3e}"
+        assert worst <= bound, f"{what}: sensitive element moved {worst:.3e} > {bound:.3e}"
     return r, int(sens.sum())
 
 

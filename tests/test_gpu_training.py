@@ -11,6 +11,7 @@ from workloads import get_config, reduced_config, make_params, make_batch, make_
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-4
+TOL_BF16 = 2e-2   # bf16 operands, fp32 accumulation
 
 
 def _gpu_run(torch, cfg, ordering, steps, dev):
@@ -35,6 +36,7 @@ CASES = [
     ("mlp8x1024", "reduced"),
     ("linear4x8192", "reduced"),
     ("vgg11", "reduced"),
+    ("tblock12", "reduced"),
 ]
 
 
@@ -47,20 +49,24 @@ def test_training_parity(gpu, name, how):
     import torch
     cfg = _cfg(name, how)
     K = cfg["steps"]
+    tol = TOL_BF16 if cfg["dtype"] == "bf16" else TOL
     ref = oracle.run(cfg, "eager", steps=K)
     runs = {o: _gpu_run(torch, cfg, o, K, gpu) for o in ("eager", "ff", "bf")}
+    worst = 0.0
     for o, st in runs.items():
-        assert rel(st["losses"], ref["losses"]) <= TOL, (o, st["losses"], ref["losses"])
-        assert abs(st["eval_loss"] - ref["eval_loss"]) <= TOL * abs(ref["eval_loss"])
+        assert rel(st["losses"], ref["losses"]) <= tol, (o, st["losses"], ref["losses"])
+        assert abs(st["eval_loss"] - ref["eval_loss"]) <= tol * abs(ref["eval_loss"])
         for k in ref["params"]:
-            check_param(st["params"][k], ref["params"][k], cfg["opt"], K, TOL,
+            check_param(st["params"][k], ref["params"][k], cfg["opt"], K, tol,
                         ref["min_sqrt_vhat"].get(k), what=f"{o} {k}")
-            assert rel(st["m"][k], ref["m"][k]) <= TOL, (o, k)
+            assert rel(st["m"][k], ref["m"][k]) <= tol, (o, k)
+            worst = max(worst, rel(st["m"][k], ref["m"][k]))
             if cfg["opt"]["kind"] != "sgd":
-                assert rel(st["v"][k], ref["v"][k]) <= TOL, (o, k)
+                assert rel(st["v"][k], ref["v"][k]) <= tol, (o, k)
             assert st["step"][k] == ref["step"][k] == K
             assert st["count"][k] == 0
         assert all(st["updated"])
+    print(f"{name}: largest relative error of m over all tensors and orderings {worst:.2e}")
     assert not any(runs["ff"]["pending"])   # Alg. 2: every layer pending before the flush
     # The orderings only move the same updates in time: identical bits on the GPU
     # wherever they run the same contractions (forward-fusion's forward shares the
@@ -231,3 +237,45 @@ def test_vgg_full_size_first_step(gpu):
         assert st["step"][k] == ref["step"][k] == 1
         assert st["count"][k] == 0
     print("vgg11 step 1: flipped decisions per node", flips)
+
+
+@pytest.mark.timeout(400)
+def test_tblock_full_size_first_step(gpu):
+    """The 12-block bf16 Transformer stack at 4096 tokens, hidden 1024, FFN 4096:
+    the first AdamW step under each ordering against the oracle's first step
+    (bf16 tolerance; Adam's eps-dominated elements under the parity rule), and
+    backward-fusion bit for bit equal to eager."""
+    import torch
+    from paper_2104_00237_amd.trainer import Trainer
+    cfg = get_config("tblock12")
+    ref = oracle.run(cfg, "eager", steps=1)
+    init = make_params(cfg)
+    x, y = make_batch(cfg, 1)
+    out = {}
+    for o in ("eager", "ff", "bf"):
+        tr = Trainer(cfg, init, gpu)
+        tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
+        loss = tr.loss_history()
+        if o == "ff":
+            tr.flush()
+        st = tr.state()
+        out[o] = st
+        assert rel(loss, ref["losses"]) <= TOL_BF16, (o, loss, ref["losses"])
+        worst, und = 0.0, []
+        for k in ref["params"]:
+            _, n = check_param(st["params"][k], ref["params"][k], cfg["opt"], 1, TOL_BF16,
+                               ref["min_sqrt_vhat"].get(k), what=f"{o} {k}", ref_m=ref["m"][k],
+                               grad_tol=TOL_BF16)
+            und.append(n / ref["params"][k].size)
+            assert rel(st["m"][k], ref["m"][k]) <= TOL_BF16, (o, k)
+            assert rel(st["v"][k], ref["v"][k]) <= TOL_BF16, (o, k)
+            assert st["step"][k] == 1
+            worst = max(worst, rel(st["m"][k], ref["m"][k]))
+        print(f"tblock12 {o}: loss {loss[0]:.6f} (oracle {ref['losses'][0]:.6f}), "
+              f"largest relative error of m {worst:.2e}, elements held to Adam's bound: "
+              f"median {np.median(und):.1%} max {np.max(und):.1%} of a tensor")
+        del tr
+        torch.cuda.empty_cache()
+    for k in ref["params"]:
+        np.testing.assert_array_equal(out["bf"]["params"][k], out["eager"]["params"][k])
+        np.testing.assert_array_equal(out["bf"]["v"][k], out["eager"]["v"][k])

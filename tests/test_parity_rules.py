@@ -49,3 +49,33 @@ def test_sgd_has_no_exclusions():
     gpu[3] += 1e-3
     with pytest.raises(AssertionError):
         check_param(gpu, ref, dict(kind="sgd", lr=0.1), 5, 1e-4, None)
+
+
+def test_check_param_undetermined_adam_step():
+    """After one Adam step, an element whose oracle gradient is within the gradient
+    tolerance of zero may move anywhere within Adam's bound; an element with a
+    clear gradient may not, and nor may one beyond the bound."""
+    rng = np.random.default_rng(3)
+    ref = rng.standard_normal(1000) * 1e-3
+    m = rng.standard_normal(1000)
+    m[7] = 1e-4 * np.abs(m).max()            # within 2e-2 of zero
+    vh = np.full(1000, 1.0)
+    gpu = ref.copy()
+    gpu[7] += 2 * ADAM["lr"]                  # the other direction
+    r, n = check_param(gpu, ref, ADAM, 1, 2e-2, vh, ref_m=m, grad_tol=2e-2)
+    assert n >= 1
+    with pytest.raises(AssertionError):
+        check_param(gpu, ref, ADAM, 1, 2e-2, vh)
+    far = ref.copy()
+    far[7] += 10 * ADAM["lr"]                 # beyond Adam's largest move
+    with pytest.raises(AssertionError):
+        check_param(far, ref, ADAM, 1, 2e-2, vh, ref_m=m, grad_tol=2e-2)
+    big = int(np.argmax(np.abs(m)))
+    bad = ref.copy()
+    bad[big] += 2 * ADAM["lr"]
+    with pytest.raises(AssertionError):       # a clear gradient fixes the step
+        check_param(bad, ref, ADAM, 1, 2e-2, vh, ref_m=m, grad_tol=2e-2)
+    flat = np.full(1000, 1e-6)
+    flat[0] = 1.0
+    with pytest.raises(AssertionError):       # nearly everything undetermined
+        check_param(ref, ref, ADAM, 1, 2e-2, vh, ref_m=flat, grad_tol=2e-2)
