@@ -65,8 +65,10 @@ typedef enum of_act { OF_ACT_NONE = 0, OF_ACT_RELU = 1, OF_ACT_GELU = 2 } of_act
 /*
  * Optimizer policy pi (Appendix A, Alg. 1).  `step` is the 1-based index t of
  * the update being applied; the caller owns and increments it.  Bias
- * corrections 1 - beta^t are computed in float64 by every kernel that updates,
- * from the step it is given.
+ * corrections 1 - beta^t are computed in float64 (beta^t by binary
+ * exponentiation): by the library at the call when `step` is given by value,
+ * by each updating kernel from *step_dev otherwise -- the same arithmetic, so
+ * both give identical results.
  *
  *   OF_OPT_SGD    momentum (Appendix A, Eq. for pi_2) with coupled weight decay:
  *                   g' = g + wd*w;  m = momentum*m + g';  w -= lr*m

@@ -9,8 +9,9 @@
 namespace opfuse {
 
 // Optimizer hyperparameters as the kernels consume them.  The step-dependent
-// bias corrections are computed by opt_prepare() at kernel start, in float64,
-// from the step passed by value or read from device memory.
+// bias corrections are computed in float64 on the host when the step is given
+// by value, else by opt_prepare() in the kernel from the device step counter
+// (the same arithmetic, so both give the same bits).
 struct OptK {
   int kind;          // of_opt_kind
   float lr, wd, mom;
@@ -19,19 +20,39 @@ struct OptK {
   float decay;       // 1 - lr * wd  (AdamW)
   int64_t step;
   const int64_t* step_dev;
-  float step_size;   // lr / (1 - beta1^t)       (set by opt_prepare)
-  float rsqrt_bc2;   // 1 / sqrt(1 - beta2^t)    (set by opt_prepare)
+  float step_size;   // lr / (1 - beta1^t)
+  float rsqrt_bc2;   // 1 / sqrt(1 - beta2^t)
+  int prepared;      // step_size / rsqrt_bc2 already set (step given by value)
 };
 
 OptK make_optk(const of_opt& o);
 
-__device__ __forceinline__ void opt_prepare(OptK& o) {
-  if (o.kind == OF_OPT_SGD) return;
-  const int64_t t = o.step_dev ? *o.step_dev : o.step;
-  const double bc1 = 1.0 - pow((double)o.b1, (double)t);
-  const double bc2 = 1.0 - pow((double)o.b2, (double)t);
+// beta^t by binary exponentiation in float64: a fixed sequence of correctly
+// rounded multiplications, so the host and every kernel get the same value.
+__host__ __device__ inline double pow_steps(double b, int64_t t) {
+  double r = 1.0;
+  while (t > 0) {
+    if (t & 1) r *= b;
+    b *= b;
+    t >>= 1;
+  }
+  return r;
+}
+
+// The Adam bias corrections of update t, in float64, rounded once to float.
+__host__ __device__ inline void opt_constants(OptK& o, int64_t t) {
+  const double bc1 = 1.0 - pow_steps((double)o.b1, t);
+  const double bc2 = 1.0 - pow_steps((double)o.b2, t);
   o.step_size = (float)((double)o.lr / bc1);
   o.rsqrt_bc2 = (float)(1.0 / sqrt(bc2));
+}
+
+// Kernels call this before their first update: with a step given by value the
+// host has already set the constants; with a device step counter they are
+// computed here, from the step the kernel reads when it runs.
+__device__ __forceinline__ void opt_prepare(OptK& o) {
+  if (o.kind == OF_OPT_SGD || o.prepared) return;
+  opt_constants(o, *o.step_dev);
 }
 
 // The one per-element update used by every kernel that changes a parameter

@@ -43,10 +43,14 @@ namespace opfuse {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_>
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_, bool DIRECT_ = false>
 struct Tile {
   static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_, WR = WR_;
   static constexpr int NS = NS_;  // operand chunks in the register ring
+  // DIRECT: operands go from memory straight into the MFMA registers (no LDS
+  // staging); only for one 32x32 output block whose 4 waves split the reduction.
+  static constexpr bool DIRECT = DIRECT_;
+  static_assert(!DIRECT || (BP == 32 && BQ == 32 && WR == 4), "direct tiles are 32x32, 4-way split");
   static_assert(WP * WQ * WR == 4, "a workgroup is 4 wavefronts");
   static constexpr int WTP = BP / WP, WTQ = BQ / WQ;   // wavefront tile
   static constexpr int TP = WTP / 32, TQ = WTQ / 32;   // 32x32 MFMA blocks per wavefront
@@ -68,11 +72,14 @@ using T64x64 = Tile<64, 64, 16, 2, 2, 1, 6>;
 using T128x64 = Tile<128, 64, 16, 2, 2, 1, 4>;
 using T128x128 = Tile<128, 128, 16, 2, 2, 1, 3>;
 using T256x32 = Tile<256, 32, 16, 4, 1, 1, 3>;
+using T32x32D = Tile<32, 32, 32, 1, 1, 4, 8, true>;   // 8 blocks of 8 in flight per wave
 
-enum TileId { TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32, TI_COUNT };
-static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256};
-static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32};
-static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16};
+enum TileId {
+  TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32, TI_32x32D, TI_COUNT
+};
+static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256, 32};
+static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32, 32};
+static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16, 32};
 
 
 // A BX (output dim) x BR (reduction) tile of one operand, held in registers as
@@ -291,7 +298,6 @@ struct FFTileLoad {
 template <class T, int EPI, bool VEC, bool CONV>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, int r_split,
                                                    float* partial, int vec_epi) {
-  if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
   constexpr bool A_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF || EPI == EPI_DGRAD);
   constexpr bool B_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF);
   constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
@@ -359,6 +365,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     }
   }
 
+  // (after the prefetch above is in flight, so its latency hides this)
+  if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+
   // Register ring of NS operand chunks: the loads of chunk c+NS-1 are issued
   // before chunk c is stored to LDS and multiplied, so NS-1 chunks are in
   // flight per workgroup.  The loop runs to a multiple of NS; chunks past the
@@ -391,6 +400,72 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       lb[slot].load(pr.B, pr, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
   };
 
+  if constexpr (T::DIRECT) {
+    // Wave wr takes the blocks of 8 reduction elements b = wr, wr+4, wr+8, ...
+    // of this split; lane (row, h) holds elements 8b+4h .. 8b+4h+3 of its A row
+    // and its B row, and MFMA step e pairs element e of both halves (the same
+    // pairing for A and B, so every product of the block is summed once).
+    // Reduction-contiguous operands take one 128-bit load per block, the
+    // others four 32-bit loads that are coalesced across the lanes.  NS blocks
+    // are in flight per wave.
+    const int row = lane & 31, h = lane >> 5;
+    const int nr = rend - rbeg;
+    const int nblk = (nr + 7) >> 3;
+    const int myblk = nblk > wr ? (nblk - wr + 3) >> 2 : 0;
+    const rsrc_t rsa = make_rsrc(pr.A + (int64_t)p0 * pr.a_sp + (int64_t)rbeg * pr.a_sr);
+    const rsrc_t rsb = make_rsrc(pr.B + (int64_t)q0 * pr.b_sq + (int64_t)rbeg * pr.b_sr);
+    float4 ra[NS], rb[NS];
+    auto ld = [&](const rsrc_t& rs, int64_t s_x, int64_t s_r, bool rc, int x, int nx,
+                  int r) -> float4 {
+      if (rc && VEC) {
+        const bool ok = x < nx && r < nr;
+        return bload4(rs, ok ? (uint32_t)((x * s_x + r) * 4) : kOOB);
+      }
+      float e[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const bool ok = x < nx && r + k < nr;
+        e[k] = bload1(rs, ok ? (uint32_t)((x * s_x + (r + k) * s_r) * 4) : kOOB);
+      }
+      return make_float4(e[0], e[1], e[2], e[3]);
+    };
+    auto dload = [&](int slot, int i) {
+      const int r = 8 * (wr + 4 * i) + 4 * h;
+      ra[slot] = ld(rsa, pr.a_sp, pr.a_sr, A_RC, row, np, r);
+      rb[slot] = ld(rsb, pr.b_sq, pr.b_sr, B_RC, row, nq, r);
+    };
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) dload(s, s);
+    for (int i0 = 0; i0 < myblk; i0 += NS) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const int i = i0 + s;
+        dload((s + NS - 1) % NS, i + NS - 1);
+        if (i < myblk) {
+          const float av[4] = {ra[s].x, ra[s].y, ra[s].z, ra[s].w};
+          const float bv[4] = {rb[s].x, rb[s].y, rb[s].z, rb[s].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], acc[0][0], 0, 0, 0);
+          if constexpr (WG) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dbsum = __fadd_rn(dbsum, av[e]);
+          }
+        }
+      }
+    }
+    if (do_db) {
+      // Sum the 8 partial column sums of dZ (4 waves x 2 halves) in order.
+      __syncthreads();
+      smem[(wr * 2 + h) * 32 + row] = dbsum;
+      __syncthreads();
+      if (tid < 32) {
+        float s8 = smem[tid];
+        for (int k = 1; k < 8; ++k) s8 = __fadd_rn(s8, smem[k * 32 + tid]);
+        dbsum = s8;
+      }
+    }
+  } else {
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s) issue(s, s);
 
@@ -434,6 +509,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       }
     }
   }
+  }  // !DIRECT
   // Every wavefront is done with the operand buffers before they are reused.
   __syncthreads();
 
@@ -564,9 +640,15 @@ static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
   if (P <= 64 && ntiles(TI_64x64, P, Q) >= 64) return make_cfg(TI_64x64, P, Q, R, 1024, 8);
   // Larger outputs: the biggest tile that still gives one workgroup per CU; no
   // reduction split (each split costs a second kernel, ~4 us back to back).
+  // A forward or data gradient that lands on 32x32 tiles loads its operands
+  // straight into the matrix-core registers (its A operand is reduction-
+  // contiguous; measured faster there, slower for the weight gradient).
   const int order[4] = {TI_128x128, TI_128x64, TI_64x64, TI_32x32};
   for (int i = 0; i < 4; ++i)
-    if (ntiles(order[i], P, Q) >= 256) return make_cfg(order[i], P, Q, R, 256, 16);
+    if (ntiles(order[i], P, Q) >= 256) {
+      const bool direct = order[i] == TI_32x32 && (kind == EPI_FWD || kind == EPI_DGRAD);
+      return make_cfg(direct ? TI_32x32D : order[i], P, Q, R, 256, 16);
+    }
   return make_cfg(TI_32x32, P, Q, R, 1024, 64);
 }
 
@@ -627,6 +709,11 @@ static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const Epi
       if constexpr (EPI == EPI_FWD_FF) return hipErrorInvalidValue;
       else return launch_t<T128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_256x32: return launch_t<T256x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_32x32D:
+      // direct loads exist for strided operands only; the same tiling otherwise
+      if constexpr (EPI == EPI_FWD_FF) return launch_t<T32x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+      else if (pr.conv) return launch_t<T32x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+      else return launch_t<T32x32D, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
   }
   return hipErrorInvalidValue;
 }

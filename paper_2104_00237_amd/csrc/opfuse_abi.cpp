@@ -264,6 +264,11 @@ OptK make_optk(const of_opt& o) {
   k.step_dev = o.step_dev;
   k.step_size = 0.f;
   k.rsqrt_bc2 = 0.f;
+  k.prepared = 0;
+  if (o.step_dev == nullptr && o.kind != OF_OPT_SGD) {
+    opt_constants(k, o.step);
+    k.prepared = 1;
+  }
   return k;
 }
 }  // namespace opfuse

@@ -558,11 +558,14 @@ class Trainer:
         self.ws_side = torch.empty((wss + 15) // 16 * 4, **f32)
         self.losses = torch.zeros(4096, **f32)
         self.t = 0
-        # Device copy of the 1-based index of the update being applied: advanced in
-        # stream order right before each step's updates, read by the kernels when
-        # they run, so one launch sequence (or a captured graph) serves every step.
+        # The 1-based index of the update being applied travels by value in
+        # launched steps.  A captured step instead reads it from this device
+        # counter, advanced in stream order right before the step's updates, so
+        # one captured launch sequence serves every later step.
         self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
-        self.opt = L.make_opt(self.hyper, 0, self.step_dev.data_ptr())
+        self.opt_dev = L.make_opt(self.hyper, 0, self.step_dev.data_ptr())
+        self.opt = self.opt_dev
+        self.capturing = False
         self.stream = torch.cuda.current_stream(self.device)
         self.side = torch.cuda.Stream(self.device)
         self.side_done = torch.cuda.Event()
@@ -580,11 +583,16 @@ class Trainer:
         return self.stream.cuda_stream
 
     def _advance(self, ps):
-        """Next update index for parameters ps (host mirror + device counter)."""
+        """Next update index for parameters ps; sets the optimizer argument the
+        step's updating launches take (by value, or the advanced device counter)."""
         step = ps[0].step + 1
         if any(p.step + 1 != step for p in ps):
             raise RuntimeError("parameters out of step: this trainer keeps one update counter")
-        L.of_step_advance(self.step_dev.data_ptr(), 1, self._s())
+        if self.capturing:
+            L.of_step_advance(self.step_dev.data_ptr(), 1, self._s())
+            self.opt = self.opt_dev
+        else:
+            self.opt = L.make_opt(self.hyper, step)
         return step
 
     def _t0(self, cls, stream, op=None):
@@ -703,15 +711,19 @@ class Trainer:
                  [op.updated for op in self.ops], self.t, self.pending_ordering)
         g = torch.cuda.CUDAGraph()
         cap = torch.cuda.Stream(self.device)
+        # the device counter holds the index of the last applied update
+        self.step_dev.fill_(next(iter(self.params.values())).step)
         cap.wait_stream(self.stream)
         main = self.stream
         torch.cuda.synchronize(self.device)
         try:
             self.stream = cap
+            self.capturing = True
             with torch.cuda.graph(g, stream=cap):
                 self.step(x, y, ordering)
         finally:
             self.stream = main
+            self.capturing = False
         flags = [op.updated for op in self.ops]
         for p, (st, cn) in zip(self.params.values(), saved[0]):
             p.step, p.count = st, cn
