@@ -30,6 +30,8 @@
 namespace opfuse {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
 typedef float floatx16_t __attribute__((ext_vector_type(16)));
 
 template <int BP_, int BQ_, int BR_, int WP_, int WQ_>
@@ -58,9 +60,14 @@ static const int kBTileBP[BTI_COUNT] = {64, 128};
 static const int kBTileBQ[BTI_COUNT] = {64, 128};
 static const int kBTileBR[BTI_COUNT] = {32, 32};
 
+// Two fp32 values to packed bf16, round to nearest even (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t cvt2(float a, float b) {
+  const float2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
 __device__ __forceinline__ uint2 pack_bf16x4(float a, float b, float c, float d) {
-  return make_uint2((uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16),
-                    (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16));
+  return make_uint2(cvt2(a, b), cvt2(c, d));
 }
 
 __device__ __forceinline__ uint2 bload8(rsrc_t r, uint32_t off) {
@@ -128,15 +135,13 @@ struct BLoad {
     }
   }
 
-  // Element k (0..3) of vector j of item i, as bf16 bits.
+  // Element k (0..3) of vector j of item i: bf16 bits, or the fp32 value.
   __device__ __forceinline__ uint32_t bits(int i, int j, int k) const {
-    if constexpr (BF) {
-      const uint32_t w = (k < 2) ? h[i][j].x : h[i][j].y;
-      return (k & 1) ? (w >> 16) : (w & 0xffffu);
-    } else {
-      const float v = k == 0 ? f[i][j].x : k == 1 ? f[i][j].y : k == 2 ? f[i][j].z : f[i][j].w;
-      return f32_to_bf16(v);
-    }
+    const uint32_t w = (k < 2) ? h[i][j].x : h[i][j].y;
+    return (k & 1) ? (w >> 16) : (w & 0xffffu);
+  }
+  __device__ __forceinline__ float val(int i, int j, int k) const {
+    return k == 0 ? f[i][j].x : k == 1 ? f[i][j].y : k == 2 ? f[i][j].z : f[i][j].w;
   }
 
   __device__ __forceinline__ void store(uint16_t* lds, int tid) const {
@@ -156,8 +161,12 @@ struct BLoad {
         // transpose the 4 x 4 block: row x+k gets elements k of vectors 0..3
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const uint2 q = make_uint2(bits(i, 0, k) | (bits(i, 1, k) << 16),
-                                     bits(i, 2, k) | (bits(i, 3, k) << 16));
+          uint2 q;
+          if constexpr (BF)
+            q = make_uint2(bits(i, 0, k) | (bits(i, 1, k) << 16),
+                           bits(i, 2, k) | (bits(i, 3, k) << 16));
+          else
+            q = pack_bf16x4(val(i, 0, k), val(i, 1, k), val(i, 2, k), val(i, 3, k));
           *reinterpret_cast<uint2*>(&lds[plane * PL + (x + k) * 8 + slot]) = q;
         }
       }
