@@ -88,8 +88,16 @@ __global__ __launch_bounds__(256) void rows_update_kernel(of_param p, const floa
   opt_prepare(o);
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= p.numel) return;
+  // loads of 8 rows are issued before their (in-order) accumulation
   float s = g[i];
-  for (int64_t r = 1; r < rows; ++r) s = __fadd_rn(s, g[r * ld + i]);
+  for (int64_t r0 = 1; r0 < rows; r0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = r0 + k < rows ? g[(r0 + k) * ld + i] : 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (r0 + k < rows) s = __fadd_rn(s, v[k]);
+  }
   update1(o, p, s, i);
 }
 

@@ -452,8 +452,12 @@ class TBlockNet:
                 if ff:
                     op.updated = True
                 if name == "proj":
+                    tr._t0("add", tr.stream)
                     L.of_add(xin, blk["o"].data_ptr(), n, blk["h"].data_ptr(), tr._s())
+                    tr._t1("add", tr.stream)
+            tr._t0("add", tr.stream)
             L.of_add(blk["h"].data_ptr(), blk["w"].data_ptr(), n, blk["y"].data_ptr(), tr._s())
+            tr._t1("add", tr.stream)
             xin = blk["y"].data_ptr()
 
     def _block_in(self, k, x):
@@ -486,7 +490,9 @@ class TBlockNet:
 
     def _ln_bwd(self, op, dy, x, mu, rs, dres, dx, fused, done):
         tr = self.tr
+        tr._t0("ln_bwd", tr.stream, op)
         op.bwd(tr, dy, x, mu, rs, dres, dx)
+        tr._t1("ln_bwd", tr.stream)
         if fused:
             # the row partials are complete: update gamma and beta on the side stream
             _side_after_main(tr)
