@@ -34,9 +34,10 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float float2_t __attribute__((ext_vector_type(2)));
 typedef float floatx16_t __attribute__((ext_vector_type(16)));
 
-template <int BP_, int BQ_, int BR_, int WP_, int WQ_>
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int NS_>
 struct BTile {
   static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_;
+  static constexpr int NS = NS_;   // operand chunks in the register ring
   static_assert(WP * WQ == 4, "a workgroup is 4 wavefronts");
   static_assert(BR % 16 == 0, "whole MFMA reduction steps");
   static constexpr int WTP = BP / WP, WTQ = BQ / WQ;
@@ -52,8 +53,8 @@ struct BTile {
   static_assert(SMX <= 64 * 1024, "LDS per workgroup");
 };
 
-using BT128x128 = BTile<128, 128, 32, 2, 2>;
-using BT64x64 = BTile<64, 64, 32, 2, 2>;
+using BT128x128 = BTile<128, 128, 32, 2, 2, 2>;
+using BT64x64 = BTile<64, 64, 32, 2, 2, 3>;
 
 enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_COUNT };
 static const int kBTileBP[BTI_COUNT] = {64, 128};
@@ -203,17 +204,20 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wp = wave % T::WP, wq = wave / T::WP;
-  const int p0 = blockIdx.x * T::BP, q0 = blockIdx.y * T::BQ;
+  int tx, ty;
+  xcd_tile(tx, ty);
+  const int p0 = tx * T::BP, q0 = ty * T::BQ;
   const int split = blockIdx.z, S = gridDim.z;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
-  const bool do_db = WG && ea.with_db && blockIdx.y == 0;
+  const bool do_db = WG && ea.with_db && ty == 0;
 
   using LA = BLoad<T::BP, T::BR, A_RC, false, VA>;
   using LB = BLoad<T::BQ, T::BR, B_RC, BBF, VB>;
-  LA la;
-  LB lb;
+  constexpr int NS = T::NS;
+  LA la[NS];
+  LB lb[NS];
   float dbs[LA::PER][4];
 #pragma unroll
   for (int i = 0; i < LA::PER; ++i) dbs[i][0] = dbs[i][1] = dbs[i][2] = dbs[i][3] = 0.f;
@@ -227,22 +231,32 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
       for (int k = 0; k < 16; ++k) acc[i][j][k] = 0.f;
 
   const int np = pr.P - p0, nq = pr.Q - q0;
-  auto issue = [&](int c) {
+  // Register ring of NS chunks: chunk c+NS-1 is requested before chunk c is
+  // staged and multiplied; chunks past the end load nothing (every offset is
+  // out of range) and are skipped.
+  auto issue = [&](int slot, int c) {
     const int r0 = rbeg + c * T::BR;
     const int nr = c < nch ? rend - r0 : 0;
-    la.load(pr.A, pr.a_sp, pr.a_sr, p0, r0, np, nr, tid);
-    lb.load(pr.B, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
+    la[slot].load(pr.A, pr.a_sp, pr.a_sr, p0, r0, np, nr, tid);
+    lb[slot].load(pr.B, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
   };
 
   constexpr int SA = (T::BR / 8) * T::PLA;   // A part of a stage
-  issue(0);
-  for (int c = 0; c < nch; ++c) {
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s) issue(s, s);
+  for (int c0 = 0; c0 < nch; c0 += NS) {
+#pragma unroll
+   for (int s = 0; s < NS; ++s) {
+    const int c = c0 + s;
+    issue((s + NS - 1) % NS, c + NS - 1);
     uint16_t* buf = smem + (c & 1) * T::STAGE;
-    la.store(buf, tid);
-    lb.store(buf + SA, tid);
-    if (do_db) la.colsum(dbs);
-    issue(c + 1);
+    if (c < nch) {
+      la[s].store(buf, tid);
+      lb[s].store(buf + SA, tid);
+      if (do_db) la[s].colsum(dbs);
+    }
     __syncthreads();
+    if (c >= nch) continue;
     const uint16_t* a_s = buf;
     const uint16_t* b_s = buf + SA;
 #pragma unroll
@@ -263,6 +277,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
         for (int j = 0; j < T::TQ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+   }
   }
   __syncthreads();
 

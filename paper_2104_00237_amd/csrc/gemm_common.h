@@ -27,6 +27,35 @@ __device__ __forceinline__ float bload1(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 
+// ------------------------------------------------------------ tile order
+// Workgroups are dispatched to the 8 XCDs (each with its own L2) round-robin
+// by linear workgroup index.  Tiles are renumbered so that each XCD owns one
+// rectangular block of the output (the 8 blocks tile the grid), so an XCD's L2
+// fetches only the operand rows and columns of its block instead of nearly
+// all of both operands.  Grids whose tile counts do not factor that way keep
+// the plain order.  Every tile is still computed exactly once.
+__device__ __forceinline__ void xcd_tile(int& tx, int& ty) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  tx = blockIdx.x;
+  ty = blockIdx.y;
+  if ((gx * gy) % 8 != 0) return;
+  // 8 = sx * sy blocks with sx | gx and sy | gy; prefer the squarest blocks
+  int sx = 0, best = 1 << 30;
+  for (int c = 1; c <= 8; c *= 2) {
+    const int r = 8 / c;
+    if (gx % c || gy % r) continue;
+    const int bw = gx / c, bh = gy / r;
+    const int score = bw > bh ? bw - bh : bh - bw;
+    if (score < best) { best = score; sx = c; }
+  }
+  if (sx == 0) return;
+  const int sy = 8 / sx, bw = gx / sx, bh = gy / sy;
+  const int lin = blockIdx.x + gx * blockIdx.y;
+  const int xcd = lin & 7, j = lin >> 3;            // j < bw * bh
+  tx = (xcd % sx) * bw + j % bw;
+  ty = (xcd / sx) * bh + j / bw;
+}
+
 // ----------------------------------------------------------------- epilogues
 // c[0..n) are the results for (p, q..q+n-1).  vec: 128-bit memory paths allowed
 // (bit 0: out/z/prev, bit 1: parameter arrays); only used when n == 4.

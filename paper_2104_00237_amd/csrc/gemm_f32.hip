@@ -308,12 +308,14 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wp = wave % T::WP, wq = (wave / T::WP) % T::WQ, wr = wave / (T::WP * T::WQ);
-  const int p0 = blockIdx.x * T::BP, q0 = blockIdx.y * T::BQ;
+  int tx, ty;
+  xcd_tile(tx, ty);
+  const int p0 = tx * T::BP, q0 = ty * T::BQ;
   const int split = blockIdx.z, S = gridDim.z;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
-  const bool do_db = WG && ea.with_db && blockIdx.y == 0;
+  const bool do_db = WG && ea.with_db && ty == 0;
 
   // Buffer b (0/1) of the A and B tiles: A at b*STAGE, B at b*STAGE + BR*LDA.
   constexpr int STAGE = T::BR * (T::LDA + T::LDB);
