@@ -71,6 +71,12 @@ __device__ __forceinline__ uint2 pack_bf16x4(float a, float b, float c, float d)
   return make_uint2(cvt2(a, b), cvt2(c, d));
 }
 
+// Row of a plane that tile row x is stored in: the low two bits are XORed
+// with bits 4-5, so the four 8-byte stores of a transposed 4x4 item (rows
+// 4l+k of lane l) spread over all bank groups instead of every 4th lane
+// colliding; the rows a wave reads for one MFMA stay one contiguous block.
+__device__ __forceinline__ int swz(int x) { return x ^ ((x >> 4) & 3); }
+
 __device__ __forceinline__ uint2 bload8(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
@@ -157,7 +163,7 @@ struct BLoad {
         uint2 q;
         if constexpr (BF) q = h[i][0];
         else q = pack_bf16x4(f[i][0].x, f[i][0].y, f[i][0].z, f[i][0].w);
-        *reinterpret_cast<uint2*>(&lds[plane * PL + x * 8 + slot]) = q;
+        *reinterpret_cast<uint2*>(&lds[plane * PL + swz(x) * 8 + slot]) = q;
       } else {
         // transpose the 4 x 4 block: row x+k gets elements k of vectors 0..3
 #pragma unroll
@@ -168,7 +174,7 @@ struct BLoad {
                            bits(i, 2, k) | (bits(i, 3, k) << 16));
           else
             q = pack_bf16x4(val(i, 0, k), val(i, 1, k), val(i, 2, k), val(i, 3, k));
-          *reinterpret_cast<uint2*>(&lds[plane * PL + (x + k) * 8 + slot]) = q;
+          *reinterpret_cast<uint2*>(&lds[plane * PL + swz(x + k) * 8 + slot]) = q;
         }
       }
     }
@@ -266,11 +272,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
 #pragma unroll
       for (int i = 0; i < T::TP; ++i)
         a[i] = *reinterpret_cast<const bf16x8_t*>(
-            &a_s[plane * T::PLA + (wp * T::WTP + i * 32 + (lane & 31)) * 8]);
+            &a_s[plane * T::PLA + swz(wp * T::WTP + i * 32 + (lane & 31)) * 8]);
 #pragma unroll
       for (int j = 0; j < T::TQ; ++j)
         b[j] = *reinterpret_cast<const bf16x8_t*>(
-            &b_s[plane * T::PLB + (wq * T::WTQ + j * 32 + (lane & 31)) * 8]);
+            &b_s[plane * T::PLB + swz(wq * T::WTQ + j * 32 + (lane & 31)) * 8]);
 #pragma unroll
       for (int i = 0; i < T::TP; ++i)
 #pragma unroll
