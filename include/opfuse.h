@@ -174,8 +174,9 @@ of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param*
  * with `opt`, writes back W, m, v (and w_bf16), and Y = act(X W'^T + b') is
  * computed from the updated values.  Each element is updated exactly once.
  * The update is applied while the W tiles are loaded for the contraction when
- * M fits one row tile of the forward (M <= 256); for larger M the same update
- * runs as a separate pass just before the contraction, with identical results.
+ * M fits one row tile of the forward (fp32 operands, M <= 64); for larger M,
+ * and for bf16 operands, the same update runs as a separate pass just before
+ * the contraction, with identical results.
  * opt == NULL means nothing is pending (the first iteration): identical to
  * of_linear_fwd.  b/gb: both NULL when !has_bias.  Workspace: OF_LINEAR_FWD.
  */

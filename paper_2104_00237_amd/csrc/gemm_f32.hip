@@ -707,7 +707,7 @@ static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const Epi
     case TI_64x64: return launch_t<T64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_128x64: return launch_t<T128x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_128x128:
-      // Never chosen for a forward with M <= 256, the only forward-fusion case.
+      // Never chosen for a forward with M <= 64, the only forward-fusion case.
       if constexpr (EPI == EPI_FWD_FF) return hipErrorInvalidValue;
       else return launch_t<T128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_256x32: return launch_t<T256x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);

@@ -303,6 +303,9 @@ of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param*
   return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream);
 }
 
+// Largest M whose forward-fusion applies the update in the W-tile prologue.
+constexpr int64_t kFusedForwardMaxRows = 64;
+
 of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_param* W,
                               const float* gW, const of_param* b, const float* gb,
                               const of_opt* opt, float* z, float* y, void* ws, size_t ws_bytes,
@@ -323,9 +326,11 @@ of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_
   if ((st = check_ws(d, EPI_FWD_FF, ws, ws_bytes)) != OF_OK) return st;
   const hipStream_t s = (hipStream_t)stream;
   const OptK ok = make_optk(*opt);
-  if (d->M > 256 || d->dtype == OF_BF16) {
-    // The forward's row tiles cannot cover M (several workgroups read each W
-    // tile), or the operands are bf16 (whose kernel has no update prologue):
+  if (d->M > kFusedForwardMaxRows || d->dtype == OF_BF16) {
+    // One row tile per W element needs M rows per workgroup; beyond
+    // kFusedForwardMaxRows that tiling only fills the GPU with a reduction
+    // split whose partials and second pass cost more than a separate update
+    // pass (measured on MI355X), and bf16 operands have no update prologue:
     // the identical update runs as one pass right before the contraction.
     of_param ps[2] = {*W, d->has_bias ? *b : of_param{}};
     const float* gs[2] = {gW, gb};
