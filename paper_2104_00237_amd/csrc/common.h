@@ -196,7 +196,7 @@ struct EpiArgs {
   OptK opt;
 };
 
-size_t gemm_workspace_bytes(int kind, int P, int Q, int R);
+size_t gemm_workspace_bytes(int kind, int P, int Q, int R, int conv = 0);
 hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                        hipStream_t stream);
 // bf16-operand contractions (operands rounded to bf16, fp32 accumulation);

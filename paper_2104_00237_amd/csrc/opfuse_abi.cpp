@@ -233,7 +233,7 @@ GemmProblem conv_problem(const of_conv_desc* d, int kind, const float* a, const 
 
 size_t conv_ws(const of_conv_desc* d, int kind) {
   const GemmProblem pr = conv_problem(d, kind, nullptr, nullptr);
-  return gemm_workspace_bytes(kind, pr.P, pr.Q, pr.R);
+  return gemm_workspace_bytes(kind, pr.P, pr.Q, pr.R, 1);
 }
 
 of_status check_conv_ws(const of_conv_desc* d, int kind, const void* ws, size_t ws_bytes) {

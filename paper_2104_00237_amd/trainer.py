@@ -230,10 +230,12 @@ class LayerNormOp:
 
 
 def _side_after_main(tr):
-    """Order the side stream after everything enqueued so far on the main stream."""
-    ev = torch.cuda.Event()
+    """Order the side stream after everything enqueued so far on the main stream;
+    returns the event it waits for."""
+    ev = torch.cuda.Event(enable_timing=tr.timer is not None)
     ev.record(tr.stream)
     tr.side.wait_event(ev)
+    return ev
 
 
 class ChainNet:
@@ -356,8 +358,8 @@ class ChainNet:
                 # dgrad on the main stream, event, fused wgrad + update on the side
                 if i > 0:
                     self._dgrad(i, op)
-                _side_after_main(tr)
-                tr._t0("wgrad_bf", tr.side, op)
+                gate = _side_after_main(tr)
+                tr._t0_after("wgrad_bf", tr.side, op, gate)
                 op.wgrad_fused(tr, self.gz[i].data_ptr(), self._in(i, x), tr.side.cuda_stream)
                 tr._t1("wgrad_bf", tr.side)
             self._pool_bwd(i)
@@ -479,8 +481,8 @@ class TBlockNet:
             tr._t0("dgrad", tr.stream, op)
             op.dgrad(tr, dz, prev, act_prev, dx)
             tr._t1("dgrad", tr.stream)
-            _side_after_main(tr)
-            tr._t0("wgrad_bf", tr.side, op)
+            gate = _side_after_main(tr)
+            tr._t0_after("wgrad_bf", tr.side, op, gate)
             op.wgrad_fused(tr, dz, x, tr.side.cuda_stream)
             tr._t1("wgrad_bf", tr.side)
             done(op)
@@ -604,6 +606,10 @@ class Trainer:
     def _t0(self, cls, stream, op=None):
         if self.timer is not None:
             self.timer.start(cls, stream, op)
+
+    def _t0_after(self, cls, stream, op, gate):
+        if self.timer is not None:
+            self.timer.start_after(cls, stream, op, gate)
 
     def _t1(self, cls, stream):
         if self.timer is not None:
@@ -813,7 +819,13 @@ class Trainer:
 
 
 class KernelTimer:
-    """HIP events around chosen launch classes, recorded on the launch's stream."""
+    """HIP events around chosen launch classes, recorded on the launch's stream.
+
+    A launch on a stream that first waits for another stream's event is timed
+    from the later of that event and a start event recorded on its own stream:
+    an event recorded on a stream that is idle when the wait is enqueued can
+    take its timestamp before the wait is satisfied, which would add the wait
+    to the kernel's time."""
 
     def __init__(self, classes):
         self.classes = set(classes)
@@ -829,6 +841,13 @@ class KernelTimer:
             e.record(stream)
             self._open[cls] = (e, op)
 
+    def start_after(self, cls, stream, op, gate):
+        """Start a launch on `stream` that waits for `gate` (a timing event)."""
+        if cls in self.classes:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            self._open[cls] = ((gate, e), op)
+
     def stop(self, cls, stream):
         if cls in self.classes:
             e0, op = self._open.pop(cls)
@@ -842,7 +861,14 @@ class KernelTimer:
     def durations(self, cls):
         """[(milliseconds, op)] of every recorded launch of `cls` (synchronises)."""
         torch.cuda.synchronize()
-        return [(e0.elapsed_time(e1), op) for e0, e1, op in self.records[cls]]
+        out = []
+        for e0, e1, op in self.records[cls]:
+            if isinstance(e0, tuple):
+                gate, start = e0
+                out.append((min(gate.elapsed_time(e1), start.elapsed_time(e1)), op))
+            else:
+                out.append((e0.elapsed_time(e1), op))
+        return out
 
     @staticmethod
     def marker_overhead_ms(stream, samples=50):
