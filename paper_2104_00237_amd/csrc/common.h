@@ -168,6 +168,26 @@ enum EpiKind {
 //   forward  C[m, co]   = sum_k X~(m, k) W[co, k]     m=(n,h,w), k=(r,s,c)
 //   dgrad    C[m, c]    = sum_k dY~(m, k) W~(c, k)    k=(r,s,co): dY at (h+1-r, w+1-s)
 //   wgrad    C[co, k]   = sum_m dY[m, co] X~(k, m)
+// Division by a fixed divisor d as a multiply-high and a shift (the
+// round-up method of Granlund and Montgomery): for 0 <= n < 2^31,
+// n / d == (umulhi(n, m) + n) >> s with s = ceil(log2 d) and
+// m = floor(2^32 (2^s - d) / d) + 1.  Set on the host by make_fastdiv().
+struct FastDiv {
+  uint32_t d, m, s;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t s = 0;
+  while ((1ull << s) < d) ++s;
+  const uint64_t m = ((1ull << 32) * ((1ull << s) - d)) / d + 1;
+  return FastDiv{d, (uint32_t)m, s};
+}
+
+__device__ __forceinline__ int fdiv(int n, const FastDiv& f) {
+  const uint32_t t = __umulhi((uint32_t)n, f.m);
+  return (int)((t + (uint32_t)n) >> f.s);
+}
+
 struct GemmProblem {
   const float* A; int64_t a_sp, a_sr;
   const float* B; int64_t b_sq, b_sr;
@@ -175,6 +195,7 @@ struct GemmProblem {
   int conv;                     // 0: strided operands; 1: convolution gathers
   int cN, cH, cW, cC, cCout;    // convolution geometry (input N, H, W, C; Cout)
   int a_bf16, b_bf16;           // bf16 kernels: the operand is stored as bf16 (else fp32)
+  FastDiv dW, dH, dC, dCout;    // convolution: divisors of the gather index arithmetic
 };
 
 struct EpiArgs {

@@ -152,20 +152,40 @@ __device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& 
     const int n = min(4, Q - q);
     float c[4] = {0.f, 0.f, 0.f, 0.f};
     const float* src = partial + (int64_t)p * Q + q;
+    // The loads of 8 splits are issued before they are added in split order,
+    // so a long split list is not one dependent chain of loads.
     if (n == 4 && (Q & 3) == 0) {
       float4 s = ld4(src);
-      for (int k = 1; k < S; ++k) {
-        const float4 t = ld4(src + k * PQ);
-        s.x = __fadd_rn(s.x, t.x); s.y = __fadd_rn(s.y, t.y);
-        s.z = __fadd_rn(s.z, t.z); s.w = __fadd_rn(s.w, t.w);
+      for (int k0 = 1; k0 < S; k0 += 8) {
+        float4 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          t[u] = k0 + u < S ? ld4(src + (int64_t)(k0 + u) * PQ) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (k0 + u < S) {
+            s.x = __fadd_rn(s.x, t[u].x); s.y = __fadd_rn(s.y, t[u].y);
+            s.z = __fadd_rn(s.z, t[u].z); s.w = __fadd_rn(s.w, t[u].w);
+          }
+        }
       }
       c[0] = s.x; c[1] = s.y; c[2] = s.z; c[3] = s.w;
     } else {
-      for (int e = 0; e < n; ++e) {
-        float s = src[e];
-        for (int k = 1; k < S; ++k) s = __fadd_rn(s, src[k * PQ + e]);
-        c[e] = s;
+      float s4[4];
+      for (int e = 0; e < n; ++e) s4[e] = src[e];
+      for (int k0 = 1; k0 < S; k0 += 8) {
+        float t[8][4];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            t[u][e] = (k0 + u < S && e < n) ? src[(int64_t)(k0 + u) * PQ + e] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (k0 + u < S)
+            for (int e = 0; e < n; ++e) s4[e] = __fadd_rn(s4[e], t[u][e]);
       }
+      for (int e = 0; e < n; ++e) c[e] = s4[e];
     }
     const float* bias = nullptr;
     if ((EPI == EPI_FWD || EPI == EPI_FWD_FF) && ea.bias) bias = ea.bias + q;
@@ -175,7 +195,14 @@ __device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& 
     const float* dbp = partial + (int64_t)S * PQ;
     for (int p = blockIdx.x * 256 + threadIdx.x; p < P; p += gridDim.x * 256) {
       float s = dbp[p];
-      for (int k = 1; k < S; ++k) s = __fadd_rn(s, dbp[(int64_t)k * P + p]);
+      for (int k0 = 1; k0 < S; k0 += 8) {
+        float t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t[u] = k0 + u < S ? dbp[(int64_t)(k0 + u) * P + p] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (k0 + u < S) s = __fadd_rn(s, t[u]);
+      }
       bias_epilogue<EPI>(ea, p, s);
     }
   }

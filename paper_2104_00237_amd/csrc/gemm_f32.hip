@@ -155,14 +155,17 @@ __device__ __forceinline__ int64_t gather_off(const GemmProblem& g, int x, int r
   // FWD_A: x = m, r = k = (tap, c).  DGRAD_A: x = m, r = k = (tap, co).
   // WGRAD_B: x = k = (tap, c), r = m.  DGRAD_B: x = c, r = k = (tap, co).
   if constexpr (KIND == G_DGRAD_B) {
-    const int co = r % g.cCout, tap = r / g.cCout;
+    const int tap = fdiv(r, g.dCout), co = r - tap * g.cCout;
     return ((int64_t)co * 9 + tap) * g.cC + x;
   } else {
     const int m = (KIND == G_WGRAD_B) ? r : x;
     const int k = (KIND == G_WGRAD_B) ? x : r;
     const int ch = (KIND == G_DGRAD_A) ? g.cCout : g.cC;
-    const int w = m % g.cW, t = m / g.cW, h = t % g.cH, n = t / g.cH;
-    const int c = k % ch, tap = k / ch, rr = tap / 3, ss = tap % 3;
+    const FastDiv& fch = (KIND == G_DGRAD_A) ? g.dCout : g.dC;
+    const int t = fdiv(m, g.dW), w = m - t * g.cW;
+    const int n = fdiv(t, g.dH), h = t - n * g.cH;
+    const int tap = fdiv(k, fch), c = k - tap * ch;
+    const int rr = tap / 3, ss = tap - 3 * rr;
     const int hi = (KIND == G_DGRAD_A) ? h + 1 - rr : h + rr - 1;
     const int wi = (KIND == G_DGRAD_A) ? w + 1 - ss : w + ss - 1;
     ok = ok && hi >= 0 && hi < g.cH && wi >= 0 && wi < g.cW;
@@ -295,9 +298,11 @@ struct FFTileLoad {
 };
 
 // -------------------------------------------------------------------- kernel
-template <class T, int EPI, bool VEC, bool CONV>
+// VECS: bit 0 -- 128-bit loads of A allowed, bit 1 -- of B.
+template <class T, int EPI, int VECS, bool CONV>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, int r_split,
                                                    float* partial, int vec_epi) {
+  constexpr bool VA = (VECS & 1) != 0, VB = (VECS & 2) != 0;
   constexpr bool A_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF || EPI == EPI_DGRAD);
   constexpr bool B_RC = (EPI == EPI_FWD || EPI == EPI_FWD_FF);
   constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
@@ -378,15 +383,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   constexpr int NS = (EPI == EPI_FWD_FF) ? 2 : T::NS;
   using ALoad = std::conditional_t<
       CONV && (EPI == EPI_FWD || EPI == EPI_DGRAD),
-      GatherLoad<T::BP, T::BR, true, VEC, EPI == EPI_FWD ? G_FWD_A : G_DGRAD_A>,
-      TileLoad<T::BP, T::BR, A_RC, VEC>>;
+      GatherLoad<T::BP, T::BR, true, VA, EPI == EPI_FWD ? G_FWD_A : G_DGRAD_A>,
+      TileLoad<T::BP, T::BR, A_RC, VA>>;
   using BLoad = std::conditional_t<
-      CONV && EPI == EPI_DGRAD, GatherLoad<T::BQ, T::BR, false, VEC, G_DGRAD_B>,
-      std::conditional_t<CONV && WG, GatherLoad<T::BQ, T::BR, false, VEC, G_WGRAD_B>,
-                         TileLoad<T::BQ, T::BR, B_RC, VEC>>>;
+      CONV && EPI == EPI_DGRAD, GatherLoad<T::BQ, T::BR, false, VB, G_DGRAD_B>,
+      std::conditional_t<CONV && WG, GatherLoad<T::BQ, T::BR, false, VB, G_WGRAD_B>,
+                         TileLoad<T::BQ, T::BR, B_RC, VB>>>;
   ALoad la[NS];
   BLoad lb[(EPI == EPI_FWD_FF) ? 1 : NS];
-  FFTileLoad<T::BQ, T::BR, VEC> lf[(EPI == EPI_FWD_FF) ? NS : 1];
+  FFTileLoad<T::BQ, T::BR, VB> lf[(EPI == EPI_FWD_FF) ? NS : 1];
   const int64_t ldw = pr.b_sq;  // FF: W row stride (= K)
   const int np = pr.P - p0, nq = pr.Q - q0;
 
@@ -417,9 +422,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     const rsrc_t rsa = make_rsrc(pr.A + (int64_t)p0 * pr.a_sp + (int64_t)rbeg * pr.a_sr);
     const rsrc_t rsb = make_rsrc(pr.B + (int64_t)q0 * pr.b_sq + (int64_t)rbeg * pr.b_sr);
     float4 ra[NS], rb[NS];
-    auto ld = [&](const rsrc_t& rs, int64_t s_x, int64_t s_r, bool rc, int x, int nx,
+    auto ld = [&](const rsrc_t& rs, int64_t s_x, int64_t s_r, bool rc, bool vec, int x, int nx,
                   int r) -> float4 {
-      if (rc && VEC) {
+      if (rc && vec) {
         const bool ok = x < nx && r < nr;
         return bload4(rs, ok ? (uint32_t)((x * s_x + r) * 4) : kOOB);
       }
@@ -433,8 +438,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     };
     auto dload = [&](int slot, int i) {
       const int r = 8 * (wr + 4 * i) + 4 * h;
-      ra[slot] = ld(rsa, pr.a_sp, pr.a_sr, A_RC, row, np, r);
-      rb[slot] = ld(rsb, pr.b_sq, pr.b_sr, B_RC, row, nq, r);
+      ra[slot] = ld(rsa, pr.a_sp, pr.a_sr, A_RC, VA, row, np, r);
+      rb[slot] = ld(rsb, pr.b_sq, pr.b_sr, B_RC, VB, row, nq, r);
     };
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s) dload(s, s);
@@ -655,16 +660,16 @@ static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
 }
 
 // Convolutions: the tile and reduction split that minimise a cost model fitted
-// to measured implicit-GEMM times on MI355X (the VGG-11 layer shapes, within 4%
+// to measured implicit-GEMM times on MI355X (the VGG-11 layer shapes, within 2%
 // of the best measured choice in total).  A workgroup alone runs its tile at
 // kEff of a CU's fp32 matrix rate; kConc workgroups share a CU; a split adds a
 // second pass (fixed cost plus reading and writing the partials).  The rule
 // depends on (P, Q, R) only, so the eager and backward-fusion weight gradients
 // still share their tiling.
 static GemmCfg select_cfg_conv(int P, int Q, int R) {
-  static const double kEff[6] = {0.38, 0.45, 0.756, 0.555, 0.379, 0.413};
-  static const int kConc[6] = {2, 4, 3, 1, 4, 4};
-  static const int kSplits[7] = {1, 2, 4, 8, 16, 32, 64};
+  static const double kEff[6] = {0.489, 0.283, 0.617, 0.488, 0.714, 0.765};
+  static const int kConc[6] = {1, 4, 3, 4, 2, 1};
+  static const int kSplits[8] = {1, 2, 4, 8, 16, 32, 64, 128};
   const double cu_rate = 157.3e12 / 256;  // fp32 matrix flop/s per CU
   double best = 1e30;
   GemmCfg pick{TI_32x32, 1, (R + 31) / 32 * 32};
@@ -677,7 +682,7 @@ static GemmCfg select_cfg_conv(int P, int Q, int R) {
       const double W = (double)ntiles(t, P, Q) * Se;
       const double per = (double)kTileBP[t] * kTileBQ[t] * r_split * 2 / (kEff[t] * cu_rate) * 1e6;
       double T = per * std::max(1.0, W / (256.0 * kConc[t]));
-      if (Se > 1) T += 2.15 + (double)P * Q * Se * 8 / 5e12 * 1e6;
+      if (Se > 1) T += 1.97 + (double)P * Q * Se * 8 / 5e12 * 1e6;
       if (T < best) {
         best = T;
         pick = GemmCfg{t, Se, r_split};
@@ -716,23 +721,24 @@ template <class T, int EPI>
 static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                            int vec_ops, int vec_epi, hipStream_t stream) {
   dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
-  // 128-bit operand loads only when both operands allow them.
   if constexpr (EPI != EPI_FWD_FF) {
     if (pr.conv) {
-      if (vec_ops == 3)
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, true, true>), grid, dim3(256), 0, stream, pr, ea,
-                           c.r_split, (float*)ws, vec_epi);
-      else
-        hipLaunchKernelGGL((gemm_kernel<T, EPI, false, true>), grid, dim3(256), 0, stream, pr,
-                           ea, c.r_split, (float*)ws, vec_epi);
+      // convolutions: 128-bit gathers per operand (the channel counts differ)
+      switch (vec_ops) {
+        case 3: hipLaunchKernelGGL((gemm_kernel<T, EPI, 3, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
+        case 2: hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
+        case 1: hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
+        default: hipLaunchKernelGGL((gemm_kernel<T, EPI, 0, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi);
+      }
       return hipGetLastError();
     }
   }
+  // 128-bit operand loads only when both operands allow them.
   if (vec_ops == 3)
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, true, false>), grid, dim3(256), 0, stream, pr, ea,
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 3, false>), grid, dim3(256), 0, stream, pr, ea,
                        c.r_split, (float*)ws, vec_epi);
   else
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, false, false>), grid, dim3(256), 0, stream, pr, ea,
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, 0, false>), grid, dim3(256), 0, stream, pr, ea,
                        c.r_split, (float*)ws, vec_epi);
   return hipGetLastError();
 }

@@ -220,6 +220,8 @@ GemmProblem conv_problem(const of_conv_desc* d, int kind, const float* a, const 
   GemmProblem pr{};
   pr.conv = 1;
   pr.cN = (int)d->N; pr.cH = (int)d->H; pr.cW = (int)d->W; pr.cC = C; pr.cCout = Co;
+  pr.dW = make_fastdiv((uint32_t)d->W); pr.dH = make_fastdiv((uint32_t)d->H);
+  pr.dC = make_fastdiv((uint32_t)C); pr.dCout = make_fastdiv((uint32_t)Co);
   pr.A = a; pr.B = b;
   if (kind == EPI_FWD) {          // A = x gathered, B = W [Cout, 9C]
     pr.P = NHW; pr.Q = Co; pr.R = 9 * C; pr.b_sq = 9 * C; pr.b_sr = 1;
