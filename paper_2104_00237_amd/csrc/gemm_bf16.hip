@@ -24,6 +24,8 @@
 // eager and backward-fusion weight gradients share the tiling rule).
 
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 
 #include "gemm_common.h"
 
@@ -368,7 +370,7 @@ static int64_t bntiles(int t, int P, int Q) {
 // 128x128 tiles when the output has enough of them, else 64x64; the reduction
 // is split until there are about 256 workgroups (at least 4 chunks per split).
 // The eager and backward-fusion weight gradients share this rule.
-static BCfg bselect(int kind, int P, int Q, int R) {
+static BCfg bselect_default(int kind, int P, int Q, int R) {
   (void)kind;
   const int t = bntiles(BTI_128x128, P, Q) >= 64 ? BTI_128x128 : BTI_64x64;
   const int BR = kBTileBR[t];
@@ -379,6 +381,21 @@ static BCfg bselect(int kind, int P, int Q, int R) {
   S = (R + r_split - 1) / r_split;
   return BCfg{t, S, r_split};
 }
+
+#ifdef OPFUSE_TUNING
+// Tuning builds only: OPFUSE_BF16_CFG="tile,S" overrides the bf16 tiling.
+static BCfg bselect(int kind, int P, int Q, int R) {
+  const char* e = getenv("OPFUSE_BF16_CFG");
+  if (!e) return bselect_default(kind, P, Q, R);
+  int t = 1, S = 1;
+  sscanf(e, "%d,%d", &t, &S);
+  const int BR = kBTileBR[t];
+  const int r_split = ((R + S - 1) / S + BR - 1) / BR * BR;
+  return BCfg{t, (R + r_split - 1) / r_split, r_split};
+}
+#else
+static BCfg bselect(int kind, int P, int Q, int R) { return bselect_default(kind, P, Q, R); }
+#endif
 
 size_t gemm_bf16_workspace_bytes(int kind, int P, int Q, int R) {
   const BCfg c = bselect(kind, P, Q, R);
