@@ -251,7 +251,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
 
   constexpr int SA = (T::BR / 8) * T::PLA;   // A part of a stage
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s) issue(s, s);
+  for (int s = 0; s < NS - 1; ++s) {
+    issue(s, s);
+    __builtin_amdgcn_sched_barrier(0);  // chunk 0 stays the oldest load
+  }
   for (int c0 = 0; c0 < nch; c0 += NS) {
 #pragma unroll
    for (int s = 0; s < NS; ++s) {

@@ -15,10 +15,17 @@ namespace opfuse {
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr uint32_t kOOB = 0x80000000u;  // beyond num_records: reads as 0
 
+// `base` must be the same in every lane (a tile origin): buffer descriptors
+// live in scalar registers.  Reading it from the first lane says so to the
+// compiler, which otherwise may not prove it and wraps every load in a loop
+// over the distinct values.
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
+  const uint64_t a = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* ub = (void*)(((uint64_t)hi << 32) | lo);
   // raw buffer, stride 0, 2^31-1 bytes addressable from `base`
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff,
-                                           0x00020000);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, 0x7fffffff, 0x00020000);
 }
 __device__ __forceinline__ float4 bload4(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));

@@ -7,6 +7,9 @@
 // reduction chunk (their partial tiles are summed in wave order).  Operand
 // tiles go global -> registers -> LDS ([r][x] layout, double buffered); the
 // next chunk's global loads are issued before the current chunk's MFMAs.
+// A forward or data gradient on 32x32 tiles can instead load its operands
+// straight into the matrix-core registers (gemm_direct_kernel, which runs
+// v_mfma_f32_16x16x4_f32 on 16x16 sub-blocks).
 // A grid-level split of the reduction (gridDim.z > 1) writes partial tiles to
 // the workspace and a second kernel sums them in split order and runs the
 // epilogue, so every result is deterministic and the same shape always uses
@@ -42,15 +45,12 @@
 namespace opfuse {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_, bool DIRECT_ = false>
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_>
 struct Tile {
   static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_, WR = WR_;
   static constexpr int NS = NS_;  // operand chunks in the register ring
-  // DIRECT: operands go from memory straight into the MFMA registers (no LDS
-  // staging); only for one 32x32 output block whose 4 waves split the reduction.
-  static constexpr bool DIRECT = DIRECT_;
-  static_assert(!DIRECT || (BP == 32 && BQ == 32 && WR == 4), "direct tiles are 32x32, 4-way split");
   static_assert(WP * WQ * WR == 4, "a workgroup is 4 wavefronts");
   static constexpr int WTP = BP / WP, WTQ = BQ / WQ;   // wavefront tile
   static constexpr int TP = WTP / 32, TQ = WTQ / 32;   // 32x32 MFMA blocks per wavefront
@@ -72,14 +72,17 @@ using T64x64 = Tile<64, 64, 16, 2, 2, 1, 6>;
 using T128x64 = Tile<128, 64, 16, 2, 2, 1, 4>;
 using T128x128 = Tile<128, 128, 16, 2, 2, 1, 3>;
 using T256x32 = Tile<256, 32, 16, 4, 1, 1, 3>;
-using T32x32D = Tile<32, 32, 32, 1, 1, 4, 8, true>;   // 8 blocks of 8 in flight per wave
 
+// TI_32x32D, TI_32x32D8: 32x32 blocks with operands loaded straight into the
+// matrix-core registers by 4 or 8 wavefronts (gemm_direct_kernel; forward and
+// data gradient of linear layers only, the LDS-staged 32x32 tile elsewhere).
 enum TileId {
-  TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32, TI_32x32D, TI_COUNT
+  TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32,
+  TI_32x32D, TI_32x32D8, TI_COUNT
 };
-static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256, 32};
-static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32, 32};
-static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16, 32};
+static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256, 32, 32};
+static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32, 32, 32};
+static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16, 32, 32};
 
 
 // A BX (output dim) x BR (reduction) tile of one operand, held in registers as
@@ -407,74 +410,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       lb[slot].load(pr.B, pr, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
   };
 
-  if constexpr (T::DIRECT) {
-    // Wave wr takes the blocks of 8 reduction elements b = wr, wr+4, wr+8, ...
-    // of this split; lane (row, h) holds elements 8b+4h .. 8b+4h+3 of its A row
-    // and its B row, and MFMA step e pairs element e of both halves (the same
-    // pairing for A and B, so every product of the block is summed once).
-    // Reduction-contiguous operands take one 128-bit load per block, the
-    // others four 32-bit loads that are coalesced across the lanes.  NS blocks
-    // are in flight per wave.
-    const int row = lane & 31, h = lane >> 5;
-    const int nr = rend - rbeg;
-    const int nblk = (nr + 7) >> 3;
-    const int myblk = nblk > wr ? (nblk - wr + 3) >> 2 : 0;
-    const rsrc_t rsa = make_rsrc(pr.A + (int64_t)p0 * pr.a_sp + (int64_t)rbeg * pr.a_sr);
-    const rsrc_t rsb = make_rsrc(pr.B + (int64_t)q0 * pr.b_sq + (int64_t)rbeg * pr.b_sr);
-    float4 ra[NS], rb[NS];
-    auto ld = [&](const rsrc_t& rs, int64_t s_x, int64_t s_r, bool rc, bool vec, int x, int nx,
-                  int r) -> float4 {
-      if (rc && vec) {
-        const bool ok = x < nx && r < nr;
-        return bload4(rs, ok ? (uint32_t)((x * s_x + r) * 4) : kOOB);
-      }
-      float e[4];
+  // In-order prologue (the scheduling barriers keep chunk 0 oldest), so the
+  // loop waits for one chunk at a time instead of draining the ring.
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const bool ok = x < nx && r + k < nr;
-        e[k] = bload1(rs, ok ? (uint32_t)((x * s_x + (r + k) * s_r) * 4) : kOOB);
-      }
-      return make_float4(e[0], e[1], e[2], e[3]);
-    };
-    auto dload = [&](int slot, int i) {
-      const int r = 8 * (wr + 4 * i) + 4 * h;
-      ra[slot] = ld(rsa, pr.a_sp, pr.a_sr, A_RC, VA, row, np, r);
-      rb[slot] = ld(rsb, pr.b_sq, pr.b_sr, B_RC, VB, row, nq, r);
-    };
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s) dload(s, s);
-    for (int i0 = 0; i0 < myblk; i0 += NS) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int i = i0 + s;
-        dload((s + NS - 1) % NS, i + NS - 1);
-        if (i < myblk) {
-          const float av[4] = {ra[s].x, ra[s].y, ra[s].z, ra[s].w};
-          const float bv[4] = {rb[s].x, rb[s].y, rb[s].z, rb[s].w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], acc[0][0], 0, 0, 0);
-          if constexpr (WG) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) dbsum = __fadd_rn(dbsum, av[e]);
-          }
-        }
-      }
-    }
-    if (do_db) {
-      // Sum the 8 partial column sums of dZ (4 waves x 2 halves) in order.
-      __syncthreads();
-      smem[(wr * 2 + h) * 32 + row] = dbsum;
-      __syncthreads();
-      if (tid < 32) {
-        float s8 = smem[tid];
-        for (int k = 1; k < 8; ++k) s8 = __fadd_rn(s8, smem[k * 32 + tid]);
-        dbsum = s8;
-      }
-    }
-  } else {
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s) issue(s, s);
+  for (int s = 0; s < NS - 1; ++s) {
+    issue(s, s);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 
   for (int c0 = 0; c0 < nch; c0 += NS) {
 #pragma unroll
@@ -516,7 +458,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       }
     }
   }
-  }  // !DIRECT
   // Every wavefront is done with the operand buffers before they are reused.
   __syncthreads();
 
@@ -593,6 +534,156 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   if (do_db && tid < T::BP && p0 + tid < pr.P) {
     if (S > 1) partial[(int64_t)S * pr.P * pr.Q + (int64_t)split * pr.P + p0 + tid] = dbsum;
     else bias_epilogue<EPI>(ea, p0 + tid, dbsum);
+  }
+}
+
+// ------------------------------------------------------- direct 32x32 tiles
+// One 32x32 output block per workgroup of NW wavefronts, for the forward and
+// the data gradient.  Operands go from memory straight into the MFMA operand
+// registers (no LDS staging).  Each wave runs v_mfma_f32_16x16x4_f32 on the
+// 2x2 sub-blocks of 16x16.  The waves split the reduction into blocks of 16
+// elements and wave w takes blocks w, w+NW, w+2NW, ... of its split; lane
+// (row, g), g = lane/16, holds elements 16b+4g .. 16b+4g+3 of rows row and
+// row+16 of A and of B, and MFMA step e pairs element e of the four groups
+// (the same pairing for A and B, so every product of a block is summed
+// exactly once).  Four lanes share each row, so a 128-bit load reads 64
+// contiguous bytes per row.  A reduction-contiguous operand takes one 128-bit
+// load per row and block, the other kind four 32-bit loads that are coalesced
+// across the lanes.  NS blocks are in flight per wave.  The NW partial tiles
+// are summed in wave order through LDS before the epilogue.
+template <int EPI, int NW, int NS, int VECS>
+__global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, EpiArgs ea,
+                                                              int r_split, float* partial,
+                                                              int vec_epi) {
+  static_assert(EPI == EPI_FWD || EPI == EPI_DGRAD, "forward and data gradient only");
+  static_assert(NW >= 4 && NW <= 16 && NS >= 2, "shape");
+  constexpr bool VA = (VECS & 1) != 0, VB = (VECS & 2) != 0;
+  constexpr bool B_RC = (EPI == EPI_FWD);  // dgrad: W is output-contiguous
+  constexpr int KB = 16;                   // reduction elements per block
+  __shared__ __attribute__((aligned(16))) float Cs[NW * 32 * 32];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int tx, ty;
+  xcd_tile(tx, ty);
+  const int p0 = tx * 32, q0 = ty * 32;
+  const int split = blockIdx.z, S = gridDim.z;
+  const int rbeg = split * r_split;
+  const int rend = min(pr.R, rbeg + r_split);
+  const int np = pr.P - p0, nq = pr.Q - q0;
+
+  // Epilogue item of thread tid < 256: row ep, columns eq .. eq+3 of the block.
+  // The data gradient loads its saved tensor (for act') before the main loop.
+  const int ep = tid >> 3, eq = (tid & 7) * 4;
+  const bool pref = EPI == EPI_DGRAD && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE;
+  float4 pf = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (pref) {
+    const bool ok = tid < 256 && ep < np && eq + 3 < nq;
+    const rsrc_t rp = make_rsrc(ea.prev + (int64_t)p0 * ea.ldp + q0);
+    pf = bload4(rp, ok ? (uint32_t)((ep * ea.ldp + eq) * 4) : kOOB);
+  }
+
+  const int row = lane & 15, grp = lane >> 4;
+  const int nr = rend - rbeg;
+  const int nblk = (nr + KB - 1) / KB;
+  const int myblk = nblk > wave ? (nblk - wave + NW - 1) / NW : 0;
+  const rsrc_t rsa = make_rsrc(pr.A + (int64_t)p0 * pr.a_sp + (int64_t)rbeg * pr.a_sr);
+  const rsrc_t rsb = make_rsrc(pr.B + (int64_t)q0 * pr.b_sq + (int64_t)rbeg * pr.b_sr);
+  auto ld = [&](const rsrc_t& rs, int64_t s_x, int64_t s_r, bool rc, bool vec, int x, int nx,
+                int r) -> float4 {
+    if (rc && vec) {
+      const bool ok = x < nx && r < nr;
+      return bload4(rs, ok ? (uint32_t)((x * s_x + r) * 4) : kOOB);
+    }
+    float e[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bool ok = x < nx && r + k < nr;
+      e[k] = bload1(rs, ok ? (uint32_t)((x * s_x + (r + k) * s_r) * 4) : kOOB);
+    }
+    return make_float4(e[0], e[1], e[2], e[3]);
+  };
+  float4 ra[NS][2], rb[NS][2];  // [slot][row half]
+  auto dload = [&](int slot, int i) {
+    const int r = KB * (wave + NW * i) + 4 * grp;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      ra[slot][hh] = ld(rsa, pr.a_sp, pr.a_sr, true, VA, row + 16 * hh, np, r);
+      rb[slot][hh] = ld(rsb, pr.b_sq, pr.b_sr, B_RC, VB, row + 16 * hh, nq, r);
+    }
+  };
+
+  floatx4 acc[2][2];  // sub-block (row half of A, row half of B)
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[a][b][k] = 0.f;
+  // Blocks past this wave's last one load nothing (every offset out of range).
+  // The prologue issues the blocks in order (the scheduling barriers keep it
+  // so): the loop head then waits only for the oldest block, not for the whole
+  // ring, which it would if block 0 were issued last.
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s) {
+    dload(s, s);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int i0 = 0; i0 < myblk; i0 += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const int i = i0 + s;
+      dload((s + NS - 1) % NS, i + NS - 1);
+      if (i < myblk) {
+        const float av[2][4] = {{ra[s][0].x, ra[s][0].y, ra[s][0].z, ra[s][0].w},
+                                {ra[s][1].x, ra[s][1].y, ra[s][1].z, ra[s][1].w}};
+        const float bv[2][4] = {{rb[s][0].x, rb[s][0].y, rb[s][0].z, rb[s][0].w},
+                                {rb[s][1].x, rb[s][1].y, rb[s][1].z, rb[s][1].w}};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+              acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a][e], bv[b][e], acc[a][b], 0, 0, 0);
+      }
+    }
+  }
+
+  // Partial tile of wave w at Cs[w][32][32] (MFMA 16x16 layout: lane holds
+  // column lane%16 and rows 4*(lane/16) + k of its sub-block).
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        Cs[(wave * 32 + 16 * a + 4 * grp + k) * 32 + 16 * b + row] = acc[a][b][k];
+  __syncthreads();
+  if (tid >= 256) return;
+  const int gp = p0 + ep, gq = q0 + eq;
+  if (gp >= pr.P || gq >= pr.Q) return;
+  float4 sum = *reinterpret_cast<const float4*>(Cs + ep * 32 + eq);
+#pragma unroll
+  for (int w = 1; w < NW; ++w) {
+    const float4 t = *reinterpret_cast<const float4*>(Cs + (w * 32 + ep) * 32 + eq);
+    sum.x = __fadd_rn(sum.x, t.x); sum.y = __fadd_rn(sum.y, t.y);
+    sum.z = __fadd_rn(sum.z, t.z); sum.w = __fadd_rn(sum.w, t.w);
+  }
+  const float c[4] = {sum.x, sum.y, sum.z, sum.w};
+  const int n = min(4, pr.Q - gq);
+  if (S > 1) {
+    float* dst = partial + ((int64_t)split * pr.P + gp) * pr.Q + gq;
+    if (n == 4 && (pr.Q & 3) == 0) st4(dst, sum);
+    else for (int e = 0; e < n; ++e) dst[e] = c[e];
+  } else if (pref && n == 4) {
+    const float4 r = make_float4(__fmul_rn(c[0], act_grad(ea.act, pf.x)),
+                                 __fmul_rn(c[1], act_grad(ea.act, pf.y)),
+                                 __fmul_rn(c[2], act_grad(ea.act, pf.z)),
+                                 __fmul_rn(c[3], act_grad(ea.act, pf.w)));
+    st4(ea.out + (int64_t)gp * ea.ldo + gq, r);
+  } else {
+    const float* bias = (EPI == EPI_FWD && ea.bias) ? ea.bias + gq : nullptr;
+    epilogue<EPI>(ea, gp, gq, c, n, bias, vec_epi);
   }
 }
 
@@ -743,6 +834,25 @@ static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArg
   return hipGetLastError();
 }
 
+template <int EPI, int NW, int NS>
+static hipError_t launch_direct(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea,
+                                void* ws, int vec_ops, int vec_epi, hipStream_t stream) {
+  dim3 grid((pr.P + 31) / 32, (pr.Q + 31) / 32, c.S);
+  // The data gradient's B operand (W) is output-contiguous and never takes
+  // 128-bit loads, so only A's flag matters there.
+  const int v = EPI == EPI_FWD ? (vec_ops == 3 ? 3 : 0) : (vec_ops & 1);
+  if (v == 3)
+    hipLaunchKernelGGL((gemm_direct_kernel<EPI, NW, NS, 3>), grid, dim3(64 * NW), 0, stream, pr,
+                       ea, c.r_split, (float*)ws, vec_epi);
+  else if (v == 1)
+    hipLaunchKernelGGL((gemm_direct_kernel<EPI, NW, NS, 1>), grid, dim3(64 * NW), 0, stream, pr,
+                       ea, c.r_split, (float*)ws, vec_epi);
+  else
+    hipLaunchKernelGGL((gemm_direct_kernel<EPI, NW, NS, 0>), grid, dim3(64 * NW), 0, stream, pr,
+                       ea, c.r_split, (float*)ws, vec_epi);
+  return hipGetLastError();
+}
+
 template <int EPI>
 static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                               int vec_ops, int vec_epi, hipStream_t s) {
@@ -757,10 +867,16 @@ static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const Epi
       else return launch_t<T128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_256x32: return launch_t<T256x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_32x32D:
-      // direct loads exist for strided operands only; the same tiling otherwise
-      if constexpr (EPI == EPI_FWD_FF) return launch_t<T32x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
-      else if (pr.conv) return launch_t<T32x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
-      else return launch_t<T32x32D, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_32x32D8:
+      // direct loads exist for the linear forward and data gradient; the same
+      // tiling through LDS otherwise
+      if constexpr (EPI == EPI_FWD || EPI == EPI_DGRAD) {
+        if (!pr.conv) {
+          if (c.tile == TI_32x32D) return launch_direct<EPI, 4, 4>(c, pr, ea, ws, vec_ops, vec_epi, s);
+          return launch_direct<EPI, 8, 4>(c, pr, ea, ws, vec_ops, vec_epi, s);
+        }
+      }
+      return launch_t<T32x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
   }
   return hipErrorInvalidValue;
 }

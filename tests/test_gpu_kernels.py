@@ -44,6 +44,8 @@ def _ws(torch, dev, nbytes):
 SHAPES = [  # (M, N, K): tails in every dimension, split reductions, tiny and wide
     (32, 128, 64), (33, 10, 27), (72, 168, 200), (256, 1024, 1024), (64, 520, 520),
     (130, 96, 44), (300, 70, 257), (64, 2048, 4096), (1, 5, 3),
+    # direct-load 32x32 tiles with tails: scalar loads (K % 4 != 0), partial blocks
+    (300, 1030, 1001), (290, 1028, 1100),
 ]
 
 
