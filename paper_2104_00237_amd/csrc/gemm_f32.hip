@@ -66,7 +66,7 @@ struct Tile {
 };
 
 // Tile menu (P x Q per workgroup, reduction chunk, wavefront split).
-using T32x32 = Tile<32, 32, 32, 1, 1, 4, 8>;
+using T32x32 = Tile<32, 32, 32, 1, 1, 4, 4>;
 using T64x32 = Tile<64, 32, 32, 2, 1, 2, 4>;
 using T64x64 = Tile<64, 64, 16, 2, 2, 1, 6>;
 using T128x64 = Tile<128, 64, 16, 2, 2, 1, 4>;
@@ -338,11 +338,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
 #pragma unroll
       for (int k = 0; k < 16; ++k) acc[i][j][k] = 0.f;
 
-  // Epilogue operands of small tiles are loaded before the main loop so their
+  // Epilogue operands of small tiles are loaded during the main loop so their
   // latency hides behind it: the parameter and history tile of backward-fusion
   // (this workgroup is their only reader and writer) and the previous layer's
-  // saved tensor of the data gradient.  Thread t handles the float4 items
-  // t, t+256, ... of the tile in row-major order.
+  // saved tensor of the data gradient.  They are issued after the first
+  // operand chunks, which are then not queued behind them.  Thread t handles
+  // the float4 items t, t+256, ... of the tile in row-major order.
   constexpr int NQ4 = T::BQ / 4;
   constexpr int ITEMS = T::BP * NQ4;
   constexpr int EPT = (ITEMS + 255) / 256;
@@ -352,31 +353,30 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   float4 pf_w[NPF], pf_m[NPF], pf_v[NPF];
   const bool pref = (PREF_BF && S == 1 && (vec_epi & 2) && ea.gW == nullptr) ||
                     (PREF_DG && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE);
-  if constexpr (PREF_BF || PREF_DG) {
-    if (pref) {
-      const int64_t ld = PREF_BF ? ea.ldo : ea.ldp;
-      const int64_t org = (int64_t)p0 * ld + q0;
-      const rsrc_t r0 = make_rsrc(PREF_BF ? ea.W.w + org : ea.prev + org);
-      const rsrc_t r1 = make_rsrc(PREF_BF ? ea.W.m + org : ea.prev + org);
-      const rsrc_t r2 = make_rsrc((PREF_BF && ea.opt.kind != OF_OPT_SGD) ? ea.W.v + org
-                                                                         : ea.W.m + org);
+  auto prefetch = [&]() {
+    if constexpr (PREF_BF || PREF_DG) {
+      if (pref) {
+        const int64_t ld = PREF_BF ? ea.ldo : ea.ldp;
+        const int64_t org = (int64_t)p0 * ld + q0;
+        const rsrc_t r0 = make_rsrc(PREF_BF ? ea.W.w + org : ea.prev + org);
+        const rsrc_t r1 = make_rsrc(PREF_BF ? ea.W.m + org : ea.prev + org);
+        const rsrc_t r2 = make_rsrc((PREF_BF && ea.opt.kind != OF_OPT_SGD) ? ea.W.v + org
+                                                                           : ea.W.m + org);
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        const int idx = tid + e * 256;
-        const int p = idx / NQ4, q = (idx % NQ4) * 4;
-        const bool ok = idx < ITEMS && p0 + p < pr.P && q0 + q + 3 < pr.Q;
-        const uint32_t off = ok ? (uint32_t)((p * ld + q) * 4) : kOOB;
-        pf_w[e] = bload4(r0, off);
-        if constexpr (PREF_BF) {
-          pf_m[e] = bload4(r1, off);
-          pf_v[e] = bload4(r2, off);
+        for (int e = 0; e < EPT; ++e) {
+          const int idx = tid + e * 256;
+          const int p = idx / NQ4, q = (idx % NQ4) * 4;
+          const bool ok = idx < ITEMS && p0 + p < pr.P && q0 + q + 3 < pr.Q;
+          const uint32_t off = ok ? (uint32_t)((p * ld + q) * 4) : kOOB;
+          pf_w[e] = bload4(r0, off);
+          if constexpr (PREF_BF) {
+            pf_m[e] = bload4(r1, off);
+            pf_v[e] = bload4(r2, off);
+          }
         }
       }
     }
-  }
-
-  // (after the prefetch above is in flight, so its latency hides this)
-  if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+  };
 
   // Register ring of NS operand chunks: the loads of chunk c+NS-1 are issued
   // before chunk c is stored to LDS and multiplied, so NS-1 chunks are in
@@ -417,6 +417,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     issue(s, s);
     __builtin_amdgcn_sched_barrier(0);
   }
+  prefetch();
+  // (after the loads above are in flight, so their latency hides this)
+  if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
 
   for (int c0 = 0; c0 < nch; c0 += NS) {
 #pragma unroll
