@@ -215,4 +215,86 @@ __device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& 
   }
 }
 
+// Long split lists: G = 8 consecutive lanes (one wave holds whole groups)
+// share each float4 item of the output.  Lane j sums the splits
+// j*SG .. (j+1)*SG - 1 in split order (SG = ceil(S / 8)); the group's first
+// lane then adds the 8 sums in lane order and runs the epilogue.  A single
+// thread per item would wait for S / 8 load latencies in a row.  The order
+// is fixed, so every ordering that shares a tiling still gets the same bits.
+// The bias-gradient partials are summed the same way.
+template <int EPI>
+__device__ __forceinline__ void split_reduce_coop_body(int P, int Q, int S, EpiArgs& ea,
+                                                       const float* __restrict__ partial,
+                                                       int vec_epi, int with_db) {
+  if (EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+  const int nq4 = (Q + 3) / 4;
+  const int64_t total = (int64_t)P * nq4;
+  const int64_t PQ = (int64_t)P * Q;
+  const int lane = threadIdx.x & 63, j = lane & 7, lead = lane & ~7;
+  const int SG = (S + 7) / 8;
+  const int kb = min(S, j * SG), ke = min(S, kb + SG);
+  const int64_t groups = (int64_t)gridDim.x * 32;
+  // lanes [0, 4): this lane's partial sums of the item's (up to) 4 elements
+  auto lane_sum = [&](const float* src, int n, bool v4, float (&acc)[4]) {
+    for (int e = 0; e < 4; ++e) acc[e] = 0.f;
+    for (int k0 = kb; k0 < ke; k0 += 8) {
+      float4 t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + u;
+        if (k < ke) {
+          const float* a = src + (int64_t)k * PQ;
+          t[u] = v4 ? ld4(a) : make_float4(a[0], n > 1 ? a[1] : 0.f, n > 2 ? a[2] : 0.f,
+                                           n > 3 ? a[3] : 0.f);
+        } else {
+          t[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (k0 + u < ke) {
+          acc[0] = __fadd_rn(acc[0], t[u].x); acc[1] = __fadd_rn(acc[1], t[u].y);
+          acc[2] = __fadd_rn(acc[2], t[u].z); acc[3] = __fadd_rn(acc[3], t[u].w);
+        }
+      }
+    }
+  };
+  for (int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3; idx < total; idx += groups) {
+    const int p = (int)(idx / nq4), q = (int)(idx % nq4) * 4;
+    const int n = min(4, Q - q);
+    float acc[4];
+    lane_sum(partial + (int64_t)p * Q + q, n, n == 4 && (Q & 3) == 0, acc);
+    float c[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      c[e] = __shfl(acc[e], lead);
+#pragma unroll
+      for (int g = 1; g < 8; ++g) c[e] = __fadd_rn(c[e], __shfl(acc[e], lead + g));
+    }
+    if (j == 0) {
+      const float* bias = nullptr;
+      if ((EPI == EPI_FWD || EPI == EPI_FWD_FF) && ea.bias) bias = ea.bias + q;
+      epilogue<EPI == EPI_FWD_FF ? EPI_FWD : EPI>(ea, p, q, c, n, bias, vec_epi);
+    }
+  }
+  if (with_db) {
+    const float* dbp = partial + (int64_t)S * PQ;
+    for (int64_t p = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3; p < P; p += groups) {
+      float acc = 0.f;
+      for (int k0 = kb; k0 < ke; k0 += 8) {
+        float t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t[u] = k0 + u < ke ? dbp[(int64_t)(k0 + u) * P + p] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (k0 + u < ke) acc = __fadd_rn(acc, t[u]);
+      }
+      float s = __shfl(acc, lead);
+#pragma unroll
+      for (int g = 1; g < 8; ++g) s = __fadd_rn(s, __shfl(acc, lead + g));
+      if (j == 0) bias_epilogue<EPI>(ea, (int)p, s);
+    }
+  }
+}
+
 }  // namespace opfuse

@@ -68,7 +68,7 @@ struct Tile {
 // Tile menu (P x Q per workgroup, reduction chunk, wavefront split).
 using T32x32 = Tile<32, 32, 32, 1, 1, 4, 4>;
 using T64x32 = Tile<64, 32, 32, 2, 1, 2, 4>;
-using T64x64 = Tile<64, 64, 16, 2, 2, 1, 6>;
+using T64x64 = Tile<64, 64, 16, 2, 2, 1, 4>;
 using T128x64 = Tile<128, 64, 16, 2, 2, 1, 4>;
 using T128x128 = Tile<128, 128, 16, 2, 2, 1, 3>;
 using T256x32 = Tile<256, 32, 16, 4, 1, 1, 3>;
@@ -690,6 +690,15 @@ __global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, Ep
   }
 }
 
+// Sum the split partials (8 lanes per output item for long split lists),
+// then run the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void split_reduce_coop_kernel(int P, int Q, int S, EpiArgs ea,
+                                                                const float* __restrict__ partial,
+                                                                int vec_epi, int with_db) {
+  split_reduce_coop_body<EPI>(P, Q, S, ea, partial, vec_epi, with_db);
+}
+
 // Sum the split partials in split order, then run the epilogue.
 template <int EPI>
 __global__ __launch_bounds__(256) void split_reduce_kernel(int P, int Q, int S, EpiArgs ea,
@@ -884,10 +893,20 @@ static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const Epi
   return hipErrorInvalidValue;
 }
 
+// Split counts from which 8 lanes share each output item of the reduction pass.
+constexpr int kCoopSplits = 16;
+
 template <int EPI>
 static hipError_t launch_reduce(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea,
                                 void* ws, int vec_epi, int with_db, hipStream_t s) {
   const int64_t work = (int64_t)pr.P * ((pr.Q + 3) / 4);
+  if (c.S >= kCoopSplits) {
+    const int64_t lanes = std::max<int64_t>(work, with_db ? pr.P : 0) * 8;
+    const int blocks = (int)std::min<int64_t>(2048, std::max<int64_t>(1, (lanes + 255) / 256));
+    hipLaunchKernelGGL((split_reduce_coop_kernel<EPI>), dim3(blocks), dim3(256), 0, s, pr.P, pr.Q,
+                       c.S, ea, (const float*)ws, vec_epi, with_db);
+    return hipGetLastError();
+  }
   const int blocks = (int)std::min<int64_t>(2048, std::max<int64_t>(1, (work + 255) / 256));
   hipLaunchKernelGGL((split_reduce_kernel<EPI>), dim3(blocks), dim3(256), 0, s, pr.P, pr.Q, c.S,
                      ea, (const float*)ws, vec_epi, with_db);
