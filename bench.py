@@ -337,6 +337,8 @@ def main():
     _, _, probe, _ = time_ordering(torch, cfg, "bf", batches, 2, 3, classes)
     totals = {c: sum(d for d, _ in probe.durations(c)) for c in classes}
     dom = max(totals, key=totals.get)
+    print("[bench] launch-class totals (ms over the probe steps): " +
+          ", ".join(f"{c} {t:.3f}" for c, t in totals.items()), file=sys.stderr, flush=True)
     ms_dom_step, _, timer, _ = time_ordering(torch, cfg, "bf", batches, args.warmup, args.steps,
                                              (dom,))
     launches = {d["name"]: d for d in layer_launches(cfg)}
@@ -345,7 +347,8 @@ def main():
     # one) and report the group with the largest total time.
     by_shape = {}
     for d_ms, op in recs:
-        by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name))
+        if op is not None:
+            by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name))
     costed = [k for k in by_shape if launches[by_shape[k][0][1]].get(dom)]
     shape = max(costed, key=lambda s: sum(d for d, _ in by_shape[s]))
     durs = [d for d, _ in by_shape[shape]]

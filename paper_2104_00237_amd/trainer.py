@@ -345,7 +345,7 @@ class ChainNet:
     def backward_fused(self, x, done):
         """Backward-fusion: `done(op)` is called after each layer's update is enqueued."""
         tr = self.tr
-        timed = tr.timer is not None and tr.timer.wants("wgrad_bf")
+        timed = tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad"))
         for i in reversed(range(len(self.ops))):
             op = self.ops[i]
             if op.kind == "linear" and not timed:
@@ -477,7 +477,7 @@ class TBlockNet:
             tr._t0("wgrad", tr.stream, op)
             op.wgrad(tr, dz, x)
             tr._t1("wgrad", tr.stream)
-        elif tr.timer is not None and tr.timer.wants("wgrad_bf"):
+        elif tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad")):
             tr._t0("dgrad", tr.stream, op)
             op.dgrad(tr, dz, prev, act_prev, dx)
             tr._t1("dgrad", tr.stream)
