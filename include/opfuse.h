@@ -115,6 +115,27 @@ typedef struct of_param {
   int64_t numel;
 } of_param;
 
+/*
+ * A pending update carried by a forward launch (forward-fusion of a later
+ * operator, Appendix B.1, Alg. 2): up to two tensors, each with its pending
+ * gradient, updated with `opt` by extra workgroups of the forward's kernel.
+ * A gradient is one vector of numel elements (rows == 1) or `rows` row
+ * partials [rows, numel] summed in row order (a LayerNorm parameter's
+ * gradient).  t2.w == NULL: one tensor.  Every element gets exactly the
+ * operations of of_optimizer_step (vector) or of_elementwise_fused_update
+ * (rows), so results are bit-identical to those passes.  The carried tensors
+ * must not overlap anything the forward reads or writes.
+ */
+typedef struct of_carry {
+  of_param t1;
+  const float* g1;
+  int64_t rows1;
+  of_param t2;
+  const float* g2;
+  int64_t rows2;
+  of_opt opt;
+} of_carry;
+
 typedef struct of_linear_desc {
   int64_t M, N, K;   /* rows, output features, input features (all >= 1) */
   int64_t ldx;       /* row stride of X in elements; 0 means K */
@@ -186,6 +207,18 @@ of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_
                               size_t ws_bytes, void* stream);
 
 /*
+ * of_linear_fwd whose launch also applies a later operator's pending update
+ * (forward-fusion): `next` is applied by extra workgroups of the same kernel,
+ * overlapping the contraction, so the later operator's forward finds its
+ * parameters updated without a launch of its own.  next == NULL: identical to
+ * of_linear_fwd.  Y is bit-identical to of_linear_fwd's, and the carried
+ * tensors to a separate update pass.
+ */
+of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_param* W,
+                              const float* b, float* z, float* y, const of_carry* next,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Data gradient with the OLD weights (the dependency rule after Alg. 3):
  *   dX = (dZ W) * act_prev'(prev)
  * dz: [M, ldy].  prev: the previous layer's saved tensor, [M, ldx]: its Y for
@@ -243,6 +276,11 @@ size_t of_conv_workspace_size(const of_conv_desc* d, int32_t op);
 /* Forward node of a convolution layer (Fig. 1(a)): y = act(conv(x, W) + b). */
 of_status of_conv_fwd(const of_conv_desc* d, const float* x, const of_param* W, const float* b,
                       float* y, void* ws, size_t ws_bytes, void* stream);
+
+/* of_conv_fwd carrying a later operator's pending update, as of_linear_fwd_carry. */
+of_status of_conv_fwd_carry(const of_conv_desc* d, const float* x, const of_param* W,
+                            const float* b, float* y, const of_carry* next, void* ws,
+                            size_t ws_bytes, void* stream);
 
 /*
  * Data gradient with the OLD filter (the dependency rule after Alg. 3):

@@ -38,6 +38,11 @@ class OfParam(ctypes.Structure):
                 ("numel", c_int64)]
 
 
+class OfCarry(ctypes.Structure):
+    _fields_ = [("t1", OfParam), ("g1", c_void_p), ("rows1", c_int64),
+                ("t2", OfParam), ("g2", c_void_p), ("rows2", c_int64), ("opt", OfOpt)]
+
+
 class OfLinearDesc(ctypes.Structure):
     _fields_ = [("M", c_int64), ("N", c_int64), ("K", c_int64), ("ldx", c_int64),
                 ("ldy", c_int64), ("dtype", c_int32), ("act", c_int32), ("has_bias", c_int32)]
@@ -61,6 +66,8 @@ _SIGS = {
     "of_linear_workspace_size": (c_size_t, [P(OfLinearDesc), c_int32]),
     "of_linear_fwd": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_void_p,
                                 c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_linear_fwd_carry": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_void_p,
+                                      c_void_p, P(OfCarry), c_void_p, c_size_t, c_void_p]),
     "of_linear_fwd_fused": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p,
                                       P(OfParam), c_void_p, P(OfOpt), c_void_p, c_void_p,
                                       c_void_p, c_size_t, c_void_p]),
@@ -79,6 +86,8 @@ _SIGS = {
     "of_conv_workspace_size": (c_size_t, [P(OfConvDesc), c_int32]),
     "of_conv_fwd": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_void_p, c_void_p,
                               c_size_t, c_void_p]),
+    "of_conv_fwd_carry": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_void_p,
+                                    P(OfCarry), c_void_p, c_size_t, c_void_p]),
     "of_conv_bwd_data": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_int32,
                                    c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_conv_bwd_weight": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, c_void_p, c_void_p,
@@ -162,7 +171,7 @@ def of_layernorm_partial_rows(M):
     return load().of_layernorm_partial_rows(M)
 
 
-for _n in ("of_linear_fwd", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
+for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
@@ -178,6 +187,12 @@ def make_opt(hyper, step, step_dev=None):
     return OfOpt(OPT_KINDS[hyper["kind"]], hyper["lr"], hyper.get("weight_decay", 0.0),
                  hyper.get("momentum", 0.0), hyper.get("beta1", 0.0), hyper.get("beta2", 0.0),
                  hyper.get("eps", 0.0), step, step_dev)
+
+
+def make_carry(opt, t1, g1, rows1=1, t2=None, g2=None, rows2=1):
+    """of_carry: tensor t1 (an OfParam) with gradient g1 (device pointer; `rows1`
+    row partials), and optionally t2 / g2."""
+    return OfCarry(t1, g1, rows1, t2 if t2 is not None else OfParam(), g2, rows2, opt)
 
 
 def param_of(w, m, v=None, w_bf16=None):

@@ -198,6 +198,22 @@ struct GemmProblem {
   FastDiv dW, dH, dC, dCout;    // convolution: divisors of the gather index arithmetic
 };
 
+// An update carried by a contraction launch (forward-fusion of a later
+// operator): the workgroups of the z-slices from z0 on apply the optimizer to
+// up to two tensors instead of computing tiles.  A tensor's gradient is one
+// vector (rows == 1) or `rows` row partials of stride `ld`, summed in row order.
+struct CarryTensor {
+  of_param p;           // p.w == nullptr: no tensor
+  const float* g;
+  int64_t rows, ld;
+  int vec;              // 128-bit paths allowed (vector gradients)
+};
+struct CarryArgs {
+  CarryTensor t[2];
+  OptK opt;
+  int z0;               // z-slices of the contraction itself; 0: nothing carried
+};
+
 struct EpiArgs {
   // outputs
   float* out; int64_t ldo;      // y (FWD), dx (DGRAD), dw (WGRAD)
@@ -215,6 +231,7 @@ struct EpiArgs {
   const float* gb;              // FF: pending bias gradient; BF: extra bias gradient
   int with_db;                  // WGRAD: db != NULL; WGRAD_BF: b.w != NULL
   OptK opt;
+  CarryArgs carry;              // FWD: a later operator's update (carry.z0 == 0: none)
 };
 
 size_t gemm_workspace_bytes(int kind, int P, int Q, int R, int conv = 0);

@@ -209,13 +209,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
   constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
   __shared__ __attribute__((aligned(16))) unsigned char smem_raw[T::SMX];
   uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
+  if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+    carry_update(ea.carry);  // a later operator's update rides on this launch
+    return;
+  }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wp = wave % T::WP, wq = wave / T::WP;
   int tx, ty;
   xcd_tile(tx, ty);
   const int p0 = tx * T::BP, q0 = ty * T::BQ;
-  const int split = blockIdx.z, S = gridDim.z;
+  const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
@@ -364,6 +368,7 @@ __global__ __launch_bounds__(256) void split_reduce_bf16_kernel(int P, int Q, in
 // --------------------------------------------------------------- host side
 struct BCfg {
   int tile, S, r_split;
+  int cz = 0;   // z-slices of carried-update workgroups after the splits
 };
 
 static int64_t bntiles(int t, int P, int Q) {
@@ -409,7 +414,7 @@ size_t gemm_bf16_workspace_bytes(int kind, int P, int Q, int R) {
 template <class T, int EPI, bool VA, bool VB>
 static hipError_t blaunch_v(const BCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                             int vec_epi, hipStream_t s) {
-  dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
+  dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S + c.cz);
   if (pr.b_bf16)
     hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, true>), grid, dim3(256), 0, s, pr, ea,
                        c.r_split, (float*)ws, vec_epi);
@@ -458,10 +463,17 @@ static int bvec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* v
   return (va ? 1 : 0) | (vb ? 2 : 0);
 }
 
-hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, void* ws,
                             hipStream_t stream) {
   if (pr.a_bf16 || pr.conv) return hipErrorInvalidValue;
-  const BCfg c = bselect(kind, pr.P, pr.Q, pr.R);
+  BCfg c = bselect(kind, pr.P, pr.Q, pr.R);
+  EpiArgs ea = ea_in;
+  ea.carry.z0 = 0;
+  if (ea.carry.t[0].p.w || ea.carry.t[1].p.w) {
+    if (kind != EPI_FWD) return hipErrorInvalidValue;  // only a forward carries an update
+    c.cz = carry_slices(ea.carry, bntiles(c.tile, pr.P, pr.Q));
+    ea.carry.z0 = c.S;
+  }
   int vec_epi = 0;
   const int vec_ops = bvec_flags(pr, kind, ea, &vec_epi);
   const int with_db = (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) && ea.with_db;

@@ -3,6 +3,8 @@
 // weight gradient, backward-fusion update) and the split-reduction pass.
 #pragma once
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace opfuse {
@@ -61,6 +63,60 @@ __device__ __forceinline__ void xcd_tile(int& tx, int& ty) {
   const int xcd = lin & 7, j = lin >> 3;            // j < bw * bh
   tx = (xcd % sx) * bw + j % bw;
   ty = (xcd / sx) * bh + j / bw;
+}
+
+// ------------------------------------------------------------ carried update
+// Run by the workgroups of the z-slices from c.z0 on, grid-stride over the
+// carried tensors.  Each element gets the same operations as in the eager
+// optimizer pass (vector gradients) or the rows-mode update (row partials).
+__device__ __forceinline__ void carry_update(const CarryArgs& c) {
+  OptK o = c.opt;
+  opt_prepare(o);
+  const int64_t slice = (int64_t)gridDim.x * gridDim.y;
+  const int64_t u = ((int64_t)(blockIdx.z - c.z0) * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t U = (int64_t)(gridDim.z - c.z0) * slice;
+  for (int k = 0; k < 2; ++k) {
+    const CarryTensor& T = c.t[k];
+    if (T.p.w == nullptr) continue;
+    const int64_t n = T.p.numel;
+    if (T.rows == 1) {
+      for (int64_t i = (u * 256 + threadIdx.x) * 4; i < n; i += U * 1024) {
+        if (T.vec && i + 3 < n) {
+          update4(o, T.p, ld4(T.g + i), i);
+        } else {
+          for (int64_t e = i; e < n && e < i + 4; ++e) update1(o, T.p, T.g[e], e);
+        }
+      }
+    } else {
+      for (int64_t i = u * 256 + threadIdx.x; i < n; i += U * 256) {
+        float s = T.g[i];
+        for (int64_t r0 = 1; r0 < T.rows; r0 += 8) {
+          float v[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] = r0 + q < T.rows ? T.g[(r0 + q) * T.ld + i] : 0.f;
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (r0 + q < T.rows) s = __fadd_rn(s, v[q]);
+        }
+        update1(o, T.p, s, i);
+      }
+    }
+  }
+}
+
+// z-slices of carry workgroups for a contraction whose slice has `slice`
+// workgroups: about one workgroup per 256 work items (a float4 of a vector
+// gradient, an element of a rows gradient), at most 256 workgroups.
+inline int carry_slices(const CarryArgs& c, int64_t slice) {
+  int64_t items = 0;
+  for (int k = 0; k < 2; ++k) {
+    const CarryTensor& T = c.t[k];
+    if (T.p.w == nullptr) continue;
+    items += T.rows == 1 ? (T.p.numel + 3) / 4 : T.p.numel;
+  }
+  if (items == 0) return 0;
+  const int64_t want = std::min<int64_t>(256, (items + 255) / 256);
+  return (int)((want + slice - 1) / slice);
 }
 
 // ----------------------------------------------------------------- epilogues

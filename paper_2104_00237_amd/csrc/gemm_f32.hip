@@ -313,13 +313,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   constexpr int SMEM = T::SMX + (EPI == EPI_FWD_FF ? T::BQ : 0);
   static_assert(SMEM * 4 <= 64 * 1024, "LDS per workgroup");
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
+  if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+    carry_update(ea.carry);  // a later operator's update rides on this launch
+    return;
+  }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wp = wave % T::WP, wq = (wave / T::WP) % T::WQ, wr = wave / (T::WP * T::WQ);
   int tx, ty;
   xcd_tile(tx, ty);
   const int p0 = tx * T::BP, q0 = ty * T::BQ;
-  const int split = blockIdx.z, S = gridDim.z;
+  const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
@@ -564,12 +568,16 @@ __global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, Ep
   constexpr bool B_RC = (EPI == EPI_FWD);  // dgrad: W is output-contiguous
   constexpr int KB = 16;                   // reduction elements per block
   __shared__ __attribute__((aligned(16))) float Cs[NW * 32 * 32];
+  if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+    carry_update(ea.carry);  // a later operator's update rides on this launch
+    return;
+  }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int tx, ty;
   xcd_tile(tx, ty);
   const int p0 = tx * 32, q0 = ty * 32;
-  const int split = blockIdx.z, S = gridDim.z;
+  const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int np = pr.P - p0, nq = pr.Q - q0;
@@ -713,6 +721,7 @@ struct GemmCfg {
   int tile;
   int S;        // grid-level reduction splits
   int r_split;  // reduction elements per split (multiple of the tile's BR)
+  int cz = 0;   // z-slices of carried-update workgroups after the splits
 };
 
 static int64_t ntiles(int t, int P, int Q) {
@@ -759,6 +768,11 @@ static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
       const bool direct = order[i] == TI_32x32 && (kind == EPI_FWD || kind == EPI_DGRAD);
       return make_cfg(direct ? TI_32x32D : order[i], P, Q, R, 256, 16);
     }
+  // Fewer than 256 blocks of 32x32 (a narrow classifier, a short batch): a
+  // forward or data gradient takes direct 32x32 tiles, unsplit while the
+  // reduction is short (its second pass would cost more than the split saves).
+  if (kind == EPI_FWD || kind == EPI_DGRAD)
+    return make_cfg(TI_32x32D, P, Q, R, R <= 1024 ? 1 : 64, 16);
   return make_cfg(TI_32x32, P, Q, R, 1024, 64);
 }
 
@@ -823,7 +837,7 @@ size_t gemm_workspace_bytes(int kind, int P, int Q, int R, int conv) {
 template <class T, int EPI>
 static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                            int vec_ops, int vec_epi, hipStream_t stream) {
-  dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S);
+  dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S + c.cz);
   if constexpr (EPI != EPI_FWD_FF) {
     if (pr.conv) {
       // convolutions: 128-bit gathers per operand (the channel counts differ)
@@ -849,7 +863,7 @@ static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArg
 template <int EPI, int NW, int NS>
 static hipError_t launch_direct(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea,
                                 void* ws, int vec_ops, int vec_epi, hipStream_t stream) {
-  dim3 grid((pr.P + 31) / 32, (pr.Q + 31) / 32, c.S);
+  dim3 grid((pr.P + 31) / 32, (pr.Q + 31) / 32, c.S + c.cz);
   // The data gradient's B operand (W) is output-contiguous and never takes
   // 128-bit loads, so only A's flag matters there.
   const int v = EPI == EPI_FWD ? (vec_ops == 3 ? 3 : 0) : (vec_ops & 1);
@@ -951,9 +965,16 @@ static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* ve
   return (va ? 1 : 0) | (vb ? 2 : 0);
 }
 
-hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
+hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, void* ws,
                        hipStream_t stream) {
-  const GemmCfg c = select_cfg(kind, pr.P, pr.Q, pr.R, pr.conv);
+  GemmCfg c = select_cfg(kind, pr.P, pr.Q, pr.R, pr.conv);
+  EpiArgs ea = ea_in;
+  ea.carry.z0 = 0;
+  if (ea.carry.t[0].p.w || ea.carry.t[1].p.w) {
+    if (kind != EPI_FWD) return hipErrorInvalidValue;  // only a forward carries an update
+    c.cz = carry_slices(ea.carry, ntiles(c.tile, pr.P, pr.Q));
+    ea.carry.z0 = c.S;
+  }
   int vec_epi = 0;
   const int vec_ops = vec_flags(pr, kind, ea, &vec_epi);
   const bool wg = (kind == EPI_WGRAD || kind == EPI_WGRAD_BF);

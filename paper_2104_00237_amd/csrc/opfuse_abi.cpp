@@ -69,6 +69,36 @@ of_status check_param(const of_param* p, const char* name, int64_t numel, int ki
   return OF_OK;
 }
 
+// Validates `c` and fills `out` (z0 is left to the launcher).
+of_status make_carry(const of_carry* c, CarryArgs* out) {
+  memset(out, 0, sizeof(*out));
+  if (c == nullptr) return OF_OK;
+  of_status st = check_opt(&c->opt);
+  if (st != OF_OK) return st;
+  const of_param* ts[2] = {&c->t1, &c->t2};
+  const float* gs[2] = {c->g1, c->g2};
+  const int64_t rows[2] = {c->rows1, c->rows2};
+  for (int k = 0; k < 2; ++k) {
+    if (k == 1 && c->t2.w == nullptr) break;
+    const char* name = k == 0 ? "next->t1" : "next->t2";
+    REQUIRE(ts[k]->numel >= 1, OF_EINVAL, "%s->numel must be >= 1", name);
+    if ((st = check_param(ts[k], name, ts[k]->numel, c->opt.kind, true)) != OF_OK) return st;
+    REQUIRE(gs[k] != nullptr && al4(gs[k]), gs[k] ? OF_EALIGN : OF_EINVAL,
+            "the gradient of %s must be non-NULL and 4-byte aligned", name);
+    REQUIRE(rows[k] >= 1, OF_EINVAL, "the gradient rows of %s must be >= 1", name);
+    CarryTensor& T = out->t[k];
+    T.p = *ts[k];
+    T.g = gs[k];
+    T.rows = rows[k];
+    T.ld = ts[k]->numel;
+    T.vec = rows[k] == 1 && aligned16(T.p.w) && aligned16(T.p.m) && aligned16(T.g) &&
+            (c->opt.kind == OF_OPT_SGD || aligned16(T.p.v)) &&
+            (T.p.w_bf16 == nullptr || (((uintptr_t)T.p.w_bf16) & 7u) == 0);
+  }
+  out->opt = make_optk(c->opt);
+  return OF_OK;
+}
+
 of_status check_linear(const of_linear_desc* d) {
   REQUIRE(d != nullptr, OF_EINVAL, "desc is NULL");
   REQUIRE(d->M >= 1 && d->N >= 1 && d->K >= 1, OF_EINVAL, "M, N, K must be >= 1 (got %lld %lld %lld)",
@@ -165,7 +195,7 @@ void set_weight_operand(const of_linear_desc* d, const of_param* W, GemmProblem&
 
 // Launch helpers shared by the entry points (arguments already validated).
 of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
-                  float* z, float* y, void* ws, hipStream_t s) {
+                  float* z, float* y, void* ws, hipStream_t s, const CarryArgs* carry = nullptr) {
   GemmProblem pr{x, ldx_of(d), 1, nullptr, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
   set_weight_operand(d, W, pr);
   EpiArgs ea = empty_epi();
@@ -173,6 +203,7 @@ of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, co
   ea.z = z; ea.ldz = ldy_of(d);
   ea.act = d->act;
   ea.bias = d->has_bias ? b : nullptr;
+  if (carry) ea.carry = *carry;
   return hip_status(gemm_dispatch(d, EPI_FWD, pr, ea, ws, s), "of_linear_fwd launch");
 }
 
@@ -292,6 +323,12 @@ size_t of_linear_workspace_size(const of_linear_desc* d, int32_t op) {
 
 of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
                         float* z, float* y, void* ws, size_t ws_bytes, void* stream) {
+  return of_linear_fwd_carry(d, x, W, b, z, y, nullptr, ws, ws_bytes, stream);
+}
+
+of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_param* W,
+                              const float* b, float* z, float* y, const of_carry* next,
+                              void* ws, size_t ws_bytes, void* stream) {
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
   REQUIRE(x && W && W->w && y, OF_EINVAL, "x, W, W->w and y are required");
@@ -302,7 +339,9 @@ of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param*
   REQUIRE((((uintptr_t)W->w_bf16) & 1u) == 0, OF_EALIGN, "W->w_bf16 must be 2-byte aligned");
   if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
-  return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream);
+  CarryArgs carry;
+  if ((st = make_carry(next, &carry)) != OF_OK) return st;
+  return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream, next ? &carry : nullptr);
 }
 
 // Largest M whose forward-fusion applies the update in the W-tile prologue.
@@ -445,6 +484,12 @@ size_t of_conv_workspace_size(const of_conv_desc* d, int32_t op) {
 
 of_status of_conv_fwd(const of_conv_desc* d, const float* x, const of_param* W, const float* b,
                       float* y, void* ws, size_t ws_bytes, void* stream) {
+  return of_conv_fwd_carry(d, x, W, b, y, nullptr, ws, ws_bytes, stream);
+}
+
+of_status of_conv_fwd_carry(const of_conv_desc* d, const float* x, const of_param* W,
+                            const float* b, float* y, const of_carry* next, void* ws,
+                            size_t ws_bytes, void* stream) {
   of_status st = check_conv(d);
   if (st != OF_OK) return st;
   REQUIRE(x && W && W->w && y, OF_EINVAL, "x, W, W->w and y are required");
@@ -453,6 +498,7 @@ of_status of_conv_fwd(const of_conv_desc* d, const float* x, const of_param* W, 
   REQUIRE(al4(x) && al4(W->w) && al4(b) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
   if ((st = check_conv_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
   EpiArgs ea = empty_epi();
+  if ((st = make_carry(next, &ea.carry)) != OF_OK) return st;
   ea.out = y; ea.ldo = d->Cout;
   ea.act = d->act;
   ea.bias = d->has_bias ? b : nullptr;

@@ -27,6 +27,8 @@ Orderings (Section 3, Fig. 1(b)-(d)):
 
 Torch is used for device memory, streams and events only.
 """
+import ctypes
+
 import numpy as np
 import torch
 
@@ -98,6 +100,30 @@ def _update(tr, p, stream):
     L.of_elementwise_fused_update(p.p, ptr, rows, ld, tr.opt, stream)
 
 
+def _self_update(tr, params):
+    """Forward-fusion of an operator no earlier launch carried: its pending
+    update as its own pass right before its forward (one launch for vector
+    gradients, a7 per row-partial gradient)."""
+    vec = [p for p in params if p.rows is None]
+    if vec:
+        arr = (L.OfParam * len(vec))(*[p.p for p in vec])
+        gp = (ctypes.c_void_p * len(vec))(*[p.g.data_ptr() for p in vec])
+        L.of_optimizer_step(len(vec), arr, gp, tr.opt, tr._s())
+    for p in params:
+        if p.rows is not None:
+            _update(tr, p, tr._s())
+
+
+def _carry_of(tr, params):
+    """of_carry of an operator's (at most two) parameters and pending gradients."""
+    (a, b) = (params[0], params[1] if len(params) > 1 else None)
+    pa = a.pending()
+    if b is None:
+        return L.make_carry(tr.opt, a.p, pa[0], pa[1])
+    pb = b.pending()
+    return L.make_carry(tr.opt, a.p, pa[0], pa[1], b.p, pb[0], pb[1])
+
+
 class LinearOp:
     """f = act(X W^T + b) on a [M, K] input (row stride ldx)."""
 
@@ -112,13 +138,21 @@ class LinearOp:
         self.updated = True
         self.params = [W] if b is None else [W, b]
         self.out_shape = (M, N)
+        # Forward-fusion: an fp32 layer with M <= 64 rows applies its pending
+        # update while its own W tiles load (one row tile covers M); any other
+        # layer has it carried by the previous operator's forward launch.
+        self.prologue_ff = dtype == L.OF_F32 and M <= 64
 
     def ws(self, which):
         return L.of_linear_workspace_size(self.desc, which)
 
-    def fwd(self, tr, x, y, z=None):
-        L.of_linear_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z, y,
-                        *tr.ws_main_args(), tr._s())
+    def fwd(self, tr, x, y, z=None, carry=None):
+        if carry is None:
+            L.of_linear_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z, y,
+                            *tr.ws_main_args(), tr._s())
+        else:
+            L.of_linear_fwd_carry(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z,
+                                  y, carry, *tr.ws_main_args(), tr._s())
 
     def fwd_ff(self, tr, x, y, z=None):
         b = self.b
@@ -167,16 +201,15 @@ class ConvOp:
     def ws(self, which):
         return L.of_conv_workspace_size(self.desc, which)
 
-    def fwd(self, tr, x, y):
-        L.of_conv_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, y,
-                      *tr.ws_main_args(), tr._s())
+    prologue_ff = False   # the filter-tile prologue is not fused: carried or own pass
 
-    def fwd_ff(self, tr, x, y):
-        # The pending update runs element-wise right before the forward; the
-        # filter-tile prologue of the convolution is not fused.
-        for p in self.params:
-            _update(tr, p, tr._s())
-        self.fwd(tr, x, y)
+    def fwd(self, tr, x, y, carry=None):
+        if carry is None:
+            L.of_conv_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, y,
+                          *tr.ws_main_args(), tr._s())
+        else:
+            L.of_conv_fwd_carry(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, y,
+                                carry, *tr.ws_main_args(), tr._s())
 
     def dgrad(self, tr, g, prev, act_prev, dx):
         L.of_conv_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
@@ -212,10 +245,7 @@ class LayerNormOp:
         L.of_layernorm_fwd(x, self.M, self.D, self.g.w.data_ptr(), self.b.w.data_ptr(), self.eps,
                            y, mu, rs, tr._s())
 
-    def fwd_ff(self, tr, x, y, mu, rs):
-        for p in self.params:
-            _update(tr, p, tr._s())
-        self.fwd(tr, x, y, mu, rs)
+    prologue_ff = False   # gamma and beta are carried by the previous launch, or updated first
 
     def bwd(self, tr, dy, x, mu, rs, dres, dx):
         """dx (+ dres) and the parameter-gradient row partials."""
@@ -292,16 +322,26 @@ class ChainNet:
 
     def forward(self, x, fused):
         tr = self.tr
+        n = len(self.ops)
         for i, op in enumerate(self.ops):
-            if fused and not op.updated:
+            if fused and not op.updated and op.prologue_ff:
                 tr._t0("fwd_ff", tr.stream, op)
                 op.fwd_ff(tr, self._in(i, x), self.y[i].data_ptr())
                 tr._t1("fwd_ff", tr.stream)
                 op.updated = True
             else:
+                if fused and not op.updated:
+                    _self_update(tr, op.params)   # no earlier launch carried it
+                    op.updated = True
+                nxt = self.ops[i + 1] if i + 1 < n else None
+                carry = None
+                if fused and nxt is not None and not nxt.updated and not nxt.prologue_ff:
+                    carry = _carry_of(tr, nxt.params)
                 tr._t0("fwd", tr.stream, op)
-                op.fwd(tr, self._in(i, x), self.y[i].data_ptr())
+                op.fwd(tr, self._in(i, x), self.y[i].data_ptr(), carry=carry)
                 tr._t1("fwd", tr.stream)
+                if carry is not None:
+                    nxt.updated = True   # its update is enqueued with this launch
             if self.pool[i]:
                 N, H, W, C = op.out_shape
                 L.of_maxpool2x2_fwd(self.y[i].data_ptr(), N, H, W, C, self.p[i].data_ptr(),
@@ -428,39 +468,48 @@ class TBlockNet:
         tr = self.tr
         d, n = self.d, self.M * self.d
         xin = x.data_ptr()
-        for blk in self.blocks:
-            for name in ("ln1", "qkv", "proj", "ln2", "fc1", "fc2"):
-                op = blk[name]
-                ff = fused and not op.updated
-                cls = "fwd_ff" if ff else "fwd"
-                tr._t0(cls, tr.stream, op)
-                if name == "ln1":
-                    (op.fwd_ff if ff else op.fwd)(tr, xin, blk["a"].data_ptr(),
-                                                  blk["mu1"].data_ptr(), blk["rs1"].data_ptr())
-                elif name == "qkv":
-                    (op.fwd_ff if ff else op.fwd)(tr, blk["a"].data_ptr(), blk["qkv_out"].data_ptr())
-                elif name == "proj":
-                    (op.fwd_ff if ff else op.fwd)(tr, blk["qkv_out"].data_ptr() + 8 * d,
-                                                  blk["o"].data_ptr())
-                elif name == "ln2":
-                    (op.fwd_ff if ff else op.fwd)(tr, blk["h"].data_ptr(), blk["c"].data_ptr(),
-                                                  blk["mu2"].data_ptr(), blk["rs2"].data_ptr())
-                elif name == "fc1":
-                    (op.fwd_ff if ff else op.fwd)(tr, blk["c"].data_ptr(), blk["g"].data_ptr(),
-                                                  blk["u"].data_ptr())
-                else:
-                    (op.fwd_ff if ff else op.fwd)(tr, blk["g"].data_ptr(), blk["w"].data_ptr())
-                tr._t1(cls, tr.stream)
-                if ff:
-                    op.updated = True
-                if name == "proj":
-                    tr._t0("add", tr.stream)
-                    L.of_add(xin, blk["o"].data_ptr(), n, blk["h"].data_ptr(), tr._s())
-                    tr._t1("add", tr.stream)
-            tr._t0("add", tr.stream)
-            L.of_add(blk["h"].data_ptr(), blk["w"].data_ptr(), n, blk["y"].data_ptr(), tr._s())
-            tr._t1("add", tr.stream)
-            xin = blk["y"].data_ptr()
+        order = [(b, name) for b in range(len(self.blocks))
+                 for name in ("ln1", "qkv", "proj", "ln2", "fc1", "fc2")]
+        for k, (bi, name) in enumerate(order):
+            blk = self.blocks[bi]
+            op = blk[name]
+            if fused and not op.updated:
+                _self_update(tr, op.params)   # no earlier launch carried it
+                op.updated = True
+            # a linear's launch carries the next operator's pending update
+            carry, nxt = None, None
+            if fused and name not in ("ln1", "ln2") and k + 1 < len(order):
+                nb, nn = order[k + 1]
+                nxt = self.blocks[nb][nn]
+                if not nxt.updated:
+                    carry = _carry_of(tr, nxt.params)
+            tr._t0("fwd", tr.stream, op)
+            if name == "ln1":
+                op.fwd(tr, xin, blk["a"].data_ptr(), blk["mu1"].data_ptr(), blk["rs1"].data_ptr())
+            elif name == "qkv":
+                op.fwd(tr, blk["a"].data_ptr(), blk["qkv_out"].data_ptr(), carry=carry)
+            elif name == "proj":
+                op.fwd(tr, blk["qkv_out"].data_ptr() + 8 * d, blk["o"].data_ptr(), carry=carry)
+            elif name == "ln2":
+                op.fwd(tr, blk["h"].data_ptr(), blk["c"].data_ptr(), blk["mu2"].data_ptr(),
+                       blk["rs2"].data_ptr())
+            elif name == "fc1":
+                op.fwd(tr, blk["c"].data_ptr(), blk["g"].data_ptr(), blk["u"].data_ptr(),
+                       carry=carry)
+            else:
+                op.fwd(tr, blk["g"].data_ptr(), blk["w"].data_ptr(), carry=carry)
+            tr._t1("fwd", tr.stream)
+            if carry is not None:
+                nxt.updated = True   # its update is enqueued with this launch
+            if name == "proj":       # h = x + attention output
+                tr._t0("add", tr.stream)
+                L.of_add(xin, blk["o"].data_ptr(), n, blk["h"].data_ptr(), tr._s())
+                tr._t1("add", tr.stream)
+            elif name == "fc2":      # y = h + MLP output, the next block's input
+                tr._t0("add", tr.stream)
+                L.of_add(blk["h"].data_ptr(), blk["w"].data_ptr(), n, blk["y"].data_ptr(), tr._s())
+                tr._t1("add", tr.stream)
+                xin = blk["y"].data_ptr()
 
     def _block_in(self, k, x):
         return x.data_ptr() if k == 0 else self.blocks[k - 1]["y"].data_ptr()

@@ -151,3 +151,27 @@ def test_bf16_shadow_and_norm_validation(lib):
     assert L.of_layernorm_partial_rows(4096) == 64 and L.of_layernorm_partial_rows(1) == 1
     assert _status(L.of_reduce_rows, FAKE, 2, 3, 8, FAKE, None) == L.OF_EINVAL   # ld < n
     assert _status(L.of_add, FAKE, None, 8, FAKE, None) == L.OF_EINVAL
+
+
+def test_carry_validation(lib):
+    """of_linear_fwd_carry / of_conv_fwd_carry reject a malformed carried update
+    before any HIP call (the forward's own arguments are valid)."""
+    d = _desc()
+    W = _param(16 * 12)
+    adam = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 1)
+
+    def fwd(carry):
+        return _status(L.of_linear_fwd_carry, d, FAKE, W, None, None, FAKE, carry, None, 0, None)
+
+    assert fwd(L.make_carry(adam, _param(0), FAKE)) == L.OF_EINVAL          # empty tensor
+    assert fwd(L.make_carry(adam, _param(8, v=None), FAKE)) == L.OF_EINVAL  # Adam needs v
+    assert fwd(L.make_carry(adam, _param(8), None)) == L.OF_EINVAL          # no gradient
+    assert fwd(L.make_carry(adam, _param(8), FAKE + 2)) == L.OF_EALIGN      # misaligned gradient
+    assert fwd(L.make_carry(adam, _param(8), FAKE, rows1=0)) == L.OF_EINVAL
+    bad = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 0)
+    assert fwd(L.make_carry(bad, _param(8), FAKE)) == L.OF_EINVAL           # step 0
+    assert fwd(L.make_carry(adam, _param(8), FAKE, t2=_param(4), g2=None)) == L.OF_EINVAL
+    cd = L.OfConvDesc(2, 4, 4, 3, 8, L.OF_ACT_RELU, 0)
+    Wc = _param(8 * 9 * 3)
+    assert _status(L.of_conv_fwd_carry, cd, FAKE, Wc, None, FAKE,
+                   L.make_carry(adam, _param(8), None), FAKE, 1 << 20, None) == L.OF_EINVAL

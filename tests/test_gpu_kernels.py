@@ -46,6 +46,8 @@ SHAPES = [  # (M, N, K): tails in every dimension, split reductions, tiny and wi
     (130, 96, 44), (300, 70, 257), (64, 2048, 4096), (1, 5, 3),
     # direct-load 32x32 tiles with tails: scalar loads (K % 4 != 0), partial blocks
     (300, 1030, 1001), (290, 1028, 1100),
+    # few output tiles and a long reduction: direct tiles with a split
+    (100, 50, 3000), (200, 30, 2050),
 ]
 
 
