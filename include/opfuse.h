@@ -116,23 +116,22 @@ typedef struct of_param {
 } of_param;
 
 /*
- * A pending update carried by a forward launch (forward-fusion of a later
- * operator, Appendix B.1, Alg. 2): up to two tensors, each with its pending
- * gradient, updated with `opt` by extra workgroups of the forward's kernel.
- * A gradient is one vector of numel elements (rows == 1) or `rows` row
- * partials [rows, numel] summed in row order (a LayerNorm parameter's
- * gradient).  t2.w == NULL: one tensor.  Every element gets exactly the
+ * Pending updates carried by a forward launch (forward-fusion of later
+ * operators, Appendix B.1, Alg. 2): n tensors (1 <= n <= OF_CARRY_MAX), each
+ * with its pending gradient g[i], updated with `opt` by extra workgroups of
+ * the forward's kernel.  A gradient is one vector of numel elements
+ * (rows[i] == 1) or rows[i] row partials [rows, numel] summed in row order (a
+ * LayerNorm parameter's gradient).  Every element gets exactly the
  * operations of of_optimizer_step (vector) or of_elementwise_fused_update
  * (rows), so results are bit-identical to those passes.  The carried tensors
- * must not overlap anything the forward reads or writes.
+ * must not overlap each other or anything the forward reads or writes.
  */
+#define OF_CARRY_MAX 4
 typedef struct of_carry {
-  of_param t1;
-  const float* g1;
-  int64_t rows1;
-  of_param t2;
-  const float* g2;
-  int64_t rows2;
+  int32_t n;
+  of_param t[OF_CARRY_MAX];
+  const float* g[OF_CARRY_MAX];
+  int64_t rows[OF_CARRY_MAX];
   of_opt opt;
 } of_carry;
 

@@ -38,9 +38,12 @@ class OfParam(ctypes.Structure):
                 ("numel", c_int64)]
 
 
+OF_CARRY_MAX = 4
+
+
 class OfCarry(ctypes.Structure):
-    _fields_ = [("t1", OfParam), ("g1", c_void_p), ("rows1", c_int64),
-                ("t2", OfParam), ("g2", c_void_p), ("rows2", c_int64), ("opt", OfOpt)]
+    _fields_ = [("n", c_int32), ("t", OfParam * OF_CARRY_MAX), ("g", c_void_p * OF_CARRY_MAX),
+                ("rows", c_int64 * OF_CARRY_MAX), ("opt", OfOpt)]
 
 
 class OfLinearDesc(ctypes.Structure):
@@ -189,10 +192,17 @@ def make_opt(hyper, step, step_dev=None):
                  hyper.get("eps", 0.0), step, step_dev)
 
 
-def make_carry(opt, t1, g1, rows1=1, t2=None, g2=None, rows2=1):
-    """of_carry: tensor t1 (an OfParam) with gradient g1 (device pointer; `rows1`
-    row partials), and optionally t2 / g2."""
-    return OfCarry(t1, g1, rows1, t2 if t2 is not None else OfParam(), g2, rows2, opt)
+def make_carry(opt, tensors):
+    """of_carry of [(OfParam, gradient device pointer, rows), ...] (at most
+    OF_CARRY_MAX), all updated with `opt`."""
+    c = OfCarry()
+    c.n = len(tensors)
+    for i, (p, g, rows) in enumerate(tensors):
+        c.t[i] = p
+        c.g[i] = g
+        c.rows[i] = rows
+    c.opt = opt
+    return c
 
 
 def param_of(w, m, v=None, w_bf16=None):

@@ -198,10 +198,11 @@ struct GemmProblem {
   FastDiv dW, dH, dC, dCout;    // convolution: divisors of the gather index arithmetic
 };
 
-// An update carried by a contraction launch (forward-fusion of a later
-// operator): the workgroups of the z-slices from z0 on apply the optimizer to
-// up to two tensors instead of computing tiles.  A tensor's gradient is one
-// vector (rows == 1) or `rows` row partials of stride `ld`, summed in row order.
+// Updates carried by a contraction launch (forward-fusion of later
+// operators): the workgroups of the z-slices from z0 on apply the optimizer to
+// up to OF_CARRY_MAX tensors instead of computing tiles.  A tensor's gradient
+// is one vector (rows == 1) or `rows` row partials of stride `ld`, summed in
+// row order.
 struct CarryTensor {
   of_param p;           // p.w == nullptr: no tensor
   const float* g;
@@ -209,7 +210,7 @@ struct CarryTensor {
   int vec;              // 128-bit paths allowed (vector gradients)
 };
 struct CarryArgs {
-  CarryTensor t[2];
+  CarryTensor t[OF_CARRY_MAX];
   OptK opt;
   int z0;               // z-slices of the contraction itself; 0: nothing carried
 };

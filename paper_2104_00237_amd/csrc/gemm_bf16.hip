@@ -209,9 +209,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
   constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
   __shared__ __attribute__((aligned(16))) unsigned char smem_raw[T::SMX];
   uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
-  if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
-    carry_update(ea.carry);  // a later operator's update rides on this launch
-    return;
+  if constexpr (EPI == EPI_FWD) {
+    if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+      carry_update(ea.carry);  // a later operator's update rides on this launch
+      return;
+    }
   }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -469,7 +471,7 @@ hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_i
   BCfg c = bselect(kind, pr.P, pr.Q, pr.R);
   EpiArgs ea = ea_in;
   ea.carry.z0 = 0;
-  if (ea.carry.t[0].p.w || ea.carry.t[1].p.w) {
+  if (ea.carry.t[0].p.w) {
     if (kind != EPI_FWD) return hipErrorInvalidValue;  // only a forward carries an update
     c.cz = carry_slices(ea.carry, bntiles(c.tile, pr.P, pr.Q));
     ea.carry.z0 = c.S;

@@ -75,7 +75,10 @@ __device__ __forceinline__ void carry_update(const CarryArgs& c) {
   const int64_t slice = (int64_t)gridDim.x * gridDim.y;
   const int64_t u = ((int64_t)(blockIdx.z - c.z0) * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
   const int64_t U = (int64_t)(gridDim.z - c.z0) * slice;
-  for (int k = 0; k < 2; ++k) {
+  // (unrolled: the tensors are indexed statically, so the arguments stay in
+  // scalar registers instead of being copied to per-lane scratch)
+#pragma unroll
+  for (int k = 0; k < OF_CARRY_MAX; ++k) {
     const CarryTensor& T = c.t[k];
     if (T.p.w == nullptr) continue;
     const int64_t n = T.p.numel;
@@ -109,7 +112,7 @@ __device__ __forceinline__ void carry_update(const CarryArgs& c) {
 // gradient, an element of a rows gradient), at most 256 workgroups.
 inline int carry_slices(const CarryArgs& c, int64_t slice) {
   int64_t items = 0;
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < OF_CARRY_MAX; ++k) {
     const CarryTensor& T = c.t[k];
     if (T.p.w == nullptr) continue;
     items += T.rows == 1 ? (T.p.numel + 3) / 4 : T.p.numel;

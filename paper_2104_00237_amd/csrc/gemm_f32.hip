@@ -313,9 +313,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   constexpr int SMEM = T::SMX + (EPI == EPI_FWD_FF ? T::BQ : 0);
   static_assert(SMEM * 4 <= 64 * 1024, "LDS per workgroup");
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
-  if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
-    carry_update(ea.carry);  // a later operator's update rides on this launch
-    return;
+  if constexpr (EPI == EPI_FWD) {
+    if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+      carry_update(ea.carry);  // a later operator's update rides on this launch
+      return;
+    }
   }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -568,9 +570,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, Ep
   constexpr bool B_RC = (EPI == EPI_FWD);  // dgrad: W is output-contiguous
   constexpr int KB = 16;                   // reduction elements per block
   __shared__ __attribute__((aligned(16))) float Cs[NW * 32 * 32];
-  if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
-    carry_update(ea.carry);  // a later operator's update rides on this launch
-    return;
+  if constexpr (EPI == EPI_FWD) {
+    if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+      carry_update(ea.carry);  // a later operator's update rides on this launch
+      return;
+    }
   }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -970,7 +974,7 @@ hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, vo
   GemmCfg c = select_cfg(kind, pr.P, pr.Q, pr.R, pr.conv);
   EpiArgs ea = ea_in;
   ea.carry.z0 = 0;
-  if (ea.carry.t[0].p.w || ea.carry.t[1].p.w) {
+  if (ea.carry.t[0].p.w) {
     if (kind != EPI_FWD) return hipErrorInvalidValue;  // only a forward carries an update
     c.cz = carry_slices(ea.carry, ntiles(c.tile, pr.P, pr.Q));
     ea.carry.z0 = c.S;

@@ -73,25 +73,25 @@ of_status check_param(const of_param* p, const char* name, int64_t numel, int ki
 of_status make_carry(const of_carry* c, CarryArgs* out) {
   memset(out, 0, sizeof(*out));
   if (c == nullptr) return OF_OK;
+  REQUIRE(c->n >= 1 && c->n <= OF_CARRY_MAX, OF_EINVAL, "next->n is %d, not in [1, %d]",
+          (int)c->n, OF_CARRY_MAX);
   of_status st = check_opt(&c->opt);
   if (st != OF_OK) return st;
-  const of_param* ts[2] = {&c->t1, &c->t2};
-  const float* gs[2] = {c->g1, c->g2};
-  const int64_t rows[2] = {c->rows1, c->rows2};
-  for (int k = 0; k < 2; ++k) {
-    if (k == 1 && c->t2.w == nullptr) break;
-    const char* name = k == 0 ? "next->t1" : "next->t2";
-    REQUIRE(ts[k]->numel >= 1, OF_EINVAL, "%s->numel must be >= 1", name);
-    if ((st = check_param(ts[k], name, ts[k]->numel, c->opt.kind, true)) != OF_OK) return st;
-    REQUIRE(gs[k] != nullptr && al4(gs[k]), gs[k] ? OF_EALIGN : OF_EINVAL,
-            "the gradient of %s must be non-NULL and 4-byte aligned", name);
-    REQUIRE(rows[k] >= 1, OF_EINVAL, "the gradient rows of %s must be >= 1", name);
+  for (int k = 0; k < c->n; ++k) {
+    char name[24];
+    snprintf(name, sizeof(name), "next->t[%d]", k);
+    const of_param& P = c->t[k];
+    REQUIRE(P.numel >= 1, OF_EINVAL, "%s.numel must be >= 1", name);
+    if ((st = check_param(&P, name, P.numel, c->opt.kind, true)) != OF_OK) return st;
+    REQUIRE(c->g[k] != nullptr, OF_EINVAL, "next->g[%d] is NULL", k);
+    REQUIRE(al4(c->g[k]), OF_EALIGN, "next->g[%d] must be 4-byte aligned", k);
+    REQUIRE(c->rows[k] >= 1, OF_EINVAL, "next->rows[%d] must be >= 1", k);
     CarryTensor& T = out->t[k];
-    T.p = *ts[k];
-    T.g = gs[k];
-    T.rows = rows[k];
-    T.ld = ts[k]->numel;
-    T.vec = rows[k] == 1 && aligned16(T.p.w) && aligned16(T.p.m) && aligned16(T.g) &&
+    T.p = P;
+    T.g = c->g[k];
+    T.rows = c->rows[k];
+    T.ld = P.numel;
+    T.vec = T.rows == 1 && aligned16(T.p.w) && aligned16(T.p.m) && aligned16(T.g) &&
             (c->opt.kind == OF_OPT_SGD || aligned16(T.p.v)) &&
             (T.p.w_bf16 == nullptr || (((uintptr_t)T.p.w_bf16) & 7u) == 0);
   }

@@ -115,13 +115,8 @@ def _self_update(tr, params):
 
 
 def _carry_of(tr, params):
-    """of_carry of an operator's (at most two) parameters and pending gradients."""
-    (a, b) = (params[0], params[1] if len(params) > 1 else None)
-    pa = a.pending()
-    if b is None:
-        return L.make_carry(tr.opt, a.p, pa[0], pa[1])
-    pb = b.pending()
-    return L.make_carry(tr.opt, a.p, pa[0], pa[1], b.p, pb[0], pb[1])
+    """of_carry of parameters (at most OF_CARRY_MAX) with their pending gradients."""
+    return L.make_carry(tr.opt, [(p.p, p.pending()[0], p.pending()[1]) for p in params])
 
 
 class LinearOp:
@@ -476,13 +471,23 @@ class TBlockNet:
             if fused and not op.updated:
                 _self_update(tr, op.params)   # no earlier launch carried it
                 op.updated = True
-            # a linear's launch carries the next operator's pending update
-            carry, nxt = None, None
-            if fused and name not in ("ln1", "ln2") and k + 1 < len(order):
-                nb, nn = order[k + 1]
-                nxt = self.blocks[nb][nn]
-                if not nxt.updated:
-                    carry = _carry_of(tr, nxt.params)
+            # A linear's launch carries the next operators' pending updates: the
+            # next one, and through a LayerNorm (whose kernel carries nothing)
+            # the one after it too.
+            carry, carried = None, []
+            if fused and name not in ("ln1", "ln2"):
+                k2 = k + 1
+                while k2 < len(order) and len(carried) < 2:
+                    nb, nn = order[k2]
+                    nxt = self.blocks[nb][nn]
+                    if nxt.updated:
+                        break
+                    carried.append(nxt)
+                    if nn not in ("ln1", "ln2"):
+                        break
+                    k2 += 1
+                if carried:
+                    carry = _carry_of(tr, [p for o in carried for p in o.params])
             tr._t0("fwd", tr.stream, op)
             if name == "ln1":
                 op.fwd(tr, xin, blk["a"].data_ptr(), blk["mu1"].data_ptr(), blk["rs1"].data_ptr())
@@ -499,8 +504,8 @@ class TBlockNet:
             else:
                 op.fwd(tr, blk["g"].data_ptr(), blk["w"].data_ptr(), carry=carry)
             tr._t1("fwd", tr.stream)
-            if carry is not None:
-                nxt.updated = True   # its update is enqueued with this launch
+            for o in carried:
+                o.updated = True     # their updates are enqueued with this launch
             if name == "proj":       # h = x + attention output
                 tr._t0("add", tr.stream)
                 L.of_add(xin, blk["o"].data_ptr(), n, blk["h"].data_ptr(), tr._s())

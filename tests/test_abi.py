@@ -163,15 +163,19 @@ def test_carry_validation(lib):
     def fwd(carry):
         return _status(L.of_linear_fwd_carry, d, FAKE, W, None, None, FAKE, carry, None, 0, None)
 
-    assert fwd(L.make_carry(adam, _param(0), FAKE)) == L.OF_EINVAL          # empty tensor
-    assert fwd(L.make_carry(adam, _param(8, v=None), FAKE)) == L.OF_EINVAL  # Adam needs v
-    assert fwd(L.make_carry(adam, _param(8), None)) == L.OF_EINVAL          # no gradient
-    assert fwd(L.make_carry(adam, _param(8), FAKE + 2)) == L.OF_EALIGN      # misaligned gradient
-    assert fwd(L.make_carry(adam, _param(8), FAKE, rows1=0)) == L.OF_EINVAL
+    assert fwd(L.make_carry(adam, [])) == L.OF_EINVAL                      # n = 0
+    over = L.make_carry(adam, [(_param(8), FAKE, 1)])
+    over.n = L.OF_CARRY_MAX + 1
+    assert fwd(over) == L.OF_EINVAL                                        # n > max
+    assert fwd(L.make_carry(adam, [(_param(0), FAKE, 1)])) == L.OF_EINVAL  # empty tensor
+    assert fwd(L.make_carry(adam, [(_param(8, v=None), FAKE, 1)])) == L.OF_EINVAL  # Adam needs v
+    assert fwd(L.make_carry(adam, [(_param(8), None, 1)])) == L.OF_EINVAL  # no gradient
+    assert fwd(L.make_carry(adam, [(_param(8), FAKE + 2, 1)])) == L.OF_EALIGN
+    assert fwd(L.make_carry(adam, [(_param(8), FAKE, 0)])) == L.OF_EINVAL  # rows 0
+    assert fwd(L.make_carry(adam, [(_param(8), FAKE, 1), (_param(4), None, 1)])) == L.OF_EINVAL
     bad = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 0)
-    assert fwd(L.make_carry(bad, _param(8), FAKE)) == L.OF_EINVAL           # step 0
-    assert fwd(L.make_carry(adam, _param(8), FAKE, t2=_param(4), g2=None)) == L.OF_EINVAL
+    assert fwd(L.make_carry(bad, [(_param(8), FAKE, 1)])) == L.OF_EINVAL  # step 0
     cd = L.OfConvDesc(2, 4, 4, 3, 8, L.OF_ACT_RELU, 0)
     Wc = _param(8 * 9 * 3)
     assert _status(L.of_conv_fwd_carry, cd, FAKE, Wc, None, FAKE,
-                   L.make_carry(adam, _param(8), None), FAKE, 1 << 20, None) == L.OF_EINVAL
+                   L.make_carry(adam, [(_param(8), None, 1)]), FAKE, 1 << 20, None) == L.OF_EINVAL

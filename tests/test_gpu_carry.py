@@ -68,12 +68,8 @@ class _T:
                 assert torch.equal(a[k], b[k]), k
 
 
-def _carry(L, opt, t1, t2=None):
-    c1 = t1.copies[0]
-    if t2 is None:
-        return L.make_carry(opt, c1["p"], c1["g"], t1.rows)
-    c2 = t2.copies[0]
-    return L.make_carry(opt, c1["p"], c1["g"], t1.rows, c2["p"], c2["g"], t2.rows)
+def _carry(L, opt, *ts):
+    return L.make_carry(opt, [(t.copies[0]["p"], t.copies[0]["g"], t.rows) for t in ts])
 
 
 CASES = [  # (M, N, K, dtype): direct tiles, staged tiles, split reduction, bf16
@@ -115,7 +111,8 @@ def test_linear_fwd_carry_bits(env, M, N, K, dt, kind):
 
 @pytest.mark.parametrize("rows", [1, 5, 64])
 def test_linear_fwd_carry_rows(env, rows):
-    """A LayerNorm-style pair of vectors with row-partial gradients."""
+    """A LayerNorm-style pair of vectors with row-partial gradients, and the next
+    layer's weight and bias with vector gradients (four carried tensors)."""
     torch, L, dev = env
     M, N, K = 256, 1024, 1024
     X = torch.randn(M, K, device=dev)
@@ -129,16 +126,18 @@ def test_linear_fwd_carry_rows(env, rows):
     opt = L.make_opt(HYPERS["adamw"], 2)
     gam = _T(torch, L, dev, 1024, "adamw", 3, rows=rows)
     bet = _T(torch, L, dev, 1024, "adamw", 4, rows=rows)
+    w2 = _T(torch, L, dev, 4096 * 1024, "adamw", 7, shadow=True)
+    b2 = _T(torch, L, dev, 4096, "adamw", 8)
     L.of_linear_fwd(d, X.data_ptr(), Wp, None, None, Y0.data_ptr(), ws.data_ptr(),
                     ws.numel() * 4, 0)
-    gam.reference_update(L, opt)
-    bet.reference_update(L, opt)
+    for t in (gam, bet, w2, b2):
+        t.reference_update(L, opt)
     L.of_linear_fwd_carry(d, X.data_ptr(), Wp, None, None, Y1.data_ptr(),
-                          _carry(L, opt, gam, bet), ws.data_ptr(), ws.numel() * 4, 0)
+                          _carry(L, opt, gam, bet, w2, b2), ws.data_ptr(), ws.numel() * 4, 0)
     torch.cuda.synchronize()
     assert torch.equal(Y0, Y1)
-    gam.same(torch)
-    bet.same(torch)
+    for t in (gam, bet, w2, b2):
+        t.same(torch)
 
 
 @pytest.mark.parametrize("N,H,C,Co", [(8, 16, 64, 128), (128, 4, 256, 512), (4, 7, 3, 16)])
