@@ -55,8 +55,8 @@ struct BTile {
   static_assert(SMX <= 64 * 1024, "LDS per workgroup");
 };
 
-using BT128x128 = BTile<128, 128, 32, 2, 2, 2>;
-using BT64x64 = BTile<64, 64, 32, 2, 2, 3>;
+using BT128x128 = BTile<128, 128, 32, 2, 2, 4>;
+using BT64x64 = BTile<64, 64, 32, 2, 2, 4>;
 
 enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_COUNT };
 static const int kBTileBP[BTI_COUNT] = {64, 128};
