@@ -378,14 +378,20 @@ static int64_t bntiles(int t, int P, int Q) {
 }
 
 // 128x128 tiles when the output has enough of them, else 64x64; the reduction
-// is split until there are about 256 workgroups (at least 4 chunks per split).
+// is split until there are about 256 workgroups, and for a forward until no
+// split spans more than 2048 elements (at least 4 chunks per split).
 // The eager and backward-fusion weight gradients share this rule.
 static BCfg bselect_default(int kind, int P, int Q, int R) {
-  (void)kind;
   const int t = bntiles(BTI_128x128, P, Q) >= 64 ? BTI_128x128 : BTI_64x64;
   const int BR = kBTileBR[t];
   const int64_t nt = bntiles(t, P, Q);
   int S = (int)std::max<int64_t>(1, (256 + nt - 1) / nt);
+  // A forward with a long reduction splits further, to at most 2048 elements
+  // per split (measured on MI355X at 4096 tokens).  The gradients keep the
+  // plain rule: backward-fusion runs them beside each other on two streams,
+  // where the extra workgroups and second passes cost more than they save.
+  if (kind == EPI_FWD)
+    while (S < 8 && (R + S - 1) / S > 2048) S *= 2;
   S = std::min(S, std::min(8, std::max(1, R / (4 * BR))));
   int r_split = (((R + S - 1) / S) + BR - 1) / BR * BR;
   S = (R + r_split - 1) / r_split;
