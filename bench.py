@@ -348,19 +348,20 @@ def main():
     by_shape = {}
     for d_ms, op in recs:
         if op is not None:
-            by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name))
+            by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name, op))
     costed = [k for k in by_shape if launches[by_shape[k][0][1]].get(dom)]
-    shape = max(costed, key=lambda s: sum(d for d, _ in by_shape[s]))
-    durs = [d for d, _ in by_shape[shape]]
+    shape = max(costed, key=lambda s: sum(d for d, _, _ in by_shape[s]))
+    durs = [d for d, _, _ in by_shape[shape]]
     per = launches[by_shape[shape][0][1]][dom]
     # Each launch is bracketed by an event pair on its own stream; the pair's own
     # cost (an empty pair on the same stream) is taken off.
     from paper_2104_00237_amd.trainer import KernelTimer
-    dom_stream = torch.cuda.Stream() if dom == "wgrad_bf" else torch.cuda.current_stream()
+    on_side = dom == "wgrad_bf" and getattr(by_shape[shape][0][2], "overlap_update", False)
+    dom_stream = torch.cuda.Stream() if on_side else torch.cuda.current_stream()
     marker_ms = KernelTimer.marker_overhead_ms(dom_stream)
     avg_s = (float(np.mean(durs)) - marker_ms) / 1e3
     roof = kernel_roofline(per[0], per[1], avg_s, mfma_peak(cfg))
-    roof.update(kernel=dom, layers=sorted({n for _, n in by_shape[shape]}),
+    roof.update(kernel=dom, layers=sorted({n for _, n, _ in by_shape[shape]}),
                 shape=f"{shape[0]} GEMM M={shape[1]} N={shape[2]} K={shape[3]}",
                 avg_us=round(avg_s * 1e6, 3), launches=len(durs),
                 bracketed_avg_us=round(float(np.mean(durs)) * 1e3, 3),
