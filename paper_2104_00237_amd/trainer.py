@@ -945,15 +945,30 @@ class KernelTimer:
         return out
 
     @staticmethod
-    def marker_overhead_ms(stream, samples=50):
-        """Mean elapsed time of an event pair with nothing between it on `stream`:
-        the cost of the markers themselves, which bracketing a kernel adds."""
-        pairs = []
-        for _ in range(samples):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            e1.record(stream)
-            pairs.append((e0, e1))
-        torch.cuda.synchronize()
-        return float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+    def marker_overhead_ms(stream, samples=40):
+        """What an event pair adds to the time it brackets on `stream`, taken as a
+        bracketed launch sees it: pairs queued behind work around one and around
+        two back-to-back launches of the same copy kernel (medians B1, B2).
+        B1 = c + k and B2 = c + 2k + g give 2*B1 - B2 = c - g, so a bracketed
+        time minus this is the kernel's duration plus one back-to-back gap (an
+        empty pair on an idle stream costs more than a pair around a launch)."""
+        a = torch.empty(1 << 22, device=torch.cuda.current_device())
+        b = torch.empty_like(a)
+
+        def bracket(nk):
+            pairs = []
+            with torch.cuda.stream(stream):
+                for _ in range(samples):
+                    b.copy_(a)   # the pair is queued behind work, as in a step
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    for _ in range(nk):
+                        b.copy_(a)
+                    e1.record(stream)
+                    pairs.append((e0, e1))
+            torch.cuda.synchronize()
+            return float(np.median([x.elapsed_time(y) for x, y in pairs]))
+
+        bracket(1)   # warm
+        return max(0.0, 2.0 * bracket(1) - bracket(2))
