@@ -40,7 +40,8 @@ template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int NS_>
 struct BTile {
   static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_;
   static constexpr int NS = NS_;   // operand chunks in the register ring
-  static_assert(WP * WQ == 4, "a workgroup is 4 wavefronts");
+  static constexpr int NW = WP * WQ, NT = 64 * NW;
+  static_assert(NW == 4 || NW == 8, "a workgroup is 4 or 8 wavefronts");
   static_assert(BR % 16 == 0, "whole MFMA reduction steps");
   static constexpr int WTP = BP / WP, WTQ = BQ / WQ;
   static constexpr int TP = WTP / 32, TQ = WTQ / 32;
@@ -49,19 +50,39 @@ struct BTile {
   static constexpr int PLA = BP * 8 + 8, PLB = BQ * 8 + 8;
   static constexpr int STAGE = (BR / 8) * (PLA + PLB);          // bf16 elements per stage
   static constexpr int SM_MAIN = 2 * STAGE * 2;                  // bytes, two stages
-  static constexpr int LDC = (BP * (BQ + 4) * 4 <= 60 * 1024) ? BQ + 4 : BQ;
-  static constexpr int SM_C = BP * LDC * 4;                      // bytes
+  // The fp32 accumulators are staged through LDS for the epilogue in NPASS
+  // bands of PR rows, each band at most 64 KB with rows padded by 4 floats.
+  static constexpr int LDC = BQ + 4;
+  static constexpr int NPASS = (BP * LDC * 4 <= 65536)       ? 1
+                               : ((BP / 2) * LDC * 4 <= 65536) ? 2
+                               : ((BP / 4) * LDC * 4 <= 65536) ? 4 : 8;
+  static constexpr int PR = BP / NPASS;
+  static_assert(PR % 32 == 0, "a band holds whole 32-row MFMA blocks");
+  static constexpr int SM_C = PR * LDC * 4;                      // bytes
   static constexpr int SMX = SM_MAIN > SM_C ? SM_MAIN : SM_C;
-  static_assert(SMX <= 64 * 1024, "LDS per workgroup");
+  static_assert(SMX <= 160 * 1024, "LDS per workgroup");
 };
 
 using BT128x128 = BTile<128, 128, 32, 2, 2, 4>;
 using BT64x64 = BTile<64, 64, 32, 2, 2, 4>;
-
-enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_COUNT };
-static const int kBTileBP[BTI_COUNT] = {64, 128};
-static const int kBTileBQ[BTI_COUNT] = {64, 128};
-static const int kBTileBR[BTI_COUNT] = {32, 32};
+// Eight wavefronts (two per SIMD, each on a 64x64 sub-tile) share one A tile
+// over 256 output columns, so each A byte fetched feeds twice the outputs.
+using BT128x256 = BTile<128, 256, 64, 2, 4, 2>;
+#ifdef OPFUSE_TUNING
+using BT128x128R64 = BTile<128, 128, 64, 2, 2, 2>;
+using BT128x256R32 = BTile<128, 256, 32, 2, 4, 4>;
+using BT256x128 = BTile<256, 128, 32, 4, 2, 4>;
+enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_128x256, BTI_128x128R64, BTI_128x256R32,
+               BTI_256x128, BTI_COUNT };
+static const int kBTileBP[BTI_COUNT] = {64, 128, 128, 128, 128, 256};
+static const int kBTileBQ[BTI_COUNT] = {64, 128, 256, 128, 256, 128};
+static const int kBTileBR[BTI_COUNT] = {32, 32, 64, 64, 32, 32};
+#else
+enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_128x256, BTI_COUNT };
+static const int kBTileBP[BTI_COUNT] = {64, 128, 128};
+static const int kBTileBQ[BTI_COUNT] = {64, 128, 256};
+static const int kBTileBR[BTI_COUNT] = {32, 32, 64};
+#endif
 
 // Two fp32 values to packed bf16, round to nearest even (one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t cvt2(float a, float b) {
@@ -90,20 +111,27 @@ __device__ __forceinline__ uint32_t bload_u16(rsrc_t r, uint32_t off) {
 // its global loads and its LDS store.  RC: the reduction index is contiguous
 // in memory.  BF: the source holds bf16 (else fp32).  VEC: 128-bit (fp32) or
 // 64-bit (bf16) loads are allowed: aligned base, strides a multiple of 4
-// elements and the contiguous extent ending on a quad boundary.
+// elements and the contiguous extent ending on a quad boundary (for a bf16
+// source with a contiguous reduction index: 16-byte aligned, strides and
+// extent multiples of 8, loaded as 128-bit octets).
 // An item is a quad along r (RC) or a 4 x 4 block (r, x) (not RC).
-template <int BX, int BR, bool RC, bool BF, bool VEC>
+template <int BX, int BR, bool RC, bool BF, bool VEC, int NT>
 struct BLoad {
-  static constexpr int NQ = RC ? BX * (BR / 4) : (BR / 4) * (BX / 4);  // items
-  static constexpr int PER = (NQ + 255) / 256;
+  // A bf16 source with a contiguous reduction index moves 8 elements (one
+  // 16-byte load, one 16-byte LDS store) per item when vector loads are allowed.
+  static constexpr bool W8 = RC && BF && VEC;
+  static constexpr int QW = W8 ? 8 : 4;          // reduction elements per RC item
+  static constexpr int NQ = RC ? BX * (BR / QW) : (BR / 4) * (BX / 4);  // items
+  static constexpr int PER = (NQ + NT - 1) / NT;
   static constexpr int NV = RC ? 1 : 4;          // vectors per item
   static constexpr int PL = BX * 8 + 8;          // plane stride (bf16 elements)
-  // raw data: fp32 float4 or bf16 quads (as uint2), NV per item
+  // raw data: fp32 float4, bf16 quads (as uint2) or bf16 octets (as uint4)
   float4 f[BF ? 1 : PER][BF ? 1 : NV];
-  uint2 h[BF ? PER : 1][BF ? NV : 1];
+  uint2 h[(BF && !W8) ? PER : 1][(BF && !W8) ? NV : 1];
+  uint4 o[W8 ? PER : 1];
 
   __device__ __forceinline__ static void coords(int idx, int& x, int& r) {
-    if (RC) { x = idx / (BR / 4); r = (idx % (BR / 4)) * 4; }
+    if (RC) { x = idx / (BR / QW); r = (idx % (BR / QW)) * QW; }
     else    { r = (idx / (BX / 4)) * 4; x = (idx % (BX / 4)) * 4; }
   }
 
@@ -113,10 +141,18 @@ struct BLoad {
     const rsrc_t rs = make_rsrc((const char*)tensor + ((int64_t)x0 * s_x + (int64_t)r0 * s_r) * ES);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int idx = tid + i * 256;
+      const int idx = tid + i * NT;
       int x, r;
       coords(idx, x, r);
-      const bool live = idx < NQ;
+      const bool live = (NQ % NT == 0) || idx < NQ;
+      if constexpr (W8) {
+        // vector loads of a bf16 operand need the reduction extent to be a
+        // multiple of 8, so an octet is whole or absent
+        const bool ok = live && x < nx && r < nr;
+        const uint32_t off = ok ? (uint32_t)((x * s_x + r) * 2) : kOOB;
+        o[i] = __builtin_bit_cast(uint4, bload4(rs, off));
+        continue;
+      }
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
         // vector j: RC -> the quad (x, r..r+3); else the quad (x..x+3, r+j)
@@ -156,12 +192,14 @@ struct BLoad {
   __device__ __forceinline__ void store(uint16_t* lds, int tid) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int idx = tid + i * 256;
-      if (idx >= NQ) continue;
+      const int idx = tid + i * NT;
+      if (NQ % NT != 0 && idx >= NQ) continue;
       int x, r;
       coords(idx, x, r);
       const int plane = r >> 3, slot = r & 7;   // slot is 0 or 4
-      if (RC) {
+      if constexpr (W8) {
+        *reinterpret_cast<uint4*>(&lds[plane * PL + swz(x) * 8]) = o[i];
+      } else if (RC) {
         uint2 q;
         if constexpr (BF) q = h[i][0];
         else q = pack_bf16x4(f[i][0].x, f[i][0].y, f[i][0].z, f[i][0].w);
@@ -200,8 +238,8 @@ struct BLoad {
 // Operand roles per contraction (see the fp32 kernels): forward A = X (RC),
 // B = W (RC); data gradient A = dZ (RC), B = W (output-contiguous); weight
 // gradient A = dZ, B = X (both output-contiguous).
-template <class T, int EPI, bool VA, bool VB, bool BBF>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs ea, int r_split,
+template <class T, int EPI, bool VA, bool VB, bool BBF, bool ABF>
+__global__ __launch_bounds__(T::NT) void gemm_bf16_kernel(GemmProblem pr, EpiArgs ea, int r_split,
                                                         float* partial, int vec_epi) {
   if (EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
   constexpr bool A_RC = (EPI == EPI_FWD || EPI == EPI_DGRAD);
@@ -211,7 +249,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
   uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
   if constexpr (EPI == EPI_FWD) {
     if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
-      carry_update(ea.carry);  // a later operator's update rides on this launch
+      carry_update<T::NT>(ea.carry);  // a later operator's update rides on this launch
       return;
     }
   }
@@ -227,8 +265,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
   const bool do_db = WG && ea.with_db && ty == 0;
 
-  using LA = BLoad<T::BP, T::BR, A_RC, false, VA>;
-  using LB = BLoad<T::BQ, T::BR, B_RC, BBF, VB>;
+  static_assert(!ABF || EPI == EPI_FWD, "a bf16 A operand only in a forward");
+  using LA = BLoad<T::BP, T::BR, A_RC, ABF, VA, T::NT>;
+  using LB = BLoad<T::BQ, T::BR, B_RC, BBF, VB, T::NT>;
   constexpr int NS = T::NS;
   LA la[NS];
   LB lb[NS];
@@ -298,41 +337,49 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
   }
   __syncthreads();
 
-  // Stage the accumulators through LDS in row-major order (MFMA 32x32 layout:
-  // lane holds column lane%32 and rows 8*(k/4) + 4*(lane/32) + k%4).
+  // Stage the accumulators through LDS in row-major order, one band of PR
+  // rows at a time (MFMA 32x32 layout: lane holds column lane%32 and rows
+  // 8*(k/4) + 4*(lane/32) + k%4), and run the epilogue on each band.
   float* Cs = reinterpret_cast<float*>(smem_raw);
-#pragma unroll
-  for (int i = 0; i < T::TP; ++i)
-#pragma unroll
-    for (int j = 0; j < T::TQ; ++j)
-#pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int p = wp * T::WTP + i * 32 + (k >> 2) * 8 + (lane >> 5) * 4 + (k & 3);
-        const int q = wq * T::WTQ + j * 32 + (lane & 31);
-        Cs[p * T::LDC + q] = acc[i][j][k];
-      }
-  __syncthreads();
-
   constexpr int NQ4 = T::BQ / 4;
-  constexpr int ITEMS = T::BP * NQ4;
-  constexpr int EPT = (ITEMS + 255) / 256;
+  constexpr int ITEMS = T::PR * NQ4;
+  constexpr int EPT = (ITEMS + T::NT - 1) / T::NT;
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int idx = tid + e * 256;
-    if (idx >= ITEMS) break;
-    const int p = idx / NQ4, q = (idx % NQ4) * 4;
-    const int gp = p0 + p, gq = q0 + q;
-    if (gp >= pr.P || gq >= pr.Q) continue;
-    const float4 cv = *reinterpret_cast<const float4*>(&Cs[p * T::LDC + q]);
-    const float c[4] = {cv.x, cv.y, cv.z, cv.w};
-    const int n = min(4, pr.Q - gq);
-    if (S > 1) {
-      float* dst = partial + ((int64_t)split * pr.P + gp) * pr.Q + gq;
-      if (n == 4 && (pr.Q & 3) == 0) st4(dst, cv);
-      else for (int k = 0; k < n; ++k) dst[k] = c[k];
-    } else {
-      const float* bias = (EPI == EPI_FWD && ea.bias) ? ea.bias + gq : nullptr;
-      epilogue<EPI>(ea, gp, gq, c, n, bias, vec_epi);
+  for (int h = 0; h < T::NPASS; ++h) {
+    if (h) __syncthreads();   // the previous band has been read
+#pragma unroll
+    for (int i = 0; i < T::TP; ++i) {
+      const int rb = wp * T::WTP + i * 32 - h * T::PR;   // block's first row in the band
+      if (rb < 0 || rb >= T::PR) continue;
+#pragma unroll
+      for (int j = 0; j < T::TQ; ++j)
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int p = rb + (k >> 2) * 8 + (lane >> 5) * 4 + (k & 3);
+          const int q = wq * T::WTQ + j * 32 + (lane & 31);
+          Cs[p * T::LDC + q] = acc[i][j][k];
+        }
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int idx = tid + e * T::NT;
+      if (ITEMS % T::NT != 0 && idx >= ITEMS) break;
+      const int p = idx / NQ4, q = (idx % NQ4) * 4;
+      const int gp = p0 + h * T::PR + p, gq = q0 + q;
+      if (gp >= pr.P || gq >= pr.Q) continue;
+      const float4 cv = *reinterpret_cast<const float4*>(&Cs[p * T::LDC + q]);
+      const float c[4] = {cv.x, cv.y, cv.z, cv.w};
+      const int n = min(4, pr.Q - gq);
+      if (S > 1) {
+        float* dst = partial + ((int64_t)split * pr.P + gp) * pr.Q + gq;
+        if (n == 4 && (pr.Q & 3) == 0) st4(dst, cv);
+        else for (int k = 0; k < n; ++k) dst[k] = c[k];
+      } else {
+        const float* bias = (EPI == EPI_FWD && ea.bias) ? ea.bias + gq : nullptr;
+        epilogue<EPI>(ea, gp, gq, c, n, bias, vec_epi);
+      }
     }
   }
 
@@ -344,7 +391,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmProblem pr, EpiArgs 
     float* red = reinterpret_cast<float*>(smem_raw);  // [RQ][BP]
 #pragma unroll
     for (int i = 0; i < LA::PER; ++i) {
-      const int idx = tid + i * 256;
+      const int idx = tid + i * T::NT;
       if (idx < LA::NQ) {
         const int rq = idx / (T::BP / 4), x = (idx % (T::BP / 4)) * 4;
         for (int k = 0; k < 4; ++k) red[rq * T::BP + x + k] = dbs[i][k];
@@ -377,12 +424,21 @@ static int64_t bntiles(int t, int P, int Q) {
   return (int64_t)((P + kBTileBP[t] - 1) / kBTileBP[t]) * ((Q + kBTileBQ[t] - 1) / kBTileBQ[t]);
 }
 
-// 128x128 tiles when the output has enough of them, else 64x64; the reduction
-// is split until there are about 256 workgroups, and for a forward until no
-// split spans more than 2048 elements (at least 4 chunks per split).
-// The eager and backward-fusion weight gradients share this rule.
+// 128x256 eight-wave tiles for large outputs (at least 512 of them) and, in
+// a forward, for long reductions (at least 128 tiles, 2048 or more reduction
+// elements); else 128x128 tiles when the output has enough of them, else
+// 64x64.  The reduction is split until there are about 256 workgroups, and
+// for a forward until no split spans more than 2048 elements (at least 4
+// chunks per split).  Gradients keep whole reductions on the wide tiles:
+// backward-fusion runs them beside each other on two streams, where fewer,
+// split workgroups lose what they gain alone (measured on MI355X).  The eager
+// and backward-fusion weight gradients share this rule.
 static BCfg bselect_default(int kind, int P, int Q, int R) {
-  const int t = bntiles(BTI_128x128, P, Q) >= 64 ? BTI_128x128 : BTI_64x64;
+  const int64_t nw = bntiles(BTI_128x256, P, Q);
+  const bool wide = nw >= 512 || (kind == EPI_FWD && nw >= 128 && R >= 2048);
+  const int t = wide                                    ? BTI_128x256
+                : bntiles(BTI_128x128, P, Q) >= 64      ? BTI_128x128
+                                                        : BTI_64x64;
   const int BR = kBTileBR[t];
   const int64_t nt = bntiles(t, P, Q);
   int S = (int)std::max<int64_t>(1, (256 + nt - 1) / nt);
@@ -405,6 +461,8 @@ static BCfg bselect(int kind, int P, int Q, int R) {
   if (!e) return bselect_default(kind, P, Q, R);
   int t = 1, S = 1;
   sscanf(e, "%d,%d", &t, &S);
+  t = std::max(0, std::min(t, (int)BTI_COUNT - 1));
+  S = std::max(1, S);
   const int BR = kBTileBR[t];
   const int r_split = ((R + S - 1) / S + BR - 1) / BR * BR;
   return BCfg{t, (R + r_split - 1) / r_split, r_split};
@@ -423,12 +481,20 @@ template <class T, int EPI, bool VA, bool VB>
 static hipError_t blaunch_v(const BCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                             int vec_epi, hipStream_t s) {
   dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S + c.cz);
+  if constexpr (EPI == EPI_FWD) {
+    if (pr.a_bf16) {
+      if (!pr.b_bf16) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, true, true>), grid, dim3(T::NT), 0, s,
+                         pr, ea, c.r_split, (float*)ws, vec_epi);
+      return hipGetLastError();
+    }
+  }
   if (pr.b_bf16)
-    hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, true>), grid, dim3(256), 0, s, pr, ea,
-                       c.r_split, (float*)ws, vec_epi);
+    hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, true, false>), grid, dim3(T::NT), 0, s, pr,
+                       ea, c.r_split, (float*)ws, vec_epi);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, false>), grid, dim3(256), 0, s, pr, ea,
-                       c.r_split, (float*)ws, vec_epi);
+    hipLaunchKernelGGL((gemm_bf16_kernel<T, EPI, VA, VB, false, false>), grid, dim3(T::NT), 0, s, pr,
+                       ea, c.r_split, (float*)ws, vec_epi);
   return hipGetLastError();
 }
 
@@ -446,19 +512,31 @@ static hipError_t blaunch_t(const BCfg& c, const GemmProblem& pr, const EpiArgs&
 template <int EPI>
 static hipError_t blaunch_kind(const BCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                                int vec_ops, int vec_epi, hipStream_t s) {
-  if (c.tile == BTI_128x128) return blaunch_t<BT128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
-  return blaunch_t<BT64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+  switch (c.tile) {
+    case BTI_128x128: return blaunch_t<BT128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case BTI_128x256: return blaunch_t<BT128x256, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+#ifdef OPFUSE_TUNING
+    case BTI_128x128R64: return blaunch_t<BT128x128R64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case BTI_128x256R32: return blaunch_t<BT128x256R32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case BTI_256x128: return blaunch_t<BT256x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+#endif
+    default: return blaunch_t<BT64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+  }
 }
 
 static int bvec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* vec_epi) {
   const bool a_rc = (kind == EPI_FWD || kind == EPI_DGRAD);
   const bool b_rc = (kind == EPI_FWD);
-  // fp32 quads: 16-byte aligned rows; bf16 quads: 8-byte aligned rows
-  const bool va = aligned16(pr.A) && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % 4 == 0) &&
-                  ((a_rc ? pr.R : pr.P) % 4 == 0);
-  const bool b_al = pr.b_bf16 ? (((uintptr_t)pr.B & 7u) == 0) : aligned16(pr.B);
-  const bool vb = b_al && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % 4 == 0) &&
-                  ((b_rc ? pr.R : pr.Q) % 4 == 0);
+  // fp32 quads: 16-byte aligned rows; bf16 quads: 8-byte aligned rows; bf16
+  // octets (a bf16 operand whose reduction index is contiguous): 16-byte
+  // aligned rows and a reduction extent that is a multiple of 8
+  const int ga = pr.a_bf16 && a_rc ? 8 : 4, gb = pr.b_bf16 && b_rc ? 8 : 4;
+  const bool a_al = pr.a_bf16 && !a_rc ? (((uintptr_t)pr.A & 7u) == 0) : aligned16(pr.A);
+  const bool va = a_al && ((pr.a_sr == 1 ? pr.a_sp : pr.a_sr) % ga == 0) &&
+                  ((a_rc ? pr.R : pr.P) % ga == 0);
+  const bool b_al = pr.b_bf16 && !b_rc ? (((uintptr_t)pr.B & 7u) == 0) : aligned16(pr.B);
+  const bool vb = b_al && ((pr.b_sr == 1 ? pr.b_sq : pr.b_sr) % gb == 0) &&
+                  ((b_rc ? pr.R : pr.Q) % gb == 0);
   int ve = 0;
   if (aligned16(ea.out) && ea.ldo % 4 == 0 && (ea.z == nullptr || (aligned16(ea.z) && ea.ldz % 4 == 0)) &&
       (ea.prev == nullptr || (aligned16(ea.prev) && ea.ldp % 4 == 0)))
@@ -471,9 +549,14 @@ static int bvec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* v
   return (va ? 1 : 0) | (vb ? 2 : 0);
 }
 
-hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, void* ws,
+hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr_in, const EpiArgs& ea_in, void* ws,
                             hipStream_t stream) {
-  if (pr.a_bf16 || pr.conv) return hipErrorInvalidValue;
+  GemmProblem pr = pr_in;
+#ifdef OPFUSE_TUNING
+  // Tuning builds only: read a forward's A operand as bf16 (timing only).
+  if (kind == EPI_FWD && getenv("OPFUSE_TUNE_ABF")) pr.a_bf16 = 1;
+#endif
+  if ((pr.a_bf16 && kind != EPI_FWD) || pr.conv) return hipErrorInvalidValue;
   BCfg c = bselect(kind, pr.P, pr.Q, pr.R);
   EpiArgs ea = ea_in;
   ea.carry.z0 = 0;

@@ -69,6 +69,8 @@ __device__ __forceinline__ void xcd_tile(int& tx, int& ty) {
 // Run by the workgroups of the z-slices from c.z0 on, grid-stride over the
 // carried tensors.  Each element gets the same operations as in the eager
 // optimizer pass (vector gradients) or the rows-mode update (row partials).
+// NT: threads per workgroup of the launch the update rides on.
+template <int NT = 256>
 __device__ __forceinline__ void carry_update(const CarryArgs& c) {
   OptK o = c.opt;
   opt_prepare(o);
@@ -83,7 +85,7 @@ __device__ __forceinline__ void carry_update(const CarryArgs& c) {
     if (T.p.w == nullptr) continue;
     const int64_t n = T.p.numel;
     if (T.rows == 1) {
-      for (int64_t i = (u * 256 + threadIdx.x) * 4; i < n; i += U * 1024) {
+      for (int64_t i = (u * NT + threadIdx.x) * 4; i < n; i += U * NT * 4) {
         if (T.vec && i + 3 < n) {
           update4(o, T.p, ld4(T.g + i), i);
         } else {
@@ -91,7 +93,7 @@ __device__ __forceinline__ void carry_update(const CarryArgs& c) {
         }
       }
     } else {
-      for (int64_t i = u * 256 + threadIdx.x; i < n; i += U * 256) {
+      for (int64_t i = u * NT + threadIdx.x; i < n; i += U * NT) {
         float s = T.g[i];
         for (int64_t r0 = 1; r0 < T.rows; r0 += 8) {
           float v[8];

@@ -57,6 +57,10 @@ def _shadow(torch, dev, w32):
 SHAPES = [  # (M, N, K): ragged tails, vector paths, split reductions, block shapes
     (37, 70, 53), (64, 128, 96), (130, 96, 44), (200, 168, 160), (512, 256, 1024),
     (4096, 1024, 1024), (4096, 3072, 1024), (4096, 1024, 4096),
+    # eight-wave 128x256 tiles: a forward with a long reduction (vector and
+    # scalar loads, ragged in every dimension), a data gradient with at least
+    # 512 output tiles and a ragged reduction
+    (2000, 2000, 2056), (1999, 2001, 2050), (4100, 300, 4090),
 ]
 
 

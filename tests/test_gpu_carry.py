@@ -72,9 +72,10 @@ def _carry(L, opt, *ts):
     return L.make_carry(opt, [(t.copies[0]["p"], t.copies[0]["g"], t.rows) for t in ts])
 
 
-CASES = [  # (M, N, K, dtype): direct tiles, staged tiles, split reduction, bf16
+CASES = [  # (M, N, K, dtype): direct tiles, staged tiles, split reduction, bf16,
+    # bf16 on eight-wave 128x256 tiles (512-thread workgroups carry the update)
     (256, 1024, 1024, "f32"), (1024, 512, 256, "f32"), (100, 50, 3000, "f32"),
-    (72, 168, 200, "f32"), (512, 1024, 1024, "bf16"),
+    (72, 168, 200, "f32"), (512, 1024, 1024, "bf16"), (1024, 4096, 2048, "bf16"),
 ]
 
 
