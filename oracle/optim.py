@@ -15,8 +15,13 @@ adam  Adam (Kingma & Ba, Alg. 1; the optimizer of the paper's experimental
 adamw Adam with decoupled weight decay (Loshchilov & Hutter):
           theta <- theta * (1 - eta * wd), then the Adam step on the raw g.
 
+clip_scale  the global-norm clipping factor (forward-fusion's global-information
+      step; see its docstring).
+
 Pinned by: closed forms on hand-set tensors (constant gradient) in
-tests/test_oracle_optim.py.
+tests/test_oracle_optim.py; clip_scale by a 3-4-5 closed form, the norm of the
+concatenated gradients (numpy.linalg.norm) and the clipped norm in
+tests/test_oracle_clip.py.
 """
 import numpy as np
 
@@ -42,6 +47,28 @@ def adamw(theta, g, m, v, step, lr, beta1, beta2, eps, weight_decay, **_):
 
 
 POLICIES = {"sgd": sgd, "adam": adam, "adamw": adamw}
+
+
+def clip_scale(grads, max_norm):
+    """Factor for clipping gradients by their global norm, and that norm.
+
+    Forward-fusion may change the gradients using information from every
+    parameter before any of them is updated, and global-norm clipping is the
+    example the paper gives (Appendix B.1; Table 1, "Global Info."); backward-
+    fusion cannot, since it updates each tensor before the others' gradients
+    exist (Section 3, "Backward-Fusion").  The paper names the operation
+    without a formula; this takes the common definition:
+        norm  = sqrt(sum over all gradient elements of g^2)
+        scale = max_norm / (norm + 1e-6), capped at 1
+    and every gradient is multiplied by scale before the optimizer uses it.
+    A NaN norm gives a NaN scale (an infinite one gives 0).
+    """
+    total = 0.0
+    for g in grads:
+        total += float(np.sum(np.square(np.asarray(g, np.float64))))
+    norm = float(np.sqrt(total))
+    s = max_norm / (norm + 1e-6)
+    return (1.0 if s > 1.0 else s), norm
 
 
 def apply(param, hyper):

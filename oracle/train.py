@@ -22,6 +22,9 @@ Readings where the paper is silent:
     of the node; flush() applies it (an evaluation forward does the same).
   * The update applied during forward t+1 is eager's update t, counted when
     it is applied.
+  * Global-norm clipping (optional `clip_norm` in the optimizer dict): eager
+    and forward-fusion scale every gradient of the step right after the
+    backward pass; backward-fusion refuses it (Table 1).
 
 Returned by run(): per-step losses (loss t uses theta^(t-1)), the evaluation
 loss at theta^(K), final values / histories / step counters of every
@@ -49,7 +52,7 @@ import numpy as np
 from workloads import make_params, make_batch, make_eval_batch
 from . import layers as L
 from .losses import LOSSES
-from .optim import apply as apply_optimizer
+from .optim import apply as apply_optimizer, clip_scale
 
 
 class Model:
@@ -59,6 +62,7 @@ class Model:
         self.loss = loss
         self.hyper = hyper
         self.last_argmax = {}
+        self.last_clip = None         # (scale, norm) of the last clipped step
 
     # -- plain passes ---------------------------------------------------
     def forward(self, x, before_node=None):
@@ -101,10 +105,24 @@ class Model:
         return LOSSES[self.loss](out, target)[0]
 
     # -- orderings ------------------------------------------------------
+    def clip(self):
+        """Global-norm clipping of every accumulated gradient when the optimizer
+        dict sets `clip_norm` (Appendix B.1): after the backward pass, before
+        any of these gradients is consumed.  Records (scale, norm)."""
+        max_norm = self.hyper.get("clip_norm")
+        if max_norm is None:
+            return
+        ps = [p for p in self.params.values() if p.grad is not None]
+        scale, norm = clip_scale([p.grad for p in ps], max_norm)
+        self.last_clip = (scale, norm)
+        for p in ps:
+            p.grad = p.grad * scale
+
     def step_eager(self, x, target):
         out, tape = self.forward(x)
         loss, dout = self.loss_and_grad(out, target)
         self.backward(tape, dout)
+        self.clip()
         for p in self.params.values():
             if p.grad is not None:
                 apply_optimizer(p, self.hyper)
@@ -124,6 +142,7 @@ class Model:
         out, tape = self.forward(x, before_node=before)
         loss, dout = self.loss_and_grad(out, target)
         self.backward(tape, dout, after_node=after)
+        self.clip()   # the pending gradients, before the next forward consumes them
         return loss
 
     def flush(self):
@@ -136,6 +155,10 @@ class Model:
                 op.updated = True
 
     def step_bf(self, x, target, race_bug=False):
+        if self.hyper.get("clip_norm") is not None:
+            raise ValueError("backward-fusion updates each tensor before the other gradients "
+                             "exist, so it cannot clip by the global norm (Table 1)")
+
         def count(op):
             for p in op.params:
                 p.count += 1
@@ -284,6 +307,7 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
     Returns a dict: losses, eval_loss, params / m / v (float64 arrays by name),
     step (int by name), updated (per node, after the run), count (by name),
     argmax (max-pool window positions of step 1, by node index),
+    clips ((scale, norm) of each step's global-norm clipping, or None),
     snapshots {t: state after step t (t = 0: the initial state)} for t in
     `snapshots` -- params / m / v copies, step counters, the gradient the
     update of step t consumed and min_sqrt_vhat up to step t (eager ordering).
@@ -295,6 +319,7 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
     hyper = cfg["opt"]
     min_vhat = {}
     snaps = {}
+    clips = []
 
     def snap():
         ps = model.params
@@ -319,6 +344,7 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
             losses.append(model.step_bf(x, y, race_bug=race_bug))
         else:
             raise ValueError(ordering)
+        clips.append(model.last_clip)
         if t == 1:
             argmax = dict(model.last_argmax)
         if hyper["kind"] != "sgd":
@@ -347,6 +373,7 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
         updated_before_flush=updated_before_flush,
         updated=[op.updated for op, _, _ in model.nodes],
         argmax=argmax,
+        clips=clips,
         min_sqrt_vhat=min_vhat,
         snapshots=snaps,
     )
