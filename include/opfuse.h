@@ -97,6 +97,13 @@ typedef struct of_opt {
    * (for launches captured once and replayed, e.g. in a HIP graph; see
    * of_step_advance).  The value there must be >= 1 when they run. */
   const int64_t* step_dev;
+  /* Optional device address of a gradient scale, read by the kernels when they
+   * run: every gradient element is multiplied by it (rounded to fp32) before
+   * the update uses it.  NULL means 1, which leaves every result bit-identical
+   * to an unscaled update.  of_grad_clip_scale writes the factor for
+   * global-norm clipping; only orderings that update after the whole backward
+   * pass (eager, forward-fusion) can use that factor (Table 1). */
+  const float* grad_scale;
 } of_opt;
 
 /*
@@ -349,6 +356,36 @@ of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t
  */
 of_status of_optimizer_step(int32_t n, const of_param* params, const float* const* grads,
                             const of_opt* opt, void* stream);
+
+/*
+ * Global-norm gradient clipping factor (the global-information step that
+ * forward-fusion allows and backward-fusion does not: Appendix B.1, Table 1).
+ * Over the gradients of n tensors,
+ *   norm  = sqrt(sum over every element e of every tensor of g[e]^2)
+ *   scale = max_norm / (norm + 1e-6), capped at 1  (NaN norm: NaN; infinite: 0)
+ * and writes scale, and norm when `norm` is not NULL (one fp32 each, device
+ * memory), in stream order.  Pass `scale` as of_opt.grad_scale to the updates
+ * that consume these gradients.
+ * A gradient is a vector [numel] (rows == 1) or row partials [rows, ld]
+ * (row stride ld >= numel, 0 meaning numel) whose element is the sum of its
+ * rows in row order in fp32 -- exactly the value the rows-mode update uses.
+ * Squares are summed in float64, in a fixed order (deterministic); the
+ * result matches the float64 definition to about 1e-15 relative.
+ * grads: HOST array of n entries holding device pointers; n >= 1.
+ * ws: device workspace of at least OF_CLIP_WS_BYTES bytes, 8-byte aligned.
+ * max_norm must be > 0 and finite.
+ */
+typedef struct of_grad_ref {
+  const float* g;
+  int64_t numel;   /* >= 1 */
+  int64_t rows;    /* >= 1 */
+  int64_t ld;      /* row stride of row partials in elements; 0 means numel */
+} of_grad_ref;
+
+#define OF_CLIP_WS_BYTES 2048
+
+of_status of_grad_clip_scale(int32_t n, const of_grad_ref* grads, float max_norm, float* scale,
+                             float* norm, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Adds `delta` to the device step counter *step_dev in stream order (one

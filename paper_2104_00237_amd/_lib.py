@@ -30,7 +30,8 @@ c_int32, c_int64, c_float, c_void_p, c_size_t = (ctypes.c_int32, ctypes.c_int64,
 class OfOpt(ctypes.Structure):
     _fields_ = [("kind", c_int32), ("lr", c_float), ("weight_decay", c_float),
                 ("momentum", c_float), ("beta1", c_float), ("beta2", c_float),
-                ("eps", c_float), ("step", c_int64), ("step_dev", c_void_p)]
+                ("eps", c_float), ("step", c_int64), ("step_dev", c_void_p),
+                ("grad_scale", c_void_p)]
 
 
 class OfParam(ctypes.Structure):
@@ -44,6 +45,13 @@ OF_CARRY_MAX = 4
 class OfCarry(ctypes.Structure):
     _fields_ = [("n", c_int32), ("t", OfParam * OF_CARRY_MAX), ("g", c_void_p * OF_CARRY_MAX),
                 ("rows", c_int64 * OF_CARRY_MAX), ("opt", OfOpt)]
+
+
+OF_CLIP_WS_BYTES = 2048
+
+
+class OfGradRef(ctypes.Structure):
+    _fields_ = [("g", c_void_p), ("numel", c_int64), ("rows", c_int64), ("ld", c_int64)]
 
 
 class OfLinearDesc(ctypes.Structure):
@@ -86,6 +94,8 @@ _SIGS = {
                                               P(OfOpt), c_void_p]),
     "of_optimizer_step": (c_int32, [c_int32, P(OfParam), P(c_void_p), P(OfOpt), c_void_p]),
     "of_step_advance": (c_int32, [c_void_p, c_int64, c_void_p]),
+    "of_grad_clip_scale": (c_int32, [c_int32, P(OfGradRef), c_float, c_void_p, c_void_p,
+                                     c_void_p, c_size_t, c_void_p]),
     "of_conv_workspace_size": (c_size_t, [P(OfConvDesc), c_int32]),
     "of_conv_fwd": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_void_p, c_void_p,
                               c_size_t, c_void_p]),
@@ -176,7 +186,7 @@ def of_layernorm_partial_rows(M):
 
 for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
-           "of_step_advance", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
+           "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
            "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_layernorm_fwd", "of_layernorm_bwd",
            "of_reduce_rows", "of_add"):
@@ -184,12 +194,18 @@ for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_line
 del _n
 
 
-def make_opt(hyper, step, step_dev=None):
+def make_opt(hyper, step, step_dev=None, grad_scale=None):
     """of_opt from a workload's optimizer dict and the 1-based update index
-    (or a device address holding it)."""
+    (or a device address holding it), with an optional device address of a
+    gradient scale (e.g. the global-norm clipping factor)."""
     return OfOpt(OPT_KINDS[hyper["kind"]], hyper["lr"], hyper.get("weight_decay", 0.0),
                  hyper.get("momentum", 0.0), hyper.get("beta1", 0.0), hyper.get("beta2", 0.0),
-                 hyper.get("eps", 0.0), step, step_dev)
+                 hyper.get("eps", 0.0), step, step_dev, grad_scale)
+
+
+def grad_refs(items):
+    """HOST array of of_grad_ref from [(device pointer, numel, rows, ld), ...]."""
+    return (OfGradRef * len(items))(*[OfGradRef(g, n, r, ld) for g, n, r, ld in items])
 
 
 def make_carry(opt, tensors):

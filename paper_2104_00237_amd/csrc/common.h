@@ -23,6 +23,8 @@ struct OptK {
   float step_size;   // lr / (1 - beta1^t)
   float rsqrt_bc2;   // 1 / sqrt(1 - beta2^t)
   int prepared;      // step_size / rsqrt_bc2 already set (step given by value)
+  const float* gscale_dev;  // optional gradient scale in device memory
+  float gscale;      // the scale in use (1 unless read from gscale_dev)
 };
 
 OptK make_optk(const of_opt& o);
@@ -50,7 +52,9 @@ __host__ __device__ inline void opt_constants(OptK& o, int64_t t) {
 // Kernels call this before their first update: with a step given by value the
 // host has already set the constants; with a device step counter they are
 // computed here, from the step the kernel reads when it runs.
+// A gradient scale given by address is read here too.
 __device__ __forceinline__ void opt_prepare(OptK& o) {
+  if (o.gscale_dev) o.gscale = *o.gscale_dev;
   if (o.kind == OF_OPT_SGD || o.prepared) return;
   opt_constants(o, *o.step_dev);
 }
@@ -60,6 +64,7 @@ __device__ __forceinline__ void opt_prepare(OptK& o) {
 // explicitly rounded (the sources are also built with -ffp-contract=off), so
 // the same gradient gives the same bits in every ordering and kernel.
 __device__ __forceinline__ void opt_update(const OptK& o, float& w, float g, float& m, float& v) {
+  g = __fmul_rn(g, o.gscale);   // the gradient scale (exact when it is 1)
   if (o.kind == OF_OPT_SGD) {
     // Momentum policy pi_2 with coupled weight decay.
     const float gp = __fmaf_rn(o.wd, w, g);
@@ -250,6 +255,8 @@ hipError_t launch_multi_update(int n, const of_param* params, const float* const
 hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, int64_t ld,
                               const OptK& o, hipStream_t stream);
 hipError_t launch_step_advance(int64_t* step_dev, int64_t delta, hipStream_t stream);
+hipError_t launch_grad_clip(int n, const of_grad_ref* grads, float max_norm, float* scale,
+                            float* norm, double* partial, hipStream_t stream);
 hipError_t launch_maxpool_fwd(const float* x, int64_t N, int64_t H, int64_t W, int64_t C,
                               float* y, uint8_t* arg, hipStream_t s);
 hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, const float* mask_src,

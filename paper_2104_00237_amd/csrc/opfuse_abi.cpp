@@ -48,6 +48,8 @@ of_status check_opt(const of_opt* o) {
   REQUIRE(o->step_dev != nullptr || o->step >= 1, OF_EINVAL, "opt->step must be >= 1 (got %lld)",
           (long long)o->step);
   REQUIRE((((uintptr_t)o->step_dev) & 7u) == 0, OF_EALIGN, "opt->step_dev must be 8-byte aligned");
+  REQUIRE((((uintptr_t)o->grad_scale) & 3u) == 0, OF_EALIGN,
+          "opt->grad_scale must be 4-byte aligned");
   REQUIRE(std::isfinite(o->lr) && std::isfinite(o->weight_decay), OF_EINVAL,
           "opt->lr / weight_decay must be finite");
   if (o->kind != OF_OPT_SGD) {
@@ -295,6 +297,8 @@ OptK make_optk(const of_opt& o) {
   k.decay = (float)(1.0 - (double)o.lr * (double)o.weight_decay);
   k.step = o.step;
   k.step_dev = o.step_dev;
+  k.gscale_dev = o.grad_scale;
+  k.gscale = 1.f;
   k.step_size = 0.f;
   k.rsqrt_bc2 = 0.f;
   k.prepared = 0;
@@ -623,6 +627,31 @@ of_status of_optimizer_step(int32_t n, const of_param* params, const float* cons
   }
   return hip_status(launch_multi_update(n, params, grads, make_optk(*opt), (hipStream_t)stream),
                     "of_optimizer_step launch");
+}
+
+of_status of_grad_clip_scale(int32_t n, const of_grad_ref* grads, float max_norm, float* scale,
+                             float* norm, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(n >= 1 && grads != nullptr, OF_EINVAL, "n >= 1 and grads are required");
+  REQUIRE(std::isfinite(max_norm) && max_norm > 0.f, OF_EINVAL,
+          "max_norm must be finite and > 0 (got %g)", (double)max_norm);
+  REQUIRE(scale != nullptr, OF_EINVAL, "scale is NULL");
+  REQUIRE(al4(scale) && (norm == nullptr || al4(norm)), OF_EALIGN,
+          "scale / norm must be 4-byte aligned");
+  REQUIRE(ws != nullptr && ws_bytes >= OF_CLIP_WS_BYTES, OF_EWORKSPACE,
+          "workspace of %d bytes required (got %zu)", (int)OF_CLIP_WS_BYTES, ws_bytes);
+  REQUIRE((((uintptr_t)ws) & 7u) == 0, OF_EALIGN, "ws must be 8-byte aligned");
+  for (int32_t i = 0; i < n; ++i) {
+    const of_grad_ref& g = grads[i];
+    REQUIRE(g.g != nullptr, OF_EINVAL, "grads[%d].g is NULL", (int)i);
+    REQUIRE(al4(g.g), OF_EALIGN, "grads[%d].g must be 4-byte aligned", (int)i);
+    REQUIRE(g.numel >= 1 && g.rows >= 1, OF_EINVAL, "grads[%d]: numel and rows must be >= 1",
+            (int)i);
+    REQUIRE(g.ld == 0 || g.ld >= g.numel, OF_EINVAL, "grads[%d].ld must be 0 or >= numel",
+            (int)i);
+  }
+  return hip_status(launch_grad_clip(n, grads, max_norm, scale, norm, (double*)ws,
+                                     (hipStream_t)stream),
+                    "of_grad_clip_scale launch");
 }
 
 of_status of_step_advance(int64_t* step_dev, int64_t delta, void* stream) {

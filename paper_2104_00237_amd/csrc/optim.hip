@@ -108,6 +108,112 @@ hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, i
   return hipGetLastError();
 }
 
+// ------------------------------------------------ global-norm clipping
+// Pass 1: workgroup b sums the squares of its grid-stride share of the
+// gradients of up to CLIP_MAX tensors in float64, in a fixed order (per-lane
+// accumulators, then a fixed tree), and writes (first launch) or adds (later
+// launches, stream-ordered) its partial.  A row-partial gradient's element is
+// its rows summed in row order in fp32, as the rows-mode update sums them.
+// Pass 2: one workgroup sums the CLIP_WG partials with a fixed tree and
+// writes the factor (and the norm).
+
+constexpr int CLIP_MAX = 32;
+constexpr int CLIP_WG = OF_CLIP_WS_BYTES / 8;   // partials, one per workgroup
+static_assert(CLIP_WG == 256, "one partial per workgroup of the sum pass");
+
+struct ClipEntry {
+  const float* g;
+  int64_t numel, rows, ld;
+  int vec;   // a 16-byte aligned vector gradient
+};
+
+struct ClipArgs {
+  int n, accumulate;
+  ClipEntry e[CLIP_MAX];
+};
+
+__device__ __forceinline__ double wg_sum256(double x, double* red) {
+  const int tid = threadIdx.x;
+  red[tid] = x;
+  __syncthreads();
+#pragma unroll
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) red[tid] = red[tid] + red[tid + w];
+    __syncthreads();
+  }
+  return red[0];
+}
+
+__global__ __launch_bounds__(256) void grad_sumsq_kernel(ClipArgs a, double* __restrict__ partial) {
+  __shared__ double red[256];
+  const int64_t lane = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  for (int t = 0; t < a.n; ++t) {
+    const ClipEntry& E = a.e[t];
+    if (E.rows == 1 && E.vec) {
+      for (int64_t i = lane * 4; i < E.numel; i += stride * 4) {
+        if (i + 3 < E.numel) {
+          const float4 v = ld4(E.g + i);
+          s0 += (double)v.x * (double)v.x;
+          s1 += (double)v.y * (double)v.y;
+          s2 += (double)v.z * (double)v.z;
+          s3 += (double)v.w * (double)v.w;
+        } else {
+          for (int64_t k = i; k < E.numel; ++k) s0 += (double)E.g[k] * (double)E.g[k];
+        }
+      }
+    } else if (E.rows == 1) {
+      for (int64_t i = lane; i < E.numel; i += stride) s0 += (double)E.g[i] * (double)E.g[i];
+    } else {
+      for (int64_t i = lane; i < E.numel; i += stride) {
+        float x = E.g[i];
+        for (int64_t r = 1; r < E.rows; ++r) x = __fadd_rn(x, E.g[r * E.ld + i]);
+        s0 += (double)x * (double)x;
+      }
+    }
+  }
+  const double tot = wg_sum256((s0 + s1) + (s2 + s3), red);
+  if (threadIdx.x == 0) partial[blockIdx.x] = a.accumulate ? partial[blockIdx.x] + tot : tot;
+}
+
+__global__ __launch_bounds__(256) void clip_finish_kernel(const double* __restrict__ partial,
+                                                          float max_norm, float* scale,
+                                                          float* norm) {
+  __shared__ double red[256];
+  const double tot = wg_sum256(partial[threadIdx.x], red);
+  if (threadIdx.x == 0) {
+    const double nrm = sqrt(tot);
+    const double f = (double)max_norm / (nrm + 1e-6);
+    scale[0] = (float)(f > 1.0 ? 1.0 : f);   // NaN stays NaN
+    if (norm) norm[0] = (float)nrm;
+  }
+}
+
+hipError_t launch_grad_clip(int n, const of_grad_ref* grads, float max_norm, float* scale,
+                            float* norm, double* partial, hipStream_t stream) {
+  for (int b = 0; b < n; b += CLIP_MAX) {
+    ClipArgs a;
+    a.n = std::min(CLIP_MAX, n - b);
+    a.accumulate = b > 0;
+    for (int i = 0; i < a.n; ++i) {
+      const of_grad_ref& g = grads[b + i];
+      ClipEntry& E = a.e[i];
+      E.g = g.g;
+      E.numel = g.numel;
+      E.rows = g.rows;
+      E.ld = g.ld ? g.ld : g.numel;
+      E.vec = g.rows == 1 && aligned16(g.g);
+    }
+    hipLaunchKernelGGL(grad_sumsq_kernel, dim3(CLIP_WG), dim3(256), 0, stream, a, partial);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(clip_finish_kernel, dim3(1), dim3(256), 0, stream, partial, max_norm, scale,
+                     norm);
+  return hipGetLastError();
+}
+
 __global__ void step_advance_kernel(int64_t* step, int64_t delta) {
   if (threadIdx.x == 0) *step += delta;
 }

@@ -645,7 +645,16 @@ class Trainer:
         # counter, advanced in stream order right before the step's updates, so
         # one captured launch sequence serves every later step.
         self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
-        self.opt_dev = L.make_opt(self.hyper, 0, self.step_dev.data_ptr())
+        # Global-norm clipping (optimizer dict `clip_norm`): the factor and the
+        # norm live on the device, written after each backward pass and read by
+        # the updates that consume those gradients.
+        self.clip_norm = self.hyper.get("clip_norm")
+        self.grad_scale = None
+        if self.clip_norm is not None:
+            self.clip_out = torch.ones(2, **f32)           # (scale, norm)
+            self.clip_ws = torch.empty(L.OF_CLIP_WS_BYTES // 4, **f32)
+            self.grad_scale = self.clip_out.data_ptr()
+        self.opt_dev = L.make_opt(self.hyper, 0, self.step_dev.data_ptr(), self.grad_scale)
         self.opt = self.opt_dev
         self.capturing = False
         self.stream = torch.cuda.current_stream(self.device)
@@ -674,8 +683,27 @@ class Trainer:
             L.of_step_advance(self.step_dev.data_ptr(), 1, self._s())
             self.opt = self.opt_dev
         else:
-            self.opt = L.make_opt(self.hyper, step)
+            self.opt = L.make_opt(self.hyper, step, None, self.grad_scale)
         return step
+
+    def _clip(self, vector):
+        """Global-norm clipping factor of the gradients just computed (Appendix
+        B.1): `vector` -- every gradient is in p.g (eager); else the pending ones
+        (forward-fusion: LayerNorm gradients as row partials)."""
+        if self.clip_norm is None:
+            return
+        items = []
+        for p in self.params.values():
+            if vector or p.rows is None:
+                items.append((p.g.data_ptr(), p.numel, 1, 0))
+            else:
+                ptr, rows, ld = p.pending()
+                items.append((ptr, p.numel, rows, ld))
+        self._t0("clip", self.stream)
+        L.of_grad_clip_scale(len(items), L.grad_refs(items), self.clip_norm,
+                             self.clip_out.data_ptr(), self.clip_out.data_ptr() + 4,
+                             self.clip_ws.data_ptr(), L.OF_CLIP_WS_BYTES, self._s())
+        self._t1("clip", self.stream)
 
     def _t0(self, cls, stream, op=None):
         if self.timer is not None:
@@ -723,6 +751,7 @@ class Trainer:
         self._loss(y)
         self.eager_reduce = True
         self.net.backward_plain(x)
+        self._clip(vector=True)
         ps = list(self.params.values())
         step = self._advance(ps)
         arr = (L.OfParam * len(ps))(*[p.p for p in ps])
@@ -744,6 +773,7 @@ class Trainer:
         # gradients stay pending (LayerNorm's as row partials)
         self.eager_reduce = False
         self.net.backward_plain(x)
+        self._clip(vector=False)
         for op in self.ops:
             op.updated = False
 
@@ -760,6 +790,9 @@ class Trainer:
         self.pending_ordering = None
 
     def _step_bf(self, x, y):
+        if self.clip_norm is not None:
+            raise ValueError("backward-fusion updates each tensor before the other gradients "
+                             "exist, so it cannot clip by the global norm (Table 1)")
         # The forward of each layer at this step needs its update from the last
         # step: the previous step ended with the main stream joining the side one.
         for op in self.ops:

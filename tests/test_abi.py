@@ -179,3 +179,34 @@ def test_carry_validation(lib):
     Wc = _param(8 * 9 * 3)
     assert _status(L.of_conv_fwd_carry, cd, FAKE, Wc, None, FAKE,
                    L.make_carry(adam, [(_param(8), None, 1)]), FAKE, 1 << 20, None) == L.OF_EINVAL
+
+
+def test_clip_validation(lib):
+    """of_grad_clip_scale rejects malformed arguments, and an optimizer with a
+    misaligned gradient-scale address is rejected, before any HIP call."""
+    ok = [(FAKE, 100, 1, 0), (FAKE, 10, 3, 16)]
+
+    def clip(items, max_norm=1.0, scale=FAKE, norm=None, ws=FAKE, ws_bytes=L.OF_CLIP_WS_BYTES,
+             n=None):
+        refs = L.grad_refs(items) if items else None
+        return _status(L.of_grad_clip_scale, len(items) if n is None else n, refs, max_norm,
+                       scale, norm, ws, ws_bytes, None)
+
+    assert clip([], n=0) == L.OF_EINVAL                              # no tensors
+    assert clip(ok, max_norm=0.0) == L.OF_EINVAL
+    assert clip(ok, max_norm=float("nan")) == L.OF_EINVAL
+    assert clip(ok, max_norm=float("inf")) == L.OF_EINVAL
+    assert clip(ok, scale=None) == L.OF_EINVAL
+    assert clip(ok, scale=FAKE + 2) == L.OF_EALIGN
+    assert clip(ok, norm=FAKE + 1) == L.OF_EALIGN
+    assert clip(ok, ws=None) == L.OF_EWORKSPACE
+    assert clip(ok, ws_bytes=L.OF_CLIP_WS_BYTES - 8) == L.OF_EWORKSPACE
+    assert clip(ok, ws=FAKE + 4) == L.OF_EALIGN
+    assert clip([(None, 100, 1, 0)]) == L.OF_EINVAL                  # no gradient
+    assert clip([(FAKE + 2, 100, 1, 0)]) == L.OF_EALIGN
+    assert clip([(FAKE, 0, 1, 0)]) == L.OF_EINVAL                    # empty tensor
+    assert clip([(FAKE, 10, 0, 0)]) == L.OF_EINVAL                   # rows 0
+    assert clip([(FAKE, 10, 2, 9)]) == L.OF_EINVAL                   # ld < numel
+    opt = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1, None, FAKE + 2)
+    assert _status(L.of_optimizer_step, 1, (L.OfParam * 1)(_param(8)),
+                   (ctypes.c_void_p * 1)(FAKE), opt, None) == L.OF_EALIGN
