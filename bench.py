@@ -6,7 +6,9 @@ three orderings run on the same inputs in the same process:
   eager  forward, backward writing every gradient, one multi-tensor optimizer launch
   ff     forward-fusion (update applied while the next forward loads W)
   bf     backward-fusion (update in the weight-gradient epilogue, second stream)
-The headline is backward-fusion.  `value` is its update bandwidth: the
+  bfm    backward-fusion with each layer's data gradient merged into the update's
+         read of W (fp32 linear layers with at most 64 rows; linear4x8192)
+The headline is backward-fusion (the faster of bf and bfm where bfm applies).  `value` is its update bandwidth: the
 parameter and optimizer-state bytes the fused step must move, over its step
 time.
 
@@ -47,6 +49,7 @@ def state_bytes_per_param(kind, ordering):
     (Fig. 2 accounting): eager = fwd R theta, dgrad R theta, wgrad W g, opt
     R theta,g,hist W theta,hist; ff = fused fwd R theta,g,hist W theta,hist,
     dgrad R theta, wgrad W g; bf = fwd R theta, dgrad R theta, fused wgrad
+    R theta,hist W theta,hist; bfm = fwd R theta, merged dgrad + update
     R theta,hist W theta,hist.
     """
     h = 2 if kind != "sgd" else 1          # history tensors (m, v) or (momentum)
@@ -55,6 +58,8 @@ def state_bytes_per_param(kind, ordering):
         return 4 + 4 + 4 + (upd + 4)
     if ordering == "ff":
         return (upd + 4) + 4 + 4
+    if ordering == "bfm":
+        return 4 + upd
     return 4 + 4 + upd
 
 
@@ -116,6 +121,11 @@ def layer_launches(cfg):
             dgrad=(f, yb + w + xb + (xb if act_prev else 0)) if j > 0 else None,
             wgrad=(f, yb + xb + w + bb),
             wgrad_bf=(f, yb + xb + upd(N * K) + (upd(N) if bias else 0)),
+            # merged data gradient + update: dZ, X, the state once, dX (+ the saved
+            # tensor for the activation derivative)
+            wgrad_bfm=((2 * f, yb + xb + upd(N * K) + (upd(N) if bias else 0) + xb
+                        + (xb if act_prev else 0)) if j > 0 else
+                       (f, yb + xb + upd(N * K) + (upd(N) if bias else 0))),
             extra=extra,
         ))
     return out
@@ -166,8 +176,8 @@ def step_cost(cfg, ordering):
     F = B = 0
     for d in L:
         fk = "fwd_ff" if ordering == "ff" else "fwd"
-        wk = "wgrad_bf" if ordering == "bf" else "wgrad"
-        for k in (fk, "dgrad", wk):
+        wk = {"bf": "wgrad_bf", "bfm": "wgrad_bfm"}.get(ordering, "wgrad")
+        for k in ((fk, wk) if ordering == "bfm" else (fk, "dgrad", wk)):
             if d.get(k) is not None:
                 F += d[k][0]
                 B += d[k][1]
@@ -225,7 +235,10 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     captured once per resident batch (the step-dependent optimizer constants are
     read from the device step counter); else each step is launched from Python."""
     from paper_2104_00237_amd.trainer import Trainer, KernelTimer
-    tr = Trainer(cfg, make_params(cfg), "cuda:0")
+    merge = ordering == "bfm"
+    if merge:
+        ordering = "bf"
+    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge)
     n = len(batches)
     for t in range(max(warmup, 1)):
         x, y = batches[t % n]
@@ -319,8 +332,10 @@ def main():
         batches.append((torch.as_tensor(x).to(dev), torch.as_tensor(y).to(dev)))
     torch.cuda.synchronize()
 
+    # the merged backward applies to fp32 linear chains of at most 64 rows
+    mergeable = cfg["kind"] == "mlp" and cfg["dtype"] == "f32" and cfg["batch"] <= 64
     res = {}
-    for o in ("eager", "ff", "bf"):
+    for o in ("eager", "ff", "bf") + (("bfm",) if mergeable else ()):
         ms, host_ms, _, _ = time_ordering(torch, cfg, o, batches, args.warmup, args.steps,
                                           graph=False)
         ms_g = None
@@ -331,16 +346,21 @@ def main():
         print(f"[bench] {o}: {ms:.4f} ms/step launched (host {host_ms:.4f}), "
               f"graph replay {ms_g} ms/step", file=sys.stderr, flush=True)
 
-    # Dominant kernel of the fused (bf) step: one instrumented pass finds the class
-    # with the largest total time; the timed pass then brackets only that class.
+    # The headline backward-fusion variant: the faster one.
+    head = "bfm" if mergeable and res["bfm"]["ms"] < res["bf"]["ms"] else "bf"
+    # Dominant kernel of the fused step: one instrumented pass finds the class
+    # with the largest total time; the timed pass then brackets only that class
+    # (bfm brackets each layer's merged pass -- its kernel and the data-gradient
+    # sum -- as wgrad_bf).
     classes = ("fwd", "dgrad", "wgrad_bf", "loss")
-    _, _, probe, _ = time_ordering(torch, cfg, "bf", batches, 2, 3, classes)
+    _, _, probe, _ = time_ordering(torch, cfg, head, batches, 2, 3, classes)
     totals = {c: sum(d for d, _ in probe.durations(c)) for c in classes}
     dom = max(totals, key=totals.get)
     print("[bench] launch-class totals (ms over the probe steps): " +
           ", ".join(f"{c} {t:.3f}" for c, t in totals.items()), file=sys.stderr, flush=True)
-    ms_dom_step, _, timer, _ = time_ordering(torch, cfg, "bf", batches, args.warmup, args.steps,
+    ms_dom_step, _, timer, _ = time_ordering(torch, cfg, head, batches, args.warmup, args.steps,
                                              (dom,))
+    cost_key = "wgrad_bfm" if (head == "bfm" and dom == "wgrad_bf") else dom
     launches = {d["name"]: d for d in layer_launches(cfg)}
     recs = timer.durations(dom)
     # Group launches by layer shape (the repeated hidden layers of an MLP share
@@ -349,19 +369,25 @@ def main():
     for d_ms, op in recs:
         if op is not None:
             by_shape.setdefault((op.kind, op.M, op.N, op.K), []).append((d_ms, op.name, op))
-    costed = [k for k in by_shape if launches[by_shape[k][0][1]].get(dom)]
+    costed = [k for k in by_shape if launches[by_shape[k][0][1]].get(cost_key)]
     shape = max(costed, key=lambda s: sum(d for d, _, _ in by_shape[s]))
+    if cost_key == "wgrad_bfm":
+        # the first layer has no data gradient: its merged pass is the plain update
+        grp = [(d, n, o) for d, n, o in by_shape[shape] if launches[n]["dgrad"] is not None]
+        by_shape[shape] = grp or by_shape[shape]
     durs = [d for d, _, _ in by_shape[shape]]
-    per = launches[by_shape[shape][0][1]][dom]
+    per = launches[by_shape[shape][0][1]][cost_key]
     # Each launch is bracketed by an event pair on its own stream; the pair's own
     # cost (an empty pair on the same stream) is taken off.
     from paper_2104_00237_amd.trainer import KernelTimer
-    on_side = dom == "wgrad_bf" and getattr(by_shape[shape][0][2], "overlap_update", False)
+    on_side = (dom == "wgrad_bf" and head == "bf"
+               and getattr(by_shape[shape][0][2], "overlap_update", False))
     dom_stream = torch.cuda.Stream() if on_side else torch.cuda.current_stream()
     marker_ms = KernelTimer.marker_overhead_ms(dom_stream)
     avg_s = (float(np.mean(durs)) - marker_ms) / 1e3
     roof = kernel_roofline(per[0], per[1], avg_s, mfma_peak(cfg))
-    roof.update(kernel=dom, layers=sorted({n for _, n, _ in by_shape[shape]}),
+    roof.update(kernel=("merged_bwd" if cost_key == "wgrad_bfm" else dom),
+                layers=sorted({n for _, n, _ in by_shape[shape]}),
                 shape=f"{shape[0]} GEMM M={shape[1]} N={shape[2]} K={shape[3]}",
                 avg_us=round(avg_s * 1e6, 3), launches=len(durs),
                 bracketed_avg_us=round(float(np.mean(durs)) * 1e3, 3),
@@ -371,10 +397,10 @@ def main():
 
     n_params = sum(d["nparams"] for d in launches.values())
     kind = cfg["opt"]["kind"]
-    upd_bytes = n_params * state_bytes_per_param(kind, "bf")
-    bf_s = res["bf"]["ms"] / 1e3
+    upd_bytes = n_params * state_bytes_per_param(kind, head)
+    bf_s = res[head]["ms"] / 1e3
     value = upd_bytes / bf_s / 1e9
-    F, B = step_cost(cfg, "bf")
+    F, B = step_cost(cfg, head)
     step_roof_s = max(B / PEAK_HBM, F / mfma_peak(cfg))
 
     out = {
@@ -384,7 +410,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(res["bf"]["ms"], 4),
+        "ms_per_step": round(res[head]["ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -392,21 +418,25 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "global_batch": cfg["batch"],
                    "layers": describe_layers(cfg),
-                   "optimizer": kind, "ordering": "backward-fusion",
+                   "optimizer": kind,
+                   "ordering": ("backward-fusion, data gradient merged into the update"
+                                if head == "bfm" else "backward-fusion"),
                    "parallelism": "single-gpu"},
         "eager_ms_per_step": round(res["eager"]["ms"], 4),
         "ff_ms_per_step": round(res["ff"]["ms"], 4),
         "bf_ms_per_step": round(res["bf"]["ms"], 4),
         "speedup_bf_vs_eager": round(res["eager"]["ms"] / res["bf"]["ms"], 4),
         "speedup_ff_vs_eager": round(res["eager"]["ms"] / res["ff"]["ms"], 4),
+        **({"bfm_ms_per_step": round(res["bfm"]["ms"], 4),
+            "speedup_bfm_vs_eager": round(res["eager"]["ms"] / res["bfm"]["ms"], 4)}
+           if mergeable else {}),
         "ms_per_step_graph_replay": {o: (round(r["ms_graph"], 4) if r["ms_graph"] else None)
                                      for o, r in res.items()},
         "host_ms_per_step": {o: round(r["host_ms"], 4) for o, r in res.items()},
         "timing": "steps launched from the host scheduler; graph replay reported beside",
         "step_roofline": {"flops": F, "bytes": B, "roofline_ms": round(step_roof_s * 1e3, 5),
                           "frac": round(step_roof_s / bf_s, 4)},
-        "update_bytes_per_step": {o: n_params * state_bytes_per_param(kind, o)
-                                  for o in ("eager", "ff", "bf")},
+        "update_bytes_per_step": {o: n_params * state_bytes_per_param(kind, o) for o in res},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -162,7 +162,8 @@ typedef struct of_conv_desc {
 typedef enum of_linear_op {
   OF_LINEAR_FWD = 0,        /* of_linear_fwd, of_linear_fwd_fused */
   OF_LINEAR_BWD_DATA = 1,   /* of_linear_bwd_data, the dgrad half of of_linear_bwd_fused */
-  OF_LINEAR_BWD_WEIGHT = 2  /* of_linear_bwd_weight, the wgrad half of of_linear_bwd_fused */
+  OF_LINEAR_BWD_WEIGHT = 2, /* of_linear_bwd_weight, the wgrad half of of_linear_bwd_fused */
+  OF_LINEAR_BWD_MERGED = 3  /* of_linear_bwd_merged (0 when the descriptor is unsupported there) */
 } of_linear_op;
 
 typedef enum of_conv_op {
@@ -270,6 +271,32 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
                               int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
                               void* ws_update, size_t ws_update_bytes, void* stream,
                               void* update_stream);
+
+/*
+ * Backward-fusion with the data gradient merged into the update's read of W
+ * (Section 3 "Backward-Fusion": the parameter reads of the input-gradient
+ * computation and of the optimizer are merged into one).  Computes what
+ * of_linear_bwd_fused computes, in one pass over W, m, v:
+ *   dX = (dZ W_old) * act_prev'(prev)   (if dx_prev != NULL)
+ *   W, m, v <- update(W, dZ^T X (+ gW_partial), m, v)
+ *   b, m, v <- update(b, sum over rows of dZ (+ gb_partial), ...)  (if b != NULL)
+ * Each W element is read once, used by the data gradient (old value, so the
+ * dependency rule after Alg. 3 holds within the kernel) and by the update, and
+ * written once; dW is never stored.  The data gradient is summed over row
+ * ranges of W in a fixed order, so results are deterministic, but they are
+ * rounded differently from of_linear_bwd_fused's (not bit-identical to it).
+ * Supported: dtype OF_F32, M <= 64 (the parameter-bound case), K, ldx and ldy
+ * <= 2^22; otherwise OF_EUNSUPPORTED.
+ * Arguments as in of_linear_bwd_fused; prev and dx_prev have row stride ldx.
+ * ws: at least of_linear_workspace_size(d, OF_LINEAR_BWD_MERGED) bytes when
+ * dx_prev != NULL (the data-gradient partials), else may be NULL.  Everything
+ * is enqueued on `stream`.
+ */
+of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const float* x,
+                               const of_param* W, const of_param* b, const float* gW_partial,
+                               const float* gb_partial, const of_opt* opt, const float* prev,
+                               int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
+                               void* stream);
 
 /* ------------------------------------------------- convolution layers */
 /*

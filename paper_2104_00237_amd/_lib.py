@@ -18,7 +18,7 @@ STATUS_NAMES = {0: "OF_OK", 1: "OF_EINVAL", 2: "OF_EUNSUPPORTED", 3: "OF_EALIGN"
 OF_F32, OF_BF16 = 0, 1
 OF_ACT_NONE, OF_ACT_RELU, OF_ACT_GELU = 0, 1, 2
 OF_OPT_SGD, OF_OPT_ADAM, OF_OPT_ADAMW = 0, 1, 2
-OF_LINEAR_FWD, OF_LINEAR_BWD_DATA, OF_LINEAR_BWD_WEIGHT = 0, 1, 2
+OF_LINEAR_FWD, OF_LINEAR_BWD_DATA, OF_LINEAR_BWD_WEIGHT, OF_LINEAR_BWD_MERGED = 0, 1, 2, 3
 OF_CONV_FWD, OF_CONV_BWD_DATA, OF_CONV_BWD_WEIGHT = 0, 1, 2
 ACTS = {"none": OF_ACT_NONE, "relu": OF_ACT_RELU, "gelu": OF_ACT_GELU}
 OPT_KINDS = {"sgd": OF_OPT_SGD, "adam": OF_OPT_ADAM, "adamw": OF_OPT_ADAMW}
@@ -90,6 +90,9 @@ _SIGS = {
                                       P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
                                       c_int32, c_void_p, c_void_p, c_size_t, c_void_p, c_size_t,
                                       c_void_p, c_void_p]),
+    "of_linear_bwd_merged": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, P(OfParam),
+                                       P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
+                                       c_int32, c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_elementwise_fused_update": (c_int32, [P(OfParam), c_void_p, c_int64, c_int64,
                                               P(OfOpt), c_void_p]),
     "of_optimizer_step": (c_int32, [c_int32, P(OfParam), P(c_void_p), P(OfOpt), c_void_p]),
@@ -185,7 +188,7 @@ def of_layernorm_partial_rows(M):
 
 
 for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
-           "of_linear_bwd_fused", "of_elementwise_fused_update", "of_optimizer_step",
+           "of_linear_bwd_fused", "of_linear_bwd_merged", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
            "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_layernorm_fwd", "of_layernorm_bwd",

@@ -249,6 +249,23 @@ size_t gemm_bf16_workspace_bytes(int kind, int P, int Q, int R);
 hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                             hipStream_t stream);
 
+// Backward-fusion of a linear layer with at most 64 token rows whose data
+// gradient is merged into the update's read of W (fp32 operands).
+struct MergedLaunch {
+  const float* dz; int64_t ldz;     // dZ [M, ldz]
+  const float* x; int64_t ldx;      // X [M, ldx]; also the row stride of prev and dx
+  of_param W; const float* gW;      // gW: extra gradient of earlier uses (or NULL)
+  of_param b; const float* gb;      // b.w == NULL: no bias
+  OptK opt;
+  const float* prev; int act_prev;  // the previous layer's saved tensor and activation
+  float* dx;                        // NULL: no data gradient
+  float* part;                      // workspace: merged_workspace_bytes(M, N, K)
+  int M, N, K;
+};
+constexpr int kMergedMaxM = 64;
+size_t merged_workspace_bytes(int M, int N, int K);
+hipError_t merged_bwd_launch(const MergedLaunch& L, hipStream_t stream);
+
 // ------------------------------------------------------ elementwise / losses
 hipError_t launch_multi_update(int n, const of_param* params, const float* const* grads,
                                const OptK& o, hipStream_t stream);

@@ -316,11 +316,25 @@ int of_version(void) { return OF_VERSION; }
 
 const char* of_last_error(void) { return g_err.c_str(); }
 
+// The merged backward's supported descriptors.
+of_status check_merged(const of_linear_desc* d) {
+  REQUIRE(d->dtype == OF_F32, OF_EUNSUPPORTED, "of_linear_bwd_merged takes fp32 operands only");
+  REQUIRE(d->M <= kMergedMaxM, OF_EUNSUPPORTED, "of_linear_bwd_merged needs M <= %d (got %lld)",
+          kMergedMaxM, (long long)d->M);
+  REQUIRE(d->K <= (1LL << 22) && ldx_of(d) <= (1LL << 22) && ldy_of(d) <= (1LL << 22),
+          OF_EUNSUPPORTED, "of_linear_bwd_merged needs K, ldx and ldy <= 2^22");
+  return OF_OK;
+}
+
 size_t of_linear_workspace_size(const of_linear_desc* d, int32_t op) {
   if (check_linear(d) != OF_OK) return 0;
-  if (op < OF_LINEAR_FWD || op > OF_LINEAR_BWD_WEIGHT) {
+  if (op < OF_LINEAR_FWD || op > OF_LINEAR_BWD_MERGED) {
     fail(OF_EINVAL, "op %d is not an of_linear_op", (int)op);
     return 0;
+  }
+  if (op == OF_LINEAR_BWD_MERGED) {
+    if (check_merged(d) != OF_OK) return 0;
+    return merged_workspace_bytes((int)d->M, (int)d->N, (int)d->K);
   }
   return ws_needed(d, kind_of(op));
 }
@@ -474,6 +488,45 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
   ea.opt = make_optk(*opt);
   return hip_status(gemm_dispatch(d, EPI_WGRAD_BF, wgrad_problem(d, dz, x), ea, ws_update, su),
                     "of_linear_bwd_fused launch");
+}
+
+of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const float* x,
+                               const of_param* W, const of_param* b, const float* gW_partial,
+                               const float* gb_partial, const of_opt* opt, const float* prev,
+                               int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
+                               void* stream) {
+  of_status st = check_linear(d);
+  if (st != OF_OK) return st;
+  if ((st = check_merged(d)) != OF_OK) return st;
+  if ((st = check_opt(opt)) != OF_OK) return st;
+  REQUIRE(dz && x, OF_EINVAL, "dz and x are required");
+  if ((st = check_param(W, "W", d->N * d->K, opt->kind, true)) != OF_OK) return st;
+  if (b) {
+    if ((st = check_param(b, "b", d->N, opt->kind, true)) != OF_OK) return st;
+  }
+  REQUIRE(al4(dz) && al4(x) && al4(gW_partial) && al4(gb_partial) && al4(dx_prev) && al4(prev),
+          OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_shadow(d, W)) != OF_OK) return st;
+  const size_t need = merged_workspace_bytes((int)d->M, (int)d->N, (int)d->K);
+  if (dx_prev) {
+    if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
+    REQUIRE(ws_bytes >= need, OF_EWORKSPACE,
+            "workspace of %zu bytes is smaller than the %zu needed", ws_bytes, need);
+    REQUIRE(ws != nullptr, OF_EWORKSPACE, "workspace is NULL");
+    REQUIRE((((uintptr_t)ws) & 15u) == 0, OF_EALIGN, "workspace must be 16-byte aligned");
+  }
+  MergedLaunch L;
+  L.dz = dz; L.ldz = ldy_of(d);
+  L.x = x; L.ldx = ldx_of(d);
+  L.W = *W; L.gW = gW_partial;
+  if (b) { L.b = *b; } else { memset(&L.b, 0, sizeof(L.b)); }
+  L.gb = b ? gb_partial : nullptr;
+  L.opt = make_optk(*opt);
+  L.prev = prev; L.act_prev = act_prev;
+  L.dx = dx_prev;
+  L.part = (float*)ws;
+  L.M = (int)d->M; L.N = (int)d->N; L.K = (int)d->K;
+  return hip_status(merged_bwd_launch(L, (hipStream_t)stream), "of_linear_bwd_merged launch");
 }
 
 size_t of_conv_workspace_size(const of_conv_desc* d, int32_t op) {

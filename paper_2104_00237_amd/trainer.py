@@ -144,8 +144,15 @@ class LinearOp:
         # MI355X: with 1024x1024 layers the two-stream step is bound by its host
         # calls, and the overlap gains less than they cost).
         self.overlap_update = N * K >= (1 << 22) or 2.0 * M * N * K >= 4e9
+        # Backward-fusion with the data gradient merged into the update's read
+        # of W (of_linear_bwd_merged): fp32 layers with M <= 64 rows, when the
+        # trainer asks for it.
+        self.merge_ok = dtype == L.OF_F32 and M <= 64
+        self.merge_dgrad = False
 
     def ws(self, which):
+        if which == L.OF_LINEAR_BWD_MERGED and not self.merge_ok:
+            return 0
         return L.of_linear_workspace_size(self.desc, which)
 
     def fwd(self, tr, x, y, z=None, carry=None):
@@ -175,6 +182,12 @@ class LinearOp:
         b = self.b
         L.of_linear_bwd_fused(self.desc, g, x, self.W.p, b.p if b else None, None, None, tr.opt,
                               None, 0, None, None, 0, *tr.ws_side_args(), stream, None)
+
+    def bwd_merged(self, tr, g, x, prev, act_prev, dx):
+        """Data gradient (old W) and fused update in one pass over W, m, v."""
+        b = self.b
+        L.of_linear_bwd_merged(self.desc, g, x, self.W.p, b.p if b else None, None, None,
+                               tr.opt, prev, act_prev, dx, *tr.ws_main_args(), tr._s())
 
     def bwd_fused(self, tr, g, x, prev, act_prev, dx):
         """Data gradient on the main stream, then the fused update: on the side
@@ -392,7 +405,13 @@ class ChainNet:
         timed = tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad"))
         for i in reversed(range(len(self.ops))):
             op = self.ops[i]
-            if op.kind == "linear" and not timed:
+            if op.kind == "linear" and op.merge_dgrad:
+                # one kernel reads W once for the data gradient and the update
+                dx, prev, act_prev = self._dgrad_target(i) if i > 0 else (None, None, 0)
+                tr._t0("wgrad_bf", tr.stream, op)
+                op.bwd_merged(tr, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx)
+                tr._t1("wgrad_bf", tr.stream)
+            elif op.kind == "linear" and not timed:
                 # one library call: dgrad with the old W on the main stream, then
                 # the fused update on the side stream behind an event
                 dx, prev, act_prev = self._dgrad_target(i) if i > 0 else (None, None, 0)
@@ -609,7 +628,9 @@ class TBlockNet:
 class Trainer:
     """Trains one workload on one GPU under a chosen ordering."""
 
-    def __init__(self, cfg, init, device="cuda:0"):
+    def __init__(self, cfg, init, device="cuda:0", merge_dgrad=False):
+        """merge_dgrad: backward-fusion runs each fp32 linear layer with at most
+        64 rows as one merged data-gradient + update pass (of_linear_bwd_merged)."""
         L.load()
         self.cfg, self.hyper = cfg, cfg["opt"]
         self.device = torch.device(device)
@@ -631,8 +652,13 @@ class Trainer:
             raise NotImplementedError(f"model kind {cfg['kind']!r} has no GPU path in this build")
         self.ops = self.net.ops
         self.eager_reduce = True
+        for op in self.ops:
+            if op.kind == "linear" and merge_dgrad and op.merge_ok:
+                op.merge_dgrad = True
         f32 = dict(dtype=torch.float32, device=self.device)
         wsm = max([op.ws(w) for op in self.ops for w in (0, 1, 2)] + [16])
+        wsm = max([wsm] + [op.ws(L.OF_LINEAR_BWD_MERGED) for op in self.ops if op.kind == "linear"
+                           and op.merge_dgrad])
         wss = max([op.ws(2) for op in self.ops] + [16])
         if cfg["loss"] == "mse":
             wsm = max(wsm, L.of_mse_workspace_size(*self.net.out.shape))

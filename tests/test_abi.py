@@ -122,6 +122,37 @@ def test_fused_entry_validation(lib):
     assert "step" in L.of_last_error()
 
 
+def test_merged_entry_validation(lib):
+    opt = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 1)
+    d = _desc(M=64, N=8192, K=8192)
+    W = _param(8192 * 8192)
+    need = L.of_linear_workspace_size(d, L.OF_LINEAR_BWD_MERGED)
+    # partials of a few row ranges: more than nothing, at most an eighth of W
+    assert 64 * 8192 * 4 <= need <= 8192 * 8192 * 4 // 8
+    args = (FAKE, FAKE, W, None, None, None, opt, None, L.OF_ACT_NONE)
+    assert _status(L.of_linear_bwd_merged, d, *args, FAKE, FAKE, need - 4, None) == L.OF_EWORKSPACE
+    assert _status(L.of_linear_bwd_merged, d, *args, FAKE, None, need, None) == L.OF_EWORKSPACE
+    assert _status(L.of_linear_bwd_merged, d, *args, FAKE, FAKE + 8, need, None) == L.OF_EALIGN
+    # unsupported: more than 64 token rows, bf16 operands, very wide rows
+    for bad in (_desc(M=65, N=8192, K=8192), _desc(M=64, N=8192, K=8192, dtype=L.OF_BF16),
+                _desc(M=8, N=4, K=(1 << 22) + 1)):
+        Wb = _param(bad.N * bad.K)
+        assert L.of_linear_workspace_size(bad, L.OF_LINEAR_BWD_MERGED) == 0
+        assert _status(L.of_linear_bwd_merged, bad, FAKE, FAKE, Wb, None, None, None, opt, None,
+                       L.OF_ACT_NONE, FAKE, FAKE, 1 << 30, None) == L.OF_EUNSUPPORTED
+    # the usual argument errors
+    assert _status(L.of_linear_bwd_merged, d, None, FAKE, W, None, None, None, opt, None, 0,
+                   None, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_bwd_merged, d, FAKE, FAKE, _param(7), None, None, None, opt, None,
+                   0, None, None, 0, None) == L.OF_EINVAL
+    assert _status(L.of_linear_bwd_merged, d, FAKE, FAKE, W, None, None, None, opt, None,
+                   L.OF_ACT_RELU, FAKE, FAKE, need, None) == L.OF_EINVAL  # ReLU needs prev
+    assert _status(L.of_linear_bwd_merged, d, FAKE, FAKE, W, _param(3), None, None, opt, None, 0,
+                   None, None, 0, None) == L.OF_EINVAL  # bias of the wrong size
+    opt.step = 0
+    assert _status(L.of_linear_bwd_merged, d, *args, FAKE, FAKE, need, None) == L.OF_EINVAL
+
+
 def test_loss_validation(lib):
     assert _status(L.of_xent_fwd_bwd, FAKE, FAKE, 0, 10, 0, FAKE, FAKE, None) == L.OF_EINVAL
     assert _status(L.of_xent_fwd_bwd, FAKE, FAKE + 4, 4, 10, 0, FAKE, FAKE, None) == L.OF_EALIGN
