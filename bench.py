@@ -221,7 +221,8 @@ def traffic_for(kernel_class, workload):
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
-    src = os.path.join(ROOT, "paper_2104_00237_amd", "csrc", "gemm_f32.hip")
+    srcfile = "merged.hip" if kernel_class == "merged_bwd" else "gemm_f32.hip"
+    src = os.path.join(ROOT, "paper_2104_00237_amd", "csrc", srcfile)
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     rec = json.load(open(path)).get(f"{workload}:{kernel_class}")
     if not rec or rec.get("source_sha") != digest:
@@ -393,7 +394,8 @@ def main():
                 bracketed_avg_us=round(float(np.mean(durs)) * 1e3, 3),
                 marker_us=round(marker_ms * 1e3, 3),
                 algorithmic_bytes=per[1], algorithmic_flops=per[0],
-                traffic=traffic_for(dom, args.workload))
+                traffic=traffic_for("merged_bwd" if cost_key == "wgrad_bfm" else dom,
+                                    args.workload))
 
     n_params = sum(d["nparams"] for d in launches.values())
     kind = cfg["opt"]["kind"]
