@@ -48,6 +48,8 @@ SHAPES = [  # (M, N, K): tails in every dimension, split reductions, tiny and wi
     (300, 1030, 1001), (290, 1028, 1100),
     # few output tiles and a long reduction: direct tiles with a split
     (100, 50, 3000), (200, 30, 2050),
+    # at most 64 rows against a wide weight: ragged columns and reduction splits
+    (33, 1030, 2052), (17, 600, 4000), (1, 2048, 1024),
 ]
 
 
@@ -238,7 +240,9 @@ def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
 
 
 @pytest.mark.parametrize("M,N,K", [(72, 168, 200), (256, 1024, 1024), (64, 520, 520), (33, 10, 27),
-                                   (256, 300, 130), (1, 8, 4)])
+                                   (256, 300, 130), (1, 8, 4),
+                                   # a wide weight and at most 64 rows: split reductions
+                                   (64, 2048, 4096), (33, 1030, 2052), (17, 600, 4000)])
 @pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"])
 def test_fwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     """Forward-fusion (Alg. 2): the pending update is applied while W is loaded and
@@ -287,6 +291,27 @@ def test_fwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
         np.testing.assert_array_equal(Ye.cpu().numpy(), Y.cpu().numpy())
     else:
         assert rel(Ye.cpu().numpy(), Y.cpu().numpy()) <= TOL
+
+
+@pytest.mark.parametrize("ldx", [4097, 4100])
+def test_forward_row_strides(env, ldx):
+    """A 64-row forward over a 2048 x 4096 weight with X rows of stride ldx: 4100
+    keeps 128-bit operand loads, 4097 does not; the workspace query covers both."""
+    torch, L, dev = env
+    M, N, K = 64, 2048, 4096
+    r = _rng(ldx)
+    xf = r.standard_normal((M, ldx)).astype(np.float32)
+    w = (r.standard_normal((N, K)) * 0.05).astype(np.float32)
+    b = r.standard_normal(N).astype(np.float32)
+    z = xf[:, :K].astype(np.float64) @ w.astype(np.float64).T + b
+    d = L.OfLinearDesc(M, N, K, ldx, 0, L.OF_F32, L.OF_ACT_NONE, 1)
+    X, Wt, Bt = _t(torch, dev, xf), _t(torch, dev, w), _t(torch, dev, b)
+    Y = torch.full((M, N), float("nan"), device=dev)
+    ws = _ws(torch, dev, L.of_linear_workspace_size(d, L.OF_LINEAR_FWD))
+    L.of_linear_fwd(d, X.data_ptr(), L.OfParam(Wt.data_ptr(), None, None, None, N * K),
+                    Bt.data_ptr(), None, Y.data_ptr(), ws.data_ptr(), ws.numel() * 4, 0)
+    torch.cuda.synchronize()
+    assert rel(Y.cpu().numpy(), z) <= TOL
 
 
 @pytest.mark.parametrize("B,C", [(32, 10), (256, 10), (300, 17), (1, 1)])
