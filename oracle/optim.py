@@ -15,11 +15,25 @@ adam  Adam (Kingma & Ba, Alg. 1; the optimizer of the paper's experimental
 adamw Adam with decoupled weight decay (Loshchilov & Hutter):
           theta <- theta * (1 - eta * wd), then the Adam step on the raw g.
 
+adagrad, rmsprop, adadelta  the other optimizers of the paper's comparison
+      (Section 4, "Various Models and Optimizers", Fig. 7: SGD, SGD with
+      momentum, Adagrad, RMSprop, Adam, Adadelta, weight decay applied unless
+      stated).  The paper gives no formulas; these are the published methods
+      (Duchi et al. 2011; Tieleman & Hinton's RMSprop; Zeiler 2012) in the form
+      PyTorch implements them, with coupled weight decay g' = g + wd * theta:
+      adagrad   v += g'^2;  theta -= eta * g' / (sqrt(v) + eps)
+      rmsprop   v = alpha v + (1 - alpha) g'^2;  s = g' / (sqrt(v) + eps)
+                momentum 0: theta -= eta * s;  else m = momentum m + s, theta -= eta * m
+      adadelta  v = rho v + (1 - rho) g'^2;  d = sqrt(m + eps) / sqrt(v + eps) * g'
+                m = rho m + (1 - rho) d^2;  theta -= eta * d
+      (v: squared-gradient state, m: momentum buffer or squared-update state).
+
 clip_scale  the global-norm clipping factor (forward-fusion's global-information
       step; see its docstring).
 
 Pinned by: closed forms on hand-set tensors (constant gradient) in
-tests/test_oracle_optim.py; clip_scale by a 3-4-5 closed form, the norm of the
+tests/test_oracle_optim.py, where adagrad, rmsprop and adadelta are also run
+against torch.optim's implementations in float64; clip_scale by a 3-4-5 closed form, the norm of the
 concatenated gradients (numpy.linalg.norm) and the clipped norm in
 tests/test_oracle_clip.py.
 """
@@ -46,7 +60,32 @@ def adamw(theta, g, m, v, step, lr, beta1, beta2, eps, weight_decay, **_):
     return adam(theta, g, m, v, step, lr, beta1, beta2, eps, 0.0)
 
 
-POLICIES = {"sgd": sgd, "adam": adam, "adamw": adamw}
+def adagrad(theta, g, m, v, step, lr, eps, weight_decay=0.0, **_):
+    g = g + weight_decay * theta
+    v = v + g * g
+    return theta - lr * g / (np.sqrt(v) + eps), m, v
+
+
+def rmsprop(theta, g, m, v, step, lr, alpha, eps, weight_decay=0.0, momentum=0.0, **_):
+    g = g + weight_decay * theta
+    v = alpha * v + (1.0 - alpha) * g * g
+    s = g / (np.sqrt(v) + eps)
+    if momentum != 0.0:
+        m = momentum * m + s
+        return theta - lr * m, m, v
+    return theta - lr * s, m, v
+
+
+def adadelta(theta, g, m, v, step, lr, rho, eps, weight_decay=0.0, **_):
+    g = g + weight_decay * theta
+    v = rho * v + (1.0 - rho) * g * g
+    d = np.sqrt(m + eps) / np.sqrt(v + eps) * g
+    m = rho * m + (1.0 - rho) * d * d
+    return theta - lr * d, m, v
+
+
+POLICIES = {"sgd": sgd, "adam": adam, "adamw": adamw, "adagrad": adagrad, "rmsprop": rmsprop,
+            "adadelta": adadelta}
 
 
 def clip_scale(grads, max_norm):

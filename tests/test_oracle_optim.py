@@ -100,3 +100,66 @@ def test_adam_zero_gradient_no_motion():
     _, traj = _run("adam", [0.4, -0.2], [[0.0, 0.0]] * 3, lr=1e-3, beta1=0.9, beta2=0.999,
                    eps=1e-8, weight_decay=0.0)
     np.testing.assert_array_equal(traj[-1], [0.4, -0.2])
+
+
+# ---------------------------------------------------------------- Fig. 7's other optimizers
+def test_adagrad_constant_gradient_closed_form():
+    # With wd = 0 and a constant g the accumulated sum after s updates is s g^2, so
+    # theta_t = theta_0 - eta * sum_{s=1..t} g / (sqrt(s) |g| + eps).
+    g, eta, eps, T = np.array([0.5, -2.0, 1e-3]), 0.1, 1e-10, 7
+    _, traj = _run("adagrad", [1.0, 1.0, 1.0], [g] * T, lr=eta, eps=eps, weight_decay=0.0)
+    s = np.arange(1, T + 1)[:, None]
+    want = 1.0 - eta * np.cumsum(g / (np.sqrt(s) * np.abs(g) + eps), axis=0)
+    np.testing.assert_allclose(np.array(traj), want, rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("momentum", [0.0, 0.9])
+def test_rmsprop_constant_gradient_closed_form(momentum):
+    # With wd = 0 and a constant g: v_s = (1 - alpha^s) g^2, so each step's
+    # normalised gradient is u_s = g / (sqrt(1 - alpha^s) |g| + eps); without
+    # momentum theta moves by -eta u_s, with it by -eta sum_{r<=s} mu^(s-r) u_r.
+    g, eta, alpha, eps, T = np.array([0.3, -4.0]), 0.01, 0.99, 1e-8, 6
+    _, traj = _run("rmsprop", [0.0, 0.0], [g] * T, lr=eta, alpha=alpha, eps=eps,
+                   momentum=momentum, weight_decay=0.0)
+    s = np.arange(1, T + 1)[:, None]
+    u = g / (np.sqrt(1.0 - alpha ** s) * np.abs(g) + eps)
+    buf = np.array([sum(momentum ** (t - r) * u[r] for r in range(t + 1)) for t in range(T)])
+    want = -eta * np.cumsum(buf if momentum else u, axis=0)
+    np.testing.assert_allclose(np.array(traj), want, rtol=1e-12, atol=1e-15)
+
+
+def test_adadelta_first_step_closed_form():
+    # From m = v = 0: v_1 = (1 - rho) g^2 and d_1 = sqrt(eps / ((1 - rho) g^2 + eps)) g,
+    # so with g^2 >> eps the first move is about sqrt(eps / (1 - rho)) sign(g).
+    g, rho, eps, lr = np.array([2.0, -0.5, 0.0]), 0.9, 1e-6, 1.0
+    p, traj = _run("adadelta", [0.0, 0.0, 0.0], [g], lr=lr, rho=rho, eps=eps, weight_decay=0.0)
+    d1 = np.sqrt(eps / ((1.0 - rho) * g * g + eps)) * g
+    np.testing.assert_allclose(traj[0], -lr * d1, rtol=1e-14, atol=0)
+    np.testing.assert_allclose(p.m, (1.0 - rho) * d1 * d1, rtol=1e-14, atol=0)
+    assert traj[0][2] == 0.0   # zero gradient: no move
+
+
+@pytest.mark.parametrize("kind,hyper,torch_cls,torch_kw", [
+    ("adagrad", dict(lr=0.05, eps=1e-10, weight_decay=1e-2), "Adagrad",
+     dict(lr=0.05, eps=1e-10, weight_decay=1e-2)),
+    ("rmsprop", dict(lr=0.01, alpha=0.99, eps=1e-8, weight_decay=1e-3, momentum=0.0), "RMSprop",
+     dict(lr=0.01, alpha=0.99, eps=1e-8, weight_decay=1e-3)),
+    ("rmsprop", dict(lr=0.01, alpha=0.9, eps=1e-8, weight_decay=1e-3, momentum=0.8), "RMSprop",
+     dict(lr=0.01, alpha=0.9, eps=1e-8, weight_decay=1e-3, momentum=0.8)),
+    ("adadelta", dict(lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-2), "Adadelta",
+     dict(lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-2)),
+])
+def test_fig7_optimizers_match_torch_optim(kind, hyper, torch_cls, torch_kw):
+    """The same published methods as implemented by torch.optim (float64, CPU),
+    over random gradients with coupled weight decay."""
+    import torch
+    rng = np.random.default_rng(11)
+    th0 = rng.standard_normal(64)
+    gs = rng.standard_normal((8, 64))
+    p, traj = _run(kind, th0, gs, **hyper)
+    t = torch.tensor(th0, dtype=torch.float64, requires_grad=True)
+    opt = getattr(torch.optim, torch_cls)([t], **torch_kw)
+    for i, g in enumerate(gs):
+        t.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        np.testing.assert_allclose(traj[i], t.detach().numpy(), rtol=1e-12, atol=1e-14)
