@@ -40,6 +40,17 @@ PEAK_BF16_MFMA = 2.5e15    # flop/s, dense
 
 METRIC = "fused train-step time & update GB/s vs unfused eager; % of HBM/MFMA roofline"
 
+# --optimizer: the workload with another of the optimizers Fig. 7 compares
+# (PyTorch's default hyperparameters; weight decay applied, as in the figure).
+FIG7_OPTIMIZERS = {
+    "sgd": dict(kind="sgd", lr=0.01, momentum=0.0, weight_decay=1e-4),
+    "sgd_momentum": dict(kind="sgd", lr=0.01, momentum=0.9, weight_decay=1e-4),
+    "adagrad": dict(kind="adagrad", lr=0.01, eps=1e-10, weight_decay=1e-4),
+    "rmsprop": dict(kind="rmsprop", lr=0.01, alpha=0.99, eps=1e-8, weight_decay=1e-4),
+    "adam": dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-4),
+    "adadelta": dict(kind="adadelta", lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-4),
+}
+
 
 # ----------------------------------------------------------------- cost model
 def state_bytes_per_param(kind, ordering):
@@ -299,6 +310,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mlp8x1024")
+    ap.add_argument("--optimizer", choices=sorted(FIG7_OPTIMIZERS), default=None,
+                    help="replace the workload's optimizer (Fig. 7's set)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -322,6 +335,8 @@ def main():
 
     import torch
     cfg = get_config(args.workload)
+    if args.optimizer:
+        cfg = dict(cfg, opt=FIG7_OPTIMIZERS[args.optimizer])
     if cfg["kind"] not in ("mlp", "vgg", "tblock"):
         print(f"workload {args.workload} has no GPU path in this build", file=sys.stderr)
         sys.exit(2)
@@ -420,7 +435,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "global_batch": cfg["batch"],
                    "layers": describe_layers(cfg),
-                   "optimizer": kind,
+                   "optimizer": args.optimizer or kind,
                    "ordering": ("backward-fusion, data gradient merged into the update"
                                 if head == "bfm" else "backward-fusion"),
                    "parallelism": "single-gpu"},

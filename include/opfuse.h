@@ -77,20 +77,35 @@ typedef enum of_act { OF_ACT_NONE = 0, OF_ACT_RELU = 1, OF_ACT_GELU = 2 } of_act
  *                   m = b1 m + (1-b1) g';  v = b2 v + (1-b2) g'^2
  *                   w -= (lr/(1-b1^t)) * m / (sqrt(v)/sqrt(1-b2^t) + eps)
  *   OF_OPT_ADAMW  w *= (1 - lr*wd), then the Adam step on the raw g.
+ *   The other optimizers of the paper's comparison (Section 4, "Various Models
+ *   and Optimizers", Fig. 7), with coupled weight decay g' = g + wd*w:
+ *   OF_OPT_ADAGRAD   v += g'^2;  w -= lr * g' / (sqrt(v) + eps)
+ *                    (v starts at 0; m is not used but must be given)
+ *   OF_OPT_RMSPROP   v = beta2 v + (1-beta2) g'^2;  s = g' / (sqrt(v) + eps)
+ *                    momentum == 0: w -= lr * s;  else m = momentum m + s, w -= lr * m
+ *                    (beta2 is the smoothing constant alpha)
+ *   OF_OPT_ADADELTA  v = beta2 v + (1-beta2) g'^2
+ *                    d = sqrt((m + eps) / (v + eps)) * g'
+ *                    m = beta2 m + (1-beta2) d^2;  w -= lr * d
+ *                    (beta2 is the decay rate rho; m accumulates squared updates)
+ *   All of them keep v (and m), so every entry point takes them as for Adam.
  *
  * Every kernel that updates a parameter uses one shared per-element update
  * with explicitly rounded operations, so all orderings compute bit-identical
  * values from identical gradients.
  */
-typedef enum of_opt_kind { OF_OPT_SGD = 0, OF_OPT_ADAM = 1, OF_OPT_ADAMW = 2 } of_opt_kind;
+typedef enum of_opt_kind {
+  OF_OPT_SGD = 0, OF_OPT_ADAM = 1, OF_OPT_ADAMW = 2,
+  OF_OPT_ADAGRAD = 3, OF_OPT_RMSPROP = 4, OF_OPT_ADADELTA = 5
+} of_opt_kind;
 
 typedef struct of_opt {
   int32_t kind;
   float lr;
   float weight_decay;
-  float momentum;   /* SGD only */
+  float momentum;   /* SGD, RMSprop */
   float beta1;      /* Adam / AdamW */
-  float beta2;
+  float beta2;      /* Adam / AdamW; RMSprop alpha; Adadelta rho */
   float eps;
   int64_t step;     /* >= 1; ignored when step_dev is not NULL */
   /* Optional device address of the step, read by the kernels when they run
@@ -110,7 +125,8 @@ typedef struct of_opt {
  * A trainable tensor theta with its history (Fig. 2, "History").
  *   w       fp32 master values [numel]
  *   m       SGD momentum buffer or Adam first moment [numel] (required)
- *   v       Adam second moment [numel] (required for Adam/AdamW, ignored for SGD)
+ *   v       Adam second moment, or the squared-gradient state of Adagrad,
+ *           RMSprop and Adadelta [numel] (required unless SGD, ignored for SGD)
  *   w_bf16  optional bf16 copy of w (round to nearest even), rewritten by every
  *           update when not NULL; it is the matmul operand when dtype is OF_BF16
  */

@@ -230,7 +230,7 @@ def candidate_steps(cfg, state, t, max_decisions=8, seed=0):
             loss = model.step_eager(x, y)
             ps = model.params
             vh = {}
-            if cfg["opt"]["kind"] != "sgd":
+            if cfg["opt"]["kind"] in ("adam", "adamw"):
                 for k, p in ps.items():
                     r = np.sqrt(p.v / (1.0 - cfg["opt"]["beta2"] ** p.step))
                     vh[k] = np.where(r > 0.0, r, np.inf)
@@ -347,7 +347,7 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
         clips.append(model.last_clip)
         if t == 1:
             argmax = dict(model.last_argmax)
-        if hyper["kind"] != "sgd":
+        if hyper["kind"] in ("adam", "adamw"):
             for k, p in model.params.items():
                 if p.step > 0:
                     r = np.sqrt(p.v / (1.0 - hyper["beta2"] ** p.step))

@@ -18,10 +18,12 @@ STATUS_NAMES = {0: "OF_OK", 1: "OF_EINVAL", 2: "OF_EUNSUPPORTED", 3: "OF_EALIGN"
 OF_F32, OF_BF16 = 0, 1
 OF_ACT_NONE, OF_ACT_RELU, OF_ACT_GELU = 0, 1, 2
 OF_OPT_SGD, OF_OPT_ADAM, OF_OPT_ADAMW = 0, 1, 2
+OF_OPT_ADAGRAD, OF_OPT_RMSPROP, OF_OPT_ADADELTA = 3, 4, 5
 OF_LINEAR_FWD, OF_LINEAR_BWD_DATA, OF_LINEAR_BWD_WEIGHT, OF_LINEAR_BWD_MERGED = 0, 1, 2, 3
 OF_CONV_FWD, OF_CONV_BWD_DATA, OF_CONV_BWD_WEIGHT = 0, 1, 2
 ACTS = {"none": OF_ACT_NONE, "relu": OF_ACT_RELU, "gelu": OF_ACT_GELU}
-OPT_KINDS = {"sgd": OF_OPT_SGD, "adam": OF_OPT_ADAM, "adamw": OF_OPT_ADAMW}
+OPT_KINDS = {"sgd": OF_OPT_SGD, "adam": OF_OPT_ADAM, "adamw": OF_OPT_ADAMW,
+             "adagrad": OF_OPT_ADAGRAD, "rmsprop": OF_OPT_RMSPROP, "adadelta": OF_OPT_ADADELTA}
 
 c_int32, c_int64, c_float, c_void_p, c_size_t = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                                   ctypes.c_void_p, ctypes.c_size_t)
@@ -201,8 +203,10 @@ def make_opt(hyper, step, step_dev=None, grad_scale=None):
     """of_opt from a workload's optimizer dict and the 1-based update index
     (or a device address holding it), with an optional device address of a
     gradient scale (e.g. the global-norm clipping factor)."""
+    # the squared-gradient decay travels in beta2 (RMSprop's alpha, Adadelta's rho)
+    beta2 = hyper.get("beta2", hyper.get("alpha", hyper.get("rho", 0.0)))
     return OfOpt(OPT_KINDS[hyper["kind"]], hyper["lr"], hyper.get("weight_decay", 0.0),
-                 hyper.get("momentum", 0.0), hyper.get("beta1", 0.0), hyper.get("beta2", 0.0),
+                 hyper.get("momentum", 0.0), hyper.get("beta1", 0.0), beta2,
                  hyper.get("eps", 0.0), step, step_dev, grad_scale)
 
 

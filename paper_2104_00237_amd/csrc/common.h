@@ -55,7 +55,8 @@ __host__ __device__ inline void opt_constants(OptK& o, int64_t t) {
 // A gradient scale given by address is read here too.
 __device__ __forceinline__ void opt_prepare(OptK& o) {
   if (o.gscale_dev) o.gscale = *o.gscale_dev;
-  if (o.kind == OF_OPT_SGD || o.prepared) return;
+  if (o.kind != OF_OPT_ADAM && o.kind != OF_OPT_ADAMW) return;   // no step-dependent constants
+  if (o.prepared) return;
   opt_constants(o, *o.step_dev);
 }
 
@@ -63,6 +64,9 @@ __device__ __forceinline__ void opt_prepare(OptK& o) {
 // (Appendix A, Alg. 1: theta_t = theta_{t-1} + pi(...)).  All operations are
 // explicitly rounded (the sources are also built with -ffp-contract=off), so
 // the same gradient gives the same bits in every ordering and kernel.
+// __fsqrt_rn is the hardware square root (within 1 ulp, the same instruction
+// everywhere); no divisor is a bare square root, which the compiler could turn
+// into a reciprocal-square-root product in some kernels only.
 __device__ __forceinline__ void opt_update(const OptK& o, float& w, float g, float& m, float& v) {
   g = __fmul_rn(g, o.gscale);   // the gradient scale (exact when it is 1)
   if (o.kind == OF_OPT_SGD) {
@@ -70,6 +74,33 @@ __device__ __forceinline__ void opt_update(const OptK& o, float& w, float g, flo
     const float gp = __fmaf_rn(o.wd, w, g);
     m = __fmaf_rn(o.mom, m, gp);
     w = __fmaf_rn(-o.lr, m, w);
+  } else if (o.kind == OF_OPT_ADAGRAD) {
+    // v: running sum of squared gradients.
+    const float gp = __fmaf_rn(o.wd, w, g);
+    v = __fmaf_rn(gp, gp, v);
+    w = __fsub_rn(w, __fdiv_rn(__fmul_rn(o.lr, gp), __fadd_rn(__fsqrt_rn(v), o.eps)));
+  } else if (o.kind == OF_OPT_RMSPROP) {
+    // v: decaying average of squared gradients (decay b2); m: momentum buffer.
+    const float gp = __fmaf_rn(o.wd, w, g);
+    v = __fmaf_rn(o.b2, v, __fmul_rn(__fmul_rn(o.omb2, gp), gp));
+    const float step = __fdiv_rn(gp, __fadd_rn(__fsqrt_rn(v), o.eps));
+    if (o.mom != 0.f) {
+      m = __fmaf_rn(o.mom, m, step);
+      w = __fmaf_rn(-o.lr, m, w);
+    } else {
+      w = __fmaf_rn(-o.lr, step, w);
+    }
+  } else if (o.kind == OF_OPT_ADADELTA) {
+    // v: decaying average of squared gradients; m: of squared updates (decay b2).
+    const float gp = __fmaf_rn(o.wd, w, g);
+    v = __fmaf_rn(o.b2, v, __fmul_rn(__fmul_rn(o.omb2, gp), gp));
+    // sqrt((m + eps) / (v + eps)) rather than a quotient of square roots: a
+    // division by a bare hardware square root may be rewritten as a product
+    // with a reciprocal square root in some kernels and not in others
+    const float delta =
+        __fmul_rn(__fsqrt_rn(__fdiv_rn(__fadd_rn(m, o.eps), __fadd_rn(v, o.eps))), gp);
+    m = __fmaf_rn(o.b2, m, __fmul_rn(__fmul_rn(o.omb2, delta), delta));
+    w = __fmaf_rn(-o.lr, delta, w);
   } else {
     float gp = g;
     if (o.kind == OF_OPT_ADAMW) {

@@ -43,7 +43,7 @@ bool al4(const void* p) { return (((uintptr_t)p) & 3u) == 0; }
 
 of_status check_opt(const of_opt* o) {
   REQUIRE(o != nullptr, OF_EINVAL, "opt is NULL");
-  REQUIRE(o->kind == OF_OPT_SGD || o->kind == OF_OPT_ADAM || o->kind == OF_OPT_ADAMW, OF_EINVAL,
+  REQUIRE(o->kind >= OF_OPT_SGD && o->kind <= OF_OPT_ADADELTA, OF_EINVAL,
           "opt->kind %d is not an of_opt_kind", (int)o->kind);
   REQUIRE(o->step_dev != nullptr || o->step >= 1, OF_EINVAL, "opt->step must be >= 1 (got %lld)",
           (long long)o->step);
@@ -56,6 +56,10 @@ of_status check_opt(const of_opt* o) {
     REQUIRE(o->beta1 >= 0.f && o->beta1 < 1.f && o->beta2 >= 0.f && o->beta2 < 1.f, OF_EINVAL,
             "opt->beta1 / beta2 must be in [0, 1)");
   }
+  if (o->kind == OF_OPT_ADAGRAD || o->kind == OF_OPT_RMSPROP || o->kind == OF_OPT_ADADELTA) {
+    REQUIRE(o->eps > 0.f && std::isfinite(o->eps), OF_EINVAL,
+            "opt->eps must be > 0 for Adagrad, RMSprop and Adadelta");
+  }
   return OF_OK;
 }
 
@@ -65,7 +69,8 @@ of_status check_param(const of_param* p, const char* name, int64_t numel, int ki
           (long long)p->numel, (long long)numel);
   if (need_w) REQUIRE(p->w != nullptr, OF_EINVAL, "%s->w is NULL", name);
   REQUIRE(p->m != nullptr, OF_EINVAL, "%s->m is NULL", name);
-  if (kind != OF_OPT_SGD) REQUIRE(p->v != nullptr, OF_EINVAL, "%s->v is NULL (Adam needs v)", name);
+  if (kind != OF_OPT_SGD)
+    REQUIRE(p->v != nullptr, OF_EINVAL, "%s->v is NULL (every optimizer but SGD needs v)", name);
   REQUIRE(al4(p->w) && al4(p->m) && al4(p->v), OF_EALIGN, "%s arrays must be 4-byte aligned", name);
   REQUIRE((((uintptr_t)p->w_bf16) & 1u) == 0, OF_EALIGN, "%s->w_bf16 must be 2-byte aligned", name);
   return OF_OK;

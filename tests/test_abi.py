@@ -98,6 +98,14 @@ def test_optimizer_validation(lib):
     grads = (ctypes.c_void_p * 2)(FAKE, FAKE)
     assert _status(L.of_optimizer_step, 2, arr, grads, opt, None) == L.OF_EINVAL
     assert _status(L.of_optimizer_step, 0, arr, grads, opt, None) == L.OF_EINVAL
+    # Fig. 7's other optimizers: known kinds, but eps must be positive; v is required
+    for k in ("adagrad", "rmsprop", "adadelta"):
+        o = L.make_opt(dict(kind=k, lr=0.01, eps=0.0), 1)
+        assert _status(L.of_elementwise_fused_update, p, g, 1, 0, o, None) == L.OF_EINVAL
+        assert "eps" in L.of_last_error()
+        o.eps = 1e-8
+        assert _status(L.of_elementwise_fused_update, _param(100, v=None), g, 1, 0, o,
+                       None) == L.OF_EINVAL
     sgd = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1)
     # SGD needs no v; a NULL m is still an error.
     assert _status(L.of_elementwise_fused_update, _param(10, m=None, v=None), g, 1, 0, sgd,

@@ -118,7 +118,12 @@ HYPERS = {
     "sgd": dict(kind="sgd", lr=0.01, momentum=0.9, weight_decay=1e-4),
     "adam": dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0),
     "adamw": dict(kind="adamw", lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01),
+    # the other optimizers of Fig. 7
+    "adagrad": dict(kind="adagrad", lr=0.01, eps=1e-10, weight_decay=1e-4),
+    "rmsprop": dict(kind="rmsprop", lr=1e-3, alpha=0.99, eps=1e-8, weight_decay=1e-4, momentum=0.9),
+    "adadelta": dict(kind="adadelta", lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-4),
 }
+FIG7 = ["adagrad", "rmsprop", "adadelta"]
 
 
 class _Param:
@@ -128,6 +133,13 @@ class _Param:
         r = _rng(seed)
         self.w = r.standard_normal(shape).astype(np.float32) * 0.1
         self.m = r.standard_normal(shape).astype(np.float32) * 0.01 if step > 1 else np.zeros(shape, np.float32)
+        if kind == "adadelta":
+            self.m = np.abs(self.m) * 1e-2   # Adadelta's squared-update state is >= 0
+        if kind in FIG7 and step > 1:
+            # Adagrad / RMSprop divide by sqrt(v): a history with sqrt(v) >= 0.07
+            # keeps the float32 rounding of a contraction's gradient (~1e-7) from
+            # being amplified by 1/sqrt(v) past the tolerance.
+            self.v = ((0.5 + r.random(shape)) * 1e-2).astype(np.float32)
         self.v = (r.random(shape).astype(np.float32) * 1e-4) if (step > 1 and kind != "sgd") else np.zeros(shape, np.float32)
         self.W = _t(torch, dev, self.w)
         self.M = _t(torch, dev, self.m)
@@ -152,7 +164,7 @@ class _Param:
             assert rel(self.V.cpu().numpy(), ref.v) <= tol
 
 
-@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"])
+@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"] + FIG7)
 @pytest.mark.parametrize("step", [1, 7])
 def test_optimizer_step_multi_tensor(env, kind, step):
     torch, L, dev = env
@@ -168,7 +180,7 @@ def test_optimizer_step_multi_tensor(env, kind, step):
         p.check(p.oracle(g, HYPERS[kind]))
 
 
-@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"])
+@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"] + FIG7)
 @pytest.mark.parametrize("rows", [1, 5, 300])
 def test_elementwise_fused_update(env, kind, rows):
     torch, L, dev = env
@@ -188,7 +200,7 @@ def test_elementwise_fused_update(env, kind, rows):
 
 @pytest.mark.parametrize("M,N,K", [(72, 168, 200), (256, 1024, 1024), (64, 520, 520), (33, 10, 27),
                                    (300, 70, 257)])
-@pytest.mark.parametrize("kind", ["sgd", "adam"])
+@pytest.mark.parametrize("kind", ["sgd", "adam"] + FIG7)
 def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     """Backward-fusion (Alg. 3): dgrad with the old W, then the update in the wgrad
     epilogue.  Checked against the oracle, and bit for bit against the eager pair
@@ -243,7 +255,7 @@ def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
                                    (256, 300, 130), (1, 8, 4),
                                    # a wide weight and at most 64 rows: split reductions
                                    (64, 2048, 4096), (33, 1030, 2052), (17, 600, 4000)])
-@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"])
+@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"] + FIG7)
 def test_fwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     """Forward-fusion (Alg. 2): the pending update is applied while W is loaded and
     the forward uses the updated values.  Checked against the oracle and bit for bit

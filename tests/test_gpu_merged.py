@@ -20,6 +20,9 @@ HYPERS = {
     "sgd": dict(kind="sgd", lr=0.01, momentum=0.9, weight_decay=1e-4),
     "adam": dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0),
     "adamw": dict(kind="adamw", lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01),
+    "adagrad": dict(kind="adagrad", lr=0.01, eps=1e-10, weight_decay=1e-4),
+    "rmsprop": dict(kind="rmsprop", lr=1e-3, alpha=0.99, eps=1e-8, weight_decay=1e-4, momentum=0.9),
+    "adadelta": dict(kind="adadelta", lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-4),
 }
 
 
@@ -53,6 +56,12 @@ class _Param:
         r = np.random.default_rng(seed)
         self.w = (r.standard_normal(shape) * 0.1).astype(np.float32)
         self.m = (r.standard_normal(shape) * 0.01).astype(np.float32)
+        if kind == "adadelta":
+            self.m = np.abs(self.m) * 1e-2   # squared-update state is >= 0
+        if kind in ("adagrad", "rmsprop", "adadelta"):
+            # sqrt(v) >= 0.07: the 1/sqrt(v) sensitivity of the update to the
+            # gradient's float32 rounding stays well inside the tolerance
+            self.v = ((0.5 + r.random(shape)) * 1e-2).astype(np.float32)
         self.v = (r.random(shape) * 1e-4).astype(np.float32) if kind != "sgd" else None
         self.W, self.M = _t(torch, dev, self.w), _t(torch, dev, self.m)
         self.V = _t(torch, dev, self.v) if kind != "sgd" else None
@@ -99,7 +108,7 @@ SHAPES = [(64, 520, 520), (33, 10, 27), (1, 8, 4), (32, 128, 64), (64, 2048, 409
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
-@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"])
+@pytest.mark.parametrize("kind", ["sgd", "adam", "adamw", "adagrad", "rmsprop", "adadelta"])
 def test_merged_matches_oracle(env, M, N, K, kind):
     """dX with the OLD W, the update of W and b from dZ^T X and sum(dZ)."""
     torch, L, dev = env

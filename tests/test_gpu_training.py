@@ -279,3 +279,41 @@ def test_tblock_full_size_first_step(gpu):
     for k in ref["params"]:
         np.testing.assert_array_equal(out["bf"]["params"][k], out["eager"]["params"][k])
         np.testing.assert_array_equal(out["bf"]["v"][k], out["eager"]["v"][k])
+
+
+# Adagrad's and RMSprop's first step is g / (|g| sqrt(c) + eps), whose derivative
+# in g is up to 1/eps: eps = 1e-4 keeps float32 gradient rounding (~1e-8 here)
+# far inside the tolerance (with PyTorch's 1e-10 / 1e-8 an element with |g| near
+# eps could move by a sizable fraction of a step in any float32 run).
+FIG7_HYPERS = {
+    "adagrad": dict(kind="adagrad", lr=0.01, eps=1e-4, weight_decay=1e-4),
+    "rmsprop": dict(kind="rmsprop", lr=1e-3, alpha=0.99, eps=1e-4, weight_decay=1e-4, momentum=0.9),
+    "rmsprop_nomom": dict(kind="rmsprop", lr=1e-3, alpha=0.99, eps=1e-4, weight_decay=1e-4),
+    "adadelta": dict(kind="adadelta", lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-4),
+}
+
+
+@pytest.mark.parametrize("opt", sorted(FIG7_HYPERS))
+def test_fig7_optimizer_training(gpu, opt):
+    """The 3-layer MLP trained with each of Fig. 7's other optimizers under the three
+    orderings: every ordering against the oracle's eager run, and bit for bit
+    against the GPU's eager run (the update is the same per-element arithmetic)."""
+    import torch
+    cfg = dict(get_config("mlp3"), opt=FIG7_HYPERS[opt])
+    K = cfg["steps"]
+    ref = oracle.run(cfg, "eager", steps=K)
+    runs = {o: _gpu_run(torch, cfg, o, K, gpu) for o in ("eager", "ff", "bf")}
+    for o, st in runs.items():
+        assert rel(st["losses"], ref["losses"]) <= TOL, (o, st["losses"], ref["losses"])
+        assert abs(st["eval_loss"] - ref["eval_loss"]) <= TOL * abs(ref["eval_loss"])
+        for k in ref["params"]:
+            check_param(st["params"][k], ref["params"][k], cfg["opt"], K, TOL, None,
+                        what=f"{o} {k}")
+            assert rel(st["m"][k], ref["m"][k]) <= TOL, (o, k)
+            assert rel(st["v"][k], ref["v"][k]) <= TOL, (o, k)
+            assert st["step"][k] == ref["step"][k] == K
+    for o in ("ff", "bf"):
+        np.testing.assert_array_equal(runs[o]["losses"], runs["eager"]["losses"])
+        for k in ref["params"]:
+            np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
+            np.testing.assert_array_equal(runs[o]["v"][k], runs["eager"]["v"][k])
