@@ -312,6 +312,8 @@ def main():
     ap.add_argument("--workload", default="mlp8x1024")
     ap.add_argument("--optimizer", choices=sorted(FIG7_OPTIMIZERS), default=None,
                     help="replace the workload's optimizer (Fig. 7's set)")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="replace the workload's batch (rows per step; Figs. 4-5 sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -337,6 +339,8 @@ def main():
     cfg = get_config(args.workload)
     if args.optimizer:
         cfg = dict(cfg, opt=FIG7_OPTIMIZERS[args.optimizer])
+    if args.batch:
+        cfg = dict(cfg, batch=args.batch)
     if cfg["kind"] not in ("mlp", "vgg", "tblock"):
         print(f"workload {args.workload} has no GPU path in this build", file=sys.stderr)
         sys.exit(2)

@@ -290,13 +290,16 @@ __global__ __launch_bounds__(256) void merged_dx_kernel(const float* __restrict_
 }  // namespace
 
 // Row ranges for an M x N x K layer: about two workgroups per compute unit
-// (512 in all), with the partials (S * M * K) at most an eighth of W, and
-// `per` whole chunks of MG_BN rows per range.
+// (512 in all) and `per` whole chunks of MG_BN rows per range.  A W of more
+// than 64 MB (streamed from HBM) keeps the partials (S * M * K) at most an
+// eighth of W; a smaller one stays in the caches and takes as many ranges as
+// the workgroup target asks (a 1024 x 1024 layer would otherwise run on 16
+// workgroups).
 void merged_plan(int M, int N, int K, int* S, int* per) {
   const int strips = (K + MG_BK - 1) / MG_BK;
   const int chunks = (N + MG_BN - 1) / MG_BN;
   int s = std::max(1, (512 + strips - 1) / strips);
-  s = std::min(s, std::max(1, N / (8 * M)));
+  if ((int64_t)N * K * 4 > (64LL << 20)) s = std::min(s, std::max(1, N / (8 * M)));
   s = std::min(s, chunks);
   *per = (chunks + s - 1) / s;
   *S = (chunks + *per - 1) / *per;
