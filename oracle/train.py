@@ -49,7 +49,7 @@ import itertools
 
 import numpy as np
 
-from workloads import make_params, make_batch, make_eval_batch
+from workloads import make_params, make_batch, make_eval_batch, mlp_ties
 from . import layers as L
 from .losses import LOSSES
 from .optim import apply as apply_optimizer, clip_scale
@@ -255,10 +255,15 @@ def new_model(cfg, init=None, seed=0):
     kind = cfg["kind"]
     if kind == "mlp":
         n_layers = len(cfg["dims"]) - 1
+        tie = mlp_ties(cfg)
+        lin = {}
         cur = "input"
         for i in range(1, n_layers + 1):
             z = f"z{i}"
-            nodes.append((L.Linear(P(f"fc{i}.weight"), P(f"fc{i}.bias")), [cur], z))
+            # a tied layer is the same operator applied again (one `updated` flag,
+            # its parameters counted once per use)
+            lin[i] = lin[tie[i]] if i in tie else L.Linear(P(f"fc{i}.weight"), P(f"fc{i}.bias"))
+            nodes.append((lin[i], [cur], z))
             cur = z
             if i < n_layers and cfg["act"] == "relu":
                 nodes.append((L.ReLU(), [z], f"a{i}"))

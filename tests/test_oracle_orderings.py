@@ -130,6 +130,8 @@ def test_ff_first_iteration_applies_nothing():
 
 @pytest.mark.parametrize("name,over", [
     ("mlp3", dict(dims=[5, 7, 6, 4], batch=3, classes=4)),
+    # layer 3 applies layer 2's parameters again: their gradient sums both uses
+    ("mlp4tied", dict(dims=[5, 6, 6, 6, 4], batch=3, classes=4)),
     ("linear4x8192", dict(dims=[6] * 5, batch=3)),
     ("tblock12", dict(blocks=2, hidden=6, ffn=10, batch=4, dtype="f32")),
     ("vgg11", dict(channels=[3, 4, 4, 4, 5, 5, 5, 5], batch=2)),
@@ -290,3 +292,22 @@ def test_decision_search_pool_flip_routes_the_gradient():
         apply(p, cfg["opt"])
     for k, p in model.params.items():
         np.testing.assert_array_equal(st["params"][k], p.value)
+
+
+def test_tied_mlp_orderings_and_counts():
+    """The tied MLP workload: eager, forward-fusion and backward-fusion give the same
+    bits, each shared tensor is updated once per step (step = K) and has two forward
+    uses per step, and its gradient is the sum of both uses' contributions (it differs
+    from either use alone)."""
+    cfg = get_config("mlp4tied")
+    runs = {o: run(cfg, o) for o in ("eager", "ff", "bf")}
+    for o in ("ff", "bf"):
+        np.testing.assert_array_equal(runs[o]["losses"], runs["eager"]["losses"])
+        for k in runs["eager"]["params"]:
+            np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
+    assert set(runs["eager"]["step"].values()) == {cfg["steps"]}
+    assert "fc3.weight" not in runs["eager"]["params"]
+    model = new_model(cfg)
+    x = np.random.default_rng(0).standard_normal((cfg["batch"], cfg["dims"][0]))
+    model.forward(x, before_node=lambda op: [setattr(p, "count", p.count + 1) for p in op.params])
+    assert model.params["fc2.weight"].count == 2 and model.params["fc1.weight"].count == 1

@@ -54,6 +54,13 @@ CONFIGS = {
         loss="xent", classes=10, dtype="f32", steps=10,
         opt=dict(kind="sgd", lr=0.1, momentum=0.9, weight_decay=5e-4),
     ),
+    # A parameter used twice in one step (Alg. 2's `updated` flag, Alg. 3's
+    # `count`): layer 3 applies layer 2's weight and bias again.
+    "mlp4tied": dict(
+        kind="mlp", dims=[64, 128, 128, 128, 10], act="relu", bias=True, tie={3: 2},
+        batch=32, loss="xent", classes=10, dtype="f32", steps=5,
+        opt=dict(kind="sgd", lr=0.01, momentum=0.9, weight_decay=1e-4),
+    ),
     # Parameter-bound stack: 4 linear layers 8192x8192, no bias, no activation.
     "linear4x8192": dict(
         kind="mlp", dims=[8192] * 5, act="none", bias=False,
@@ -67,6 +74,7 @@ CONFIGS = {
 # seconds.  Sizes are chosen to span several GPU tiles and leave ragged tails.
 _REDUCED = {
     "mlp3": {},
+    "mlp4tied": {},
     "mlp8x1024": dict(dims=[200, 168, 168, 168, 10], batch=72, steps=4),
     "tblock12": dict(blocks=2, hidden=96, ffn=160, batch=136, steps=3),
     # The full learning rate (0.1, no normalisation layers) diverges within a few
@@ -94,6 +102,19 @@ def reduced_config(name, **overrides):
     return cfg
 
 
+def mlp_ties(cfg):
+    """{layer: earlier layer whose weight and bias it applies again} (1-based) of
+    an MLP workload; checked to be a same-shape, earlier, untied layer."""
+    tie = {int(k): int(v) for k, v in cfg.get("tie", {}).items()}
+    dims = cfg["dims"]
+    for i, j in tie.items():
+        if not (1 <= j < i <= len(dims) - 1) or j in tie:
+            raise ValueError(f"layer {i} cannot apply layer {j}'s parameters")
+        if (dims[i - 1], dims[i]) != (dims[j - 1], dims[j]):
+            raise ValueError(f"layers {i} and {j} have different shapes")
+    return tie
+
+
 def param_specs(cfg):
     """Trainable tensors in model order: list of (name, shape, init, fan_in).
 
@@ -103,7 +124,10 @@ def param_specs(cfg):
     kind = cfg["kind"]
     if kind == "mlp":
         dims = cfg["dims"]
+        tie = mlp_ties(cfg)
         for i in range(len(dims) - 1):
+            if i + 1 in tie:
+                continue   # applies an earlier layer's parameters
             specs.append((f"fc{i + 1}.weight", (dims[i + 1], dims[i]), "kaiming", dims[i]))
             if cfg["bias"]:
                 specs.append((f"fc{i + 1}.bias", (dims[i + 1],), "zeros", dims[i]))
