@@ -90,6 +90,17 @@ class ParamBuf:
             self.g.copy_(g)
 
 
+def _unique(ps):
+    """Parameters in first-use order, each once (a shared operator is listed once
+    per use)."""
+    seen, out = set(), []
+    for p in ps:
+        if id(p) not in seen:
+            seen.add(id(p))
+            out.append(p)
+    return out
+
+
 def _ptr(t):
     return t.data_ptr() if t is not None else None
 
@@ -173,29 +184,40 @@ class LinearOp:
         L.of_linear_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
                              tr._s())
 
-    def wgrad(self, tr, g, x):
+    def wgrad(self, tr, g, x, accumulate=0):
+        """Plain weight gradient into W.g (and b.g); accumulate=1 adds to what an
+        earlier use of a shared parameter left there."""
         L.of_linear_bwd_weight(self.desc, g, x, self.W.g.data_ptr(),
-                               self.b.g.data_ptr() if self.b else None, 0, *tr.ws_main_args(),
-                               tr._s())
+                               self.b.g.data_ptr() if self.b else None, accumulate,
+                               *tr.ws_main_args(), tr._s())
 
-    def wgrad_fused(self, tr, g, x, stream):
+    def _partials(self, partial):
+        """(gW, gb) of earlier uses of a shared parameter for the fused update."""
+        if not partial:
+            return None, None
+        return self.W.g.data_ptr(), (self.b.g.data_ptr() if self.b else None)
+
+    def wgrad_fused(self, tr, g, x, stream, partial=False):
         b = self.b
-        L.of_linear_bwd_fused(self.desc, g, x, self.W.p, b.p if b else None, None, None, tr.opt,
-                              None, 0, None, None, 0, *tr.ws_side_args(), stream, None)
+        L.of_linear_bwd_fused(self.desc, g, x, self.W.p, b.p if b else None,
+                              *self._partials(partial), tr.opt, None, 0, None, None, 0,
+                              *tr.ws_side_args(), stream, None)
 
-    def bwd_merged(self, tr, g, x, prev, act_prev, dx):
+    def bwd_merged(self, tr, g, x, prev, act_prev, dx, partial=False):
         """Data gradient (old W) and fused update in one pass over W, m, v."""
         b = self.b
-        L.of_linear_bwd_merged(self.desc, g, x, self.W.p, b.p if b else None, None, None,
-                               tr.opt, prev, act_prev, dx, *tr.ws_main_args(), tr._s())
+        L.of_linear_bwd_merged(self.desc, g, x, self.W.p, b.p if b else None,
+                               *self._partials(partial), tr.opt, prev, act_prev, dx,
+                               *tr.ws_main_args(), tr._s())
 
-    def bwd_fused(self, tr, g, x, prev, act_prev, dx):
+    def bwd_fused(self, tr, g, x, prev, act_prev, dx, partial=False):
         """Data gradient on the main stream, then the fused update: on the side
         stream (behind an event) or in stream order (one call)."""
         b = self.b
-        L.of_linear_bwd_fused(self.desc, g, x, self.W.p, b.p if b else None, None, None, tr.opt,
-                              prev, act_prev, dx, *tr.ws_main_args(), *tr.ws_side_args(),
-                              tr._s(), tr.side.cuda_stream if self.overlap_update else None)
+        L.of_linear_bwd_fused(self.desc, g, x, self.W.p, b.p if b else None,
+                              *self._partials(partial), tr.opt, prev, act_prev, dx,
+                              *tr.ws_main_args(), *tr.ws_side_args(), tr._s(),
+                              tr.side.cuda_stream if self.overlap_update else None)
 
 
 class ConvOp:
@@ -232,14 +254,18 @@ class ConvOp:
         L.of_conv_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
                            tr._s())
 
-    def wgrad(self, tr, g, x):
+    def wgrad(self, tr, g, x, accumulate=0):
         L.of_conv_bwd_weight(self.desc, g, x, self.W.g.data_ptr(),
-                             self.b.g.data_ptr() if self.b else None, 0, *tr.ws_main_args(),
-                             tr._s())
+                             self.b.g.data_ptr() if self.b else None, accumulate,
+                             *tr.ws_main_args(), tr._s())
 
-    def wgrad_fused(self, tr, g, x, stream):
+    def wgrad_fused(self, tr, g, x, stream, partial=False):
+        """Fused weight gradient + update; partial: add the gradient earlier uses
+        of a shared filter left in W.g / b.g."""
         b = self.b
-        L.of_conv_wgrad_fused(self.desc, g, x, self.W.p, b.p if b else None, None, None, tr.opt,
+        gw = self.W.g.data_ptr() if partial else None
+        gb = b.g.data_ptr() if (partial and b) else None
+        L.of_conv_wgrad_fused(self.desc, g, x, self.W.p, b.p if b else None, gw, gb, tr.opt,
                               *tr.ws_side_args(), stream)
 
 
@@ -295,10 +321,21 @@ class ChainNet:
         if cfg["kind"] == "mlp":
             M, dims = cfg["batch"], cfg["dims"]
             nl = len(dims) - 1
+            tie = {int(k): int(v) for k, v in cfg.get("tie", {}).items()}
             for i in range(1, nl + 1):
-                W = pb(f"fc{i}.weight")
-                b = pb(f"fc{i}.bias") if cfg["bias"] else None
-                self.ops.append(LinearOp(f"fc{i}", W, b, M, cfg["act"] if i < nl else "none"))
+                act = cfg["act"] if i < nl else "none"
+                if i in tie:
+                    # the same operator applied again (Alg. 2 / Alg. 3 shared parameters)
+                    if not 1 <= tie[i] < i or (dims[i - 1], dims[i]) != (dims[tie[i] - 1], dims[tie[i]]):
+                        raise ValueError(f"layer {i} cannot apply layer {tie[i]}'s parameters")
+                    src = self.ops[tie[i] - 1]
+                    if src.act != act:
+                        raise NotImplementedError("a tied layer must have its source's activation")
+                    self.ops.append(src)
+                else:
+                    W = pb(f"fc{i}.weight")
+                    b = pb(f"fc{i}.bias") if cfg["bias"] else None
+                    self.ops.append(LinearOp(f"fc{i}", W, b, M, act))
                 self.pool.append(False)
         else:
             N, s = cfg["batch"], cfg["image"]
@@ -390,32 +427,49 @@ class ChainNet:
 
     def backward_plain(self, x):
         tr = self.tr
+        seen = set()   # operators whose gradient this backward pass has started
         for i in reversed(range(len(self.ops))):
             op = self.ops[i]
             if i > 0:
                 self._dgrad(i, op)
             tr._t0("wgrad", tr.stream, op)
-            op.wgrad(tr, self.gz[i].data_ptr(), self._in(i, x))
+            op.wgrad(tr, self.gz[i].data_ptr(), self._in(i, x), int(id(op) in seen))
             tr._t1("wgrad", tr.stream)
+            seen.add(id(op))
             self._pool_bwd(i)
 
     def backward_fused(self, x, done):
         """Backward-fusion: `done(op)` is called after each layer's update is enqueued."""
         tr = self.tr
         timed = tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad"))
+        seen = set()
         for i in reversed(range(len(self.ops))):
             op = self.ops[i]
-            if op.kind == "linear" and op.merge_dgrad:
+            partial = id(op) in seen          # earlier uses' gradient is in W.g / b.g
+            seen.add(id(op))
+            if any(p.count > 1 for p in op.params):
+                # A shared parameter with backward uses still to come (Alg. 3:
+                # count > 0 after this one): its data gradient with the old W and
+                # its weight gradient into the gradient buffer; the last use
+                # updates.
+                if i > 0:
+                    self._dgrad(i, op)
+                tr._t0("wgrad", tr.stream, op)
+                op.wgrad(tr, self.gz[i].data_ptr(), self._in(i, x), int(partial))
+                tr._t1("wgrad", tr.stream)
+            elif op.kind == "linear" and op.merge_dgrad:
                 # one kernel reads W once for the data gradient and the update
                 dx, prev, act_prev = self._dgrad_target(i) if i > 0 else (None, None, 0)
                 tr._t0("wgrad_bf", tr.stream, op)
-                op.bwd_merged(tr, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx)
+                op.bwd_merged(tr, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx,
+                              partial)
                 tr._t1("wgrad_bf", tr.stream)
             elif op.kind == "linear" and not timed:
                 # one library call: dgrad with the old W on the main stream, then
                 # the fused update on the side stream behind an event
                 dx, prev, act_prev = self._dgrad_target(i) if i > 0 else (None, None, 0)
-                op.bwd_fused(tr, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx)
+                op.bwd_fused(tr, self.gz[i].data_ptr(), self._in(i, x), prev, act_prev, dx,
+                             partial)
             else:
                 # the same order by hand (events can then bracket the fused kernel):
                 # dgrad on the main stream, then the fused wgrad + update, behind
@@ -425,11 +479,12 @@ class ChainNet:
                 if op.overlap_update:
                     gate = _side_after_main(tr)
                     tr._t0_after("wgrad_bf", tr.side, op, gate)
-                    op.wgrad_fused(tr, self.gz[i].data_ptr(), self._in(i, x), tr.side.cuda_stream)
+                    op.wgrad_fused(tr, self.gz[i].data_ptr(), self._in(i, x), tr.side.cuda_stream,
+                                   partial)
                     tr._t1("wgrad_bf", tr.side)
                 else:
                     tr._t0("wgrad_bf", tr.stream, op)
-                    op.wgrad_fused(tr, self.gz[i].data_ptr(), self._in(i, x), tr._s())
+                    op.wgrad_fused(tr, self.gz[i].data_ptr(), self._in(i, x), tr._s(), partial)
                     tr._t1("wgrad_bf", tr.stream)
             self._pool_bwd(i)
             done(op)
@@ -789,7 +844,7 @@ class Trainer:
             p.step = step
 
     def _step_ff(self, x, y):
-        pending = [p for op in self.ops if not op.updated for p in op.params]
+        pending = _unique([p for op in self.ops if not op.updated for p in op.params])
         if pending:
             step = self._advance(pending)
             for p in pending:
@@ -805,7 +860,7 @@ class Trainer:
 
     def flush(self):
         """Apply every update forward-fusion still holds (what the next forward would do)."""
-        pending = [p for op in self.ops if not op.updated for p in op.params]
+        pending = _unique([p for op in self.ops if not op.updated for p in op.params])
         if pending:
             step = self._advance(pending)
             for p in pending:
@@ -829,11 +884,11 @@ class Trainer:
         step = self._advance(list(self.params.values()))
 
         def done(op):
+            # Alg. 3: a use's gradient is complete; the last use (count 0) updated
             for p in op.params:
                 p.count -= 1
-                if p.count != 0:
-                    raise NotImplementedError("shared parameters are not supported on the GPU path")
-                p.step = step
+                if p.count == 0:
+                    p.step = step
 
         self.net.backward_fused(x, done)
         self.side_done.record(self.side)

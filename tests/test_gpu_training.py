@@ -317,3 +317,49 @@ def test_fig7_optimizer_training(gpu, opt):
         for k in ref["params"]:
             np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
             np.testing.assert_array_equal(runs[o]["v"][k], runs["eager"]["v"][k])
+
+
+def _gpu_run_merge(torch, cfg, ordering, steps, dev, merge):
+    from paper_2104_00237_amd.trainer import Trainer
+    tr = Trainer(cfg, make_params(cfg), dev, merge_dgrad=merge)
+    for t in range(1, steps + 1):
+        x, y = make_batch(cfg, t)
+        tr.step(torch.as_tensor(x).to(dev), torch.as_tensor(y).to(dev), ordering)
+    losses = tr.loss_history()
+    if ordering == "ff":
+        tr.flush()
+    st = tr.state()
+    st.update(losses=losses)
+    return st
+
+
+@pytest.mark.parametrize("opt", ["sgd", "adam"])
+def test_shared_parameter_training(gpu, opt):
+    """Layer 3 applies layer 2's weight and bias again.  Eager sums both uses'
+    gradients before the optimizer; forward-fusion updates the operator once, at
+    its first forward (Alg. 2's `updated` flag); backward-fusion writes the later
+    use's gradient to a buffer and the last backward use's fused update adds it
+    (Alg. 3's `count`), also with the merged data gradient.  Every ordering against
+    the oracle's eager run; the unmerged orderings bit for bit against each other."""
+    import torch
+    cfg = get_config("mlp4tied")
+    if opt == "adam":
+        cfg["opt"] = dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                          weight_decay=0.0)
+    K = cfg["steps"]
+    ref = oracle.run(cfg, "eager", steps=K)
+    runs = {o: _gpu_run_merge(torch, cfg, o, K, gpu, False) for o in ("eager", "ff", "bf")}
+    runs["bf_merged"] = _gpu_run_merge(torch, cfg, "bf", K, gpu, True)
+    for o, st in runs.items():
+        assert rel(st["losses"], ref["losses"]) <= TOL, (o, st["losses"], ref["losses"])
+        assert sorted(st["params"]) == sorted(ref["params"])
+        for k in ref["params"]:
+            check_param(st["params"][k], ref["params"][k], cfg["opt"], K, TOL,
+                        ref["min_sqrt_vhat"].get(k), what=f"{o} {k}")
+            assert rel(st["m"][k], ref["m"][k]) <= TOL, (o, k)
+            assert st["step"][k] == ref["step"][k] == K, (o, k)
+            assert st["count"][k] == 0
+    for o in ("ff", "bf"):
+        np.testing.assert_array_equal(runs[o]["losses"], runs["eager"]["losses"])
+        for k in ref["params"]:
+            np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
