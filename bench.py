@@ -53,6 +53,16 @@ FIG7_OPTIMIZERS = {
 
 
 # ----------------------------------------------------------------- cost model
+def n_state(hyper):
+    """Optimizer state tensors the kernels stream per parameter: the momentum
+    buffer (SGD), m and v (Adam, AdamW, Adadelta, RMSprop with momentum), or v
+    alone (Adagrad, RMSprop without momentum)."""
+    k = hyper["kind"]
+    if k == "sgd" or k == "adagrad" or (k == "rmsprop" and not hyper.get("momentum", 0.0)):
+        return 1
+    return 2
+
+
 def state_bytes_per_param(kind, ordering):
     """Parameter + optimizer-state bytes one parameter costs per step (fp32).
 
@@ -63,7 +73,7 @@ def state_bytes_per_param(kind, ordering):
     R theta,hist W theta,hist; bfm = fwd R theta, merged dgrad + update
     R theta,hist W theta,hist.
     """
-    h = 2 if kind != "sgd" else 1          # history tensors (m, v) or (momentum)
+    h = kind if isinstance(kind, int) else (2 if kind != "sgd" else 1)   # state tensors
     upd = 4 * (2 + 2 * h)                  # R theta,hist + W theta,hist
     if ordering == "eager":
         return 4 + 4 + 4 + (upd + 4)
@@ -84,8 +94,7 @@ def layer_launches(cfg):
     pending update in an element-wise pass before the forward, counted in
     fwd_ff.  `extra` holds the max-pool bytes (forward, backward) after a layer.
     """
-    kind = cfg["opt"]["kind"]
-    h = 2 if kind != "sgd" else 1
+    h = n_state(cfg["opt"])
 
     def upd(n):                      # R theta,hist + W theta,hist
         return 4 * n * (2 + 2 * h)
@@ -148,7 +157,7 @@ def tblock_launches(cfg):
     gradients as fp32; the fused update also rewrites the shadow.  LayerNorm
     and the residual adds count as `extra` bytes of their block."""
     M, d, f, nb = cfg["batch"], cfg["hidden"], cfg["ffn"], cfg["blocks"]
-    h = 2 if cfg["opt"]["kind"] != "sgd" else 1
+    h = n_state(cfg["opt"])
     G = min(64, max(1, (M + 63) // 64))
     out = []
     for b in range(1, nb + 1):
@@ -194,7 +203,7 @@ def step_cost(cfg, ordering):
                 B += d[k][1]
         B += d["extra"]
     n = sum(d["nparams"] for d in L)
-    h = 2 if cfg["opt"]["kind"] != "sgd" else 1
+    h = n_state(cfg["opt"])
     if ordering == "eager":
         B += n * 4 * (3 + 2 * h)           # R w, g, hist; W w, hist
     B += 4 * L[-1]["M"] * L[-1]["N"] * 2   # loss: R logits, W their gradient
@@ -418,7 +427,8 @@ def main():
 
     n_params = sum(d["nparams"] for d in launches.values())
     kind = cfg["opt"]["kind"]
-    upd_bytes = n_params * state_bytes_per_param(kind, head)
+    nst = n_state(cfg["opt"])
+    upd_bytes = n_params * state_bytes_per_param(nst, head)
     bf_s = res[head]["ms"] / 1e3
     value = upd_bytes / bf_s / 1e9
     F, B = step_cost(cfg, head)
@@ -457,7 +467,7 @@ def main():
         "timing": "steps launched from the host scheduler; graph replay reported beside",
         "step_roofline": {"flops": F, "bytes": B, "roofline_ms": round(step_roof_s * 1e3, 5),
                           "frac": round(step_roof_s / bf_s, 4)},
-        "update_bytes_per_step": {o: n_params * state_bytes_per_param(kind, o) for o in res},
+        "update_bytes_per_step": {o: n_params * state_bytes_per_param(nst, o) for o in res},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
@@ -469,7 +479,7 @@ def main():
             cores = min(cores, max(blas)) if blas else cores
         except Exception:
             pass
-        eager_bytes = n_params * state_bytes_per_param(kind, "eager")
+        eager_bytes = n_params * state_bytes_per_param(nst, "eager")
         out["cpu_baseline"] = {"value": round(eager_bytes / dt / 1e9, 4), "unit": "GB/s",
                                "cores": cores, "kind": "oracle",
                                "ms_per_step": round(dt * 1e3, 2),

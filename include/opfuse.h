@@ -124,7 +124,10 @@ typedef struct of_opt {
 /*
  * A trainable tensor theta with its history (Fig. 2, "History").
  *   w       fp32 master values [numel]
- *   m       SGD momentum buffer or Adam first moment [numel] (required)
+ *   m       SGD momentum buffer, Adam first moment, RMSprop momentum buffer or
+ *           Adadelta squared-update average [numel]; required, except for Adagrad
+ *           and RMSprop with momentum 0, which keep no m: there it may be NULL
+ *           and is then neither read nor written
  *   v       Adam second moment, or the squared-gradient state of Adagrad,
  *           RMSprop and Adadelta [numel] (required unless SGD, ignored for SGD)
  *   w_bf16  optional bf16 copy of w (round to nearest even), rewritten by every

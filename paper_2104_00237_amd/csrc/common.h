@@ -155,8 +155,11 @@ __device__ __forceinline__ void st_bf16x4(uint16_t* p, float4 w) {
 }
 
 // Update 4 consecutive parameter elements at `off` (all valid, 16B aligned).
+// P.m may be NULL for an optimizer that keeps no m (Adagrad, RMSprop without
+// momentum): it is then neither read nor written.
 __device__ __forceinline__ float4 update4(const OptK& o, const of_param& P, float4 g, int64_t off) {
-  float4 w = ld4(P.w + off), m = ld4(P.m + off);
+  float4 w = ld4(P.w + off);
+  float4 m = P.m ? ld4(P.m + off) : make_float4(0.f, 0.f, 0.f, 0.f);
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   const bool adam = o.kind != OF_OPT_SGD;
   if (adam) v = ld4(P.v + off);
@@ -165,19 +168,19 @@ __device__ __forceinline__ float4 update4(const OptK& o, const of_param& P, floa
   opt_update(o, w.z, g.z, m.z, v.z);
   opt_update(o, w.w, g.w, m.w, v.w);
   st4(P.w + off, w);
-  st4(P.m + off, m);
+  if (P.m) st4(P.m + off, m);
   if (adam) st4(P.v + off, v);
   if (P.w_bf16) st_bf16x4(P.w_bf16 + off, w);
   return w;
 }
 
 __device__ __forceinline__ float update1(const OptK& o, const of_param& P, float g, int64_t off) {
-  float w = P.w[off], m = P.m[off], v = 0.f;
+  float w = P.w[off], m = P.m ? P.m[off] : 0.f, v = 0.f;
   const bool adam = o.kind != OF_OPT_SGD;
   if (adam) v = P.v[off];
   opt_update(o, w, g, m, v);
   P.w[off] = w;
-  P.m[off] = m;
+  if (P.m) P.m[off] = m;
   if (adam) P.v[off] = v;
   if (P.w_bf16) P.w_bf16[off] = f32_to_bf16(w);
   return w;

@@ -29,6 +29,13 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
   // raw buffer, stride 0, 2^31-1 bytes addressable from `base`
   return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, 0x7fffffff, 0x00020000);
 }
+// Descriptor of `base + off` elements, or of nothing when `base` is NULL (an
+// optional state tensor): every load through it reads 0 and every store is
+// dropped, without touching memory.
+__device__ __forceinline__ rsrc_t make_rsrc_opt(const float* base, int64_t off) {
+  if (base == nullptr) return __builtin_amdgcn_make_buffer_rsrc((void*)nullptr, (short)0, 0, 0x00020000);
+  return make_rsrc(base + off);
+}
 __device__ __forceinline__ float4 bload4(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }

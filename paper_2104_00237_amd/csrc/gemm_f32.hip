@@ -226,8 +226,8 @@ struct FFTileLoad {
     const bool adam = ea.opt.kind != OF_OPT_SGD;
     base = (int64_t)x0 * ldw + r0;
     const rsrc_t rw = make_rsrc(ea.W.w + base), rg = make_rsrc(ea.gW + base);
-    const rsrc_t rm = make_rsrc(ea.W.m + base);
-    const rsrc_t rv = make_rsrc(adam ? ea.W.v + base : ea.W.m + base);
+    const rsrc_t rm = make_rsrc_opt(ea.W.m, base);
+    const rsrc_t rv = adam ? make_rsrc(ea.W.v + base) : rm;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int idx = tid + i * 256;
@@ -278,7 +278,7 @@ struct FFTileLoad {
       if (valid[i] == 0xf && ((uintptr_t)(ea.W.w + o) & 15u) == 0) {
         for (int e = 0; e < 4; ++e) opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
         st4(ea.W.w + o, w[i]);
-        st4(ea.W.m + o, m[i]);
+        if (ea.W.m) st4(ea.W.m + o, m[i]);
         if (adam) st4(ea.W.v + o, v[i]);
         if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + o, w[i]);
       } else if (valid[i]) {
@@ -286,7 +286,7 @@ struct FFTileLoad {
           if (valid[i] & (1 << e)) {
             opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
             ea.W.w[o + e] = pw[e];
-            ea.W.m[o + e] = pm[e];
+            if (ea.W.m) ea.W.m[o + e] = pm[e];
             if (adam) ea.W.v[o + e] = pv[e];
             if (ea.W.w_bf16) ea.W.w_bf16[o + e] = f32_to_bf16(pw[e]);
           }
@@ -365,9 +365,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
         const int64_t ld = PREF_BF ? ea.ldo : ea.ldp;
         const int64_t org = (int64_t)p0 * ld + q0;
         const rsrc_t r0 = make_rsrc(PREF_BF ? ea.W.w + org : ea.prev + org);
-        const rsrc_t r1 = make_rsrc(PREF_BF ? ea.W.m + org : ea.prev + org);
-        const rsrc_t r2 = make_rsrc((PREF_BF && ea.opt.kind != OF_OPT_SGD) ? ea.W.v + org
-                                                                           : ea.W.m + org);
+        const rsrc_t r1 = PREF_BF ? make_rsrc_opt(ea.W.m, org) : make_rsrc(ea.prev + org);
+        const rsrc_t r2 = (PREF_BF && ea.opt.kind != OF_OPT_SGD) ? make_rsrc(ea.W.v + org) : r1;
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
           const int idx = tid + e * 256;
@@ -522,7 +521,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
         opt_update(ea.opt, w.w, c[3], m.w, v.w);
         const int64_t oo = (int64_t)gp * ea.ldo + gq;
         st4(ea.W.w + oo, w);
-        st4(ea.W.m + oo, m);
+        if (ea.W.m) st4(ea.W.m + oo, m);
         if (ea.opt.kind != OF_OPT_SGD) st4(ea.W.v + oo, v);
         if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + oo, w);
       } else if constexpr (PREF_DG) {

@@ -65,9 +65,9 @@ struct ParFrag {
                                        bool kok, bool adam) {
     const int64_t base = (int64_t)n0 * a.K;
     const rsrc_t rw = make_rsrc(a.W.w + base);
-    const rsrc_t rm = make_rsrc(a.W.m + base);
-    const rsrc_t rv = make_rsrc((adam ? a.W.v : a.W.m) + base);
-    const rsrc_t rg = make_rsrc((HAS_G ? a.gW : a.W.m) + base);
+    const rsrc_t rm = make_rsrc_opt(a.W.m, base);   // no m: reads 0
+    const rsrc_t rv = adam ? make_rsrc(a.W.v + base) : rm;
+    const rsrc_t rg = HAS_G ? make_rsrc(a.gW + base) : rm;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int n = acc_row(i, h);
@@ -182,8 +182,8 @@ __device__ __forceinline__ void merged_chunk(const MergedArgs& a, MergedState<MB
   {
     const int64_t base = (int64_t)n0 * a.K;
     const rsrc_t rw = make_rsrc(a.W.w + base);
-    const rsrc_t rm = make_rsrc(a.W.m + base);
-    const rsrc_t rv = make_rsrc((st.adam ? a.W.v : a.W.m) + base);
+    const rsrc_t rm = make_rsrc_opt(a.W.m, base);   // no m: stores dropped
+    const rsrc_t rv = st.adam ? make_rsrc(a.W.v + base) : rm;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int n = acc_row(i, h);

@@ -63,12 +63,20 @@ of_status check_opt(const of_opt* o) {
   return OF_OK;
 }
 
-of_status check_param(const of_param* p, const char* name, int64_t numel, int kind, bool need_w) {
+// Whether the optimizer keeps the m tensor (Adagrad and RMSprop without
+// momentum do not; their m may be NULL and is then never touched).
+bool uses_m(const of_opt& o) {
+  return !(o.kind == OF_OPT_ADAGRAD || (o.kind == OF_OPT_RMSPROP && o.momentum == 0.f));
+}
+
+of_status check_param(const of_param* p, const char* name, int64_t numel, const of_opt& opt,
+                      bool need_w) {
+  const int kind = opt.kind;
   REQUIRE(p != nullptr, OF_EINVAL, "%s is NULL", name);
   REQUIRE(p->numel == numel, OF_EINVAL, "%s->numel is %lld, expected %lld", name,
           (long long)p->numel, (long long)numel);
   if (need_w) REQUIRE(p->w != nullptr, OF_EINVAL, "%s->w is NULL", name);
-  REQUIRE(p->m != nullptr, OF_EINVAL, "%s->m is NULL", name);
+  if (uses_m(opt)) REQUIRE(p->m != nullptr, OF_EINVAL, "%s->m is NULL", name);
   if (kind != OF_OPT_SGD)
     REQUIRE(p->v != nullptr, OF_EINVAL, "%s->v is NULL (every optimizer but SGD needs v)", name);
   REQUIRE(al4(p->w) && al4(p->m) && al4(p->v), OF_EALIGN, "%s arrays must be 4-byte aligned", name);
@@ -89,7 +97,7 @@ of_status make_carry(const of_carry* c, CarryArgs* out) {
     snprintf(name, sizeof(name), "next->t[%d]", k);
     const of_param& P = c->t[k];
     REQUIRE(P.numel >= 1, OF_EINVAL, "%s.numel must be >= 1", name);
-    if ((st = check_param(&P, name, P.numel, c->opt.kind, true)) != OF_OK) return st;
+    if ((st = check_param(&P, name, P.numel, c->opt, true)) != OF_OK) return st;
     REQUIRE(c->g[k] != nullptr, OF_EINVAL, "next->g[%d] is NULL", k);
     REQUIRE(al4(c->g[k]), OF_EALIGN, "next->g[%d] must be 4-byte aligned", k);
     REQUIRE(c->rows[k] >= 1, OF_EINVAL, "next->rows[%d] must be >= 1", k);
@@ -379,9 +387,9 @@ of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_
   if (st != OF_OK) return st;
   if ((st = check_opt(opt)) != OF_OK) return st;
   REQUIRE(x && y && gW, OF_EINVAL, "x, y and gW are required");
-  if ((st = check_param(W, "W", d->N * d->K, opt->kind, true)) != OF_OK) return st;
+  if ((st = check_param(W, "W", d->N * d->K, *opt, true)) != OF_OK) return st;
   if (d->has_bias) {
-    if ((st = check_param(b, "b", d->N, opt->kind, true)) != OF_OK) return st;
+    if ((st = check_param(b, "b", d->N, *opt, true)) != OF_OK) return st;
     REQUIRE(gb != nullptr, OF_EINVAL, "has_bias is set but gb is NULL");
   }
   REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z");
@@ -456,9 +464,9 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
   if (st != OF_OK) return st;
   if ((st = check_opt(opt)) != OF_OK) return st;
   REQUIRE(dz && x, OF_EINVAL, "dz and x are required");
-  if ((st = check_param(W, "W", d->N * d->K, opt->kind, true)) != OF_OK) return st;
+  if ((st = check_param(W, "W", d->N * d->K, *opt, true)) != OF_OK) return st;
   if (b) {
-    if ((st = check_param(b, "b", d->N, opt->kind, true)) != OF_OK) return st;
+    if ((st = check_param(b, "b", d->N, *opt, true)) != OF_OK) return st;
   }
   REQUIRE(al4(dz) && al4(x) && al4(gW_partial) && al4(gb_partial) && al4(dx_prev), OF_EALIGN,
           "fp32 pointers must be 4-byte aligned");
@@ -505,9 +513,9 @@ of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const f
   if ((st = check_merged(d)) != OF_OK) return st;
   if ((st = check_opt(opt)) != OF_OK) return st;
   REQUIRE(dz && x, OF_EINVAL, "dz and x are required");
-  if ((st = check_param(W, "W", d->N * d->K, opt->kind, true)) != OF_OK) return st;
+  if ((st = check_param(W, "W", d->N * d->K, *opt, true)) != OF_OK) return st;
   if (b) {
-    if ((st = check_param(b, "b", d->N, opt->kind, true)) != OF_OK) return st;
+    if ((st = check_param(b, "b", d->N, *opt, true)) != OF_OK) return st;
   }
   REQUIRE(al4(dz) && al4(x) && al4(gW_partial) && al4(gb_partial) && al4(dx_prev) && al4(prev),
           OF_EALIGN, "fp32 pointers must be 4-byte aligned");
@@ -612,9 +620,9 @@ of_status of_conv_wgrad_fused(const of_conv_desc* d, const float* dy, const floa
   if (st != OF_OK) return st;
   if ((st = check_opt(opt)) != OF_OK) return st;
   REQUIRE(dy && x, OF_EINVAL, "dy and x are required");
-  if ((st = check_param(W, "W", 9 * d->C * d->Cout, opt->kind, true)) != OF_OK) return st;
+  if ((st = check_param(W, "W", 9 * d->C * d->Cout, *opt, true)) != OF_OK) return st;
   if (b) {
-    if ((st = check_param(b, "b", d->Cout, opt->kind, true)) != OF_OK) return st;
+    if ((st = check_param(b, "b", d->Cout, *opt, true)) != OF_OK) return st;
   }
   REQUIRE(al4(dy) && al4(x) && al4(gW_partial) && al4(gb_partial), OF_EALIGN,
           "fp32 pointers must be 4-byte aligned");
@@ -655,7 +663,7 @@ of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t
   of_status st = check_opt(opt);
   if (st != OF_OK) return st;
   REQUIRE(p != nullptr && p->numel >= 1, OF_EINVAL, "p is NULL or p->numel < 1");
-  if ((st = check_param(p, "p", p->numel, opt->kind, true)) != OF_OK) return st;
+  if ((st = check_param(p, "p", p->numel, *opt, true)) != OF_OK) return st;
   REQUIRE(g != nullptr, OF_EINVAL, "g is NULL");
   REQUIRE(al4(g), OF_EALIGN, "g must be 4-byte aligned");
   REQUIRE(g_rows >= 1, OF_EINVAL, "g_rows must be >= 1");
@@ -679,7 +687,7 @@ of_status of_optimizer_step(int32_t n, const of_param* params, const float* cons
     char name[32];
     snprintf(name, sizeof(name), "params[%d]", (int)i);
     REQUIRE(params[i].numel >= 1, OF_EINVAL, "%s.numel < 1", name);
-    if ((st = check_param(&params[i], name, params[i].numel, opt->kind, true)) != OF_OK) return st;
+    if ((st = check_param(&params[i], name, params[i].numel, *opt, true)) != OF_OK) return st;
     REQUIRE(grads[i] != nullptr, OF_EINVAL, "grads[%d] is NULL", (int)i);
     REQUIRE(al4(grads[i]), OF_EALIGN, "grads[%d] must be 4-byte aligned", (int)i);
   }

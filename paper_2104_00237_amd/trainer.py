@@ -706,6 +706,11 @@ class Trainer:
         else:
             raise NotImplementedError(f"model kind {cfg['kind']!r} has no GPU path in this build")
         self.ops = self.net.ops
+        # Adagrad and RMSprop without momentum keep no m: the kernels get a NULL m
+        # and neither read nor write it (m stays zero on the host side too).
+        if kind == "adagrad" or (kind == "rmsprop" and not self.hyper.get("momentum", 0.0)):
+            for p in self.params.values():
+                p.p.m = None
         self.eager_reduce = True
         for op in self.ops:
             if op.kind == "linear" and merge_dgrad and op.merge_ok:

@@ -106,6 +106,19 @@ def test_optimizer_validation(lib):
         o.eps = 1e-8
         assert _status(L.of_elementwise_fused_update, _param(100, v=None), g, 1, 0, o,
                        None) == L.OF_EINVAL
+    # m may be NULL only where the optimizer keeps none (Adagrad, RMSprop without momentum)
+    no_m = _param(100, m=None)
+    for hy in (dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8),
+               dict(kind="rmsprop", lr=1e-3, alpha=0.99, eps=1e-8, momentum=0.9)):
+        assert _status(L.of_elementwise_fused_update, no_m, g, 1, 0, L.make_opt(hy, 1),
+                       None) == L.OF_EINVAL
+        assert "->m is NULL" in L.of_last_error()
+    for hy in (dict(kind="adagrad", lr=0.01, eps=1e-10),
+               dict(kind="rmsprop", lr=1e-3, alpha=0.99, eps=1e-8)):
+        # accepted: validation fails on the missing gradient instead
+        assert _status(L.of_elementwise_fused_update, no_m, None, 1, 0, L.make_opt(hy, 1),
+                       None) == L.OF_EINVAL
+        assert "->m is NULL" not in L.of_last_error()
     sgd = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1)
     # SGD needs no v; a NULL m is still an error.
     assert _status(L.of_elementwise_fused_update, _param(10, m=None, v=None), g, 1, 0, sgd,
