@@ -58,11 +58,11 @@ class _Param:
         self.m = (r.standard_normal(shape) * 0.01).astype(np.float32)
         if kind == "adadelta":
             self.m = np.abs(self.m) * 1e-2   # squared-update state is >= 0
+        self.v = (r.random(shape) * 1e-4).astype(np.float32) if kind != "sgd" else None
         if kind in ("adagrad", "rmsprop", "adadelta"):
             # sqrt(v) >= 0.07: the 1/sqrt(v) sensitivity of the update to the
             # gradient's float32 rounding stays well inside the tolerance
             self.v = ((0.5 + r.random(shape)) * 1e-2).astype(np.float32)
-        self.v = (r.random(shape) * 1e-4).astype(np.float32) if kind != "sgd" else None
         self.W, self.M = _t(torch, dev, self.w), _t(torch, dev, self.m)
         self.V = _t(torch, dev, self.v) if kind != "sgd" else None
         self.p = L.OfParam(self.W.data_ptr(), self.M.data_ptr(),
