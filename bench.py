@@ -323,6 +323,9 @@ def main():
                     help="replace the workload's optimizer (Fig. 7's set)")
     ap.add_argument("--batch", type=int, default=None,
                     help="replace the workload's batch (rows per step; Figs. 4-5 sweep)")
+    ap.add_argument("--dims", default=None, metavar="WIDTHxDEPTH",
+                    help="MLP workloads: DEPTH hidden layers of WIDTH (parameters per layer, "
+                         "Fig. 6 sweep); the input and output widths follow WIDTH and the classes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -350,6 +353,13 @@ def main():
         cfg = dict(cfg, opt=FIG7_OPTIMIZERS[args.optimizer])
     if args.batch:
         cfg = dict(cfg, batch=args.batch)
+    if args.dims:
+        if cfg["kind"] != "mlp":
+            print("--dims applies to MLP workloads", file=sys.stderr)
+            sys.exit(2)
+        w, dpt = (int(v) for v in args.dims.lower().split("x"))
+        out = cfg["classes"] if cfg["loss"] == "xent" else w
+        cfg = dict(cfg, dims=[w] * (dpt + 1) + ([out] if cfg["loss"] == "xent" else []))
     if cfg["kind"] not in ("mlp", "vgg", "tblock"):
         print(f"workload {args.workload} has no GPU path in this build", file=sys.stderr)
         sys.exit(2)

@@ -746,6 +746,13 @@ class Trainer:
         self.stream = torch.cuda.current_stream(self.device)
         self.side = torch.cuda.Stream(self.device)
         self.side_done = torch.cuda.Event()
+        # Whether backward-fusion puts any update on the side stream: a chain of
+        # light layers updates in stream order and needs no join at the step's
+        # end (two runtime calls fewer per step); the Transformer blocks update
+        # their LayerNorm parameters there.
+        self.uses_side = (not isinstance(self.net, ChainNet) or
+                          any(op.overlap_update and not getattr(op, "merge_dgrad", False)
+                              for op in self.ops))
         self.pending_ordering = None
         self.timer = None   # optional KernelTimer: HIP events around chosen launch classes
 
@@ -880,7 +887,8 @@ class Trainer:
             raise ValueError("backward-fusion updates each tensor before the other gradients "
                              "exist, so it cannot clip by the global norm (Table 1)")
         # The forward of each layer at this step needs its update from the last
-        # step: the previous step ended with the main stream joining the side one.
+        # step: the previous step ended with the main stream joining the side one
+        # (when any update ran there).
         for op in self.ops:
             for p in op.params:
                 p.count += 1
@@ -896,8 +904,10 @@ class Trainer:
                     p.step = step
 
         self.net.backward_fused(x, done)
-        self.side_done.record(self.side)
-        self.stream.wait_event(self.side_done)
+        if self.uses_side:
+            # the next forward reads parameters the side stream updated
+            self.side_done.record(self.side)
+            self.stream.wait_event(self.side_done)
 
     # ------------------------------------------------------------- graphs
     def capture(self, x, y, ordering):
