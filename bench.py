@@ -288,6 +288,30 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     return ms, host_s / steps * 1e3, timer, losses
 
 
+STAGES = {"forward": ("fwd", "fwd_ff", "loss"),
+          "backward": ("dgrad", "wgrad", "wgrad_bf", "ln_bwd", "add"),
+          "optimizer": ("opt", "clip")}
+
+
+def stage_breakdown(torch, cfg, batches, ordering, steps, marker_ms):
+    """Fig. 3-style split of one ordering's step into forward, backward and
+    optimizer kernel time (ms per step): every launch class bracketed by events
+    on its own stream, the event pair's cost taken off each launch.  Kernels
+    that overlap on two streams (backward-fusion's updates) are both counted, so
+    the stages can sum to more than the step."""
+    classes = [c for cs in STAGES.values() for c in cs]
+    ms, _, timer, _ = time_ordering(torch, cfg, ordering, batches, 3, steps, classes)
+    out = {}
+    for stage, cs in STAGES.items():
+        tot = 0.0
+        for c in cs:
+            durs = timer.durations(c)
+            tot += sum(max(d - marker_ms, 0.0) for d, _ in durs)
+        out[stage] = round(tot / steps, 4)
+    out["step_bracketed"] = round(ms, 4)
+    return out
+
+
 def cpu_baseline(cfg, budget_s=15.0):
     """Oracle eager steps on this host, seconds per step of `cfg`.  The 12-block
     Transformer stack is sampled as one block (same width and tokens) and its
@@ -435,6 +459,10 @@ def main():
                 traffic=traffic_for("merged_bwd" if cost_key == "wgrad_bfm" else dom,
                                     args.workload))
 
+    # Fig. 3 analogue: forward / backward / optimizer kernel time of each ordering
+    main_marker = KernelTimer.marker_overhead_ms(torch.cuda.current_stream())
+    breakdown = {o: stage_breakdown(torch, cfg, batches, o, 10, main_marker) for o in res}
+
     n_params = sum(d["nparams"] for d in launches.values())
     kind = cfg["opt"]["kind"]
     nst = n_state(cfg["opt"])
@@ -479,6 +507,8 @@ def main():
                           "frac": round(step_roof_s / bf_s, 4)},
         "update_bytes_per_step": {o: n_params * state_bytes_per_param(nst, o) for o in res},
         "roofline": roof,
+        "stage_breakdown_ms": breakdown,
+        "optimizer_share_eager": round(breakdown["eager"]["optimizer"] / res["eager"]["ms"], 4),
     }
     if not args.no_cpu_baseline:
         dt, n = cpu_baseline(cfg, args.cpu_budget)
