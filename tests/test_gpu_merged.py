@@ -323,3 +323,25 @@ def test_merged_window_full_size(env):
                         b["min_sqrt_vhat"].get(k), what=f"step {s + 1} {k}")
             assert rel(st["m"][k], b["m"][k]) <= TOL, (s, k)
             assert rel(st["v"][k], b["v"][k]) <= TOL, (s, k)
+
+
+def test_merged_largest_supported_row(env):
+    """K = 2^22, the widest row the merged kernel takes (its 32-bit buffer offsets
+    stay in range there): 2 token rows, 8 output rows (128 MB of W), every output
+    against the oracle."""
+    torch, L, dev = env
+    M, N, K = 2, 8, 1 << 22
+    r = np.random.default_rng(17)
+    hyper, step = HYPERS["adam"], 2
+    x = r.standard_normal((M, K)).astype(np.float32)
+    dz = (r.standard_normal((M, N)) * 0.05).astype(np.float32)
+    Wp = _Param(torch, L, dev, (N, K), "adam", 18, step)
+    dw = dz.astype(np.float64).T @ x.astype(np.float64)
+    dx = dz.astype(np.float64) @ Wp.w.astype(np.float64)
+    refW = Wp.oracle(dw, hyper)
+    d = L.OfLinearDesc(M, N, K, 0, 0, L.OF_F32, L.OF_ACT_NONE, 0)
+    X, DZ = _t(torch, dev, x), _t(torch, dev, dz)
+    DX = torch.full((M, K), float("nan"), device=dev)
+    _run_merged(torch, L, dev, d, DZ, X, Wp, None, None, None, hyper, step, None, 0, DX)
+    assert rel(DX.cpu().numpy(), dx) <= TOL
+    Wp.check(refW)
