@@ -509,6 +509,19 @@ def main():
         "roofline": roof,
         "stage_breakdown_ms": breakdown,
         "optimizer_share_eager": round(breakdown["eager"]["optimizer"] / res["eager"]["ms"], 4),
+        # the separate optimizer pass alone: R w, g, state and W w, state per parameter
+        "eager_optimizer_GBps": (round(n_params * 4 * (3 + 2 * nst) /
+                                       (breakdown["eager"]["optimizer"] / 1e3) / 1e9, 1)
+                                 if breakdown["eager"]["optimizer"] > 0 else None),
+        "tflops_per_s": round(F / bf_s / 1e12, 3),
+        # the speedup model's inputs (Section 4): t_opt of the eager step and, per
+        # fused ordering, t_saved = eager - fused step time and the share of t_opt saved
+        "t_opt_ms": breakdown["eager"]["optimizer"],
+        "t_saved_ms": {o: round(res["eager"]["ms"] - res[o]["ms"], 4) for o in res if o != "eager"},
+        "t_opt_saved_frac": ({o: round((res["eager"]["ms"] - res[o]["ms"]) /
+                                       breakdown["eager"]["optimizer"], 3)
+                              for o in res if o != "eager"}
+                             if breakdown["eager"]["optimizer"] > 0 else None),
     }
     if not args.no_cpu_baseline:
         dt, n = cpu_baseline(cfg, args.cpu_budget)
