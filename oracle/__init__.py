@@ -9,7 +9,11 @@ computes, written from the paper:
   * forward-fusion (Appendix B.1, Alg. 2) and backward-fusion (Appendix B.2,
     Alg. 3, with the dependency rule stated after Alg. 3);
   * the optimizer policies of Appendix A (Alg. 1, gradient descent and
-    momentum) plus Adam / AdamW as used by the workloads.
+    momentum) plus Adam / AdamW as used by the workloads, and Adagrad,
+    RMSprop and Adadelta, the other optimizers of the comparison in Fig. 7;
+  * global-norm gradient clipping (the global-information step forward-fusion
+    permits, Appendix B.1, Table 1) and parameters shared by two layers (the
+    `updated` flag of Alg. 2 and `count` of Alg. 3).
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  The product (the HIP library and its Python binding)
