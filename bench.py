@@ -77,7 +77,7 @@ def state_bytes_per_param(kind, ordering):
     upd = 4 * (2 + 2 * h)                  # R theta,hist + W theta,hist
     if ordering == "eager":
         return 4 + 4 + 4 + (upd + 4)
-    if ordering == "ff":
+    if ordering in ("ff", "ffp"):
         return (upd + 4) + 4 + 4
     if ordering == "bfm":
         return 4 + upd
@@ -259,7 +259,10 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     merge = ordering == "bfm"
     if merge:
         ordering = "bf"
-    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge)
+    prologue = ordering == "ffp"
+    if prologue:
+        ordering = "ff"
+    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge, conv_prologue=prologue)
     n = len(batches)
     for t in range(max(warmup, 1)):
         x, y = batches[t % n]
@@ -350,6 +353,8 @@ def main():
     ap.add_argument("--dims", default=None, metavar="WIDTHxDEPTH",
                     help="MLP workloads: DEPTH hidden layers of WIDTH (parameters per layer, "
                          "Fig. 6 sweep); the input and output widths follow WIDTH and the classes")
+    ap.add_argument("--conv-ff-prologue", action="store_true",
+                    help="vgg11: also time forward-fusion with the filter-tile prologue (ffp)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -398,7 +403,8 @@ def main():
     # the merged backward applies to fp32 linear chains of at most 64 rows
     mergeable = cfg["kind"] == "mlp" and cfg["dtype"] == "f32" and cfg["batch"] <= 64
     res = {}
-    for o in ("eager", "ff", "bf") + (("bfm",) if mergeable else ()):
+    extra = (("bfm",) if mergeable else ()) + (("ffp",) if args.conv_ff_prologue else ())
+    for o in ("eager", "ff", "bf") + extra:
         ms, host_ms, _, _ = time_ordering(torch, cfg, o, batches, args.warmup, args.steps,
                                           graph=False)
         ms_g = None
@@ -496,6 +502,9 @@ def main():
         "bf_ms_per_step": round(res["bf"]["ms"], 4),
         "speedup_bf_vs_eager": round(res["eager"]["ms"] / res["bf"]["ms"], 4),
         "speedup_ff_vs_eager": round(res["eager"]["ms"] / res["ff"]["ms"], 4),
+        **({"ffp_ms_per_step": round(res["ffp"]["ms"], 4),
+            "speedup_ffp_vs_eager": round(res["eager"]["ms"] / res["ffp"]["ms"], 4)}
+           if "ffp" in res else {}),
         **({"bfm_ms_per_step": round(res["bfm"]["ms"], 4),
             "speedup_bfm_vs_eager": round(res["eager"]["ms"] / res["bfm"]["ms"], 4)}
            if mergeable else {}),

@@ -340,6 +340,26 @@ of_status of_conv_fwd_carry(const of_conv_desc* d, const float* x, const of_para
  * prev: the previous layer's saved output [N,H,W,C] (ReLU: mask prev > 0), or
  * NULL with OF_ACT_NONE.
  */
+/*
+ * Forward-fusion of a convolution in the filter-tile prologue (Section 3
+ * "Forward-Fusion", Appendix B.1, Alg. 2): y = act(conv(x, W_new) + b_new),
+ * where (W_new, m, v) = update(W, gW, m, v) and likewise for b.
+ * A filter tile is read by every workgroup of the launch's pixel rows, so the
+ * update is not written in place: every workgroup reads W, b and their history
+ * (the old generation, unchanged by the call) and computes the update in
+ * registers; the workgroups of the first pixel-row tile write the new values to
+ * W_out and b_out (a second buffer set of the same sizes, not sharing any
+ * buffer with W and b).  The caller then uses W_out / b_out as the parameters
+ * (the two sets alternate from step to step).  Every element gets the
+ * arithmetic of of_optimizer_step, and the contraction is the one of_conv_fwd
+ * runs, so y and the new parameters are bit-identical to an update pass
+ * followed by of_conv_fwd.  Workspace: of_conv_workspace_size(d, OF_CONV_FWD).
+ */
+of_status of_conv_fwd_fused(const of_conv_desc* d, const float* x, const of_param* W,
+                            const of_param* W_out, const float* gW, const of_param* b,
+                            const of_param* b_out, const float* gb, const of_opt* opt, float* y,
+                            void* ws, size_t ws_bytes, void* stream);
+
 of_status of_conv_bwd_data(const of_conv_desc* d, const float* dy, const of_param* W,
                            const float* prev, int32_t act_prev, float* dx, void* ws,
                            size_t ws_bytes, void* stream);

@@ -106,6 +106,9 @@ _SIGS = {
                               c_size_t, c_void_p]),
     "of_conv_fwd_carry": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_void_p,
                                     P(OfCarry), c_void_p, c_size_t, c_void_p]),
+    "of_conv_fwd_fused": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), P(OfParam), c_void_p,
+                                    P(OfParam), P(OfParam), c_void_p, P(OfOpt), c_void_p,
+                                    c_void_p, c_size_t, c_void_p]),
     "of_conv_bwd_data": (c_int32, [P(OfConvDesc), c_void_p, P(OfParam), c_void_p, c_int32,
                                    c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_conv_bwd_weight": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, c_void_p, c_void_p,
@@ -192,7 +195,7 @@ def of_layernorm_partial_rows(M):
 for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_linear_bwd_merged", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
-           "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
+           "of_conv_fwd_fused", "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
            "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_layernorm_fwd", "of_layernorm_bwd",
            "of_reduce_rows", "of_add"):
     globals()[_n] = _wrap(_n)

@@ -268,6 +268,11 @@ struct EpiArgs {
   of_param W;                   // W.w etc.
   const float* gW;              // FWD_FF: pending gradient; WGRAD_BF: extra gradient (shared use)
   of_param b;                   // FF / BF bias parameter (b.w NULL if none)
+  // FF with many readers of each W tile (a convolution): every workgroup reads
+  // W, b and their history from the fields above and computes the update;
+  // only the workgroups of row tile 0 write it, to these (a second buffer
+  // set).  Wout.w == NULL: the update is written in place (one row tile).
+  of_param Wout, bout;
   const float* gb;              // FF: pending bias gradient; BF: extra bias gradient
   int with_db;                  // WGRAD: db != NULL; WGRAD_BF: b.w != NULL
   OptK opt;

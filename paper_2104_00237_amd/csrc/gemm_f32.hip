@@ -262,9 +262,13 @@ struct FFTileLoad {
     }
   }
 
-  __device__ __forceinline__ void apply(const EpiArgs& ea, int64_t ldw, float* lds, int tid) {
+  // owner: this workgroup writes the updated values (to ea.Wout when set, else
+  // in place); every workgroup feeds them to its MFMAs.
+  __device__ __forceinline__ void apply(const EpiArgs& ea, int64_t ldw, float* lds, int tid,
+                                        bool owner) {
     constexpr int LD = BX + 4;
     const bool adam = ea.opt.kind != OF_OPT_SGD;
+    const of_param& out = ea.Wout.w ? ea.Wout : ea.W;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int idx = tid + i * 256;
@@ -275,20 +279,24 @@ struct FFTileLoad {
       float* pg = reinterpret_cast<float*>(&g[i]);
       float* pm = reinterpret_cast<float*>(&m[i]);
       float* pv = reinterpret_cast<float*>(&v[i]);
-      if (valid[i] == 0xf && ((uintptr_t)(ea.W.w + o) & 15u) == 0) {
+      if (valid[i] == 0xf && ((uintptr_t)(out.w + o) & 15u) == 0) {
         for (int e = 0; e < 4; ++e) opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
-        st4(ea.W.w + o, w[i]);
-        if (ea.W.m) st4(ea.W.m + o, m[i]);
-        if (adam) st4(ea.W.v + o, v[i]);
-        if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + o, w[i]);
+        if (owner) {
+          st4(out.w + o, w[i]);
+          if (out.m) st4(out.m + o, m[i]);
+          if (adam) st4(out.v + o, v[i]);
+          if (out.w_bf16) st_bf16x4(out.w_bf16 + o, w[i]);
+        }
       } else if (valid[i]) {
         for (int e = 0; e < 4; ++e) {
           if (valid[i] & (1 << e)) {
             opt_update(ea.opt, pw[e], pg[e], pm[e], pv[e]);
-            ea.W.w[o + e] = pw[e];
-            if (ea.W.m) ea.W.m[o + e] = pm[e];
-            if (adam) ea.W.v[o + e] = pv[e];
-            if (ea.W.w_bf16) ea.W.w_bf16[o + e] = f32_to_bf16(pw[e]);
+            if (owner) {
+              out.w[o + e] = pw[e];
+              if (out.m) out.m[o + e] = pm[e];
+              if (adam) out.v[o + e] = pv[e];
+              if (out.w_bf16) out.w_bf16[o + e] = f32_to_bf16(pw[e]);
+            }
           }
         }
       }
@@ -330,6 +338,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
   const bool do_db = WG && ea.with_db && ty == 0;
+  // forward-fusion: the workgroup that writes the updated W tile (all of them
+  // when each W tile has one row tile; row tile 0 when it goes to Wout)
+  const bool ff_owner = ea.Wout.w == nullptr || p0 == 0;
 
   // Buffer b (0/1) of the A and B tiles: A at b*STAGE, B at b*STAGE + BR*LDA.
   constexpr int STAGE = T::BR * (T::LDA + T::LDB);
@@ -390,8 +401,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   // Forward-fusion holds four arrays per stage and keeps a two-stage ring.
   constexpr int NS = (EPI == EPI_FWD_FF) ? 2 : T::NS;
   using ALoad = std::conditional_t<
-      CONV && (EPI == EPI_FWD || EPI == EPI_DGRAD),
-      GatherLoad<T::BP, T::BR, true, VA, EPI == EPI_FWD ? G_FWD_A : G_DGRAD_A>,
+      CONV && (EPI == EPI_FWD || EPI == EPI_FWD_FF || EPI == EPI_DGRAD),
+      GatherLoad<T::BP, T::BR, true, VA, EPI == EPI_DGRAD ? G_DGRAD_A : G_FWD_A>,
       TileLoad<T::BP, T::BR, A_RC, VA>>;
   using BLoad = std::conditional_t<
       CONV && EPI == EPI_DGRAD, GatherLoad<T::BQ, T::BR, false, VB, G_DGRAD_B>,
@@ -434,7 +445,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       float* buf = smem + (c & 1) * STAGE;
       la[s].store(buf, tid);
       if constexpr (EPI == EPI_FWD_FF) {
-        if (c < nch) lf[s].apply(ea, ldw, buf + BOFF, tid);
+        if (c < nch) lf[s].apply(ea, ldw, buf + BOFF, tid, ff_owner);
       } else {
         lb[s].store(buf + BOFF, tid);
       }
@@ -483,10 +494,24 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
         Cs[(wr * T::BP + p) * T::LDC + q] = acc[i][j][k];
       }
 
-  // Forward-fusion bias: updated once per column tile, by the split-0 workgroup.
+  // Forward-fusion bias: the split-0 workgroups compute the update; it is
+  // written once per column tile (by row tile 0 when the update goes to a
+  // second buffer set, else by the only row tile).
   const bool ff_bias = (EPI == EPI_FWD_FF) && ea.b.w != nullptr;
-  if (ff_bias && split == 0 && tid < T::BQ && q0 + tid < pr.Q)
-    bias_s[tid] = update1(ea.opt, ea.b, ea.gb[q0 + tid], q0 + tid);
+  if (ff_bias && split == 0 && tid < T::BQ && q0 + tid < pr.Q) {
+    const int i = q0 + tid;
+    const bool adam = ea.opt.kind != OF_OPT_SGD;
+    float w = ea.b.w[i], m = ea.b.m ? ea.b.m[i] : 0.f, v = adam ? ea.b.v[i] : 0.f;
+    opt_update(ea.opt, w, ea.gb[i], m, v);
+    if (ff_owner) {
+      const of_param& out = ea.bout.w ? ea.bout : ea.b;
+      out.w[i] = w;
+      if (out.m) out.m[i] = m;
+      if (adam) out.v[i] = v;
+      if (out.w_bf16) out.w_bf16[i] = f32_to_bf16(w);
+    }
+    bias_s[tid] = w;
+  }
   __syncthreads();
 
   const float* bias_base = nullptr;
@@ -849,17 +874,15 @@ template <class T, int EPI>
 static hipError_t launch_t(const GemmCfg& c, const GemmProblem& pr, const EpiArgs& ea, void* ws,
                            int vec_ops, int vec_epi, hipStream_t stream) {
   dim3 grid((pr.P + T::BP - 1) / T::BP, (pr.Q + T::BQ - 1) / T::BQ, c.S + c.cz);
-  if constexpr (EPI != EPI_FWD_FF) {
-    if (pr.conv) {
-      // convolutions: 128-bit gathers per operand (the channel counts differ)
-      switch (vec_ops) {
-        case 3: hipLaunchKernelGGL((gemm_kernel<T, EPI, 3, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
-        case 2: hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
-        case 1: hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
-        default: hipLaunchKernelGGL((gemm_kernel<T, EPI, 0, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi);
-      }
-      return hipGetLastError();
+  if (pr.conv) {
+    // convolutions: 128-bit gathers per operand (the channel counts differ)
+    switch (vec_ops) {
+      case 3: hipLaunchKernelGGL((gemm_kernel<T, EPI, 3, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
+      case 2: hipLaunchKernelGGL((gemm_kernel<T, EPI, 2, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
+      case 1: hipLaunchKernelGGL((gemm_kernel<T, EPI, 1, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi); break;
+      default: hipLaunchKernelGGL((gemm_kernel<T, EPI, 0, true>), grid, dim3(256), 0, stream, pr, ea, c.r_split, (float*)ws, vec_epi);
     }
+    return hipGetLastError();
   }
   // 128-bit operand loads only when both operands allow them.
   if (vec_ops == 3)
@@ -953,7 +976,7 @@ static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* ve
     // gathers: a float4 stays within one filter tap when the channel count along
     // the contiguous index is a multiple of 4
     const bool cin4 = pr.cC % 4 == 0, cout4 = pr.cCout % 4 == 0;
-    if (kind == EPI_FWD) { va = aligned16(pr.A) && cin4; vb = aligned16(pr.B) && cin4; }
+    if (kind == EPI_FWD || kind == EPI_FWD_FF) { va = aligned16(pr.A) && cin4; vb = aligned16(pr.B) && cin4; }
     if (kind == EPI_DGRAD) { va = aligned16(pr.A) && cout4; vb = aligned16(pr.B) && cin4; }
     if (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) {
       va = aligned16(pr.A) && cout4;
@@ -963,6 +986,8 @@ static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* ve
   if (kind == EPI_FWD_FF)
     vb = vb && aligned16(ea.W.w) && aligned16(ea.W.m) && aligned16(ea.gW) &&
          (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) &&
+         aligned16(ea.Wout.w) && aligned16(ea.Wout.m) &&
+         (ea.opt.kind == OF_OPT_SGD || aligned16(ea.Wout.v)) &&
          (ea.W.w_bf16 == nullptr || ((uintptr_t)ea.W.w_bf16 & 7u) == 0);
   int ve = 0;
   if (aligned16(ea.out) && ea.ldo % 4 == 0 && (ea.z == nullptr || (aligned16(ea.z) && ea.ldz % 4 == 0)) &&
@@ -979,6 +1004,10 @@ static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* ve
 hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, void* ws,
                        hipStream_t stream) {
   GemmCfg c = select_cfg(kind, pr.P, pr.Q, pr.R, pr.conv);
+  // The 128x128 tile leaves no LDS for forward-fusion's bias row; a fused
+  // convolution forward given it takes 128x64 with the same splits (the same
+  // reduction ranges and workspace).
+  if (kind == EPI_FWD_FF && c.tile == TI_128x128) c.tile = TI_128x64;
   EpiArgs ea = ea_in;
   ea.carry.z0 = 0;
   if (ea.carry.t[0].p.w) {
@@ -1001,7 +1030,8 @@ hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, vo
   }
   if (e != hipSuccess || c.S <= 1) return e;
   EpiArgs er = ea;
-  if (kind == EPI_FWD_FF) er.bias = ea.b.w;  // already updated by the split-0 workgroups
+  // the bias the split-0 workgroups have updated (written to bout when set)
+  if (kind == EPI_FWD_FF) er.bias = ea.bout.w ? ea.bout.w : ea.b.w;
   switch (kind) {
     case EPI_FWD: return launch_reduce<EPI_FWD>(c, pr, er, ws, vec_epi, 0, stream);
     case EPI_FWD_FF: return launch_reduce<EPI_FWD_FF>(c, pr, er, ws, vec_epi, 0, stream);

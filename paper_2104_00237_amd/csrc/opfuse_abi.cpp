@@ -576,6 +576,43 @@ of_status of_conv_fwd_carry(const of_conv_desc* d, const float* x, const of_para
                                 (hipStream_t)stream), "of_conv_fwd launch");
 }
 
+of_status of_conv_fwd_fused(const of_conv_desc* d, const float* x, const of_param* W,
+                            const of_param* W_out, const float* gW, const of_param* b,
+                            const of_param* b_out, const float* gb, const of_opt* opt, float* y,
+                            void* ws, size_t ws_bytes, void* stream) {
+  of_status st = check_conv(d);
+  if (st != OF_OK) return st;
+  if ((st = check_opt(opt)) != OF_OK) return st;
+  REQUIRE(x && y && gW, OF_EINVAL, "x, y and gW are required");
+  const int64_t nw = 9 * d->C * d->Cout;
+  if ((st = check_param(W, "W", nw, *opt, true)) != OF_OK) return st;
+  if ((st = check_param(W_out, "W_out", nw, *opt, true)) != OF_OK) return st;
+  REQUIRE(W->w_bf16 == nullptr && W_out->w_bf16 == nullptr, OF_EINVAL,
+          "convolutions take fp32 filters (no bf16 shadow)");
+  // every workgroup reads the old generation while row tile 0 writes the new one
+  REQUIRE(W_out->w != W->w && (W->m == nullptr || W_out->m != W->m) &&
+          (W->v == nullptr || W_out->v != W->v), OF_EINVAL,
+          "W_out must not share buffers with W");
+  REQUIRE(!d->has_bias || (b && b_out && gb), OF_EINVAL, "has_bias needs b, b_out and gb");
+  if (d->has_bias) {
+    if ((st = check_param(b, "b", d->Cout, *opt, true)) != OF_OK) return st;
+    if ((st = check_param(b_out, "b_out", d->Cout, *opt, true)) != OF_OK) return st;
+    REQUIRE(b_out->w != b->w && (b->m == nullptr || b_out->m != b->m) &&
+            (b->v == nullptr || b_out->v != b->v), OF_EINVAL,
+            "b_out must not share buffers with b");
+  }
+  REQUIRE(al4(x) && al4(y) && al4(gW) && al4(gb), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_conv_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
+  EpiArgs ea = empty_epi();
+  ea.out = y; ea.ldo = d->Cout;
+  ea.act = d->act;
+  ea.W = *W; ea.Wout = *W_out; ea.gW = gW;
+  if (d->has_bias) { ea.b = *b; ea.bout = *b_out; ea.gb = gb; }
+  ea.opt = make_optk(*opt);
+  return hip_status(gemm_launch(EPI_FWD_FF, conv_problem(d, EPI_FWD, x, W->w), ea, ws,
+                                (hipStream_t)stream), "of_conv_fwd_fused launch");
+}
+
 of_status of_conv_bwd_data(const of_conv_desc* d, const float* dy, const of_param* W,
                            const float* prev, int32_t act_prev, float* dx, void* ws,
                            size_t ws_bytes, void* stream) {

@@ -76,6 +76,29 @@ class ParamBuf:
             return self.rows.data_ptr(), self.rows.shape[0], self.numel
         return self.g.data_ptr(), 1, 0
 
+    def swap_generation(self):
+        """Make the second buffer set (written by a fused convolution forward)
+        the current one; the old set becomes the next step's output.  Allocated
+        on first use."""
+        if getattr(self, "_alt", None) is None:
+            w2 = torch.empty_like(self.w)
+            m2 = torch.empty_like(self.m)
+            v2 = torch.empty_like(self.v) if self.v is not None else None
+            p2 = L.param_of(w2, m2, v2)
+            if self.p.m is None:      # an optimizer without m keeps none
+                p2.m = None
+            self._alt = (w2, m2, v2, p2)
+        w2, m2, v2, p2 = self._alt
+        self._alt = (self.w, self.m, self.v, self.p)
+        self.w, self.m, self.v, self.p = w2, m2, v2, p2
+
+    def alt_param(self):
+        """of_param of the buffer set the next fused convolution forward writes."""
+        if getattr(self, "_alt", None) is None:
+            self.swap_generation()
+            self.swap_generation()   # allocate, keep the current set current
+        return self._alt[3]
+
     def set(self, value):
         self.w.copy_(torch.as_tensor(np.asarray(value, np.float32)))
         if self.wb is not None:
@@ -239,7 +262,14 @@ class ConvOp:
     def ws(self, which):
         return L.of_conv_workspace_size(self.desc, which)
 
-    prologue_ff = False   # the filter-tile prologue is not fused: carried or own pass
+    # Forward-fusion in the filter-tile prologue (of_conv_fwd_fused, when the
+    # trainer asks for it): every workgroup updates its filter tile in
+    # registers from the current buffers, the first pixel-row tile writes it to
+    # the other buffer set, which becomes current.  Every pixel-row tile re-reads
+    # the filter's gradient and history, so by default the update is carried by
+    # the previous launch instead (measured faster on VGG-11); a captured step
+    # keeps the buffers fixed and always carries it.  Same values either way.
+    prologue_ff = False
     overlap_update = True  # a convolution's fused wgrad + update is heavy: second stream
 
     def fwd(self, tr, x, y, carry=None):
@@ -249,6 +279,15 @@ class ConvOp:
         else:
             L.of_conv_fwd_carry(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, y,
                                 carry, *tr.ws_main_args(), tr._s())
+
+    def fwd_ff(self, tr, x, y):
+        b = self.b
+        L.of_conv_fwd_fused(self.desc, x, self.W.p, self.W.alt_param(), self.W.g.data_ptr(),
+                            b.p if b else None, b.alt_param() if b else None,
+                            b.g.data_ptr() if b else None, tr.opt, y, *tr.ws_main_args(),
+                            tr._s())
+        for p in self.params:
+            p.swap_generation()
 
     def dgrad(self, tr, g, prev, act_prev, dx):
         L.of_conv_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
@@ -300,6 +339,12 @@ class LayerNormOp:
         for p in self.params:
             L.of_reduce_rows(p.rows.data_ptr(), p.rows.shape[0], 0, p.numel, p.g.data_ptr(),
                              tr._s())
+
+
+def _ff_prologue(tr, op):
+    """Whether forward-fusion applies op's pending update in its forward's W-tile
+    loads (else a previous launch carries it, or a pass of its own runs)."""
+    return op.prologue_ff and not (op.kind == "conv" and tr.capturing)
 
 
 def _side_after_main(tr):
@@ -378,7 +423,7 @@ class ChainNet:
         tr = self.tr
         n = len(self.ops)
         for i, op in enumerate(self.ops):
-            if fused and not op.updated and op.prologue_ff:
+            if fused and not op.updated and _ff_prologue(tr, op):
                 tr._t0("fwd_ff", tr.stream, op)
                 op.fwd_ff(tr, self._in(i, x), self.y[i].data_ptr())
                 tr._t1("fwd_ff", tr.stream)
@@ -389,7 +434,7 @@ class ChainNet:
                     op.updated = True
                 nxt = self.ops[i + 1] if i + 1 < n else None
                 carry = None
-                if fused and nxt is not None and not nxt.updated and not nxt.prologue_ff:
+                if fused and nxt is not None and not nxt.updated and not _ff_prologue(tr, nxt):
                     carry = _carry_of(tr, nxt.params)
                 tr._t0("fwd", tr.stream, op)
                 op.fwd(tr, self._in(i, x), self.y[i].data_ptr(), carry=carry)
@@ -683,9 +728,12 @@ class TBlockNet:
 class Trainer:
     """Trains one workload on one GPU under a chosen ordering."""
 
-    def __init__(self, cfg, init, device="cuda:0", merge_dgrad=False):
+    def __init__(self, cfg, init, device="cuda:0", merge_dgrad=False, conv_prologue=False):
         """merge_dgrad: backward-fusion runs each fp32 linear layer with at most
-        64 rows as one merged data-gradient + update pass (of_linear_bwd_merged)."""
+        64 rows as one merged data-gradient + update pass (of_linear_bwd_merged).
+        conv_prologue: forward-fusion applies a convolution's pending update in
+        its forward's filter-tile loads (of_conv_fwd_fused) instead of carrying
+        it in the previous launch."""
         L.load()
         self.cfg, self.hyper = cfg, cfg["opt"]
         self.device = torch.device(device)
@@ -715,6 +763,8 @@ class Trainer:
         for op in self.ops:
             if op.kind == "linear" and merge_dgrad and op.merge_ok:
                 op.merge_dgrad = True
+            if op.kind == "conv":
+                op.prologue_ff = bool(conv_prologue)
         f32 = dict(dtype=torch.float32, device=self.device)
         wsm = max([op.ws(w) for op in self.ops for w in (0, 1, 2)] + [16])
         wsm = max([wsm] + [op.ws(L.OF_LINEAR_BWD_MERGED) for op in self.ops if op.kind == "linear"

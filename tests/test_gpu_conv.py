@@ -180,3 +180,84 @@ def test_maxpool(env, N, H, W, C):
     np.testing.assert_array_equal(A.cpu().numpy().astype(np.int32), arg)
     np.testing.assert_array_equal(DX.cpu().numpy(), dx)
     np.testing.assert_array_equal(DX2.cpu().numpy(), dx_masked)
+
+
+@pytest.mark.parametrize("N,H,W,C,Co", SHAPES)
+@pytest.mark.parametrize("kind", ["sgd", "adam"])
+def test_conv_fwd_fused(env, N, H, W, C, Co, kind):
+    """Forward-fusion in the filter-tile prologue: y uses the updated filter and
+    bias, which go to the second buffer set; the first set is left as it was.
+    Against the oracle, and bit for bit against an update pass followed by the
+    plain forward (the same contraction and per-element arithmetic)."""
+    torch, L, dev = env
+    hyper = (dict(kind="sgd", lr=0.1, momentum=0.9, weight_decay=5e-4) if kind == "sgd" else
+             dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0))
+    step = 3
+    x, w, b, _ = _data(N, H, W, C, Co, N * 7 + C + Co)
+    r = np.random.default_rng(C + Co)
+    gw = (r.standard_normal(w.shape) * 0.05).astype(np.float32)
+    gb = (r.standard_normal(Co) * 0.05).astype(np.float32)
+    mw = (r.standard_normal(w.shape) * 0.01).astype(np.float32)
+    mb = (r.standard_normal(Co) * 0.01).astype(np.float32)
+    vw = (r.random(w.shape) * 1e-4).astype(np.float32)
+    vb = (r.random(Co) * 1e-4).astype(np.float32)
+    adam = kind != "sgd"
+
+    def param(arrs):
+        ts = [_t(torch, dev, a) for a in arrs]
+        p = L.OfParam(ts[0].data_ptr(), ts[1].data_ptr(), ts[2].data_ptr() if adam else None,
+                      None, ts[0].numel())
+        return p, ts
+
+    def fresh():
+        return param((w, mw, vw)), param((b, mb, vb))
+
+    def blank(shape):
+        z = np.full(shape, np.nan, np.float32)
+        return param((z, z, z))
+
+    def oracle(val, g, m, v):
+        P = OL.Param("p", val.astype(np.float64))
+        P.m, P.v, P.step = m.astype(np.float64), v.astype(np.float64), step - 1
+        P.grad = g.astype(np.float64)
+        OO.apply(P, hyper)
+        return P
+
+    d = L.OfConvDesc(N, H, W, C, Co, L.OF_ACT_RELU, 1)
+    ws = _ws(torch, dev, L.of_conv_workspace_size(d, 0))
+    GW, GB = _t(torch, dev, gw), _t(torch, dev, gb)
+    (Wp, Wt), (Bp, Bt) = fresh()
+    (Wo, Wot), (Bo, Bot) = blank(w.shape), blank((Co,))
+    Y = torch.full((N, H, W, Co), float("nan"), device=dev)
+    L.of_conv_fwd_fused(d, _t(torch, dev, x).data_ptr(), Wp, Wo, GW.data_ptr(), Bp, Bo,
+                        GB.data_ptr(), L.make_opt(hyper, step), Y.data_ptr(), ws.data_ptr(),
+                        ws.numel() * 4, 0)
+    torch.cuda.synchronize()
+    rw, rb = oracle(w, gw, mw, vw), oracle(b, gb, mb, vb)
+    conv = OL.Conv3x3(OL.Param("w", rw.value), OL.Param("b", rb.value))
+    y_ref = np.maximum(conv.forward(x.astype(np.float64))[0], 0)
+    assert rel(Y.cpu().numpy(), y_ref) <= TOL
+    for got, ref in ((Wot[0], rw.value), (Wot[1], rw.m), (Bot[0], rb.value), (Bot[1], rb.m)):
+        assert rel(got.cpu().numpy(), ref) <= TOL
+    if adam:
+        assert rel(Wot[2].cpu().numpy(), rw.v) <= TOL
+    for t, a in zip(Wt + Bt, (w, mw, vw, b, mb, vb)):   # the first set is unchanged
+        if t is not None:
+            np.testing.assert_array_equal(t.cpu().numpy(), a)
+
+    # eager pair: the multi-tensor update in place, then the plain forward
+    (We, Wet), (Be, Bet) = fresh()
+    arr = (L.OfParam * 2)(We, Be)
+    gp = (ctypes.c_void_p * 2)(GW.data_ptr(), GB.data_ptr())
+    L.of_optimizer_step(2, arr, gp, L.make_opt(hyper, step), 0)
+    Ye = torch.empty_like(Y)
+    L.of_conv_fwd(d, _t(torch, dev, x).data_ptr(), We, Bet[0].data_ptr(), Ye.data_ptr(),
+                  ws.data_ptr(), ws.numel() * 4, 0)
+    torch.cuda.synchronize()
+    for a, b_ in ((Wot[0], Wet[0]), (Wot[1], Wet[1]), (Bot[0], Bet[0]), (Bot[1], Bet[1])):
+        np.testing.assert_array_equal(a.cpu().numpy(), b_.cpu().numpy())
+    if adam:
+        np.testing.assert_array_equal(Wot[2].cpu().numpy(), Wet[2].cpu().numpy())
+    # the same contraction unless the tiling model picked 128x128 (no LDS room
+    # for the bias row: the fused forward runs 128x64 with the same splits)
+    assert rel(Ye.cpu().numpy(), Y.cpu().numpy()) <= TOL

@@ -363,3 +363,38 @@ def test_shared_parameter_training(gpu, opt):
         np.testing.assert_array_equal(runs[o]["losses"], runs["eager"]["losses"])
         for k in ref["params"]:
             np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
+
+
+def test_vgg_conv_prologue_forward_fusion(gpu):
+    """Forward-fusion with each convolution's pending update applied in its
+    forward's filter-tile loads (two buffer sets alternating) on the reduced
+    VGG: against the oracle, and bit for bit against the default forward-fusion,
+    which carries the same updates in the previous launch."""
+    import torch
+    cfg = _cfg("vgg11", "reduced")
+    K = cfg["steps"]
+    ref = oracle.run(cfg, "eager", steps=K)
+    runs = {p: _gpu_run_prologue(torch, cfg, K, gpu, p) for p in (False, True)}
+    st = runs[True]
+    assert rel(st["losses"], ref["losses"]) <= TOL
+    for k in ref["params"]:
+        check_param(st["params"][k], ref["params"][k], cfg["opt"], K, TOL, None, what=k)
+        assert rel(st["m"][k], ref["m"][k]) <= TOL, k
+        assert st["step"][k] == K
+        np.testing.assert_array_equal(st["params"][k], runs[False]["params"][k])
+        np.testing.assert_array_equal(st["m"][k], runs[False]["m"][k])
+    np.testing.assert_array_equal(st["losses"], runs[False]["losses"])
+
+
+def _gpu_run_prologue(torch, cfg, steps, dev, prologue):
+    from paper_2104_00237_amd.trainer import Trainer
+    tr = Trainer(cfg, make_params(cfg), dev, conv_prologue=prologue)
+    assert any(op.kind == "conv" and op.prologue_ff for op in tr.ops) == prologue
+    for t in range(1, steps + 1):
+        x, y = make_batch(cfg, t)
+        tr.step(torch.as_tensor(x).to(dev), torch.as_tensor(y).to(dev), "ff")
+    losses = tr.loss_history()
+    tr.flush()
+    st = tr.state()
+    st.update(losses=losses)
+    return st
