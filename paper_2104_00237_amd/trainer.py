@@ -972,6 +972,13 @@ class Trainer:
             raise RuntimeError("capture forward-fusion after one ff step (steady state)")
         if self.pending_ordering == "ff" and ordering != "ff":
             self.flush()
+        # A graph holds the parameter buffers current now; the convolutions'
+        # filter-tile prologue would alternate them, so from here on their
+        # updates are carried by the previous launch (the same values) in
+        # launched steps too.
+        for op in self.ops:
+            if op.kind == "conv":
+                op.prologue_ff = False
         saved = ([(p.step, p.count) for p in self.params.values()],
                  [op.updated for op in self.ops], self.t, self.pending_ordering)
         g = torch.cuda.CUDAGraph()

@@ -45,3 +45,31 @@ def test_graph_replays_match_steps(gpu, name, ordering):
         a, b = ref.state(), cap.state()
         for n in a["params"]:
             np.testing.assert_array_equal(b["params"][n], a["params"][n])
+
+
+def test_conv_prologue_then_capture(gpu):
+    """A trainer that uses the convolutions' filter-tile prologue (alternating
+    buffer sets) and is then captured: the replays and later launched steps carry
+    the updates instead, and every step matches a trainer that always carried
+    them, bit for bit."""
+    import torch
+    from paper_2104_00237_amd.trainer import Trainer
+    from workloads import reduced_config, make_params, make_batch
+    cfg = reduced_config("vgg11")
+    batches = [tuple(torch.as_tensor(a).to(gpu) for a in make_batch(cfg, t)) for t in range(1, 5)]
+    runs = []
+    for prologue in (True, False):
+        tr = Trainer(cfg, make_params(cfg), gpu, conv_prologue=prologue)
+        tr.step(*batches[0], "ff")
+        tr.step(*batches[1], "ff")          # prologue steps (generations swapped)
+        g = tr.capture(*batches[2], "ff")
+        g()
+        tr.step(*batches[3], "ff")          # launched again after the capture
+        tr.flush()
+        torch.cuda.synchronize()
+        runs.append((tr.state(), tr.loss_history()))
+    (a, la), (b, lb) = runs
+    np.testing.assert_array_equal(la, lb)
+    for k in a["params"]:
+        np.testing.assert_array_equal(a["params"][k], b["params"][k])
+        np.testing.assert_array_equal(a["m"][k], b["m"][k])
