@@ -291,6 +291,28 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     return ms, host_s / steps * 1e3, timer, losses
 
 
+def median_step_ms(torch, cfg, ordering, batches, warmup, steps):
+    """Median step time of one ordering, each launched step bracketed by its own
+    event pair on the step's stream (a pass of its own, so the mean above is
+    timed without per-step markers)."""
+    from paper_2104_00237_amd.trainer import Trainer
+    merge = ordering == "bfm"
+    prologue = ordering == "ffp"
+    o = "bf" if merge else "ff" if prologue else ordering
+    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge, conv_prologue=prologue)
+    n = len(batches)
+    for t in range(max(warmup, 1)):
+        tr.step(*batches[t % n], o)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(tr.stream)
+    for t in range(steps):
+        tr.step(*batches[(warmup + t) % n], o)
+        evs[t + 1].record(tr.stream)
+    torch.cuda.synchronize()
+    return float(np.median([evs[t].elapsed_time(evs[t + 1]) for t in range(steps)]))
+
+
 STAGES = {"forward": ("fwd", "fwd_ff", "loss"),
           "backward": ("dgrad", "wgrad", "wgrad_bf", "ln_bwd", "add"),
           "optimizer": ("opt", "clip")}
@@ -465,6 +487,8 @@ def main():
                 traffic=traffic_for("merged_bwd" if cost_key == "wgrad_bfm" else dom,
                                     args.workload))
 
+    medians = {o: round(median_step_ms(torch, cfg, o, batches, args.warmup, args.steps), 4)
+               for o in res}
     # Fig. 3 analogue: forward / backward / optimizer kernel time of each ordering
     main_marker = KernelTimer.marker_overhead_ms(torch.cuda.current_stream())
     breakdown = {o: stage_breakdown(torch, cfg, batches, o, 10, main_marker) for o in res}
@@ -511,6 +535,7 @@ def main():
         "ms_per_step_graph_replay": {o: (round(r["ms_graph"], 4) if r["ms_graph"] else None)
                                      for o, r in res.items()},
         "host_ms_per_step": {o: round(r["host_ms"], 4) for o, r in res.items()},
+        "median_ms_per_step": medians,
         "timing": "steps launched from the host scheduler; graph replay reported beside",
         "step_roofline": {"flops": F, "bytes": B, "roofline_ms": round(step_roof_s * 1e3, 5),
                           "frac": round(step_roof_s / bf_s, 4)},
