@@ -13,7 +13,9 @@ computes, written from the paper:
     RMSprop and Adadelta, the other optimizers of the comparison in Fig. 7;
   * global-norm gradient clipping (the global-information step forward-fusion
     permits, Appendix B.1, Table 1) and parameters shared by two layers (the
-    `updated` flag of Alg. 2 and `count` of Alg. 3).
+    `updated` flag of Alg. 2 and `count` of Alg. 3);
+  * the depthwise 3x3 convolution of the small-parameter layers (MobileNetV2,
+    Fig. 3 and Table 2), pinned to the full convolution's direct loops.
 
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  The product (the HIP library and its Python binding)

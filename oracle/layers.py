@@ -17,6 +17,7 @@ Definitions (the readings where the paper is silent):
   gelu        y = z * Phi(z) (exact erf form); dz = dy (Phi(z) + z phi(z))
   layernorm   over the last axis, biased variance, eps inside the sqrt
   conv3x3     cross-correlation, stride 1, zero padding 1, NHWC / [Cout,3,3,Cin]
+  dwconv3x3   the same per channel (depthwise, multiplier 1), filter [3,3,C]
   maxpool2x2  stride 2; the argmax is the first maximum of the window in
               row-major order (strict >), reported as its window position 0..3
   bf16        matmul operands rounded to bfloat16 just before the product
@@ -201,6 +202,53 @@ class Conv3x3(Op):
                 dxp[:, r:r + h, s:s + wd, :] += dy @ w[:, r, s, :]
                 dw[:, r, s, :] = np.tensordot(dy, xp[:, r:r + h, s:s + wd, :],
                                               axes=([0, 1, 2], [0, 1, 2]))
+        grads = (dw,) if self.b is None else (dw, dy.sum(axis=(0, 1, 2)))
+        return (dxp[:, 1:-1, 1:-1, :],), grads
+
+
+class DepthwiseConv3x3(Op):
+    """Depthwise 3x3 cross-correlation (one filter per channel), stride 1, zero pad 1,
+    NHWC input, [3,3,C] filter: y[n,h,w,c] = b[c] + sum over taps of
+    x[n,h+ky-1,w+kx-1,c] w[ky,kx,c].  The small-parameter layers of MobileNetV2,
+    the network of the paper's Fig. 3 and Table 2."""
+
+    def __init__(self, w, b=None):
+        super().__init__()
+        self.w, self.b = w, b
+        self.params = (w,) if b is None else (w, b)
+
+    def forward(self, x):
+        n, h, wd, _ = x.shape
+        xp = np.pad(x, ((0, 0), (1, 1), (1, 1), (0, 0)))
+        w = self.w.value
+        y = np.zeros(x.shape)
+        for r in range(3):
+            for s in range(3):
+                y += xp[:, r:r + h, s:s + wd, :] * w[r, s, :]
+        if self.b is not None:
+            y += self.b.value
+        return y, xp
+
+    def abs_bound(self, x):
+        """sum over taps of |x||w| + |b|: the scale of the rounding error of y."""
+        n, h, wd, _ = x.shape
+        xp = np.pad(np.abs(x), ((0, 0), (1, 1), (1, 1), (0, 0)))
+        w = np.abs(self.w.value)
+        s = np.zeros(x.shape)
+        for r in range(3):
+            for c in range(3):
+                s += xp[:, r:r + h, c:c + wd, :] * w[r, c, :]
+        return s + np.abs(self.b.value) if self.b is not None else s
+
+    def backward(self, xp, dy):
+        n, h, wd, _ = dy.shape
+        w = self.w.value
+        dxp = np.zeros_like(xp)
+        dw = np.zeros_like(w)
+        for r in range(3):
+            for s in range(3):
+                dxp[:, r:r + h, s:s + wd, :] += dy * w[r, s, :]
+                dw[r, s, :] = (dy * xp[:, r:r + h, s:s + wd, :]).sum(axis=(0, 1, 2))
         grads = (dw,) if self.b is None else (dw, dy.sum(axis=(0, 1, 2)))
         return (dxp[:, 1:-1, 1:-1, :],), grads
 

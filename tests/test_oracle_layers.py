@@ -141,6 +141,27 @@ def test_conv3x3_matches_direct_loops_and_grads():
     _check_op(op, [x])
 
 
+def test_dwconv3x3_is_block_diagonal_conv_loops_and_grads():
+    """Depthwise = the full 3x3 conv with a channel-diagonal filter (checked by direct
+    loops); its gradients pass finite differences."""
+    rng = np.random.default_rng(16)
+    x = rng.standard_normal((2, 5, 4, 3))
+    w, b = _P(rng, (3, 3, 3)), _P(rng, (3,))
+    full = np.zeros((3, 3, 3, 3))
+    for c in range(3):
+        full[c, :, :, c] = w.value[:, :, c]
+    op = L.DepthwiseConv3x3(w, b)
+    y, _ = op.forward(x)
+    np.testing.assert_allclose(y, _conv_loops(x, full, b.value), rtol=1e-13, atol=1e-13)
+    # a one-hot input picks single filter taps out, transposed through the padding
+    e = np.zeros((1, 3, 3, 3))
+    e[0, 1, 1, 2] = 1.0
+    ye, _ = L.DepthwiseConv3x3(L.Param("w", w.value), None).forward(e)
+    np.testing.assert_array_equal(ye[0, :, :, 2], w.value[::-1, ::-1, 2])
+    np.testing.assert_array_equal(ye[0, :, :, :2], 0.0)
+    _check_op(op, [x])
+
+
 def test_maxpool_first_max_and_grad():
     x = np.zeros((1, 2, 4, 1))
     x[0, :, :, 0] = [[1, 3, 2, 2], [3, 0, 2, 2]]   # window 1: tie 3/3, window 2: all equal
