@@ -384,6 +384,51 @@ of_status of_conv_wgrad_fused(const of_conv_desc* d, const float* dy, const floa
                               const float* gb_partial, const of_opt* opt, void* ws,
                               size_t ws_bytes, void* stream);
 
+/* ------------------------------------------- depthwise 3x3 convolutions */
+/*
+ * The small-parameter layers where the paper sees its largest gains
+ * (Section 5, speedup against parameters per layer; MobileNetV2 in Fig. 3 and
+ * Table 2): one 3x3 filter per channel (channel multiplier 1), stride 1, zero
+ * padding 1.  Descriptor: of_conv_desc with Cout == C.  x, y, dy, dx, prev are
+ * [N,H,W,C] NHWC; the filter W is [3,3,C] (tap-major, channels contiguous);
+ * the bias is [C].  act is OF_ACT_NONE or OF_ACT_RELU.  All pointers are
+ * device memory owned by the caller.  Errors: OF_EINVAL for NULL or
+ * inconsistent arguments (Cout != C), OF_EUNSUPPORTED for tensors of 2^31
+ * elements or more, OF_EALIGN for misaligned pointers, OF_EWORKSPACE for a
+ * short workspace; nothing is launched then.
+ */
+
+/* Bytes of workspace the filter-gradient calls need (0 for an invalid desc). */
+size_t of_dwconv_workspace_size(const of_conv_desc* d);
+
+/* Forward node: y[n,h,w,c] = act(b[c] + sum over taps of
+ * x[n,h+ky-1,w+kx-1,c] * W[ky,kx,c]). */
+of_status of_dwconv_fwd(const of_conv_desc* d, const float* x, const float* W, const float* b,
+                        float* y, void* stream);
+
+/* Data gradient with the OLD filter: dx[n,h,w,c] = (sum over taps of
+ * dy[n,h-ky+1,w-kx+1,c] * W[ky,kx,c]) * act_prev'(prev); act_prev is
+ * OF_ACT_NONE (prev may be NULL) or OF_ACT_RELU (mask prev > 0). */
+of_status of_dwconv_bwd_data(const of_conv_desc* d, const float* dy, const float* W,
+                             const float* prev, int32_t act_prev, float* dx, void* stream);
+
+/* Eager filter gradient: dw[ky,kx,c] = sum over n,h,w of dy[n,h,w,c] *
+ * x[n,h+ky-1,w+kx-1,c]; db[c] = sum of dy (db may be NULL); accumulate = 1
+ * adds to dw / db.  Deterministic (fixed slice order). */
+of_status of_dwconv_bwd_weight(const of_conv_desc* d, const float* dy, const float* x, float* dw,
+                               float* db, int32_t accumulate, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* Backward-fusion (Section 3 "Backward-Fusion", Alg. 3): the filter and bias
+ * gradients of of_dwconv_bwd_weight (+ gW_partial / gb_partial when given) are
+ * applied by `opt` to W, b and their history in the reduction's last pass and
+ * never stored.  The result is bit-identical to of_dwconv_bwd_weight followed
+ * by of_optimizer_step.  The caller runs of_dwconv_bwd_data first (old W). */
+of_status of_dwconv_wgrad_fused(const of_conv_desc* d, const float* dy, const float* x,
+                                const of_param* W, const of_param* b, const float* gW_partial,
+                                const float* gb_partial, const of_opt* opt, void* ws,
+                                size_t ws_bytes, void* stream);
+
 /*
  * 2x2 max-pool, stride 2 (H, W even): y [N,H/2,W/2,C]; argmax [N,H/2,W/2,C]
  * holds the window position 0..3 of the first maximum in row-major window

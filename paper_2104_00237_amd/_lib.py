@@ -116,6 +116,15 @@ _SIGS = {
     "of_conv_wgrad_fused": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, P(OfParam), P(OfParam),
                                       c_void_p, c_void_p, P(OfOpt), c_void_p, c_size_t,
                                       c_void_p]),
+    "of_dwconv_workspace_size": (c_size_t, [P(OfConvDesc)]),
+    "of_dwconv_fwd": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+    "of_dwconv_bwd_data": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, c_void_p, c_int32,
+                                     c_void_p, c_void_p]),
+    "of_dwconv_bwd_weight": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_int32, c_void_p, c_size_t, c_void_p]),
+    "of_dwconv_wgrad_fused": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, P(OfParam),
+                                        P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
+                                        c_size_t, c_void_p]),
     "of_maxpool2x2_fwd": (c_int32, [c_void_p, c_int64, c_int64, c_int64, c_int64, c_void_p,
                                     c_void_p, c_void_p]),
     "of_maxpool2x2_bwd": (c_int32, [c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64,
@@ -188,6 +197,10 @@ def of_conv_workspace_size(desc, op):
     return load().of_conv_workspace_size(ctypes.byref(desc), op)
 
 
+def of_dwconv_workspace_size(desc):
+    return load().of_dwconv_workspace_size(ctypes.byref(desc))
+
+
 def of_layernorm_partial_rows(M):
     return load().of_layernorm_partial_rows(M)
 
@@ -197,7 +210,8 @@ for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_line
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_fwd_fused", "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
            "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_layernorm_fwd", "of_layernorm_bwd",
-           "of_reduce_rows", "of_add"):
+           "of_reduce_rows", "of_add", "of_dwconv_fwd", "of_dwconv_bwd_data",
+           "of_dwconv_bwd_weight", "of_dwconv_wgrad_fused"):
     globals()[_n] = _wrap(_n)
 del _n
 

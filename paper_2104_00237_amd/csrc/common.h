@@ -305,6 +305,18 @@ constexpr int kMergedMaxM = 64;
 size_t merged_workspace_bytes(int M, int N, int K);
 hipError_t merged_bwd_launch(const MergedLaunch& L, hipStream_t stream);
 
+// ------------------------------------------------------ depthwise 3x3 conv
+size_t dw_workspace_bytes(const of_conv_desc& d);
+hipError_t launch_dw_fwd(const of_conv_desc& d, const float* x, const float* w, const float* b,
+                         float* y, hipStream_t stream);
+hipError_t launch_dw_dgrad(const of_conv_desc& d, const float* dy, const float* w,
+                           const float* prev, int act_prev, float* dx, hipStream_t stream);
+// o == NULL: eager (writes or adds dw, db); else backward-fusion of W and b.
+hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* x, float* dw,
+                           float* db, int accumulate, const of_param* W, const of_param* b,
+                           const float* gW, const float* gb, const OptK* o, void* ws,
+                           hipStream_t stream);
+
 // ------------------------------------------------------ elementwise / losses
 hipError_t launch_multi_update(int n, const of_param* params, const float* const* grads,
                                const OptK& o, hipStream_t stream);

@@ -1,0 +1,222 @@
+// Depthwise 3x3 convolution (one filter per channel, stride 1, zero pad 1),
+// NHWC activations, filter [3,3,C] (tap-major, channels contiguous), bias [C].
+// These layers have few parameters and little arithmetic per byte, so every
+// kernel here is bound by HBM traffic, not by the matrix cores: consecutive
+// lanes take consecutive channels (coalesced 256-byte wave accesses) and the
+// nine neighbour reads of a pixel come from L1/L2.
+//
+// Filter gradient: dW[ky,kx,c] = sum over (n,h,w) of dy[n,h,w,c] *
+// x[n,h+ky-1,w+kx-1,c], db[c] = sum of dy[n,h,w,c].  Pass 1 splits the pixels
+// over S slices; each workgroup (64 channels x 4 pixel streams) writes the ten
+// per-channel sums of its slice.  Pass 2 adds the S slices in slice order and
+// either writes dW / db (eager) or applies the optimizer to W, b and their
+// history right there (backward-fusion: the filter gradient is never stored).
+// Both passes are deterministic, and the fused pass applies the same
+// per-element update as the eager optimizer kernel, so the two give the same
+// bits.
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace opfuse {
+
+constexpr int DW_CB = 64;     // channels per workgroup in pass 1
+constexpr int DW_TAPS = 10;   // nine filter taps + the bias sum
+
+struct DwShape {
+  int N, H, W, C;
+};
+
+__global__ __launch_bounds__(256) void dw_fwd_kernel(const float* __restrict__ x,
+                                                     const float* __restrict__ w,
+                                                     const float* __restrict__ b,
+                                                     float* __restrict__ y, DwShape s, int act,
+                                                     int total) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int c = i % s.C, p = i / s.C;
+  const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+  float acc = 0.f;
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    const int hh = row + ky - 1;
+    if (hh < 0 || hh >= s.H) continue;
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int ww = col + kx - 1;
+      if (ww < 0 || ww >= s.W) continue;
+      acc = __fmaf_rn(x[((n * s.H + hh) * s.W + ww) * s.C + c], w[(ky * 3 + kx) * s.C + c], acc);
+    }
+  }
+  const float z = b ? __fadd_rn(acc, b[c]) : acc;
+  y[i] = act_fwd(act, z);
+}
+
+// dx[n,h,w,c] = sum over taps of dy[n,h-ky+1,w-kx+1,c] * W[ky,kx,c], times the
+// previous layer's activation derivative (ReLU: its saved output > 0).
+__global__ __launch_bounds__(256) void dw_dgrad_kernel(const float* __restrict__ dy,
+                                                       const float* __restrict__ w,
+                                                       const float* __restrict__ prev,
+                                                       int act_prev, float* __restrict__ dx,
+                                                       DwShape s, int total) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int c = i % s.C, p = i / s.C;
+  const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+  float acc = 0.f;
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    const int hh = row - ky + 1;
+    if (hh < 0 || hh >= s.H) continue;
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int ww = col - kx + 1;
+      if (ww < 0 || ww >= s.W) continue;
+      acc = __fmaf_rn(dy[((n * s.H + hh) * s.W + ww) * s.C + c], w[(ky * 3 + kx) * s.C + c], acc);
+    }
+  }
+  dx[i] = act_prev == OF_ACT_NONE ? acc : __fmul_rn(acc, act_grad(act_prev, prev[i]));
+}
+
+// Pass 1: workgroup (cb, slice) sums its slice's pixels for 64 channels.
+__global__ __launch_bounds__(256) void dw_wgrad_partial_kernel(const float* __restrict__ dy,
+                                                               const float* __restrict__ x,
+                                                               float* __restrict__ part,
+                                                               DwShape s, int per_slice) {
+  __shared__ float red[4][DW_TAPS][DW_CB];
+  const int cl = threadIdx.x & (DW_CB - 1), sub = threadIdx.x >> 6;
+  const int c = blockIdx.x * DW_CB + cl;
+  const int P = s.N * s.H * s.W;
+  const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
+  float acc[DW_TAPS];
+#pragma unroll
+  for (int k = 0; k < DW_TAPS; ++k) acc[k] = 0.f;
+  if (c < s.C) {
+    for (int p = p0 + sub; p < p1; p += 4) {
+      const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+      const float g = dy[p * s.C + c];
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        const int hh = row + ky - 1;
+        const bool rin = hh >= 0 && hh < s.H;
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          const int ww = col + kx - 1;
+          if (rin && ww >= 0 && ww < s.W)
+            acc[ky * 3 + kx] = __fmaf_rn(g, x[((n * s.H + hh) * s.W + ww) * s.C + c], acc[ky * 3 + kx]);
+        }
+      }
+      acc[9] = __fadd_rn(acc[9], g);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < DW_TAPS; ++k) red[sub][k][cl] = acc[k];
+  __syncthreads();
+  for (int j = threadIdx.x; j < DW_TAPS * DW_CB; j += 256) {
+    const int k = j / DW_CB, l = j % DW_CB, cc = blockIdx.x * DW_CB + l;
+    const float v = __fadd_rn(__fadd_rn(__fadd_rn(red[0][k][l], red[1][k][l]), red[2][k][l]),
+                              red[3][k][l]);
+    if (cc < s.C) part[((int64_t)blockIdx.y * DW_TAPS + k) * s.C + cc] = v;
+  }
+}
+
+struct DwReduce {
+  const float* part;
+  int S, C;
+  // eager
+  float* dw;
+  float* db;
+  int accumulate;
+  // fused
+  int fused;
+  of_param W, b;
+  const float* gW;
+  const float* gb;
+};
+
+// Pass 2: one thread per filter element (and bias element).
+__global__ __launch_bounds__(256) void dw_wgrad_reduce_kernel(DwReduce r, OptK o) {
+  if (r.fused) opt_prepare(o);
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= DW_TAPS * r.C) return;
+  const int k = j / r.C, c = j % r.C;
+  const bool bias = k == 9;
+  if (bias && !(r.fused ? r.b.w != nullptr : r.db != nullptr)) return;
+  float g = r.part[j];
+  for (int sl = 1; sl < r.S; ++sl) g = __fadd_rn(g, r.part[(int64_t)sl * DW_TAPS * r.C + j]);
+  if (!r.fused) {
+    float* dst = bias ? r.db + c : r.dw + j;
+    *dst = r.accumulate ? __fadd_rn(*dst, g) : g;
+    return;
+  }
+  const float* gp = bias ? r.gb : r.gW;
+  const int off = bias ? c : j;
+  if (gp) g = __fadd_rn(g, gp[off]);
+  update1(o, bias ? r.b : r.W, g, off);
+}
+
+namespace {
+int dw_slices(const of_conv_desc& d) {
+  const int64_t P = d.N * d.H * d.W;
+  const int64_t cb = (d.C + DW_CB - 1) / DW_CB;
+  const int64_t want = std::max<int64_t>(1, 1024 / cb);
+  return (int)std::max<int64_t>(1, std::min<int64_t>((P + 255) / 256, want));
+}
+DwShape dw_shape(const of_conv_desc& d) {
+  return DwShape{(int)d.N, (int)d.H, (int)d.W, (int)d.C};
+}
+}  // namespace
+
+size_t dw_workspace_bytes(const of_conv_desc& d) {
+  return (size_t)dw_slices(d) * DW_TAPS * (size_t)d.C * sizeof(float);
+}
+
+hipError_t launch_dw_fwd(const of_conv_desc& d, const float* x, const float* w, const float* b,
+                         float* y, hipStream_t stream) {
+  const int total = (int)(d.N * d.H * d.W * d.C);
+  hipLaunchKernelGGL(dw_fwd_kernel, dim3((total + 255) / 256), dim3(256), 0, stream, x, w,
+                     d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_dgrad(const of_conv_desc& d, const float* dy, const float* w,
+                           const float* prev, int act_prev, float* dx, hipStream_t stream) {
+  const int total = (int)(d.N * d.H * d.W * d.C);
+  hipLaunchKernelGGL(dw_dgrad_kernel, dim3((total + 255) / 256), dim3(256), 0, stream, dy, w,
+                     prev, act_prev, dx, dw_shape(d), total);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* x, float* dw,
+                           float* db, int accumulate, const of_param* W, const of_param* b,
+                           const float* gW, const float* gb, const OptK* o, void* ws,
+                           hipStream_t stream) {
+  const int S = dw_slices(d);
+  const int64_t P = d.N * d.H * d.W;
+  const int per = (int)((P + S - 1) / S);
+  const int cb = (int)((d.C + DW_CB - 1) / DW_CB);
+  float* part = static_cast<float*>(ws);
+  hipLaunchKernelGGL(dw_wgrad_partial_kernel, dim3(cb, S), dim3(256), 0, stream, dy, x, part,
+                     dw_shape(d), per);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  DwReduce r{};
+  r.part = part;
+  r.S = S;
+  r.C = (int)d.C;
+  r.dw = dw;
+  r.db = db;
+  r.accumulate = accumulate;
+  r.fused = o != nullptr;
+  if (W) r.W = *W;
+  if (b) r.b = *b;
+  r.gW = gW;
+  r.gb = gb;
+  const int n = DW_TAPS * (int)d.C;
+  hipLaunchKernelGGL(dw_wgrad_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, r,
+                     o ? *o : OptK{});
+  return hipGetLastError();
+}
+
+}  // namespace opfuse

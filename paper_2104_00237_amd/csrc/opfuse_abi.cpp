@@ -675,6 +675,94 @@ of_status of_conv_wgrad_fused(const of_conv_desc* d, const float* dy, const floa
                                 (hipStream_t)stream), "of_conv_wgrad_fused launch");
 }
 
+namespace {
+of_status check_dw(const of_conv_desc* d) {
+  REQUIRE(d != nullptr, OF_EINVAL, "desc is NULL");
+  REQUIRE(d->N >= 1 && d->H >= 1 && d->W >= 1 && d->C >= 1, OF_EINVAL,
+          "N, H, W, C must be >= 1");
+  REQUIRE(d->Cout == d->C, OF_EINVAL, "a depthwise convolution needs Cout == C (got %lld, %lld)",
+          (long long)d->Cout, (long long)d->C);
+  REQUIRE(d->N * d->H * d->W * d->C < (1LL << 31), OF_EUNSUPPORTED,
+          "activation tensors must have < 2^31 elements");
+  REQUIRE(d->act == OF_ACT_NONE || d->act == OF_ACT_RELU, OF_EUNSUPPORTED,
+          "depthwise convolutions support OF_ACT_NONE and OF_ACT_RELU");
+  return OF_OK;
+}
+
+of_status check_dw_ws(const of_conv_desc* d, const void* ws, size_t ws_bytes) {
+  const size_t need = dw_workspace_bytes(*d);
+  REQUIRE(ws_bytes >= need, OF_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu needed",
+          ws_bytes, need);
+  REQUIRE(ws != nullptr, OF_EWORKSPACE, "workspace is NULL");
+  REQUIRE((((uintptr_t)ws) & 15u) == 0, OF_EALIGN, "workspace must be 16-byte aligned");
+  return OF_OK;
+}
+}  // namespace
+
+size_t of_dwconv_workspace_size(const of_conv_desc* d) {
+  if (check_dw(d) != OF_OK) return 0;
+  return dw_workspace_bytes(*d);
+}
+
+of_status of_dwconv_fwd(const of_conv_desc* d, const float* x, const float* W, const float* b,
+                        float* y, void* stream) {
+  of_status st = check_dw(d);
+  if (st != OF_OK) return st;
+  REQUIRE(x && W && y, OF_EINVAL, "x, W and y are required");
+  REQUIRE(!d->has_bias || b, OF_EINVAL, "has_bias is set but b is NULL");
+  REQUIRE(al4(x) && al4(W) && al4(b) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_dw_fwd(*d, x, W, b, y, (hipStream_t)stream), "of_dwconv_fwd launch");
+}
+
+of_status of_dwconv_bwd_data(const of_conv_desc* d, const float* dy, const float* W,
+                             const float* prev, int32_t act_prev, float* dx, void* stream) {
+  of_status st = check_dw(d);
+  if (st != OF_OK) return st;
+  REQUIRE(dy && W && dx, OF_EINVAL, "dy, W and dx are required");
+  REQUIRE(act_prev == OF_ACT_NONE || act_prev == OF_ACT_RELU, OF_EUNSUPPORTED,
+          "act_prev must be OF_ACT_NONE or OF_ACT_RELU");
+  REQUIRE(act_prev == OF_ACT_NONE || prev, OF_EINVAL, "act_prev needs prev");
+  REQUIRE(al4(dy) && al4(W) && al4(prev) && al4(dx), OF_EALIGN,
+          "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_dw_dgrad(*d, dy, W, prev, act_prev, dx, (hipStream_t)stream),
+                    "of_dwconv_bwd_data launch");
+}
+
+of_status of_dwconv_bwd_weight(const of_conv_desc* d, const float* dy, const float* x, float* dw,
+                               float* db, int32_t accumulate, void* ws, size_t ws_bytes,
+                               void* stream) {
+  of_status st = check_dw(d);
+  if (st != OF_OK) return st;
+  REQUIRE(dy && x && dw, OF_EINVAL, "dy, x and dw are required");
+  REQUIRE(accumulate == 0 || accumulate == 1, OF_EINVAL, "accumulate must be 0 or 1");
+  REQUIRE(al4(dy) && al4(x) && al4(dw) && al4(db), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  if ((st = check_dw_ws(d, ws, ws_bytes)) != OF_OK) return st;
+  return hip_status(launch_dw_wgrad(*d, dy, x, dw, db, accumulate, nullptr, nullptr, nullptr,
+                                    nullptr, nullptr, ws, (hipStream_t)stream),
+                    "of_dwconv_bwd_weight launch");
+}
+
+of_status of_dwconv_wgrad_fused(const of_conv_desc* d, const float* dy, const float* x,
+                                const of_param* W, const of_param* b, const float* gW_partial,
+                                const float* gb_partial, const of_opt* opt, void* ws,
+                                size_t ws_bytes, void* stream) {
+  of_status st = check_dw(d);
+  if (st != OF_OK) return st;
+  if ((st = check_opt(opt)) != OF_OK) return st;
+  REQUIRE(dy && x, OF_EINVAL, "dy and x are required");
+  if ((st = check_param(W, "W", 9 * d->C, *opt, true)) != OF_OK) return st;
+  if (b) {
+    if ((st = check_param(b, "b", d->C, *opt, true)) != OF_OK) return st;
+  }
+  REQUIRE(al4(dy) && al4(x) && al4(gW_partial) && al4(gb_partial), OF_EALIGN,
+          "fp32 pointers must be 4-byte aligned");
+  if ((st = check_dw_ws(d, ws, ws_bytes)) != OF_OK) return st;
+  const OptK o = make_optk(*opt);
+  return hip_status(launch_dw_wgrad(*d, dy, x, nullptr, nullptr, 0, W, b, gW_partial,
+                                    b ? gb_partial : nullptr, &o, ws, (hipStream_t)stream),
+                    "of_dwconv_wgrad_fused launch");
+}
+
 of_status of_maxpool2x2_fwd(const float* x, int64_t N, int64_t H, int64_t W, int64_t C, float* y,
                             uint8_t* argmax, void* stream) {
   REQUIRE(x && y && argmax, OF_EINVAL, "x, y and argmax are required");

@@ -262,3 +262,37 @@ def test_clip_validation(lib):
     opt = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1, None, FAKE + 2)
     assert _status(L.of_optimizer_step, 1, (L.OfParam * 1)(_param(8)),
                    (ctypes.c_void_p * 1)(FAKE), opt, None) == L.OF_EALIGN
+
+
+def test_depthwise_validation(lib):
+    opt = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1)
+    d = L.OfConvDesc(2, 5, 7, 3, 3, L.OF_ACT_RELU, 1)
+    need = L.of_dwconv_workspace_size(d)
+    assert need >= 10 * 3 * 4
+    bad = L.OfConvDesc(2, 5, 7, 3, 4, L.OF_ACT_NONE, 1)  # Cout != C
+    assert L.of_dwconv_workspace_size(bad) == 0
+    assert _status(L.of_dwconv_fwd, bad, FAKE, FAKE, FAKE, FAKE, None) == L.OF_EINVAL
+    gelu = L.OfConvDesc(2, 5, 7, 3, 3, L.OF_ACT_GELU, 1)
+    assert _status(L.of_dwconv_fwd, gelu, FAKE, FAKE, FAKE, FAKE, None) == L.OF_EUNSUPPORTED
+    huge = L.OfConvDesc(1 << 12, 1 << 10, 1 << 10, 3, 3, L.OF_ACT_NONE, 0)
+    assert _status(L.of_dwconv_fwd, huge, FAKE, FAKE, None, FAKE, None) == L.OF_EUNSUPPORTED
+    assert _status(L.of_dwconv_fwd, d, FAKE, FAKE, None, FAKE, None) == L.OF_EINVAL  # bias
+    assert _status(L.of_dwconv_fwd, d, FAKE + 2, FAKE, FAKE, FAKE, None) == L.OF_EALIGN
+    assert _status(L.of_dwconv_bwd_data, d, FAKE, FAKE, None, L.OF_ACT_RELU, FAKE,
+                   None) == L.OF_EINVAL
+    assert _status(L.of_dwconv_bwd_data, d, FAKE, FAKE, FAKE, L.OF_ACT_GELU, FAKE,
+                   None) == L.OF_EUNSUPPORTED
+    assert _status(L.of_dwconv_bwd_weight, d, FAKE, FAKE, FAKE, None, 0, FAKE, need - 4,
+                   None) == L.OF_EWORKSPACE
+    assert _status(L.of_dwconv_bwd_weight, d, FAKE, FAKE, FAKE, None, 2, FAKE, need,
+                   None) == L.OF_EINVAL
+    W, b = _param(27), _param(3)
+    assert _status(L.of_dwconv_wgrad_fused, d, FAKE, FAKE, _param(26), b, None, None, opt, FAKE,
+                   need, None) == L.OF_EINVAL
+    assert _status(L.of_dwconv_wgrad_fused, d, FAKE, FAKE, W, _param(4), None, None, opt, FAKE,
+                   need, None) == L.OF_EINVAL
+    assert _status(L.of_dwconv_wgrad_fused, d, FAKE, FAKE, W, b, None, None, opt, FAKE + 4,
+                   need, None) == L.OF_EALIGN
+    opt.step = 0
+    assert _status(L.of_dwconv_wgrad_fused, d, FAKE, FAKE, W, b, None, None, opt, FAKE, need,
+                   None) == L.OF_EINVAL

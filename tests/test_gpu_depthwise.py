@@ -1,0 +1,189 @@
+"""Depthwise 3x3 convolutions on the GPU against the oracle: forward (bias, ReLU),
+data gradient with the old filter and the previous layer's ReLU mask, eager filter
+gradient, and backward-fusion (filter and bias gradients applied by the optimizer in
+the reduction and never stored), which must give the same bits as the eager
+filter gradient followed by the optimizer step.
+
+Tolerances come from the fp32 arithmetic: each result is a sum of products whose
+rounding error is at most n u sum|terms| for a chain of n additions (u = 2^-24).
+The forward and data gradient chain 10 terms; the filter gradient chains at most
+per-thread pixels + 4 + slices <= 1500 additions for the shapes here, so 1e-4 of
+the absolute-value sum bounds it.  Updated parameters use the kernels' common
+relative bound (1e-4 of the largest reference value)."""
+import numpy as np
+import pytest
+
+from oracle import layers as OL
+from oracle import optim as OO
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # N, H, W, C: single pixel, ragged channel tails, several slices, MobileNetV2 sizes
+    (1, 1, 1, 1), (2, 5, 7, 3), (3, 9, 11, 67), (4, 8, 8, 64), (8, 14, 14, 96),
+    (2, 28, 28, 130), (32, 56, 56, 144),
+]
+HYPERS = {
+    "sgd": dict(kind="sgd", lr=0.05, momentum=0.9, weight_decay=5e-4),
+    "adam": dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0),
+    "adagrad": dict(kind="adagrad", lr=0.01, eps=1e-10, weight_decay=1e-4),
+}
+
+
+def rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    den = np.max(np.abs(b))
+    return float(np.max(np.abs(a - b)) / (den if den > 0 else 1.0))
+
+
+@pytest.fixture(scope="module")
+def env(gpu):
+    import torch
+    from paper_2104_00237_amd import _lib as L
+    L.load()
+    return torch, L, gpu
+
+
+def _t(torch, dev, a):
+    return torch.as_tensor(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+
+def _inputs(shape, seed):
+    r = np.random.default_rng(seed)
+    n, h, w, c = shape
+    x = r.standard_normal(shape).astype(np.float32)
+    dy = (r.standard_normal(shape) * 0.1).astype(np.float32)
+    wt = (r.standard_normal((3, 3, c)) * 0.3).astype(np.float32)
+    b = (r.standard_normal(c) * 0.1).astype(np.float32)
+    prev = np.maximum(r.standard_normal(shape), 0).astype(np.float32)  # a ReLU output
+    return x, dy, wt, b, prev
+
+
+def _oracle(x, dy, wt, b):
+    op = OL.DepthwiseConv3x3(OL.Param("w", wt.astype(np.float64)), OL.Param("b", b.astype(np.float64)))
+    y, xp = op.forward(x.astype(np.float64))
+    (dx,), (dw, db) = op.backward(xp, dy.astype(np.float64))
+    ab = OL.DepthwiseConv3x3(OL.Param("w", np.abs(wt).astype(np.float64)),
+                             OL.Param("b", np.abs(b).astype(np.float64)))
+    ybound = ab.abs_bound(x.astype(np.float64))
+    _, xpa = ab.forward(np.abs(x).astype(np.float64))
+    (dxb,), (dwb, dbb) = ab.backward(xpa, np.abs(dy).astype(np.float64))
+    return dict(y=y, dx=dx, dw=dw, db=db, yb=ybound, dxb=dxb, dwb=dwb, dbb=dbb)
+
+
+def _within(got, ref, bound, k):
+    err = np.abs(got.astype(np.float64) - ref)
+    assert np.all(err <= k * bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_depthwise_fwd_dgrad_wgrad(env, shape):
+    torch, L, dev = env
+    x, dy, wt, b, prev = _inputs(shape, sum(shape))
+    ref = _oracle(x, dy, wt, b)
+    n, h, w, c = shape
+    s = torch.cuda.current_stream().cuda_stream
+    X, DY, Wt, B, PR = (_t(torch, dev, a) for a in (x, dy, wt, b, prev))
+    for act in (L.OF_ACT_NONE, L.OF_ACT_RELU):
+        d = L.OfConvDesc(n, h, w, c, c, act, 1)
+        Y = torch.empty(shape, device=dev)
+        L.of_dwconv_fwd(d, X.data_ptr(), Wt.data_ptr(), B.data_ptr(), Y.data_ptr(), s)
+        r = ref["y"] if act == L.OF_ACT_NONE else np.maximum(ref["y"], 0)
+        _within(Y.cpu().numpy(), r, ref["yb"], 1e-6)
+    d = L.OfConvDesc(n, h, w, c, c, L.OF_ACT_NONE, 0)
+    Y = torch.empty(shape, device=dev)
+    L.of_dwconv_fwd(d, X.data_ptr(), Wt.data_ptr(), None, Y.data_ptr(), s)
+    _within(Y.cpu().numpy(), ref["y"] - b.astype(np.float64), ref["yb"], 1e-6)
+    # data gradient, plain and through the previous layer's ReLU mask
+    DX = torch.empty(shape, device=dev)
+    L.of_dwconv_bwd_data(d, DY.data_ptr(), Wt.data_ptr(), None, L.OF_ACT_NONE, DX.data_ptr(), s)
+    _within(DX.cpu().numpy(), ref["dx"], ref["dxb"], 1e-6)
+    L.of_dwconv_bwd_data(d, DY.data_ptr(), Wt.data_ptr(), PR.data_ptr(), L.OF_ACT_RELU,
+                         DX.data_ptr(), s)
+    got = DX.cpu().numpy()
+    _within(got, ref["dx"] * (prev > 0), ref["dxb"], 1e-6)
+    assert np.all(got[prev <= 0] == 0)
+    # eager filter gradient: write, then accumulate onto itself
+    ws = torch.empty(max(4, L.of_dwconv_workspace_size(d) // 4), device=dev)
+    DW, DB = torch.empty((3, 3, c), device=dev), torch.empty(c, device=dev)
+    L.of_dwconv_bwd_weight(d, DY.data_ptr(), X.data_ptr(), DW.data_ptr(), DB.data_ptr(), 0,
+                           ws.data_ptr(), ws.numel() * 4, s)
+    dw1, db1 = DW.cpu().numpy(), DB.cpu().numpy()
+    _within(dw1, ref["dw"], ref["dwb"], 1e-4)
+    _within(db1, ref["db"], ref["dbb"], 1e-4)
+    L.of_dwconv_bwd_weight(d, DY.data_ptr(), X.data_ptr(), DW.data_ptr(), DB.data_ptr(), 1,
+                           ws.data_ptr(), ws.numel() * 4, s)
+    np.testing.assert_array_equal(DW.cpu().numpy(), (dw1 + dw1).astype(np.float32))
+    np.testing.assert_array_equal(DB.cpu().numpy(), (db1 + db1).astype(np.float32))
+    # a second call with the same inputs gives the same bits (fixed reduction order)
+    L.of_dwconv_bwd_weight(d, DY.data_ptr(), X.data_ptr(), DW.data_ptr(), None, 0,
+                           ws.data_ptr(), ws.numel() * 4, s)
+    np.testing.assert_array_equal(DW.cpu().numpy(), dw1)
+
+
+_ORACLE = {}
+
+
+class _P:
+    def __init__(self, torch, L, dev, a, seed):
+        r = np.random.default_rng(seed)
+        self.w0 = a.copy()
+        self.m0 = (r.standard_normal(a.shape) * 0.01).astype(np.float32)
+        self.v0 = ((0.5 + r.random(a.shape)) * 1e-3).astype(np.float32)
+        self.W, self.M, self.V = (_t(torch, dev, t) for t in (self.w0, self.m0, self.v0))
+        self.p = L.OfParam(self.W.data_ptr(), self.M.data_ptr(), self.V.data_ptr(), None,
+                           self.W.numel())
+
+    def state(self):
+        return [t.cpu().numpy() for t in (self.W, self.M, self.V)]
+
+
+@pytest.mark.parametrize("kind", sorted(HYPERS))
+@pytest.mark.parametrize("shape", [(2, 5, 7, 3), (3, 9, 11, 67), (8, 14, 14, 96),
+                                   (32, 56, 56, 144)])
+@pytest.mark.parametrize("with_partial", [False, True])
+def test_depthwise_backward_fusion(env, kind, shape, with_partial):
+    torch, L, dev = env
+    hyper = HYPERS[kind]
+    x, dy, wt, b, _ = _inputs(shape, 7 + sum(shape))
+    n, h, w, c = shape
+    d = L.OfConvDesc(n, h, w, c, c, L.OF_ACT_NONE, 1)
+    s = torch.cuda.current_stream().cuda_stream
+    X, DY = _t(torch, dev, x), _t(torch, dev, dy)
+    r = np.random.default_rng(5)
+    gwp = (r.standard_normal((3, 3, c)) * 0.05).astype(np.float32)
+    gbp = (r.standard_normal(c) * 0.05).astype(np.float32)
+    GWP, GBP = _t(torch, dev, gwp), _t(torch, dev, gbp)
+    ws = torch.empty(max(4, L.of_dwconv_workspace_size(d) // 4), device=dev)
+    opt = L.make_opt(hyper, 3)
+    # fused
+    Wf, Bf = _P(torch, L, dev, wt, 1), _P(torch, L, dev, b, 2)
+    L.of_dwconv_wgrad_fused(d, DY.data_ptr(), X.data_ptr(), Wf.p, Bf.p,
+                            GWP.data_ptr() if with_partial else None,
+                            GBP.data_ptr() if with_partial else None, opt, ws.data_ptr(),
+                            ws.numel() * 4, s)
+    # eager: the filter gradient (accumulated onto the earlier use's), then the optimizer
+    We, Be = _P(torch, L, dev, wt, 1), _P(torch, L, dev, b, 2)
+    DW = GWP.clone() if with_partial else torch.empty((3, 3, c), device=dev)
+    DB = GBP.clone() if with_partial else torch.empty(c, device=dev)
+    L.of_dwconv_bwd_weight(d, DY.data_ptr(), X.data_ptr(), DW.data_ptr(), DB.data_ptr(),
+                           int(with_partial), ws.data_ptr(), ws.numel() * 4, s)
+    L.of_optimizer_step(2, (L.OfParam * 2)(We.p, Be.p),
+                        (L.c_void_p * 2)(DW.data_ptr(), DB.data_ptr()), opt, s)
+    torch.cuda.synchronize()
+    for a, e in zip(Wf.state() + Bf.state(), We.state() + Be.state()):
+        np.testing.assert_array_equal(a, e)
+    # against the oracle's gradient and update (one oracle run per shape)
+    key = (shape, 7 + sum(shape))
+    if key not in _ORACLE:
+        _ORACLE[key] = _oracle(x, dy, wt, b)
+    ref = _ORACLE[key]
+    for P, g, extra in ((Wf, ref["dw"], gwp), (Bf, ref["db"], gbp)):
+        Q = OL.Param("p", P.w0.astype(np.float64))
+        Q.m, Q.v, Q.step = P.m0.astype(np.float64), P.v0.astype(np.float64), 2
+        Q.grad = g + (extra.astype(np.float64) if with_partial else 0.0)
+        OO.apply(Q, hyper)
+        assert rel(P.W.cpu().numpy(), Q.value) <= 1e-4
+        if kind != "adagrad":
+            assert rel(P.M.cpu().numpy(), Q.m) <= 1e-4
+        if kind != "sgd":
+            assert rel(P.V.cpu().numpy(), Q.v) <= 1e-4
