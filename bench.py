@@ -337,6 +337,84 @@ def stage_breakdown(torch, cfg, batches, ordering, steps, marker_ms):
     return out
 
 
+# MobileNetV2's 17 depthwise 3x3 layers (H = W, C) at their output resolution; the
+# stride-2 ones are taken at stride 1 on their output size (the kernels are stride 1).
+MBV2_DEPTHWISE = [(112, 32), (56, 96), (56, 144), (28, 144), (28, 192), (28, 192), (14, 192),
+                  (14, 384), (14, 384), (14, 384), (14, 384), (14, 576), (14, 576), (7, 576),
+                  (7, 960), (7, 960), (7, 960)]
+
+
+def depthwise_stack(torch, batch, steps, warmup):
+    """Backward of MobileNetV2's depthwise layers (batch 32, SGD with momentum): eager
+    (data gradient, filter gradient written, one multi-tensor optimizer launch over all
+    filters and biases) against backward-fusion (data gradient, filter gradient whose
+    reduction applies the update), plus the forward's HBM rate.  Returns milliseconds
+    per pass over the 17 layers."""
+    from paper_2104_00237_amd import _lib as L
+    dev = "cuda:0"
+    hyper = dict(kind="sgd", lr=0.05, momentum=0.9, weight_decay=4e-5)
+    g = torch.Generator(device=dev).manual_seed(0)
+    layers = []
+    for hw, c in MBV2_DEPTHWISE:
+        d = L.OfConvDesc(batch, hw, hw, c, c, L.OF_ACT_RELU, 1)
+        t = dict(d=d, x=torch.randn((batch, hw, hw, c), device=dev, generator=g),
+                 dy=torch.randn((batch, hw, hw, c), device=dev, generator=g) * 0.1)
+        t["y"], t["dx"] = torch.empty_like(t["x"]), torch.empty_like(t["x"])
+        t["ws"] = torch.empty(max(4, L.of_dwconv_workspace_size(d) // 4), device=dev)
+        for nm, shape in (("W", (3, 3, c)), ("b", (c,))):
+            w, m = torch.randn(shape, device=dev, generator=g) * 0.1, torch.zeros(shape, device=dev)
+            t[nm] = (w, m, L.OfParam(w.data_ptr(), m.data_ptr(), None, None, w.numel()),
+                     torch.empty(shape, device=dev))
+        layers.append(t)
+    s = torch.cuda.current_stream().cuda_stream
+    opt = L.make_opt(hyper, 1)
+
+    def fwd():
+        for t in layers:
+            L.of_dwconv_fwd(t["d"], t["x"].data_ptr(), t["W"][0].data_ptr(), t["b"][0].data_ptr(),
+                            t["y"].data_ptr(), s)
+
+    def eager():
+        for t in layers:
+            L.of_dwconv_bwd_data(t["d"], t["dy"].data_ptr(), t["W"][0].data_ptr(),
+                                 t["x"].data_ptr(), L.OF_ACT_RELU, t["dx"].data_ptr(), s)
+            L.of_dwconv_bwd_weight(t["d"], t["dy"].data_ptr(), t["x"].data_ptr(),
+                                   t["W"][3].data_ptr(), t["b"][3].data_ptr(), 0,
+                                   t["ws"].data_ptr(), t["ws"].numel() * 4, s)
+        ps = [t[k][2] for t in layers for k in ("W", "b")]
+        gs = [t[k][3].data_ptr() for t in layers for k in ("W", "b")]
+        L.of_optimizer_step(len(ps), (L.OfParam * len(ps))(*ps), (L.c_void_p * len(gs))(*gs),
+                            opt, s)
+
+    def bf():
+        for t in layers:
+            L.of_dwconv_bwd_data(t["d"], t["dy"].data_ptr(), t["W"][0].data_ptr(),
+                                 t["x"].data_ptr(), L.OF_ACT_RELU, t["dx"].data_ptr(), s)
+            L.of_dwconv_wgrad_fused(t["d"], t["dy"].data_ptr(), t["x"].data_ptr(), t["W"][2],
+                                    t["b"][2], None, None, opt, t["ws"].data_ptr(),
+                                    t["ws"].numel() * 4, s)
+
+    res = {}
+    for name, fn in (("forward", fwd), ("eager_backward", eager), ("bf_backward", bf)):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / steps
+    act_bytes = sum(2 * batch * hw * hw * c * 4 for hw, c in MBV2_DEPTHWISE)
+    n_params = sum(10 * c for _, c in MBV2_DEPTHWISE)
+    return {"layers": len(MBV2_DEPTHWISE), "batch": batch, "params": n_params,
+            "optimizer": "sgd_momentum",
+            **{k + "_ms": round(v, 4) for k, v in res.items()},
+            "bf_speedup_backward": round(res["eager_backward"] / res["bf_backward"], 3),
+            "forward_GBps": round(act_bytes / (res["forward"] * 1e-3) / 1e9, 1)}
+
+
 def cpu_baseline(cfg, budget_s=15.0):
     """Oracle eager steps on this host, seconds per step of `cfg`.  The 12-block
     Transformer stack is sampled as one block (same width and tokens) and its
@@ -377,6 +455,9 @@ def main():
                          "Fig. 6 sweep); the input and output widths follow WIDTH and the classes")
     ap.add_argument("--conv-ff-prologue", action="store_true",
                     help="vgg11: also time forward-fusion with the filter-tile prologue (ffp)")
+    ap.add_argument("--depthwise", action="store_true",
+                    help="also time MobileNetV2's depthwise 3x3 layers (batch 32): eager "
+                         "vs backward-fusion backward, and the forward's HBM rate")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -574,6 +655,8 @@ def main():
                                          + (" (one of its blocks, time x blocks)"
                                             if cfg["kind"] == "tblock" else "")
                                          + f" (oracle, numpy, {cores} host threads)"}
+    if args.depthwise:
+        out["depthwise_mbv2"] = depthwise_stack(torch, 32, args.steps, args.warmup)
     print(json.dumps(out))
 
 

@@ -7,13 +7,15 @@
 //
 // Filter gradient: dW[ky,kx,c] = sum over (n,h,w) of dy[n,h,w,c] *
 // x[n,h+ky-1,w+kx-1,c], db[c] = sum of dy[n,h,w,c].  Pass 1 splits the pixels
-// over S slices; each workgroup (64 channels x 4 pixel streams) writes the ten
-// per-channel sums of its slice.  Pass 2 adds the S slices in slice order and
-// either writes dW / db (eager) or applies the optimizer to W, b and their
-// history right there (backward-fusion: the filter gradient is never stored).
-// Both passes are deterministic, and the fused pass applies the same
-// per-element update as the eager optimizer kernel, so the two give the same
-// bits.
+// over S slices; each workgroup (64 channels x 4 pixel streams, or 16 channel
+// quads x 16 pixel streams when C % 4 == 0 and the tensors are 16-byte
+// aligned) writes the ten per-channel sums of its slice.  Pass 2 adds the S
+// slices in slice order and either writes dW / db (eager) or applies the
+// optimizer to W, b and their history right there (backward-fusion: the
+// filter gradient is never stored).  A shape always takes the same pass-1
+// kernel, so both passes are deterministic, and the fused pass applies the
+// same per-element update as the eager optimizer kernel: the two give the
+// same bits.
 
 #include <algorithm>
 
@@ -121,6 +123,125 @@ __global__ __launch_bounds__(256) void dw_wgrad_partial_kernel(const float* __re
   }
 }
 
+// ---- four-channel variants (C % 4 == 0, 16-byte aligned tensors): one thread
+// per channel quad, 128-bit loads and stores; every element takes the same
+// arithmetic, in the same order, as in the one-channel kernels above.
+__device__ __forceinline__ float4 fma4(float4 a, float4 b, float4 c) {
+  return make_float4(__fmaf_rn(a.x, b.x, c.x), __fmaf_rn(a.y, b.y, c.y), __fmaf_rn(a.z, b.z, c.z),
+                     __fmaf_rn(a.w, b.w, c.w));
+}
+
+__global__ __launch_bounds__(256) void dw_fwd4_kernel(const float* __restrict__ x,
+                                                      const float* __restrict__ w,
+                                                      const float* __restrict__ b,
+                                                      float* __restrict__ y, DwShape s, int act,
+                                                      int quads) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= quads) return;
+  const int Cq = s.C >> 2;
+  const int c = (i % Cq) * 4, p = i / Cq;
+  const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    const int hh = row + ky - 1;
+    if (hh < 0 || hh >= s.H) continue;
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int ww = col + kx - 1;
+      if (ww < 0 || ww >= s.W) continue;
+      acc = fma4(ld4(x + ((n * s.H + hh) * s.W + ww) * s.C + c), ld4(w + (ky * 3 + kx) * s.C + c), acc);
+    }
+  }
+  if (b) {
+    const float4 bb = ld4(b + c);
+    acc = make_float4(__fadd_rn(acc.x, bb.x), __fadd_rn(acc.y, bb.y), __fadd_rn(acc.z, bb.z),
+                      __fadd_rn(acc.w, bb.w));
+  }
+  st4(y + (int64_t)i * 4, make_float4(act_fwd(act, acc.x), act_fwd(act, acc.y), act_fwd(act, acc.z),
+                                      act_fwd(act, acc.w)));
+}
+
+__global__ __launch_bounds__(256) void dw_dgrad4_kernel(const float* __restrict__ dy,
+                                                        const float* __restrict__ w,
+                                                        const float* __restrict__ prev,
+                                                        int act_prev, float* __restrict__ dx,
+                                                        DwShape s, int quads) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= quads) return;
+  const int Cq = s.C >> 2;
+  const int c = (i % Cq) * 4, p = i / Cq;
+  const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    const int hh = row - ky + 1;
+    if (hh < 0 || hh >= s.H) continue;
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int ww = col - kx + 1;
+      if (ww < 0 || ww >= s.W) continue;
+      acc = fma4(ld4(dy + ((n * s.H + hh) * s.W + ww) * s.C + c), ld4(w + (ky * 3 + kx) * s.C + c), acc);
+    }
+  }
+  if (act_prev != OF_ACT_NONE) {
+    const float4 pv = ld4(prev + (int64_t)i * 4);
+    acc = make_float4(__fmul_rn(acc.x, act_grad(act_prev, pv.x)), __fmul_rn(acc.y, act_grad(act_prev, pv.y)),
+                      __fmul_rn(acc.z, act_grad(act_prev, pv.z)), __fmul_rn(acc.w, act_grad(act_prev, pv.w)));
+  }
+  st4(dx + (int64_t)i * 4, acc);
+}
+
+// Pass 1, four channels per thread: 16 channel quads (64 channels) x 16 pixel
+// streams per workgroup.
+__global__ __launch_bounds__(256) void dw_wgrad_partial4_kernel(const float* __restrict__ dy,
+                                                                const float* __restrict__ x,
+                                                                float* __restrict__ part,
+                                                                DwShape s, int per_slice) {
+  __shared__ float red[16][DW_TAPS][DW_CB];
+  const int q = threadIdx.x & 15, sub = threadIdx.x >> 4;
+  const int c = blockIdx.x * DW_CB + q * 4;
+  const int P = s.N * s.H * s.W;
+  const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
+  float4 acc[DW_TAPS];
+#pragma unroll
+  for (int k = 0; k < DW_TAPS; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (c < s.C) {
+    for (int p = p0 + sub; p < p1; p += 16) {
+      const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+      const float4 g = ld4(dy + p * s.C + c);
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        const int hh = row + ky - 1;
+        const bool rin = hh >= 0 && hh < s.H;
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          const int ww = col + kx - 1;
+          if (rin && ww >= 0 && ww < s.W)
+            acc[ky * 3 + kx] = fma4(g, ld4(x + ((n * s.H + hh) * s.W + ww) * s.C + c), acc[ky * 3 + kx]);
+        }
+      }
+      acc[9] = make_float4(__fadd_rn(acc[9].x, g.x), __fadd_rn(acc[9].y, g.y),
+                           __fadd_rn(acc[9].z, g.z), __fadd_rn(acc[9].w, g.w));
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < DW_TAPS; ++k) {
+    red[sub][k][q * 4 + 0] = acc[k].x;
+    red[sub][k][q * 4 + 1] = acc[k].y;
+    red[sub][k][q * 4 + 2] = acc[k].z;
+    red[sub][k][q * 4 + 3] = acc[k].w;
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < DW_TAPS * DW_CB; j += 256) {
+    const int k = j / DW_CB, l = j % DW_CB, cc = blockIdx.x * DW_CB + l;
+    float v = red[0][k][l];
+#pragma unroll
+    for (int u = 1; u < 16; ++u) v = __fadd_rn(v, red[u][k][l]);
+    if (cc < s.C) part[((int64_t)blockIdx.y * DW_TAPS + k) * s.C + cc] = v;
+  }
+}
+
 struct DwReduce {
   const float* part;
   int S, C;
@@ -175,6 +296,12 @@ size_t dw_workspace_bytes(const of_conv_desc& d) {
 hipError_t launch_dw_fwd(const of_conv_desc& d, const float* x, const float* w, const float* b,
                          float* y, hipStream_t stream) {
   const int total = (int)(d.N * d.H * d.W * d.C);
+  if (d.C % 4 == 0 && aligned16(x) && aligned16(w) && aligned16(b) && aligned16(y)) {
+    const int quads = total / 4;
+    hipLaunchKernelGGL(dw_fwd4_kernel, dim3((quads + 255) / 256), dim3(256), 0, stream, x, w,
+                       d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, quads);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(dw_fwd_kernel, dim3((total + 255) / 256), dim3(256), 0, stream, x, w,
                      d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, total);
   return hipGetLastError();
@@ -183,6 +310,12 @@ hipError_t launch_dw_fwd(const of_conv_desc& d, const float* x, const float* w, 
 hipError_t launch_dw_dgrad(const of_conv_desc& d, const float* dy, const float* w,
                            const float* prev, int act_prev, float* dx, hipStream_t stream) {
   const int total = (int)(d.N * d.H * d.W * d.C);
+  if (d.C % 4 == 0 && aligned16(dy) && aligned16(w) && aligned16(prev) && aligned16(dx)) {
+    const int quads = total / 4;
+    hipLaunchKernelGGL(dw_dgrad4_kernel, dim3((quads + 255) / 256), dim3(256), 0, stream, dy, w,
+                       prev, act_prev, dx, dw_shape(d), quads);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(dw_dgrad_kernel, dim3((total + 255) / 256), dim3(256), 0, stream, dy, w,
                      prev, act_prev, dx, dw_shape(d), total);
   return hipGetLastError();
@@ -197,8 +330,12 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
   const int per = (int)((P + S - 1) / S);
   const int cb = (int)((d.C + DW_CB - 1) / DW_CB);
   float* part = static_cast<float*>(ws);
-  hipLaunchKernelGGL(dw_wgrad_partial_kernel, dim3(cb, S), dim3(256), 0, stream, dy, x, part,
-                     dw_shape(d), per);
+  if (d.C % 4 == 0 && aligned16(dy) && aligned16(x))
+    hipLaunchKernelGGL(dw_wgrad_partial4_kernel, dim3(cb, S), dim3(256), 0, stream, dy, x, part,
+                       dw_shape(d), per);
+  else
+    hipLaunchKernelGGL(dw_wgrad_partial_kernel, dim3(cb, S), dim3(256), 0, stream, dy, x, part,
+                       dw_shape(d), per);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   DwReduce r{};
