@@ -264,8 +264,17 @@ __global__ __launch_bounds__(256) void dw_wgrad_reduce_kernel(DwReduce r, OptK o
   const int k = j / r.C, c = j % r.C;
   const bool bias = k == 9;
   if (bias && !(r.fused ? r.b.w != nullptr : r.db != nullptr)) return;
+  // the loads of 8 slices are issued before their (in-order) accumulation
+  const int64_t ld = (int64_t)DW_TAPS * r.C;
   float g = r.part[j];
-  for (int sl = 1; sl < r.S; ++sl) g = __fadd_rn(g, r.part[(int64_t)sl * DW_TAPS * r.C + j]);
+  for (int s0 = 1; s0 < r.S; s0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = s0 + k < r.S ? r.part[(s0 + k) * ld + j] : 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (s0 + k < r.S) g = __fadd_rn(g, v[k]);
+  }
   if (!r.fused) {
     float* dst = bias ? r.db + c : r.dw + j;
     *dst = r.accumulate ? __fadd_rn(*dst, g) : g;
