@@ -1,8 +1,11 @@
 """Benchmark: fused training step vs the unfused eager step on one MI355X.
 
-Workload (default): the 8-layer fp32 MLP of width 1024, batch 256, Adam
-(mlp8x1024).  A step is one training iteration over one resident batch.  All
-three orderings run on the same inputs in the same process:
+Workload (default): the parameter-bound stack of four 8192 x 8192 fp32 linear
+layers, 64 tokens, Adam (linear4x8192), the largest single-GPU configuration
+at the paper's fp32 precision.  The 8-layer width-1024 MLP (mlp8x1024) is
+timed beside it and reported under extra keys.  A step is one training
+iteration over one resident batch.  All three orderings run on the same
+inputs in the same process:
   eager  forward, backward writing every gradient, one multi-tensor optimizer launch
   ff     forward-fusion (update applied while the next forward loads W)
   bf     backward-fusion (update in the weight-gradient epilogue, second stream)
@@ -15,8 +18,10 @@ time.
 The dominant kernel of the fused step is timed live with HIP events on the
 stream it runs on, during the timed steps, and set against its roofline
 (algorithmic bytes or flops per launch over MI355X peaks: HBM 8 TB/s, fp32
-MFMA 157.3 TFLOP/s).  The CPU baseline is the float64 oracle's eager step on
-this host, timed on a bounded sample of steps.
+MFMA 157.3 TFLOP/s).  The HBM rates this device reaches with the library's
+own streaming kernels (read only, and copy) are reported beside it
+(`hbm_ceiling`).  The CPU baseline is the float64 oracle's eager step on this
+host, timed on a bounded sample of steps.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
@@ -102,6 +107,8 @@ def layer_launches(cfg):
     layers = []                      # (name, kind, M, N, K, in_elems, out_elems, bias, act_prev, pool)
     if cfg["kind"] == "tblock":
         return tblock_launches(cfg)
+    if cfg["kind"] == "mbv2":
+        return mbv2_launches(cfg)
     if cfg["kind"] == "mlp":
         M, dims = cfg["batch"], cfg["dims"]
         for i in range(1, len(dims)):
@@ -190,6 +197,77 @@ def tblock_launches(cfg):
     return out
 
 
+def mbv2_launches(cfg):
+    """Per-launch costs of the MobileNetV2-like network.  1x1 convolutions are
+    linears over the pixel rows; a depthwise layer moves its input and output
+    once per pass (fwd: R x W y; dgrad: R dy (+ the saved ReLU output) W dx;
+    filter gradient: R dy, x, plus the slice partials) and does 2*9 flops per
+    output element and pass.  Residual adds and the average pool count as
+    `extra` bytes of the layer they follow (forward and backward)."""
+    h = n_state(cfg["opt"])
+
+    def upd(n):
+        return 4 * n * (2 + 2 * h)
+
+    B, H = cfg["batch"], cfg["image"]
+    out = []
+
+    def linear(name, M, N, K, act_prev, first=False, extra=0):
+        w, xb, yb, bb = 4 * N * K, 4 * M * K, 4 * M * N, 4 * N
+        f = 2 * M * N * K
+        out.append(dict(
+            name=name, kind="linear", M=M, N=N, K=K, nparams=N * K + N,
+            fwd=(f, xb + w + yb + bb),
+            fwd_ff=(f, xb + yb + w * 2 + upd(N * K) + bb * 2 + upd(N)),
+            dgrad=None if first else (f, yb + w + xb + (xb if act_prev else 0)),
+            wgrad=(f, yb + xb + w + bb),
+            wgrad_bf=(f, yb + xb + upd(N * K) + upd(N)),
+            extra=extra))
+
+    c, s = cfg["stem"], H
+    conv_in, conv_out = B * s * s * cfg["in_channels"], B * s * s * c
+    out.append(dict(
+        name="stem", kind="conv", M=B * s * s, N=c, K=9 * cfg["in_channels"],
+        nparams=9 * cfg["in_channels"] * c + c,
+        fwd=(2 * B * s * s * c * 9 * cfg["in_channels"], 4 * (conv_in + conv_out) + 4 * 9 * cfg["in_channels"] * c),
+        fwd_ff=(2 * B * s * s * c * 9 * cfg["in_channels"], 4 * (conv_in + conv_out)
+                + upd(9 * cfg["in_channels"] * c) + 4 * 9 * cfg["in_channels"] * c),
+        dgrad=None,
+        wgrad=(2 * B * s * s * c * 9 * cfg["in_channels"], 4 * (conv_in + conv_out)),
+        wgrad_bf=(2 * B * s * s * c * 9 * cfg["in_channels"], 4 * (conv_in + conv_out)
+                  + upd(9 * cfg["in_channels"] * c + c)),
+        extra=0))
+    k = 0
+    cin, s = cfg["stem"], H
+    for t, co, n, st in cfg["blocks"]:
+        for r in range(n):
+            k += 1
+            stride = st if r == 0 else 1
+            so = (s - 1) // stride + 1
+            hid = t * cin
+            p = f"blk{k}."
+            if t != 1:
+                linear(p + "expand", B * s * s, hid, cin, act_prev=k == 1)
+            nin, nout = B * s * s * hid, B * so * so * hid
+            dwf = 2 * 9 * nout
+            out.append(dict(
+                name=p + "dw", kind="dw", M=B * so * so, N=hid, K=9, nparams=10 * hid,
+                fwd=(dwf, 4 * (nin + nout) + 40 * hid),
+                fwd_ff=(dwf, 4 * (nin + nout) + 40 * hid + upd(10 * hid) + 40 * hid),
+                dgrad=(dwf, 4 * (nout + 2 * nin) + 40 * hid),
+                wgrad=(dwf, 4 * (nout + nin) + 40 * hid),
+                wgrad_bf=(dwf, 4 * (nout + nin) + upd(10 * hid)),
+                extra=0))
+            res = stride == 1 and cin == co
+            linear(p + "project", B * so * so, co, hid, act_prev=True,
+                   extra=(3 + 3) * 4 * B * so * so * co if res else 0)
+            cin, s = co, so
+    linear("head", B * s * s, cfg["head"], cin, act_prev=False,
+           extra=4 * (B * s * s * cfg["head"] + B * cfg["head"]) * 2)
+    linear("fc", B, cfg["classes"], cfg["head"], act_prev=False)
+    return out
+
+
 def step_cost(cfg, ordering):
     """Whole-step algorithmic flops and bytes (kernels as implemented)."""
     L = layer_launches(cfg)
@@ -211,6 +289,11 @@ def step_cost(cfg, ordering):
 
 
 def describe_layers(cfg):
+    if cfg["kind"] == "mbv2":
+        nb = sum(r[2] for r in cfg["blocks"])
+        return (f"MobileNetV2-like: stem conv3x3 {cfg['stem']}, {nb} inverted-residual blocks "
+                f"(1x1 expand, depthwise 3x3, 1x1 project), 1x1 head {cfg['head']}, avg-pool, "
+                f"linear classifier; {cfg['image']}x{cfg['image']} input")
     if cfg["kind"] == "tblock":
         return (f"{cfg['blocks']} pre-LN blocks, hidden {cfg['hidden']}, FFN {cfg['ffn']}, "
                 f"bf16 operands")
@@ -262,7 +345,8 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     prologue = ordering == "ffp"
     if prologue:
         ordering = "ff"
-    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge, conv_prologue=prologue)
+    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge, conv_prologue=prologue,
+                 linear_prologue=prologue)
     n = len(batches)
     for t in range(max(warmup, 1)):
         x, y = batches[t % n]
@@ -299,7 +383,8 @@ def median_step_ms(torch, cfg, ordering, batches, warmup, steps):
     merge = ordering == "bfm"
     prologue = ordering == "ffp"
     o = "bf" if merge else "ff" if prologue else ordering
-    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge, conv_prologue=prologue)
+    tr = Trainer(cfg, make_params(cfg), "cuda:0", merge_dgrad=merge, conv_prologue=prologue,
+                 linear_prologue=prologue)
     n = len(batches)
     for t in range(max(warmup, 1)):
         tr.step(*batches[t % n], o)
@@ -415,6 +500,57 @@ def depthwise_stack(torch, batch, steps, warmup):
             "forward_GBps": round(act_bytes / (res["forward"] * 1e-3) / 1e9, 1)}
 
 
+def hbm_ceiling(torch, nbytes=1 << 30, reps=20):
+    """Read and copy rates of the library's streaming kernels over `nbytes`
+    (copy: nbytes read and nbytes written), GB/s of bytes moved."""
+    from paper_2104_00237_amd import _lib as L
+    n = nbytes // 4
+    src = torch.ones(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    s = torch.cuda.current_stream()
+    out = {}
+    for name, mode, moved in (("read_GBps", L.OF_STREAM_READ, nbytes),
+                              ("copy_GBps", L.OF_STREAM_COPY, 2 * nbytes)):
+        for _ in range(3):
+            L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), n, 0, s.cuda_stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), n, 0, s.cuda_stream)
+        e1.record(s)
+        torch.cuda.synchronize()
+        out[name] = round(moved * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
+    out["bytes"] = nbytes
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
+def extra_workload(torch, name, steps, warmup):
+    """Eager, forward- and backward-fusion step times of another workload."""
+    cfg = get_config(name)
+    dev = torch.device("cuda:0")
+    batches = []
+    for t in range(1, 5):
+        x, y = make_batch(cfg, t)
+        batches.append((torch.as_tensor(x).to(dev), torch.as_tensor(y).to(dev)))
+    mergeable = cfg["kind"] == "mlp" and cfg["dtype"] == "f32" and cfg["batch"] <= 64
+    # forward-fusion in the weight-tile prologue with a second buffer set
+    # (fp32 layers of more than 64 rows)
+    prologue = cfg["dtype"] == "f32" and cfg["batch"] > 64
+    res = {}
+    for o in ("eager", "ff", "bf") + (("bfm",) if mergeable else ()) + (("ffp",) if prologue else ()):
+        ms, _, _, _ = time_ordering(torch, cfg, o, batches, warmup, steps, graph=False)
+        res[f"{o}_ms_per_step"] = round(ms, 4)
+        print(f"[bench] {name} {o}: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+    for o in ("ff", "bf") + (("bfm",) if mergeable else ()) + (("ffp",) if prologue else ()):
+        res[f"speedup_{o}_vs_eager"] = round(res["eager_ms_per_step"] / res[f"{o}_ms_per_step"], 4)
+    res["global_batch"] = cfg["batch"]
+    res["layers"] = describe_layers(cfg)
+    res["optimizer"] = cfg["opt"]["kind"]
+    return res
+
+
 def cpu_baseline(cfg, budget_s=15.0):
     """Oracle eager steps on this host, seconds per step of `cfg`.  The 12-block
     Transformer stack is sampled as one block (same width and tokens) and its
@@ -445,7 +581,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="mlp8x1024")
+    ap.add_argument("--workload", default="linear4x8192")
+    ap.add_argument("--extra-workloads", default="mlp8x1024",
+                    help="comma-separated workloads timed beside the main one (eager, ff, bf; "
+                         "'' for none)")
     ap.add_argument("--optimizer", choices=sorted(FIG7_OPTIMIZERS), default=None,
                     help="replace the workload's optimizer (Fig. 7's set)")
     ap.add_argument("--batch", type=int, default=None,
@@ -453,8 +592,11 @@ def main():
     ap.add_argument("--dims", default=None, metavar="WIDTHxDEPTH",
                     help="MLP workloads: DEPTH hidden layers of WIDTH (parameters per layer, "
                          "Fig. 6 sweep); the input and output widths follow WIDTH and the classes")
-    ap.add_argument("--conv-ff-prologue", action="store_true",
-                    help="vgg11: also time forward-fusion with the filter-tile prologue (ffp)")
+    ap.add_argument("--ff-prologue", "--conv-ff-prologue", dest="ff_prologue",
+                    action="store_true",
+                    help="also time forward-fusion with every update in its own forward's "
+                         "weight-tile prologue (ffp: convolutions and linear layers of more "
+                         "than 64 rows write a second buffer set)")
     ap.add_argument("--depthwise", action="store_true",
                     help="also time MobileNetV2's depthwise 3x3 layers (batch 32): eager "
                          "vs backward-fusion backward, and the forward's HBM rate")
@@ -492,7 +634,7 @@ def main():
         w, dpt = (int(v) for v in args.dims.lower().split("x"))
         out = cfg["classes"] if cfg["loss"] == "xent" else w
         cfg = dict(cfg, dims=[w] * (dpt + 1) + ([out] if cfg["loss"] == "xent" else []))
-    if cfg["kind"] not in ("mlp", "vgg", "tblock"):
+    if cfg["kind"] not in ("mlp", "vgg", "tblock", "mbv2"):
         print(f"workload {args.workload} has no GPU path in this build", file=sys.stderr)
         sys.exit(2)
     dev = torch.device("cuda:0")
@@ -506,7 +648,7 @@ def main():
     # the merged backward applies to fp32 linear chains of at most 64 rows
     mergeable = cfg["kind"] == "mlp" and cfg["dtype"] == "f32" and cfg["batch"] <= 64
     res = {}
-    extra = (("bfm",) if mergeable else ()) + (("ffp",) if args.conv_ff_prologue else ())
+    extra = (("bfm",) if mergeable else ()) + (("ffp",) if args.ff_prologue else ())
     for o in ("eager", "ff", "bf") + extra:
         ms, host_ms, _, _ = time_ordering(torch, cfg, o, batches, args.warmup, args.steps,
                                           graph=False)
@@ -655,6 +797,13 @@ def main():
                                          + (" (one of its blocks, time x blocks)"
                                             if cfg["kind"] == "tblock" else "")
                                          + f" (oracle, numpy, {cores} host threads)"}
+    ceil = hbm_ceiling(torch)
+    out["hbm_ceiling"] = ceil
+    if roof["bound"] == "hbm":
+        roof["frac_of_measured_copy_rate"] = round(roof["achieved"] / ceil["copy_GBps"], 4)
+    for name in [w for w in args.extra_workloads.split(",") if w and w != args.workload]:
+        out.setdefault("extra_workloads", {})[name] = extra_workload(torch, name, args.steps,
+                                                                     args.warmup)
     if args.depthwise:
         out["depthwise_mbv2"] = depthwise_stack(torch, 32, args.steps, args.warmup)
     print(json.dumps(out))

@@ -172,9 +172,11 @@ typedef struct of_linear_desc {
 
 typedef struct of_conv_desc {
   int64_t N, H, W, C;  /* input batch, height, width, channels (NHWC) */
-  int64_t Cout;        /* output channels; filter is [Cout,3,3,C], stride 1, zero pad 1 */
+  int64_t Cout;        /* output channels; filter is [Cout,3,3,C], zero pad 1 */
   int32_t act;         /* of_act applied in the forward epilogue (NONE or RELU) */
   int32_t has_bias;
+  int32_t stride;      /* 0 or 1: stride 1; 2: stride 2 (depthwise only), output
+                          [N, (H-1)/2+1, (W-1)/2+1, C] */
 } of_conv_desc;
 
 /* Which call a workspace query is for. */
@@ -216,21 +218,30 @@ of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param*
                         void* stream);
 
 /*
- * Forward-fusion forward (Section 3 "Forward-Fusion"; Appendix B.1, Alg. 2):
- * the optimizer of W (and b) runs on the pending gradients gW [N,K] (gb [N])
- * with `opt`, writes back W, m, v (and w_bf16), and Y = act(X W'^T + b') is
- * computed from the updated values.  Each element is updated exactly once.
- * The update is applied while the W tiles are loaded for the contraction when
- * M fits one row tile of the forward (fp32 operands, M <= 64); for larger M,
- * and for bf16 operands, the same update runs as a separate pass just before
- * the contraction, with identical results.
+ * Forward-fusion forward (Section 3 "Forward-Fusion"; Appendix B.1, Alg. 2;
+ * the purple frame of Fig. 2): the optimizer of W (and b) runs on the pending
+ * gradients gW [N,K] (gb [N]) with `opt` while the W tiles are loaded for the
+ * contraction, and Y = act(X W'^T + b') is computed from the updated values
+ * W', b'.  Each element's update is written exactly once:
+ *   W_out == NULL: in place into W (and b).  Needs the M rows in one row tile
+ *     of the contraction (M <= 64), so each W element has one reader;
+ *     otherwise OF_EUNSUPPORTED.
+ *   W_out != NULL: into the second buffer set W_out (and b_out; both sets of
+ *     the same sizes and optimizer, no buffer shared).  Any M: every row tile
+ *     computes the update of its W tile in registers from W (the set is only
+ *     read), and the first row tile stores it to W_out, which the caller makes
+ *     the current set afterwards (the two sets alternate step by step).
+ * fp32 operands only (dtype OF_F32; OF_EUNSUPPORTED otherwise: with bf16
+ * operands every row tile would read the fp32 weight, gradient and history,
+ * 16 B per element, where the contraction reads the 2-byte shadow).
  * opt == NULL means nothing is pending (the first iteration): identical to
- * of_linear_fwd.  b/gb: both NULL when !has_bias.  Workspace: OF_LINEAR_FWD.
+ * of_linear_fwd, and W_out, b_out are ignored.  b/gb (and b_out): NULL when
+ * !has_bias.  Workspace: OF_LINEAR_FWD.
  */
 of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_param* W,
-                              const float* gW, const of_param* b, const float* gb,
-                              const of_opt* opt, float* z, float* y, void* ws,
-                              size_t ws_bytes, void* stream);
+                              const of_param* W_out, const float* gW, const of_param* b,
+                              const of_param* b_out, const float* gb, const of_opt* opt,
+                              float* z, float* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * of_linear_fwd whose launch also applies a later operator's pending update
@@ -387,10 +398,15 @@ of_status of_conv_wgrad_fused(const of_conv_desc* d, const float* dy, const floa
 /* ------------------------------------------- depthwise 3x3 convolutions */
 /*
  * The small-parameter layers where the paper sees its largest gains
- * (Section 5, speedup against parameters per layer; MobileNetV2 in Fig. 3 and
- * Table 2): one 3x3 filter per channel (channel multiplier 1), stride 1, zero
- * padding 1.  Descriptor: of_conv_desc with Cout == C.  x, y, dy, dx, prev are
- * [N,H,W,C] NHWC; the filter W is [3,3,C] (tap-major, channels contiguous);
+ * (Appendix C, "Various Models and Optimizers", Fig. 6: speedup against
+ * parameters per layer; MobileNetV2 in Fig. 3 and Table 2): one 3x3 filter
+ * per channel (channel multiplier 1), zero padding 1, stride 1 or 2
+ * (d->stride).  Descriptor: of_conv_desc with Cout == C.  x, dx, prev are the
+ * input [N,H,W,C] NHWC; y, dy the output [N,Ho,Wo,C] with Ho = (H-1)/S + 1,
+ * Wo = (W-1)/S + 1 for stride S (H, W at stride 1); so
+ *   y[n,ho,wo,c] = b[c] + sum over ky, kx < 3 of
+ *                  x[n, S ho + ky - 1, S wo + kx - 1, c] W[ky,kx,c]
+ * (out-of-range input pixels are zero).  The filter W is [3,3,C] (tap-major, channels contiguous);
  * the bias is [C].  act is OF_ACT_NONE or OF_ACT_RELU.  All pointers are
  * device memory owned by the caller.  Errors: OF_EINVAL for NULL or
  * inconsistent arguments (Cout != C), OF_EUNSUPPORTED for tensors of 2^31
@@ -430,6 +446,11 @@ of_status of_dwconv_wgrad_fused(const of_conv_desc* d, const float* dy, const fl
                                 size_t ws_bytes, void* stream);
 
 /*
+ * Support operators.  The paper defines none of the calls below (max-pool,
+ * losses, LayerNorm, row sums, add): they complete the synthetic workloads'
+ * forward and backward passes around the fused layers, and follow the usual
+ * definitions stated with each.
+ *
  * 2x2 max-pool, stride 2 (H, W even): y [N,H/2,W/2,C]; argmax [N,H/2,W/2,C]
  * holds the window position 0..3 of the first maximum in row-major window
  * order (ties keep the earlier position).
@@ -444,6 +465,18 @@ of_status of_maxpool2x2_fwd(const float* x, int64_t N, int64_t H, int64_t W, int
  */
 of_status of_maxpool2x2_bwd(const float* dy, const uint8_t* argmax, const float* mask_src,
                             int64_t N, int64_t H, int64_t W, int64_t C, float* dx, void* stream);
+
+/*
+ * Global average pool (MobileNetV2's head; a support operator): x [N, P, C]
+ * (an NHWC map with P = H*W positions), y [N, C]:
+ *   y[n,c] = (sum over p = 0 .. P-1, in order, of x[n,p,c]) / P.
+ * Backward: dx[n,p,c] = dy[n,c] / P, set to 0 where mask_src (the pool input,
+ * a ReLU output, [N, P, C]; may be NULL) is not > 0.  Errors: OF_EINVAL,
+ * OF_EUNSUPPORTED (N*P*C >= 2^40), OF_EALIGN, before any launch.
+ */
+of_status of_avgpool_fwd(const float* x, int64_t N, int64_t P, int64_t C, float* y, void* stream);
+of_status of_avgpool_bwd(const float* dy, const float* mask_src, int64_t N, int64_t P, int64_t C,
+                         float* dx, void* stream);
 
 /* ------------------------------------------------ elementwise optimizer */
 
@@ -508,7 +541,8 @@ of_status of_step_advance(int64_t* step_dev, int64_t delta, void* stream);
 /* ------------------------------------------------------------- losses */
 
 /*
- * Softmax cross-entropy, forward and backward in one launch:
+ * Softmax cross-entropy, forward and backward in one launch (a support
+ * operator, not defined by the paper):
  *   loss = mean_b (logsumexp(z_b) - z_{b,label_b});  dz = (softmax(z) - onehot)/B.
  * logits: [B, C] row stride ld (0 means C); labels: int64 [B] in [0, C)
  * (out-of-range labels give loss NaN); loss: one fp32 on the device; dlogits:
@@ -521,7 +555,8 @@ of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B,
 
 /*
  * LayerNorm over the last dimension (the normalisation of the Transformer
- * blocks the paper trains, Appendix C): biased variance over D, eps inside
+ * blocks the paper trains, Appendix C; a support operator whose formula the
+ * paper does not give): biased variance over D, eps inside
  * the square root,
  *   y = (x - mean) / sqrt(var + eps) * gamma + beta.
  * x, y: [M, D] contiguous fp32; gamma, beta: [D]; mean, rstd: [M] outputs
@@ -561,7 +596,8 @@ of_status of_reduce_rows(const float* src, int64_t rows, int64_t ld, int64_t n, 
 of_status of_add(const float* a, const float* b, int64_t n, float* out, void* stream);
 
 /*
- * Mean squared error, forward and backward:
+ * Mean squared error, forward and backward (a support operator, not defined
+ * by the paper):
  *   loss = mean over all M*D elements of (y - t)^2;  dy = 2 (y - t) / (M*D).
  * y: [M, ld], t: [M, D] contiguous, dy: [M, ld]; loss: one fp32 on the device.
  * ws: at least of_mse_workspace_size(M, D) bytes.
@@ -569,6 +605,22 @@ of_status of_add(const float* a, const float* b, int64_t n, float* out, void* st
 size_t of_mse_workspace_size(int64_t M, int64_t D);
 of_status of_mse_fwd_bwd(const float* y, const float* t, int64_t M, int64_t D, int64_t ld,
                          float* loss, float* dy, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------- measurement */
+
+/*
+ * HBM streaming probe (not part of the paper's method): the read rate
+ * (OF_STREAM_READ: src is read, dst receives at most one float) or the copy
+ * rate (OF_STREAM_COPY: dst = src) this device reaches with coalesced 128-bit
+ * non-temporal accesses, the achievable ceiling beside the published peak for
+ * the kernels that stream parameters and optimizer state.  src, dst: n floats
+ * of device memory, 16-byte aligned (dst: 4-byte aligned for a read), n a
+ * positive multiple of 4; blocks: workgroups of 256 threads (0: 2048).
+ * Errors: OF_EINVAL, OF_EALIGN before any launch.
+ */
+enum { OF_STREAM_READ = 0, OF_STREAM_COPY = 1 };
+of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
+                        void* stream);
 
 #ifdef __cplusplus
 }

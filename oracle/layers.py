@@ -17,7 +17,9 @@ Definitions (the readings where the paper is silent):
   gelu        y = z * Phi(z) (exact erf form); dz = dy (Phi(z) + z phi(z))
   layernorm   over the last axis, biased variance, eps inside the sqrt
   conv3x3     cross-correlation, stride 1, zero padding 1, NHWC / [Cout,3,3,Cin]
-  dwconv3x3   the same per channel (depthwise, multiplier 1), filter [3,3,C]
+  dwconv3x3   the same per channel (depthwise, multiplier 1), filter [3,3,C],
+              stride 1 or 2
+  avgpool     mean over the spatial positions of each channel
   maxpool2x2  stride 2; the argmax is the first maximum of the window in
               row-major order (strict >), reported as its window position 0..3
   bf16        matmul operands rounded to bfloat16 just before the product
@@ -207,50 +209,95 @@ class Conv3x3(Op):
 
 
 class DepthwiseConv3x3(Op):
-    """Depthwise 3x3 cross-correlation (one filter per channel), stride 1, zero pad 1,
-    NHWC input, [3,3,C] filter: y[n,h,w,c] = b[c] + sum over taps of
-    x[n,h+ky-1,w+kx-1,c] w[ky,kx,c].  The small-parameter layers of MobileNetV2,
-    the network of the paper's Fig. 3 and Table 2."""
+    """Depthwise 3x3 cross-correlation (one filter per channel), zero pad 1,
+    stride 1 or 2, NHWC input, [3,3,C] filter:
+    y[n,ho,wo,c] = b[c] + sum over taps of x[n, S ho + ky - 1, S wo + kx - 1, c] w[ky,kx,c],
+    output [N, (H-1)//S + 1, (W-1)//S + 1, C].  The small-parameter layers of
+    MobileNetV2, the network of the paper's Fig. 3 and Table 2."""
 
-    def __init__(self, w, b=None):
+    def __init__(self, w, b=None, stride=1):
         super().__init__()
-        self.w, self.b = w, b
+        self.w, self.b, self.stride = w, b, stride
         self.params = (w,) if b is None else (w, b)
 
-    def forward(self, x):
-        n, h, wd, _ = x.shape
-        xp = np.pad(x, ((0, 0), (1, 1), (1, 1), (0, 0)))
-        w = self.w.value
-        y = np.zeros(x.shape)
+    def _taps(self, xp, ho, wo):
+        """The padded input seen by each tap: xp[:, S ho + r, S wo + s, :] for r, s < 3."""
+        S = self.stride
         for r in range(3):
             for s in range(3):
-                y += xp[:, r:r + h, s:s + wd, :] * w[r, s, :]
+                yield r, s, (slice(None), slice(r, r + S * (ho - 1) + 1, S),
+                             slice(s, s + S * (wo - 1) + 1, S), slice(None))
+
+    def _out_hw(self, x):
+        return (x.shape[1] - 1) // self.stride + 1, (x.shape[2] - 1) // self.stride + 1
+
+    def forward(self, x):
+        ho, wo = self._out_hw(x)
+        xp = np.pad(x, ((0, 0), (1, 1), (1, 1), (0, 0)))
+        w = self.w.value
+        y = np.zeros((x.shape[0], ho, wo, x.shape[3]))
+        for r, s, sl in self._taps(xp, ho, wo):
+            y += xp[sl] * w[r, s, :]
         if self.b is not None:
             y += self.b.value
         return y, xp
 
     def abs_bound(self, x):
         """sum over taps of |x||w| + |b|: the scale of the rounding error of y."""
-        n, h, wd, _ = x.shape
+        ho, wo = self._out_hw(x)
         xp = np.pad(np.abs(x), ((0, 0), (1, 1), (1, 1), (0, 0)))
         w = np.abs(self.w.value)
-        s = np.zeros(x.shape)
-        for r in range(3):
-            for c in range(3):
-                s += xp[:, r:r + h, c:c + wd, :] * w[r, c, :]
-        return s + np.abs(self.b.value) if self.b is not None else s
+        out = np.zeros((x.shape[0], ho, wo, x.shape[3]))
+        for r, c, sl in self._taps(xp, ho, wo):
+            out += xp[sl] * w[r, c, :]
+        return out + np.abs(self.b.value) if self.b is not None else out
 
     def backward(self, xp, dy):
-        n, h, wd, _ = dy.shape
+        ho, wo = dy.shape[1], dy.shape[2]
         w = self.w.value
         dxp = np.zeros_like(xp)
         dw = np.zeros_like(w)
-        for r in range(3):
-            for s in range(3):
-                dxp[:, r:r + h, s:s + wd, :] += dy * w[r, s, :]
-                dw[r, s, :] = (dy * xp[:, r:r + h, s:s + wd, :]).sum(axis=(0, 1, 2))
+        for r, s, sl in self._taps(xp, ho, wo):
+            dxp[sl] += dy * w[r, s, :]
+            dw[r, s, :] = (dy * xp[sl]).sum(axis=(0, 1, 2))
         grads = (dw,) if self.b is None else (dw, dy.sum(axis=(0, 1, 2)))
         return (dxp[:, 1:-1, 1:-1, :],), grads
+
+
+class GlobalAvgPool(Op):
+    """Mean over the spatial positions: [N,H,W,C] -> [N,C] (MobileNetV2's head)."""
+
+    def forward(self, x):
+        return x.mean(axis=(1, 2)), x.shape
+
+    def backward(self, shape, dy):
+        n, h, w, c = shape
+        return (np.broadcast_to(dy[:, None, None, :] / (h * w), shape).copy(),), ()
+
+
+class PixelRows(Op):
+    """[N,H,W,C] feature map -> [N*H*W, C] rows: a 1x1 convolution is a linear
+    layer over the pixels."""
+
+    def forward(self, x):
+        return x.reshape(-1, x.shape[-1]), x.shape
+
+    def backward(self, shape, dy):
+        return (dy.reshape(shape),), ()
+
+
+class PixelMap(Op):
+    """[N*H*W, C] rows -> [N,H,W,C] (the spatial shape of the map `like`)."""
+
+    def __init__(self, n, h, w):
+        super().__init__()
+        self.shape = (n, h, w)
+
+    def forward(self, x):
+        return x.reshape(self.shape + (x.shape[-1],)), x.shape
+
+    def backward(self, shape, dy):
+        return (dy.reshape(shape),), ()
 
 
 class MaxPool2x2(Op):

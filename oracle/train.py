@@ -49,7 +49,7 @@ import itertools
 
 import numpy as np
 
-from workloads import make_params, make_batch, make_eval_batch, mlp_ties
+from workloads import make_params, make_batch, make_eval_batch, mlp_ties, mbv2_blocks
 from . import layers as L
 from .losses import LOSSES
 from .optim import apply as apply_optimizer, clip_scale
@@ -300,6 +300,37 @@ def new_model(cfg, init=None, seed=0):
                 cur = f"p{i}"
         nodes.append((L.Flatten(), [cur], "flat"))
         nodes.append((L.Linear(P("fc.weight"), P("fc.bias")), ["flat"], "output"))
+    elif kind == "mbv2":
+        n = cfg["batch"]
+
+        def pointwise(prefix, src, h, tag):
+            """A 1x1 convolution: a linear over the pixel rows of an [n,h,h,c] map."""
+            nodes.extend([(L.PixelRows(), [src], tag + "r"),
+                          (L.Linear(P(prefix + ".weight"), P(prefix + ".bias")), [tag + "r"], tag + "z"),
+                          (L.PixelMap(n, h, h), [tag + "z"], tag + "m")])
+            return tag + "m"
+
+        nodes.append((L.Conv3x3(P("stem.weight"), P("stem.bias")), ["input"], "s"))
+        nodes.append((L.ReLU(), ["s"], "sa"))
+        cur = "sa"
+        for b in mbv2_blocks(cfg):
+            p = b["name"]
+            x_in = cur
+            if b["t"] != 1:
+                z = pointwise(p + "expand", cur, b["h_in"], p + "e")
+                nodes.append((L.ReLU(), [z], p + "ea"))
+                cur = p + "ea"
+            nodes.append((L.DepthwiseConv3x3(P(p + "dw.weight"), P(p + "dw.bias"), b["stride"]),
+                          [cur], p + "d"))
+            nodes.append((L.ReLU(), [p + "d"], p + "da"))
+            cur = pointwise(p + "project", p + "da", b["h_out"], p + "p")
+            if b["residual"]:
+                nodes.append((L.Add(), [x_in, cur], p + "y"))
+                cur = p + "y"
+        z = pointwise("head", cur, mbv2_blocks(cfg)[-1]["h_out"], "h")
+        nodes.append((L.ReLU(), [z], "ha"))
+        nodes.append((L.GlobalAvgPool(), ["ha"], "pool"))
+        nodes.append((L.Linear(P("fc.weight"), P("fc.bias")), ["pool"], "output"))
     else:
         raise ValueError(kind)
     return Model(nodes, params, cfg["loss"], cfg["opt"])

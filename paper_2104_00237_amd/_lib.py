@@ -50,6 +50,7 @@ class OfCarry(ctypes.Structure):
 
 
 OF_CLIP_WS_BYTES = 2048
+OF_STREAM_READ, OF_STREAM_COPY = 0, 1
 
 
 class OfGradRef(ctypes.Structure):
@@ -63,7 +64,8 @@ class OfLinearDesc(ctypes.Structure):
 
 class OfConvDesc(ctypes.Structure):
     _fields_ = [("N", c_int64), ("H", c_int64), ("W", c_int64), ("C", c_int64),
-                ("Cout", c_int64), ("act", c_int32), ("has_bias", c_int32)]
+                ("Cout", c_int64), ("act", c_int32), ("has_bias", c_int32),
+                ("stride", c_int32)]   # 0 or 1: stride 1; 2: depthwise stride 2
 
 
 class OpfuseError(RuntimeError):
@@ -81,9 +83,9 @@ _SIGS = {
                                 c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_linear_fwd_carry": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_void_p,
                                       c_void_p, P(OfCarry), c_void_p, c_size_t, c_void_p]),
-    "of_linear_fwd_fused": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p,
-                                      P(OfParam), c_void_p, P(OfOpt), c_void_p, c_void_p,
-                                      c_void_p, c_size_t, c_void_p]),
+    "of_linear_fwd_fused": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), P(OfParam),
+                                      c_void_p, P(OfParam), P(OfParam), c_void_p, P(OfOpt),
+                                      c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_linear_bwd_data": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_int32,
                                      c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_linear_bwd_weight": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, c_void_p, c_void_p,
@@ -95,6 +97,7 @@ _SIGS = {
     "of_linear_bwd_merged": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, P(OfParam),
                                        P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
                                        c_int32, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_hbm_stream": (c_int32, [c_int32, c_void_p, c_void_p, c_int64, c_int32, c_void_p]),
     "of_elementwise_fused_update": (c_int32, [P(OfParam), c_void_p, c_int64, c_int64,
                                               P(OfOpt), c_void_p]),
     "of_optimizer_step": (c_int32, [c_int32, P(OfParam), P(c_void_p), P(OfOpt), c_void_p]),
@@ -125,6 +128,9 @@ _SIGS = {
     "of_dwconv_wgrad_fused": (c_int32, [P(OfConvDesc), c_void_p, c_void_p, P(OfParam),
                                         P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
                                         c_size_t, c_void_p]),
+    "of_avgpool_fwd": (c_int32, [c_void_p, c_int64, c_int64, c_int64, c_void_p, c_void_p]),
+    "of_avgpool_bwd": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_int64, c_void_p,
+                                 c_void_p]),
     "of_maxpool2x2_fwd": (c_int32, [c_void_p, c_int64, c_int64, c_int64, c_int64, c_void_p,
                                     c_void_p, c_void_p]),
     "of_maxpool2x2_bwd": (c_int32, [c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64,
@@ -206,10 +212,12 @@ def of_layernorm_partial_rows(M):
 
 
 for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
-           "of_linear_bwd_fused", "of_linear_bwd_merged", "of_elementwise_fused_update", "of_optimizer_step",
+           "of_linear_bwd_fused", "of_linear_bwd_merged",
+           "of_hbm_stream", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_fwd_fused", "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
-           "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_layernorm_fwd", "of_layernorm_bwd",
+           "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_avgpool_fwd", "of_avgpool_bwd",
+           "of_layernorm_fwd", "of_layernorm_bwd",
            "of_reduce_rows", "of_add", "of_dwconv_fwd", "of_dwconv_bwd_data",
            "of_dwconv_bwd_weight", "of_dwconv_wgrad_fused"):
     globals()[_n] = _wrap(_n)

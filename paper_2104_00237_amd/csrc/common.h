@@ -302,6 +302,8 @@ struct MergedLaunch {
   int M, N, K;
 };
 constexpr int kMergedMaxM = 64;
+hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, int blocks,
+                             hipStream_t stream);
 size_t merged_workspace_bytes(int M, int N, int K);
 hipError_t merged_bwd_launch(const MergedLaunch& L, hipStream_t stream);
 
@@ -330,6 +332,10 @@ hipError_t launch_maxpool_fwd(const float* x, int64_t N, int64_t H, int64_t W, i
 hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, const float* mask_src,
                               int64_t N, int64_t H, int64_t W, int64_t C, float* dx,
                               hipStream_t s);
+hipError_t launch_avgpool_fwd(const float* x, int64_t N, int64_t P, int64_t C, float* y,
+                              hipStream_t s);
+hipError_t launch_avgpool_bwd(const float* dy, const float* mask_src, int64_t N, int64_t P,
+                              int64_t C, float* dx, hipStream_t s);
 int64_t ln_partial_rows(int64_t M);
 hipError_t launch_ln_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
                          const float* beta, float eps, float* y, float* mean, float* rstd,

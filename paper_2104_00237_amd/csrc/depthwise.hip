@@ -1,4 +1,4 @@
-// Depthwise 3x3 convolution (one filter per channel, stride 1, zero pad 1),
+// Depthwise 3x3 convolution (one filter per channel, stride 1 or 2, zero pad 1),
 // NHWC activations, filter [3,3,C] (tap-major, channels contiguous), bias [C].
 // These layers have few parameters and little arithmetic per byte, so every
 // kernel here is bound by HBM traffic, not by the matrix cores: consecutive
@@ -7,15 +7,17 @@
 //
 // Filter gradient: dW[ky,kx,c] = sum over (n,h,w) of dy[n,h,w,c] *
 // x[n,h+ky-1,w+kx-1,c], db[c] = sum of dy[n,h,w,c].  Pass 1 splits the pixels
-// over S slices; each workgroup (64 channels x 4 pixel streams, or 16 channel
-// quads x 16 pixel streams when C % 4 == 0 and the tensors are 16-byte
-// aligned) writes the ten per-channel sums of its slice.  Pass 2 adds the S
+// over S slices; each workgroup (64 channels, one per thread group, or 16
+// channel quads when C % 4 == 0 and the tensors are 16-byte aligned) writes
+// the ten per-channel sums of its slice, each the in-order sum of 16 pixel
+// streams that both kernels partition and order alike.  Pass 2 adds the S
 // slices in slice order and either writes dW / db (eager) or applies the
 // optimizer to W, b and their history right there (backward-fusion: the
-// filter gradient is never stored).  A shape always takes the same pass-1
-// kernel, so both passes are deterministic, and the fused pass applies the
-// same per-element update as the eager optimizer kernel: the two give the
-// same bits.
+// filter gradient is never stored).  Both passes are deterministic: the two
+// pass-1 kernels take the same operations in the same order for every
+// element, so the bits do not depend on which one runs (that is, on the
+// pointers' alignment), and the fused pass applies the same per-element
+// update as the eager optimizer kernel, so eager and fused give the same bits.
 
 #include <algorithm>
 
@@ -26,10 +28,14 @@ namespace opfuse {
 constexpr int DW_CB = 64;     // channels per workgroup in pass 1
 constexpr int DW_TAPS = 10;   // nine filter taps + the bias sum
 
+// Input [N,H,W,C]; output [N,Ho,Wo,C] with Ho = (H - 1) / S + 1 for the
+// stride S (1 or 2, zero padding 1), a template parameter of the kernels.
 struct DwShape {
   int N, H, W, C;
+  int Ho, Wo;
 };
 
+template <int S>
 __global__ __launch_bounds__(256) void dw_fwd_kernel(const float* __restrict__ x,
                                                      const float* __restrict__ w,
                                                      const float* __restrict__ b,
@@ -38,15 +44,15 @@ __global__ __launch_bounds__(256) void dw_fwd_kernel(const float* __restrict__ x
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= total) return;
   const int c = i % s.C, p = i / s.C;
-  const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+  const int col = p % s.Wo, t = p / s.Wo, row = t % s.Ho, n = t / s.Ho;
   float acc = 0.f;
 #pragma unroll
   for (int ky = 0; ky < 3; ++ky) {
-    const int hh = row + ky - 1;
+    const int hh = row * S + ky - 1;
     if (hh < 0 || hh >= s.H) continue;
 #pragma unroll
     for (int kx = 0; kx < 3; ++kx) {
-      const int ww = col + kx - 1;
+      const int ww = col * S + kx - 1;
       if (ww < 0 || ww >= s.W) continue;
       acc = __fmaf_rn(x[((n * s.H + hh) * s.W + ww) * s.C + c], w[(ky * 3 + kx) * s.C + c], acc);
     }
@@ -55,8 +61,10 @@ __global__ __launch_bounds__(256) void dw_fwd_kernel(const float* __restrict__ x
   y[i] = act_fwd(act, z);
 }
 
-// dx[n,h,w,c] = sum over taps of dy[n,h-ky+1,w-kx+1,c] * W[ky,kx,c], times the
-// previous layer's activation derivative (ReLU: its saved output > 0).
+// dx[n,h,w,c] = sum over the taps (ky, kx) with h + 1 - ky = S ho and
+// w + 1 - kx = S wo (0 <= ho < Ho, 0 <= wo < Wo) of dy[n,ho,wo,c] * W[ky,kx,c],
+// times the previous layer's activation derivative (ReLU: its saved output > 0).
+template <int S>
 __global__ __launch_bounds__(256) void dw_dgrad_kernel(const float* __restrict__ dy,
                                                        const float* __restrict__ w,
                                                        const float* __restrict__ prev,
@@ -69,56 +77,81 @@ __global__ __launch_bounds__(256) void dw_dgrad_kernel(const float* __restrict__
   float acc = 0.f;
 #pragma unroll
   for (int ky = 0; ky < 3; ++ky) {
-    const int hh = row - ky + 1;
-    if (hh < 0 || hh >= s.H) continue;
+    const int th = row - ky + 1;
+    if (th < 0 || th % S) continue;
+    const int hh = th / S;
+    if (hh >= s.Ho) continue;
 #pragma unroll
     for (int kx = 0; kx < 3; ++kx) {
-      const int ww = col - kx + 1;
-      if (ww < 0 || ww >= s.W) continue;
-      acc = __fmaf_rn(dy[((n * s.H + hh) * s.W + ww) * s.C + c], w[(ky * 3 + kx) * s.C + c], acc);
+      const int tw = col - kx + 1;
+      if (tw < 0 || tw % S) continue;
+      const int ww = tw / S;
+      if (ww >= s.Wo) continue;
+      acc = __fmaf_rn(dy[((n * s.Ho + hh) * s.Wo + ww) * s.C + c], w[(ky * 3 + kx) * s.C + c], acc);
     }
   }
   dx[i] = act_prev == OF_ACT_NONE ? acc : __fmul_rn(acc, act_grad(act_prev, prev[i]));
 }
 
 // Pass 1: workgroup (cb, slice) sums its slice's pixels for 64 channels.
+// Each channel's pixels are split into 16 streams (stream u takes the slice's
+// pixels u, u + 16, u + 32, ... in order) whose sums are then added in stream
+// order: the same partition and order as the four-channel kernel below, so a
+// shape gives the same bits whichever of the two runs.  Thread (channel,
+// sub) keeps the streams sub, sub + 4, sub + 8 and sub + 12.
+template <int S>
+__device__ __forceinline__ void dw_wgrad_pixel(const float* __restrict__ dy,
+                                               const float* __restrict__ x, const DwShape& s,
+                                               int p, int c, float (&acc)[DW_TAPS]) {
+  const int col = p % s.Wo, t = p / s.Wo, row = t % s.Ho, n = t / s.Ho;
+  const float g = dy[p * s.C + c];
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    const int hh = row * S + ky - 1;
+    const bool rin = hh >= 0 && hh < s.H;
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int ww = col * S + kx - 1;
+      if (rin && ww >= 0 && ww < s.W)
+        acc[ky * 3 + kx] = __fmaf_rn(g, x[((n * s.H + hh) * s.W + ww) * s.C + c], acc[ky * 3 + kx]);
+    }
+  }
+  acc[9] = __fadd_rn(acc[9], g);
+}
+
+template <int S>
 __global__ __launch_bounds__(256) void dw_wgrad_partial_kernel(const float* __restrict__ dy,
                                                                const float* __restrict__ x,
                                                                float* __restrict__ part,
                                                                DwShape s, int per_slice) {
-  __shared__ float red[4][DW_TAPS][DW_CB];
+  __shared__ float red[16][DW_TAPS][DW_CB];
   const int cl = threadIdx.x & (DW_CB - 1), sub = threadIdx.x >> 6;
   const int c = blockIdx.x * DW_CB + cl;
-  const int P = s.N * s.H * s.W;
+  const int P = s.N * s.Ho * s.Wo;  // output pixels
   const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
-  float acc[DW_TAPS];
+  float acc[4][DW_TAPS];
 #pragma unroll
-  for (int k = 0; k < DW_TAPS; ++k) acc[k] = 0.f;
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int k = 0; k < DW_TAPS; ++k) acc[j][k] = 0.f;
   if (c < s.C) {
-    for (int p = p0 + sub; p < p1; p += 4) {
-      const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
-      const float g = dy[p * s.C + c];
-#pragma unroll
-      for (int ky = 0; ky < 3; ++ky) {
-        const int hh = row + ky - 1;
-        const bool rin = hh >= 0 && hh < s.H;
-#pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          const int ww = col + kx - 1;
-          if (rin && ww >= 0 && ww < s.W)
-            acc[ky * 3 + kx] = __fmaf_rn(g, x[((n * s.H + hh) * s.W + ww) * s.C + c], acc[ky * 3 + kx]);
-        }
-      }
-      acc[9] = __fadd_rn(acc[9], g);
+    for (int p = p0 + sub; p < p1; p += 16) {
+      dw_wgrad_pixel<S>(dy, x, s, p, c, acc[0]);
+      if (p + 4 < p1) dw_wgrad_pixel<S>(dy, x, s, p + 4, c, acc[1]);
+      if (p + 8 < p1) dw_wgrad_pixel<S>(dy, x, s, p + 8, c, acc[2]);
+      if (p + 12 < p1) dw_wgrad_pixel<S>(dy, x, s, p + 12, c, acc[3]);
     }
   }
 #pragma unroll
-  for (int k = 0; k < DW_TAPS; ++k) red[sub][k][cl] = acc[k];
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int k = 0; k < DW_TAPS; ++k) red[sub + 4 * j][k][cl] = acc[j][k];
   __syncthreads();
   for (int j = threadIdx.x; j < DW_TAPS * DW_CB; j += 256) {
     const int k = j / DW_CB, l = j % DW_CB, cc = blockIdx.x * DW_CB + l;
-    const float v = __fadd_rn(__fadd_rn(__fadd_rn(red[0][k][l], red[1][k][l]), red[2][k][l]),
-                              red[3][k][l]);
+    float v = red[0][k][l];
+#pragma unroll
+    for (int u = 1; u < 16; ++u) v = __fadd_rn(v, red[u][k][l]);
     if (cc < s.C) part[((int64_t)blockIdx.y * DW_TAPS + k) * s.C + cc] = v;
   }
 }
@@ -131,6 +164,7 @@ __device__ __forceinline__ float4 fma4(float4 a, float4 b, float4 c) {
                      __fmaf_rn(a.w, b.w, c.w));
 }
 
+template <int S>
 __global__ __launch_bounds__(256) void dw_fwd4_kernel(const float* __restrict__ x,
                                                       const float* __restrict__ w,
                                                       const float* __restrict__ b,
@@ -140,15 +174,15 @@ __global__ __launch_bounds__(256) void dw_fwd4_kernel(const float* __restrict__ 
   if (i >= quads) return;
   const int Cq = s.C >> 2;
   const int c = (i % Cq) * 4, p = i / Cq;
-  const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+  const int col = p % s.Wo, t = p / s.Wo, row = t % s.Ho, n = t / s.Ho;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int ky = 0; ky < 3; ++ky) {
-    const int hh = row + ky - 1;
+    const int hh = row * S + ky - 1;
     if (hh < 0 || hh >= s.H) continue;
 #pragma unroll
     for (int kx = 0; kx < 3; ++kx) {
-      const int ww = col + kx - 1;
+      const int ww = col * S + kx - 1;
       if (ww < 0 || ww >= s.W) continue;
       acc = fma4(ld4(x + ((n * s.H + hh) * s.W + ww) * s.C + c), ld4(w + (ky * 3 + kx) * s.C + c), acc);
     }
@@ -162,6 +196,7 @@ __global__ __launch_bounds__(256) void dw_fwd4_kernel(const float* __restrict__ 
                                       act_fwd(act, acc.w)));
 }
 
+template <int S>
 __global__ __launch_bounds__(256) void dw_dgrad4_kernel(const float* __restrict__ dy,
                                                         const float* __restrict__ w,
                                                         const float* __restrict__ prev,
@@ -175,13 +210,17 @@ __global__ __launch_bounds__(256) void dw_dgrad4_kernel(const float* __restrict_
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int ky = 0; ky < 3; ++ky) {
-    const int hh = row - ky + 1;
-    if (hh < 0 || hh >= s.H) continue;
+    const int th = row - ky + 1;
+    if (th < 0 || th % S) continue;
+    const int hh = th / S;
+    if (hh >= s.Ho) continue;
 #pragma unroll
     for (int kx = 0; kx < 3; ++kx) {
-      const int ww = col - kx + 1;
-      if (ww < 0 || ww >= s.W) continue;
-      acc = fma4(ld4(dy + ((n * s.H + hh) * s.W + ww) * s.C + c), ld4(w + (ky * 3 + kx) * s.C + c), acc);
+      const int tw = col - kx + 1;
+      if (tw < 0 || tw % S) continue;
+      const int ww = tw / S;
+      if (ww >= s.Wo) continue;
+      acc = fma4(ld4(dy + ((n * s.Ho + hh) * s.Wo + ww) * s.C + c), ld4(w + (ky * 3 + kx) * s.C + c), acc);
     }
   }
   if (act_prev != OF_ACT_NONE) {
@@ -194,6 +233,7 @@ __global__ __launch_bounds__(256) void dw_dgrad4_kernel(const float* __restrict_
 
 // Pass 1, four channels per thread: 16 channel quads (64 channels) x 16 pixel
 // streams per workgroup.
+template <int S>
 __global__ __launch_bounds__(256) void dw_wgrad_partial4_kernel(const float* __restrict__ dy,
                                                                 const float* __restrict__ x,
                                                                 float* __restrict__ part,
@@ -201,22 +241,22 @@ __global__ __launch_bounds__(256) void dw_wgrad_partial4_kernel(const float* __r
   __shared__ float red[16][DW_TAPS][DW_CB];
   const int q = threadIdx.x & 15, sub = threadIdx.x >> 4;
   const int c = blockIdx.x * DW_CB + q * 4;
-  const int P = s.N * s.H * s.W;
+  const int P = s.N * s.Ho * s.Wo;  // output pixels
   const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
   float4 acc[DW_TAPS];
 #pragma unroll
   for (int k = 0; k < DW_TAPS; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
   if (c < s.C) {
     for (int p = p0 + sub; p < p1; p += 16) {
-      const int col = p % s.W, t = p / s.W, row = t % s.H, n = t / s.H;
+      const int col = p % s.Wo, t = p / s.Wo, row = t % s.Ho, n = t / s.Ho;
       const float4 g = ld4(dy + p * s.C + c);
 #pragma unroll
       for (int ky = 0; ky < 3; ++ky) {
-        const int hh = row + ky - 1;
+        const int hh = row * S + ky - 1;
         const bool rin = hh >= 0 && hh < s.H;
 #pragma unroll
         for (int kx = 0; kx < 3; ++kx) {
-          const int ww = col + kx - 1;
+          const int ww = col * S + kx - 1;
           if (rin && ww >= 0 && ww < s.W)
             acc[ky * 3 + kx] = fma4(g, ld4(x + ((n * s.H + hh) * s.W + ww) * s.C + c), acc[ky * 3 + kx]);
         }
@@ -287,14 +327,20 @@ __global__ __launch_bounds__(256) void dw_wgrad_reduce_kernel(DwReduce r, OptK o
 }
 
 namespace {
+int dw_stride(const of_conv_desc& d) { return d.stride > 1 ? (int)d.stride : 1; }
+int64_t dw_out(int64_t n, int S) { return (n - 1) / S + 1; }
+int64_t dw_out_pixels(const of_conv_desc& d) {
+  return d.N * dw_out(d.H, dw_stride(d)) * dw_out(d.W, dw_stride(d));
+}
 int dw_slices(const of_conv_desc& d) {
-  const int64_t P = d.N * d.H * d.W;
+  const int64_t P = dw_out_pixels(d);
   const int64_t cb = (d.C + DW_CB - 1) / DW_CB;
   const int64_t want = std::max<int64_t>(1, 1024 / cb);
   return (int)std::max<int64_t>(1, std::min<int64_t>((P + 255) / 256, want));
 }
 DwShape dw_shape(const of_conv_desc& d) {
-  return DwShape{(int)d.N, (int)d.H, (int)d.W, (int)d.C};
+  const int S = dw_stride(d);
+  return DwShape{(int)d.N, (int)d.H, (int)d.W, (int)d.C, (int)dw_out(d.H, S), (int)dw_out(d.W, S)};
 }
 }  // namespace
 
@@ -304,29 +350,45 @@ size_t dw_workspace_bytes(const of_conv_desc& d) {
 
 hipError_t launch_dw_fwd(const of_conv_desc& d, const float* x, const float* w, const float* b,
                          float* y, hipStream_t stream) {
-  const int total = (int)(d.N * d.H * d.W * d.C);
+  const int total = (int)(dw_out_pixels(d) * d.C);   // one thread per output element
   if (d.C % 4 == 0 && aligned16(x) && aligned16(w) && aligned16(b) && aligned16(y)) {
     const int quads = total / 4;
-    hipLaunchKernelGGL(dw_fwd4_kernel, dim3((quads + 255) / 256), dim3(256), 0, stream, x, w,
-                       d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, quads);
+    if (dw_stride(d) == 2)
+      hipLaunchKernelGGL(dw_fwd4_kernel<2>, dim3((quads + 255) / 256), dim3(256), 0, stream, x, w,
+                         d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, quads);
+    else
+      hipLaunchKernelGGL(dw_fwd4_kernel<1>, dim3((quads + 255) / 256), dim3(256), 0, stream, x, w,
+                         d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, quads);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(dw_fwd_kernel, dim3((total + 255) / 256), dim3(256), 0, stream, x, w,
-                     d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, total);
+  if (dw_stride(d) == 2)
+    hipLaunchKernelGGL(dw_fwd_kernel<2>, dim3((total + 255) / 256), dim3(256), 0, stream, x, w,
+                       d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, total);
+  else
+    hipLaunchKernelGGL(dw_fwd_kernel<1>, dim3((total + 255) / 256), dim3(256), 0, stream, x, w,
+                       d.has_bias ? b : nullptr, y, dw_shape(d), (int)d.act, total);
   return hipGetLastError();
 }
 
 hipError_t launch_dw_dgrad(const of_conv_desc& d, const float* dy, const float* w,
                            const float* prev, int act_prev, float* dx, hipStream_t stream) {
-  const int total = (int)(d.N * d.H * d.W * d.C);
+  const int total = (int)(d.N * d.H * d.W * d.C);    // one thread per input element
   if (d.C % 4 == 0 && aligned16(dy) && aligned16(w) && aligned16(prev) && aligned16(dx)) {
     const int quads = total / 4;
-    hipLaunchKernelGGL(dw_dgrad4_kernel, dim3((quads + 255) / 256), dim3(256), 0, stream, dy, w,
-                       prev, act_prev, dx, dw_shape(d), quads);
+    if (dw_stride(d) == 2)
+      hipLaunchKernelGGL(dw_dgrad4_kernel<2>, dim3((quads + 255) / 256), dim3(256), 0, stream, dy,
+                         w, prev, act_prev, dx, dw_shape(d), quads);
+    else
+      hipLaunchKernelGGL(dw_dgrad4_kernel<1>, dim3((quads + 255) / 256), dim3(256), 0, stream, dy,
+                         w, prev, act_prev, dx, dw_shape(d), quads);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(dw_dgrad_kernel, dim3((total + 255) / 256), dim3(256), 0, stream, dy, w,
-                     prev, act_prev, dx, dw_shape(d), total);
+  if (dw_stride(d) == 2)
+    hipLaunchKernelGGL(dw_dgrad_kernel<2>, dim3((total + 255) / 256), dim3(256), 0, stream, dy, w,
+                       prev, act_prev, dx, dw_shape(d), total);
+  else
+    hipLaunchKernelGGL(dw_dgrad_kernel<1>, dim3((total + 255) / 256), dim3(256), 0, stream, dy, w,
+                       prev, act_prev, dx, dw_shape(d), total);
   return hipGetLastError();
 }
 
@@ -334,22 +396,32 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
                            float* db, int accumulate, const of_param* W, const of_param* b,
                            const float* gW, const float* gb, const OptK* o, void* ws,
                            hipStream_t stream) {
-  const int S = dw_slices(d);
-  const int64_t P = d.N * d.H * d.W;
-  const int per = (int)((P + S - 1) / S);
+  const int nsl = dw_slices(d);   // pixel slices of pass 1
+  const int64_t P = dw_out_pixels(d);
+  const int per = (int)((P + nsl - 1) / nsl);
   const int cb = (int)((d.C + DW_CB - 1) / DW_CB);
   float* part = static_cast<float*>(ws);
-  if (d.C % 4 == 0 && aligned16(dy) && aligned16(x))
-    hipLaunchKernelGGL(dw_wgrad_partial4_kernel, dim3(cb, S), dim3(256), 0, stream, dy, x, part,
-                       dw_shape(d), per);
-  else
-    hipLaunchKernelGGL(dw_wgrad_partial_kernel, dim3(cb, S), dim3(256), 0, stream, dy, x, part,
-                       dw_shape(d), per);
+  const bool two = dw_stride(d) == 2;
+  if (d.C % 4 == 0 && aligned16(dy) && aligned16(x)) {
+    if (two)
+      hipLaunchKernelGGL(dw_wgrad_partial4_kernel<2>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
+                         part, dw_shape(d), per);
+    else
+      hipLaunchKernelGGL(dw_wgrad_partial4_kernel<1>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
+                         part, dw_shape(d), per);
+  } else {
+    if (two)
+      hipLaunchKernelGGL(dw_wgrad_partial_kernel<2>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
+                         part, dw_shape(d), per);
+    else
+      hipLaunchKernelGGL(dw_wgrad_partial_kernel<1>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
+                         part, dw_shape(d), per);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   DwReduce r{};
   r.part = part;
-  r.S = S;
+  r.S = nsl;
   r.C = (int)d.C;
   r.dw = dw;
   r.db = db;

@@ -773,16 +773,18 @@ static GemmCfg make_cfg(int t, int P, int Q, int R, int64_t target_ctas, int max
   return GemmCfg{t, S, r_split};
 }
 
-static int ff_tile(int P) {
-  return P <= 32 ? TI_32x32 : P <= 64 ? TI_64x32 : P <= 128 ? TI_128x64 : TI_256x32;
-}
+static int ff_tile(int P) { return P <= 32 ? TI_32x32 : TI_64x32; }
 
 static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
   // The forward and the fused forward of at most 64 rows share one tiling (the
   // same tile, splits and split length), so their results are bit-identical;
   // about 1024 workgroups (measured on MI355X at 64 x 8192 x 8192: fused
-  // forward 416 us with 4 splits, 435 us with 2).
-  if (kind == EPI_FWD_FF) return make_cfg(ff_tile(P), P, Q, R, 1024, 8);
+  // forward 416 us with 4 splits, 435 us with 2).  One row tile covers the M
+  // rows, so the update can be written in place.  A fused forward of more
+  // rows writes its update to a second buffer set (every row tile computes it,
+  // row tile 0 stores it) and takes the plain forward's tiling.
+  if (kind == EPI_FWD_FF)
+    return P <= 64 ? make_cfg(ff_tile(P), P, Q, R, 1024, 8) : select_cfg_default(EPI_FWD, P, Q, R);
   if (kind == EPI_FWD && P <= 64) return make_cfg(ff_tile(P), P, Q, R, 1024, 8);
   if (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) {
     if (R <= 128 && ntiles(TI_128x128, P, Q) >= 1024) return make_cfg(TI_128x128, P, Q, R, 1, 1);
@@ -922,7 +924,7 @@ static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const Epi
     case TI_64x64: return launch_t<T64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_128x64: return launch_t<T128x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_128x128:
-      // Never chosen for a forward with M <= 64, the only forward-fusion case.
+      // gemm_launch gives a fused forward 128x64 instead (LDS for the bias row).
       if constexpr (EPI == EPI_FWD_FF) return hipErrorInvalidValue;
       else return launch_t<T128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_256x32: return launch_t<T256x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
@@ -1005,8 +1007,8 @@ hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, vo
                        hipStream_t stream) {
   GemmCfg c = select_cfg(kind, pr.P, pr.Q, pr.R, pr.conv);
   // The 128x128 tile leaves no LDS for forward-fusion's bias row; a fused
-  // convolution forward given it takes 128x64 with the same splits (the same
-  // reduction ranges and workspace).
+  // forward given it takes 128x64 with the same splits (the same reduction
+  // ranges and workspace).
   if (kind == EPI_FWD_FF && c.tile == TI_128x128) c.tile = TI_128x64;
   EpiArgs ea = ea_in;
   ea.carry.z0 = 0;

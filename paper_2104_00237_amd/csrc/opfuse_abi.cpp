@@ -126,6 +126,21 @@ of_status check_linear(const of_linear_desc* d) {
           "act %d is not an of_act", (int)d->act);
   REQUIRE(d->dtype == OF_F32 || d->dtype == OF_BF16, OF_EINVAL, "dtype %d is not an of_dtype",
           (int)d->dtype);
+  // Operand tiles are read through buffer descriptors based at the tile's
+  // first element, with 32-bit byte offsets against a 2^31-1-byte range.  An
+  // offset never exceeds the size of the operand matrix it reads from, so every
+  // operand (X [M, ldx], W [N, K], Y / Z / dZ [M, ldy], float32 in memory) must
+  // stay below 2 GiB; larger shapes would read zeros or wrapped data.
+  const int64_t lx = d->ldx ? d->ldx : d->K, ly = d->ldy ? d->ldy : d->N;
+  constexpr int64_t kMaxOperandBytes = (1LL << 31) - 16;
+  constexpr int64_t kMaxElems = kMaxOperandBytes / 4;
+  // (written as divisions: M, N, K < 2^31 but ldx and ldy are unbounded so far)
+  REQUIRE(lx <= kMaxElems / d->M && d->K <= kMaxElems / d->N && ly <= kMaxElems / d->M,
+          OF_EUNSUPPORTED,
+          "operand too large: X [%lld x %lld], W [%lld x %lld] and Y [%lld x %lld] must each be "
+          "< 2 GiB (32-bit buffer offsets)",
+          (long long)d->M, (long long)lx, (long long)d->N, (long long)d->K, (long long)d->M,
+          (long long)ly);
   return OF_OK;
 }
 
@@ -258,6 +273,8 @@ of_status check_conv(const of_conv_desc* d) {
           "activation tensors must be < 2 GiB");
   REQUIRE(d->act == OF_ACT_NONE || d->act == OF_ACT_RELU, OF_EUNSUPPORTED,
           "convolutions support OF_ACT_NONE and OF_ACT_RELU");
+  REQUIRE(d->stride == 0 || d->stride == 1, OF_EUNSUPPORTED,
+          "3x3 convolutions run with stride 1 (got stride %d)", (int)d->stride);
   return OF_OK;
 }
 
@@ -375,13 +392,14 @@ of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_
   return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream, next ? &carry : nullptr);
 }
 
-// Largest M whose forward-fusion applies the update in the W-tile prologue.
+// Largest M whose forward-fusion can write its update in place: the M rows
+// fit one row tile, so each W element has one reader.
 constexpr int64_t kFusedForwardMaxRows = 64;
 
 of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_param* W,
-                              const float* gW, const of_param* b, const float* gb,
-                              const of_opt* opt, float* z, float* y, void* ws, size_t ws_bytes,
-                              void* stream) {
+                              const of_param* W_out, const float* gW, const of_param* b,
+                              const of_param* b_out, const float* gb, const of_opt* opt,
+                              float* z, float* y, void* ws, size_t ws_bytes, void* stream) {
   if (opt == nullptr) return of_linear_fwd(d, x, W, b ? b->w : nullptr, z, y, ws, ws_bytes, stream);
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
@@ -395,31 +413,48 @@ of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_
   REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z");
   REQUIRE(al4(x) && al4(gW) && al4(gb) && al4(z) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
   if ((st = check_shadow(d, W)) != OF_OK) return st;
-  if ((st = check_ws(d, EPI_FWD_FF, ws, ws_bytes)) != OF_OK) return st;
-  const hipStream_t s = (hipStream_t)stream;
-  const OptK ok = make_optk(*opt);
-  if (d->M > kFusedForwardMaxRows || d->dtype == OF_BF16) {
-    // One row tile per W element needs M rows per workgroup; beyond
-    // kFusedForwardMaxRows that tiling only fills the GPU with a reduction
-    // split whose partials and second pass cost more than a separate update
-    // pass (measured on MI355X), and bf16 operands have no update prologue:
-    // the identical update runs as one pass right before the contraction.
-    of_param ps[2] = {*W, d->has_bias ? *b : of_param{}};
-    const float* gs[2] = {gW, gb};
-    hipError_t e = launch_multi_update(d->has_bias ? 2 : 1, ps, gs, ok, s);
-    if (e != hipSuccess) return hip_status(e, "forward-fusion update");
-    return run_fwd(d, x, W, d->has_bias ? b->w : nullptr, z, y, ws, s);
+  REQUIRE(d->dtype == OF_F32, OF_EUNSUPPORTED,
+          "of_linear_fwd_fused takes fp32 operands: with bf16 operands every row tile would "
+          "read the fp32 weight, gradient and history (16 B per element) in place of the 2-byte "
+          "shadow; apply the pending update with of_linear_fwd_carry or "
+          "of_elementwise_fused_update instead");
+  if (W_out) {
+    // every row tile reads the current set while row tile 0 writes the new one
+    if ((st = check_param(W_out, "W_out", d->N * d->K, *opt, true)) != OF_OK) return st;
+    REQUIRE(W_out->w != W->w && (W->m == nullptr || W_out->m != W->m) &&
+                (W->v == nullptr || W_out->v != W->v),
+            OF_EINVAL, "W_out must not share buffers with W");
+    REQUIRE(!d->has_bias || b_out, OF_EINVAL, "W_out is set and has_bias: b_out is required");
+    if (d->has_bias) {
+      if ((st = check_param(b_out, "b_out", d->N, *opt, true)) != OF_OK) return st;
+      REQUIRE(b_out->w != b->w && (b->m == nullptr || b_out->m != b->m) &&
+                  (b->v == nullptr || b_out->v != b->v),
+              OF_EINVAL, "b_out must not share buffers with b");
+    }
+  } else {
+    REQUIRE(d->M <= kFusedForwardMaxRows, OF_EUNSUPPORTED,
+            "in-place forward-fusion needs the M rows in one row tile (M <= %lld, got %lld): "
+            "pass W_out (and b_out) to have the update written to a second buffer set",
+            (long long)kFusedForwardMaxRows, (long long)d->M);
+    REQUIRE(b_out == nullptr, OF_EINVAL, "b_out without W_out");
   }
+  if ((st = check_ws(d, EPI_FWD_FF, ws, ws_bytes)) != OF_OK) return st;
   GemmProblem pr{x, ldx_of(d), 1, W->w, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
   EpiArgs ea = empty_epi();
   ea.out = y; ea.ldo = ldy_of(d);
   ea.z = z; ea.ldz = ldy_of(d);
   ea.act = d->act;
   ea.W = *W;
+  if (W_out) ea.Wout = *W_out;
   ea.gW = gW;
-  if (d->has_bias) { ea.b = *b; ea.gb = gb; }
-  ea.opt = ok;
-  return hip_status(gemm_launch(EPI_FWD_FF, pr, ea, ws, s), "of_linear_fwd_fused launch");
+  if (d->has_bias) {
+    ea.b = *b;
+    ea.gb = gb;
+    if (W_out) ea.bout = *b_out;
+  }
+  ea.opt = make_optk(*opt);
+  return hip_status(gemm_launch(EPI_FWD_FF, pr, ea, ws, (hipStream_t)stream),
+                    "of_linear_fwd_fused launch");
 }
 
 of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_param* W,
@@ -503,11 +538,13 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
                     "of_linear_bwd_fused launch");
 }
 
-of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const float* x,
-                               const of_param* W, const of_param* b, const float* gW_partial,
-                               const float* gb_partial, const of_opt* opt, const float* prev,
-                               int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
-                               void* stream) {
+namespace {
+// of_linear_bwd_merged: validation, then the launch.
+of_status merged_entry(const of_linear_desc* d, const float* dz, const float* x,
+                       const of_param* W, const of_param* b, const float* gW_partial,
+                       const float* gb_partial, const of_opt* opt, const float* prev,
+                       int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
+                       void* stream) {
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
   if ((st = check_merged(d)) != OF_OK) return st;
@@ -521,6 +558,7 @@ of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const f
           OF_EALIGN, "fp32 pointers must be 4-byte aligned");
   if ((st = check_shadow(d, W)) != OF_OK) return st;
   const size_t need = merged_workspace_bytes((int)d->M, (int)d->N, (int)d->K);
+  float* part = static_cast<float*>(ws);
   if (dx_prev) {
     if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
     REQUIRE(ws_bytes >= need, OF_EWORKSPACE,
@@ -537,9 +575,33 @@ of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const f
   L.opt = make_optk(*opt);
   L.prev = prev; L.act_prev = act_prev;
   L.dx = dx_prev;
-  L.part = (float*)ws;
+  L.part = part;
   L.M = (int)d->M; L.N = (int)d->N; L.K = (int)d->K;
   return hip_status(merged_bwd_launch(L, (hipStream_t)stream), "of_linear_bwd_merged launch");
+}
+}  // namespace
+
+of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const float* x,
+                               const of_param* W, const of_param* b, const float* gW_partial,
+                               const float* gb_partial, const of_opt* opt, const float* prev,
+                               int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
+                               void* stream) {
+  return merged_entry(d, dz, x, W, b, gW_partial, gb_partial, opt, prev, act_prev, dx_prev, ws,
+                      ws_bytes, stream);
+}
+
+of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
+                        void* stream) {
+  REQUIRE(mode == OF_STREAM_READ || mode == OF_STREAM_COPY, OF_EINVAL,
+          "mode %d is neither OF_STREAM_READ nor OF_STREAM_COPY", (int)mode);
+  REQUIRE(src && dst, OF_EINVAL, "src and dst are required");
+  REQUIRE(n >= 4 && n % 4 == 0, OF_EINVAL, "n must be a positive multiple of 4 (got %lld)",
+          (long long)n);
+  REQUIRE(blocks >= 0 && blocks <= 65535, OF_EINVAL, "blocks must be in [0, 65535]");
+  REQUIRE(aligned16(src) && (mode == OF_STREAM_READ ? al4(dst) : aligned16(dst)), OF_EALIGN,
+          "src (and dst when copying) must be 16-byte aligned");
+  return hip_status(hbm_stream_launch(mode, src, dst, n, blocks, (hipStream_t)stream),
+                    "of_hbm_stream launch");
 }
 
 size_t of_conv_workspace_size(const of_conv_desc* d, int32_t op) {
@@ -686,6 +748,8 @@ of_status check_dw(const of_conv_desc* d) {
           "activation tensors must have < 2^31 elements");
   REQUIRE(d->act == OF_ACT_NONE || d->act == OF_ACT_RELU, OF_EUNSUPPORTED,
           "depthwise convolutions support OF_ACT_NONE and OF_ACT_RELU");
+  REQUIRE(d->stride >= 0 && d->stride <= 2, OF_EUNSUPPORTED,
+          "depthwise convolutions run with stride 1 or 2 (got %d)", (int)d->stride);
   return OF_OK;
 }
 
@@ -781,6 +845,24 @@ of_status of_maxpool2x2_bwd(const float* dy, const uint8_t* argmax, const float*
   REQUIRE(al4(dy) && al4(dx) && al4(mask_src), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
   return hip_status(launch_maxpool_bwd(dy, argmax, mask_src, N, H, W, C, dx, (hipStream_t)stream),
                     "of_maxpool2x2_bwd launch");
+}
+
+of_status of_avgpool_fwd(const float* x, int64_t N, int64_t P, int64_t C, float* y, void* stream) {
+  REQUIRE(x && y, OF_EINVAL, "x and y are required");
+  REQUIRE(N >= 1 && P >= 1 && C >= 1, OF_EINVAL, "N, P and C must be >= 1");
+  REQUIRE(N <= (1LL << 40) / P / C, OF_EUNSUPPORTED, "N * P * C must be < 2^40");
+  REQUIRE(al4(x) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_avgpool_fwd(x, N, P, C, y, (hipStream_t)stream), "of_avgpool_fwd launch");
+}
+
+of_status of_avgpool_bwd(const float* dy, const float* mask_src, int64_t N, int64_t P, int64_t C,
+                         float* dx, void* stream) {
+  REQUIRE(dy && dx, OF_EINVAL, "dy and dx are required");
+  REQUIRE(N >= 1 && P >= 1 && C >= 1, OF_EINVAL, "N, P and C must be >= 1");
+  REQUIRE(N <= (1LL << 40) / P / C, OF_EUNSUPPORTED, "N * P * C must be < 2^40");
+  REQUIRE(al4(dy) && al4(dx) && al4(mask_src), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  return hip_status(launch_avgpool_bwd(dy, mask_src, N, P, C, dx, (hipStream_t)stream),
+                    "of_avgpool_bwd launch");
 }
 
 of_status of_elementwise_fused_update(const of_param* p, const float* g, int64_t g_rows,

@@ -1,0 +1,79 @@
+// HBM streaming probes: the read and read+write rates this device achieves
+// with plain coalesced 128-bit accesses.  They give the achievable ceiling
+// that the parameter-bound kernels (the fused and merged updates, which
+// stream W and the optimizer state once) are measured against, beside the
+// published 8 TB/s.  Not part of the paper's method.
+//
+// Each thread moves UNROLL float4s per pass, all loads issued before any use,
+// so a workgroup of 256 threads has UNROLL * 4 KiB in flight; the grid strides
+// over the buffer.  Loads and stores are non-temporal: the data is touched
+// once and should not displace anything in the caches.
+
+#include "common.h"
+
+namespace opfuse {
+
+namespace {
+
+constexpr int kStreamUnroll = 8;
+typedef float v4f __attribute__((ext_vector_type(4)));  // a native vector: non-temporal builtins take it
+
+template <int U>
+__global__ __launch_bounds__(256) void stream_read_kernel(const v4f* __restrict__ src,
+                                                          int64_t n4, float* __restrict__ sink) {
+  const int64_t stride = (int64_t)gridDim.x * 256 * U;
+  float acc = 0.f;
+  int64_t i = (int64_t)blockIdx.x * 256 * U + threadIdx.x;
+  for (; i + (U - 1) * 256 < n4; i += stride) {
+    v4f v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(src + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+  }
+  for (int u = 0; u < U; ++u) {
+    const int64_t j = i + u * 256;
+    if (j < n4) {
+      const v4f t = src[j];
+      acc += (t.x + t.y) + (t.z + t.w);
+    }
+  }
+  // The sum is stored only if it equals a value it practically never takes;
+  // the branch keeps the loads live without a store per thread.
+  if (acc == 1.2345678e-30f) sink[0] = acc;
+}
+
+template <int U>
+__global__ __launch_bounds__(256) void stream_copy_kernel(const v4f* __restrict__ src,
+                                                          v4f* __restrict__ dst, int64_t n4) {
+  const int64_t stride = (int64_t)gridDim.x * 256 * U;
+  int64_t i = (int64_t)blockIdx.x * 256 * U + threadIdx.x;
+  for (; i + (U - 1) * 256 < n4; i += stride) {
+    v4f v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(src + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < U; ++u) __builtin_nontemporal_store(v[u], dst + i + u * 256);
+  }
+  for (int u = 0; u < U; ++u) {
+    const int64_t j = i + u * 256;
+    if (j < n4) dst[j] = src[j];
+  }
+}
+
+}  // namespace
+
+hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, int blocks,
+                             hipStream_t stream) {
+  const int64_t n4 = n / 4;
+  if (blocks <= 0) blocks = 2048;  // 8 workgroups per compute unit
+  if (mode == 0)
+    hipLaunchKernelGGL(stream_read_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
+                       reinterpret_cast<const v4f*>(src), n4, dst);
+  else
+    hipLaunchKernelGGL(stream_copy_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
+                       reinterpret_cast<const v4f*>(src), reinterpret_cast<v4f*>(dst), n4);
+  return hipGetLastError();
+}
+
+}  // namespace opfuse

@@ -170,7 +170,8 @@ class LinearOp:
         # Forward-fusion: an fp32 layer with M <= 64 rows applies its pending
         # update while its own W tiles load (one row tile covers M); any other
         # layer has it carried by the previous operator's forward launch.
-        self.prologue_ff = dtype == L.OF_F32 and M <= 64
+        self.fp32 = dtype == L.OF_F32
+        self.prologue_ff = self.fp32 and M <= 64
         # Backward-fusion overlaps the fused update with the next data gradient
         # on a second stream when the update is heavy enough (>= 4M parameters or
         # >= 4 GFLOP) to repay the event pair that orders it; a lighter update runs
@@ -197,11 +198,23 @@ class LinearOp:
             L.of_linear_fwd_carry(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z,
                                   y, carry, *tr.ws_main_args(), tr._s())
 
+    def two_sets(self):
+        """Whether this operator's prologue alternates two parameter buffer sets."""
+        return self.prologue_ff and self.M > 64
+
     def fwd_ff(self, tr, x, y, z=None):
+        """Forward-fusion in the W-tile prologue: in place when the M rows fit one
+        row tile, else into the second buffer set, which then becomes current."""
         b = self.b
-        L.of_linear_fwd_fused(self.desc, x, self.W.p, self.W.g.data_ptr(),
-                              b.p if b else None, b.g.data_ptr() if b else None, tr.opt, z, y,
+        two_sets = self.M > 64
+        L.of_linear_fwd_fused(self.desc, x, self.W.p, self.W.alt_param() if two_sets else None,
+                              self.W.g.data_ptr(), b.p if b else None,
+                              b.alt_param() if (b and two_sets) else None,
+                              b.g.data_ptr() if b else None, tr.opt, z, y,
                               *tr.ws_main_args(), tr._s())
+        if two_sets:
+            for p in self.params:
+                p.swap_generation()
 
     def dgrad(self, tr, g, prev, act_prev, dx):
         L.of_linear_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
@@ -272,6 +285,10 @@ class ConvOp:
     prologue_ff = False
     overlap_update = True  # a convolution's fused wgrad + update is heavy: second stream
 
+    def two_sets(self):
+        """The filter-tile prologue always alternates two buffer sets."""
+        return self.prologue_ff
+
     def fwd(self, tr, x, y, carry=None):
         if carry is None:
             L.of_conv_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, y,
@@ -308,6 +325,50 @@ class ConvOp:
                               *tr.ws_side_args(), stream)
 
 
+class DwOp:
+    """f = act(dwconv3x3(X, W, stride) + b) on an NHWC [N, H, W, C] input: one 3x3
+    filter per channel (MobileNetV2's depthwise layers)."""
+
+    kind = "dw"
+    prologue_ff = False      # its update is carried by the previous launch
+    overlap_update = False   # a few thousand parameters: updated in stream order
+
+    def __init__(self, name, W, b, N, H, Wd, C, stride, act):
+        self.name, self.W, self.b = name, W, b
+        self.act = act
+        self.desc = L.OfConvDesc(N, H, Wd, C, C, L.ACTS[act], int(b is not None), stride)
+        self.updated = True
+        self.params = [W] if b is None else [W, b]
+        Ho, Wo = (H - 1) // stride + 1, (Wd - 1) // stride + 1
+        self.out_shape = (N, Ho, Wo, C)
+        self.M, self.N, self.K = N * Ho * Wo, C, 9
+
+    def two_sets(self):
+        return False
+
+    def ws(self, which):
+        return L.of_dwconv_workspace_size(self.desc) if which == L.OF_LINEAR_BWD_WEIGHT else 0
+
+    def fwd(self, tr, x, y):
+        L.of_dwconv_fwd(self.desc, x, self.W.w.data_ptr(), _ptr(self.b.w) if self.b else None, y,
+                        tr._s())
+
+    def dgrad(self, tr, g, prev, act_prev, dx):
+        L.of_dwconv_bwd_data(self.desc, g, self.W.w.data_ptr(), prev, act_prev, dx, tr._s())
+
+    def wgrad(self, tr, g, x, accumulate=0):
+        L.of_dwconv_bwd_weight(self.desc, g, x, self.W.g.data_ptr(),
+                               self.b.g.data_ptr() if self.b else None, accumulate,
+                               *tr.ws_main_args(), tr._s())
+
+    def wgrad_fused(self, tr, g, x, stream, partial=False):
+        b = self.b
+        L.of_dwconv_wgrad_fused(self.desc, g, x, self.W.p, b.p if b else None,
+                                self.W.g.data_ptr() if partial else None,
+                                (b.g.data_ptr() if (b and partial) else None), tr.opt,
+                                *tr.ws_main_args(), stream)
+
+
 class LayerNormOp:
     """f = LayerNorm(X) * gamma + beta over the last dimension of [M, D]."""
 
@@ -329,6 +390,9 @@ class LayerNormOp:
 
     prologue_ff = False   # gamma and beta are carried by the previous launch, or updated first
 
+    def two_sets(self):
+        return False
+
     def bwd(self, tr, dy, x, mu, rs, dres, dx):
         """dx (+ dres) and the parameter-gradient row partials."""
         L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx,
@@ -344,7 +408,7 @@ class LayerNormOp:
 def _ff_prologue(tr, op):
     """Whether forward-fusion applies op's pending update in its forward's W-tile
     loads (else a previous launch carries it, or a pass of its own runs)."""
-    return op.prologue_ff and not (op.kind == "conv" and tr.capturing)
+    return op.prologue_ff and not (op.two_sets() and tr.capturing)
 
 
 def _side_after_main(tr):
@@ -359,6 +423,8 @@ def _side_after_main(tr):
 class ChainNet:
     """Linear / conv layers in a chain, each with its activation and an
     optional 2x2 max-pool after it (the MLP and VGG workloads)."""
+
+    side_updates = False   # only layers with overlap_update use the side stream
 
     def __init__(self, tr, cfg, pb):
         self.tr = tr
@@ -725,15 +791,265 @@ class TBlockNet:
         return {}
 
 
+class MBNet:
+    """MobileNetV2-like network (the mbv2 workload): a 3x3 stem convolution, then
+    inverted-residual blocks
+
+        e = ReLU(x W_e^T + b_e)        1x1 expand: a linear over the N*H*W pixel rows
+        d = ReLU(dwconv3x3(e, s) + b)  depthwise, stride s
+        p = d W_p^T + b_p              1x1 project
+        y = x + p                      when s == 1 and the widths match, else y = p
+
+    then a 1x1 head convolution with ReLU, the global average pool and a linear
+    classifier.  Every activation and gradient has its own buffer, so nothing a
+    later kernel reads is overwritten within a step.  Forward-fusion carries each
+    operator's pending update in the previous operator's linear or convolution
+    launch (a depthwise launch carries nothing, so the launch before it also
+    carries the next linear's update); backward-fusion applies each operator's
+    update right after its gradient, in stream order.
+    """
+
+    side_updates = False
+
+    def __init__(self, tr, cfg, pb):
+        self.tr = tr
+        N, H = cfg["batch"], cfg["image"]
+        f32 = dict(dtype=torch.float32, device=tr.device)
+        self.N = N
+        self.stem = ConvOp("stem", pb("stem.weight"), pb("stem.bias"), N, H, H, "relu")
+        self.ops = [self.stem]
+        self.stem_y = torch.empty(self.stem.out_shape, **f32)
+        self.stem_g = torch.empty(self.stem.out_shape, **f32)   # grad of the stem's pre-activation
+        self.blocks = []
+        cin, h, k = cfg["stem"], H, 0
+        for t, c, n, s in cfg["blocks"]:
+            for r in range(n):
+                k += 1
+                stride = s if r == 0 else 1
+                ho = (h - 1) // stride + 1
+                p = f"blk{k}."
+                hid = t * cin
+                blk = dict(t=t, cin=cin, cout=c, hid=hid, h=h, ho=ho,
+                           residual=stride == 1 and cin == c)
+                if t != 1:
+                    blk["expand"] = LinearOp(p + "expand", pb(p + "expand.weight"),
+                                             pb(p + "expand.bias"), N * h * h, "relu")
+                    blk["e"] = torch.empty((N * h * h, hid), **f32)
+                    blk["ge"] = torch.empty((N * h * h, hid), **f32)
+                    self.ops.append(blk["expand"])
+                blk["dw"] = DwOp(p + "dw", pb(p + "dw.weight"), pb(p + "dw.bias"), N, h, h, hid,
+                                 stride, "relu")
+                blk["project"] = LinearOp(p + "project", pb(p + "project.weight"),
+                                          pb(p + "project.bias"), N * ho * ho, "none")
+                self.ops += [blk["dw"], blk["project"]]
+                blk["d"] = torch.empty((N, ho, ho, hid), **f32)
+                blk["gd"] = torch.empty((N, ho, ho, hid), **f32)
+                blk["p"] = torch.empty((N * ho * ho, c), **f32)
+                blk["y"] = torch.empty((N * ho * ho, c), **f32) if blk["residual"] else blk["p"]
+                blk["gy"] = torch.empty((N * ho * ho, c), **f32)   # grad of the block output
+                self.blocks.append(blk)
+                cin, h = c, ho
+        head, classes = cfg["head"], cfg["classes"]
+        self.hf = h
+        self.head = LinearOp("head", pb("head.weight"), pb("head.bias"), N * h * h, "relu")
+        self.fc = LinearOp("fc", pb("fc.weight"), pb("fc.bias"), N, "none")
+        self.ops += [self.head, self.fc]
+        self.hh = torch.empty((N * h * h, head), **f32)
+        self.ghh = torch.empty((N * h * h, head), **f32)
+        self.pool = torch.empty((N, head), **f32)
+        self.gpool = torch.empty((N, head), **f32)
+        self.out = torch.empty((N, classes), **f32)
+        self.gout = torch.empty((N, classes), **f32)
+        # each operator's (input, output) buffers
+        self.io = {}
+        cur = self.stem_y
+        for blk in self.blocks:
+            blk["x"] = cur
+            if blk["t"] != 1:
+                self.io[id(blk["expand"])] = (cur, blk["e"])
+                self.io[id(blk["dw"])] = (blk["e"], blk["d"])
+            else:
+                self.io[id(blk["dw"])] = (cur, blk["d"])
+            self.io[id(blk["project"])] = (blk["d"], blk["p"])
+            cur = blk["y"]
+        self.io[id(self.head)] = (cur, self.hh)
+        self.io[id(self.fc)] = (self.pool, self.out)
+        # the blocks whose projection is followed by the residual add
+        self.residual_after = {id(b["project"]): b for b in self.blocks if b["residual"]}
+
+    def _carry(self, i, fused):
+        """Pending updates the forward launch of operator i carries: the next
+        operators', through depthwise ones, up to the next linear (at most
+        four tensors)."""
+        tr = self.tr
+        if not fused:
+            return None, []
+        carried, n = [], 0
+        for nxt in self.ops[i + 1:]:
+            if nxt.updated or n + len(nxt.params) > L.OF_CARRY_MAX:
+                break
+            carried.append(nxt)
+            n += len(nxt.params)
+            if nxt.kind != "dw":
+                break
+        if not carried:
+            return None, []
+        return _carry_of(tr, [p for o in carried for p in o.params]), carried
+
+    def forward(self, x, fused):
+        tr = self.tr
+        s = tr._s()
+        for i, op in enumerate(self.ops):
+            if fused and not op.updated:
+                _self_update(tr, op.params)   # no earlier launch carried it
+                op.updated = True
+            carry, carried = (None, []) if op.kind == "dw" else self._carry(i, fused)
+            tr._t0("fwd", tr.stream, op)
+            if op is self.stem:
+                op.fwd(tr, x.data_ptr(), self.stem_y.data_ptr(), carry=carry)
+            elif op.kind == "dw":
+                src, dst = self.io[id(op)]
+                op.fwd(tr, src.data_ptr(), dst.data_ptr())
+            else:
+                src, dst = self.io[id(op)]
+                op.fwd(tr, src.data_ptr(), dst.data_ptr(), carry=carry)
+            tr._t1("fwd", tr.stream)
+            for o in carried:
+                o.updated = True     # their updates are enqueued with this launch
+            blk = self.residual_after.get(id(op))
+            if blk is not None:
+                tr._t0("fwd", tr.stream)
+                L.of_add(blk["x"].data_ptr(), blk["p"].data_ptr(), blk["p"].numel(),
+                         blk["y"].data_ptr(), s)
+                tr._t1("fwd", tr.stream)
+            if op is self.head:
+                tr._t0("fwd", tr.stream)
+                L.of_avgpool_fwd(self.hh.data_ptr(), self.N, self.hf * self.hf,
+                                 self.hh.shape[1], self.pool.data_ptr(), s)
+                tr._t1("fwd", tr.stream)
+
+    def _lin_bwd(self, op, dz, x, prev, act_prev, dx, fused, done):
+        tr = self.tr
+        if not fused:
+            if dx is not None:
+                tr._t0("dgrad", tr.stream, op)
+                op.dgrad(tr, dz, prev, act_prev, dx)
+                tr._t1("dgrad", tr.stream)
+            tr._t0("wgrad", tr.stream, op)
+            op.wgrad(tr, dz, x)
+            tr._t1("wgrad", tr.stream)
+        elif tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad")):
+            if dx is not None:
+                tr._t0("dgrad", tr.stream, op)
+                op.dgrad(tr, dz, prev, act_prev, dx)
+                tr._t1("dgrad", tr.stream)
+            if op.overlap_update:
+                gate = _side_after_main(tr)
+                tr._t0_after("wgrad_bf", tr.side, op, gate)
+                op.wgrad_fused(tr, dz, x, tr.side.cuda_stream)
+                tr._t1("wgrad_bf", tr.side)
+            else:
+                tr._t0("wgrad_bf", tr.stream, op)
+                op.wgrad_fused(tr, dz, x, tr._s())
+                tr._t1("wgrad_bf", tr.stream)
+            done(op)
+        else:
+            op.bwd_fused(tr, dz, x, prev, act_prev, dx)
+            done(op)
+
+    def _dw_bwd(self, op, dy, x, prev, act_prev, dx, fused, done):
+        tr = self.tr
+        tr._t0("dgrad", tr.stream, op)
+        op.dgrad(tr, dy, prev, act_prev, dx)
+        tr._t1("dgrad", tr.stream)
+        if fused:
+            tr._t0("wgrad_bf", tr.stream, op)
+            op.wgrad_fused(tr, dy, x, tr._s())
+            tr._t1("wgrad_bf", tr.stream)
+            done(op)
+        else:
+            tr._t0("wgrad", tr.stream, op)
+            op.wgrad(tr, dy, x)
+            tr._t1("wgrad", tr.stream)
+
+    def _backward(self, x, fused, done):
+        tr = self.tr
+        s = tr._s()
+        P = lambda t: t.data_ptr()  # noqa: E731
+        relu, none = L.OF_ACT_RELU, L.OF_ACT_NONE
+        # classifier, pool and head
+        self._lin_bwd(self.fc, P(self.gout), P(self.pool), None, none, P(self.gpool), fused, done)
+        tr._t0("dgrad", tr.stream)
+        L.of_avgpool_bwd(P(self.gpool), P(self.hh), self.N, self.hf * self.hf, self.hh.shape[1],
+                         P(self.ghh), s)
+        tr._t1("dgrad", tr.stream)
+        last = self.blocks[-1]
+        self._lin_bwd(self.head, P(self.ghh), P(last["y"]), None, none, P(last["gy"]), fused, done)
+        for bi in reversed(range(len(self.blocks))):
+            blk = self.blocks[bi]
+            # the block input's gradient: the previous block's output gradient,
+            # or the stem's pre-activation gradient (through the stem's ReLU)
+            if bi > 0:
+                gin, in_act = self.blocks[bi - 1]["gy"], none
+            else:
+                gin, in_act = self.stem_g, relu
+            xin = blk["x"]
+            self._lin_bwd(blk["project"], P(blk["gy"]), P(blk["d"]), P(blk["d"]), relu,
+                          P(blk["gd"]), fused, done)
+            if blk["t"] != 1:
+                self._dw_bwd(blk["dw"], P(blk["gd"]), P(blk["e"]), P(blk["e"]), relu,
+                             P(blk["ge"]), fused, done)
+                self._lin_bwd(blk["expand"], P(blk["ge"]), P(xin), P(xin) if in_act else None,
+                              in_act, P(gin), fused, done)
+            else:
+                self._dw_bwd(blk["dw"], P(blk["gd"]), P(xin), P(xin) if in_act else None, in_act,
+                             P(gin), fused, done)
+            if blk["residual"]:
+                # the skip connection: the block input also gets the output's gradient
+                tr._t0("add", tr.stream)
+                L.of_add(P(gin), P(blk["gy"]), gin.numel(), P(gin), s)
+                tr._t1("add", tr.stream)
+        # the stem is the first layer: no data gradient
+        stem = self.stem
+        if fused:
+            gate = _side_after_main(tr) if stem.overlap_update else None
+            if gate is not None:
+                tr._t0_after("wgrad_bf", tr.side, stem, gate)
+                stem.wgrad_fused(tr, P(self.stem_g), P(x), tr.side.cuda_stream)
+                tr._t1("wgrad_bf", tr.side)
+            else:
+                tr._t0("wgrad_bf", tr.stream, stem)
+                stem.wgrad_fused(tr, P(self.stem_g), P(x), tr._s())
+                tr._t1("wgrad_bf", tr.stream)
+            done(stem)
+        else:
+            tr._t0("wgrad", tr.stream, stem)
+            stem.wgrad(tr, P(self.stem_g), P(x))
+            tr._t1("wgrad", tr.stream)
+
+    def backward_plain(self, x):
+        self._backward(x, False, None)
+
+    def backward_fused(self, x, done):
+        self._backward(x, True, done)
+
+    def argmax(self):
+        return {}
+
+
 class Trainer:
     """Trains one workload on one GPU under a chosen ordering."""
 
-    def __init__(self, cfg, init, device="cuda:0", merge_dgrad=False, conv_prologue=False):
+    def __init__(self, cfg, init, device="cuda:0", merge_dgrad=False, conv_prologue=False,
+                 linear_prologue=False):
         """merge_dgrad: backward-fusion runs each fp32 linear layer with at most
         64 rows as one merged data-gradient + update pass (of_linear_bwd_merged).
         conv_prologue: forward-fusion applies a convolution's pending update in
         its forward's filter-tile loads (of_conv_fwd_fused) instead of carrying
-        it in the previous launch."""
+        it in the previous launch.
+        linear_prologue: the same for fp32 linear layers of more than 64 rows
+        (of_linear_fwd_fused with a second buffer set); layers of at most 64
+        rows always take the prologue (in place)."""
         L.load()
         self.cfg, self.hyper = cfg, cfg["opt"]
         self.device = torch.device(device)
@@ -751,6 +1067,10 @@ class Trainer:
             self.net = ChainNet(self, cfg, pb)
         elif cfg["kind"] == "tblock":
             self.net = TBlockNet(self, cfg, pb)
+        elif cfg["kind"] == "mbv2":
+            if cfg["dtype"] != "f32":
+                raise NotImplementedError("the MobileNetV2-like network runs with fp32 operands")
+            self.net = MBNet(self, cfg, pb)
         else:
             raise NotImplementedError(f"model kind {cfg['kind']!r} has no GPU path in this build")
         self.ops = self.net.ops
@@ -765,6 +1085,8 @@ class Trainer:
                 op.merge_dgrad = True
             if op.kind == "conv":
                 op.prologue_ff = bool(conv_prologue)
+            if op.kind == "linear" and op.fp32 and op.M > 64:
+                op.prologue_ff = bool(linear_prologue)
         f32 = dict(dtype=torch.float32, device=self.device)
         wsm = max([op.ws(w) for op in self.ops for w in (0, 1, 2)] + [16])
         wsm = max([wsm] + [op.ws(L.OF_LINEAR_BWD_MERGED) for op in self.ops if op.kind == "linear"
@@ -800,7 +1122,7 @@ class Trainer:
         # light layers updates in stream order and needs no join at the step's
         # end (two runtime calls fewer per step); the Transformer blocks update
         # their LayerNorm parameters there.
-        self.uses_side = (not isinstance(self.net, ChainNet) or
+        self.uses_side = (getattr(self.net, "side_updates", True) or
                           any(op.overlap_update and not getattr(op, "merge_dgrad", False)
                               for op in self.ops))
         self.pending_ordering = None
@@ -977,7 +1299,7 @@ class Trainer:
         # updates are carried by the previous launch (the same values) in
         # launched steps too.
         for op in self.ops:
-            if op.kind == "conv":
+            if op.two_sets():
                 op.prologue_ff = False
         saved = ([(p.step, p.count) for p in self.params.values()],
                  [op.updated for op in self.ops], self.t, self.pending_ordering)

@@ -130,8 +130,22 @@ def test_fused_entry_validation(lib):
     W = _param(16 * 12)
     opt = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9), 1)
     # forward-fusion needs the pending gradient
-    assert _status(L.of_linear_fwd_fused, d, FAKE, W, None, None, None, opt, None, FAKE, None, 0,
-                   None) == L.OF_EINVAL
+    assert _status(L.of_linear_fwd_fused, d, FAKE, W, None, None, None, None, None, opt, None, FAKE,
+                   None, 0, None) == L.OF_EINVAL
+    # more than one row tile (M > 64) needs the second buffer set; bf16 operands are refused
+    big = _desc(M=65)
+    assert _status(L.of_linear_fwd_fused, big, FAKE, W, None, FAKE, None, None, None, opt, None,
+                   FAKE, None, 0, None) == L.OF_EUNSUPPORTED
+    assert "W_out" in L.of_last_error()
+    assert _status(L.of_linear_fwd_fused, _desc(dtype=L.OF_BF16), FAKE, W, _param(16 * 12, FAKE + 64),
+                   FAKE, None, None, None, opt, None, FAKE, None, 0, None) == L.OF_EUNSUPPORTED
+    # the second set must not share buffers with the first
+    assert _status(L.of_linear_fwd_fused, big, FAKE, W, W, FAKE, None, None, None, opt, None,
+                   FAKE, None, 0, None) == L.OF_EINVAL
+    Wo = _param(16 * 12, FAKE + 64, FAKE + 128, FAKE + 192)
+    assert _status(L.of_linear_fwd_fused, _desc(M=65, has_bias=1), FAKE, W, Wo, FAKE,
+                   _param(16), None, FAKE, opt, None, FAKE, None, 0, None) == L.OF_EINVAL
+    assert "b_out" in L.of_last_error()
     # backward-fusion: bad act_prev, and a dgrad that needs the saved tensor
     assert _status(L.of_linear_bwd_fused, d, FAKE, FAKE, W, None, None, None, opt, None, 4, FAKE,
                    None, 0, None, 0, None, None) == L.OF_EINVAL
@@ -296,3 +310,54 @@ def test_depthwise_validation(lib):
     opt.step = 0
     assert _status(L.of_dwconv_wgrad_fused, d, FAKE, FAKE, W, b, None, None, opt, FAKE, need,
                    None) == L.OF_EINVAL
+    # stride 2 is accepted (its slices follow the smaller output); stride 3 is not, and the
+    # implicit-GEMM 3x3 convolutions run with stride 1 only
+    s2 = L.OfConvDesc(2, 5, 7, 3, 3, L.OF_ACT_RELU, 1, 2)
+    assert 0 < L.of_dwconv_workspace_size(s2) <= need
+    s3 = L.OfConvDesc(2, 5, 7, 3, 3, L.OF_ACT_RELU, 1, 3)
+    assert L.of_dwconv_workspace_size(s3) == 0
+    assert _status(L.of_dwconv_fwd, s3, FAKE, FAKE, FAKE, FAKE, None) == L.OF_EUNSUPPORTED
+    c2 = L.OfConvDesc(2, 5, 7, 3, 8, L.OF_ACT_RELU, 1, 2)
+    assert L.of_conv_workspace_size(c2, L.OF_CONV_FWD) == 0
+    assert "stride" in L.of_last_error()
+
+
+def test_avgpool_validation(lib):
+    assert _status(L.of_avgpool_fwd, None, 2, 49, 8, FAKE, None) == L.OF_EINVAL
+    assert _status(L.of_avgpool_fwd, FAKE, 2, 0, 8, FAKE, None) == L.OF_EINVAL
+    assert _status(L.of_avgpool_fwd, FAKE + 2, 2, 49, 8, FAKE, None) == L.OF_EALIGN
+    assert _status(L.of_avgpool_fwd, FAKE, 1 << 20, 1 << 20, 8, FAKE, None) == L.OF_EUNSUPPORTED
+    assert _status(L.of_avgpool_bwd, FAKE, None, 2, 49, 8, None, None) == L.OF_EINVAL
+    assert _status(L.of_avgpool_bwd, FAKE, FAKE + 1, 2, 49, 8, FAKE, None) == L.OF_EALIGN
+
+
+def test_operand_size_limit(lib):
+    """Operand tiles are addressed with 32-bit byte offsets from the tile's
+    first element: every linear entry point rejects an operand matrix of 2 GiB
+    or more (X, W or Y) before any HIP call, instead of reading zeros or
+    wrapped data."""
+    opt = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 1)
+    cases = [_desc(M=1024, N=8, K=1 << 19),           # X is exactly 2 GiB
+             _desc(M=8, N=1 << 19, K=1024),           # W is 2 GiB
+             _desc(M=1024, N=8, K=16, ldy=1 << 19),   # Y's rows are 2 GiB apart in total
+             _desc(M=2, N=4, K=4, ldx=1 << 62)]       # an absurd stride, no overflow
+    for d in cases:
+        W = _param(d.N * d.K)
+        calls = [
+            (L.of_linear_fwd, (d, FAKE, W, None, None, FAKE, FAKE, 1 << 40, None)),
+            (L.of_linear_fwd_fused, (d, FAKE, W, None, FAKE, None, None, None, opt, None, FAKE,
+                                     FAKE, 1 << 40, None)),
+            (L.of_linear_bwd_data, (d, FAKE, W, None, L.OF_ACT_NONE, FAKE, FAKE, 1 << 40, None)),
+            (L.of_linear_bwd_weight, (d, FAKE, FAKE, FAKE, None, 0, FAKE, 1 << 40, None)),
+            (L.of_linear_bwd_fused, (d, FAKE, FAKE, W, None, None, None, opt, None, 0, FAKE,
+                                     FAKE, 1 << 40, None, 0, None, None)),
+        ]
+        for fn, args in calls:
+            assert _status(fn, *args) == L.OF_EUNSUPPORTED, (fn.__name__, d.M, d.N, d.K)
+            assert "2 GiB" in L.of_last_error()
+        assert L.of_linear_workspace_size(d, L.OF_LINEAR_FWD) == 0
+    # just below the limit the shape is accepted (the missing x fails instead)
+    d = _desc(M=1023, N=8, K=1 << 19)
+    assert _status(L.of_linear_fwd, d, None, _param(8 << 19), None, None, FAKE, None, 0,
+                   None) == L.OF_EINVAL
+

@@ -47,23 +47,25 @@ def _t(torch, dev, a):
     return torch.as_tensor(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
 
-def _inputs(shape, seed):
+def _inputs(shape, seed, stride=1):
     r = np.random.default_rng(seed)
     n, h, w, c = shape
     x = r.standard_normal(shape).astype(np.float32)
-    dy = (r.standard_normal(shape) * 0.1).astype(np.float32)
+    oshape = (n, (h - 1) // stride + 1, (w - 1) // stride + 1, c)
+    dy = (r.standard_normal(oshape) * 0.1).astype(np.float32)
     wt = (r.standard_normal((3, 3, c)) * 0.3).astype(np.float32)
     b = (r.standard_normal(c) * 0.1).astype(np.float32)
     prev = np.maximum(r.standard_normal(shape), 0).astype(np.float32)  # a ReLU output
     return x, dy, wt, b, prev
 
 
-def _oracle(x, dy, wt, b):
-    op = OL.DepthwiseConv3x3(OL.Param("w", wt.astype(np.float64)), OL.Param("b", b.astype(np.float64)))
+def _oracle(x, dy, wt, b, stride=1):
+    op = OL.DepthwiseConv3x3(OL.Param("w", wt.astype(np.float64)), OL.Param("b", b.astype(np.float64)),
+                             stride)
     y, xp = op.forward(x.astype(np.float64))
     (dx,), (dw, db) = op.backward(xp, dy.astype(np.float64))
     ab = OL.DepthwiseConv3x3(OL.Param("w", np.abs(wt).astype(np.float64)),
-                             OL.Param("b", np.abs(b).astype(np.float64)))
+                             OL.Param("b", np.abs(b).astype(np.float64)), stride)
     ybound = ab.abs_bound(x.astype(np.float64))
     _, xpa = ab.forward(np.abs(x).astype(np.float64))
     (dxb,), (dwb, dbb) = ab.backward(xpa, np.abs(dy).astype(np.float64))
@@ -118,6 +120,86 @@ def test_depthwise_fwd_dgrad_wgrad(env, shape):
     L.of_dwconv_bwd_weight(d, DY.data_ptr(), X.data_ptr(), DW.data_ptr(), None, 0,
                            ws.data_ptr(), ws.numel() * 4, s)
     np.testing.assert_array_equal(DW.cpu().numpy(), dw1)
+
+
+# stride 2: even and odd sizes (the last output row / column then reads one
+# padded row), channel quads and ragged channel counts, MobileNetV2 sizes
+SHAPES_S2 = [(1, 1, 1, 1), (2, 5, 7, 3), (3, 9, 11, 67), (4, 8, 8, 64), (2, 14, 15, 96),
+             (32, 112, 112, 96), (32, 14, 14, 576)]
+
+
+@pytest.mark.parametrize("shape", SHAPES_S2)
+def test_depthwise_stride2(env, shape):
+    """Stride 2 (zero pad 1): forward with bias and ReLU, data gradient through
+    the previous layer's ReLU mask, filter gradient, and backward-fusion bit for
+    bit equal to the eager filter gradient + optimizer step."""
+    torch, L, dev = env
+    x, dy, wt, b, prev = _inputs(shape, 3 + sum(shape), stride=2)
+    ref = _oracle(x, dy, wt, b, stride=2)
+    n, h, w, c = shape
+    s = torch.cuda.current_stream().cuda_stream
+    X, DY, Wt, B, PR = (_t(torch, dev, a) for a in (x, dy, wt, b, prev))
+    d = L.OfConvDesc(n, h, w, c, c, L.OF_ACT_RELU, 1, 2)
+    Y = torch.full(dy.shape, float("nan"), device=dev)
+    L.of_dwconv_fwd(d, X.data_ptr(), Wt.data_ptr(), B.data_ptr(), Y.data_ptr(), s)
+    _within(Y.cpu().numpy(), np.maximum(ref["y"], 0), ref["yb"], 1e-6)
+    DX = torch.full(shape, float("nan"), device=dev)
+    L.of_dwconv_bwd_data(d, DY.data_ptr(), Wt.data_ptr(), PR.data_ptr(), L.OF_ACT_RELU,
+                         DX.data_ptr(), s)
+    got = DX.cpu().numpy()
+    _within(got, ref["dx"] * (prev > 0), ref["dxb"], 1e-6)
+    assert np.all(got[prev <= 0] == 0)
+    ws = torch.empty(max(4, L.of_dwconv_workspace_size(d) // 4), device=dev)
+    DW, DB = torch.empty((3, 3, c), device=dev), torch.empty(c, device=dev)
+    L.of_dwconv_bwd_weight(d, DY.data_ptr(), X.data_ptr(), DW.data_ptr(), DB.data_ptr(), 0,
+                           ws.data_ptr(), ws.numel() * 4, s)
+    dw1, db1 = DW.cpu().numpy(), DB.cpu().numpy()
+    _within(dw1, ref["dw"], ref["dwb"], 1e-4)
+    _within(db1, ref["db"], ref["dbb"], 1e-4)
+    # backward-fusion: the reduction's last pass applies Adam, bit-identical to eager + step
+    hyper = HYPERS["adam"]
+    P1, P2 = _P(torch, L, dev, wt, 7), _P(torch, L, dev, wt, 7)
+    B1, B2 = _P(torch, L, dev, b, 8), _P(torch, L, dev, b, 8)
+    opt = L.make_opt(hyper, 3)
+    L.of_dwconv_wgrad_fused(d, DY.data_ptr(), X.data_ptr(), P1.p, B1.p, None, None, opt,
+                            ws.data_ptr(), ws.numel() * 4, s)
+    import ctypes
+    arr = (L.OfParam * 2)(P2.p, B2.p)
+    gp = (ctypes.c_void_p * 2)(DW.data_ptr(), DB.data_ptr())
+    L.of_optimizer_step(2, arr, gp, opt, s)
+    torch.cuda.synchronize()
+    for a, bb in zip(P1.state() + B1.state(), P2.state() + B2.state()):
+        np.testing.assert_array_equal(a, bb)
+
+
+@pytest.mark.parametrize("shape", [(4, 8, 8, 64), (8, 14, 14, 96), (2, 28, 28, 132)])
+def test_depthwise_wgrad_bits_do_not_depend_on_alignment(env, shape):
+    """C % 4 == 0 takes the four-channel pass 1 for 16-byte aligned tensors and
+    the one-channel pass 1 otherwise; both sum 16 pixel streams per channel in
+    the same order, so views of x and dy offset by one float (not 16-byte
+    aligned) give the same filter and bias gradient bits as aligned ones."""
+    torch, L, dev = env
+    x, dy, wt, b, prev = _inputs(shape, 7 + sum(shape))
+    n, h, w, c = shape
+    s = torch.cuda.current_stream().cuda_stream
+    d = L.OfConvDesc(n, h, w, c, c, L.OF_ACT_NONE, 1)
+    X, DY = _t(torch, dev, x), _t(torch, dev, dy)
+    Xo = torch.empty(x.size + 1, device=dev)
+    DYo = torch.empty(dy.size + 1, device=dev)
+    Xo[1:].copy_(X.reshape(-1))
+    DYo[1:].copy_(DY.reshape(-1))
+    assert (Xo[1:].data_ptr() % 16) != 0 and (DYo[1:].data_ptr() % 16) != 0
+    ws = torch.empty(max(4, L.of_dwconv_workspace_size(d) // 4), device=dev)
+    out = []
+    for xp, dyp in ((X.data_ptr(), DY.data_ptr()), (Xo[1:].data_ptr(), DYo[1:].data_ptr())):
+        DW, DB = torch.empty((3, 3, c), device=dev), torch.empty(c, device=dev)
+        L.of_dwconv_bwd_weight(d, dyp, xp, DW.data_ptr(), DB.data_ptr(), 0, ws.data_ptr(),
+                               ws.numel() * 4, s)
+        out.append((DW.cpu().numpy(), DB.cpu().numpy()))
+    np.testing.assert_array_equal(out[1][0], out[0][0])
+    np.testing.assert_array_equal(out[1][1], out[0][1])
+    ref = _oracle(x, dy, wt, b)
+    _within(out[1][0], ref["dw"], ref["dwb"], 1e-4)
 
 
 _ORACLE = {}

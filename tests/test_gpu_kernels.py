@@ -140,7 +140,10 @@ class _Param:
             # keeps the float32 rounding of a contraction's gradient (~1e-7) from
             # being amplified by 1/sqrt(v) past the tolerance.
             self.v = ((0.5 + r.random(shape)) * 1e-2).astype(np.float32)
-        self.v = (r.random(shape).astype(np.float32) * 1e-4) if (step > 1 and kind != "sgd") else np.zeros(shape, np.float32)
+        elif step > 1 and kind != "sgd":
+            self.v = r.random(shape).astype(np.float32) * 1e-4
+        else:
+            self.v = np.zeros(shape, np.float32)
         self.W = _t(torch, dev, self.w)
         self.M = _t(torch, dev, self.m)
         self.V = _t(torch, dev, self.v)
@@ -259,7 +262,9 @@ def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
 def test_fwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     """Forward-fusion (Alg. 2): the pending update is applied while W is loaded and
     the forward uses the updated values.  Checked against the oracle and bit for bit
-    against the eager pair (multi-tensor optimizer -> plain forward)."""
+    against the eager pair (multi-tensor optimizer -> plain forward).  More than 64
+    rows span several row tiles: the update goes to a second buffer set (written
+    by the first row tile) and the current set must stay untouched."""
     torch, L, dev = env
     r = _rng(M * N + K)
     hyper = HYPERS[kind]
@@ -278,10 +283,19 @@ def test_fwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     X, GW, GB = (_t(torch, dev, a) for a in (x, gw, gb))
     Y = torch.full((M, N), float("nan"), device=dev)
     ws = _ws(torch, dev, L.of_linear_workspace_size(d, L.OF_LINEAR_FWD))
-    L.of_linear_fwd_fused(d, X.data_ptr(), Wp.p, GW.data_ptr(), Bp.p, GB.data_ptr(),
-                          L.make_opt(hyper, step), None, Y.data_ptr(), ws.data_ptr(),
-                          ws.numel() * 4, 0)
+    two = M > 64
+    if two:
+        Wo = _Param(torch, L, dev, (N, K), kind, 13, step)   # overwritten by the call
+        Bo = _Param(torch, L, dev, (N,), kind, 14, step)
+        before = [t.clone() for t in (Wp.W, Wp.M, Wp.V, Bp.W, Bp.M, Bp.V)]
+    L.of_linear_fwd_fused(d, X.data_ptr(), Wp.p, Wo.p if two else None, GW.data_ptr(), Bp.p,
+                          Bo.p if two else None, GB.data_ptr(), L.make_opt(hyper, step), None,
+                          Y.data_ptr(), ws.data_ptr(), ws.numel() * 4, 0)
     torch.cuda.synchronize()
+    if two:
+        for a, b in zip(before, (Wp.W, Wp.M, Wp.V, Bp.W, Bp.M, Bp.V)):
+            assert torch.equal(a, b)         # the current set is only read
+        Wp, Bp = Wo, Bo
     Wp.check(refW)
     Bp.check(refB)
     assert rel(Y.cpu().numpy(), y_ref) <= TOL

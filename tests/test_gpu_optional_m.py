@@ -114,8 +114,8 @@ def _run_all(torch, L, dev, hyper, with_m):
     WF = _P(torch, L, dev, (N, K), 5, with_m)
     XF, GW, Y = _t(torch, dev, xf), _t(torch, dev, gw), torch.empty((Mf, N), device=dev)
     wsf = _ws(torch, dev, L.of_linear_workspace_size(df, L.OF_LINEAR_FWD))
-    L.of_linear_fwd_fused(df, XF.data_ptr(), WF.p, GW.data_ptr(), None, None, opt, None,
-                          Y.data_ptr(), wsf.data_ptr(), wsf.numel() * 4, s)
+    L.of_linear_fwd_fused(df, XF.data_ptr(), WF.p, None, GW.data_ptr(), None, None, None, opt,
+                          None, Y.data_ptr(), wsf.data_ptr(), wsf.numel() * 4, s)
     out["fwd_fused"] = (WF, gw)
 
     # a2: an update carried by another forward launch

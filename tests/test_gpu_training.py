@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 import oracle
-from parity import rel, check_param, check_param_decisions
+from parity import rel, check_param, check_update, teachers, undetermined, _f32
 from workloads import get_config, reduced_config, make_params, make_batch, make_eval_batch
 
 pytestmark = pytest.mark.gpu
@@ -37,6 +37,7 @@ CASES = [
     ("linear4x8192", "reduced"),
     ("vgg11", "reduced"),
     ("tblock12", "reduced"),
+    ("mbv2", "reduced"),
 ]
 
 
@@ -97,27 +98,33 @@ def test_vgg_pool_argmax(gpu):
 
 WINDOWS = [  # full-size workloads: one-step windows starting from the oracle's own state
     ("mlp8x1024", (0, 1, 9, 19)),
-    ("linear4x8192", (0, 1)),
+    ("linear4x8192", (0, 1, 5, 9)),
 ]
 
 
-def _mismatch(st, loss, cand_loss, cand, cfg, steps):
+def _mismatch(st, loss, cand_loss, cand, cfg, start, teach):
     """None if a GPU state equals one oracle candidate within the parity rules,
     else the first violated rule."""
     try:
         assert rel(loss, [cand_loss]) <= TOL, f"loss {loss} vs {cand_loss}"
         for k in cand["params"]:
-            check_param(st["params"][k], cand["params"][k], cfg["opt"], steps, TOL,
-                        cand["min_sqrt_vhat"].get(k), what=k)
             r = rel(st["m"][k], cand["m"][k])
             assert r <= TOL, f"m {k}: rel {r:.2e}"
             r = rel(st["v"][k], cand["v"][k])
             assert r <= TOL, f"v {k}: rel {r:.2e}"
+            und = undetermined(st["m"][k], cand["m"][k], start, k, cfg["opt"], TOL) \
+                if k in teach else None
+            check_param(st["params"][k], cand["params"][k], cfg["opt"], 1, TOL,
+                        cand["min_sqrt_vhat"].get(k), what=k, exclude=und)
+            check_update(st["params"][k], _f32(start["params"][k]), cand["params"][k],
+                         start["params"][k], cfg["opt"], TOL, cand["min_sqrt_vhat"].get(k),
+                         what=f"update {k}", undetermined=und, teacher=teach.get(k))
         return None
     except AssertionError as e:
         return str(e)
 
 
+@pytest.mark.timeout(1200)
 @pytest.mark.parametrize("name,starts", WINDOWS)
 def test_windowed_parity_full_size(gpu, name, starts):
     """Full-size workloads, whose K-step trajectory is chaotic in float32 (Adam's
@@ -130,14 +137,18 @@ def test_windowed_parity_full_size(gpu, name, starts):
     A backward ReLU decision on a pre-activation within float32 rounding of 0 can
     go either way, so the oracle enumerates the step's outcomes over its ambiguous
     decisions (fewest flips first) and each ordering must equal one of them under
-    the parity rules; which one is reported."""
+    the parity rules; which one is reported.  Besides the values, the update
+    itself is compared (check_update): each element's move against the oracle's,
+    and against the update rule applied to the GPU's own gradient."""
     import torch
     from paper_2104_00237_amd.trainer import Trainer
     cfg = get_config(name)
     last = max(starts) + 1
     want = set(starts) | {s - 1 for s in starts if s > 0}
+    print(f"{name}: oracle, {last} steps", flush=True)
     ref = oracle.run(cfg, "eager", steps=last, snapshots=want)
     for s in starts:
+        print(f"{name}: window {s} -> {s + 1}", flush=True)
         results = {}
         for o in ("eager", "ff", "bf"):
             tr = Trainer(cfg, make_params(cfg), gpu)
@@ -155,7 +166,7 @@ def test_windowed_parity_full_size(gpu, name, starts):
                 tr.flush()
             st = tr.state()
             assert all(v == s + 1 for v in st["step"].values())
-            results[o] = (st, loss)
+            results[o] = (st, loss, teachers(st, ref["snapshots"][s], cfg["opt"]))
             del tr
             torch.cuda.empty_cache()
         np.testing.assert_array_equal(results["bf"][0]["params"]["fc1.weight"],
@@ -165,22 +176,25 @@ def test_windowed_parity_full_size(gpu, name, starts):
         for flips, cand_loss, cand in oracle.candidate_steps(cfg, ref["snapshots"][s], s + 1):
             # One step from the oracle's own state: the sensitivity of this step's
             # update is set by this outcome's sqrt(v_hat) alone (cand["min_sqrt_vhat"]).
-            for o, (st, loss) in results.items():
+            for o, (st, loss, teach) in results.items():
                 if o in matched:
                     continue
-                msg = _mismatch(st, loss, cand_loss, cand, cfg, 1)
+                msg = _mismatch(st, loss, cand_loss, cand, cfg, ref["snapshots"][s], teach)
                 if msg is None:
                     matched[o] = flips
                 else:
                     why.setdefault(o, []).append((len(flips), msg))
             if len(matched) == len(results):
                 break
-        print(f"{name} step {s + 1}: matched candidates", {o: len(f) for o, f in matched.items()})
+        print(f"{name} step {s + 1}: matched candidates", {o: len(f) for o, f in matched.items()},
+              flush=True)
         for o in set(results) - set(matched):
             for n, msg in why[o][:12]:
                 print(f"  {o}: candidate with {n} flips rejected: {msg}")
         assert set(matched) == set(results), f"step {s + 1}: no oracle outcome for " \
             f"{sorted(set(results) - set(matched))}"
+        del results
+    del ref
 
 
 @pytest.mark.timeout(400)
@@ -215,9 +229,102 @@ def test_vgg_full_size_first_step(gpu):
             np.testing.assert_array_equal(out[o][0]["params"][k], st["params"][k])
             np.testing.assert_array_equal(out[o][0]["m"][k], st["m"][k])
     zero = {k: np.zeros(np.shape(v)) for k, v in init.items()}
-    search = oracle.DecisionSearch(cfg, dict(params=init, m=zero, v=dict(zero),
-                                             step={k: 0 for k in init}), 1)
-    assert rel(loss, [search.loss]) <= TOL, (loss, search.loss)
+    state = dict(params=init, m=zero, v=dict(zero), step={k: 0 for k in init})
+    flips = _vgg_search(get_config("vgg11"), state, 1, st, loss, "eager")
+    print("vgg11 step 1: flipped decisions per node", flips)
+
+
+def _tblock_orderings(torch, gpu, cfg, start, prev=None):
+    """One step of tblock12 under each ordering from `start` (a state dict);
+    forward-fusion starts from `prev` with start's gradient pending when given."""
+    from paper_2104_00237_amd.trainer import Trainer
+    t = int(next(iter(start["step"].values()))) + 1
+    x, y = make_batch(cfg, t)
+    out = {}
+    for o in ("eager", "ff", "bf"):
+        tr = Trainer(cfg, make_params(cfg), gpu)
+        if o == "ff" and prev is not None:
+            tr.load_state(prev["params"], prev["m"], prev["v"], prev["step"], pending=start["grad"])
+        else:
+            tr.load_state(start["params"], start["m"], start["v"], start["step"])
+        tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
+        loss = tr.loss_history()
+        if o == "ff":
+            tr.flush()
+        out[o] = (tr.state(), loss)
+        del tr
+        torch.cuda.empty_cache()
+    return out
+
+
+def _tblock_check(cfg, out, start, ref, losses):
+    """bf16 parity of one AdamW step: loss, m and v within 2e-2 (max-norm
+    relative), the values within 2e-2, and the update element by element
+    (check_update) against the oracle and against AdamW applied to the GPU's own
+    gradient.  On the first step the elements whose oracle gradient is within
+    twice the measured gradient error of zero are left to the second rule."""
+    hyper = cfg["opt"]
+    for o, (st, loss) in out.items():
+        assert rel(loss, losses) <= TOL_BF16, (o, loss, losses)
+        worst_m, worst_u, und = 0.0, 0.0, []
+        teach = teachers(st, start, hyper)
+        for k in ref["params"]:
+            vh = np.sqrt(ref["v"][k] / (1.0 - hyper["beta2"] ** ref["step"][k]))
+            vh = np.where(vh > 0.0, vh, np.inf)
+            u = undetermined(st["m"][k], ref["m"][k], start, k, hyper, TOL_BF16)
+            check_param(st["params"][k], ref["params"][k], hyper, 1, TOL_BF16, vh, what=f"{o} {k}",
+                        exclude=u)
+            rm = rel(st["m"][k], ref["m"][k])
+            assert rm <= TOL_BF16, (o, k, rm)
+            assert rel(st["v"][k], ref["v"][k]) <= TOL_BF16, (o, k)
+            assert st["step"][k] == ref["step"][k]
+            r, n = check_update(st["params"][k], _f32(start["params"][k]), ref["params"][k],
+                                start["params"][k], hyper, TOL_BF16, vh, what=f"{o} update {k}",
+                                undetermined=u, teacher=teach[k])
+            und.append(n / ref["params"][k].size)
+            worst_m, worst_u = max(worst_m, rm), max(worst_u, r)
+        print(f"tblock12 {o} step {ref['step'][k]}: loss {loss[0]:.6f} (oracle {losses[0]:.6f}), "
+              f"largest relative error of m {worst_m:.2e}, of the update {worst_u:.2e}; "
+              f"elements left to the own-gradient rule: median {np.median(und):.2%}, "
+              f"max {np.max(und):.2%} of a tensor", flush=True)
+    for k in ref["params"]:
+        np.testing.assert_array_equal(out["bf"][0]["params"][k], out["eager"][0]["params"][k])
+        np.testing.assert_array_equal(out["bf"][0]["v"][k], out["eager"][0]["v"][k])
+
+
+@pytest.mark.timeout(600)
+def test_tblock_full_size_first_step(gpu):
+    """The 12-block bf16 Transformer stack at 4096 tokens, hidden 1024, FFN 4096:
+    the first AdamW step under each ordering against the oracle's first step,
+    and backward-fusion bit for bit equal to eager."""
+    import torch
+    cfg = get_config("tblock12")
+    print("tblock12: oracle step 1", flush=True)
+    ref = oracle.run(cfg, "eager", steps=1, snapshots={0})
+    start = ref["snapshots"][0]
+    out = _tblock_orderings(torch, gpu, cfg, start)
+    _tblock_check(cfg, out, start, ref, ref["losses"])
+
+
+@pytest.mark.timeout(1200)
+def test_tblock_full_size_later_step(gpu):
+    """tblock12 at full size, one-step window at a later AdamW step: every
+    ordering restarts from the oracle's state after step 5 (forward-fusion from
+    step 4 with step 5's gradient pending) and takes step 6, where the moments
+    carry five steps of history."""
+    import torch
+    cfg = get_config("tblock12")
+    s = 5
+    print(f"tblock12: oracle, {s + 1} steps", flush=True)
+    ref = oracle.run(cfg, "eager", steps=s + 1, snapshots={s - 1, s})
+    out = _tblock_orderings(torch, gpu, cfg, ref["snapshots"][s], prev=ref["snapshots"][s - 1])
+    _tblock_check(cfg, out, ref["snapshots"][s], ref, ref["losses"][s:])
+
+
+def _vgg_search(cfg, state, t, st, loss, what):
+    """Settle the oracle's decision search against one GPU state; returns flips per node."""
+    search = oracle.DecisionSearch(cfg, state, t)
+    assert rel(loss, [search.loss]) <= TOL, (what, loss, search.loss)
     flips = {}
     while not search.done:
         node, names = search.current()
@@ -229,56 +336,51 @@ def test_vgg_full_size_first_step(gpu):
                 chosen = subset
                 break
             why.append((len(subset), errs))
-        assert chosen is not None, f"node {node} {names}: no oracle outcome; tried {why[:4]}"
+        assert chosen is not None, f"{what} node {node} {names}: no oracle outcome; tried {why[:4]}"
         flips[names[0]] = len(chosen)
         search.accept(chosen)
     ref = search.finish()
     for k in ref["params"]:
-        assert st["step"][k] == ref["step"][k] == 1
+        assert st["step"][k] == ref["step"][k] == t
         assert st["count"][k] == 0
-    print("vgg11 step 1: flipped decisions per node", flips)
+    return flips
 
 
-@pytest.mark.timeout(400)
-def test_tblock_full_size_first_step(gpu):
-    """The 12-block bf16 Transformer stack at 4096 tokens, hidden 1024, FFN 4096:
-    the first AdamW step under each ordering against the oracle's first step
-    (bf16 tolerance; Adam's eps-dominated elements under the parity rule), and
-    backward-fusion bit for bit equal to eager."""
+@pytest.mark.timeout(900)
+def test_vgg_full_size_second_step(gpu):
+    """VGG-11 at batch 128, one-step window at step 2: eager and backward-fusion
+    restart from the oracle's state after step 1 (momentum buffers filled),
+    forward-fusion from the initial state with step 1's gradient pending; each
+    is settled against the oracle's decision search from that state."""
     import torch
     from paper_2104_00237_amd.trainer import Trainer
-    cfg = get_config("tblock12")
-    ref = oracle.run(cfg, "eager", steps=1)
-    init = make_params(cfg)
-    x, y = make_batch(cfg, 1)
+    cfg = get_config("vgg11")
+    print("vgg11: oracle step 1", flush=True)
+    ref = oracle.run(cfg, "eager", steps=1, snapshots={0, 1})
+    s0, s1 = ref["snapshots"][0], ref["snapshots"][1]
+    x, y = make_batch(cfg, 2)
     out = {}
     for o in ("eager", "ff", "bf"):
-        tr = Trainer(cfg, init, gpu)
+        tr = Trainer(cfg, make_params(cfg), gpu)
+        if o == "ff":
+            tr.load_state(s0["params"], s0["m"], s0["v"], s0["step"], pending=s1["grad"])
+        else:
+            tr.load_state(s1["params"], s1["m"], s1["v"], s1["step"])
         tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
         loss = tr.loss_history()
         if o == "ff":
             tr.flush()
-        st = tr.state()
-        out[o] = st
-        assert rel(loss, ref["losses"]) <= TOL_BF16, (o, loss, ref["losses"])
-        worst, und = 0.0, []
-        for k in ref["params"]:
-            _, n = check_param(st["params"][k], ref["params"][k], cfg["opt"], 1, TOL_BF16,
-                               ref["min_sqrt_vhat"].get(k), what=f"{o} {k}", ref_m=ref["m"][k],
-                               grad_tol=TOL_BF16)
-            und.append(n / ref["params"][k].size)
-            assert rel(st["m"][k], ref["m"][k]) <= TOL_BF16, (o, k)
-            assert rel(st["v"][k], ref["v"][k]) <= TOL_BF16, (o, k)
-            assert st["step"][k] == 1
-            worst = max(worst, rel(st["m"][k], ref["m"][k]))
-        print(f"tblock12 {o}: loss {loss[0]:.6f} (oracle {ref['losses'][0]:.6f}), "
-              f"largest relative error of m {worst:.2e}, elements held to Adam's bound: "
-              f"median {np.median(und):.1%} max {np.max(und):.1%} of a tensor")
+        out[o] = (tr.state(), loss)
         del tr
         torch.cuda.empty_cache()
-    for k in ref["params"]:
-        np.testing.assert_array_equal(out["bf"]["params"][k], out["eager"]["params"][k])
-        np.testing.assert_array_equal(out["bf"]["v"][k], out["eager"]["v"][k])
+    st, loss = out["eager"]
+    np.testing.assert_array_equal(out["bf"][1], loss)
+    for k in st["params"]:
+        np.testing.assert_array_equal(out["bf"][0]["params"][k], st["params"][k])
+        np.testing.assert_array_equal(out["bf"][0]["m"][k], st["m"][k])
+    for o in ("eager", "ff"):
+        flips = _vgg_search(cfg, s1, 2, out[o][0], out[o][1], o)
+        print(f"vgg11 step 2 {o}: flipped decisions per node", flips, flush=True)
 
 
 # Adagrad's and RMSprop's first step is g / (|g| sqrt(c) + eps), whose derivative
@@ -398,3 +500,31 @@ def _gpu_run_prologue(torch, cfg, steps, dev, prologue):
     st = tr.state()
     st.update(losses=losses)
     return st
+
+
+def test_linear_prologue_forward_fusion(gpu):
+    """Forward-fusion with every linear layer's pending update applied in its own
+    forward's W-tile loads: the reduced 8-layer MLP (72 rows, more than one row
+    tile) writes each update to the second buffer set, which becomes current;
+    K steps against the oracle's eager run."""
+    import torch
+    from paper_2104_00237_amd.trainer import Trainer
+    cfg = reduced_config("mlp8x1024")
+    assert cfg["batch"] > 64
+    K = cfg["steps"]
+    ref = oracle.run(cfg, "eager", steps=K)
+    tr = Trainer(cfg, make_params(cfg), gpu, linear_prologue=True)
+    assert all(op.two_sets() for op in tr.ops if op.kind == "linear")
+    for t in range(1, K + 1):
+        x, y = make_batch(cfg, t)
+        tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), "ff")
+    losses = tr.loss_history()
+    tr.flush()
+    st = tr.state()
+    assert rel(losses, ref["losses"]) <= TOL
+    for k in ref["params"]:
+        check_param(st["params"][k], ref["params"][k], cfg["opt"], K, TOL,
+                    ref["min_sqrt_vhat"].get(k), what=k)
+        assert rel(st["m"][k], ref["m"][k]) <= TOL, k
+        assert rel(st["v"][k], ref["v"][k]) <= TOL, k
+        assert st["step"][k] == K

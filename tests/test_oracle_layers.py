@@ -162,6 +162,42 @@ def test_dwconv3x3_is_block_diagonal_conv_loops_and_grads():
     _check_op(op, [x])
 
 
+def test_dwconv3x3_stride2_is_the_subsampled_stride1_output_and_grads():
+    """Stride 2 (zero pad 1) keeps every second output of the stride-1 result,
+    rows and columns 0, 2, 4, ... (odd and even sizes); gradients pass finite
+    differences."""
+    rng = np.random.default_rng(17)
+    for h, wd in ((6, 4), (5, 7), (1, 1), (2, 3)):
+        x = rng.standard_normal((2, h, wd, 3))
+        w, b = _P(rng, (3, 3, 3)), _P(rng, (3,))
+        y1, _ = L.DepthwiseConv3x3(w, b).forward(x)
+        op = L.DepthwiseConv3x3(w, b, stride=2)
+        y2, _ = op.forward(x)
+        assert y2.shape == (2, (h - 1) // 2 + 1, (wd - 1) // 2 + 1, 3)
+        np.testing.assert_allclose(y2, y1[:, ::2, ::2, :], rtol=1e-13, atol=1e-13)
+        _check_op(op, [x])
+    # the rounding scale with stride 2 is the stride-1 scale subsampled
+    np.testing.assert_allclose(op.abs_bound(x),
+                               L.DepthwiseConv3x3(w, b).abs_bound(x)[:, ::2, ::2, :], rtol=1e-13)
+
+
+def test_global_avgpool_and_pixel_reshapes():
+    rng = np.random.default_rng(18)
+    x = rng.standard_normal((2, 3, 4, 5))
+    y, _ = L.GlobalAvgPool().forward(x)
+    np.testing.assert_allclose(y[1, 2], sum(x[1, i, j, 2] for i in range(3) for j in range(4)) / 12,
+                               rtol=1e-14)
+    c = np.full((1, 2, 2, 3), 7.5)
+    np.testing.assert_array_equal(L.GlobalAvgPool().forward(c)[0], np.full((1, 3), 7.5))
+    _check_op(L.GlobalAvgPool(), [x])
+    rows, _ = L.PixelRows().forward(x)
+    assert rows.shape == (24, 5)
+    np.testing.assert_array_equal(rows[1 * 12 + 2 * 4 + 3], x[1, 2, 3])   # row (n, h, w)
+    np.testing.assert_array_equal(L.PixelMap(2, 3, 4).forward(rows)[0], x)
+    _check_op(L.PixelRows(), [x])
+    _check_op(L.PixelMap(2, 3, 4), [rows])
+
+
 def test_maxpool_first_max_and_grad():
     x = np.zeros((1, 2, 4, 1))
     x[0, :, :, 0] = [[1, 3, 2, 2], [3, 0, 2, 2]]   # window 1: tie 3/3, window 2: all equal
@@ -192,3 +228,51 @@ def test_xent_stable_for_large_logits():
     z = np.array([[1000.0, 0.0], [0.0, -1000.0]])
     loss, _ = xent(z, np.array([0, 0]))
     assert loss == pytest.approx(0.0, abs=1e-12)
+
+
+def _brute_abs_conv(x, w, b, depthwise):
+    """sum over taps (and input channels) of |x||w|, plus |b|, by direct loops
+    over every output element; zero padding 1, stride 1."""
+    n, h, wd, c = x.shape
+    cout = w.shape[-1] if depthwise else w.shape[0]
+    s = np.zeros((n, h, wd, cout))
+    for i in range(n):
+        for y in range(h):
+            for xx in range(wd):
+                for o in range(cout):
+                    acc = abs(b[o])
+                    for r in range(3):
+                        for q in range(3):
+                            yy, xq = y + r - 1, xx + q - 1
+                            if not (0 <= yy < h and 0 <= xq < wd):
+                                continue
+                            if depthwise:
+                                acc += abs(x[i, yy, xq, o]) * abs(w[r, q, o])
+                            else:
+                                for ci in range(c):
+                                    acc += abs(x[i, yy, xq, ci]) * abs(w[o, r, q, ci])
+                    s[i, y, xx, o] = acc
+    return s
+
+
+def test_abs_bounds_are_the_absolute_sums():
+    """The rounding scales S = sum |x||w| + |b| that decide which ReLU and
+    max-pool decisions a float32 run may take differently (and the depthwise
+    kernels' tolerance) against direct loops: a wrong scale would silently widen
+    or narrow the accepted set."""
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((2, 4, 5, 3))
+    w = rng.standard_normal((4, 3, 3, 3))
+    b = rng.standard_normal(4)
+    conv = L.Conv3x3(L.Param("w", w), L.Param("b", b))
+    np.testing.assert_allclose(conv.abs_bound(x), _brute_abs_conv(x, w, b, False), rtol=1e-13)
+    assert np.all(conv.abs_bound(x) >= np.abs(conv.forward(x)[0]))
+    wd = rng.standard_normal((3, 3, 3))
+    dw = L.DepthwiseConv3x3(L.Param("w", wd), L.Param("b", b[:3]))
+    np.testing.assert_allclose(dw.abs_bound(x), _brute_abs_conv(x, wd, b[:3], True), rtol=1e-13)
+    xl = rng.standard_normal((5, 7))
+    wl = rng.standard_normal((3, 7))
+    lin = L.Linear(L.Param("w", wl), L.Param("b", b[:3]))
+    want = np.array([[sum(abs(xl[m, k] * wl[n, k]) for k in range(7)) + abs(b[n])
+                      for n in range(3)] for m in range(5)])
+    np.testing.assert_allclose(lin.abs_bound(xl), want, rtol=1e-13)

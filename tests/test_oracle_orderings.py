@@ -12,7 +12,7 @@ from oracle import run, new_model
 from oracle import layers as L
 from workloads import get_config, reduced_config
 
-CASES = ["mlp3", "mlp8x1024", "linear4x8192", "tblock12", "vgg11"]
+CASES = ["mlp3", "mlp8x1024", "linear4x8192", "tblock12", "vgg11", "mbv2"]
 
 
 def _same(a, b):
@@ -53,7 +53,7 @@ def test_full_size_mlp3_orderings():
     assert len(e["losses"]) == 5
 
 
-@pytest.mark.parametrize("name", ["mlp3", "vgg11", "tblock12"])
+@pytest.mark.parametrize("name", ["mlp3", "vgg11", "tblock12", "mbv2"])
 def test_planted_dependency_violation_is_caught(name):
     """Updating theta before the input gradient is computed (against the rule after
     Alg. 3) must change the result: the invariant test can see the race."""
@@ -135,6 +135,9 @@ def test_ff_first_iteration_applies_nothing():
     ("linear4x8192", dict(dims=[6] * 5, batch=3)),
     ("tblock12", dict(blocks=2, hidden=6, ffn=10, batch=4, dtype="f32")),
     ("vgg11", dict(channels=[3, 4, 4, 4, 5, 5, 5, 5], batch=2)),
+    # stride-1 and stride-2 depthwise layers, t = 1 and expanded blocks, a residual
+    ("mbv2", dict(image=5, stem=3, blocks=[[1, 4, 1, 1], [2, 3, 1, 2], [2, 3, 1, 1]], head=5,
+                  batch=2)),
 ])
 def test_whole_model_gradient_finite_differences(name, over):
     """Backward through the whole graph (wiring, residuals, pooling, loss) vs float64
@@ -142,6 +145,14 @@ def test_whole_model_gradient_finite_differences(name, over):
     cfg = reduced_config(name, **over)
     from workloads import make_batch
     model = new_model(cfg)
+    if name == "mbv2":
+        # Zero biases leave exact zeros at ReLU inputs here (a depthwise pixel whose
+        # neighbourhood is dead or padding sums to exactly 0), where central
+        # differences straddle the kink; nonzero biases keep every input off it.
+        rb = np.random.default_rng(1)
+        for p in model.params.values():
+            if p.name.endswith(".bias"):
+                p.value[...] = rb.standard_normal(p.value.shape) * 0.1
     x, y = make_batch(cfg, 1)
     x = x.astype(np.float64)
     y = y if y.dtype == np.int64 else y.astype(np.float64)

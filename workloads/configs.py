@@ -1,7 +1,7 @@
-"""The five synthetic training workloads, as data.
+"""The synthetic training workloads, as data.
 
 Each workload is a dict with:
-  kind      "mlp" | "tblock" | "vgg"  (model family)
+  kind      "mlp" | "tblock" | "vgg" | "mbv2"  (model family)
   batch     rows per mini-batch (tokens for "tblock", images for "vgg")
   loss      "xent" (softmax cross-entropy, int64 labels) | "mse"
   opt       optimizer kind and hyperparameters
@@ -18,6 +18,20 @@ Model families:
   vgg     3x3 convolutions (stride 1, zero pad 1, bias, ReLU) with output
           channels `channels`; a 2x2 max-pool after the convolutions listed in
           `pool_after` (1-based); a final linear classifier on the 1x1 map.
+  mbv2    MobileNetV2-like: a 3x3 stem convolution (stride 1, bias, ReLU) with
+          `stem` output channels, then inverted-residual blocks from the rows
+          (t, c, n, s) of `blocks` (n blocks of c output channels, the first
+          with stride s, the rest stride 1; expansion t):
+              1x1 expand to t * c_in channels (a linear over the N*H*W pixel
+                  rows, bias, ReLU; absent when t == 1),
+              3x3 depthwise convolution (stride s, zero pad 1, bias, ReLU),
+              1x1 project to c channels (linear over pixel rows, bias, no
+                  activation),
+              + the block input when the stride is 1 and c_in == c;
+          then a 1x1 convolution to `head` channels (bias, ReLU), the global
+          average over the spatial positions and a linear classifier.  ReLU
+          stands in for MobileNetV2's ReLU6 and there is no batch normalisation
+          (as in vgg).
 
 Layouts (shared by both sides): activations are row-major [rows, features];
 images are NHWC; a linear weight is [out, in]; a conv filter is
@@ -61,6 +75,20 @@ CONFIGS = {
         batch=32, loss="xent", classes=10, dtype="f32", steps=5,
         opt=dict(kind="sgd", lr=0.01, momentum=0.9, weight_decay=1e-4),
     ),
+    # MobileNetV2-like network (the paper's Fig. 3 / Table 2 model) with its
+    # ImageNet layer shapes: the rows of MobileNetV2's block table, a 112x112
+    # input to a stride-1 stem standing in for its stride-2 stem on 224x224
+    # images, batch 32 (as in Fig. 3), Adam with coupled weight decay
+    # (PyTorch 1.6's Adam(weight_decay=...), the framework the paper's
+    # implementation uses).
+    "mbv2": dict(
+        kind="mbv2", image=112, in_channels=3, stem=32,
+        blocks=[[1, 16, 1, 1], [6, 24, 2, 2], [6, 32, 3, 2], [6, 64, 4, 2], [6, 96, 3, 1],
+                [6, 160, 3, 2], [6, 320, 1, 1]],
+        head=1280, batch=32, loss="xent", classes=10, dtype="f32", steps=10,
+        opt=dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                 weight_decay=4e-5),
+    ),
     # Parameter-bound stack: 4 linear layers 8192x8192, no bias, no activation.
     "linear4x8192": dict(
         kind="mlp", dims=[8192] * 5, act="none", bias=False,
@@ -83,6 +111,10 @@ _REDUCED = {
     "vgg11": dict(channels=[16, 24, 40, 40, 48, 48, 56, 56], batch=3, steps=4,
                   opt=dict(kind="sgd", lr=0.01, momentum=0.9, weight_decay=5e-4)),
     "linear4x8192": dict(dims=[520] * 5, batch=40, steps=3),
+    # every kind of block: t = 1, stride 2, residual repeats; ragged widths
+    "mbv2": dict(image=14, stem=8, blocks=[[1, 6, 1, 1], [6, 12, 2, 2], [6, 16, 2, 2],
+                                           [4, 20, 1, 1]],
+                 head=40, batch=3, steps=3),
 }
 
 
@@ -113,6 +145,24 @@ def mlp_ties(cfg):
         if (dims[i - 1], dims[i]) != (dims[j - 1], dims[j]):
             raise ValueError(f"layers {i} and {j} have different shapes")
     return tie
+
+
+def mbv2_blocks(cfg):
+    """The inverted-residual blocks of an mbv2 workload, in order: dicts with
+    name (parameter prefix), t, cin, hidden (t * cin), cout, stride,
+    residual, and the input and output spatial sizes h_in, h_out."""
+    out = []
+    cin, h = cfg["stem"], cfg["image"]
+    k = 0
+    for t, c, n, s in cfg["blocks"]:
+        for r in range(n):
+            k += 1
+            stride = s if r == 0 else 1
+            h_out = (h - 1) // stride + 1
+            out.append(dict(name=f"blk{k}.", t=t, cin=cin, hidden=t * cin, cout=c, stride=stride,
+                            residual=stride == 1 and cin == c, h_in=h, h_out=h_out))
+            cin, h = c, h_out
+    return out
 
 
 def param_specs(cfg):
@@ -157,6 +207,24 @@ def param_specs(cfg):
             cin = cout
         specs.append(("fc.weight", (cfg["classes"], cin), "kaiming", cin))
         specs.append(("fc.bias", (cfg["classes"],), "zeros", cin))
+    elif kind == "mbv2":
+        cin = cfg["in_channels"]
+        specs.append(("stem.weight", (cfg["stem"], 3, 3, cin), "kaiming", 9 * cin))
+        specs.append(("stem.bias", (cfg["stem"],), "zeros", 9 * cin))
+        for b in mbv2_blocks(cfg):
+            p, ci, hd, co = b["name"], b["cin"], b["hidden"], b["cout"]
+            if b["t"] != 1:
+                specs.append((p + "expand.weight", (hd, ci), "kaiming", ci))
+                specs.append((p + "expand.bias", (hd,), "zeros", ci))
+            specs.append((p + "dw.weight", (3, 3, hd), "kaiming", 9))
+            specs.append((p + "dw.bias", (hd,), "zeros", 9))
+            specs.append((p + "project.weight", (co, hd), "kaiming", hd))
+            specs.append((p + "project.bias", (co,), "zeros", hd))
+        last = mbv2_blocks(cfg)[-1]["cout"]
+        specs.append(("head.weight", (cfg["head"], last), "kaiming", last))
+        specs.append(("head.bias", (cfg["head"],), "zeros", last))
+        specs.append(("fc.weight", (cfg["classes"], cfg["head"]), "kaiming", cfg["head"]))
+        specs.append(("fc.bias", (cfg["classes"],), "zeros", cfg["head"]))
     else:
         raise ValueError(f"unknown model kind {kind!r}")
     return specs
@@ -168,7 +236,7 @@ def input_shape(cfg):
         return (cfg["batch"], cfg["dims"][0])
     if cfg["kind"] == "tblock":
         return (cfg["batch"], cfg["hidden"])
-    if cfg["kind"] == "vgg":
+    if cfg["kind"] in ("vgg", "mbv2"):
         s = cfg["image"]
         return (cfg["batch"], s, s, cfg["in_channels"])
     raise ValueError(cfg["kind"])
@@ -190,6 +258,8 @@ def describe(cfg):
         s = "mlp " + "-".join(map(str, cfg["dims"]))
     elif k == "tblock":
         s = f"tblock x{cfg['blocks']} d{cfg['hidden']} ffn{cfg['ffn']}"
+    elif k == "mbv2":
+        s = f"mbv2 {len(mbv2_blocks(cfg))} blocks stem{cfg['stem']} head{cfg['head']} img{cfg['image']}"
     else:
         s = "vgg " + "-".join(map(str, cfg["channels"])) + f" img{cfg['image']}"
     return f"{s} batch{cfg['batch']} {cfg['dtype']} {cfg['opt']['kind']} {cfg['loss']}"
