@@ -328,6 +328,27 @@ of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const f
                                int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
                                void* stream);
 
+/*
+ * of_linear_bwd_merged without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Arguments, results and errors as in
+ * of_linear_bwd_merged; the data-gradient partials go to a buffer the library
+ * holds in device memory: OF_MERGED_STATIC_SCRATCH_BYTES per device, kept
+ * until the process ends.  A shape whose partials need more
+ * (of_linear_workspace_size(d, OF_LINEAR_BWD_MERGED) above that; e.g. more
+ * than 65536 columns at 64 rows) returns OF_EUNSUPPORTED before any launch.
+ * No call allocates or frees memory.  Every call on one device shares the
+ * buffer: calls that overlap on a device (different streams or threads
+ * without ordering between them) race and must not be issued.  The buffer's
+ * device address is looked up on the first call made on each device.
+ */
+#define OF_MERGED_STATIC_SCRATCH_BYTES (32u << 20)
+of_status of_linear_bwd_merged_static(const of_linear_desc* d, const float* dz, const float* x,
+                                      const of_param* W, const of_param* b,
+                                      const float* gW_partial, const float* gb_partial,
+                                      const of_opt* opt, const float* prev, int32_t act_prev,
+                                      float* dx_prev, void* stream);
+
 /* ------------------------------------------------- convolution layers */
 /*
  * 3x3 convolutions (cross-correlation, stride 1, zero padding 1) as implicit

@@ -51,6 +51,7 @@ class OfCarry(ctypes.Structure):
 
 OF_CLIP_WS_BYTES = 2048
 OF_STREAM_READ, OF_STREAM_COPY = 0, 1
+OF_MERGED_STATIC_SCRATCH_BYTES = 32 << 20   # of_linear_bwd_merged_static's buffer per device
 
 
 class OfGradRef(ctypes.Structure):
@@ -97,6 +98,9 @@ _SIGS = {
     "of_linear_bwd_merged": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, P(OfParam),
                                        P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
                                        c_int32, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_linear_bwd_merged_static": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, P(OfParam),
+                                              P(OfParam), c_void_p, c_void_p, P(OfOpt), c_void_p,
+                                              c_int32, c_void_p, c_void_p]),
     "of_hbm_stream": (c_int32, [c_int32, c_void_p, c_void_p, c_int64, c_int32, c_void_p]),
     "of_elementwise_fused_update": (c_int32, [P(OfParam), c_void_p, c_int64, c_int64,
                                               P(OfOpt), c_void_p]),
@@ -212,7 +216,7 @@ def of_layernorm_partial_rows(M):
 
 
 for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
-           "of_linear_bwd_fused", "of_linear_bwd_merged",
+           "of_linear_bwd_fused", "of_linear_bwd_merged", "of_linear_bwd_merged_static",
            "of_hbm_stream", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_fwd_fused", "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",

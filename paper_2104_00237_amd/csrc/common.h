@@ -306,6 +306,10 @@ hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, 
                              hipStream_t stream);
 size_t merged_workspace_bytes(int M, int N, int K);
 hipError_t merged_bwd_launch(const MergedLaunch& L, hipStream_t stream);
+// The library-owned partials buffer of of_linear_bwd_merged_static: its size,
+// and its address on the current device (looked up once per device).
+size_t merged_scratch_bytes();
+hipError_t merged_scratch_ptr(float** ptr);
 
 // ------------------------------------------------------ depthwise 3x3 conv
 size_t dw_workspace_bytes(const of_conv_desc& d);

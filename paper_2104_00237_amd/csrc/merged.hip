@@ -23,6 +23,8 @@
 // Per parameter and step this moves R W, m, v and W W, m, v (24 B for Adam)
 // instead of the separate data gradient's extra read of W (28 B).
 
+#include <mutex>
+
 #include "gemm_common.h"
 
 namespace opfuse {
@@ -303,6 +305,41 @@ void merged_plan(int M, int N, int K, int* S, int* per) {
   s = std::min(s, chunks);
   *per = (chunks + s - 1) / s;
   *S = (chunks + *per - 1) / *per;
+}
+
+// Partials buffer of the no-allocation entry point (of_linear_bwd_merged_static),
+// for callers that cannot allocate (graph capture, serving loops).  32 MiB
+// holds the partials of every layer of at most 64 rows whose W has up to
+// 65536 columns (an 8192 x 8192 layer at 64 rows needs 16 MiB).  Each device
+// the library runs on holds its own copy until the process ends; every call on
+// a device shares it, so calls that overlap on one device race.  The partials
+// need no clearing: every element read is written earlier in the same call.
+constexpr size_t kMergedScratchBytes = OF_MERGED_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) float merged_scratch[kMergedScratchBytes / sizeof(float)];
+
+size_t merged_scratch_bytes() { return kMergedScratchBytes; }
+
+// In host code `merged_scratch` names a host-side stand-in, not device memory:
+// its device address comes from the runtime, per device, with that device
+// current, on the first call there.
+hipError_t merged_scratch_ptr(float** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(merged_scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = static_cast<float*>(addr[dev]);
+  return hipSuccess;
 }
 
 size_t merged_workspace_bytes(int M, int N, int K) {

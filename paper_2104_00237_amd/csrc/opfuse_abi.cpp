@@ -539,12 +539,13 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
 }
 
 namespace {
-// of_linear_bwd_merged: validation, then the launch.
+// Shared by of_linear_bwd_merged (caller workspace) and
+// of_linear_bwd_merged_static (library scratch: use_scratch, ws unused).
 of_status merged_entry(const of_linear_desc* d, const float* dz, const float* x,
                        const of_param* W, const of_param* b, const float* gW_partial,
                        const float* gb_partial, const of_opt* opt, const float* prev,
                        int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
-                       void* stream) {
+                       void* stream, bool use_scratch) {
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
   if ((st = check_merged(d)) != OF_OK) return st;
@@ -561,10 +562,20 @@ of_status merged_entry(const of_linear_desc* d, const float* dz, const float* x,
   float* part = static_cast<float*>(ws);
   if (dx_prev) {
     if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
-    REQUIRE(ws_bytes >= need, OF_EWORKSPACE,
-            "workspace of %zu bytes is smaller than the %zu needed", ws_bytes, need);
-    REQUIRE(ws != nullptr, OF_EWORKSPACE, "workspace is NULL");
-    REQUIRE((((uintptr_t)ws) & 15u) == 0, OF_EALIGN, "workspace must be 16-byte aligned");
+    if (use_scratch) {
+      REQUIRE(need <= merged_scratch_bytes(), OF_EUNSUPPORTED,
+              "of_linear_bwd_merged_static: this shape needs %zu bytes of partials, more than "
+              "the library's %zu-byte scratch (use of_linear_bwd_merged with a workspace)",
+              need, merged_scratch_bytes());
+      if ((st = hip_status(merged_scratch_ptr(&part), "of_linear_bwd_merged_static scratch")) !=
+          OF_OK)
+        return st;
+    } else {
+      REQUIRE(ws_bytes >= need, OF_EWORKSPACE,
+              "workspace of %zu bytes is smaller than the %zu needed", ws_bytes, need);
+      REQUIRE(ws != nullptr, OF_EWORKSPACE, "workspace is NULL");
+      REQUIRE((((uintptr_t)ws) & 15u) == 0, OF_EALIGN, "workspace must be 16-byte aligned");
+    }
   }
   MergedLaunch L;
   L.dz = dz; L.ldz = ldy_of(d);
@@ -577,7 +588,8 @@ of_status merged_entry(const of_linear_desc* d, const float* dz, const float* x,
   L.dx = dx_prev;
   L.part = part;
   L.M = (int)d->M; L.N = (int)d->N; L.K = (int)d->K;
-  return hip_status(merged_bwd_launch(L, (hipStream_t)stream), "of_linear_bwd_merged launch");
+  return hip_status(merged_bwd_launch(L, (hipStream_t)stream),
+                    use_scratch ? "of_linear_bwd_merged_static launch" : "of_linear_bwd_merged launch");
 }
 }  // namespace
 
@@ -587,7 +599,16 @@ of_status of_linear_bwd_merged(const of_linear_desc* d, const float* dz, const f
                                int32_t act_prev, float* dx_prev, void* ws, size_t ws_bytes,
                                void* stream) {
   return merged_entry(d, dz, x, W, b, gW_partial, gb_partial, opt, prev, act_prev, dx_prev, ws,
-                      ws_bytes, stream);
+                      ws_bytes, stream, false);
+}
+
+of_status of_linear_bwd_merged_static(const of_linear_desc* d, const float* dz, const float* x,
+                                      const of_param* W, const of_param* b,
+                                      const float* gW_partial, const float* gb_partial,
+                                      const of_opt* opt, const float* prev, int32_t act_prev,
+                                      float* dx_prev, void* stream) {
+  return merged_entry(d, dz, x, W, b, gW_partial, gb_partial, opt, prev, act_prev, dx_prev,
+                      nullptr, 0, stream, true);
 }
 
 of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,

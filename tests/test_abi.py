@@ -361,3 +361,28 @@ def test_operand_size_limit(lib):
     assert _status(L.of_linear_fwd, d, None, _param(8 << 19), None, None, FAKE, None, 0,
                    None) == L.OF_EINVAL
 
+
+def test_merged_static_validation(lib):
+    """The no-allocation merged backward validates like of_linear_bwd_merged and
+    rejects shapes whose partials exceed the library's buffer, before any HIP
+    call."""
+    opt = L.make_opt(dict(kind="adam", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8), 1)
+    big = _desc(M=64, N=1, K=(1 << 17) + 4)
+    assert L.of_linear_workspace_size(big, L.OF_LINEAR_BWD_MERGED) > \
+        L.OF_MERGED_STATIC_SCRATCH_BYTES
+    Wb = _param(big.N * big.K)
+    assert _status(L.of_linear_bwd_merged_static, big, FAKE, FAKE, Wb, None, None, None, opt,
+                   None, L.OF_ACT_NONE, FAKE, None) == L.OF_EUNSUPPORTED
+    assert "scratch" in L.of_last_error()
+    d = _desc(M=64, N=8192, K=8192)
+    W = _param(8192 * 8192)
+    assert L.of_linear_workspace_size(d, L.OF_LINEAR_BWD_MERGED) <= \
+        L.OF_MERGED_STATIC_SCRATCH_BYTES
+    for bad in (_desc(M=65, N=8192, K=8192), _desc(M=64, N=8192, K=8192, dtype=L.OF_BF16)):
+        assert _status(L.of_linear_bwd_merged_static, bad, FAKE, FAKE, _param(bad.N * bad.K),
+                       None, None, None, opt, None, L.OF_ACT_NONE, FAKE, None) == \
+            L.OF_EUNSUPPORTED
+    assert _status(L.of_linear_bwd_merged_static, d, None, FAKE, W, None, None, None, opt, None,
+                   0, None, None) == L.OF_EINVAL
+    assert _status(L.of_linear_bwd_merged_static, d, FAKE, FAKE, W, None, None, None, opt, None,
+                   L.OF_ACT_RELU, FAKE, None) == L.OF_EINVAL   # ReLU needs prev
