@@ -362,6 +362,59 @@ __global__ __launch_bounds__(T::NT) void gemm_bf16_kernel(GemmProblem pr, EpiArg
     }
     __syncthreads();
 
+    if constexpr (EPI == EPI_WGRAD_BF) {
+      if (S == 1 && (vec_epi & 2) && (pr.Q & 3) == 0) {
+        // Backward-fusion without a split: the W, m, v of a group of items are
+        // requested together, then updated and stored.  Item by item, each
+        // item's loads would wait behind the previous item's stores (they may
+        // alias), one memory latency per item.  Same arithmetic as update4.
+        constexpr int G = EPT < 2 ? EPT : 2;
+        const int64_t org = (int64_t)(p0 + h * T::PR) * ea.ldo + q0;
+        const rsrc_t rw = make_rsrc(ea.W.w + org);
+        const rsrc_t rm = make_rsrc_opt(ea.W.m, org);
+        const rsrc_t rv = ea.opt.kind != OF_OPT_SGD ? make_rsrc(ea.W.v + org) : rm;
+#pragma unroll
+        for (int e0 = 0; e0 < EPT; e0 += G) {
+          float4 pw[G], pm[G], pv[G];
+#pragma unroll
+          for (int u = 0; u < G; ++u) {
+            const int idx = tid + (e0 + u) * T::NT;
+            const int p = idx / NQ4, q = (idx % NQ4) * 4;
+            const bool ok = e0 + u < EPT && idx < ITEMS && p0 + h * T::PR + p < pr.P &&
+                            q0 + q < pr.Q;
+            const uint32_t off = ok ? (uint32_t)((p * ea.ldo + q) * 4) : kOOB;
+            pw[u] = bload4(rw, off);
+            pm[u] = bload4(rm, off);
+            pv[u] = bload4(rv, off);
+          }
+#pragma unroll
+          for (int u = 0; u < G; ++u) {
+            const int idx = tid + (e0 + u) * T::NT;
+            if (e0 + u >= EPT || idx >= ITEMS) break;
+            const int p = idx / NQ4, q = (idx % NQ4) * 4;
+            const int gp = p0 + h * T::PR + p, gq = q0 + q;
+            if (gp >= pr.P || gq >= pr.Q) continue;
+            const int64_t oo = (int64_t)gp * ea.ldo + gq;
+            float4 g = *reinterpret_cast<const float4*>(&Cs[p * T::LDC + q]);
+            if (ea.gW) {
+              const float4 e = ld4(ea.gW + oo);
+              g.x = __fadd_rn(e.x, g.x); g.y = __fadd_rn(e.y, g.y);
+              g.z = __fadd_rn(e.z, g.z); g.w = __fadd_rn(e.w, g.w);
+            }
+            float4 w = pw[u], m = pm[u], v = pv[u];
+            opt_update(ea.opt, w.x, g.x, m.x, v.x);
+            opt_update(ea.opt, w.y, g.y, m.y, v.y);
+            opt_update(ea.opt, w.z, g.z, m.z, v.z);
+            opt_update(ea.opt, w.w, g.w, m.w, v.w);
+            st4(ea.W.w + oo, w);
+            if (ea.W.m) st4(ea.W.m + oo, m);
+            if (ea.opt.kind != OF_OPT_SGD) st4(ea.W.v + oo, v);
+            if (ea.W.w_bf16) st_bf16x4(ea.W.w_bf16 + oo, w);
+          }
+        }
+        continue;
+      }
+    }
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
       const int idx = tid + e * T::NT;
