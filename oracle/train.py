@@ -178,10 +178,13 @@ class Model:
 def ambiguous_relu_decisions(model, x, c=1.0):
     """Backward ReLU decisions a float32 run may take differently.
 
-    A decision z > 0 is ambiguous when |z| < c * 2^-24 * sum_k |x_mk w_nk| (+|b|),
-    i.e. within the rounding scale of the float32 sum that produces z.  Returns
-    [(node index, row, column, |z| / scale)] sorted from most to least
-    ambiguous.  Only ReLUs fed directly by a Linear are examined.
+    A decision z > 0 is ambiguous when |z| < c * 2^-24 * S, with S the sum
+    of |x w| over the contraction that produced z (+|b|): the rounding scale
+    of the float32 sum (S = 0 means every term is exactly 0: not ambiguous).  ReLUs fed by a Linear (directly or through a PixelMap
+    reshape of its rows), a Conv3x3 or a DepthwiseConv3x3 are examined.
+    Returns [(node index, index of the element in the ReLU input ..., |z| /
+    scale)] sorted from most to least ambiguous; for a [rows, cols] input the
+    index is (row, column).
     """
     u = 2.0 ** -24
     env = {"input": x}
@@ -191,23 +194,28 @@ def ambiguous_relu_decisions(model, x, c=1.0):
         vals = [env[n] for n in ins]
         y, _ = op.forward(*vals)
         if isinstance(op, L.ReLU) and ins[0] in producer:
-            lin, lin_in = producer[ins[0]]
-            scale = u * lin.abs_bound(lin_in)
+            src, src_in = producer[ins[0]]
+            scale = (u * src.abs_bound(src_in)).reshape(vals[0].shape)
             ratio = np.abs(vals[0]) / np.maximum(scale, 1e-300)
-            for r, col in zip(*np.nonzero(ratio < c)):
-                out.append((i, int(r), int(col), float(ratio[r, col])))
-        if isinstance(op, L.Linear):
+            # S == 0: every term and the bias are exactly 0, so is z on any machine
+            for idx in zip(*np.nonzero((ratio < c) & (scale > 0))):
+                out.append((i,) + tuple(int(t) for t in idx) + (float(ratio[idx]),))
+        if isinstance(op, (L.Linear, L.Conv3x3, L.DepthwiseConv3x3)):
             producer[name] = (op, vals[0])
+        elif isinstance(op, L.PixelMap) and ins[0] in producer:
+            producer[name] = producer[ins[0]]   # the same values, reshaped
         env[name] = y
-    out.sort(key=lambda d: d[3])
+    out.sort(key=lambda d: d[-1])
     return out
 
 
-def candidate_steps(cfg, state, t, max_decisions=8, seed=0):
+def candidate_steps(cfg, state, t, max_decisions=8, seed=0, c=1.0):
     """Every valid float32 outcome of eager step t from `state` (a snapshot).
 
     Enumerates the subsets of the ambiguous ReLU decisions of the step (at most
-    `max_decisions`, the most ambiguous ones), fewest flips first, and yields
+    `max_decisions`, the most ambiguous ones; the threshold c of
+    ambiguous_relu_decisions allows for error carried in from earlier layers),
+    fewest flips first, and yields
     (flipped decisions, loss, state after the step) for each; for Adam-family
     optimizers the state also holds min_sqrt_vhat, the positive bias-corrected
     sqrt(v_hat) after the step (inf where v is 0), as run() reports it.
@@ -216,17 +224,24 @@ def candidate_steps(cfg, state, t, max_decisions=8, seed=0):
     x = np.asarray(x, np.float64)
     y = y if y.dtype == np.int64 else np.asarray(y, np.float64)
     probe = new_model(cfg, init=state["params"])
-    dec = ambiguous_relu_decisions(probe, x)[:max_decisions]
+    dec = ambiguous_relu_decisions(probe, x, c)[:max_decisions]
+    shapes = {}
+    env = {"input": x}
+    for i, (op, ins, name) in enumerate(probe.nodes):
+        env[name] = op.forward(*[env[n] for n in ins])[0]
+        if isinstance(op, L.ReLU):
+            shapes[i] = env[ins[0]].shape
     for nflip in range(len(dec) + 1):
         for subset in itertools.combinations(dec, nflip):
             model = new_model(cfg, init=state["params"])
             for k, p in model.params.items():
                 p.m, p.v, p.step = state["m"][k].copy(), state["v"][k].copy(), state["step"][k]
-            for i, r, col, _ in subset:
+            for d in subset:
+                i, idx = d[0], d[1:-1]
                 op = model.nodes[i][0]
                 if op.flip is None:
-                    op.flip = np.zeros((x.shape[0], model.nodes[i - 1][0].w.value.shape[0]), bool)
-                op.flip[r, col] = True
+                    op.flip = np.zeros(shapes[i], bool)
+                op.flip[idx] = True
             loss = model.step_eager(x, y)
             ps = model.params
             vh = {}

@@ -46,13 +46,17 @@ def _adam_bound(hyper):
     return hyper["lr"] * (1 - hyper["beta1"]) / np.sqrt(1 - hyper["beta2"])
 
 
-def check_param(gpu, ref, hyper, steps, tol, min_sqrt_vhat=None, what="", exclude=None):
+def check_param(gpu, ref, hyper, steps, tol, min_sqrt_vhat=None, what="", exclude=None,
+                covered=False):
     """Assert parity of one trained parameter tensor; returns (rel error, #eps-dominated).
 
     exclude (bool mask, optional): elements left out of this rule because
     check_update's teacher rule checks them (the undetermined elements of a
     first Adam step; for a tensor that starts at zero, such as a bias, their
-    value is the whole update and may take either sign)."""
+    value is the whole update and may take either sign).
+    covered: the teacher rule checks every element of this step, so the
+    eps-dominated elements need not be a small share of the tensor (their
+    Adam bound here is loose; the teacher rule is not)."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     den = max(float(np.max(np.abs(ref))), 1e-30)
@@ -65,7 +69,7 @@ def check_param(gpu, ref, hyper, steps, tol, min_sqrt_vhat=None, what="", exclud
         return r, 0
     sens = np.asarray(min_sqrt_vhat) < EPS_FACTOR * hyper["eps"]
     frac = float(sens.mean())
-    assert frac <= MAX_SENSITIVE_FRACTION, f"{what}: eps-dominated fraction {frac:.2e}"
+    assert covered or frac <= MAX_SENSITIVE_FRACTION, f"{what}: eps-dominated fraction {frac:.2e}"
     r = float(err[~sens].max() / den) if (~sens).any() else 0.0
     assert r <= tol, f"{what}: rel {r:.3e} > {tol} on well-conditioned elements"
     if sens.any():
@@ -111,7 +115,9 @@ def check_update(gpu_new, gpu_start, ref_new, ref_start, hyper, tol, min_sqrt_vh
         assert r_t <= TEACHER_TOL, f"{what}: move off the update of its own gradient by {r_t:.3e}"
     if hyper["kind"] in ("adam", "adamw") and min_sqrt_vhat is not None:
         sens = np.asarray(min_sqrt_vhat) < EPS_FACTOR * hyper["eps"]
-        assert float(sens.mean()) <= MAX_SENSITIVE_FRACTION, \
+        # with the teacher rule every element is checked exactly; without it the
+        # elements held only to Adam's bound must be few
+        assert teacher is not None or float(sens.mean()) <= MAX_SENSITIVE_FRACTION, \
             f"{what}: eps-dominated fraction {float(sens.mean()):.2e}"
         if sens.any():
             worst = float(err[sens].max())

@@ -37,7 +37,6 @@ CASES = [
     ("linear4x8192", "reduced"),
     ("vgg11", "reduced"),
     ("tblock12", "reduced"),
-    ("mbv2", "reduced"),
 ]
 
 
@@ -115,7 +114,7 @@ def _mismatch(st, loss, cand_loss, cand, cfg, start, teach):
             und = undetermined(st["m"][k], cand["m"][k], start, k, cfg["opt"], TOL) \
                 if k in teach else None
             check_param(st["params"][k], cand["params"][k], cfg["opt"], 1, TOL,
-                        cand["min_sqrt_vhat"].get(k), what=k, exclude=und)
+                        cand["min_sqrt_vhat"].get(k), what=k, exclude=und, covered=k in teach)
             check_update(st["params"][k], _f32(start["params"][k]), cand["params"][k],
                          start["params"][k], cfg["opt"], TOL, cand["min_sqrt_vhat"].get(k),
                          what=f"update {k}", undetermined=und, teacher=teach.get(k))
@@ -197,6 +196,76 @@ def test_windowed_parity_full_size(gpu, name, starts):
     del ref
 
 
+MBV2_DECISION_C = 32.0
+
+
+def test_mbv2_windows_and_orderings(gpu):
+    """The MobileNetV2-like network (reduced: every block kind, stride 2,
+    residuals).  Its float32 trajectory is chaotic under Adam (a first step of
+    +-lr on elements whose gradient sign is within rounding shifts later
+    forwards), so each step is checked as a one-step window from the oracle's
+    state, values and updates under the parity rules, for every ordering,
+    against the oracle's outcomes over the step's ambiguous ReLU decisions
+    (pre-activations within float32 rounding of 0 after a linear, depthwise or
+    convolution layer); and the three orderings, run free for K steps, are
+    bit-identical on the GPU."""
+    import torch
+    from paper_2104_00237_amd.trainer import Trainer
+    cfg = reduced_config("mbv2")
+    K = cfg["steps"]
+    ref = oracle.run(cfg, "eager", steps=K, snapshots=set(range(K + 1)))
+    for s in range(K):
+        results = {}
+        for o in ("eager", "ff", "bf"):
+            tr = Trainer(cfg, make_params(cfg), gpu)
+            if o == "ff" and s > 0:
+                a = ref["snapshots"][s - 1]
+                tr.load_state(a["params"], a["m"], a["v"], a["step"],
+                              pending=ref["snapshots"][s]["grad"])
+            else:
+                a = ref["snapshots"][s]
+                tr.load_state(a["params"], a["m"], a["v"], a["step"])
+            x, y = make_batch(cfg, s + 1)
+            tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
+            loss = tr.loss_history()
+            if o == "ff":
+                tr.flush()
+            st = tr.state()
+            assert all(v == s + 1 for v in st["step"].values())
+            results[o] = (st, loss, teachers(st, ref["snapshots"][s], cfg["opt"]))
+        matched, why = {}, {}
+        # c = 32: seventeen blocks deep, every forward activation carries a few
+        # ulps of its tensor's largest value into the next layer (2-4 measured),
+        # more than one ulp of a small element's own rounding scale
+        for flips, cand_loss, cand in oracle.candidate_steps(cfg, ref["snapshots"][s], s + 1,
+                                                              c=MBV2_DECISION_C):
+            for o, (st, loss, teach) in results.items():
+                if o in matched:
+                    continue
+                msg = _mismatch(st, loss, cand_loss, cand, cfg, ref["snapshots"][s], teach)
+                if msg is None:
+                    matched[o] = flips
+                else:
+                    why.setdefault(o, []).append((len(flips), msg))
+            if len(matched) == len(results):
+                break
+        print(f"mbv2 step {s + 1}: matched candidates", {o: len(f) for o, f in matched.items()},
+              flush=True)
+        for o in set(results) - set(matched):
+            for n, msg in why[o][:8]:
+                print(f"  {o}: candidate with {n} flips rejected: {msg}")
+        assert set(matched) == set(results), f"step {s + 1}: no oracle outcome for " \
+            f"{sorted(set(results) - set(matched))}"
+    runs = {o: _gpu_run(torch, cfg, o, K, gpu) for o in ("eager", "ff", "bf")}
+    for o in ("ff", "bf"):
+        np.testing.assert_array_equal(runs[o]["losses"], runs["eager"]["losses"])
+        for k in ref["params"]:
+            np.testing.assert_array_equal(runs[o]["params"][k], runs["eager"]["params"][k])
+            np.testing.assert_array_equal(runs[o]["m"][k], runs["eager"]["m"][k])
+            np.testing.assert_array_equal(runs[o]["v"][k], runs["eager"]["v"][k])
+        assert all(v == K for v in runs[o]["step"].values())
+
+
 @pytest.mark.timeout(400)
 def test_vgg_full_size_first_step(gpu):
     """VGG-11 at batch 128, 32x32: the first step under each ordering against the
@@ -273,7 +342,7 @@ def _tblock_check(cfg, out, start, ref, losses):
             vh = np.where(vh > 0.0, vh, np.inf)
             u = undetermined(st["m"][k], ref["m"][k], start, k, hyper, TOL_BF16)
             check_param(st["params"][k], ref["params"][k], hyper, 1, TOL_BF16, vh, what=f"{o} {k}",
-                        exclude=u)
+                        exclude=u, covered=True)
             rm = rel(st["m"][k], ref["m"][k])
             assert rm <= TOL_BF16, (o, k, rm)
             assert rel(st["v"][k], ref["v"][k]) <= TOL_BF16, (o, k)

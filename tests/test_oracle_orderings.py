@@ -322,3 +322,43 @@ def test_tied_mlp_orderings_and_counts():
     x = np.random.default_rng(0).standard_normal((cfg["batch"], cfg["dims"][0]))
     model.forward(x, before_node=lambda op: [setattr(p, "count", p.count + 1) for p in op.params])
     assert model.params["fc2.weight"].count == 2 and model.params["fc1.weight"].count == 1
+
+
+def test_ambiguous_depthwise_decision_and_flip():
+    """A depthwise pre-activation placed within float32 rounding of 0 (through
+    its bias) is reported with its NHWC index; the candidate that flips it
+    differs from the plain step exactly as a hand-flipped ReLU mask does."""
+    from oracle.train import ambiguous_relu_decisions, candidate_steps
+    from workloads import make_batch, make_params
+    cfg = reduced_config("mbv2", image=5, stem=3, blocks=[[2, 3, 1, 1]], head=4, batch=1, steps=1)
+    init = {k: np.asarray(v, np.float64) for k, v in make_params(cfg).items()}
+    rng = np.random.default_rng(4)
+    for k in init:
+        if k.endswith(".bias"):
+            init[k] = rng.standard_normal(init[k].shape) * 0.1
+    x, _ = make_batch(cfg, 1)
+    x = x.astype(np.float64)
+    model = new_model(cfg, init=init)
+    env = {"input": x}
+    for i, (op, ins, name) in enumerate(model.nodes):
+        env[name] = op.forward(*[env[n] for n in ins])[0]
+        if name == "blk1.d":
+            node_relu = i + 1
+    z = env["blk1.d"]
+    # move channel 1's bias so that pixel (0, 2, 3) sits 1e-12 above zero
+    init["blk1.dw.bias"][1] -= z[0, 2, 3, 1] - 1e-12
+    model = new_model(cfg, init=init)
+    dec = ambiguous_relu_decisions(model, x)
+    assert [d[:-1] for d in dec] == [(node_relu, 0, 2, 3, 1)]
+    state = dict(params=init, m={k: np.zeros(np.shape(v)) for k, v in init.items()},
+                 v={k: np.zeros(np.shape(v)) for k, v in init.items()}, step={k: 0 for k in init})
+    cands = list(candidate_steps(cfg, state, 1))
+    assert len(cands) == 2 and len(cands[1][0]) == 1
+    m2 = new_model(cfg, init=init)
+    m2.nodes[node_relu][0].flip = np.zeros(z.shape, bool)
+    m2.nodes[node_relu][0].flip[0, 2, 3, 1] = True
+    _, y = make_batch(cfg, 1)
+    m2.step_eager(x, y)
+    for k, p in m2.params.items():
+        np.testing.assert_array_equal(cands[1][2]["params"][k], p.value)
+    assert any(np.any(cands[1][2]["params"][k] != cands[0][2]["params"][k]) for k in init)

@@ -163,3 +163,25 @@ def test_check_update_allows_the_weights_own_float32_rounding():
     bad[4] += 5e-6                                            # 5% of a step: far beyond a rounding
     with pytest.raises(AssertionError):
         check_update(bad, w0f, ref, w0, hyper, 2e-2)
+
+
+def test_teacher_rule_lifts_the_eps_dominated_cap_only():
+    """Many eps-dominated elements fail the plain rules; with the teacher rule
+    (which checks each of them exactly) they are accepted, and a wrong move on
+    one of them is still caught."""
+    rng = np.random.default_rng(12)
+    w0 = rng.standard_normal(1000) * 0.05
+    g = rng.standard_normal(1000)
+    g[:50] = 1e-8 * rng.standard_normal(50)                # 5% eps-dominated
+    ref = _first_adam_step(w0, g, ADAM)
+    vh = np.abs(g)
+    with pytest.raises(AssertionError):
+        check_update(ref, w0, ref, w0, ADAM, 1e-4, vh)
+    with pytest.raises(AssertionError):
+        check_param(ref, ref, ADAM, 1, 1e-4, vh)
+    check_update(ref, w0, ref, w0, ADAM, 1e-4, vh, teacher=ref)
+    check_param(ref, ref, ADAM, 1, 1e-4, vh, covered=True)
+    bad = ref.copy()
+    bad[3] = w0[3] + 0.5 * (ref[3] - w0[3])
+    with pytest.raises(AssertionError):
+        check_update(bad, w0, ref, w0, ADAM, 1e-4, vh, teacher=ref)
