@@ -154,36 +154,55 @@ __device__ __forceinline__ void st_bf16x4(uint16_t* p, float4 w) {
   *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
 }
 
+// A parameter element's optimizer state (weight and history), loaded apart
+// from its update so that a kernel can issue these loads before the gradient
+// they wait for is ready.  P.m may be NULL for an optimizer that keeps no m
+// (Adagrad, RMSprop without momentum): it is then neither read nor written;
+// v is read and written for every optimizer but SGD.
+struct OptState4 { float4 w, m, v; };
+struct OptState1 { float w, m, v; };
+
+__device__ __forceinline__ OptState4 opt_load4(const OptK& o, const of_param& P, int64_t off) {
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  return OptState4{ld4(P.w + off), P.m ? ld4(P.m + off) : z,
+                   o.kind != OF_OPT_SGD ? ld4(P.v + off) : z};
+}
+
+__device__ __forceinline__ OptState1 opt_load1(const OptK& o, const of_param& P, int64_t off) {
+  return OptState1{P.w[off], P.m ? P.m[off] : 0.f, o.kind != OF_OPT_SGD ? P.v[off] : 0.f};
+}
+
+// Apply the update with gradient g to a loaded state and store it back.
+__device__ __forceinline__ float4 opt_apply4(const OptK& o, const of_param& P, OptState4 s,
+                                             float4 g, int64_t off) {
+  opt_update(o, s.w.x, g.x, s.m.x, s.v.x);
+  opt_update(o, s.w.y, g.y, s.m.y, s.v.y);
+  opt_update(o, s.w.z, g.z, s.m.z, s.v.z);
+  opt_update(o, s.w.w, g.w, s.m.w, s.v.w);
+  st4(P.w + off, s.w);
+  if (P.m) st4(P.m + off, s.m);
+  if (o.kind != OF_OPT_SGD) st4(P.v + off, s.v);
+  if (P.w_bf16) st_bf16x4(P.w_bf16 + off, s.w);
+  return s.w;
+}
+
+__device__ __forceinline__ float opt_apply1(const OptK& o, const of_param& P, OptState1 s, float g,
+                                            int64_t off) {
+  opt_update(o, s.w, g, s.m, s.v);
+  P.w[off] = s.w;
+  if (P.m) P.m[off] = s.m;
+  if (o.kind != OF_OPT_SGD) P.v[off] = s.v;
+  if (P.w_bf16) P.w_bf16[off] = f32_to_bf16(s.w);
+  return s.w;
+}
+
 // Update 4 consecutive parameter elements at `off` (all valid, 16B aligned).
-// P.m may be NULL for an optimizer that keeps no m (Adagrad, RMSprop without
-// momentum): it is then neither read nor written.
 __device__ __forceinline__ float4 update4(const OptK& o, const of_param& P, float4 g, int64_t off) {
-  float4 w = ld4(P.w + off);
-  float4 m = P.m ? ld4(P.m + off) : make_float4(0.f, 0.f, 0.f, 0.f);
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  const bool adam = o.kind != OF_OPT_SGD;
-  if (adam) v = ld4(P.v + off);
-  opt_update(o, w.x, g.x, m.x, v.x);
-  opt_update(o, w.y, g.y, m.y, v.y);
-  opt_update(o, w.z, g.z, m.z, v.z);
-  opt_update(o, w.w, g.w, m.w, v.w);
-  st4(P.w + off, w);
-  if (P.m) st4(P.m + off, m);
-  if (adam) st4(P.v + off, v);
-  if (P.w_bf16) st_bf16x4(P.w_bf16 + off, w);
-  return w;
+  return opt_apply4(o, P, opt_load4(o, P, off), g, off);
 }
 
 __device__ __forceinline__ float update1(const OptK& o, const of_param& P, float g, int64_t off) {
-  float w = P.w[off], m = P.m ? P.m[off] : 0.f, v = 0.f;
-  const bool adam = o.kind != OF_OPT_SGD;
-  if (adam) v = P.v[off];
-  opt_update(o, w, g, m, v);
-  P.w[off] = w;
-  if (P.m) P.m[off] = m;
-  if (adam) P.v[off] = v;
-  if (P.w_bf16) P.w_bf16[off] = f32_to_bf16(w);
-  return w;
+  return opt_apply1(o, P, opt_load1(o, P, off), g, off);
 }
 
 inline bool aligned16(const void* p) { return (((uintptr_t)p) & 15u) == 0; }

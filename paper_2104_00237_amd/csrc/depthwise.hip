@@ -7,17 +7,22 @@
 //
 // Filter gradient: dW[ky,kx,c] = sum over (n,h,w) of dy[n,h,w,c] *
 // x[n,h+ky-1,w+kx-1,c], db[c] = sum of dy[n,h,w,c].  Pass 1 splits the pixels
-// over S slices; each workgroup (64 channels, one per thread group, or 16
-// channel quads when C % 4 == 0 and the tensors are 16-byte aligned) writes
-// the ten per-channel sums of its slice, each the in-order sum of 16 pixel
-// streams that both kernels partition and order alike.  Pass 2 adds the S
-// slices in slice order and either writes dW / db (eager) or applies the
+// over S slices; each workgroup takes CB channels (CB from 16, 32, 48, 64,
+// whichever pads C least; one channel per thread group, or CB / 4 channel
+// quads when C % 4 == 0 and the tensors are 16-byte aligned) and writes the
+// ten per-channel sums of its slice, each the in-order sum of 16 pixel streams
+// that both kernels partition and order alike.  S is sized so that the grid
+// fills the chip (the small late layers get slices of a few dozen pixels).
+// Pass 2 adds the S slices of each sum: L lanes (a power of two up to 64) take
+// consecutive runs of slices, each in slice order, and the run sums are added
+// in lane order; it then either writes dW / db (eager) or applies the
 // optimizer to W, b and their history right there (backward-fusion: the
-// filter gradient is never stored).  Both passes are deterministic: the two
-// pass-1 kernels take the same operations in the same order for every
-// element, so the bits do not depend on which one runs (that is, on the
-// pointers' alignment), and the fused pass applies the same per-element
-// update as the eager optimizer kernel, so eager and fused give the same bits.
+// filter gradient is never stored; the parameter's state is loaded before the
+// slices are summed).  Both passes are deterministic: the two pass-1 kernels
+// take the same operations in the same order for every element, so the bits
+// do not depend on which one runs (that is, on the pointers' alignment), and
+// the fused pass applies the same per-element update as the eager optimizer
+// kernel, so eager and fused give the same bits.
 
 #include <algorithm>
 
@@ -25,8 +30,8 @@
 
 namespace opfuse {
 
-constexpr int DW_CB = 64;     // channels per workgroup in pass 1
-constexpr int DW_TAPS = 10;   // nine filter taps + the bias sum
+constexpr int DW_CB_MAX = 64;  // channels per workgroup in pass 1, at most
+constexpr int DW_TAPS = 10;    // nine filter taps + the bias sum
 
 // Input [N,H,W,C]; output [N,Ho,Wo,C] with Ho = (H - 1) / S + 1 for the
 // stride S (1 or 2, zero padding 1), a template parameter of the kernels.
@@ -93,12 +98,13 @@ __global__ __launch_bounds__(256) void dw_dgrad_kernel(const float* __restrict__
   dx[i] = act_prev == OF_ACT_NONE ? acc : __fmul_rn(acc, act_grad(act_prev, prev[i]));
 }
 
-// Pass 1: workgroup (cb, slice) sums its slice's pixels for 64 channels.
-// Each channel's pixels are split into 16 streams (stream u takes the slice's
-// pixels u, u + 16, u + 32, ... in order) whose sums are then added in stream
-// order: the same partition and order as the four-channel kernel below, so a
-// shape gives the same bits whichever of the two runs.  Thread (channel,
-// sub) keeps the streams sub, sub + 4, sub + 8 and sub + 12.
+// Pass 1: workgroup (channel block, slice) sums its slice's pixels for cb
+// channels (4 * cb threads).  Each channel's pixels are split into 16 streams
+// (stream u takes the slice's pixels u, u + 16, u + 32, ... in order) whose
+// sums are then added in stream order: the same partition and order as the
+// four-channel kernel below, so a shape gives the same bits whichever of the
+// two runs.  Thread (channel, sub) keeps the streams sub, sub + 4, sub + 8 and
+// sub + 12.  The stream sums meet in LDS, [16][10][cb] floats.
 template <int S>
 __device__ __forceinline__ void dw_wgrad_pixel(const float* __restrict__ dy,
                                                const float* __restrict__ x, const DwShape& s,
@@ -119,14 +125,26 @@ __device__ __forceinline__ void dw_wgrad_pixel(const float* __restrict__ dy,
   acc[9] = __fadd_rn(acc[9], g);
 }
 
+// The 16 stream sums of each of the 10 * cb outputs, added in stream order.
+__device__ __forceinline__ void dw_slice_sums(const float* red, int cb, int c0, int C,
+                                              float* __restrict__ part_row) {
+  for (int j = threadIdx.x; j < DW_TAPS * cb; j += blockDim.x) {
+    const int k = j / cb, l = j % cb;
+    float v = red[k * cb + l];
+#pragma unroll
+    for (int u = 1; u < 16; ++u) v = __fadd_rn(v, red[(u * DW_TAPS + k) * cb + l]);
+    if (c0 + l < C) part_row[(int64_t)k * C + c0 + l] = v;
+  }
+}
+
 template <int S>
 __global__ __launch_bounds__(256) void dw_wgrad_partial_kernel(const float* __restrict__ dy,
                                                                const float* __restrict__ x,
                                                                float* __restrict__ part,
-                                                               DwShape s, int per_slice) {
-  __shared__ float red[16][DW_TAPS][DW_CB];
-  const int cl = threadIdx.x & (DW_CB - 1), sub = threadIdx.x >> 6;
-  const int c = blockIdx.x * DW_CB + cl;
+                                                               DwShape s, int per_slice, int cb) {
+  extern __shared__ float red[];   // [16][DW_TAPS][cb]
+  const int cl = threadIdx.x % cb, sub = threadIdx.x / cb;
+  const int c = blockIdx.x * cb + cl;
   const int P = s.N * s.Ho * s.Wo;  // output pixels
   const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
   float acc[4][DW_TAPS];
@@ -145,15 +163,9 @@ __global__ __launch_bounds__(256) void dw_wgrad_partial_kernel(const float* __re
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int k = 0; k < DW_TAPS; ++k) red[sub + 4 * j][k][cl] = acc[j][k];
+    for (int k = 0; k < DW_TAPS; ++k) red[((sub + 4 * j) * DW_TAPS + k) * cb + cl] = acc[j][k];
   __syncthreads();
-  for (int j = threadIdx.x; j < DW_TAPS * DW_CB; j += 256) {
-    const int k = j / DW_CB, l = j % DW_CB, cc = blockIdx.x * DW_CB + l;
-    float v = red[0][k][l];
-#pragma unroll
-    for (int u = 1; u < 16; ++u) v = __fadd_rn(v, red[u][k][l]);
-    if (cc < s.C) part[((int64_t)blockIdx.y * DW_TAPS + k) * s.C + cc] = v;
-  }
+  dw_slice_sums(red, cb, blockIdx.x * cb, s.C, part + (int64_t)blockIdx.y * DW_TAPS * s.C);
 }
 
 // ---- four-channel variants (C % 4 == 0, 16-byte aligned tensors): one thread
@@ -231,16 +243,17 @@ __global__ __launch_bounds__(256) void dw_dgrad4_kernel(const float* __restrict_
   st4(dx + (int64_t)i * 4, acc);
 }
 
-// Pass 1, four channels per thread: 16 channel quads (64 channels) x 16 pixel
-// streams per workgroup.
+// Pass 1, four channels per thread: cb / 4 channel quads x 16 pixel streams
+// per workgroup.
 template <int S>
 __global__ __launch_bounds__(256) void dw_wgrad_partial4_kernel(const float* __restrict__ dy,
                                                                 const float* __restrict__ x,
                                                                 float* __restrict__ part,
-                                                                DwShape s, int per_slice) {
-  __shared__ float red[16][DW_TAPS][DW_CB];
-  const int q = threadIdx.x & 15, sub = threadIdx.x >> 4;
-  const int c = blockIdx.x * DW_CB + q * 4;
+                                                                DwShape s, int per_slice, int cb) {
+  extern __shared__ float red[];   // [16][DW_TAPS][cb]
+  const int nq = cb / 4;
+  const int q = threadIdx.x % nq, sub = threadIdx.x / nq;
+  const int c = blockIdx.x * cb + q * 4;
   const int P = s.N * s.Ho * s.Wo;  // output pixels
   const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
   float4 acc[DW_TAPS];
@@ -267,24 +280,20 @@ __global__ __launch_bounds__(256) void dw_wgrad_partial4_kernel(const float* __r
   }
 #pragma unroll
   for (int k = 0; k < DW_TAPS; ++k) {
-    red[sub][k][q * 4 + 0] = acc[k].x;
-    red[sub][k][q * 4 + 1] = acc[k].y;
-    red[sub][k][q * 4 + 2] = acc[k].z;
-    red[sub][k][q * 4 + 3] = acc[k].w;
+    float* r = red + (sub * DW_TAPS + k) * cb + q * 4;
+    r[0] = acc[k].x;
+    r[1] = acc[k].y;
+    r[2] = acc[k].z;
+    r[3] = acc[k].w;
   }
   __syncthreads();
-  for (int j = threadIdx.x; j < DW_TAPS * DW_CB; j += 256) {
-    const int k = j / DW_CB, l = j % DW_CB, cc = blockIdx.x * DW_CB + l;
-    float v = red[0][k][l];
-#pragma unroll
-    for (int u = 1; u < 16; ++u) v = __fadd_rn(v, red[u][k][l]);
-    if (cc < s.C) part[((int64_t)blockIdx.y * DW_TAPS + k) * s.C + cc] = v;
-  }
+  dw_slice_sums(red, cb, blockIdx.x * cb, s.C, part + (int64_t)blockIdx.y * DW_TAPS * s.C);
 }
 
 struct DwReduce {
   const float* part;
   int S, C;
+  int lanes;    // L: lanes per output element (a power of two, at most 64)
   // eager
   float* dw;
   float* db;
@@ -296,34 +305,54 @@ struct DwReduce {
   const float* gb;
 };
 
-// Pass 2: one thread per filter element (and bias element).
+// Pass 2: L consecutive lanes per filter element (and bias element).
 __global__ __launch_bounds__(256) void dw_wgrad_reduce_kernel(DwReduce r, OptK o) {
   if (r.fused) opt_prepare(o);
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= DW_TAPS * r.C) return;
-  const int k = j / r.C, c = j % r.C;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int L = r.lanes;
+  const int j = (int)(t / L), lane = (int)(t % L);
+  const bool live = j < DW_TAPS * r.C;
+  const int k = live ? j / r.C : 0, c = live ? j % r.C : 0;
   const bool bias = k == 9;
-  if (bias && !(r.fused ? r.b.w != nullptr : r.db != nullptr)) return;
-  // the loads of 8 slices are issued before their (in-order) accumulation
+  const bool want = live && (bias ? (r.fused ? r.b.w != nullptr : r.db != nullptr) : true);
+  const int off = bias ? c : j;
+  // the lead lane loads the parameter's state while the slices are summed
+  OptState1 st{0.f, 0.f, 0.f};
+  if (r.fused && want && lane == 0) st = opt_load1(o, bias ? r.b : r.W, off);
+  // lane l sums slices [l * SG, (l + 1) * SG) in order, 8 loads in flight
+  const int SG = (r.S + L - 1) / L;
+  const int kb = min(r.S, lane * SG), ke = min(r.S, kb + SG);
   const int64_t ld = (int64_t)DW_TAPS * r.C;
-  float g = r.part[j];
-  for (int s0 = 1; s0 < r.S; s0 += 8) {
-    float v[8];
+  float g = 0.f;
+  if (want) {
+    for (int s0 = kb; s0 < ke; s0 += 8) {
+      float v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = s0 + k < r.S ? r.part[(s0 + k) * ld + j] : 0.f;
+      for (int u = 0; u < 8; ++u) v[u] = s0 + u < ke ? r.part[(s0 + u) * ld + j] : 0.f;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (s0 + k < r.S) g = __fadd_rn(g, v[k]);
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < ke) g = s0 + u == kb ? v[u] : __fadd_rn(g, v[u]);
+    }
   }
+  // the run sums, added in lane order (the whole group stays within a wave)
+  if (L > 1) {
+    const int lead = (threadIdx.x & 63) & ~(L - 1);
+    float tot = __shfl(g, lead);
+    for (int u = 1; u < L; ++u) {
+      const float e = __shfl(g, lead + u);
+      if (u * SG < r.S) tot = __fadd_rn(tot, e);
+    }
+    g = tot;
+  }
+  if (!want || lane != 0) return;
   if (!r.fused) {
     float* dst = bias ? r.db + c : r.dw + j;
     *dst = r.accumulate ? __fadd_rn(*dst, g) : g;
     return;
   }
   const float* gp = bias ? r.gb : r.gW;
-  const int off = bias ? c : j;
   if (gp) g = __fadd_rn(g, gp[off]);
-  update1(o, bias ? r.b : r.W, g, off);
+  opt_apply1(o, bias ? r.b : r.W, st, g, off);
 }
 
 namespace {
@@ -332,11 +361,31 @@ int64_t dw_out(int64_t n, int S) { return (n - 1) / S + 1; }
 int64_t dw_out_pixels(const of_conv_desc& d) {
   return d.N * dw_out(d.H, dw_stride(d)) * dw_out(d.W, dw_stride(d));
 }
+// Channels per pass-1 workgroup: the width of 64, 48, 32, 16 that pads C
+// least (ties to the wider).
+int dw_cb(const of_conv_desc& d) {
+  int best = DW_CB_MAX;
+  int64_t best_pad = -1;
+  for (int cb = DW_CB_MAX; cb >= 16; cb -= 16) {
+    const int64_t pad = (d.C + cb - 1) / cb * cb - d.C;
+    if (best_pad < 0 || pad < best_pad) best = cb, best_pad = pad;
+  }
+  return best;
+}
+// Pixel slices of pass 1: enough workgroups for about 1024 threads per compute
+// unit, each slice at least 32 pixels (two per stream).
 int dw_slices(const of_conv_desc& d) {
   const int64_t P = dw_out_pixels(d);
-  const int64_t cb = (d.C + DW_CB - 1) / DW_CB;
-  const int64_t want = std::max<int64_t>(1, 1024 / cb);
-  return (int)std::max<int64_t>(1, std::min<int64_t>((P + 255) / 256, want));
+  const int cb = dw_cb(d);
+  const int64_t nblk = (d.C + cb - 1) / cb;
+  const int64_t want = std::max<int64_t>(1, (256 * 1024 / (4 * cb)) / nblk);
+  return (int)std::max<int64_t>(1, std::min<int64_t>((P + 31) / 32, want));
+}
+// Lanes per element of pass 2: runs of about 4 slices, at most a wave.
+int dw_lanes(int S) {
+  int L = 1;
+  while (L < 64 && L * 8 <= S) L *= 2;
+  return L;
 }
 DwShape dw_shape(const of_conv_desc& d) {
   const int S = dw_stride(d);
@@ -399,23 +448,26 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
   const int nsl = dw_slices(d);   // pixel slices of pass 1
   const int64_t P = dw_out_pixels(d);
   const int per = (int)((P + nsl - 1) / nsl);
-  const int cb = (int)((d.C + DW_CB - 1) / DW_CB);
+  const int cb = dw_cb(d);
+  const int nblk = (int)((d.C + cb - 1) / cb);
+  const size_t lds = (size_t)16 * DW_TAPS * cb * sizeof(float);
   float* part = static_cast<float*>(ws);
   const bool two = dw_stride(d) == 2;
+  const dim3 grid(nblk, nsl), block(4 * cb);
   if (d.C % 4 == 0 && aligned16(dy) && aligned16(x)) {
     if (two)
-      hipLaunchKernelGGL(dw_wgrad_partial4_kernel<2>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
-                         part, dw_shape(d), per);
+      hipLaunchKernelGGL(dw_wgrad_partial4_kernel<2>, grid, block, lds, stream, dy, x, part,
+                         dw_shape(d), per, cb);
     else
-      hipLaunchKernelGGL(dw_wgrad_partial4_kernel<1>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
-                         part, dw_shape(d), per);
+      hipLaunchKernelGGL(dw_wgrad_partial4_kernel<1>, grid, block, lds, stream, dy, x, part,
+                         dw_shape(d), per, cb);
   } else {
     if (two)
-      hipLaunchKernelGGL(dw_wgrad_partial_kernel<2>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
-                         part, dw_shape(d), per);
+      hipLaunchKernelGGL(dw_wgrad_partial_kernel<2>, grid, block, lds, stream, dy, x, part,
+                         dw_shape(d), per, cb);
     else
-      hipLaunchKernelGGL(dw_wgrad_partial_kernel<1>, dim3(cb, nsl), dim3(256), 0, stream, dy, x,
-                         part, dw_shape(d), per);
+      hipLaunchKernelGGL(dw_wgrad_partial_kernel<1>, grid, block, lds, stream, dy, x, part,
+                         dw_shape(d), per, cb);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -423,6 +475,7 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
   r.part = part;
   r.S = nsl;
   r.C = (int)d.C;
+  r.lanes = dw_lanes(nsl);
   r.dw = dw;
   r.db = db;
   r.accumulate = accumulate;
@@ -431,9 +484,9 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
   if (b) r.b = *b;
   r.gW = gW;
   r.gb = gb;
-  const int n = DW_TAPS * (int)d.C;
-  hipLaunchKernelGGL(dw_wgrad_reduce_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, r,
-                     o ? *o : OptK{});
+  const int64_t n = (int64_t)DW_TAPS * d.C * r.lanes;
+  hipLaunchKernelGGL(dw_wgrad_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     stream, r, o ? *o : OptK{});
   return hipGetLastError();
 }
 

@@ -213,6 +213,33 @@ __device__ __forceinline__ void bias_epilogue(const EpiArgs& ea, int p, float g)
   }
 }
 
+// Backward-fusion items of the reduction passes load the parameter's state
+// (and a shared parameter's pending gradient) before they sum the partials,
+// so that the update does not wait for one more memory round trip at the end.
+struct BfPre {
+  OptState4 st;
+  float4 e;
+};
+
+__device__ __forceinline__ BfPre bf_preload(const EpiArgs& ea, int64_t oo) {
+  BfPre b;
+  b.st = opt_load4(ea.opt, ea.W, oo);
+  b.e = ea.gW ? ld4(ea.gW + oo) : make_float4(0.f, 0.f, 0.f, 0.f);
+  return b;
+}
+
+// The vector backward-fusion epilogue on a preloaded state: the same
+// operations as epilogue<EPI_WGRAD_BF> on an item of four.
+__device__ __forceinline__ void bf_apply(const EpiArgs& ea, const BfPre& b, const float (&c)[4],
+                                         int64_t oo) {
+  float4 g = make_float4(c[0], c[1], c[2], c[3]);
+  if (ea.gW) {
+    g.x = __fadd_rn(b.e.x, g.x); g.y = __fadd_rn(b.e.y, g.y);
+    g.z = __fadd_rn(b.e.z, g.z); g.w = __fadd_rn(b.e.w, g.w);
+  }
+  opt_apply4(ea.opt, ea.W, b.st, g, oo);
+}
+
 // Sum the split partials in split order, then run the epilogue.
 template <int EPI>
 __device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& ea,
@@ -227,6 +254,10 @@ __device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& 
     const int n = min(4, Q - q);
     float c[4] = {0.f, 0.f, 0.f, 0.f};
     const float* src = partial + (int64_t)p * Q + q;
+    const int64_t oo = (int64_t)p * ea.ldo + q;
+    const bool pre = EPI == EPI_WGRAD_BF && n == 4 && (vec_epi & 2);
+    BfPre bp;
+    if (pre) bp = bf_preload(ea, oo);
     // The loads of 8 splits are issued before they are added in split order,
     // so a long split list is not one dependent chain of loads.
     if (n == 4 && (Q & 3) == 0) {
@@ -261,6 +292,10 @@ __device__ __forceinline__ void split_reduce_body(int P, int Q, int S, EpiArgs& 
             for (int e = 0; e < n; ++e) s4[e] = __fadd_rn(s4[e], t[u][e]);
       }
       for (int e = 0; e < n; ++e) c[e] = s4[e];
+    }
+    if (pre) {
+      bf_apply(ea, bp, c, oo);
+      continue;
     }
     const float* bias = nullptr;
     if ((EPI == EPI_FWD || EPI == EPI_FWD_FF) && ea.bias) bias = ea.bias + q;
@@ -330,6 +365,10 @@ __device__ __forceinline__ void split_reduce_coop_body(int P, int Q, int S, EpiA
   for (int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3; idx < total; idx += groups) {
     const int p = (int)(idx / nq4), q = (int)(idx % nq4) * 4;
     const int n = min(4, Q - q);
+    const int64_t oo = (int64_t)p * ea.ldo + q;
+    const bool pre = EPI == EPI_WGRAD_BF && n == 4 && (vec_epi & 2) && j == 0;
+    BfPre bp;
+    if (pre) bp = bf_preload(ea, oo);
     float acc[4];
     lane_sum(partial + (int64_t)p * Q + q, n, n == 4 && (Q & 3) == 0, acc);
     float c[4];
@@ -339,7 +378,9 @@ __device__ __forceinline__ void split_reduce_coop_body(int P, int Q, int S, EpiA
 #pragma unroll
       for (int g = 1; g < 8; ++g) c[e] = __fadd_rn(c[e], __shfl(acc[e], lead + g));
     }
-    if (j == 0) {
+    if (pre) {
+      bf_apply(ea, bp, c, oo);
+    } else if (j == 0) {
       const float* bias = nullptr;
       if ((EPI == EPI_FWD || EPI == EPI_FWD_FF) && ea.bias) bias = ea.bias + q;
       epilogue<EPI == EPI_FWD_FF ? EPI_FWD : EPI>(ea, p, q, c, n, bias, vec_epi);

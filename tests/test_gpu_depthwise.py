@@ -20,7 +20,7 @@ pytestmark = pytest.mark.gpu
 
 SHAPES = [  # N, H, W, C: single pixel, ragged channel tails, several slices, MobileNetV2 sizes
     (1, 1, 1, 1), (2, 5, 7, 3), (3, 9, 11, 67), (4, 8, 8, 64), (8, 14, 14, 96),
-    (2, 28, 28, 130), (32, 56, 56, 144),
+    (2, 28, 28, 130), (32, 56, 56, 144), (32, 112, 112, 32), (32, 7, 7, 960),
 ]
 HYPERS = {
     "sgd": dict(kind="sgd", lr=0.05, momentum=0.9, weight_decay=5e-4),
