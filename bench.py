@@ -693,10 +693,11 @@ def main():
     per = launches[by_shape[shape][0][1]][cost_key]
     # Each launch is bracketed by an event pair on its own stream; the pair's own
     # cost (an empty pair on the same stream) is taken off.
-    from paper_2104_00237_amd.trainer import KernelTimer
+    from paper_2104_00237_amd.trainer import KernelTimer, device_stream
     on_side = (dom == "wgrad_bf" and head == "bf"
                and getattr(by_shape[shape][0][2], "overlap_update", False))
-    dom_stream = torch.cuda.Stream() if on_side else torch.cuda.current_stream()
+    dom_stream = (device_stream(torch.device("cuda:0"), "side") if on_side
+                  else torch.cuda.current_stream())
     marker_ms = KernelTimer.marker_overhead_ms(dom_stream)
     avg_s = (float(np.mean(durs)) - marker_ms) / 1e3
     roof = kernel_roofline(per[0], per[1], avg_s, mfma_peak(cfg))

@@ -220,12 +220,13 @@ class LinearOp:
         L.of_linear_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
                              tr._s())
 
-    def wgrad(self, tr, g, x, accumulate=0):
+    def wgrad(self, tr, g, x, accumulate=0, side=False):
         """Plain weight gradient into W.g (and b.g); accumulate=1 adds to what an
-        earlier use of a shared parameter left there."""
+        earlier use of a shared parameter left there.  side: on the second
+        stream, with its workspace."""
         L.of_linear_bwd_weight(self.desc, g, x, self.W.g.data_ptr(),
                                self.b.g.data_ptr() if self.b else None, accumulate,
-                               *tr.ws_main_args(), tr._s())
+                               *_ws_args(tr, side), _stream(tr, side))
 
     def _partials(self, partial):
         """(gW, gb) of earlier uses of a shared parameter for the fused update."""
@@ -310,10 +311,10 @@ class ConvOp:
         L.of_conv_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
                            tr._s())
 
-    def wgrad(self, tr, g, x, accumulate=0):
+    def wgrad(self, tr, g, x, accumulate=0, side=False):
         L.of_conv_bwd_weight(self.desc, g, x, self.W.g.data_ptr(),
                              self.b.g.data_ptr() if self.b else None, accumulate,
-                             *tr.ws_main_args(), tr._s())
+                             *_ws_args(tr, side), _stream(tr, side))
 
     def wgrad_fused(self, tr, g, x, stream, partial=False):
         """Fused weight gradient + update; partial: add the gradient earlier uses
@@ -356,17 +357,18 @@ class DwOp:
     def dgrad(self, tr, g, prev, act_prev, dx):
         L.of_dwconv_bwd_data(self.desc, g, self.W.w.data_ptr(), prev, act_prev, dx, tr._s())
 
-    def wgrad(self, tr, g, x, accumulate=0):
+    def wgrad(self, tr, g, x, accumulate=0, side=False):
         L.of_dwconv_bwd_weight(self.desc, g, x, self.W.g.data_ptr(),
                                self.b.g.data_ptr() if self.b else None, accumulate,
-                               *tr.ws_main_args(), tr._s())
+                               *_ws_args(tr, side), _stream(tr, side))
 
     def wgrad_fused(self, tr, g, x, stream, partial=False):
         b = self.b
+        side = stream == tr.side.cuda_stream
         L.of_dwconv_wgrad_fused(self.desc, g, x, self.W.p, b.p if b else None,
                                 self.W.g.data_ptr() if partial else None,
                                 (b.g.data_ptr() if (b and partial) else None), tr.opt,
-                                *tr.ws_main_args(), stream)
+                                *_ws_args(tr, side), stream)
 
 
 class LayerNormOp:
@@ -409,6 +411,29 @@ def _ff_prologue(tr, op):
     """Whether forward-fusion applies op's pending update in its forward's W-tile
     loads (else a previous launch carries it, or a pass of its own runs)."""
     return op.prologue_ff and not (op.two_sets() and tr.capturing)
+
+
+# One side stream and one capture stream per device, made once.  HIP maps each
+# new stream onto one of a few hardware queues; a side stream made per trainer
+# can land on the main stream's queue, and its work then no longer overlaps
+# (measured: steps alternating between 4.0 and 4.9 ms on the MobileNetV2-like
+# network from one trainer to the next).  Streams keep the default priority.
+_STREAMS = {}
+
+
+def device_stream(device, role):
+    key = (str(device), role)
+    if key not in _STREAMS:
+        _STREAMS[key] = torch.cuda.Stream(device)
+    return _STREAMS[key]
+
+
+def _ws_args(tr, side):
+    return tr.ws_side_args() if side else tr.ws_main_args()
+
+
+def _stream(tr, side):
+    return tr.side.cuda_stream if side else tr._s()
 
 
 def _side_after_main(tr):
@@ -806,10 +831,25 @@ class MBNet:
     operator's pending update in the previous operator's linear or convolution
     launch (a depthwise launch carries nothing, so the launch before it also
     carries the next linear's update); backward-fusion applies each operator's
-    update right after its gradient, in stream order.
+    update right after its gradient.
+
+    Both the eager and the backward-fusion orderings run a layer's weight
+    gradient (eager: into its gradient buffer; backward-fusion: with the
+    update) on the second stream, behind an event recorded after the layer's
+    data gradient, so that it overlaps the data gradients further down; each
+    reads only buffers that no later kernel of the step writes, the data
+    gradient needs the old weights only (Alg. 3), and the main stream joins
+    the second one before the eager optimizer step or the next forward.  The
+    1x1 layers' split weight gradients are latency-bound kernels of a few
+    microseconds that fill the chip poorly on their own (measured on MI355X,
+    graph replay: every ordering about 0.2 ms faster per step); the depthwise
+    filter gradients gain nothing there and stay in stream order.
     """
 
     side_updates = False
+    side_linear = True   # 1x1 (linear) weight gradients on the second stream
+    side_dw = False      # depthwise filter gradients in stream order (measured: no gain)
+    eager_side = True    # the eager step joins the second stream before its optimizer
 
     def __init__(self, tr, cfg, pb):
         self.tr = tr
@@ -854,6 +894,7 @@ class MBNet:
         self.head = LinearOp("head", pb("head.weight"), pb("head.bias"), N * h * h, "relu")
         self.fc = LinearOp("fc", pb("fc.weight"), pb("fc.bias"), N, "none")
         self.ops += [self.head, self.fc]
+        self.set_side(self.side_linear, self.side_dw)
         self.hh = torch.empty((N * h * h, head), **f32)
         self.ghh = torch.empty((N * h * h, head), **f32)
         self.pool = torch.empty((N, head), **f32)
@@ -928,6 +969,25 @@ class MBNet:
                                  self.hh.shape[1], self.pool.data_ptr(), s)
                 tr._t1("fwd", tr.stream)
 
+    def set_side(self, linear, dw):
+        """Which weight gradients run on the second stream (both orderings)."""
+        self.side_linear, self.side_dw = linear, dw
+        for op in self.ops:
+            if isinstance(op, LinearOp):
+                op.overlap_update = linear
+
+    def _wgrad_plain(self, op, dz, x, side):
+        tr = self.tr
+        if side:
+            gate = _side_after_main(tr)
+            tr._t0_after("wgrad", tr.side, op, gate)
+            op.wgrad(tr, dz, x, side=True)
+            tr._t1("wgrad", tr.side)
+        else:
+            tr._t0("wgrad", tr.stream, op)
+            op.wgrad(tr, dz, x)
+            tr._t1("wgrad", tr.stream)
+
     def _lin_bwd(self, op, dz, x, prev, act_prev, dx, fused, done):
         tr = self.tr
         if not fused:
@@ -935,9 +995,7 @@ class MBNet:
                 tr._t0("dgrad", tr.stream, op)
                 op.dgrad(tr, dz, prev, act_prev, dx)
                 tr._t1("dgrad", tr.stream)
-            tr._t0("wgrad", tr.stream, op)
-            op.wgrad(tr, dz, x)
-            tr._t1("wgrad", tr.stream)
+            self._wgrad_plain(op, dz, x, op.overlap_update)
         elif tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad")):
             if dx is not None:
                 tr._t0("dgrad", tr.stream, op)
@@ -963,14 +1021,18 @@ class MBNet:
         op.dgrad(tr, dy, prev, act_prev, dx)
         tr._t1("dgrad", tr.stream)
         if fused:
-            tr._t0("wgrad_bf", tr.stream, op)
-            op.wgrad_fused(tr, dy, x, tr._s())
-            tr._t1("wgrad_bf", tr.stream)
+            if self.side_dw:
+                gate = _side_after_main(tr)
+                tr._t0_after("wgrad_bf", tr.side, op, gate)
+                op.wgrad_fused(tr, dy, x, tr.side.cuda_stream)
+                tr._t1("wgrad_bf", tr.side)
+            else:
+                tr._t0("wgrad_bf", tr.stream, op)
+                op.wgrad_fused(tr, dy, x, tr._s())
+                tr._t1("wgrad_bf", tr.stream)
             done(op)
         else:
-            tr._t0("wgrad", tr.stream, op)
-            op.wgrad(tr, dy, x)
-            tr._t1("wgrad", tr.stream)
+            self._wgrad_plain(op, dy, x, self.side_dw)
 
     def _backward(self, x, fused, done):
         tr = self.tr
@@ -1023,9 +1085,7 @@ class MBNet:
                 tr._t1("wgrad_bf", tr.stream)
             done(stem)
         else:
-            tr._t0("wgrad", tr.stream, stem)
-            stem.wgrad(tr, P(self.stem_g), P(x))
-            tr._t1("wgrad", tr.stream)
+            self._wgrad_plain(stem, P(self.stem_g), P(x), stem.overlap_update)
 
     def backward_plain(self, x):
         self._backward(x, False, None)
@@ -1116,7 +1176,7 @@ class Trainer:
         self.opt = self.opt_dev
         self.capturing = False
         self.stream = torch.cuda.current_stream(self.device)
-        self.side = torch.cuda.Stream(self.device)
+        self.side = device_stream(self.device, "side")
         self.side_done = torch.cuda.Event()
         # Whether backward-fusion puts any update on the side stream: a chain of
         # light layers updates in stream order and needs no join at the step's
@@ -1216,6 +1276,7 @@ class Trainer:
         self._loss(y)
         self.eager_reduce = True
         self.net.backward_plain(x)
+        self._join_plain_side()
         self._clip(vector=True)
         ps = list(self.params.values())
         step = self._advance(ps)
@@ -1226,6 +1287,14 @@ class Trainer:
         self._t1("opt", self.stream)
         for p in ps:
             p.step = step
+
+    def _join_plain_side(self):
+        """After a plain backward that computed weight gradients on the second
+        stream: the main stream waits for them (the eager optimizer step, the
+        clipping norm and the next forward's pending updates read them)."""
+        if self.uses_side and getattr(self.net, "eager_side", False):
+            self.side_done.record(self.side)
+            self.stream.wait_event(self.side_done)
 
     def _step_ff(self, x, y):
         pending = _unique([p for op in self.ops if not op.updated for p in op.params])
@@ -1238,6 +1307,7 @@ class Trainer:
         # gradients stay pending (LayerNorm's as row partials)
         self.eager_reduce = False
         self.net.backward_plain(x)
+        self._join_plain_side()
         self._clip(vector=False)
         for op in self.ops:
             op.updated = False
@@ -1304,7 +1374,7 @@ class Trainer:
         saved = ([(p.step, p.count) for p in self.params.values()],
                  [op.updated for op in self.ops], self.t, self.pending_ordering)
         g = torch.cuda.CUDAGraph()
-        cap = torch.cuda.Stream(self.device)
+        cap = device_stream(self.device, "capture")
         # the device counter holds the index of the last applied update
         self.step_dev.fill_(next(iter(self.params.values())).step)
         cap.wait_stream(self.stream)
