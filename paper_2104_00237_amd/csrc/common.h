@@ -254,6 +254,7 @@ struct GemmProblem {
   int cN, cH, cW, cC, cCout;    // convolution geometry (input N, H, W, C; Cout)
   int a_bf16, b_bf16;           // bf16 kernels: the operand is stored as bf16 (else fp32)
   FastDiv dW, dH, dC, dCout;    // convolution: divisors of the gather index arithmetic
+  int group = 0;                // tile order within an XCD's block: 0 rows of the block, g > 0 strips of g tile rows
 };
 
 // Updates carried by a contraction launch (forward-fusion of later

@@ -72,11 +72,13 @@ using BT128x256 = BTile<128, 256, 64, 2, 4, 2>;
 using BT128x128R64 = BTile<128, 128, 64, 2, 2, 2>;
 using BT128x256R32 = BTile<128, 256, 32, 2, 4, 4>;
 using BT256x128 = BTile<256, 128, 32, 4, 2, 4>;
+using BT256x256W8 = BTile<256, 256, 32, 2, 4, 2>;
+using BT256x256W4 = BTile<256, 256, 32, 2, 2, 2>;
 enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_128x256, BTI_128x128R64, BTI_128x256R32,
-               BTI_256x128, BTI_COUNT };
-static const int kBTileBP[BTI_COUNT] = {64, 128, 128, 128, 128, 256};
-static const int kBTileBQ[BTI_COUNT] = {64, 128, 256, 128, 256, 128};
-static const int kBTileBR[BTI_COUNT] = {32, 32, 64, 64, 32, 32};
+               BTI_256x128, BTI_256x256W8, BTI_256x256W4, BTI_COUNT };
+static const int kBTileBP[BTI_COUNT] = {64, 128, 128, 128, 128, 256, 256, 256};
+static const int kBTileBQ[BTI_COUNT] = {64, 128, 256, 128, 256, 128, 256, 256};
+static const int kBTileBR[BTI_COUNT] = {32, 32, 64, 64, 32, 32, 32, 32};
 #else
 enum BTileId { BTI_64x64 = 0, BTI_128x128, BTI_128x256, BTI_COUNT };
 static const int kBTileBP[BTI_COUNT] = {64, 128, 128};
@@ -257,7 +259,7 @@ __global__ __launch_bounds__(T::NT) void gemm_bf16_kernel(GemmProblem pr, EpiArg
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wp = wave % T::WP, wq = wave / T::WP;
   int tx, ty;
-  xcd_tile(tx, ty);
+  xcd_tile(tx, ty, pr.group);
   const int p0 = tx * T::BP, q0 = ty * T::BQ;
   const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
   const int rbeg = split * r_split;
@@ -508,9 +510,18 @@ static BCfg bselect_default(int kind, int P, int Q, int R) {
 }
 
 #ifdef OPFUSE_TUNING
-// Tuning builds only: OPFUSE_BF16_CFG="tile,S" overrides the bf16 tiling.
+// Tuning builds only: OPFUSE_BF16_CFG="tile,S" overrides the bf16 tiling;
+// OPFUSE_BF16_WG_S=S the split of the weight gradients alone.
 static BCfg bselect(int kind, int P, int Q, int R) {
   const char* e = getenv("OPFUSE_BF16_CFG");
+  const char* wgs = getenv("OPFUSE_BF16_WG_S");
+  if (!e && wgs && (kind == EPI_WGRAD || kind == EPI_WGRAD_BF)) {
+    BCfg c = bselect_default(kind, P, Q, R);
+    const int S = std::max(1, atoi(wgs)), BR = kBTileBR[c.tile];
+    c.r_split = ((R + S - 1) / S + BR - 1) / BR * BR;
+    c.S = (R + c.r_split - 1) / c.r_split;
+    return c;
+  }
   if (!e) return bselect_default(kind, P, Q, R);
   int t = 1, S = 1;
   sscanf(e, "%d,%d", &t, &S);
@@ -572,6 +583,8 @@ static hipError_t blaunch_kind(const BCfg& c, const GemmProblem& pr, const EpiAr
     case BTI_128x128R64: return blaunch_t<BT128x128R64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case BTI_128x256R32: return blaunch_t<BT128x256R32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case BTI_256x128: return blaunch_t<BT256x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case BTI_256x256W8: return blaunch_t<BT256x256W8, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case BTI_256x256W4: return blaunch_t<BT256x256W4, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
 #endif
     default: return blaunch_t<BT64x64, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
   }
@@ -608,6 +621,7 @@ hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr_in, const EpiArgs& e
 #ifdef OPFUSE_TUNING
   // Tuning builds only: read a forward's A operand as bf16 (timing only).
   if (kind == EPI_FWD && getenv("OPFUSE_TUNE_ABF")) pr.a_bf16 = 1;
+  if (getenv("OPFUSE_BF16_GROUP")) pr.group = atoi(getenv("OPFUSE_BF16_GROUP"));
 #endif
   if ((pr.a_bf16 && kind != EPI_FWD) || pr.conv) return hipErrorInvalidValue;
   BCfg c = bselect(kind, pr.P, pr.Q, pr.R);

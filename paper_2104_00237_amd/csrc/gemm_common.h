@@ -50,7 +50,7 @@ __device__ __forceinline__ float bload1(rsrc_t r, uint32_t off) {
 // fetches only the operand rows and columns of its block instead of nearly
 // all of both operands.  Grids whose tile counts do not factor that way keep
 // the plain order.  Every tile is still computed exactly once.
-__device__ __forceinline__ void xcd_tile(int& tx, int& ty) {
+__device__ __forceinline__ void xcd_tile(int& tx, int& ty, int group = 0) {
   const int gx = gridDim.x, gy = gridDim.y;
   tx = blockIdx.x;
   ty = blockIdx.y;
@@ -68,6 +68,14 @@ __device__ __forceinline__ void xcd_tile(int& tx, int& ty) {
   const int sy = 8 / sx, bw = gx / sx, bh = gy / sy;
   const int lin = blockIdx.x + gx * blockIdx.y;
   const int xcd = lin & 7, j = lin >> 3;            // j < bw * bh
+  if (group > 0 && bh % group == 0) {
+    // strips of `group` block rows, each walked column by column: the tiles an
+    // XCD runs at once form squares that share their operand panels in L2
+    const int strip = j / (group * bw), k = j % (group * bw);
+    tx = (xcd % sx) * bw + k / group;
+    ty = (xcd / sx) * bh + strip * group + k % group;
+    return;
+  }
   tx = (xcd % sx) * bw + j % bw;
   ty = (xcd / sx) * bh + j / bw;
 }

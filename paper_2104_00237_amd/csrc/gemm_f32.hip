@@ -789,6 +789,16 @@ static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
   if (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) {
     if (R <= 128 && ntiles(TI_128x128, P, Q) >= 1024) return make_cfg(TI_128x128, P, Q, R, 1, 1);
     if (R <= 1024 && ntiles(TI_32x32, P, Q) >= 512) return make_cfg(TI_32x32, P, Q, R, 1, 1);
+    // A very long reduction onto few outputs (the pixel rows of a 1x1
+    // convolution, 65k-400k rows onto a few hundred weights): up to 256
+    // splits, on 64x32 tiles when P > 32 so that the B operand is read once per
+    // 64 output rows (measured on MI355X at 401408 x 96 x 16: 70 us, 139 us
+    // with 32x32 tiles and at most 64 splits).
+    if (R >= 65536) return make_cfg(P > 32 ? TI_64x32 : TI_32x32, P, Q, R, 1024, 256);
+    // Many tiles over a moderate reduction (a 1x1 head of 1280 x 320 over 1568
+    // rows): 64x32 tiles, split to about 2048 workgroups (31.9 us, 42.5 us
+    // unsplit on 32x32 tiles).
+    if (R >= 1024 && ntiles(TI_32x32, P, Q) >= 256) return make_cfg(TI_64x32, P, Q, R, 2048, 16);
   }
   if (P <= 64 && ntiles(TI_64x64, P, Q) >= 64) return make_cfg(TI_64x64, P, Q, R, 1024, 8);
   // Larger outputs: the biggest tile that still gives one workgroup per CU; no
