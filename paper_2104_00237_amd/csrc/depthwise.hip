@@ -6,13 +6,13 @@
 // nine neighbour reads of a pixel come from L1/L2.
 //
 // Filter gradient: dW[ky,kx,c] = sum over (n,h,w) of dy[n,h,w,c] *
-// x[n,h+ky-1,w+kx-1,c], db[c] = sum of dy[n,h,w,c].  Pass 1 splits the pixels
-// over S slices; each workgroup takes CB channels (CB from 16, 32, 48, 64,
-// whichever pads C least; one channel per thread group, or CB / 4 channel
-// quads when C % 4 == 0 and the tensors are 16-byte aligned) and writes the
-// ten per-channel sums of its slice, each the in-order sum of 16 pixel streams
-// that both kernels partition and order alike.  S is sized so that the grid
-// fills the chip (the small late layers get slices of a few dozen pixels).
+// x[n,h+ky-1,w+kx-1,c], db[c] = sum of dy[n,h,w,c].  Pass 1 splits the output
+// pixels, in units of one column over up to 16 rows, over S slices; each
+// workgroup takes CB channels (CB from 16, 32, 48, 64, whichever pads C least;
+// one channel per thread group, or CB / 4 channel quads when C % 4 == 0 and
+// the tensors are 16-byte aligned) and writes the ten per-channel sums of its
+// slice, each the in-order sum of 16 unit streams that both kernels partition
+// and order alike.  S is sized so that the grid fills the chip.
 // Pass 2 adds the S slices of each sum: L lanes (a power of two up to 64) take
 // consecutive runs of slices, each in slice order, and the run sums are added
 // in lane order; it then either writes dW / db (eager) or applies the
@@ -98,31 +98,95 @@ __global__ __launch_bounds__(256) void dw_dgrad_kernel(const float* __restrict__
   dx[i] = act_prev == OF_ACT_NONE ? acc : __fmul_rn(acc, act_grad(act_prev, prev[i]));
 }
 
-// Pass 1: workgroup (channel block, slice) sums its slice's pixels for cb
-// channels (4 * cb threads).  Each channel's pixels are split into 16 streams
-// (stream u takes the slice's pixels u, u + 16, u + 32, ... in order) whose
-// sums are then added in stream order: the same partition and order as the
+// Pass 1: workgroup (channel block, slice) sums its slice's output pixels for
+// cb channels (4 * cb threads).  The pixels are taken in units: one column wo
+// of one image over up to DW_SEG consecutive output rows, unit
+// u = (n * Wo + wo) * nseg + seg.  A slice's units are split into 16 streams
+// (stream j takes the slice's units j, j + 16, j + 32, ... in order) whose sums
+// are then added in stream order: the same partition and order as the
 // four-channel kernel below, so a shape gives the same bits whichever of the
 // two runs.  Thread (channel, sub) keeps the streams sub, sub + 4, sub + 8 and
 // sub + 12.  The stream sums meet in LDS, [16][10][cb] floats.
-template <int S>
-__device__ __forceinline__ void dw_wgrad_pixel(const float* __restrict__ dy,
-                                               const float* __restrict__ x, const DwShape& s,
-                                               int p, int c, float (&acc)[DW_TAPS]) {
-  const int col = p % s.Wo, t = p / s.Wo, row = t % s.Ho, n = t / s.Ho;
-  const float g = dy[p * s.C + c];
+//
+// Within a unit the rows are walked top to bottom with the window's three
+// input rows of three taps held in registers, so each row step loads only the
+// input rows it has not seen yet (one at stride 1, two at stride 2) and the
+// output gradient, instead of all nine taps.
+constexpr int DW_SEG = 16;
+
+__device__ __forceinline__ float dwv_load(const float* p, float) { return *p; }
+__device__ __forceinline__ float4 dwv_load(const float* p, float4) { return ld4(p); }
+__device__ __forceinline__ float dwv_fma(float a, float b, float c) { return __fmaf_rn(a, b, c); }
+__device__ __forceinline__ float4 dwv_fma(float4 a, float4 b, float4 c) {
+  return make_float4(__fmaf_rn(a.x, b.x, c.x), __fmaf_rn(a.y, b.y, c.y), __fmaf_rn(a.z, b.z, c.z),
+                     __fmaf_rn(a.w, b.w, c.w));
+}
+__device__ __forceinline__ float dwv_add(float a, float b) { return __fadd_rn(a, b); }
+__device__ __forceinline__ float4 dwv_add(float4 a, float4 b) {
+  return make_float4(__fadd_rn(a.x, b.x), __fadd_rn(a.y, b.y), __fadd_rn(a.z, b.z),
+                     __fadd_rn(a.w, b.w));
+}
+__device__ __forceinline__ void dwv_zero(float& v) { v = 0.f; }
+__device__ __forceinline__ void dwv_zero(float4& v) { v = make_float4(0.f, 0.f, 0.f, 0.f); }
+
+// Unit u's contribution to the ten sums of channel c (V = float) or of the
+// channel quad from c (V = float4).  A tap outside the input (zero padding)
+// contributes nothing, as in the forward.
+template <int S, class V>
+__device__ __forceinline__ void dw_wgrad_unit(const float* __restrict__ dy,
+                                              const float* __restrict__ x, const DwShape& s,
+                                              int nseg, int u, int c, V (&acc)[DW_TAPS]) {
+  const int seg = u % nseg, t = u / nseg, wo = t % s.Wo, n = t / s.Wo;
+  const int h0 = seg * DW_SEG, h1 = min(s.Ho, h0 + DW_SEG);
+  bool cv[3];
+  int wc[3];
 #pragma unroll
-  for (int ky = 0; ky < 3; ++ky) {
-    const int hh = row * S + ky - 1;
-    const bool rin = hh >= 0 && hh < s.H;
+  for (int kx = 0; kx < 3; ++kx) {
+    const int ww = wo * S + kx - 1;
+    cv[kx] = ww >= 0 && ww < s.W;
+    wc[kx] = cv[kx] ? ww : 0;
+  }
+  V win[3][3];
+  bool rv[3];
+  auto load_row = [&](int hh, V (&r)[3], bool& ok) {
+    ok = hh >= 0 && hh < s.H;
+    const float* base = x + ((int64_t)n * s.H + (ok ? hh : 0)) * s.W * s.C + c;
 #pragma unroll
     for (int kx = 0; kx < 3; ++kx) {
-      const int ww = col * S + kx - 1;
-      if (rin && ww >= 0 && ww < s.W)
-        acc[ky * 3 + kx] = __fmaf_rn(g, x[((n * s.H + hh) * s.W + ww) * s.C + c], acc[ky * 3 + kx]);
+      if (ok && cv[kx]) r[kx] = dwv_load(base + (int64_t)wc[kx] * s.C, V{});
+      else dwv_zero(r[kx]);
     }
+  };
+  load_row(h0 * S - 1, win[0], rv[0]);
+  load_row(h0 * S, win[1], rv[1]);
+  load_row(h0 * S + 1, win[2], rv[2]);
+  for (int ho = h0; ho < h1; ++ho) {
+    if (ho > h0) {
+      if (S == 1) {
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          win[0][kx] = win[1][kx];
+          win[1][kx] = win[2][kx];
+        }
+        rv[0] = rv[1];
+        rv[1] = rv[2];
+        load_row(ho + 1, win[2], rv[2]);
+      } else {
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) win[0][kx] = win[2][kx];
+        rv[0] = rv[2];
+        load_row(2 * ho, win[1], rv[1]);
+        load_row(2 * ho + 1, win[2], rv[2]);
+      }
+    }
+    const V g = dwv_load(dy + (((int64_t)n * s.Ho + ho) * s.Wo + wo) * s.C + c, V{});
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < 3; ++kx)
+        if (rv[ky] && cv[kx]) acc[ky * 3 + kx] = dwv_fma(g, win[ky][kx], acc[ky * 3 + kx]);
+    acc[9] = dwv_add(acc[9], g);
   }
-  acc[9] = __fadd_rn(acc[9], g);
 }
 
 // The 16 stream sums of each of the 10 * cb outputs, added in stream order.
@@ -141,24 +205,23 @@ template <int S>
 __global__ __launch_bounds__(256) void dw_wgrad_partial_kernel(const float* __restrict__ dy,
                                                                const float* __restrict__ x,
                                                                float* __restrict__ part,
-                                                               DwShape s, int per_slice, int cb) {
+                                                               DwShape s, int per_slice, int cb,
+                                                               int nseg) {
   extern __shared__ float red[];   // [16][DW_TAPS][cb]
   const int cl = threadIdx.x % cb, sub = threadIdx.x / cb;
   const int c = blockIdx.x * cb + cl;
-  const int P = s.N * s.Ho * s.Wo;  // output pixels
-  const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
+  const int U = s.N * s.Wo * nseg;  // units
+  const int u0 = blockIdx.y * per_slice, u1 = min(U, u0 + per_slice);
   float acc[4][DW_TAPS];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int k = 0; k < DW_TAPS; ++k) acc[j][k] = 0.f;
   if (c < s.C) {
-    for (int p = p0 + sub; p < p1; p += 16) {
-      dw_wgrad_pixel<S>(dy, x, s, p, c, acc[0]);
-      if (p + 4 < p1) dw_wgrad_pixel<S>(dy, x, s, p + 4, c, acc[1]);
-      if (p + 8 < p1) dw_wgrad_pixel<S>(dy, x, s, p + 8, c, acc[2]);
-      if (p + 12 < p1) dw_wgrad_pixel<S>(dy, x, s, p + 12, c, acc[3]);
-    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      for (int u = u0 + sub + 4 * j; u < u1; u += 16)
+        dw_wgrad_unit<S, float>(dy, x, s, nseg, u, c, acc[j]);
   }
 #pragma unroll
   for (int j = 0; j < 4; ++j)
@@ -243,40 +306,25 @@ __global__ __launch_bounds__(256) void dw_dgrad4_kernel(const float* __restrict_
   st4(dx + (int64_t)i * 4, acc);
 }
 
-// Pass 1, four channels per thread: cb / 4 channel quads x 16 pixel streams
+// Pass 1, four channels per thread: cb / 4 channel quads x 16 unit streams
 // per workgroup.
 template <int S>
 __global__ __launch_bounds__(256) void dw_wgrad_partial4_kernel(const float* __restrict__ dy,
                                                                 const float* __restrict__ x,
                                                                 float* __restrict__ part,
-                                                                DwShape s, int per_slice, int cb) {
+                                                                DwShape s, int per_slice, int cb,
+                                                                int nseg) {
   extern __shared__ float red[];   // [16][DW_TAPS][cb]
   const int nq = cb / 4;
   const int q = threadIdx.x % nq, sub = threadIdx.x / nq;
   const int c = blockIdx.x * cb + q * 4;
-  const int P = s.N * s.Ho * s.Wo;  // output pixels
-  const int p0 = blockIdx.y * per_slice, p1 = min(P, p0 + per_slice);
+  const int U = s.N * s.Wo * nseg;  // units
+  const int u0 = blockIdx.y * per_slice, u1 = min(U, u0 + per_slice);
   float4 acc[DW_TAPS];
 #pragma unroll
   for (int k = 0; k < DW_TAPS; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
   if (c < s.C) {
-    for (int p = p0 + sub; p < p1; p += 16) {
-      const int col = p % s.Wo, t = p / s.Wo, row = t % s.Ho, n = t / s.Ho;
-      const float4 g = ld4(dy + p * s.C + c);
-#pragma unroll
-      for (int ky = 0; ky < 3; ++ky) {
-        const int hh = row * S + ky - 1;
-        const bool rin = hh >= 0 && hh < s.H;
-#pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          const int ww = col * S + kx - 1;
-          if (rin && ww >= 0 && ww < s.W)
-            acc[ky * 3 + kx] = fma4(g, ld4(x + ((n * s.H + hh) * s.W + ww) * s.C + c), acc[ky * 3 + kx]);
-        }
-      }
-      acc[9] = make_float4(__fadd_rn(acc[9].x, g.x), __fadd_rn(acc[9].y, g.y),
-                           __fadd_rn(acc[9].z, g.z), __fadd_rn(acc[9].w, g.w));
-    }
+    for (int u = u0 + sub; u < u1; u += 16) dw_wgrad_unit<S, float4>(dy, x, s, nseg, u, c, acc);
   }
 #pragma unroll
   for (int k = 0; k < DW_TAPS; ++k) {
@@ -372,14 +420,17 @@ int dw_cb(const of_conv_desc& d) {
   }
   return best;
 }
-// Pixel slices of pass 1: enough workgroups for about 1024 threads per compute
-// unit, each slice at least 32 pixels (two per stream).
+// Units of pass 1 (one column of one image over up to DW_SEG output rows).
+int dw_nseg(const of_conv_desc& d) { return (int)((dw_out(d.H, dw_stride(d)) + DW_SEG - 1) / DW_SEG); }
+int64_t dw_units(const of_conv_desc& d) { return d.N * dw_out(d.W, dw_stride(d)) * dw_nseg(d); }
+// Unit slices of pass 1: enough workgroups for about 1024 threads per compute
+// unit, each slice at least one unit per stream.
 int dw_slices(const of_conv_desc& d) {
-  const int64_t P = dw_out_pixels(d);
+  const int64_t U = dw_units(d);
   const int cb = dw_cb(d);
   const int64_t nblk = (d.C + cb - 1) / cb;
   const int64_t want = std::max<int64_t>(1, (256 * 1024 / (4 * cb)) / nblk);
-  return (int)std::max<int64_t>(1, std::min<int64_t>((P + 31) / 32, want));
+  return (int)std::max<int64_t>(1, std::min<int64_t>((U + 15) / 16, want));
 }
 // Lanes per element of pass 2: runs of about 4 slices, at most a wave.
 int dw_lanes(int S) {
@@ -445,9 +496,10 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
                            float* db, int accumulate, const of_param* W, const of_param* b,
                            const float* gW, const float* gb, const OptK* o, void* ws,
                            hipStream_t stream) {
-  const int nsl = dw_slices(d);   // pixel slices of pass 1
-  const int64_t P = dw_out_pixels(d);
-  const int per = (int)((P + nsl - 1) / nsl);
+  const int nsl = dw_slices(d);   // unit slices of pass 1
+  const int64_t U = dw_units(d);
+  const int per = (int)((U + nsl - 1) / nsl);
+  const int nseg = dw_nseg(d);
   const int cb = dw_cb(d);
   const int nblk = (int)((d.C + cb - 1) / cb);
   const size_t lds = (size_t)16 * DW_TAPS * cb * sizeof(float);
@@ -457,17 +509,17 @@ hipError_t launch_dw_wgrad(const of_conv_desc& d, const float* dy, const float* 
   if (d.C % 4 == 0 && aligned16(dy) && aligned16(x)) {
     if (two)
       hipLaunchKernelGGL(dw_wgrad_partial4_kernel<2>, grid, block, lds, stream, dy, x, part,
-                         dw_shape(d), per, cb);
+                         dw_shape(d), per, cb, nseg);
     else
       hipLaunchKernelGGL(dw_wgrad_partial4_kernel<1>, grid, block, lds, stream, dy, x, part,
-                         dw_shape(d), per, cb);
+                         dw_shape(d), per, cb, nseg);
   } else {
     if (two)
       hipLaunchKernelGGL(dw_wgrad_partial_kernel<2>, grid, block, lds, stream, dy, x, part,
-                         dw_shape(d), per, cb);
+                         dw_shape(d), per, cb, nseg);
     else
       hipLaunchKernelGGL(dw_wgrad_partial_kernel<1>, grid, block, lds, stream, dy, x, part,
-                         dw_shape(d), per, cb);
+                         dw_shape(d), per, cb, nseg);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
