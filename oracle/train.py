@@ -352,7 +352,7 @@ def new_model(cfg, init=None, seed=0):
 
 
 def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=None,
-        snapshots=()):
+        snapshots=(), on_step=None):
     """Train workload `cfg` for `steps` steps under `ordering` in float64.
 
     Returns a dict: losses, eval_loss, params / m / v (float64 arrays by name),
@@ -362,6 +362,8 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
     snapshots {t: state after step t (t = 0: the initial state)} for t in
     `snapshots` -- params / m / v copies, step counters, the gradient the
     update of step t consumed and min_sqrt_vhat up to step t (eager ordering).
+    on_step: optional callable given each finished step's index (progress
+    reports of long runs; it sees nothing of the arithmetic).
     """
     steps = cfg["steps"] if steps is None else steps
     model = new_model(cfg, init, seed)
@@ -406,6 +408,8 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
                     min_vhat[k] = np.minimum(min_vhat[k], r) if k in min_vhat else r
         if t in snapshots:
             snaps[t] = snap()
+        if on_step is not None:
+            on_step(t)
     updated_before_flush = [op.updated for op, _, _ in model.nodes]
     if ordering == "ff":
         model.flush()

@@ -20,3 +20,13 @@ def gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     return torch.device("cuda:0")
+
+
+@pytest.fixture
+def progress(capsys):
+    """Report a long test's steps as they finish, past pytest's output capture
+    (a run that prints nothing for minutes is taken to be hung)."""
+    def say(msg):
+        with capsys.disabled():
+            print(msg, flush=True)
+    return say

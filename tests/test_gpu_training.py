@@ -125,7 +125,7 @@ def _mismatch(st, loss, cand_loss, cand, cfg, start, teach):
 
 @pytest.mark.timeout(1200)
 @pytest.mark.parametrize("name,starts", WINDOWS)
-def test_windowed_parity_full_size(gpu, name, starts):
+def test_windowed_parity_full_size(gpu, progress, name, starts):
     """Full-size workloads, whose K-step trajectory is chaotic in float32 (Adam's
     first steps move eps-dominated elements by O(lr), which shifts later ReLU
     decisions).  The GPU restarts from the oracle's state after step s (rounded to
@@ -144,10 +144,11 @@ def test_windowed_parity_full_size(gpu, name, starts):
     cfg = get_config(name)
     last = max(starts) + 1
     want = set(starts) | {s - 1 for s in starts if s > 0}
-    print(f"{name}: oracle, {last} steps", flush=True)
-    ref = oracle.run(cfg, "eager", steps=last, snapshots=want)
+    progress(f"{name}: oracle, {last} steps")
+    ref = oracle.run(cfg, "eager", steps=last, snapshots=want,
+                     on_step=lambda t: progress(f"{name}: oracle step {t} done"))
     for s in starts:
-        print(f"{name}: window {s} -> {s + 1}", flush=True)
+        progress(f"{name}: window {s} -> {s + 1}")
         results = {}
         for o in ("eager", "ff", "bf"):
             tr = Trainer(cfg, make_params(cfg), gpu)
@@ -185,6 +186,8 @@ def test_windowed_parity_full_size(gpu, name, starts):
                     why.setdefault(o, []).append((len(flips), msg))
             if len(matched) == len(results):
                 break
+        progress(f"{name} step {s + 1}: matched candidates "
+                 f"{ {o: len(f) for o, f in matched.items()} }")
         print(f"{name} step {s + 1}: matched candidates", {o: len(f) for o, f in matched.items()},
               flush=True)
         for o in set(results) - set(matched):
@@ -326,7 +329,7 @@ def _tblock_orderings(torch, gpu, cfg, start, prev=None):
     return out
 
 
-def _tblock_check(cfg, out, start, ref, losses):
+def _tblock_check(cfg, out, start, ref, losses, say=print):
     """bf16 parity of one AdamW step: loss, m and v within 2e-2 (max-norm
     relative), the values within 2e-2, and the update element by element
     (check_update) against the oracle and against AdamW applied to the GPU's own
@@ -352,31 +355,32 @@ def _tblock_check(cfg, out, start, ref, losses):
                                 undetermined=u, teacher=teach[k])
             und.append(n / ref["params"][k].size)
             worst_m, worst_u = max(worst_m, rm), max(worst_u, r)
-        print(f"tblock12 {o} step {ref['step'][k]}: loss {loss[0]:.6f} (oracle {losses[0]:.6f}), "
-              f"largest relative error of m {worst_m:.2e}, of the update {worst_u:.2e}; "
-              f"elements left to the own-gradient rule: median {np.median(und):.2%}, "
-              f"max {np.max(und):.2%} of a tensor", flush=True)
+        say(f"tblock12 {o} step {ref['step'][k]}: loss {loss[0]:.6f} (oracle {losses[0]:.6f}), "
+            f"largest relative error of m {worst_m:.2e}, of the update {worst_u:.2e}; "
+            f"elements left to the own-gradient rule: median {np.median(und):.2%}, "
+            f"max {np.max(und):.2%} of a tensor")
     for k in ref["params"]:
         np.testing.assert_array_equal(out["bf"][0]["params"][k], out["eager"][0]["params"][k])
         np.testing.assert_array_equal(out["bf"][0]["v"][k], out["eager"][0]["v"][k])
 
 
 @pytest.mark.timeout(600)
-def test_tblock_full_size_first_step(gpu):
+def test_tblock_full_size_first_step(gpu, progress):
     """The 12-block bf16 Transformer stack at 4096 tokens, hidden 1024, FFN 4096:
     the first AdamW step under each ordering against the oracle's first step,
     and backward-fusion bit for bit equal to eager."""
     import torch
     cfg = get_config("tblock12")
-    print("tblock12: oracle step 1", flush=True)
+    progress("tblock12: oracle step 1")
     ref = oracle.run(cfg, "eager", steps=1, snapshots={0})
     start = ref["snapshots"][0]
+    progress("tblock12: step 1 on the GPU, three orderings")
     out = _tblock_orderings(torch, gpu, cfg, start)
-    _tblock_check(cfg, out, start, ref, ref["losses"])
+    _tblock_check(cfg, out, start, ref, ref["losses"], say=progress)
 
 
 @pytest.mark.timeout(1200)
-def test_tblock_full_size_later_step(gpu):
+def test_tblock_full_size_later_step(gpu, progress):
     """tblock12 at full size, one-step window at a later AdamW step: every
     ordering restarts from the oracle's state after step 5 (forward-fusion from
     step 4 with step 5's gradient pending) and takes step 6, where the moments
@@ -384,10 +388,12 @@ def test_tblock_full_size_later_step(gpu):
     import torch
     cfg = get_config("tblock12")
     s = 5
-    print(f"tblock12: oracle, {s + 1} steps", flush=True)
-    ref = oracle.run(cfg, "eager", steps=s + 1, snapshots={s - 1, s})
+    progress(f"tblock12: oracle, {s + 1} steps")
+    ref = oracle.run(cfg, "eager", steps=s + 1, snapshots={s - 1, s},
+                     on_step=lambda t: progress(f"tblock12: oracle step {t} done"))
+    progress(f"tblock12: step {s + 1} on the GPU, three orderings")
     out = _tblock_orderings(torch, gpu, cfg, ref["snapshots"][s], prev=ref["snapshots"][s - 1])
-    _tblock_check(cfg, out, ref["snapshots"][s], ref, ref["losses"][s:])
+    _tblock_check(cfg, out, ref["snapshots"][s], ref, ref["losses"][s:], say=progress)
 
 
 def _vgg_search(cfg, state, t, st, loss, what):
