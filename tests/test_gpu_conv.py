@@ -44,6 +44,9 @@ SHAPES = [  # N, H, W, C, Cout
     (2, 4, 4, 3, 8), (2, 6, 10, 3, 64), (1, 5, 7, 16, 24), (2, 8, 8, 40, 48),
     (3, 4, 4, 64, 36), (2, 2, 2, 512, 512), (128, 32, 32, 3, 64), (128, 16, 16, 64, 128),
     (16, 8, 8, 128, 256), (16, 4, 4, 256, 512), (32, 2, 2, 512, 512),
+    # a 3-channel stem of at most 32 filters over 65k pixels or more (its own tiling:
+    # 256x32 forward tiles, a weight gradient split 256 ways), ragged filter count
+    (6, 107, 107, 3, 29),
 ]
 
 
@@ -104,7 +107,8 @@ SGD = dict(kind="sgd", lr=0.1, momentum=0.9, weight_decay=5e-4)
 
 
 @pytest.mark.parametrize("N,H,W,C,Co", [(2, 6, 10, 3, 64), (2, 8, 8, 40, 48), (128, 32, 32, 3, 64),
-                                        (16, 4, 4, 256, 512), (32, 2, 2, 512, 512)])
+                                        (16, 4, 4, 256, 512), (32, 2, 2, 512, 512),
+                                        (6, 107, 107, 3, 29)])
 def test_conv_wgrad_fused(env, N, H, W, C, Co):
     """Backward-fusion for a convolution: the filter-gradient contraction's epilogue
     applies SGD with momentum (the policy pi_2) to W and b.  Checked against the

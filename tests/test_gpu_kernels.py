@@ -50,6 +50,11 @@ SHAPES = [  # (M, N, K): tails in every dimension, split reductions, tiny and wi
     (100, 50, 3000), (200, 30, 2050),
     # at most 64 rows against a wide weight: ragged columns and reduction splits
     (33, 1030, 2052), (17, 600, 4000), (1, 2048, 1024),
+    # tall, narrow products (1x1 convolutions over pixel rows): narrow forward and
+    # data-gradient tiles; weight gradients over 65k+ rows split up to 256 ways
+    (70001, 23, 37), (66000, 45, 17), (20000, 150, 30), (17000, 20, 200),
+    # many weight-gradient tiles over a moderate reduction: split 64x32 tiles
+    (1500, 600, 500),
 ]
 
 
@@ -202,7 +207,9 @@ def test_elementwise_fused_update(env, kind, rows):
 
 
 @pytest.mark.parametrize("M,N,K", [(72, 168, 200), (256, 1024, 1024), (64, 520, 520), (33, 10, 27),
-                                   (300, 70, 257)])
+                                   (300, 70, 257),
+                                   # 65k+ rows: split up to 256 ways, reduced with the update
+                                   (70001, 23, 37), (66000, 45, 17), (1500, 600, 500)])
 @pytest.mark.parametrize("kind", ["sgd", "adam"] + FIG7)
 def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     """Backward-fusion (Alg. 3): dgrad with the old W, then the update in the wgrad
@@ -257,7 +264,9 @@ def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
 @pytest.mark.parametrize("M,N,K", [(72, 168, 200), (256, 1024, 1024), (64, 520, 520), (33, 10, 27),
                                    (256, 300, 130), (1, 8, 4),
                                    # a wide weight and at most 64 rows: split reductions
-                                   (64, 2048, 4096), (33, 1030, 2052), (17, 600, 4000)])
+                                   (64, 2048, 4096), (33, 1030, 2052), (17, 600, 4000),
+                                   # a tall, narrow forward (256x32 tiles)
+                                   (70001, 23, 37)])
 @pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"] + FIG7)
 def test_fwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
     """Forward-fusion (Alg. 2): the pending update is applied while W is loaded and
