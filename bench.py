@@ -501,8 +501,9 @@ def depthwise_stack(torch, batch, steps, warmup):
 
 
 def hbm_ceiling(torch, nbytes=1 << 30, reps=20):
-    """Read and copy rates of the library's streaming kernels over `nbytes`
-    (copy: nbytes read and nbytes written), GB/s of bytes moved."""
+    """Read, copy and in-place read-modify-write rates of the library's
+    streaming kernels over `nbytes` (copy and read-modify-write: nbytes read and
+    nbytes written), GB/s of bytes moved."""
     from paper_2104_00237_amd import _lib as L
     n = nbytes // 4
     src = torch.ones(n, device="cuda:0")
@@ -510,7 +511,8 @@ def hbm_ceiling(torch, nbytes=1 << 30, reps=20):
     s = torch.cuda.current_stream()
     out = {}
     for name, mode, moved in (("read_GBps", L.OF_STREAM_READ, nbytes),
-                              ("copy_GBps", L.OF_STREAM_COPY, 2 * nbytes)):
+                              ("copy_GBps", L.OF_STREAM_COPY, 2 * nbytes),
+                              ("rmw_GBps", L.OF_STREAM_RMW, 2 * nbytes)):
         for _ in range(3):
             L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), n, 0, s.cuda_stream)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -802,6 +804,7 @@ def main():
     out["hbm_ceiling"] = ceil
     if roof["bound"] == "hbm":
         roof["frac_of_measured_copy_rate"] = round(roof["achieved"] / ceil["copy_GBps"], 4)
+        roof["frac_of_measured_rmw_rate"] = round(roof["achieved"] / ceil["rmw_GBps"], 4)
     for name in [w for w in args.extra_workloads.split(",") if w and w != args.workload]:
         out.setdefault("extra_workloads", {})[name] = extra_workload(torch, name, args.steps,
                                                                      args.warmup)

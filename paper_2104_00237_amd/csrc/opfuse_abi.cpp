@@ -613,14 +613,18 @@ of_status of_linear_bwd_merged_static(const of_linear_desc* d, const float* dz, 
 
 of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
                         void* stream) {
-  REQUIRE(mode == OF_STREAM_READ || mode == OF_STREAM_COPY, OF_EINVAL,
-          "mode %d is neither OF_STREAM_READ nor OF_STREAM_COPY", (int)mode);
-  REQUIRE(src && dst, OF_EINVAL, "src and dst are required");
+  REQUIRE(mode == OF_STREAM_READ || mode == OF_STREAM_COPY || mode == OF_STREAM_RMW, OF_EINVAL,
+          "mode %d is not OF_STREAM_READ, OF_STREAM_COPY or OF_STREAM_RMW", (int)mode);
+  REQUIRE(dst && (src || mode == OF_STREAM_RMW), OF_EINVAL,
+          "dst is required, and src unless the mode is OF_STREAM_RMW");
   REQUIRE(n >= 4 && n % 4 == 0, OF_EINVAL, "n must be a positive multiple of 4 (got %lld)",
           (long long)n);
   REQUIRE(blocks >= 0 && blocks <= 65535, OF_EINVAL, "blocks must be in [0, 65535]");
-  REQUIRE(aligned16(src) && (mode == OF_STREAM_READ ? al4(dst) : aligned16(dst)), OF_EALIGN,
-          "src (and dst when copying) must be 16-byte aligned");
+  if (mode == OF_STREAM_RMW)
+    REQUIRE(aligned16(dst), OF_EALIGN, "dst must be 16-byte aligned");
+  else
+    REQUIRE(aligned16(src) && (mode == OF_STREAM_READ ? al4(dst) : aligned16(dst)), OF_EALIGN,
+            "src (and dst when copying) must be 16-byte aligned");
   return hip_status(hbm_stream_launch(mode, src, dst, n, blocks, (hipStream_t)stream),
                     "of_hbm_stream launch");
 }

@@ -1,5 +1,5 @@
-// HBM streaming probes: the read and read+write rates this device achieves
-// with plain coalesced 128-bit accesses.  They give the achievable ceiling
+// HBM streaming probes: the read, copy and in-place read-modify-write rates
+// this device achieves with plain coalesced 128-bit accesses.  They give the achievable ceiling
 // that the parameter-bound kernels (the fused and merged updates, which
 // stream W and the optimizer state once) are measured against, beside the
 // published 8 TB/s.  Not part of the paper's method.
@@ -61,6 +61,24 @@ __global__ __launch_bounds__(256) void stream_copy_kernel(const v4f* __restrict_
   }
 }
 
+// In place: every element read, incremented and written back.
+template <int U>
+__global__ __launch_bounds__(256) void stream_rmw_kernel(v4f* __restrict__ dst, int64_t n4) {
+  const int64_t stride = (int64_t)gridDim.x * 256 * U;
+  int64_t i = (int64_t)blockIdx.x * 256 * U + threadIdx.x;
+  for (; i + (U - 1) * 256 < n4; i += stride) {
+    v4f v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(dst + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < U; ++u) __builtin_nontemporal_store(v[u] + 1.f, dst + i + u * 256);
+  }
+  for (int u = 0; u < U; ++u) {
+    const int64_t j = i + u * 256;
+    if (j < n4) dst[j] = dst[j] + 1.f;
+  }
+}
+
 }  // namespace
 
 hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, int blocks,
@@ -70,6 +88,9 @@ hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, 
   if (mode == 0)
     hipLaunchKernelGGL(stream_read_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
                        reinterpret_cast<const v4f*>(src), n4, dst);
+  else if (mode == 2)
+    hipLaunchKernelGGL(stream_rmw_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
+                       reinterpret_cast<v4f*>(dst), n4);
   else
     hipLaunchKernelGGL(stream_copy_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
                        reinterpret_cast<const v4f*>(src), reinterpret_cast<v4f*>(dst), n4);

@@ -331,6 +331,18 @@ def test_avgpool_validation(lib):
     assert _status(L.of_avgpool_bwd, FAKE, FAKE + 1, 2, 49, 8, FAKE, None) == L.OF_EALIGN
 
 
+def test_hbm_stream_validation(lib):
+    """The streaming probe: modes, required pointers and alignment are checked
+    before any launch; the read-modify-write mode takes no source."""
+    assert _status(L.of_hbm_stream, 3, FAKE, FAKE, 1024, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_COPY, None, FAKE, 1024, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW, None, None, 1024, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW, None, FAKE, 1022, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW, None, FAKE + 4, 1024, 0, None) == L.OF_EALIGN
+    assert _status(L.of_hbm_stream, L.OF_STREAM_COPY, FAKE, FAKE + 4, 1024, 0, None) == L.OF_EALIGN
+    assert _status(L.of_hbm_stream, L.OF_STREAM_READ, FAKE, FAKE, 1024, 70000, None) == L.OF_EINVAL
+
+
 def test_operand_size_limit(lib):
     """Operand tiles are addressed with 32-bit byte offsets from the tile's
     first element: every linear entry point rejects an operand matrix of 2 GiB

@@ -382,3 +382,23 @@ def test_mse(env, M, D):
     torch.cuda.synchronize()
     assert abs(loss.item() - loss_ref) <= TOL * abs(loss_ref)
     assert rel(DY.cpu().numpy(), dy_ref) <= TOL
+
+
+@pytest.mark.parametrize("n,blocks", [(4, 0), (4100, 3), (1 << 20, 0)])
+def test_hbm_stream_probes(env, n, blocks):
+    """The streaming probes behind the measured HBM ceilings do what they time:
+    a copy equals its source, the read-modify-write adds 1 to every element in
+    place, and a read writes nothing but possibly one float."""
+    torch, L, dev = env
+    src = torch.arange(n, dtype=torch.float32, device=dev)
+    dst = torch.full((n,), -1.0, device=dev)
+    L.of_hbm_stream(L.OF_STREAM_COPY, src.data_ptr(), dst.data_ptr(), n, blocks, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    L.of_hbm_stream(L.OF_STREAM_RMW, None, dst.data_ptr(), n, blocks, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src + 1)
+    sink = torch.full((n,), -1.0, device=dev)
+    L.of_hbm_stream(L.OF_STREAM_READ, src.data_ptr(), sink.data_ptr(), n, blocks, 0)
+    torch.cuda.synchronize()
+    assert int((sink != -1.0).sum()) <= 1
