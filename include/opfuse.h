@@ -602,6 +602,11 @@ int64_t of_layernorm_partial_rows(int64_t M);
  * of_elementwise_fused_update with g_rows = G (backward- or forward-fusion:
  * the gradient vector is never stored) or to of_reduce_rows (eager).
  * dx must not alias dy or x.
+ * The two halves may be computed by separate calls, e.g. on two streams
+ * (both only read dy and x): dx == NULL computes only the partials (gamma and
+ * dres are then not read and may be NULL); dgamma_rows == dbeta_rows == NULL
+ * computes only dx.  Results are bit-identical to one call.  OF_EINVAL if
+ * all three outputs are NULL or only one of the partials is.
  */
 of_status of_layernorm_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
                            const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,

@@ -94,11 +94,12 @@ __global__ __launch_bounds__(256) void ln_bwd_param_kernel(
   if (j >= D) return;
   const int64_t r0 = grp * rows_per_group, r1 = std::min(M, r0 + rows_per_group);
   float sg = 0.f, sb = 0.f;
-  // loads of 8 rows are issued before their (in-order) accumulation
-  for (int64_t rb = r0; rb < r1; rb += 8) {
-    float d[8], xv[8], mu[8], rs[8];
+  // loads of 16 rows are issued before their (in-order) accumulation; the
+  // row statistics are the same for every lane
+  for (int64_t rb = r0; rb < r1; rb += 16) {
+    float d[16], xv[16], mu[16], rs[16];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < 16; ++k) {
       const int64_t r = rb + k;
       const bool ok = r < r1;
       d[k] = ok ? dy[r * D + j] : 0.f;
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(256) void ln_bwd_param_kernel(
       rs[k] = ok ? rstd[r] : 0.f;
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < 16; ++k) {
       if (rb + k < r1) {
         const float xh = __fmul_rn(__fsub_rn(xv[k], mu[k]), rs[k]);
         sg = __fmaf_rn(d[k], xh, sg);
@@ -183,6 +184,12 @@ __global__ __launch_bounds__(256) void ln_bwd_dx_vec_kernel(
   if (row >= M) return;
   const float mu = mean[row], rs = rstd[row];
   float xh[NPL][4], g[NPL][4];
+  float4 rv[NPL];   // the residual gradient, loaded before the row sums
+#pragma unroll
+  for (int c = 0; c < NPL; ++c) {
+    const int64_t j = 4 * (lane + 64 * c);
+    rv[c] = dres && j < D ? ld4(dres + row * D + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   float s1 = 0.f, s2 = 0.f;
 #pragma unroll
   for (int c = 0; c < NPL; ++c) {
@@ -211,7 +218,7 @@ __global__ __launch_bounds__(256) void ln_bwd_dx_vec_kernel(
       for (int e = 0; e < 4; ++e)
         o[e] = __fmul_rn(rs, __fsub_rn(__fsub_rn(g[c][e], c1), __fmul_rn(xh[c][e], c2)));
       if (dres) {
-        const float4 r = ld4(dres + row * D + j);
+        const float4 r = rv[c];
         o[0] = __fadd_rn(r.x, o[0]); o[1] = __fadd_rn(r.y, o[1]);
         o[2] = __fadd_rn(r.z, o[2]); o[3] = __fadd_rn(r.w, o[3]);
       }
@@ -249,22 +256,27 @@ hipError_t launch_ln_fwd(const float* x, int64_t M, int64_t D, const float* gamm
 hipError_t launch_ln_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
                          const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
                          float* dgamma_rows, float* dbeta_rows, hipStream_t s) {
-  const dim3 g((unsigned)((M + 3) / 4));
-  switch (ln_npl(D, {dy, x, gamma, dres, dx})) {
-    case 1: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<1>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
-    case 2: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<2>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
-    case 4: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<4>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
-    case 8: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<8>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
-    default:
-      hipLaunchKernelGGL(ln_bwd_dx_kernel, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx);
+  if (dx) {
+    const dim3 g((unsigned)((M + 3) / 4));
+    switch (ln_npl(D, {dy, x, gamma, dres, dx})) {
+      case 1: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<1>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
+      case 2: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<2>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
+      case 4: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<4>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
+      case 8: hipLaunchKernelGGL(ln_bwd_dx_vec_kernel<8>, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx); break;
+      default:
+        hipLaunchKernelGGL(ln_bwd_dx_kernel, g, dim3(256), 0, s, dy, x, mean, rstd, gamma, dres, M, D, dx);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int64_t G = ln_partial_rows(M);
-  const int64_t rpg = (M + G - 1) / G;
-  hipLaunchKernelGGL(ln_bwd_param_kernel, dim3((unsigned)((D + 255) / 256), (unsigned)G), dim3(256),
-                     0, s, dy, x, mean, rstd, M, D, rpg, dgamma_rows, dbeta_rows);
-  return hipGetLastError();
+  if (dgamma_rows) {
+    const int64_t G = ln_partial_rows(M);
+    const int64_t rpg = (M + G - 1) / G;
+    hipLaunchKernelGGL(ln_bwd_param_kernel, dim3((unsigned)((D + 255) / 256), (unsigned)G),
+                       dim3(256), 0, s, dy, x, mean, rstd, M, D, rpg, dgamma_rows, dbeta_rows);
+    return hipGetLastError();
+  }
+  return hipSuccess;
 }
 
 __global__ __launch_bounds__(256) void reduce_rows_kernel(const float* __restrict__ src,
@@ -272,14 +284,14 @@ __global__ __launch_bounds__(256) void reduce_rows_kernel(const float* __restric
                                                           float* __restrict__ dst) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
-  // loads of 8 rows are issued before their (in-order) accumulation
+  // loads of 32 rows are issued before their (in-order) accumulation
   float s = src[i];
-  for (int64_t r0 = 1; r0 < rows; r0 += 8) {
-    float v[8];
+  for (int64_t r0 = 1; r0 < rows; r0 += 32) {
+    float v[32];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = r0 + k < rows ? src[(r0 + k) * ld + i] : 0.f;
+    for (int k = 0; k < 32; ++k) v[k] = r0 + k < rows ? src[(r0 + k) * ld + i] : 0.f;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
+    for (int k = 0; k < 32; ++k)
       if (r0 + k < rows) s = __fadd_rn(s, v[k]);
   }
   dst[i] = s;

@@ -988,10 +988,14 @@ int64_t of_layernorm_partial_rows(int64_t M) { return M >= 1 ? ln_partial_rows(M
 of_status of_layernorm_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
                            const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
                            float* dgamma_rows, float* dbeta_rows, void* stream) {
-  REQUIRE(dy && x && mean && rstd && gamma && dx && dgamma_rows && dbeta_rows, OF_EINVAL,
-          "dy, x, mean, rstd, gamma, dx, dgamma_rows and dbeta_rows are required");
+  REQUIRE(dy && x && mean && rstd, OF_EINVAL, "dy, x, mean and rstd are required");
+  REQUIRE(!dgamma_rows == !dbeta_rows, OF_EINVAL,
+          "dgamma_rows and dbeta_rows are given together or both NULL");
+  REQUIRE(dx || dgamma_rows, OF_EINVAL, "nothing to compute: dx and the partials are all NULL");
+  REQUIRE(!dx || gamma, OF_EINVAL, "gamma is required for dx");
   REQUIRE(M >= 1 && D >= 1, OF_EINVAL, "M and D must be >= 1");
-  REQUIRE(dx != dy && dx != x, OF_EINVAL, "dx must not alias dy or x (both are read again)");
+  REQUIRE(!dx || (dx != dy && dx != x), OF_EINVAL,
+          "dx must not alias dy or x (both are read again)");
   REQUIRE(al4(dy) && al4(x) && al4(mean) && al4(rstd) && al4(gamma) && al4(dres) && al4(dx) &&
               al4(dgamma_rows) && al4(dbeta_rows),
           OF_EALIGN, "fp32 pointers must be 4-byte aligned");

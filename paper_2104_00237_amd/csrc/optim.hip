@@ -88,17 +88,20 @@ __global__ __launch_bounds__(256) void rows_update_kernel(of_param p, const floa
   opt_prepare(o);
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= p.numel) return;
-  // loads of 8 rows are issued before their (in-order) accumulation
+  // The optimizer state is loaded before the row sum, and the loads of 32
+  // rows are issued before their (in-order) accumulation: the kernel is a
+  // chain of load round trips, as few as possible.
+  const OptState1 st = opt_load1(o, p, i);
   float s = g[i];
-  for (int64_t r0 = 1; r0 < rows; r0 += 8) {
-    float v[8];
+  for (int64_t r0 = 1; r0 < rows; r0 += 32) {
+    float v[32];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = r0 + k < rows ? g[(r0 + k) * ld + i] : 0.f;
+    for (int k = 0; k < 32; ++k) v[k] = r0 + k < rows ? g[(r0 + k) * ld + i] : 0.f;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
+    for (int k = 0; k < 32; ++k)
       if (r0 + k < rows) s = __fadd_rn(s, v[k]);
   }
-  update1(o, p, s, i);
+  opt_apply1(o, p, st, s, i);
 }
 
 hipError_t launch_rows_update(const of_param& p, const float* g, int64_t rows, int64_t ld,

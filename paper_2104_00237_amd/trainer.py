@@ -395,16 +395,24 @@ class LayerNormOp:
     def two_sets(self):
         return False
 
-    def bwd(self, tr, dy, x, mu, rs, dres, dx):
-        """dx (+ dres) and the parameter-gradient row partials."""
-        L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx,
-                           self.g.rows.data_ptr(), self.b.rows.data_ptr(), tr._s())
+    def bwd(self, tr, dy, x, mu, rs, dres, dx, side=None):
+        """dx (+ dres) on the main stream and the parameter-gradient row partials:
+        on the stream `side` when given (already ordered after dy; both launches
+        only read dy and x), else right after dx."""
+        if side is None:
+            L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx,
+                               self.g.rows.data_ptr(), self.b.rows.data_ptr(), tr._s())
+            return
+        L.of_layernorm_bwd(dy, x, mu, rs, None, None, self.M, self.D, None,
+                           self.g.rows.data_ptr(), self.b.rows.data_ptr(), side)
+        L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx, None,
+                           None, tr._s())
 
-    def reduce(self, tr):
+    def reduce(self, tr, stream=None):
         """Eager: materialise the gradient vectors from the row partials."""
         for p in self.params:
             L.of_reduce_rows(p.rows.data_ptr(), p.rows.shape[0], 0, p.numel, p.g.data_ptr(),
-                             tr._s())
+                             stream if stream is not None else tr._s())
 
 
 def _ff_prologue(tr, op):
@@ -638,8 +646,13 @@ class TBlockNet:
 
     Every tensor a later kernel reads is kept per block, and so is every
     gradient buffer, so the side stream's fused updates of block b never race
-    with the main stream's back-propagation through the blocks below.
+    with the main stream's back-propagation through the blocks below.  In the
+    plain backward (eager and forward-fusion) the LayerNorm parameter-gradient
+    partials run on the side stream, so those steps join it before their
+    optimizer step, clipping norm or next forward.
     """
+
+    eager_side = True
 
     def __init__(self, tr, cfg, pb):
         self.tr = tr
@@ -776,17 +789,30 @@ class TBlockNet:
 
     def _ln_bwd(self, op, dy, x, mu, rs, dres, dx, fused, done):
         tr = self.tr
-        tr._t0("ln_bwd", tr.stream, op)
-        op.bwd(tr, dy, x, mu, rs, dres, dx)
-        tr._t1("ln_bwd", tr.stream)
         if fused:
-            # the row partials are complete: update gamma and beta on the side stream
+            # Backward-fusion's side stream already carries the fused weight
+            # gradients of the linears, and the step's end waits for it: the
+            # partials stay on the main stream after dx (which reads the old
+            # gamma, the dependency rule of Alg. 3), only the update of gamma
+            # and beta goes to the side stream.
+            tr._t0("ln_bwd", tr.stream, op)
+            op.bwd(tr, dy, x, mu, rs, dres, dx)
+            tr._t1("ln_bwd", tr.stream)
             _side_after_main(tr)
             for p in op.params:
                 _update(tr, p, tr.side.cuda_stream)
             done(op)
-        elif tr.eager_reduce:
-            op.reduce(tr)
+            return
+        # Plain backward: the partials, and after them the eager reduce, run on
+        # the side stream beside the data gradient; the step joins it before
+        # the optimizer step (eager) or the next forward (forward-fusion), and
+        # no later kernel of the step writes dy, x or the row statistics.
+        _side_after_main(tr)
+        tr._t0("ln_bwd", tr.stream, op)
+        op.bwd(tr, dy, x, mu, rs, dres, dx, side=tr.side.cuda_stream)
+        tr._t1("ln_bwd", tr.stream)
+        if tr.eager_reduce:
+            op.reduce(tr, tr.side.cuda_stream)
 
     def _backward(self, x, fused, done):
         d = self.d

@@ -214,6 +214,13 @@ def test_bf16_shadow_and_norm_validation(lib):
                    None) == L.OF_EALIGN
     assert _status(L.of_layernorm_bwd, FAKE, FAKE + 64, FAKE, FAKE, FAKE, None, 4, 8, FAKE, FAKE,
                    FAKE, None) == L.OF_EINVAL   # dx aliases dy
+    # the halves may be computed apart, but not nothing and not one partial alone
+    assert _status(L.of_layernorm_bwd, FAKE, FAKE + 64, FAKE, FAKE, FAKE, None, 4, 8, None, None,
+                   None, None) == L.OF_EINVAL
+    assert _status(L.of_layernorm_bwd, FAKE, FAKE + 64, FAKE, FAKE, FAKE, None, 4, 8, FAKE + 128,
+                   FAKE + 256, None, None) == L.OF_EINVAL
+    assert _status(L.of_layernorm_bwd, FAKE, FAKE + 64, FAKE, FAKE, None, None, 4, 8, FAKE + 128,
+                   None, None, None) == L.OF_EINVAL   # dx needs gamma
     assert L.of_layernorm_partial_rows(4096) == 64 and L.of_layernorm_partial_rows(1) == 1
     assert _status(L.of_reduce_rows, FAKE, 2, 3, 8, FAKE, None) == L.OF_EINVAL   # ld < n
     assert _status(L.of_add, FAKE, None, 8, FAKE, None) == L.OF_EINVAL

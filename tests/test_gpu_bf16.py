@@ -215,6 +215,14 @@ def test_layernorm(env, M, D):
     DBR = torch.full((rows, D), float("nan"), device=dev)
     L.of_layernorm_bwd(DY.data_ptr(), X.data_ptr(), MU.data_ptr(), RS.data_ptr(), G.data_ptr(),
                        RES.data_ptr(), M, D, DX.data_ptr(), DGR.data_ptr(), DBR.data_ptr(), 0)
+    # the two halves computed by separate calls: the same bits
+    DX2 = torch.full((M, D), float("nan"), device=dev)
+    DGR2 = torch.full((rows, D), float("nan"), device=dev)
+    DBR2 = torch.full((rows, D), float("nan"), device=dev)
+    L.of_layernorm_bwd(DY.data_ptr(), X.data_ptr(), MU.data_ptr(), RS.data_ptr(), None, None, M,
+                       D, None, DGR2.data_ptr(), DBR2.data_ptr(), 0)
+    L.of_layernorm_bwd(DY.data_ptr(), X.data_ptr(), MU.data_ptr(), RS.data_ptr(), G.data_ptr(),
+                       RES.data_ptr(), M, D, DX2.data_ptr(), None, None, 0)
     DG = torch.empty(D, device=dev)
     DB = torch.empty(D, device=dev)
     L.of_reduce_rows(DGR.data_ptr(), rows, 0, D, DG.data_ptr(), 0)
@@ -227,6 +235,8 @@ def test_layernorm(env, M, D):
     assert rel(DB.cpu().numpy(), db) <= TOL
     # the row partials are what the fused update sums: their sum is the gradient
     assert rel(DGR.cpu().numpy().astype(np.float64).sum(0), dg) <= TOL
+    for a, b in ((DX2, DX), (DGR2, DGR), (DBR2, DBR)):
+        np.testing.assert_array_equal(a.cpu().numpy(), b.cpu().numpy())
 
 
 @pytest.mark.parametrize("n", [1, 7, 4096, 1 << 20])

@@ -12,7 +12,7 @@ from workloads import get_config, reduced_config, make_params, make_batch
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name", ["mlp3", "mlp8x1024", "mbv2"])
+@pytest.mark.parametrize("name", ["mlp3", "mlp8x1024", "mbv2", "tblock12"])
 @pytest.mark.parametrize("ordering", ["eager", "ff", "bf"])
 def test_graph_replays_match_steps(gpu, name, ordering):
     import torch
