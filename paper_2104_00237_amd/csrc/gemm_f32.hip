@@ -72,17 +72,21 @@ using T64x64 = Tile<64, 64, 16, 2, 2, 1, 4>;
 using T128x64 = Tile<128, 64, 16, 2, 2, 1, 4>;
 using T128x128 = Tile<128, 128, 16, 2, 2, 1, 3>;
 using T256x32 = Tile<256, 32, 16, 4, 1, 1, 3>;
+// 64 rows x 128 columns with the reduction layout of T64x32 (32-deep chunks,
+// each halved between two wavefronts): every output element takes the same
+// MFMA sequence as on T64x32, so results are identical to it bit for bit.
+using T64x128 = Tile<64, 128, 32, 1, 2, 2, 4>;
 
 // TI_32x32D, TI_32x32D8: 32x32 blocks with operands loaded straight into the
 // matrix-core registers by 4 or 8 wavefronts (gemm_direct_kernel; forward and
 // data gradient of linear layers only, the LDS-staged 32x32 tile elsewhere).
 enum TileId {
   TI_32x32 = 0, TI_64x32, TI_64x64, TI_128x64, TI_128x128, TI_256x32,
-  TI_32x32D, TI_32x32D8, TI_COUNT
+  TI_32x32D, TI_32x32D8, TI_64x128, TI_COUNT
 };
-static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256, 32, 32};
-static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32, 32, 32};
-static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16, 32, 32};
+static const int kTileBP[TI_COUNT] = {32, 64, 64, 128, 128, 256, 32, 32, 64};
+static const int kTileBQ[TI_COUNT] = {32, 32, 64, 64, 128, 32, 32, 32, 128};
+static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16, 32, 32, 32};
 
 
 // A BX (output dim) x BR (reduction) tile of one operand, held in registers as
@@ -319,7 +323,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   constexpr bool WG = (EPI == EPI_WGRAD || EPI == EPI_WGRAD_BF);
   // Forward-fusion also keeps the updated bias slice of its column tile.
   constexpr int SMEM = T::SMX + (EPI == EPI_FWD_FF ? T::BQ : 0);
-  static_assert(SMEM * 4 <= 64 * 1024, "LDS per workgroup");
+  static_assert(SMEM * 4 <= 160 * 1024, "LDS per workgroup");
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
   if constexpr (EPI == EPI_FWD) {
     if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
@@ -785,7 +789,15 @@ static GemmCfg select_cfg_default(int kind, int P, int Q, int R) {
   // row tile 0 stores it) and takes the plain forward's tiling.
   if (kind == EPI_FWD_FF)
     return P <= 64 ? make_cfg(ff_tile(P), P, Q, R, 1024, 8) : select_cfg_default(EPI_FWD, P, Q, R);
-  if (kind == EPI_FWD && P <= 64) return make_cfg(ff_tile(P), P, Q, R, 1024, 8);
+  if (kind == EPI_FWD && P <= 64) {
+    GemmCfg c = make_cfg(ff_tile(P), P, Q, R, 1024, 8);
+    // Between 33 and 64 rows, with enough columns to fill the chip: 64x128
+    // tiles with the same splits, whose sums equal the 64x32 tile's bit for
+    // bit; a third of the operand loads per flop (measured on MI355X at
+    // 64 x 8192 x 8192: 108 against 115 us).
+    if (P > 32 && ntiles(TI_64x128, P, Q) * c.S >= 256) c.tile = TI_64x128;
+    return c;
+  }
   if (kind == EPI_WGRAD || kind == EPI_WGRAD_BF) {
     // A short reduction onto a huge output (an 8192 x 8192 layer at 64 rows):
     // whole reductions on 64x64 tiles (measured on MI355X: plain 115 us, fused with
@@ -959,6 +971,21 @@ static hipError_t launch_kind(const GemmCfg& c, const GemmProblem& pr, const Epi
       if constexpr (EPI == EPI_FWD_FF) return hipErrorInvalidValue;
       else return launch_t<T128x128, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
     case TI_256x32: return launch_t<T256x32, EPI>(c, pr, ea, ws, vec_ops, vec_epi, s);
+    case TI_64x128:
+      // the plain forward of linear layers only (its fused counterpart keeps
+      // T64x32, whose sums it reproduces)
+      if constexpr (EPI == EPI_FWD) {
+        if (pr.conv) return hipErrorInvalidValue;
+        dim3 grid((pr.P + 63) / 64, (pr.Q + 127) / 128, c.S + c.cz);
+        if (vec_ops == 3)
+          hipLaunchKernelGGL((gemm_kernel<T64x128, EPI, 3, false>), grid, dim3(256), 0, s, pr, ea,
+                             c.r_split, (float*)ws, vec_epi);
+        else
+          hipLaunchKernelGGL((gemm_kernel<T64x128, EPI, 0, false>), grid, dim3(256), 0, s, pr, ea,
+                             c.r_split, (float*)ws, vec_epi);
+        return hipGetLastError();
+      }
+      return hipErrorInvalidValue;
     case TI_32x32D:
     case TI_32x32D8:
       // direct loads exist for the linear forward and data gradient; the same

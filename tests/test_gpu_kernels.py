@@ -265,6 +265,9 @@ def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
                                    (256, 300, 130), (1, 8, 4),
                                    # a wide weight and at most 64 rows: split reductions
                                    (64, 2048, 4096), (33, 1030, 2052), (17, 600, 4000),
+                                   # enough columns for the plain forward's 64x128 tiles
+                                   # (vector and scalar operand loads, ragged columns)
+                                   (64, 4096, 4096), (40, 4200, 2050),
                                    # a tall, narrow forward (256x32 tiles)
                                    (70001, 23, 37)])
 @pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"] + FIG7)
