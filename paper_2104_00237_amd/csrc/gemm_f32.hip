@@ -47,9 +47,14 @@ namespace opfuse {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_>
+template <int BP_, int BQ_, int BR_, int WP_, int WQ_, int WR_, int NS_, int PAD_ = 4>
 struct Tile {
   static constexpr int BP = BP_, BQ = BQ_, BR = BR_, WP = WP_, WQ = WQ_, WR = WR_;
+  // LDS row padding of the operand tiles (floats).  4 keeps rows 16-byte
+  // aligned for the vector stores of output-contiguous operands; a tile whose
+  // operands are both reduction-contiguous (stored one float at a time) may
+  // take 2, which spreads its transposing stores over all 64 banks.
+  static constexpr int PAD = PAD_;
   static constexpr int NS = NS_;  // operand chunks in the register ring
   static_assert(WP * WQ * WR == 4, "a workgroup is 4 wavefronts");
   static constexpr int WTP = BP / WP, WTQ = BQ / WQ;   // wavefront tile
@@ -57,7 +62,7 @@ struct Tile {
   static_assert(TP >= 1 && TQ >= 1 && WTP % 32 == 0 && WTQ % 32 == 0, "32x32 blocks");
   static constexpr int RW = BR / WR;                    // chunk rows per wavefront
   static_assert(RW % 2 == 0 && BR % 4 == 0, "k pairs");
-  static constexpr int LDA = BP + 4, LDB = BQ + 4;
+  static constexpr int LDA = BP + PAD, LDB = BQ + PAD;
   static constexpr int LDC = (WR * BP * (BQ + 4) * 4 <= 60 * 1024) ? BQ + 4 : BQ;
   static constexpr int SM_MAIN = 2 * BR * (LDA + LDB);
   static constexpr int SM_C = WR * BP * LDC;
@@ -75,7 +80,7 @@ using T256x32 = Tile<256, 32, 16, 4, 1, 1, 3>;
 // 64 rows x 128 columns with the reduction layout of T64x32 (32-deep chunks,
 // each halved between two wavefronts): every output element takes the same
 // MFMA sequence as on T64x32, so results are identical to it bit for bit.
-using T64x128 = Tile<64, 128, 32, 1, 2, 2, 4>;
+using T64x128 = Tile<64, 128, 32, 1, 2, 2, 4, 2>;
 
 // TI_32x32D, TI_32x32D8: 32x32 blocks with operands loaded straight into the
 // matrix-core registers by 4 or 8 wavefronts (gemm_direct_kernel; forward and
@@ -95,7 +100,7 @@ static const int kTileBR[TI_COUNT] = {32, 32, 16, 16, 16, 16, 32, 32, 32};
 // tile's first element; nx / nr are the valid extents from there (<= 0: none).
 // vec: 128-bit loads (base 16B aligned, strides and both extents' ends
 // multiples of 4 along the contiguous index).
-template <int BX, int BR, bool RC, bool VEC>
+template <int BX, int BR, bool RC, bool VEC, int PAD = 4>
 struct TileLoad {
   static constexpr int NV = BX * BR / 4;
   static constexpr int PER = (NV + 255) / 256;
@@ -110,7 +115,7 @@ struct TileLoad {
       int x, r;
       if (RC) { x = idx / (BR / 4); r = (idx % (BR / 4)) * 4; }
       else    { r = idx / (BX / 4); x = (idx % (BX / 4)) * 4; }
-      const bool live = idx < NV;
+      const bool live = NV % 256 == 0 || idx < NV;
       if constexpr (VEC) {
         const bool ok = live && x < nx && r < nr;
         const uint32_t off = ok ? (uint32_t)((x * s_x + r * s_r) * 4) : kOOB;
@@ -129,11 +134,12 @@ struct TileLoad {
   }
 
   __device__ __forceinline__ void store(float* lds, int tid) const {
-    constexpr int LD = BX + 4;
+    constexpr int LD = BX + PAD;
+    static_assert(RC || PAD % 4 == 0, "float4 stores need 16-byte aligned rows");
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int idx = tid + i * 256;
-      if (idx < NV) {
+      if (NV % 256 == 0 || idx < NV) {
         if (RC) {
           const int x = idx / (BR / 4), r = (idx % (BR / 4)) * 4;
           lds[(r + 0) * LD + x] = v[i].x;
@@ -324,6 +330,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   // Forward-fusion also keeps the updated bias slice of its column tile.
   constexpr int SMEM = T::SMX + (EPI == EPI_FWD_FF ? T::BQ : 0);
   static_assert(SMEM * 4 <= 160 * 1024, "LDS per workgroup");
+  static_assert(EPI != EPI_FWD_FF || T::PAD == 4, "the fused forward stages W with a pad of 4");
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
   if constexpr (EPI == EPI_FWD) {
     if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
@@ -407,11 +414,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   using ALoad = std::conditional_t<
       CONV && (EPI == EPI_FWD || EPI == EPI_FWD_FF || EPI == EPI_DGRAD),
       GatherLoad<T::BP, T::BR, true, VA, EPI == EPI_DGRAD ? G_DGRAD_A : G_FWD_A>,
-      TileLoad<T::BP, T::BR, A_RC, VA>>;
+      TileLoad<T::BP, T::BR, A_RC, VA, T::PAD>>;
   using BLoad = std::conditional_t<
       CONV && EPI == EPI_DGRAD, GatherLoad<T::BQ, T::BR, false, VB, G_DGRAD_B>,
       std::conditional_t<CONV && WG, GatherLoad<T::BQ, T::BR, false, VB, G_WGRAD_B>,
-                         TileLoad<T::BQ, T::BR, B_RC, VB>>>;
+                         TileLoad<T::BQ, T::BR, B_RC, VB, T::PAD>>>;
   ALoad la[NS];
   BLoad lb[(EPI == EPI_FWD_FF) ? 1 : NS];
   FFTileLoad<T::BQ, T::BR, VB> lf[(EPI == EPI_FWD_FF) ? NS : 1];
@@ -430,10 +437,102 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       lb[slot].load(pr.B, pr, pr.b_sq, pr.b_sr, q0, r0, nq, nr, tid);
   };
 
+  // One chunk's MFMAs on the operands in LDS buffer `buf`.
+  auto mfma_chunk = [&](const float* buf) {
+    const float* a_s = buf;
+    const float* b_s = buf + BOFF;
+#pragma unroll
+    for (int kk = 0; kk < T::RW; kk += 2) {
+      const int r = wr * T::RW + kk + (lane >> 5);
+      float a[T::TP], b[T::TQ];
+#pragma unroll
+      for (int i = 0; i < T::TP; ++i)
+        a[i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
+#pragma unroll
+      for (int j = 0; j < T::TQ; ++j)
+        b[j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
+#pragma unroll
+      for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TQ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  // The plain 64-row forward keeps the matrix cores fed across chunks (one
+  // wavefront per SIMD has nothing else to hide latency behind):
+  //  * every operand of chunk c is read from LDS first, into registers of
+  //    its own, so one LDS latency is exposed per chunk rather than one per
+  //    pair of reduction rows;
+  //  * chunk c+1 is stored to the other LDS buffer, and chunk c+NS's global
+  //    loads are issued, between chunk c's MFMAs;
+  //  * one barrier per chunk: buffer c&1 is written again (chunk c+2) only
+  //    after every wavefront passed the barrier that follows its reads.
+  // The MFMA sequence of each output is that of the loop further below.
+  constexpr bool PIPE = (EPI == EPI_FWD) && !CONV && std::is_same<T, T64x128>::value;
+  if constexpr (PIPE) {
+    constexpr int KS = T::RW / 2;
+    static_assert(ALoad::PER == 2 && BLoad::PER == 4 && KS == 8 && T::TP * T::TQ == 4,
+                  "the interleave below is written for this tile");
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      issue(s, s);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    la[0].store(smem, tid);
+    lb[0].store(smem + BOFF, tid);
+    __syncthreads();
+    for (int c0 = 0; c0 < nch; c0 += NS) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const int c = c0 + s;
+        const float* a_s = smem + (c & 1) * STAGE;
+        const float* b_s = a_s + BOFF;
+        float a[KS][T::TP], b[KS][T::TQ];
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+          const int r = wr * T::RW + 2 * k + (lane >> 5);
+#pragma unroll
+          for (int i = 0; i < T::TP; ++i)
+            a[k][i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
+#pragma unroll
+          for (int j = 0; j < T::TQ; ++j)
+            b[k][j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        issue(s, c + NS);   // slot s held chunk c, already in LDS
+        float* nbuf = smem + ((c + 1) & 1) * STAGE;
+        la[(s + 1) % NS].store(nbuf, tid);
+        lb[(s + 1) % NS].store(nbuf + BOFF, tid);
+        // Unconditional, so that the region has no branch: a chunk past the
+        // end holds zeros (its loads were out of range), and adding 0 leaves
+        // an accumulator that started at +0 unchanged bit for bit.
+#pragma unroll
+        for (int k = 0; k < KS; ++k)
+#pragma unroll
+          for (int i = 0; i < T::TP; ++i)
+#pragma unroll
+            for (int j = 0; j < T::TQ; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[k][i], b[k][j], acc[i][j], 0, 0, 0);
+        // 4 MFMAs, 1 global load, 2 LDS stores (two rows each), six times;
+        // then the last 8 MFMAs
+#pragma unroll
+        for (int g = 0; g < 6; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __syncthreads();
+      }
+    }
+  }
+
   // In-order prologue (the scheduling barriers keep chunk 0 oldest), so the
   // loop waits for one chunk at a time instead of draining the ring.
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s) {
+    if constexpr (PIPE) break;
     issue(s, s);
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -441,7 +540,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   // (after the loads above are in flight, so their latency hides this)
   if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
 
-  for (int c0 = 0; c0 < nch; c0 += NS) {
+  for (int c0 = 0; c0 < (PIPE ? 0 : nch); c0 += NS) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       const int c = c0 + s;
@@ -456,23 +555,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
       __syncthreads();
       if (c < nch) {
         const float* a_s = buf;
-        const float* b_s = buf + BOFF;
-#pragma unroll
-        for (int kk = 0; kk < T::RW; kk += 2) {
-          const int r = wr * T::RW + kk + (lane >> 5);
-          float a[T::TP], b[T::TQ];
-#pragma unroll
-          for (int i = 0; i < T::TP; ++i)
-            a[i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
-#pragma unroll
-          for (int j = 0; j < T::TQ; ++j)
-            b[j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
-#pragma unroll
-          for (int i = 0; i < T::TP; ++i)
-#pragma unroll
-            for (int j = 0; j < T::TQ; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
+        mfma_chunk(buf);
         if (do_db && tid < T::BP) {
           // Column sums of dZ for this tile's output rows, in reduction order.
 #pragma unroll 4
