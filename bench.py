@@ -503,22 +503,25 @@ def depthwise_stack(torch, batch, steps, warmup):
 def hbm_ceiling(torch, nbytes=1 << 30, reps=20):
     """Read, copy and in-place read-modify-write rates of the library's
     streaming kernels over `nbytes` (copy and read-modify-write: nbytes read and
-    nbytes written), GB/s of bytes moved."""
+    nbytes written; rmw3: three arrays of a third each, updated side by side as
+    W, m and v are), GB/s of bytes moved."""
     from paper_2104_00237_amd import _lib as L
     n = nbytes // 4
     src = torch.ones(n, device="cuda:0")
     dst = torch.empty_like(src)
     s = torch.cuda.current_stream()
     out = {}
-    for name, mode, moved in (("read_GBps", L.OF_STREAM_READ, nbytes),
-                              ("copy_GBps", L.OF_STREAM_COPY, 2 * nbytes),
-                              ("rmw_GBps", L.OF_STREAM_RMW, 2 * nbytes)):
+    n3 = n // 12 * 12
+    for name, mode, cnt, moved in (("read_GBps", L.OF_STREAM_READ, n, nbytes),
+                                   ("copy_GBps", L.OF_STREAM_COPY, n, 2 * nbytes),
+                                   ("rmw_GBps", L.OF_STREAM_RMW, n, 2 * nbytes),
+                                   ("rmw3_GBps", L.OF_STREAM_RMW3, n3, 8 * n3)):
         for _ in range(3):
-            L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), n, 0, s.cuda_stream)
+            L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), cnt, 0, s.cuda_stream)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(s)
         for _ in range(reps):
-            L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), n, 0, s.cuda_stream)
+            L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), cnt, 0, s.cuda_stream)
         e1.record(s)
         torch.cuda.synchronize()
         out[name] = round(moved * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
@@ -805,6 +808,7 @@ def main():
     if roof["bound"] == "hbm":
         roof["frac_of_measured_copy_rate"] = round(roof["achieved"] / ceil["copy_GBps"], 4)
         roof["frac_of_measured_rmw_rate"] = round(roof["achieved"] / ceil["rmw_GBps"], 4)
+        roof["frac_of_measured_rmw3_rate"] = round(roof["achieved"] / ceil["rmw3_GBps"], 4)
     for name in [w for w in args.extra_workloads.split(",") if w and w != args.workload]:
         out.setdefault("extra_workloads", {})[name] = extra_workload(torch, name, args.steps,
                                                                      args.warmup)

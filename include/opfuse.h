@@ -639,7 +639,10 @@ of_status of_mse_fwd_bwd(const float* y, const float* t, int64_t M, int64_t D, i
  * (OF_STREAM_READ: src is read, dst receives at most one float), the copy
  * rate (OF_STREAM_COPY: dst = src) or the in-place read-modify-write rate
  * (OF_STREAM_RMW: dst[i] += 1, src unused and may be NULL; the access pattern
- * of an optimizer update, which reads W, m, v and writes them back) this
+ * of an optimizer update, which reads W, m, v and writes them back; with
+ * OF_STREAM_RMW3 dst is three consecutive arrays of n/3 floats, n a multiple
+ * of 12, and each thread updates the same index of all three together, as
+ * an update of W, m and v does) this
  * device reaches with coalesced 128-bit non-temporal accesses, the achievable
  * ceiling beside the published peak for the kernels that stream parameters
  * and optimizer state.  src, dst: n floats of device memory, 16-byte aligned
@@ -647,7 +650,7 @@ of_status of_mse_fwd_bwd(const float* y, const float* t, int64_t M, int64_t D, i
  * workgroups of 256 threads (0: 2048).  Errors: OF_EINVAL, OF_EALIGN before
  * any launch.
  */
-enum { OF_STREAM_READ = 0, OF_STREAM_COPY = 1, OF_STREAM_RMW = 2 };
+enum { OF_STREAM_READ = 0, OF_STREAM_COPY = 1, OF_STREAM_RMW = 2, OF_STREAM_RMW3 = 3 };
 of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
                         void* stream);
 

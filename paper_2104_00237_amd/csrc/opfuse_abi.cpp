@@ -613,14 +613,20 @@ of_status of_linear_bwd_merged_static(const of_linear_desc* d, const float* dz, 
 
 of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
                         void* stream) {
-  REQUIRE(mode == OF_STREAM_READ || mode == OF_STREAM_COPY || mode == OF_STREAM_RMW, OF_EINVAL,
-          "mode %d is not OF_STREAM_READ, OF_STREAM_COPY or OF_STREAM_RMW", (int)mode);
-  REQUIRE(dst && (src || mode == OF_STREAM_RMW), OF_EINVAL,
-          "dst is required, and src unless the mode is OF_STREAM_RMW");
+  REQUIRE(mode == OF_STREAM_READ || mode == OF_STREAM_COPY || mode == OF_STREAM_RMW ||
+              mode == OF_STREAM_RMW3,
+          OF_EINVAL, "mode %d is not OF_STREAM_READ, OF_STREAM_COPY, OF_STREAM_RMW or OF_STREAM_RMW3",
+          (int)mode);
+  const bool rmw = mode == OF_STREAM_RMW || mode == OF_STREAM_RMW3;
+  REQUIRE(dst && (src || rmw), OF_EINVAL,
+          "dst is required, and src unless the mode is a read-modify-write");
   REQUIRE(n >= 4 && n % 4 == 0, OF_EINVAL, "n must be a positive multiple of 4 (got %lld)",
           (long long)n);
+  REQUIRE(mode != OF_STREAM_RMW3 || n % 12 == 0, OF_EINVAL,
+          "OF_STREAM_RMW3: n must be a multiple of 12 (three arrays of float4s; got %lld)",
+          (long long)n);
   REQUIRE(blocks >= 0 && blocks <= 65535, OF_EINVAL, "blocks must be in [0, 65535]");
-  if (mode == OF_STREAM_RMW)
+  if (rmw)
     REQUIRE(aligned16(dst), OF_EALIGN, "dst must be 16-byte aligned");
   else
     REQUIRE(aligned16(src) && (mode == OF_STREAM_READ ? al4(dst) : aligned16(dst)), OF_EALIGN,

@@ -1,4 +1,5 @@
 // HBM streaming probes: the read, copy and in-place read-modify-write rates
+// (one array, or three updated side by side)
 // this device achieves with plain coalesced 128-bit accesses.  They give the achievable ceiling
 // that the parameter-bound kernels (the fused and merged updates, which
 // stream W and the optimizer state once) are measured against, beside the
@@ -79,6 +80,39 @@ __global__ __launch_bounds__(256) void stream_rmw_kernel(v4f* __restrict__ dst, 
   }
 }
 
+// Three arrays of n3 float4s in place, element i of all three in the same
+// pass (the pattern of an update that reads W, m and v and writes them back).
+template <int U>
+__global__ __launch_bounds__(256) void stream_rmw3_kernel(v4f* __restrict__ a, int64_t n3) {
+  v4f* __restrict__ b = a + n3;
+  v4f* __restrict__ c = b + n3;
+  const int64_t stride = (int64_t)gridDim.x * 256 * U;
+  int64_t i = (int64_t)blockIdx.x * 256 * U + threadIdx.x;
+  for (; i + (U - 1) * 256 < n3; i += stride) {
+    v4f va[U], vb[U], vc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      va[u] = __builtin_nontemporal_load(a + i + u * 256);
+      vb[u] = __builtin_nontemporal_load(b + i + u * 256);
+      vc[u] = __builtin_nontemporal_load(c + i + u * 256);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      __builtin_nontemporal_store(va[u] + 1.f, a + i + u * 256);
+      __builtin_nontemporal_store(vb[u] + 1.f, b + i + u * 256);
+      __builtin_nontemporal_store(vc[u] + 1.f, c + i + u * 256);
+    }
+  }
+  for (int u = 0; u < U; ++u) {
+    const int64_t j = i + u * 256;
+    if (j < n3) {
+      a[j] = a[j] + 1.f;
+      b[j] = b[j] + 1.f;
+      c[j] = c[j] + 1.f;
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, int blocks,
@@ -91,6 +125,9 @@ hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, 
   else if (mode == 2)
     hipLaunchKernelGGL(stream_rmw_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
                        reinterpret_cast<v4f*>(dst), n4);
+  else if (mode == 3)
+    hipLaunchKernelGGL(stream_rmw3_kernel<kStreamUnroll / 2>, dim3(blocks), dim3(256), 0, stream,
+                       reinterpret_cast<v4f*>(dst), n4 / 3);
   else
     hipLaunchKernelGGL(stream_copy_kernel<kStreamUnroll>, dim3(blocks), dim3(256), 0, stream,
                        reinterpret_cast<const v4f*>(src), reinterpret_cast<v4f*>(dst), n4);

@@ -341,7 +341,11 @@ def test_avgpool_validation(lib):
 def test_hbm_stream_validation(lib):
     """The streaming probe: modes, required pointers and alignment are checked
     before any launch; the read-modify-write mode takes no source."""
-    assert _status(L.of_hbm_stream, 3, FAKE, FAKE, 1024, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, 4, FAKE, FAKE, 1024, 0, None) == L.OF_EINVAL
+    # three arrays of float4s: n a multiple of 12
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3, None, FAKE, 1024, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3, None, FAKE + 4, 1032, 0,
+                   None) == L.OF_EALIGN
     assert _status(L.of_hbm_stream, L.OF_STREAM_COPY, None, FAKE, 1024, 0, None) == L.OF_EINVAL
     assert _status(L.of_hbm_stream, L.OF_STREAM_RMW, None, None, 1024, 0, None) == L.OF_EINVAL
     assert _status(L.of_hbm_stream, L.OF_STREAM_RMW, None, FAKE, 1022, 0, None) == L.OF_EINVAL

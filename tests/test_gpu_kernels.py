@@ -401,6 +401,14 @@ def test_hbm_stream_probes(env, n, blocks):
     L.of_hbm_stream(L.OF_STREAM_RMW, None, dst.data_ptr(), n, blocks, 0)
     torch.cuda.synchronize()
     assert torch.equal(dst, src + 1)
+    # three arrays updated side by side: every element of the first 12*(n//12)
+    # gets +1, the rest is untouched
+    n3 = n // 12 * 12
+    if n3:
+        L.of_hbm_stream(L.OF_STREAM_RMW3, None, dst.data_ptr(), n3, blocks, 0)
+        torch.cuda.synchronize()
+        assert torch.equal(dst[:n3], src[:n3] + 2)
+        assert torch.equal(dst[n3:], src[n3:] + 1)
     sink = torch.full((n,), -1.0, device=dev)
     L.of_hbm_stream(L.OF_STREAM_READ, src.data_ptr(), sink.data_ptr(), n, blocks, 0)
     torch.cuda.synchronize()
