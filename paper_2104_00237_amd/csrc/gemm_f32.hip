@@ -459,8 +459,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     }
   };
 
-  // The plain 64-row forward keeps the matrix cores fed across chunks (one
-  // wavefront per SIMD has nothing else to hide latency behind):
+  // Pipelined main loop (every linear-layer contraction but the fused
+  // forward): the matrix cores stay fed across chunks, which matters most
+  // where one wavefront per SIMD has nothing else to hide latency behind.
   //  * every operand of chunk c is read from LDS first, into registers of
   //    its own, so one LDS latency is exposed per chunk rather than one per
   //    pair of reduction rows;
@@ -468,64 +469,81 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   //    loads are issued, between chunk c's MFMAs;
   //  * one barrier per chunk: buffer c&1 is written again (chunk c+2) only
   //    after every wavefront passed the barrier that follows its reads.
-  // The MFMA sequence of each output is that of the loop further below.
-  constexpr bool PIPE = (EPI == EPI_FWD) && !CONV && std::is_same<T, T64x128>::value;
+  // The MFMA sequence of each output, and the order of the bias-gradient
+  // sums, are those of the loop further below.
+  constexpr bool PIPE = (EPI != EPI_FWD_FF) && !CONV;
   if constexpr (PIPE) {
     constexpr int KS = T::RW / 2;
-    static_assert(ALoad::PER == 2 && BLoad::PER == 4 && KS == 8 && T::TP * T::TQ == 4,
-                  "the interleave below is written for this tile");
+    constexpr int NM = KS * T::TP * T::TQ;                  // MFMAs per chunk
+    constexpr int NLD = (VA ? 1 : 4) * ALoad::PER + (VB ? 1 : 4) * BLoad::PER;  // global loads
+    constexpr int NST = (A_RC ? 2 : 1) * ALoad::PER + (B_RC ? 2 : 1) * BLoad::PER;  // LDS stores
+    constexpr int NG = NM >= 8 ? NM / 4 - 1 : 1;           // interleave groups
+    constexpr int GL = (NLD + NG - 1) / NG, GS = (NST + NG - 1) / NG;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       issue(s, s);
       __builtin_amdgcn_sched_barrier(0);
     }
+    prefetch();
+    if (EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
     la[0].store(smem, tid);
     lb[0].store(smem + BOFF, tid);
     __syncthreads();
-    for (int c0 = 0; c0 < nch; c0 += NS) {
+    // Chunk c from slot s (s == c % NS, a constant after unrolling).
+    auto chunk = [&](const int c, const int s) {
+      const float* a_s = smem + (c & 1) * STAGE;
+      const float* b_s = a_s + BOFF;
+      float a[KS][T::TP], b[KS][T::TQ];
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int c = c0 + s;
-        const float* a_s = smem + (c & 1) * STAGE;
-        const float* b_s = a_s + BOFF;
-        float a[KS][T::TP], b[KS][T::TQ];
+      for (int k = 0; k < KS; ++k) {
+        const int r = wr * T::RW + 2 * k + (lane >> 5);
 #pragma unroll
-        for (int k = 0; k < KS; ++k) {
-          const int r = wr * T::RW + 2 * k + (lane >> 5);
+        for (int i = 0; i < T::TP; ++i)
+          a[k][i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
 #pragma unroll
-          for (int i = 0; i < T::TP; ++i)
-            a[k][i] = a_s[r * T::LDA + wp * T::WTP + i * 32 + (lane & 31)];
+        for (int j = 0; j < T::TQ; ++j)
+          b[k][j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
+      }
+      if (do_db && tid < T::BP) {
+        // Column sums of dZ for this tile's output rows, in reduction order.
+#pragma unroll 4
+        for (int r = 0; r < T::BR; ++r) dbsum = __fadd_rn(dbsum, a_s[r * T::LDA + tid]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      issue(s, c + NS);   // slot s held chunk c, already in LDS
+      float* nbuf = smem + ((c + 1) & 1) * STAGE;
+      la[(s + 1) % NS].store(nbuf, tid);
+      lb[(s + 1) % NS].store(nbuf + BOFF, tid);
+#pragma unroll
+      for (int k = 0; k < KS; ++k)
+#pragma unroll
+        for (int i = 0; i < T::TP; ++i)
 #pragma unroll
           for (int j = 0; j < T::TQ; ++j)
-            b[k][j] = b_s[r * T::LDB + wq * T::WTQ + j * 32 + (lane & 31)];
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        issue(s, c + NS);   // slot s held chunk c, already in LDS
-        float* nbuf = smem + ((c + 1) & 1) * STAGE;
-        la[(s + 1) % NS].store(nbuf, tid);
-        lb[(s + 1) % NS].store(nbuf + BOFF, tid);
-        // Unconditional, so that the region has no branch: a chunk past the
-        // end holds zeros (its loads were out of range), and adding 0 leaves
-        // an accumulator that started at +0 unchanged bit for bit.
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[k][i], b[k][j], acc[i][j], 0, 0, 0);
+      // 4 MFMAs, then a share of the global loads and of the LDS stores, in
+      // each group; the last MFMAs cover the stores' completion before the
+      // barrier and, after it, the next chunk's LDS reads
 #pragma unroll
-        for (int k = 0; k < KS; ++k)
-#pragma unroll
-          for (int i = 0; i < T::TP; ++i)
-#pragma unroll
-            for (int j = 0; j < T::TQ; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[k][i], b[k][j], acc[i][j], 0, 0, 0);
-        // 4 MFMAs, 1 global load, 2 LDS stores (two rows each), six times;
-        // then the last 8 MFMAs
-#pragma unroll
-        for (int g = 0; g < 6; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-        __syncthreads();
+      for (int g = 0; g < NG; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NM >= 8 ? 4 : NM, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, GL, 0);
+        __builtin_amdgcn_sched_group_barrier(0x200, GS, 0);
       }
+      if constexpr (NM >= 8) __builtin_amdgcn_sched_group_barrier(0x008, NM - 4 * NG, 0);
+      __syncthreads();
+    };
+    // Whole rounds of NS chunks without a branch between them, so each
+    // chunk's LDS reads can start among the previous chunk's last MFMAs; then
+    // the remainder.
+    const int nfull = nch / NS * NS;
+    for (int c0 = 0; c0 < nfull; c0 += NS) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) chunk(c0 + s, s);
     }
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (nfull + s < nch) chunk(nfull + s, s);
   }
 
   // In-order prologue (the scheduling barriers keep chunk 0 oldest), so the
@@ -536,9 +554,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     issue(s, s);
     __builtin_amdgcn_sched_barrier(0);
   }
-  prefetch();
-  // (after the loads above are in flight, so their latency hides this)
-  if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+  if constexpr (!PIPE) {
+    prefetch();
+    // (after the loads above are in flight, so their latency hides this)
+    if (EPI == EPI_FWD_FF || EPI == EPI_WGRAD_BF) opt_prepare(ea.opt);
+  }
 
   for (int c0 = 0; c0 < (PIPE ? 0 : nch); c0 += NS) {
 #pragma unroll
