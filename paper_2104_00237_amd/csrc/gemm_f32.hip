@@ -459,8 +459,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
     }
   };
 
-  // Pipelined main loop (every linear-layer contraction but the fused
-  // forward): the matrix cores stay fed across chunks, which matters most
+  // Pipelined main loop (every contraction but the fused forward, whose W
+  // tiles are updated between load and staging): the matrix cores stay fed
+  // across chunks, which matters most
   // where one wavefront per SIMD has nothing else to hide latency behind.
   //  * every operand of chunk c is read from LDS first, into registers of
   //    its own, so one LDS latency is exposed per chunk rather than one per
@@ -471,7 +472,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   //    after every wavefront passed the barrier that follows its reads.
   // The MFMA sequence of each output, and the order of the bias-gradient
   // sums, are those of the loop further below.
-  constexpr bool PIPE = (EPI != EPI_FWD_FF) && !CONV;
+  constexpr bool PIPE = (EPI != EPI_FWD_FF);
   if constexpr (PIPE) {
     constexpr int KS = T::RW / 2;
     constexpr int NM = KS * T::TP * T::TQ;                  // MFMAs per chunk
