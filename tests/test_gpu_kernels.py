@@ -268,6 +268,8 @@ def test_bwd_fused_matches_oracle_and_eager_bits(env, M, N, K, kind):
                                    # enough columns for the plain forward's 64x128 tiles
                                    # (vector and scalar operand loads, ragged columns)
                                    (64, 4096, 4096), (40, 4200, 2050),
+                                   # ragged columns and reduction on the vector path
+                                   (48, 4100, 4100),
                                    # a tall, narrow forward (256x32 tiles)
                                    (70001, 23, 37)])
 @pytest.mark.parametrize("kind", ["sgd", "adam", "adamw"] + FIG7)
