@@ -461,8 +461,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
 
   // Pipelined main loop (every contraction but the fused forward, whose W
   // tiles are updated between load and staging): the matrix cores stay fed
-  // across chunks, which matters most
-  // where one wavefront per SIMD has nothing else to hide latency behind.
+  // across chunks, which matters most where one wavefront per SIMD has
+  // nothing else to hide latency behind.
   //  * every operand of chunk c is read from LDS first, into registers of
   //    its own, so one LDS latency is exposed per chunk rather than one per
   //    pair of reduction rows;
