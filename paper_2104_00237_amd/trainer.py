@@ -395,18 +395,24 @@ class LayerNormOp:
     def two_sets(self):
         return False
 
-    def bwd(self, tr, dy, x, mu, rs, dres, dx, side=None):
-        """dx (+ dres) on the main stream and the parameter-gradient row partials:
-        on the stream `side` when given (already ordered after dy; both launches
-        only read dy and x), else right after dx."""
-        if side is None:
+    def bwd(self, tr, dy, x, mu, rs, dres, dx, side=None, params=True):
+        """dx (+ dres) on the main stream and, unless params is False, the
+        parameter-gradient row partials: on the stream `side` when given (already
+        ordered after dy; both launches only read dy and x), else in the same
+        call as dx."""
+        if side is None and params:
             L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx,
                                self.g.rows.data_ptr(), self.b.rows.data_ptr(), tr._s())
             return
-        L.of_layernorm_bwd(dy, x, mu, rs, None, None, self.M, self.D, None,
-                           self.g.rows.data_ptr(), self.b.rows.data_ptr(), side)
+        if params:
+            self.bwd_params(dy, x, mu, rs, side)
         L.of_layernorm_bwd(dy, x, mu, rs, self.g.w.data_ptr(), dres, self.M, self.D, dx, None,
                            None, tr._s())
+
+    def bwd_params(self, dy, x, mu, rs, stream):
+        """The parameter-gradient row partials alone, on `stream`."""
+        L.of_layernorm_bwd(dy, x, mu, rs, None, None, self.M, self.D, None,
+                           self.g.rows.data_ptr(), self.b.rows.data_ptr(), stream)
 
     def reduce(self, tr, stream=None):
         """Eager: materialise the gradient vectors from the row partials."""
@@ -649,7 +655,8 @@ class TBlockNet:
     with the main stream's back-propagation through the blocks below.  In the
     plain backward (eager and forward-fusion) the LayerNorm parameter-gradient
     partials run on the side stream, so those steps join it before their
-    optimizer step, clipping norm or next forward.
+    optimizer step, clipping norm or next forward; backward-fusion computes
+    them, and updates gamma and beta, on a second side stream.
     """
 
     eager_side = True
@@ -791,16 +798,25 @@ class TBlockNet:
         tr = self.tr
         if fused:
             # Backward-fusion's side stream already carries the fused weight
-            # gradients of the linears, and the step's end waits for it: the
-            # partials stay on the main stream after dx (which reads the old
-            # gamma, the dependency rule of Alg. 3), only the update of gamma
-            # and beta goes to the side stream.
+            # gradients of the linears, so the partials and the update of gamma
+            # and beta take a second one: the partials once dy exists, the
+            # update once dx has read the old gamma (the dependency rule of
+            # Alg. 3).  The step's end joins it (measured on tblock12:
+            # 10.67 -> 10.53 ms per step against the partials on the main
+            # stream after dx).
+            side2 = tr.side2()
+            ev = torch.cuda.Event()
+            ev.record(tr.stream)
+            side2.wait_event(ev)
+            op.bwd_params(dy, x, mu, rs, side2.cuda_stream)
             tr._t0("ln_bwd", tr.stream, op)
-            op.bwd(tr, dy, x, mu, rs, dres, dx)
+            op.bwd(tr, dy, x, mu, rs, dres, dx, side=None, params=False)
             tr._t1("ln_bwd", tr.stream)
-            _side_after_main(tr)
+            ev = torch.cuda.Event()
+            ev.record(tr.stream)
+            side2.wait_event(ev)
             for p in op.params:
-                _update(tr, p, tr.side.cuda_stream)
+                _update(tr, p, side2.cuda_stream)
             done(op)
             return
         # Plain backward: the partials, and after them the eager reduce, run on
@@ -1203,6 +1219,8 @@ class Trainer:
         self.capturing = False
         self.stream = torch.cuda.current_stream(self.device)
         self.side = device_stream(self.device, "side")
+        self._side2 = None   # a second side stream, made on first use
+        self.side2_done = torch.cuda.Event()
         self.side_done = torch.cuda.Event()
         # Whether backward-fusion puts any update on the side stream: a chain of
         # light layers updates in stream order and needs no join at the step's
@@ -1223,6 +1241,13 @@ class Trainer:
 
     def _s(self):
         return self.stream.cuda_stream
+
+    def side2(self):
+        """A second side stream (backward-fusion's LayerNorm updates), one per
+        device like the first; a step that used it joins it at its end."""
+        if self._side2 is None:
+            self._side2 = device_stream(self.device, "side2")
+        return self._side2
 
     def _advance(self, ps):
         """Next update index for parameters ps; sets the optimizer argument the
@@ -1376,6 +1401,9 @@ class Trainer:
             # the next forward reads parameters the side stream updated
             self.side_done.record(self.side)
             self.stream.wait_event(self.side_done)
+        if self._side2 is not None:
+            self.side2_done.record(self._side2)
+            self.stream.wait_event(self.side2_done)
 
     # ------------------------------------------------------------- graphs
     def capture(self, x, y, ordering):
