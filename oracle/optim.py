@@ -110,6 +110,29 @@ def clip_scale(grads, max_norm):
     return (1.0 if s > 1.0 else s), norm
 
 
+# Elements per slice when a policy is applied to a large tensor (see apply).
+SLICE = 1 << 20
+
+
+def apply_policy(policy, theta, g, m, v, step, hyper):
+    """policy(theta, g, m, v, step) over whole tensors.  Every policy above is
+    element-wise (each output element depends on the same element of the inputs
+    and on scalars only), so a large tensor is taken in slices of SLICE elements:
+    the same operations on every element, with the temporaries small enough to
+    stay in cache.  The result is identical to one call on the whole tensor."""
+    if theta.size <= SLICE:
+        return policy(theta, g, m, v, step, **hyper)
+    outs = (np.empty_like(theta), np.empty_like(m), np.empty_like(v))
+    flat_in = [np.ascontiguousarray(a).reshape(-1) for a in (theta, g, m, v)]
+    flat_out = [o.reshape(-1) for o in outs]
+    for s in range(0, theta.size, SLICE):
+        sl = slice(s, s + SLICE)
+        res = policy(*(a[sl] for a in flat_in), step, **hyper)
+        for o, r in zip(flat_out, res):
+            o[sl] = r
+    return outs
+
+
 def apply(param, hyper):
     """Execute the optimizer of one parameter: consume its accumulated gradient.
 
@@ -118,7 +141,8 @@ def apply(param, hyper):
     """
     policy = POLICIES[hyper["kind"]]
     step = param.step + 1
-    param.value, param.m, param.v = policy(param.value, param.grad, param.m, param.v, step, **hyper)
+    param.value, param.m, param.v = apply_policy(policy, param.value, param.grad, param.m,
+                                                 param.v, step, hyper)
     param.last_grad = param.grad   # kept for state snapshots only
     param.grad = None
     param.step = step

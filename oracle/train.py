@@ -52,7 +52,7 @@ import numpy as np
 from workloads import make_params, make_batch, make_eval_batch, mlp_ties, mbv2_blocks
 from . import layers as L
 from .losses import LOSSES
-from .optim import apply as apply_optimizer, clip_scale
+from .optim import SLICE, apply as apply_optimizer, clip_scale
 
 
 class Model:
@@ -351,6 +351,21 @@ def new_model(cfg, init=None, seed=0):
     return Model(nodes, params, cfg["loss"], cfg["opt"])
 
 
+def _min_sqrt_vhat(prev, v, bc2):
+    """Element-wise running minimum over steps of sqrt(v / bc2), zeros read as
+    infinite (test bookkeeping for the tolerance of Adam's update; no part of
+    the training arithmetic), taken in slices of the optimizer's slice size."""
+    out = np.empty_like(v)
+    fv, fo = v.reshape(-1), out.reshape(-1)
+    fp = prev.reshape(-1) if prev is not None else None
+    for s in range(0, v.size, SLICE):
+        sl = slice(s, s + SLICE)
+        r = np.sqrt(fv[sl] / bc2)
+        r = np.where(r > 0.0, r, np.inf)
+        fo[sl] = np.minimum(fp[sl], r) if fp is not None else r
+    return out
+
+
 def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=None,
         snapshots=(), on_step=None):
     """Train workload `cfg` for `steps` steps under `ordering` in float64.
@@ -403,9 +418,8 @@ def run(cfg, ordering, steps=None, seed=0, race_bug=False, init=None, batches=No
         if hyper["kind"] in ("adam", "adamw"):
             for k, p in model.params.items():
                 if p.step > 0:
-                    r = np.sqrt(p.v / (1.0 - hyper["beta2"] ** p.step))
-                    r = np.where(r > 0.0, r, np.inf)
-                    min_vhat[k] = np.minimum(min_vhat[k], r) if k in min_vhat else r
+                    min_vhat[k] = _min_sqrt_vhat(min_vhat.get(k), p.v,
+                                                 1.0 - hyper["beta2"] ** p.step)
         if t in snapshots:
             snaps[t] = snap()
         if on_step is not None:

@@ -163,3 +163,37 @@ def test_fig7_optimizers_match_torch_optim(kind, hyper, torch_cls, torch_kw):
         t.grad = torch.tensor(g, dtype=torch.float64)
         opt.step()
         np.testing.assert_allclose(traj[i], t.detach().numpy(), rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("kind,hyper", [
+    ("sgd", dict(lr=0.1, momentum=0.9, weight_decay=1e-3)),
+    ("adam", dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-2)),
+    ("adamw", dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=1e-2)),
+    ("adagrad", dict(lr=1e-2, eps=1e-10, weight_decay=1e-4)),
+    ("rmsprop", dict(lr=1e-2, alpha=0.99, eps=1e-8, weight_decay=1e-4, momentum=0.9)),
+    ("adadelta", dict(lr=1.0, rho=0.9, eps=1e-6, weight_decay=1e-4)),
+])
+def test_sliced_application_equals_whole_tensor(kind, hyper):
+    """apply() takes a tensor larger than SLICE slice by slice: bit-identical to
+    the policy on the whole tensor (every policy is element-wise), including a
+    ragged last slice and a non-contiguous 2-D input."""
+    r = np.random.default_rng(5)
+    n = 2 * optim.SLICE + 37
+    theta, g = r.standard_normal(n), r.standard_normal(n)
+    m, v = r.standard_normal(n) * 0.1, np.abs(r.standard_normal(n)) * 0.1
+    policy = optim.POLICIES[kind]
+    want = policy(theta, g, m, v, 3, **hyper)
+    got = optim.apply_policy(policy, theta, g, m, v, 3, hyper)
+    for a, b in zip(got, want):
+        np.testing.assert_array_equal(a, b)
+    # through apply() on a Param, from a transposed (non-contiguous) gradient
+    rows = optim.SLICE // 512 + 3
+    p = Param("w", theta[: rows * 512].reshape(rows, 512))
+    p.m, p.v = m[: rows * 512].reshape(rows, 512), v[: rows * 512].reshape(rows, 512)
+    p.step = 2
+    gt = np.ascontiguousarray(g[: rows * 512].reshape(512, rows)).T
+    p.grad = gt
+    want = policy(p.value, gt, p.m, p.v, 3, **hyper)
+    optim.apply(p, dict(hyper, kind=kind))
+    for a, b in zip((p.value, p.m, p.v), want):
+        np.testing.assert_array_equal(a, b)
