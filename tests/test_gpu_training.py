@@ -151,13 +151,13 @@ def test_windowed_parity_full_size(gpu, progress, name, starts):
         progress(f"{name}: window {s} -> {s + 1}")
         results = {}
         for o in ("eager", "ff", "bf"):
-            tr = Trainer(cfg, make_params(cfg), gpu)
+            # built on the state it loads: no random initial values to draw
+            a = ref["snapshots"][s - 1 if o == "ff" and s > 0 else s]
+            tr = Trainer(cfg, a["params"], gpu)
             if o == "ff" and s > 0:
-                a = ref["snapshots"][s - 1]
                 tr.load_state(a["params"], a["m"], a["v"], a["step"],
                               pending=ref["snapshots"][s]["grad"])
             else:
-                a = ref["snapshots"][s]
                 tr.load_state(a["params"], a["m"], a["v"], a["step"])
             x, y = make_batch(cfg, s + 1)
             tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
@@ -220,13 +220,13 @@ def test_mbv2_windows_and_orderings(gpu):
     for s in range(K):
         results = {}
         for o in ("eager", "ff", "bf"):
-            tr = Trainer(cfg, make_params(cfg), gpu)
+            # built on the state it loads: no random initial values to draw
+            a = ref["snapshots"][s - 1 if o == "ff" and s > 0 else s]
+            tr = Trainer(cfg, a["params"], gpu)
             if o == "ff" and s > 0:
-                a = ref["snapshots"][s - 1]
                 tr.load_state(a["params"], a["m"], a["v"], a["step"],
                               pending=ref["snapshots"][s]["grad"])
             else:
-                a = ref["snapshots"][s]
                 tr.load_state(a["params"], a["m"], a["v"], a["step"])
             x, y = make_batch(cfg, s + 1)
             tr.step(torch.as_tensor(x).to(gpu), torch.as_tensor(y).to(gpu), o)
@@ -314,7 +314,7 @@ def _tblock_orderings(torch, gpu, cfg, start, prev=None):
     x, y = make_batch(cfg, t)
     out = {}
     for o in ("eager", "ff", "bf"):
-        tr = Trainer(cfg, make_params(cfg), gpu)
+        tr = Trainer(cfg, (prev if o == "ff" and prev is not None else start)["params"], gpu)
         if o == "ff" and prev is not None:
             tr.load_state(prev["params"], prev["m"], prev["v"], prev["step"], pending=start["grad"])
         else:
@@ -436,7 +436,7 @@ def test_vgg_full_size_second_step(gpu):
     x, y = make_batch(cfg, 2)
     out = {}
     for o in ("eager", "ff", "bf"):
-        tr = Trainer(cfg, make_params(cfg), gpu)
+        tr = Trainer(cfg, (s0 if o == "ff" else s1)["params"], gpu)
         if o == "ff":
             tr.load_state(s0["params"], s0["m"], s0["v"], s0["step"], pending=s1["grad"])
         else:
