@@ -1,6 +1,8 @@
 import os
 import sys
 
+import time
+
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -25,8 +27,11 @@ def gpu():
 @pytest.fixture
 def progress(capsys):
     """Report a long test's steps as they finish, past pytest's output capture
-    (a run that prints nothing for minutes is taken to be hung)."""
+    (a run that prints nothing for minutes is taken to be hung), with the
+    seconds since the test started."""
+    t0 = time.monotonic()
+
     def say(msg):
         with capsys.disabled():
-            print(msg, flush=True)
+            print(f"[{time.monotonic() - t0:6.1f}s] {msg}", flush=True)
     return say

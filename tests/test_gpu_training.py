@@ -1,6 +1,8 @@
 """K-step training parity on the GPU: every ordering against the oracle's eager
 run on the same seeded inputs, and the three GPU orderings bit for bit against
 each other.  Steps and counters are compared exactly."""
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 
@@ -171,21 +173,26 @@ def test_windowed_parity_full_size(gpu, progress, name, starts):
             torch.cuda.empty_cache()
         np.testing.assert_array_equal(results["bf"][0]["params"]["fc1.weight"],
                                       results["eager"][0]["params"]["fc1.weight"])
+        progress(f"{name}: window {s} -> {s + 1}: the three GPU orderings done")
         matched = {}
         why = {}
-        for flips, cand_loss, cand in oracle.candidate_steps(cfg, ref["snapshots"][s], s + 1):
-            # One step from the oracle's own state: the sensitivity of this step's
-            # update is set by this outcome's sqrt(v_hat) alone (cand["min_sqrt_vhat"]).
-            for o, (st, loss, teach) in results.items():
-                if o in matched:
-                    continue
-                msg = _mismatch(st, loss, cand_loss, cand, cfg, ref["snapshots"][s], teach)
-                if msg is None:
-                    matched[o] = flips
-                else:
-                    why.setdefault(o, []).append((len(flips), msg))
-            if len(matched) == len(results):
-                break
+        with ThreadPoolExecutor(max_workers=len(results)) as pool:
+            for flips, cand_loss, cand in oracle.candidate_steps(cfg, ref["snapshots"][s], s + 1):
+                # One step from the oracle's own state: the sensitivity of this step's
+                # update is set by this outcome's sqrt(v_hat) alone (cand["min_sqrt_vhat"]).
+                # The orderings' checks are independent: one thread each (numpy
+                # leaves the interpreter lock in its element-wise loops).
+                jobs = {o: pool.submit(_mismatch, st, loss, cand_loss, cand, cfg,
+                                       ref["snapshots"][s], teach)
+                        for o, (st, loss, teach) in results.items() if o not in matched}
+                for o, job in jobs.items():
+                    msg = job.result()
+                    if msg is None:
+                        matched[o] = flips
+                    else:
+                        why.setdefault(o, []).append((len(flips), msg))
+                if len(matched) == len(results):
+                    break
         progress(f"{name} step {s + 1}: matched candidates "
                  f"{ {o: len(f) for o, f in matched.items()} }")
         print(f"{name} step {s + 1}: matched candidates", {o: len(f) for o, f in matched.items()},
@@ -336,7 +343,8 @@ def _tblock_check(cfg, out, start, ref, losses, say=print):
     gradient.  On the first step the elements whose oracle gradient is within
     twice the measured gradient error of zero are left to the second rule."""
     hyper = cfg["opt"]
-    for o, (st, loss) in out.items():
+
+    def one(o, st, loss):
         assert rel(loss, losses) <= TOL_BF16, (o, loss, losses)
         worst_m, worst_u, und = 0.0, 0.0, []
         teach = teachers(st, start, hyper)
@@ -355,10 +363,17 @@ def _tblock_check(cfg, out, start, ref, losses, say=print):
                                 undetermined=u, teacher=teach[k])
             und.append(n / ref["params"][k].size)
             worst_m, worst_u = max(worst_m, rm), max(worst_u, r)
-        say(f"tblock12 {o} step {ref['step'][k]}: loss {loss[0]:.6f} (oracle {losses[0]:.6f}), "
-            f"largest relative error of m {worst_m:.2e}, of the update {worst_u:.2e}; "
-            f"elements left to the own-gradient rule: median {np.median(und):.2%}, "
-            f"max {np.max(und):.2%} of a tensor")
+        return (f"tblock12 {o} step {ref['step'][k]}: loss {loss[0]:.6f} (oracle {losses[0]:.6f}), "
+                f"largest relative error of m {worst_m:.2e}, of the update {worst_u:.2e}; "
+                f"elements left to the own-gradient rule: median {np.median(und):.2%}, "
+                f"max {np.max(und):.2%} of a tensor")
+
+    # The orderings' checks are independent: one thread each; results (and the
+    # first failed assertion) are taken in ordering order.
+    with ThreadPoolExecutor(max_workers=len(out)) as pool:
+        jobs = [pool.submit(one, o, st, loss) for o, (st, loss) in out.items()]
+        for job in jobs:
+            say(job.result())
     for k in ref["params"]:
         np.testing.assert_array_equal(out["bf"][0]["params"][k], out["eager"][0]["params"][k])
         np.testing.assert_array_equal(out["bf"][0]["v"][k], out["eager"][0]["v"][k])
