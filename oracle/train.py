@@ -41,9 +41,10 @@ up to a whole step; the GPU parity tests use this to tell such elements apart.
 
 Pinned by: the ordering invariant eager == ff(flushed) == bf bit for bit, a
 planted dependency violation that breaks it, a shared-parameter toy with
-step == K (tests/test_oracle_orderings.py).  Whole K-step trajectories have no
-printed reference values in the paper: beyond the component pins and the
-invariant they are parity unpinned.
+step == K (tests/test_oracle_orderings.py); whole K-step eager trajectories of
+every model family against torch autograd + torch.optim in float64
+(tests/test_oracle_vs_torch.py).  The paper prints no reference values for
+trajectories, so these are independent-implementation pins.
 """
 import itertools
 
