@@ -161,6 +161,20 @@ typedef struct of_carry {
   of_opt opt;
 } of_carry;
 
+/*
+ * Storage of a bf16-operand layer's activations (of_linear_desc.io, bit flags;
+ * dtype OF_BF16 only, 0 otherwise).  A tensor that only bf16-operand
+ * contractions read can be kept as its bf16 rounding (uint16 bit patterns,
+ * round to nearest even): the value the contraction would round the fp32
+ * tensor to, so results are bit-identical, with half the bytes moved.
+ *   OF_IO_X_BF16  X [M, ldx] is stored as bf16: the forward's and the weight
+ *                 gradient's `x` point to it (pass it cast to the pointer
+ *                 type; 2-byte aligned).  The forward then needs W->w_bf16.
+ *   OF_IO_Y_BF16  the forward stores Y = act(Z) as bf16 [M, ldy] into `y`
+ *                 (cast; 2-byte aligned); Z, when requested, stays fp32.
+ */
+enum { OF_IO_X_BF16 = 1, OF_IO_Y_BF16 = 2 };
+
 typedef struct of_linear_desc {
   int64_t M, N, K;   /* rows, output features, input features (all >= 1) */
   int64_t ldx;       /* row stride of X in elements; 0 means K */
@@ -168,6 +182,7 @@ typedef struct of_linear_desc {
   int32_t dtype;     /* matmul operand type: OF_F32, or OF_BF16 (operands rounded to bf16, fp32 accumulate) */
   int32_t act;       /* of_act applied in the forward epilogue */
   int32_t has_bias;  /* 1: bias [N] added in the forward */
+  int32_t io;        /* OF_IO_* flags (bf16 storage of X and Y); 0: fp32 */
 } of_linear_desc;
 
 typedef struct of_conv_desc {
@@ -208,10 +223,12 @@ size_t of_linear_workspace_size(const of_linear_desc* d, int32_t op);
 /*
  * Plain forward (Fig. 1(a), the forward node of a linear layer):
  *   Z = X W^T + b,  Y = act(Z).
- * x: [M, ldx] fp32 (OF_F32) or fp32 rounded to bf16 on load (OF_BF16).
+ * x: [M, ldx] fp32 (OF_F32) or fp32 rounded to bf16 on load (OF_BF16), or
+ * bf16 as stored (OF_IO_X_BF16).
  * W: W->w is read for OF_F32, W->w_bf16 for OF_BF16.  b: [N] or NULL when
  * !has_bias.  z: [M, ldy] fp32, optional (needed by GELU's derivative);
- * y: [M, ldy] fp32, required.  Workspace: OF_LINEAR_FWD.
+ * y: [M, ldy] fp32 (bf16 with OF_IO_Y_BF16), required.  Workspace:
+ * OF_LINEAR_FWD.
  */
 of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param* W,
                         const float* b, float* z, float* y, void* ws, size_t ws_bytes,
@@ -270,7 +287,8 @@ of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_
  * Eager weight gradient (Fig. 1(b); the gradient is materialised and later
  * read and reset by the optimizer, Section 3 "Baseline"):
  *   dW = dZ^T X [N,K],  db = sum over rows of dZ [N] (db may be NULL).
- * accumulate = 1 adds into dw/db (a parameter used more than once).
+ * accumulate = 1 adds into dw/db (a parameter used more than once).  x: the
+ * forward's X [M, ldx], fp32, or bf16 as stored with OF_IO_X_BF16.
  * Workspace: OF_LINEAR_BWD_WEIGHT.
  */
 of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const float* x,
@@ -293,7 +311,8 @@ of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const f
  * (the overlap of updating with back-propagation, Section 3); the caller must
  * then order later reads of W and b after update_stream.  The two halves use
  * workspaces ws (OF_LINEAR_BWD_DATA) and ws_update (OF_LINEAR_BWD_WEIGHT),
- * which must not overlap when update_stream != NULL.
+ * which must not overlap when update_stream != NULL.  x as in
+ * of_linear_bwd_weight (bf16 with OF_IO_X_BF16).
  */
 of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const float* x,
                               const of_param* W, const of_param* b, const float* gW_partial,
@@ -586,6 +605,18 @@ of_status of_xent_fwd_bwd(const float* logits, const int64_t* labels, int64_t B,
 of_status of_layernorm_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
                            const float* beta, float eps, float* y, float* mean, float* rstd,
                            void* stream);
+
+/*
+ * of_layernorm_fwd with y stored as bf16 [M, D] (uint16 bit patterns, each the
+ * fp32 result rounded to the nearest bf16, ties to even), for an output that
+ * only bf16-operand contractions read (a transformer block's LN outputs feed
+ * its QKV and FC1 linears): the value such a contraction rounds an fp32 y to,
+ * in half the bytes.  mean and rstd are
+ * fp32 as in of_layernorm_fwd, bit-identical to it.  y must be 2-byte aligned.
+ */
+of_status of_layernorm_fwd_bf16(const float* x, int64_t M, int64_t D, const float* gamma,
+                                const float* beta, float eps, uint16_t* y, float* mean,
+                                float* rstd, void* stream);
 
 /* Number of row groups G of the parameter-gradient partials of
  * of_layernorm_bwd for M rows (1 <= G <= 64). */

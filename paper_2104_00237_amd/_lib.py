@@ -16,6 +16,7 @@ OF_OK, OF_EINVAL, OF_EUNSUPPORTED, OF_EALIGN, OF_EWORKSPACE, OF_EHIP = range(6)
 STATUS_NAMES = {0: "OF_OK", 1: "OF_EINVAL", 2: "OF_EUNSUPPORTED", 3: "OF_EALIGN",
                 4: "OF_EWORKSPACE", 5: "OF_EHIP"}
 OF_F32, OF_BF16 = 0, 1
+OF_IO_X_BF16, OF_IO_Y_BF16 = 1, 2   # of_linear_desc.io: bf16 storage of X / Y
 OF_ACT_NONE, OF_ACT_RELU, OF_ACT_GELU = 0, 1, 2
 OF_OPT_SGD, OF_OPT_ADAM, OF_OPT_ADAMW = 0, 1, 2
 OF_OPT_ADAGRAD, OF_OPT_RMSPROP, OF_OPT_ADADELTA = 3, 4, 5
@@ -60,7 +61,8 @@ class OfGradRef(ctypes.Structure):
 
 class OfLinearDesc(ctypes.Structure):
     _fields_ = [("M", c_int64), ("N", c_int64), ("K", c_int64), ("ldx", c_int64),
-                ("ldy", c_int64), ("dtype", c_int32), ("act", c_int32), ("has_bias", c_int32)]
+                ("ldy", c_int64), ("dtype", c_int32), ("act", c_int32), ("has_bias", c_int32),
+                ("io", c_int32)]
 
 
 class OfConvDesc(ctypes.Structure):
@@ -141,6 +143,8 @@ _SIGS = {
                                     c_int64, c_void_p, c_void_p]),
     "of_layernorm_fwd": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, c_void_p, c_float,
                                    c_void_p, c_void_p, c_void_p, c_void_p]),
+    "of_layernorm_fwd_bf16": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, c_void_p, c_float,
+                                        c_void_p, c_void_p, c_void_p, c_void_p]),
     "of_layernorm_partial_rows": (c_int64, [c_int64]),
     "of_layernorm_bwd": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                    c_int64, c_int64, c_void_p, c_void_p, c_void_p, c_void_p]),
@@ -221,7 +225,7 @@ for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_conv_fwd_carry", "of_line
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",
            "of_conv_fwd_fused", "of_conv_bwd_data", "of_conv_bwd_weight", "of_conv_wgrad_fused",
            "of_maxpool2x2_fwd", "of_maxpool2x2_bwd", "of_avgpool_fwd", "of_avgpool_bwd",
-           "of_layernorm_fwd", "of_layernorm_bwd",
+           "of_layernorm_fwd", "of_layernorm_fwd_bf16", "of_layernorm_bwd",
            "of_reduce_rows", "of_add", "of_dwconv_fwd", "of_dwconv_bwd_data",
            "of_dwconv_bwd_weight", "of_dwconv_wgrad_fused"):
     globals()[_n] = _wrap(_n)

@@ -278,6 +278,7 @@ struct EpiArgs {
   // outputs
   float* out; int64_t ldo;      // y (FWD), dx (DGRAD), dw (WGRAD)
   float* z; int64_t ldz;        // FWD: pre-activation (optional)
+  uint16_t* yb;                 // FWD (bf16 kernels): y stored as bf16 here, out unused
   const float* prev; int64_t ldp;  // DGRAD: saved tensor of the previous layer
   int act;                      // FWD: activation; DGRAD: previous layer's activation
   int accumulate;               // WGRAD
@@ -361,9 +362,10 @@ hipError_t launch_avgpool_fwd(const float* x, int64_t N, int64_t P, int64_t C, f
 hipError_t launch_avgpool_bwd(const float* dy, const float* mask_src, int64_t N, int64_t P,
                               int64_t C, float* dx, hipStream_t s);
 int64_t ln_partial_rows(int64_t M);
+// y: fp32 output, or NULL when yb (the output rounded to bf16) is given.
 hipError_t launch_ln_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
-                         const float* beta, float eps, float* y, float* mean, float* rstd,
-                         hipStream_t s);
+                         const float* beta, float eps, float* y, uint16_t* yb, float* mean,
+                         float* rstd, hipStream_t s);
 hipError_t launch_ln_bwd(const float* dy, const float* x, const float* mean, const float* rstd,
                          const float* gamma, const float* dres, int64_t M, int64_t D, float* dx,
                          float* dgamma_rows, float* dbeta_rows, hipStream_t s);

@@ -3,12 +3,15 @@
 // plain forward, data gradient, weight gradient, and the weight gradient with
 // the optimizer applied in its epilogue (backward-fusion).
 //
-// Operands stay in their storage type in HBM: activations and gradients are
-// fp32 and are rounded to bf16 (round to nearest even) as they are staged into
-// LDS, which is the same value as rounding them just before the product; a
-// weight operand is read from its bf16 shadow when one is given (half the
-// bytes), else rounded from the fp32 master.  Products of bf16 values are exact
-// in fp32 and the sums accumulate in fp32.
+// Operands stay in their storage type in HBM: fp32 activations and gradients
+// are rounded to bf16 (round to nearest even) as they are staged into LDS,
+// which is the same value as rounding them just before the product; an
+// activation that only these contractions read may be stored as that bf16
+// rounding by its producer and is then read as stored (the forward's X, the
+// weight gradient's X); a weight operand is read from its bf16 shadow when one
+// is given (half the bytes), else rounded from the fp32 master.  Products of
+// bf16 values are exact in fp32 and the sums accumulate in fp32.  A forward
+// may store its output Y as bf16 as well (for a consumer of the same kind).
 //
 // LDS layout: each operand tile is stored as BR/8 planes of [BX][8] bf16, so
 // the 8 consecutive reduction elements a lane feeds one MFMA are one 16-byte
@@ -605,6 +608,7 @@ static int bvec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* v
                   ((b_rc ? pr.R : pr.Q) % gb == 0);
   int ve = 0;
   if (aligned16(ea.out) && ea.ldo % 4 == 0 && (ea.z == nullptr || (aligned16(ea.z) && ea.ldz % 4 == 0)) &&
+      (ea.yb == nullptr || ((uintptr_t)ea.yb & 7u) == 0) &&
       (ea.prev == nullptr || (aligned16(ea.prev) && ea.ldp % 4 == 0)))
     ve |= 1;
   if (kind == EPI_WGRAD_BF && aligned16(ea.W.w) && aligned16(ea.W.m) && ea.ldo % 4 == 0 &&

@@ -151,12 +151,16 @@ __device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const 
     const int64_t oy = (int64_t)p * ea.ldo + q, oz = (int64_t)p * ea.ldz + q;
     if (n == 4 && (vec & 1)) {
       if (ea.z) st4(ea.z + oz, make_float4(zv[0], zv[1], zv[2], zv[3]));
-      st4(ea.out + oy, make_float4(act_fwd(ea.act, zv[0]), act_fwd(ea.act, zv[1]),
-                                   act_fwd(ea.act, zv[2]), act_fwd(ea.act, zv[3])));
+      const float4 y = make_float4(act_fwd(ea.act, zv[0]), act_fwd(ea.act, zv[1]),
+                                   act_fwd(ea.act, zv[2]), act_fwd(ea.act, zv[3]));
+      if (ea.yb) st_bf16x4(ea.yb + oy, y);
+      else st4(ea.out + oy, y);
     } else {
       for (int e = 0; e < n; ++e) {
         if (ea.z) ea.z[oz + e] = zv[e];
-        ea.out[oy + e] = act_fwd(ea.act, zv[e]);
+        const float y = act_fwd(ea.act, zv[e]);
+        if (ea.yb) ea.yb[oy + e] = f32_to_bf16(y);
+        else ea.out[oy + e] = y;
       }
     }
   } else if (EPI == EPI_DGRAD) {

@@ -3,7 +3,9 @@
 //
 // Forward: one wavefront per row; mean, then the variance of the centred
 // values, then y = (x - mean) * rstd * gamma + beta; mean and rstd are kept
-// for the backward.
+// for the backward.  y is stored as fp32, or (yb) as its bf16 rounding (round
+// to nearest even) when only a bf16-operand contraction reads it: the same
+// value the contraction would round it to, in half the bytes.
 // Backward, per row: with xh = (x - mean) * rstd and g = dy * gamma,
 //   dx = rstd * (g - mean(g) - xh * mean(g * xh))  (+ the residual gradient);
 // the parameter gradients sum dy * xh and dy over the rows.  They are written
@@ -28,6 +30,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
                                                      int64_t D, const float* __restrict__ gamma,
                                                      const float* __restrict__ beta, float eps,
                                                      float* __restrict__ y,
+                                                     uint16_t* __restrict__ yb,
                                                      float* __restrict__ mean,
                                                      float* __restrict__ rstd) {
   const int lane = threadIdx.x & 63;
@@ -44,9 +47,11 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
   }
   const float var = __fdiv_rn(wave_sum(q), (float)D);
   const float rs = __fdiv_rn(1.f, __fsqrt_rn(__fadd_rn(var, eps)));
-  float* yr = y + row * D;
-  for (int64_t j = lane; j < D; j += 64)
-    yr[j] = __fmaf_rn(__fmul_rn(__fsub_rn(xr[j], mu), rs), gamma[j], beta[j]);
+  for (int64_t j = lane; j < D; j += 64) {
+    const float o = __fmaf_rn(__fmul_rn(__fsub_rn(xr[j], mu), rs), gamma[j], beta[j]);
+    if (yb) yb[row * D + j] = f32_to_bf16(o);
+    else y[row * D + j] = o;
+  }
   if (lane == 0) {
     mean[row] = mu;
     rstd[row] = rs;
@@ -128,6 +133,7 @@ __global__ __launch_bounds__(256) void ln_fwd_vec_kernel(const float* __restrict
                                                          int64_t D, const float* __restrict__ gamma,
                                                          const float* __restrict__ beta, float eps,
                                                          float* __restrict__ y,
+                                                         uint16_t* __restrict__ yb,
                                                          float* __restrict__ mean,
                                                          float* __restrict__ rstd) {
   const int lane = threadIdx.x & 63;
@@ -156,16 +162,17 @@ __global__ __launch_bounds__(256) void ln_fwd_vec_kernel(const float* __restrict
   }
   const float var = __fdiv_rn(wave_sum(q), (float)D);
   const float rs = __fdiv_rn(1.f, __fsqrt_rn(__fadd_rn(var, eps)));
-  float* yr = y + row * D;
 #pragma unroll
   for (int c = 0; c < NPL; ++c) {
     const int64_t j = 4 * (lane + 64 * c);
     if (j < D) {
       const float4 g = ld4(gamma + j), b = ld4(beta + j);
-      st4(yr + j, make_float4(__fmaf_rn(__fmul_rn(__fsub_rn(v[c].x, mu), rs), g.x, b.x),
-                              __fmaf_rn(__fmul_rn(__fsub_rn(v[c].y, mu), rs), g.y, b.y),
-                              __fmaf_rn(__fmul_rn(__fsub_rn(v[c].z, mu), rs), g.z, b.z),
-                              __fmaf_rn(__fmul_rn(__fsub_rn(v[c].w, mu), rs), g.w, b.w)));
+      const float4 o = make_float4(__fmaf_rn(__fmul_rn(__fsub_rn(v[c].x, mu), rs), g.x, b.x),
+                                   __fmaf_rn(__fmul_rn(__fsub_rn(v[c].y, mu), rs), g.y, b.y),
+                                   __fmaf_rn(__fmul_rn(__fsub_rn(v[c].z, mu), rs), g.z, b.z),
+                                   __fmaf_rn(__fmul_rn(__fsub_rn(v[c].w, mu), rs), g.w, b.w));
+      if (yb) st_bf16x4(yb + row * D + j, o);
+      else st4(y + row * D + j, o);
     }
   }
   if (lane == 0) {
@@ -238,18 +245,20 @@ static int ln_npl(int64_t D, std::initializer_list<const void*> ptrs) {
 }
 
 hipError_t launch_ln_fwd(const float* x, int64_t M, int64_t D, const float* gamma,
-                         const float* beta, float eps, float* y, float* mean, float* rstd,
-                         hipStream_t s) {
+                         const float* beta, float eps, float* y, uint16_t* yb, float* mean,
+                         float* rstd, hipStream_t s) {
   const dim3 g((unsigned)((M + 3) / 4));
-  switch (ln_npl(D, {x, gamma, beta, y})) {
-    case 1: hipLaunchKernelGGL(ln_fwd_vec_kernel<1>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, mean, rstd); return hipGetLastError();
-    case 2: hipLaunchKernelGGL(ln_fwd_vec_kernel<2>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, mean, rstd); return hipGetLastError();
-    case 4: hipLaunchKernelGGL(ln_fwd_vec_kernel<4>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, mean, rstd); return hipGetLastError();
-    case 8: hipLaunchKernelGGL(ln_fwd_vec_kernel<8>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, mean, rstd); return hipGetLastError();
+  // a bf16 row of D (a multiple of 4) elements is stored 4 at a time: 8-byte aligned base
+  const int npl = (yb && ((uintptr_t)yb & 7u)) ? 0 : ln_npl(D, {x, gamma, beta, y});
+  switch (npl) {
+    case 1: hipLaunchKernelGGL(ln_fwd_vec_kernel<1>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, yb, mean, rstd); return hipGetLastError();
+    case 2: hipLaunchKernelGGL(ln_fwd_vec_kernel<2>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, yb, mean, rstd); return hipGetLastError();
+    case 4: hipLaunchKernelGGL(ln_fwd_vec_kernel<4>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, yb, mean, rstd); return hipGetLastError();
+    case 8: hipLaunchKernelGGL(ln_fwd_vec_kernel<8>, g, dim3(256), 0, s, x, M, D, gamma, beta, eps, y, yb, mean, rstd); return hipGetLastError();
     default: break;
   }
   hipLaunchKernelGGL(ln_fwd_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, x, M, D, gamma,
-                     beta, eps, y, mean, rstd);
+                     beta, eps, y, yb, mean, rstd);
   return hipGetLastError();
 }
 

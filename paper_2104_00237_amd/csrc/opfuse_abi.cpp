@@ -126,6 +126,10 @@ of_status check_linear(const of_linear_desc* d) {
           "act %d is not an of_act", (int)d->act);
   REQUIRE(d->dtype == OF_F32 || d->dtype == OF_BF16, OF_EINVAL, "dtype %d is not an of_dtype",
           (int)d->dtype);
+  REQUIRE((d->io & ~(OF_IO_X_BF16 | OF_IO_Y_BF16)) == 0, OF_EINVAL,
+          "io %d has bits other than OF_IO_X_BF16 | OF_IO_Y_BF16", (int)d->io);
+  REQUIRE(d->io == 0 || d->dtype == OF_BF16, OF_EINVAL,
+          "bf16 storage of X or Y (io %d) needs dtype OF_BF16", (int)d->io);
   // Operand tiles are read through buffer descriptors based at the tile's
   // first element, with 32-bit byte offsets against a 2^31-1-byte range.  An
   // offset never exceeds the size of the operand matrix it reads from, so every
@@ -223,13 +227,24 @@ void set_weight_operand(const of_linear_desc* d, const of_param* W, GemmProblem&
   }
 }
 
+bool x_bf16(const of_linear_desc* d) { return (d->io & OF_IO_X_BF16) != 0; }
+bool y_bf16(const of_linear_desc* d) { return (d->io & OF_IO_Y_BF16) != 0; }
+
+// Alignment of X's storage: 4 bytes for fp32, 2 for bf16 (OF_IO_X_BF16).
+bool x_aligned(const of_linear_desc* d, const float* x) {
+  return (((uintptr_t)x) & (x_bf16(d) ? 1u : 3u)) == 0;
+}
+
 // Launch helpers shared by the entry points (arguments already validated).
 of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
                   float* z, float* y, void* ws, hipStream_t s, const CarryArgs* carry = nullptr) {
   GemmProblem pr{x, ldx_of(d), 1, nullptr, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
   set_weight_operand(d, W, pr);
+  pr.a_bf16 = x_bf16(d) ? 1 : 0;
   EpiArgs ea = empty_epi();
-  ea.out = y; ea.ldo = ldy_of(d);
+  ea.ldo = ldy_of(d);
+  if (y_bf16(d)) ea.yb = reinterpret_cast<uint16_t*>(y);
+  else ea.out = y;
   ea.z = z; ea.ldz = ldy_of(d);
   ea.act = d->act;
   ea.bias = d->has_bias ? b : nullptr;
@@ -251,7 +266,9 @@ of_status run_dgrad(const of_linear_desc* d, const float* dz, const of_param* W,
 
 GemmProblem wgrad_problem(const of_linear_desc* d, const float* dz, const float* x) {
   // dW[n,k] = sum_m dZ[m,n] X[m,k]: A(n, m) = dZ[m*ldy + n], B(k, m) = X[m*ldx + k].
-  return GemmProblem{dz, 1, ldy_of(d), x, 1, ldx_of(d), (int)d->N, (int)d->K, (int)d->M};
+  GemmProblem pr{dz, 1, ldy_of(d), x, 1, ldx_of(d), (int)d->N, (int)d->K, (int)d->M};
+  pr.b_bf16 = x_bf16(d) ? 1 : 0;   // X stored as bf16 is read as stored
+  return pr;
 }
 
 of_status check_act_prev(int32_t act_prev, const float* prev) {
@@ -383,8 +400,13 @@ of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_
   REQUIRE(W->numel == d->N * d->K, OF_EINVAL, "W->numel must be N*K");
   REQUIRE(!d->has_bias || b, OF_EINVAL, "has_bias is set but b is NULL");
   REQUIRE(d->act != OF_ACT_GELU || z, OF_EINVAL, "GELU needs z (its derivative reads Z)");
-  REQUIRE(al4(x) && al4(W->w) && al4(b) && al4(z) && al4(y), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  REQUIRE(al4(W->w) && al4(b) && al4(z), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  REQUIRE(x_aligned(d, x), OF_EALIGN, "x must be %d-byte aligned", x_bf16(d) ? 2 : 4);
+  REQUIRE((((uintptr_t)y) & (y_bf16(d) ? 1u : 3u)) == 0, OF_EALIGN, "y must be %d-byte aligned",
+          y_bf16(d) ? 2 : 4);
   REQUIRE((((uintptr_t)W->w_bf16) & 1u) == 0, OF_EALIGN, "W->w_bf16 must be 2-byte aligned");
+  REQUIRE(!x_bf16(d) || W->w_bf16, OF_EINVAL,
+          "X stored as bf16 (OF_IO_X_BF16) needs the weight's bf16 shadow W->w_bf16");
   if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
   CarryArgs carry;
@@ -478,7 +500,8 @@ of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const f
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
   REQUIRE(dz && x && dw, OF_EINVAL, "dz, x and dw are required");
-  REQUIRE(al4(dz) && al4(x) && al4(dw) && al4(db), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  REQUIRE(al4(dz) && al4(dw) && al4(db), OF_EALIGN, "fp32 pointers must be 4-byte aligned");
+  REQUIRE(x_aligned(d, x), OF_EALIGN, "x must be %d-byte aligned", x_bf16(d) ? 2 : 4);
   if ((st = check_ws(d, EPI_WGRAD, ws, ws_bytes)) != OF_OK) return st;
   EpiArgs ea = empty_epi();
   ea.out = dw; ea.ldo = d->K;
@@ -503,8 +526,9 @@ of_status of_linear_bwd_fused(const of_linear_desc* d, const float* dz, const fl
   if (b) {
     if ((st = check_param(b, "b", d->N, *opt, true)) != OF_OK) return st;
   }
-  REQUIRE(al4(dz) && al4(x) && al4(gW_partial) && al4(gb_partial) && al4(dx_prev), OF_EALIGN,
+  REQUIRE(al4(dz) && al4(gW_partial) && al4(gb_partial) && al4(dx_prev), OF_EALIGN,
           "fp32 pointers must be 4-byte aligned");
+  REQUIRE(x_aligned(d, x), OF_EALIGN, "x must be %d-byte aligned", x_bf16(d) ? 2 : 4);
   if (dx_prev) {
     if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
     if ((st = check_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
@@ -985,8 +1009,24 @@ of_status of_layernorm_fwd(const float* x, int64_t M, int64_t D, const float* ga
   REQUIRE(std::isfinite(eps) && eps > 0.f, OF_EINVAL, "eps must be finite and > 0");
   REQUIRE(al4(x) && al4(gamma) && al4(beta) && al4(y) && al4(mean) && al4(rstd), OF_EALIGN,
           "fp32 pointers must be 4-byte aligned");
-  return hip_status(launch_ln_fwd(x, M, D, gamma, beta, eps, y, mean, rstd, (hipStream_t)stream),
+  return hip_status(launch_ln_fwd(x, M, D, gamma, beta, eps, y, nullptr, mean, rstd,
+                                  (hipStream_t)stream),
                     "of_layernorm_fwd launch");
+}
+
+of_status of_layernorm_fwd_bf16(const float* x, int64_t M, int64_t D, const float* gamma,
+                                const float* beta, float eps, uint16_t* y, float* mean,
+                                float* rstd, void* stream) {
+  REQUIRE(x && gamma && beta && y && mean && rstd, OF_EINVAL,
+          "x, gamma, beta, y, mean and rstd are required");
+  REQUIRE(M >= 1 && D >= 1, OF_EINVAL, "M and D must be >= 1");
+  REQUIRE(std::isfinite(eps) && eps > 0.f, OF_EINVAL, "eps must be finite and > 0");
+  REQUIRE(al4(x) && al4(gamma) && al4(beta) && al4(mean) && al4(rstd), OF_EALIGN,
+          "fp32 pointers must be 4-byte aligned");
+  REQUIRE((((uintptr_t)y) & 1u) == 0, OF_EALIGN, "y (bf16) must be 2-byte aligned");
+  return hip_status(launch_ln_fwd(x, M, D, gamma, beta, eps, nullptr, y, mean, rstd,
+                                  (hipStream_t)stream),
+                    "of_layernorm_fwd_bf16 launch");
 }
 
 int64_t of_layernorm_partial_rows(int64_t M) { return M >= 1 ? ln_partial_rows(M) : 0; }

@@ -158,12 +158,12 @@ class LinearOp:
 
     kind = "linear"
 
-    def __init__(self, name, W, b, M, act, dtype=L.OF_F32, ldx=0):
+    def __init__(self, name, W, b, M, act, dtype=L.OF_F32, ldx=0, io=0):
         N, K = W.w.shape
         self.name, self.W, self.b = name, W, b
         self.M, self.N, self.K = M, N, K
         self.act = act
-        self.desc = L.OfLinearDesc(M, N, K, ldx, 0, dtype, L.ACTS[act], int(b is not None))
+        self.desc = L.OfLinearDesc(M, N, K, ldx, 0, dtype, L.ACTS[act], int(b is not None), io)
         self.updated = True
         self.params = [W] if b is None else [W, b]
         self.out_shape = (M, N)
@@ -376,19 +376,21 @@ class LayerNormOp:
 
     kind = "ln"
 
-    def __init__(self, name, g, b, M, D, eps):
+    def __init__(self, name, g, b, M, D, eps, y_bf16=False):
         self.name, self.g, self.b = name, g, b
         self.M, self.D, self.eps = M, D, eps
         self.N, self.K = D, 0
         self.updated = True
         self.params = [g, b]
+        self.y_bf16 = y_bf16    # the output is stored as bf16 (only bf16 operands read it)
 
     def ws(self, which):
         return 0
 
     def fwd(self, tr, x, y, mu, rs):
-        L.of_layernorm_fwd(x, self.M, self.D, self.g.w.data_ptr(), self.b.w.data_ptr(), self.eps,
-                           y, mu, rs, tr._s())
+        fn = L.of_layernorm_fwd_bf16 if self.y_bf16 else L.of_layernorm_fwd
+        fn(x, self.M, self.D, self.g.w.data_ptr(), self.b.w.data_ptr(), self.eps, y, mu, rs,
+           tr._s())
 
     prologue_ff = False   # gamma and beta are carried by the previous launch, or updated first
 
@@ -652,7 +654,11 @@ class TBlockNet:
 
     Every tensor a later kernel reads is kept per block, and so is every
     gradient buffer, so the side stream's fused updates of block b never race
-    with the main stream's back-propagation through the blocks below.  In the
+    with the main stream's back-propagation through the blocks below.  With
+    bf16 operands, a, qkv, c and g are read by the bf16 contractions alone
+    (forward and weight gradient; GELU's derivative reads u), so their
+    producers store them as bf16 (`bf16_acts`): the rounding each contraction
+    would apply, so results are bit-identical, in half the bytes.  In the
     plain backward (eager and forward-fusion) the LayerNorm parameter-gradient
     partials run on the side stream, so those steps join it before their
     optimizer step, clipping norm or next forward; backward-fusion computes
@@ -661,7 +667,7 @@ class TBlockNet:
 
     eager_side = True
 
-    def __init__(self, tr, cfg, pb):
+    def __init__(self, tr, cfg, pb, bf16_acts=True):
         self.tr = tr
         M, d, f, nb = cfg["batch"], cfg["hidden"], cfg["ffn"], cfg["blocks"]
         self.M, self.d, self.f = M, d, f
@@ -669,40 +675,52 @@ class TBlockNet:
         eps = cfg["ln_eps"]
         G = L.of_layernorm_partial_rows(M)
         shadow = dt == L.OF_BF16
+        acts = shadow and bf16_acts
+        xb = L.OF_IO_X_BF16 if acts else 0
+        yb = L.OF_IO_Y_BF16 if acts else 0
         self.blocks = []
         self.ops = []
         for b in range(1, nb + 1):
             p = f"blk{b}."
             blk = dict(
                 ln1=LayerNormOp(p + "ln1", pb(p + "ln1.weight", rows=G), pb(p + "ln1.bias", rows=G),
-                                M, d, eps),
+                                M, d, eps, y_bf16=acts),
                 qkv=LinearOp(p + "qkv", pb(p + "qkv.weight", shadow), pb(p + "qkv.bias"), M, "none",
-                             dt),
+                             dt, io=xb | yb),
                 proj=LinearOp(p + "proj", pb(p + "proj.weight", shadow), pb(p + "proj.bias"), M,
-                              "none", dt, ldx=3 * d),
+                              "none", dt, ldx=3 * d, io=xb),
                 ln2=LayerNormOp(p + "ln2", pb(p + "ln2.weight", rows=G), pb(p + "ln2.bias", rows=G),
-                                M, d, eps),
+                                M, d, eps, y_bf16=acts),
                 fc1=LinearOp(p + "fc1", pb(p + "fc1.weight", shadow), pb(p + "fc1.bias"), M, "gelu",
-                             dt),
+                             dt, io=xb | yb),
                 fc2=LinearOp(p + "fc2", pb(p + "fc2.weight", shadow), pb(p + "fc2.bias"), M, "none",
-                             dt),
+                             dt, io=xb),
             )
             self.ops += [blk[k] for k in ("ln1", "qkv", "proj", "ln2", "fc1", "fc2")]
             self.blocks.append(blk)
         f32 = dict(dtype=torch.float32, device=tr.device)
+        act = dict(dtype=torch.bfloat16 if acts else torch.float32, device=tr.device)
 
         def t(*shape):
             return torch.empty(shape, **f32)
 
+        def ta(*shape):   # read only as a bf16 matmul operand
+            return torch.empty(shape, **act)
+
         for blk in self.blocks:
-            blk.update(a=t(M, d), mu1=t(M), rs1=t(M), qkv_out=t(M, 3 * d), o=t(M, d), h=t(M, d),
-                       c=t(M, d), mu2=t(M), rs2=t(M), u=t(M, f), g=t(M, f), w=t(M, d), y=t(M, d),
+            blk.update(a=ta(M, d), mu1=t(M), rs1=t(M), qkv_out=ta(M, 3 * d), o=t(M, d), h=t(M, d),
+                       c=ta(M, d), mu2=t(M), rs2=t(M), u=t(M, f), g=ta(M, f), w=t(M, d), y=t(M, d),
                        gy=t(M, d), gu=t(M, f), gc=t(M, d), gh=t(M, d), ga=t(M, d),
                        # the Q and K thirds of the QKV gradient stay zero
                        gqkv=torch.zeros((M, 3 * d), **f32))
         self.gx = t(M, d)   # gradient w.r.t. the network input (not used further)
         self.out = self.blocks[-1]["y"]
         self.gout = self.blocks[-1]["gy"]
+
+    def _v(self, blk):
+        """Address of the V third of the block's QKV output."""
+        q = blk["qkv_out"]
+        return q.data_ptr() + 2 * self.d * q.element_size()
 
     def forward(self, x, fused):
         tr = self.tr
@@ -739,7 +757,7 @@ class TBlockNet:
             elif name == "qkv":
                 op.fwd(tr, blk["a"].data_ptr(), blk["qkv_out"].data_ptr(), carry=carry)
             elif name == "proj":
-                op.fwd(tr, blk["qkv_out"].data_ptr() + 8 * d, blk["o"].data_ptr(), carry=carry)
+                op.fwd(tr, self._v(blk), blk["o"].data_ptr(), carry=carry)
             elif name == "ln2":
                 op.fwd(tr, blk["h"].data_ptr(), blk["c"].data_ptr(), blk["mu2"].data_ptr(),
                        blk["rs2"].data_ptr())
@@ -841,7 +859,7 @@ class TBlockNet:
                              done)
             self._ln_bwd(blk["ln2"], P["gc"], P["h"], P["mu2"], P["rs2"], P["gy"], P["gh"], fused,
                          done)
-            self._linear_bwd(blk["proj"], P["gh"], P["qkv_out"] + 8 * d, None, L.OF_ACT_NONE,
+            self._linear_bwd(blk["proj"], P["gh"], self._v(blk), None, L.OF_ACT_NONE,
                              P["gqkv"] + 8 * d, fused, done)
             self._linear_bwd(blk["qkv"], P["gqkv"], P["a"], None, L.OF_ACT_NONE, P["ga"], fused,
                              done)
@@ -1143,7 +1161,7 @@ class Trainer:
     """Trains one workload on one GPU under a chosen ordering."""
 
     def __init__(self, cfg, init, device="cuda:0", merge_dgrad=False, conv_prologue=False,
-                 linear_prologue=False):
+                 linear_prologue=False, bf16_acts=True):
         """merge_dgrad: backward-fusion runs each fp32 linear layer with at most
         64 rows as one merged data-gradient + update pass (of_linear_bwd_merged).
         conv_prologue: forward-fusion applies a convolution's pending update in
@@ -1168,7 +1186,7 @@ class Trainer:
                 raise NotImplementedError("linear / conv chains run with fp32 operands")
             self.net = ChainNet(self, cfg, pb)
         elif cfg["kind"] == "tblock":
-            self.net = TBlockNet(self, cfg, pb)
+            self.net = TBlockNet(self, cfg, pb, bf16_acts=bf16_acts)
         elif cfg["kind"] == "mbv2":
             if cfg["dtype"] != "f32":
                 raise NotImplementedError("the MobileNetV2-like network runs with fp32 operands")

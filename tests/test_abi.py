@@ -222,6 +222,13 @@ def test_bf16_shadow_and_norm_validation(lib):
     assert _status(L.of_layernorm_bwd, FAKE, FAKE + 64, FAKE, FAKE, None, None, 4, 8, FAKE + 128,
                    None, None, None) == L.OF_EINVAL   # dx needs gamma
     assert L.of_layernorm_partial_rows(4096) == 64 and L.of_layernorm_partial_rows(1) == 1
+    # bf16 output: required, 2-byte aligned (4-byte alignment is not needed)
+    assert _status(L.of_layernorm_fwd_bf16, FAKE, 4, 8, FAKE, FAKE, 1e-5, None, FAKE, FAKE,
+                   None) == L.OF_EINVAL
+    assert _status(L.of_layernorm_fwd_bf16, FAKE, 4, 8, FAKE, FAKE, 1e-5, FAKE + 1, FAKE, FAKE,
+                   None) == L.OF_EALIGN
+    assert _status(L.of_layernorm_fwd_bf16, FAKE + 2, 4, 8, FAKE, FAKE, 1e-5, FAKE, FAKE, FAKE,
+                   None) == L.OF_EALIGN
     assert _status(L.of_reduce_rows, FAKE, 2, 3, 8, FAKE, None) == L.OF_EINVAL   # ld < n
     assert _status(L.of_add, FAKE, None, 8, FAKE, None) == L.OF_EINVAL
 
@@ -409,3 +416,43 @@ def test_merged_static_validation(lib):
                    0, None, None) == L.OF_EINVAL
     assert _status(L.of_linear_bwd_merged_static, d, FAKE, FAKE, W, None, None, None, opt, None,
                    L.OF_ACT_RELU, FAKE, None) == L.OF_EINVAL   # ReLU needs prev
+
+
+def test_bf16_activation_storage_validation(lib):
+    """of_linear_desc.io: bf16 storage of X / Y needs bf16 operands, known bits,
+    the weight's shadow in a forward, and 2-byte (not 4-byte) alignment."""
+    Ws = L.OfParam(FAKE, FAKE, FAKE, FAKE, 16 * 12)
+    W = _param(16 * 12)
+    xb, yb = L.OF_IO_X_BF16, L.OF_IO_Y_BF16
+    # fp32 operands take no bf16 storage
+    assert _status(L.of_linear_fwd, _desc(io=xb), FAKE, W, None, None, FAKE, None, 0,
+                   None) == L.OF_EINVAL
+    assert "io" in L.of_last_error()
+    assert _status(L.of_linear_bwd_weight, _desc(io=xb), FAKE, FAKE, FAKE, None, 0, None, 0,
+                   None) == L.OF_EINVAL
+    assert L.of_linear_workspace_size(_desc(io=yb), L.OF_LINEAR_FWD) == 0
+    # unknown bits
+    assert _status(L.of_linear_fwd, _desc(dtype=L.OF_BF16, io=4), FAKE, Ws, None, None, FAKE,
+                   None, 0, None) == L.OF_EINVAL
+    # a forward reading bf16 X takes the weight from its bf16 shadow
+    assert _status(L.of_linear_fwd, _desc(dtype=L.OF_BF16, io=xb), FAKE, W, None, None, FAKE,
+                   None, 0, None) == L.OF_EINVAL
+    assert "w_bf16" in L.of_last_error()
+    # alignment: odd bf16 addresses fail, fp32 ones need 4 bytes
+    assert _status(L.of_linear_fwd, _desc(dtype=L.OF_BF16, io=xb), FAKE + 1, Ws, None, None,
+                   FAKE, None, 0, None) == L.OF_EALIGN
+    assert _status(L.of_linear_fwd, _desc(dtype=L.OF_BF16, io=yb), FAKE, Ws, None, None,
+                   FAKE + 1, None, 0, None) == L.OF_EALIGN
+    assert _status(L.of_linear_fwd, _desc(dtype=L.OF_BF16, io=xb), FAKE, Ws, None, None,
+                   FAKE + 2, None, 0, None) == L.OF_EALIGN     # y stays fp32
+    assert _status(L.of_linear_bwd_weight, _desc(dtype=L.OF_BF16, io=xb), FAKE, FAKE + 1, FAKE,
+                   None, 0, None, 0, None) == L.OF_EALIGN
+    assert _status(L.of_linear_bwd_weight, _desc(dtype=L.OF_BF16), FAKE, FAKE + 2, FAKE, None, 0,
+                   None, 0, None) == L.OF_EALIGN               # fp32 x
+    opt = L.make_opt(dict(kind="sgd", lr=0.1, momentum=0.9, weight_decay=0.0), 1)
+    assert _status(L.of_linear_bwd_fused, _desc(dtype=L.OF_BF16, io=xb), FAKE, FAKE + 1, Ws,
+                   None, None, None, opt, None, 0, None, None, 0, None, 0, None,
+                   None) == L.OF_EALIGN
+    # forward-fusion and the merged backward take fp32 operands only
+    assert _status(L.of_linear_fwd_fused, _desc(io=xb), FAKE, W, None, FAKE, None, None, None,
+                   opt, None, FAKE, None, 0, None) == L.OF_EINVAL

@@ -17,8 +17,8 @@ pre-LN residual blocks with bf16 matmul operands; SGD-momentum and Adam with
 coupled weight decay, AdamW; and a layer applied twice (mlp4tied: one update
 from the sum of both uses' gradients).
 
-bf16 operands (the transformer block's matmuls, Section 4's mixed-precision
-experiment): both matmul operands, and the output gradient entering the two
+bf16 operands (the transformer block's matmuls; the paper itself trains in
+float32): both matmul operands, and the output gradient entering the two
 backward products, rounded to the nearest bfloat16 (ties to even) while the
 bias gradient sums the unrounded output gradient.  The rounding here works on
 the float64 bit pattern (the oracle scales by a power of two and rounds), so
