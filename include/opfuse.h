@@ -273,6 +273,20 @@ of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_
                               void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * of_linear_fwd_carry with a residual connection added in the epilogue:
+ *   Y = act(X W^T + b) + R
+ * (a pre-LN transformer block's h = x + proj(v) and y = h + fc2(g); an
+ * inverted-residual block's input added to its projection).  The sum is
+ * rounded once, so Y equals of_linear_fwd followed by of_add, bit for bit,
+ * without storing and re-reading the branch output.  res: [M, ldy] fp32,
+ * required, 4-byte aligned; it may be y itself (fp32 Y, in place) and must
+ * not overlap y otherwise, nor z.  next may be NULL.
+ */
+of_status of_linear_fwd_res(const of_linear_desc* d, const float* x, const of_param* W,
+                            const float* b, const float* res, float* z, float* y,
+                            const of_carry* next, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Data gradient with the OLD weights (the dependency rule after Alg. 3):
  *   dX = (dZ W) * act_prev'(prev)
  * dz: [M, ldy].  prev: the previous layer's saved tensor, [M, ldx]: its Y for

@@ -141,7 +141,9 @@ inline int carry_slices(const CarryArgs& c, int64_t slice) {
 
 // ----------------------------------------------------------------- epilogues
 // c[0..n) are the results for (p, q..q+n-1).  vec: 128-bit memory paths allowed
-// (bit 0: out/z/prev, bit 1: parameter arrays); only used when n == 4.
+// (bit 0: out/z/prev/res, bit 1: parameter arrays); only used when n == 4.
+// A forward's residual R (ea.res) is added last, Y + R rounded once: the value
+// a separate element-wise addition of the two stored tensors gives.
 template <int EPI>
 __device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const float (&c)[4],
                                          int n, const float* bias, int vec) {
@@ -149,16 +151,23 @@ __device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const 
     float zv[4];
     for (int e = 0; e < 4; ++e) zv[e] = (bias && e < n) ? __fadd_rn(c[e], bias[e]) : c[e];
     const int64_t oy = (int64_t)p * ea.ldo + q, oz = (int64_t)p * ea.ldz + q;
+    const int64_t orr = (int64_t)p * ea.ldr + q;
     if (n == 4 && (vec & 1)) {
       if (ea.z) st4(ea.z + oz, make_float4(zv[0], zv[1], zv[2], zv[3]));
-      const float4 y = make_float4(act_fwd(ea.act, zv[0]), act_fwd(ea.act, zv[1]),
-                                   act_fwd(ea.act, zv[2]), act_fwd(ea.act, zv[3]));
+      float4 y = make_float4(act_fwd(ea.act, zv[0]), act_fwd(ea.act, zv[1]),
+                             act_fwd(ea.act, zv[2]), act_fwd(ea.act, zv[3]));
+      if (ea.res) {
+        const float4 r = ld4(ea.res + orr);
+        y.x = __fadd_rn(y.x, r.x); y.y = __fadd_rn(y.y, r.y);
+        y.z = __fadd_rn(y.z, r.z); y.w = __fadd_rn(y.w, r.w);
+      }
       if (ea.yb) st_bf16x4(ea.yb + oy, y);
       else st4(ea.out + oy, y);
     } else {
       for (int e = 0; e < n; ++e) {
         if (ea.z) ea.z[oz + e] = zv[e];
-        const float y = act_fwd(ea.act, zv[e]);
+        float y = act_fwd(ea.act, zv[e]);
+        if (ea.res) y = __fadd_rn(y, ea.res[orr + e]);
         if (ea.yb) ea.yb[oy + e] = f32_to_bf16(y);
         else ea.out[oy + e] = y;
       }

@@ -1155,7 +1155,8 @@ static int vec_flags(const GemmProblem& pr, int kind, const EpiArgs& ea, int* ve
          (ea.W.w_bf16 == nullptr || ((uintptr_t)ea.W.w_bf16 & 7u) == 0);
   int ve = 0;
   if (aligned16(ea.out) && ea.ldo % 4 == 0 && (ea.z == nullptr || (aligned16(ea.z) && ea.ldz % 4 == 0)) &&
-      (ea.prev == nullptr || (aligned16(ea.prev) && ea.ldp % 4 == 0)))
+      (ea.prev == nullptr || (aligned16(ea.prev) && ea.ldp % 4 == 0)) &&
+      (ea.res == nullptr || (aligned16(ea.res) && ea.ldr % 4 == 0)))
     ve |= 1;
   if (kind == EPI_WGRAD_BF && aligned16(ea.W.w) && aligned16(ea.W.m) && ea.ldo % 4 == 0 &&
       (ea.opt.kind == OF_OPT_SGD || aligned16(ea.W.v)) && (ea.gW == nullptr || aligned16(ea.gW)) &&

@@ -237,7 +237,8 @@ bool x_aligned(const of_linear_desc* d, const float* x) {
 
 // Launch helpers shared by the entry points (arguments already validated).
 of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
-                  float* z, float* y, void* ws, hipStream_t s, const CarryArgs* carry = nullptr) {
+                  float* z, float* y, void* ws, hipStream_t s, const CarryArgs* carry = nullptr,
+                  const float* res = nullptr) {
   GemmProblem pr{x, ldx_of(d), 1, nullptr, d->K, 1, (int)d->M, (int)d->N, (int)d->K};
   set_weight_operand(d, W, pr);
   pr.a_bf16 = x_bf16(d) ? 1 : 0;
@@ -245,6 +246,7 @@ of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, co
   ea.ldo = ldy_of(d);
   if (y_bf16(d)) ea.yb = reinterpret_cast<uint16_t*>(y);
   else ea.out = y;
+  ea.res = res; ea.ldr = ldy_of(d);
   ea.z = z; ea.ldz = ldy_of(d);
   ea.act = d->act;
   ea.bias = d->has_bias ? b : nullptr;
@@ -391,11 +393,27 @@ of_status of_linear_fwd(const of_linear_desc* d, const float* x, const of_param*
   return of_linear_fwd_carry(d, x, W, b, z, y, nullptr, ws, ws_bytes, stream);
 }
 
-of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_param* W,
-                              const float* b, float* z, float* y, const of_carry* next,
-                              void* ws, size_t ws_bytes, void* stream) {
+namespace {
+// of_linear_fwd_carry and of_linear_fwd_res (res: residual or NULL).
+of_status fwd_entry(const of_linear_desc* d, const float* x, const of_param* W, const float* b,
+                    const float* res, float* z, float* y, const of_carry* next, void* ws,
+                    size_t ws_bytes, void* stream) {
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
+  if (res) {
+    // read once per element by the thread that writes it: in place is safe,
+    // any other overlap with y or z is not
+    const int64_t bytes = (d->M - 1) * ldy_of(d) * 4 + d->N * 4;
+    const int64_t ybytes = (d->M - 1) * ldy_of(d) * (y_bf16(d) ? 2 : 4) + d->N * (y_bf16(d) ? 2 : 4);
+    auto apart = [&](const void* o, int64_t ob) {
+      const uintptr_t a = (uintptr_t)res, c = (uintptr_t)o;
+      return o == nullptr || a + (uintptr_t)bytes <= c || c + (uintptr_t)ob <= a;
+    };
+    REQUIRE(al4(res), OF_EALIGN, "res must be 4-byte aligned");
+    REQUIRE((res == y && !y_bf16(d)) || apart(y, ybytes), OF_EINVAL,
+            "res must be y itself (fp32 Y) or not overlap it");
+    REQUIRE(apart(z, bytes), OF_EINVAL, "res must not overlap z");
+  }
   REQUIRE(x && W && W->w && y, OF_EINVAL, "x, W, W->w and y are required");
   REQUIRE(W->numel == d->N * d->K, OF_EINVAL, "W->numel must be N*K");
   REQUIRE(!d->has_bias || b, OF_EINVAL, "has_bias is set but b is NULL");
@@ -411,7 +429,21 @@ of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_
   if ((st = check_ws(d, EPI_FWD, ws, ws_bytes)) != OF_OK) return st;
   CarryArgs carry;
   if ((st = make_carry(next, &carry)) != OF_OK) return st;
-  return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream, next ? &carry : nullptr);
+  return run_fwd(d, x, W, b, z, y, ws, (hipStream_t)stream, next ? &carry : nullptr, res);
+}
+}  // namespace
+
+of_status of_linear_fwd_carry(const of_linear_desc* d, const float* x, const of_param* W,
+                              const float* b, float* z, float* y, const of_carry* next,
+                              void* ws, size_t ws_bytes, void* stream) {
+  return fwd_entry(d, x, W, b, nullptr, z, y, next, ws, ws_bytes, stream);
+}
+
+of_status of_linear_fwd_res(const of_linear_desc* d, const float* x, const of_param* W,
+                            const float* b, const float* res, float* z, float* y,
+                            const of_carry* next, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(res != nullptr, OF_EINVAL, "res is required (of_linear_fwd_carry has none)");
+  return fwd_entry(d, x, W, b, res, z, y, next, ws, ws_bytes, stream);
 }
 
 // Largest M whose forward-fusion can write its update in place: the M rows

@@ -190,13 +190,17 @@ class LinearOp:
             return 0
         return L.of_linear_workspace_size(self.desc, which)
 
-    def fwd(self, tr, x, y, z=None, carry=None):
-        if carry is None:
-            L.of_linear_fwd(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z, y,
-                            *tr.ws_main_args(), tr._s())
+    def fwd(self, tr, x, y, z=None, carry=None, res=None):
+        """y = act(x W^T + b) (+ res, a residual connection added in the epilogue)."""
+        b = _ptr(self.b.w) if self.b else None
+        if res is not None:
+            L.of_linear_fwd_res(self.desc, x, self.W.p, b, res, z, y, carry, *tr.ws_main_args(),
+                                tr._s())
+        elif carry is None:
+            L.of_linear_fwd(self.desc, x, self.W.p, b, z, y, *tr.ws_main_args(), tr._s())
         else:
-            L.of_linear_fwd_carry(self.desc, x, self.W.p, _ptr(self.b.w) if self.b else None, z,
-                                  y, carry, *tr.ws_main_args(), tr._s())
+            L.of_linear_fwd_carry(self.desc, x, self.W.p, b, z, y, carry, *tr.ws_main_args(),
+                                  tr._s())
 
     def two_sets(self):
         """Whether this operator's prologue alternates two parameter buffer sets."""
@@ -708,8 +712,8 @@ class TBlockNet:
             return torch.empty(shape, **act)
 
         for blk in self.blocks:
-            blk.update(a=ta(M, d), mu1=t(M), rs1=t(M), qkv_out=ta(M, 3 * d), o=t(M, d), h=t(M, d),
-                       c=ta(M, d), mu2=t(M), rs2=t(M), u=t(M, f), g=ta(M, f), w=t(M, d), y=t(M, d),
+            blk.update(a=ta(M, d), mu1=t(M), rs1=t(M), qkv_out=ta(M, 3 * d), h=t(M, d),
+                       c=ta(M, d), mu2=t(M), rs2=t(M), u=t(M, f), g=ta(M, f), y=t(M, d),
                        gy=t(M, d), gu=t(M, f), gc=t(M, d), gh=t(M, d), ga=t(M, d),
                        # the Q and K thirds of the QKV gradient stay zero
                        gqkv=torch.zeros((M, 3 * d), **f32))
@@ -724,7 +728,6 @@ class TBlockNet:
 
     def forward(self, x, fused):
         tr = self.tr
-        d, n = self.d, self.M * self.d
         xin = x.data_ptr()
         order = [(b, name) for b in range(len(self.blocks))
                  for name in ("ln1", "qkv", "proj", "ln2", "fc1", "fc2")]
@@ -756,27 +759,21 @@ class TBlockNet:
                 op.fwd(tr, xin, blk["a"].data_ptr(), blk["mu1"].data_ptr(), blk["rs1"].data_ptr())
             elif name == "qkv":
                 op.fwd(tr, blk["a"].data_ptr(), blk["qkv_out"].data_ptr(), carry=carry)
-            elif name == "proj":
-                op.fwd(tr, self._v(blk), blk["o"].data_ptr(), carry=carry)
+            elif name == "proj":     # h = x + attention output (residual in the epilogue)
+                op.fwd(tr, self._v(blk), blk["h"].data_ptr(), carry=carry, res=xin)
             elif name == "ln2":
                 op.fwd(tr, blk["h"].data_ptr(), blk["c"].data_ptr(), blk["mu2"].data_ptr(),
                        blk["rs2"].data_ptr())
             elif name == "fc1":
                 op.fwd(tr, blk["c"].data_ptr(), blk["g"].data_ptr(), blk["u"].data_ptr(),
                        carry=carry)
-            else:
-                op.fwd(tr, blk["g"].data_ptr(), blk["w"].data_ptr(), carry=carry)
+            else:                    # y = h + MLP output, the next block's input
+                op.fwd(tr, blk["g"].data_ptr(), blk["y"].data_ptr(), carry=carry,
+                       res=blk["h"].data_ptr())
             tr._t1("fwd", tr.stream)
             for o in carried:
                 o.updated = True     # their updates are enqueued with this launch
-            if name == "proj":       # h = x + attention output
-                tr._t0("add", tr.stream)
-                L.of_add(xin, blk["o"].data_ptr(), n, blk["h"].data_ptr(), tr._s())
-                tr._t1("add", tr.stream)
-            elif name == "fc2":      # y = h + MLP output, the next block's input
-                tr._t0("add", tr.stream)
-                L.of_add(blk["h"].data_ptr(), blk["w"].data_ptr(), n, blk["y"].data_ptr(), tr._s())
-                tr._t1("add", tr.stream)
+            if name == "fc2":
                 xin = blk["y"].data_ptr()
 
     def _block_in(self, k, x):
@@ -944,8 +941,9 @@ class MBNet:
                 self.ops += [blk["dw"], blk["project"]]
                 blk["d"] = torch.empty((N, ho, ho, hid), **f32)
                 blk["gd"] = torch.empty((N, ho, ho, hid), **f32)
-                blk["p"] = torch.empty((N * ho * ho, c), **f32)
-                blk["y"] = torch.empty((N * ho * ho, c), **f32) if blk["residual"] else blk["p"]
+                # the block output; with a residual connection the projection's
+                # epilogue adds the block input to it
+                blk["y"] = torch.empty((N * ho * ho, c), **f32)
                 blk["gy"] = torch.empty((N * ho * ho, c), **f32)   # grad of the block output
                 self.blocks.append(blk)
                 cin, h = c, ho
@@ -971,12 +969,12 @@ class MBNet:
                 self.io[id(blk["dw"])] = (blk["e"], blk["d"])
             else:
                 self.io[id(blk["dw"])] = (cur, blk["d"])
-            self.io[id(blk["project"])] = (blk["d"], blk["p"])
+            self.io[id(blk["project"])] = (blk["d"], blk["y"])
             cur = blk["y"]
         self.io[id(self.head)] = (cur, self.hh)
         self.io[id(self.fc)] = (self.pool, self.out)
-        # the blocks whose projection is followed by the residual add
-        self.residual_after = {id(b["project"]): b for b in self.blocks if b["residual"]}
+        # the blocks whose projection adds the block input (residual connection)
+        self.residual_of = {id(b["project"]): b for b in self.blocks if b["residual"]}
 
     def _carry(self, i, fused):
         """Pending updates the forward launch of operator i carries: the next
@@ -1013,16 +1011,12 @@ class MBNet:
                 op.fwd(tr, src.data_ptr(), dst.data_ptr())
             else:
                 src, dst = self.io[id(op)]
-                op.fwd(tr, src.data_ptr(), dst.data_ptr(), carry=carry)
+                blk = self.residual_of.get(id(op))
+                op.fwd(tr, src.data_ptr(), dst.data_ptr(), carry=carry,
+                       res=blk["x"].data_ptr() if blk is not None else None)
             tr._t1("fwd", tr.stream)
             for o in carried:
                 o.updated = True     # their updates are enqueued with this launch
-            blk = self.residual_after.get(id(op))
-            if blk is not None:
-                tr._t0("fwd", tr.stream)
-                L.of_add(blk["x"].data_ptr(), blk["p"].data_ptr(), blk["p"].numel(),
-                         blk["y"].data_ptr(), s)
-                tr._t1("fwd", tr.stream)
             if op is self.head:
                 tr._t0("fwd", tr.stream)
                 L.of_avgpool_fwd(self.hh.data_ptr(), self.N, self.hf * self.hf,

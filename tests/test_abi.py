@@ -456,3 +456,27 @@ def test_bf16_activation_storage_validation(lib):
     # forward-fusion and the merged backward take fp32 operands only
     assert _status(L.of_linear_fwd_fused, _desc(io=xb), FAKE, W, None, FAKE, None, None, None,
                    opt, None, FAKE, None, 0, None) == L.OF_EINVAL
+
+
+def test_linear_fwd_res_validation(lib):
+    """of_linear_fwd_res: the residual is required, 4-byte aligned, and either y
+    itself (fp32 Y) or apart from y and z."""
+    W = _param(16 * 12)
+    Ws = L.OfParam(FAKE, FAKE, FAKE, FAKE, 16 * 12)
+    d = _desc()                     # M 8, N 16: y spans 512 bytes
+    Y = FAKE + 8192
+
+    def st(desc, res, z, y, w=W):
+        return _status(L.of_linear_fwd_res, desc, FAKE, w, None, res, z, y, None, None, 0, None)
+
+    assert st(d, None, None, Y) == L.OF_EINVAL
+    assert "res" in L.of_last_error()
+    assert st(d, Y + 2 + 4096, None, Y) == L.OF_EALIGN
+    assert st(d, Y + 64, None, Y) == L.OF_EINVAL            # overlaps y, not in place
+    assert st(d, Y - 64, None, Y) == L.OF_EINVAL
+    assert st(d, Y + 4096, Y + 4096 + 256, Y) == L.OF_EINVAL   # overlaps z
+    # bf16 Y cannot be updated in place from an fp32 residual
+    db = _desc(dtype=L.OF_BF16, io=L.OF_IO_Y_BF16)
+    assert st(db, Y, None, Y, Ws) == L.OF_EINVAL
+    # otherwise the usual checks apply
+    assert st(d, Y + 4096, None, None) == L.OF_EINVAL        # y required
