@@ -506,7 +506,9 @@ def hbm_ceiling(torch, nbytes=1 << 30, reps=20):
     nbytes written; rmw3: three arrays of a third each, updated side by side as
     W, m and v are), GB/s of bytes moved: the best over launches of 2048, 16384
     and 65535 workgroups (measured on MI355X: many short-lived workgroups
-    reach 6.1 TB/s read-modify-write where 2048 grid-striding ones reach 5.4)."""
+    reach 6.1 TB/s read-modify-write where 2048 grid-striding ones reach 5.4).
+    rmw3_columns: three 8192 x 8192 arrays in the merged backward kernel's
+    4-byte column layout and grid (its own streaming ceiling)."""
     from paper_2104_00237_amd import _lib as L
     n = nbytes // 4
     src = torch.ones(n, device="cuda:0")
@@ -514,12 +516,17 @@ def hbm_ceiling(torch, nbytes=1 << 30, reps=20):
     s = torch.cuda.current_stream()
     out = {}
     n3 = n // 12 * 12
+    chunk = 3 * 8192 * 32
+    ncol = min(3 * 8192 * 8192, n // chunk * chunk)
     for name, mode, cnt, moved in (("read_GBps", L.OF_STREAM_READ, n, nbytes),
                                    ("copy_GBps", L.OF_STREAM_COPY, n, 2 * nbytes),
                                    ("rmw_GBps", L.OF_STREAM_RMW, n, 2 * nbytes),
-                                   ("rmw3_GBps", L.OF_STREAM_RMW3, n3, 8 * n3)):
+                                   ("rmw3_GBps", L.OF_STREAM_RMW3, n3, 8 * n3),
+                                   ("rmw3_columns_GBps", L.OF_STREAM_RMW3_COLUMNS, ncol, 8 * ncol)):
+        if cnt <= 0:
+            continue
         best = 0.0
-        for blocks in (2048, 16384, 65535):
+        for blocks in ((0,) if mode == L.OF_STREAM_RMW3_COLUMNS else (2048, 16384, 65535)):
             for _ in range(3):
                 L.of_hbm_stream(mode, src.data_ptr(), dst.data_ptr(), cnt, blocks, s.cuda_stream)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -814,6 +821,9 @@ def main():
         roof["frac_of_measured_copy_rate"] = round(roof["achieved"] / ceil["copy_GBps"], 4)
         roof["frac_of_measured_rmw_rate"] = round(roof["achieved"] / ceil["rmw_GBps"], 4)
         roof["frac_of_measured_rmw3_rate"] = round(roof["achieved"] / ceil["rmw3_GBps"], 4)
+        if "rmw3_columns_GBps" in ceil:
+            roof["frac_of_measured_rmw3_columns_rate"] = round(
+                roof["achieved"] / ceil["rmw3_columns_GBps"], 4)
     for name in [w for w in args.extra_workloads.split(",") if w and w != args.workload]:
         out.setdefault("extra_workloads", {})[name] = extra_workload(torch, name, args.steps,
                                                                      args.warmup)

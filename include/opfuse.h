@@ -692,10 +692,17 @@ of_status of_mse_fwd_bwd(const float* y, const float* t, int64_t M, int64_t D, i
  * ceiling beside the published peak for the kernels that stream parameters
  * and optimizer state.  src, dst: n floats of device memory, 16-byte aligned
  * (dst: 4-byte aligned for a read), n a positive multiple of 4; blocks:
- * workgroups of 256 threads (0: 2048).  Errors: OF_EINVAL, OF_EALIGN before
- * any launch.
+ * workgroups of 256 threads (0: 2048).
+ * OF_STREAM_RMW3_COLUMNS: as OF_STREAM_RMW3 (n a multiple of 3 * 8192 * 32:
+ * three arrays of rows of 8192 floats in whole 32-row chunks), but in the
+ * access pattern of of_linear_bwd_merged's W, m, v: 4-byte accesses, a
+ * workgroup per 128 columns of a range of rows (at most 8 ranges), a lane
+ * per column holding 16 rows of each 32-row chunk in the layout of a 32 x 32
+ * fp32 MFMA accumulator; `blocks` is ignored.  That kernel's streaming
+ * ceiling.  Errors: OF_EINVAL, OF_EALIGN before any launch.
  */
-enum { OF_STREAM_READ = 0, OF_STREAM_COPY = 1, OF_STREAM_RMW = 2, OF_STREAM_RMW3 = 3 };
+enum { OF_STREAM_READ = 0, OF_STREAM_COPY = 1, OF_STREAM_RMW = 2, OF_STREAM_RMW3 = 3,
+       OF_STREAM_RMW3_COLUMNS = 4 };
 of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
                         void* stream);
 

@@ -51,7 +51,7 @@ class OfCarry(ctypes.Structure):
 
 
 OF_CLIP_WS_BYTES = 2048
-OF_STREAM_READ, OF_STREAM_COPY, OF_STREAM_RMW, OF_STREAM_RMW3 = 0, 1, 2, 3
+OF_STREAM_READ, OF_STREAM_COPY, OF_STREAM_RMW, OF_STREAM_RMW3, OF_STREAM_RMW3_COLUMNS = 0, 1, 2, 3, 4
 OF_MERGED_STATIC_SCRATCH_BYTES = 32 << 20   # of_linear_bwd_merged_static's buffer per device
 
 

@@ -670,10 +670,13 @@ of_status of_linear_bwd_merged_static(const of_linear_desc* d, const float* dz, 
 of_status of_hbm_stream(int32_t mode, const float* src, float* dst, int64_t n, int32_t blocks,
                         void* stream) {
   REQUIRE(mode == OF_STREAM_READ || mode == OF_STREAM_COPY || mode == OF_STREAM_RMW ||
-              mode == OF_STREAM_RMW3,
-          OF_EINVAL, "mode %d is not OF_STREAM_READ, OF_STREAM_COPY, OF_STREAM_RMW or OF_STREAM_RMW3",
-          (int)mode);
-  const bool rmw = mode == OF_STREAM_RMW || mode == OF_STREAM_RMW3;
+              mode == OF_STREAM_RMW3 || mode == OF_STREAM_RMW3_COLUMNS,
+          OF_EINVAL, "mode %d is not an OF_STREAM_* mode", (int)mode);
+  const bool rmw = mode == OF_STREAM_RMW || mode == OF_STREAM_RMW3 ||
+                   mode == OF_STREAM_RMW3_COLUMNS;
+  REQUIRE(mode != OF_STREAM_RMW3_COLUMNS || (n > 0 && n % (3LL * 8192 * 32) == 0), OF_EINVAL,
+          "OF_STREAM_RMW3_COLUMNS: n must be a positive multiple of 3 * 8192 * 32 (three "
+          "arrays of whole 32-row chunks of 8192-float rows; got %lld)", (long long)n);
   REQUIRE(dst && (src || rmw), OF_EINVAL,
           "dst is required, and src unless the mode is a read-modify-write");
   REQUIRE(n >= 4 && n % 4 == 0, OF_EINVAL, "n must be a positive multiple of 4 (got %lld)",

@@ -1,6 +1,7 @@
 // HBM streaming probes: the read, copy and in-place read-modify-write rates
 // (one array, or three updated side by side)
-// this device achieves with plain coalesced 128-bit accesses.  They give the achievable ceiling
+// this device achieves with plain coalesced 128-bit accesses, and the
+// three-array rate in the 4-byte column layout of the merged backward kernel.  They give the achievable ceiling
 // that the parameter-bound kernels (the fused and merged updates, which
 // stream W and the optimizer state once) are measured against, beside the
 // published 8 TB/s.  Not part of the paper's method.
@@ -9,6 +10,8 @@
 // so a workgroup of 256 threads has UNROLL * 4 KiB in flight; the grid strides
 // over the buffer.  Loads and stores are non-temporal: the data is touched
 // once and should not displace anything in the caches.
+
+#include <algorithm>
 
 #include "common.h"
 
@@ -115,8 +118,51 @@ __global__ __launch_bounds__(256) void stream_rmw3_kernel(v4f* __restrict__ a, i
 
 }  // namespace
 
+// Three arrays of rows of kColRow floats, read and written in 4-byte accesses
+// in the layout of a 32 x 32 fp32 MFMA accumulator: a workgroup owns 128
+// columns (4 wavefronts x 32) of a range of rows, walked in chunks of 32 rows;
+// a lane holds its column at rows 8 j + 4 h + e (j, e < 4; h: the wavefront
+// half).  This is how the merged backward kernel moves W, m and v, so its rate
+// is that kernel's streaming ceiling.
+constexpr int kColRow = 8192;
+
+__device__ __forceinline__ int col_acc_row(int i, int h) { return (i >> 2) * 8 + h * 4 + (i & 3); }
+
+__global__ __launch_bounds__(256) void stream_rmw3_columns_kernel(float* __restrict__ a,
+                                                                  int64_t rows, int nr) {
+  float* __restrict__ b = a + rows * kColRow;
+  float* __restrict__ c = b + rows * kColRow;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const int64_t col = (int64_t)blockIdx.x * 128 + (threadIdx.x >> 6) * 32 + (lane & 31);
+  const int64_t r0 = (int64_t)blockIdx.y * nr;
+  const int64_t r1 = r0 + nr < rows ? r0 + nr : rows;
+  for (int64_t n0 = r0; n0 < r1; n0 += 32) {   // rows is a multiple of 32
+    float va[16], vb[16], vc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t o = (n0 + col_acc_row(i, h)) * kColRow + col;
+      va[i] = a[o]; vb[i] = b[o]; vc[i] = c[o];
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t o = (n0 + col_acc_row(i, h)) * kColRow + col;
+      a[o] = va[i] + 1.f; b[o] = vb[i] + 1.f; c[o] = vc[i] + 1.f;
+    }
+  }
+}
+
 hipError_t hbm_stream_launch(int mode, const float* src, float* dst, int64_t n, int blocks,
                              hipStream_t stream) {
+  if (mode == 4) {
+    // the merged kernel's grid: 64 column strips x up to 8 row ranges
+    const int64_t rows = n / 3 / kColRow;
+    const int64_t chunks = rows / 32;
+    const int ranges = (int)std::min<int64_t>(8, chunks);
+    const int nr = (int)((chunks + ranges - 1) / ranges) * 32;
+    hipLaunchKernelGGL(stream_rmw3_columns_kernel, dim3(kColRow / 128, ranges), dim3(256), 0,
+                       stream, dst, rows, nr);
+    return hipGetLastError();
+  }
   const int64_t n4 = n / 4;
   if (blocks <= 0) blocks = 2048;  // 8 workgroups per compute unit
   if (mode == 0)

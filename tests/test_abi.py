@@ -348,7 +348,15 @@ def test_avgpool_validation(lib):
 def test_hbm_stream_validation(lib):
     """The streaming probe: modes, required pointers and alignment are checked
     before any launch; the read-modify-write mode takes no source."""
-    assert _status(L.of_hbm_stream, 4, FAKE, FAKE, 1024, 0, None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, 5, FAKE, FAKE, 1024, 0, None) == L.OF_EINVAL
+    # the merged kernel's layout: whole 32-row chunks of 8192-float rows, three arrays
+    col = 3 * 8192 * 32
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3_COLUMNS, None, FAKE, 1024, 0,
+                   None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3_COLUMNS, None, FAKE, col + 12, 0,
+                   None) == L.OF_EINVAL
+    assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3_COLUMNS, None, FAKE + 4, col, 0,
+                   None) == L.OF_EALIGN
     # three arrays of float4s: n a multiple of 12
     assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3, None, FAKE, 1024, 0, None) == L.OF_EINVAL
     assert _status(L.of_hbm_stream, L.OF_STREAM_RMW3, None, FAKE + 4, 1032, 0,

@@ -415,3 +415,20 @@ def test_hbm_stream_probes(env, n, blocks):
     L.of_hbm_stream(L.OF_STREAM_READ, src.data_ptr(), sink.data_ptr(), n, blocks, 0)
     torch.cuda.synchronize()
     assert int((sink != -1.0).sum()) <= 1
+
+
+@pytest.mark.parametrize("chunks", [1, 10, 256])
+def test_hbm_stream_columns_probe(env, chunks):
+    """The merged kernel's access pattern as a probe: three arrays of rows of 8192
+    floats, chunks of 32 rows in at most 8 row ranges (10 chunks: ranges of 2,
+    the last ones empty); two passes add 2 to every element and nothing else."""
+    torch, L, dev = env
+    n = 3 * 8192 * 32 * chunks
+    src = torch.arange(n, dtype=torch.float32, device=dev) % 1000
+    pad = torch.full((n + 64,), -7.0, device=dev)
+    pad[:n] = src
+    for _ in range(2):
+        L.of_hbm_stream(L.OF_STREAM_RMW3_COLUMNS, None, pad.data_ptr(), n, 0, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(pad[:n], src + 2)
+    assert bool((pad[n:] == -7.0).all())
