@@ -298,6 +298,20 @@ of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_
                              size_t ws_bytes, void* stream);
 
 /*
+ * of_linear_bwd_data with the gradient of a skip connection added in the
+ * epilogue: dX = (dZ W_old) * act_prev'(prev) + R (R is not multiplied by the
+ * activation's derivative: the skip connection bypasses it), e.g. the input
+ * gradient of an inverted-residual block, whose input also feeds the block's
+ * output.  Rounded once, so equal bit for bit to of_linear_bwd_data followed
+ * by of_add.  res: [M, ldx] fp32, required, 4-byte aligned; it may be dx
+ * itself and must not overlap it otherwise.  Backward-fusion pairs it with
+ * of_linear_bwd_fused with dx_prev == NULL (the update only).
+ */
+of_status of_linear_bwd_data_res(const of_linear_desc* d, const float* dz, const of_param* W,
+                                 const float* prev, int32_t act_prev, const float* res,
+                                 float* dx, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Eager weight gradient (Fig. 1(b); the gradient is materialised and later
  * read and reset by the optimizer, Section 3 "Baseline"):
  *   dW = dZ^T X [N,K],  db = sum over rows of dZ [N] (db may be NULL).

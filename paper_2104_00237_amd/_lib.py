@@ -94,6 +94,9 @@ _SIGS = {
                                       c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "of_linear_bwd_data": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p, c_int32,
                                      c_void_p, c_void_p, c_size_t, c_void_p]),
+    "of_linear_bwd_data_res": (c_int32, [P(OfLinearDesc), c_void_p, P(OfParam), c_void_p,
+                                         c_int32, c_void_p, c_void_p, c_void_p, c_size_t,
+                                         c_void_p]),
     "of_linear_bwd_weight": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_int32, c_void_p, c_size_t, c_void_p]),
     "of_linear_bwd_fused": (c_int32, [P(OfLinearDesc), c_void_p, c_void_p, P(OfParam),
@@ -222,7 +225,7 @@ def of_layernorm_partial_rows(M):
     return load().of_layernorm_partial_rows(M)
 
 
-for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_linear_fwd_res", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_weight",
+for _n in ("of_linear_fwd", "of_linear_fwd_carry", "of_linear_fwd_res", "of_conv_fwd_carry", "of_linear_fwd_fused", "of_linear_bwd_data", "of_linear_bwd_data_res", "of_linear_bwd_weight",
            "of_linear_bwd_fused", "of_linear_bwd_merged", "of_linear_bwd_merged_static",
            "of_hbm_stream", "of_elementwise_fused_update", "of_optimizer_step",
            "of_step_advance", "of_grad_clip_scale", "of_xent_fwd_bwd", "of_mse_fwd_bwd", "of_conv_fwd",

@@ -279,7 +279,7 @@ struct EpiArgs {
   float* out; int64_t ldo;      // y (FWD), dx (DGRAD), dw (WGRAD)
   float* z; int64_t ldz;        // FWD: pre-activation (optional)
   uint16_t* yb;                 // FWD (bf16 kernels): y stored as bf16 here, out unused
-  const float* res; int64_t ldr;   // FWD: residual added to y (may be NULL)
+  const float* res; int64_t ldr;   // FWD: added to y; DGRAD: added to dx (may be NULL)
   const float* prev; int64_t ldp;  // DGRAD: saved tensor of the previous layer
   int act;                      // FWD: activation; DGRAD: previous layer's activation
   int accumulate;               // WGRAD

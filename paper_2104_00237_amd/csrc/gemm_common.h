@@ -142,8 +142,9 @@ inline int carry_slices(const CarryArgs& c, int64_t slice) {
 // ----------------------------------------------------------------- epilogues
 // c[0..n) are the results for (p, q..q+n-1).  vec: 128-bit memory paths allowed
 // (bit 0: out/z/prev/res, bit 1: parameter arrays); only used when n == 4.
-// A forward's residual R (ea.res) is added last, Y + R rounded once: the value
-// a separate element-wise addition of the two stored tensors gives.
+// A residual R (ea.res: a forward's skip connection, or the gradient a data
+// gradient's skip connection adds) is added last, rounded once: the value a
+// separate element-wise addition of the two stored tensors gives.
 template <int EPI>
 __device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const float (&c)[4],
                                          int n, const float* bias, int vec) {
@@ -174,6 +175,7 @@ __device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const 
     }
   } else if (EPI == EPI_DGRAD) {
     const int64_t oo = (int64_t)p * ea.ldo + q, op = (int64_t)p * ea.ldp + q;
+    const int64_t orr = (int64_t)p * ea.ldr + q;
     if (n == 4 && (vec & 1)) {
       float4 r = make_float4(c[0], c[1], c[2], c[3]);
       if (ea.act != OF_ACT_NONE) {
@@ -183,11 +185,17 @@ __device__ __forceinline__ void epilogue(const EpiArgs& ea, int p, int q, const 
         r.z = __fmul_rn(r.z, act_grad(ea.act, s.z));
         r.w = __fmul_rn(r.w, act_grad(ea.act, s.w));
       }
+      if (ea.res) {
+        const float4 t = ld4(ea.res + orr);
+        r.x = __fadd_rn(r.x, t.x); r.y = __fadd_rn(r.y, t.y);
+        r.z = __fadd_rn(r.z, t.z); r.w = __fadd_rn(r.w, t.w);
+      }
       st4(ea.out + oo, r);
     } else {
       for (int e = 0; e < n; ++e) {
         float r = c[e];
         if (ea.act != OF_ACT_NONE) r = __fmul_rn(r, act_grad(ea.act, ea.prev[op + e]));
+        if (ea.res) r = __fadd_rn(r, ea.res[orr + e]);
         ea.out[oo + e] = r;
       }
     }

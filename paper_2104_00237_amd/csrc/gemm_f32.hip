@@ -380,7 +380,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   constexpr int NPF = (PREF_BF || PREF_DG) ? EPT : 1;
   float4 pf_w[NPF], pf_m[NPF], pf_v[NPF];
   const bool pref = (PREF_BF && S == 1 && (vec_epi & 2) && ea.gW == nullptr) ||
-                    (PREF_DG && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE);
+                    (PREF_DG && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE &&
+                     ea.res == nullptr);
   auto prefetch = [&]() {
     if constexpr (PREF_BF || PREF_DG) {
       if (pref) {
@@ -721,7 +722,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, Ep
   // Epilogue item of thread tid < 256: row ep, columns eq .. eq+3 of the block.
   // The data gradient loads its saved tensor (for act') before the main loop.
   const int ep = tid >> 3, eq = (tid & 7) * 4;
-  const bool pref = EPI == EPI_DGRAD && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE;
+  const bool pref = EPI == EPI_DGRAD && S == 1 && (vec_epi & 1) && ea.act != OF_ACT_NONE &&
+                    ea.res == nullptr;
   float4 pf = make_float4(0.f, 0.f, 0.f, 0.f);
   if (pref) {
     const bool ok = tid < 256 && ep < np && eq + 3 < nq;

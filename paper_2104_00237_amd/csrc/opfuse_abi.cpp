@@ -255,7 +255,8 @@ of_status run_fwd(const of_linear_desc* d, const float* x, const of_param* W, co
 }
 
 of_status run_dgrad(const of_linear_desc* d, const float* dz, const of_param* W, const float* prev,
-                    int32_t act_prev, float* dx, void* ws, hipStream_t s) {
+                    int32_t act_prev, float* dx, void* ws, hipStream_t s,
+                    const float* res = nullptr) {
   // dX[m,k] = sum_n dZ[m,n] W[n,k]: A = dZ (reduction-contiguous), B(k, n) = W[n*K + k].
   GemmProblem pr{dz, ldy_of(d), 1, nullptr, 1, d->K, (int)d->M, (int)d->K, (int)d->N};
   set_weight_operand(d, W, pr);
@@ -263,6 +264,7 @@ of_status run_dgrad(const of_linear_desc* d, const float* dz, const of_param* W,
   ea.out = dx; ea.ldo = ldx_of(d);
   ea.prev = prev; ea.ldp = ldx_of(d);
   ea.act = act_prev;
+  ea.res = res; ea.ldr = ldx_of(d);
   return hip_status(gemm_dispatch(d, EPI_DGRAD, pr, ea, ws, s), "dgrad launch");
 }
 
@@ -511,11 +513,21 @@ of_status of_linear_fwd_fused(const of_linear_desc* d, const float* x, const of_
                     "of_linear_fwd_fused launch");
 }
 
-of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_param* W,
-                             const float* prev, int32_t act_prev, float* dx, void* ws,
-                             size_t ws_bytes, void* stream) {
+namespace {
+// of_linear_bwd_data and of_linear_bwd_data_res (res: residual gradient or NULL).
+of_status bwd_data_entry(const of_linear_desc* d, const float* dz, const of_param* W,
+                         const float* prev, int32_t act_prev, const float* res, float* dx,
+                         void* ws, size_t ws_bytes, void* stream) {
   of_status st = check_linear(d);
   if (st != OF_OK) return st;
+  if (res) {
+    // read once per element by the thread that writes it: in place is safe
+    const int64_t bytes = ((d->M - 1) * ldx_of(d) + d->K) * 4;
+    const uintptr_t a = (uintptr_t)res, c = (uintptr_t)dx;
+    REQUIRE(al4(res), OF_EALIGN, "res must be 4-byte aligned");
+    REQUIRE(res == dx || dx == nullptr || a + (uintptr_t)bytes <= c || c + (uintptr_t)bytes <= a,
+            OF_EINVAL, "res must be dx itself or not overlap it");
+  }
   REQUIRE(dz && W && W->w && dx, OF_EINVAL, "dz, W, W->w and dx are required");
   REQUIRE(W->numel == d->N * d->K, OF_EINVAL, "W->numel must be N*K");
   if ((st = check_act_prev(act_prev, prev)) != OF_OK) return st;
@@ -523,7 +535,21 @@ of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_
   REQUIRE((((uintptr_t)W->w_bf16) & 1u) == 0, OF_EALIGN, "W->w_bf16 must be 2-byte aligned");
   if ((st = check_shadow(d, W)) != OF_OK) return st;
   if ((st = check_ws(d, EPI_DGRAD, ws, ws_bytes)) != OF_OK) return st;
-  return run_dgrad(d, dz, W, prev, act_prev, dx, ws, (hipStream_t)stream);
+  return run_dgrad(d, dz, W, prev, act_prev, dx, ws, (hipStream_t)stream, res);
+}
+}  // namespace
+
+of_status of_linear_bwd_data(const of_linear_desc* d, const float* dz, const of_param* W,
+                             const float* prev, int32_t act_prev, float* dx, void* ws,
+                             size_t ws_bytes, void* stream) {
+  return bwd_data_entry(d, dz, W, prev, act_prev, nullptr, dx, ws, ws_bytes, stream);
+}
+
+of_status of_linear_bwd_data_res(const of_linear_desc* d, const float* dz, const of_param* W,
+                                 const float* prev, int32_t act_prev, const float* res,
+                                 float* dx, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(res != nullptr, OF_EINVAL, "res is required (of_linear_bwd_data has none)");
+  return bwd_data_entry(d, dz, W, prev, act_prev, res, dx, ws, ws_bytes, stream);
 }
 
 of_status of_linear_bwd_weight(const of_linear_desc* d, const float* dz, const float* x, float* dw,

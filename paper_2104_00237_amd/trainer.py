@@ -220,9 +220,14 @@ class LinearOp:
             for p in self.params:
                 p.swap_generation()
 
-    def dgrad(self, tr, g, prev, act_prev, dx):
-        L.of_linear_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
-                             tr._s())
+    def dgrad(self, tr, g, prev, act_prev, dx, res=None):
+        """dx = (g W) * act_prev'(prev) (+ res, a skip connection's gradient)."""
+        if res is None:
+            L.of_linear_bwd_data(self.desc, g, self.W.p, prev, act_prev, dx, *tr.ws_main_args(),
+                                 tr._s())
+        else:
+            L.of_linear_bwd_data_res(self.desc, g, self.W.p, prev, act_prev, res, dx,
+                                     *tr.ws_main_args(), tr._s())
 
     def wgrad(self, tr, g, x, accumulate=0, side=False):
         """Plain weight gradient into W.g (and b.g); accumulate=1 adds to what an
@@ -251,10 +256,15 @@ class LinearOp:
                                *self._partials(partial), tr.opt, prev, act_prev, dx,
                                *tr.ws_main_args(), tr._s())
 
-    def bwd_fused(self, tr, g, x, prev, act_prev, dx, partial=False):
+    def bwd_fused(self, tr, g, x, prev, act_prev, dx, partial=False, res=None):
         """Data gradient on the main stream, then the fused update: on the side
-        stream (behind an event) or in stream order (one call)."""
+        stream (behind an event) or in stream order (one call).  res: a skip
+        connection's gradient added to dx (then the data gradient is its own
+        call, and the fused call only updates)."""
         b = self.b
+        if res is not None:
+            self.dgrad(tr, g, prev, act_prev, dx, res=res)
+            prev, act_prev, dx = None, 0, None
         L.of_linear_bwd_fused(self.desc, g, x, self.W.p, b.p if b else None,
                               *self._partials(partial), tr.opt, prev, act_prev, dx,
                               *tr.ws_main_args(), *tr.ws_side_args(), tr._s(),
@@ -1042,18 +1052,20 @@ class MBNet:
             op.wgrad(tr, dz, x)
             tr._t1("wgrad", tr.stream)
 
-    def _lin_bwd(self, op, dz, x, prev, act_prev, dx, fused, done):
+    def _lin_bwd(self, op, dz, x, prev, act_prev, dx, fused, done, dres=None):
+        """dres: the gradient of a skip connection from the layer's input, added
+        to dx in the data gradient's epilogue."""
         tr = self.tr
         if not fused:
             if dx is not None:
                 tr._t0("dgrad", tr.stream, op)
-                op.dgrad(tr, dz, prev, act_prev, dx)
+                op.dgrad(tr, dz, prev, act_prev, dx, res=dres)
                 tr._t1("dgrad", tr.stream)
             self._wgrad_plain(op, dz, x, op.overlap_update)
         elif tr.timer is not None and (tr.timer.wants("wgrad_bf") or tr.timer.wants("dgrad")):
             if dx is not None:
                 tr._t0("dgrad", tr.stream, op)
-                op.dgrad(tr, dz, prev, act_prev, dx)
+                op.dgrad(tr, dz, prev, act_prev, dx, res=dres)
                 tr._t1("dgrad", tr.stream)
             if op.overlap_update:
                 gate = _side_after_main(tr)
@@ -1066,7 +1078,7 @@ class MBNet:
                 tr._t1("wgrad_bf", tr.stream)
             done(op)
         else:
-            op.bwd_fused(tr, dz, x, prev, act_prev, dx)
+            op.bwd_fused(tr, dz, x, prev, act_prev, dx, res=dres)
             done(op)
 
     def _dw_bwd(self, op, dy, x, prev, act_prev, dx, fused, done):
@@ -1112,19 +1124,21 @@ class MBNet:
             xin = blk["x"]
             self._lin_bwd(blk["project"], P(blk["gy"]), P(blk["d"]), P(blk["d"]), relu,
                           P(blk["gd"]), fused, done)
+            # the skip connection: the block input also gets the output's gradient,
+            # added in the expand layer's data-gradient epilogue
+            skip = P(blk["gy"]) if blk["residual"] else None
             if blk["t"] != 1:
                 self._dw_bwd(blk["dw"], P(blk["gd"]), P(blk["e"]), P(blk["e"]), relu,
                              P(blk["ge"]), fused, done)
                 self._lin_bwd(blk["expand"], P(blk["ge"]), P(xin), P(xin) if in_act else None,
-                              in_act, P(gin), fused, done)
+                              in_act, P(gin), fused, done, dres=skip)
             else:
                 self._dw_bwd(blk["dw"], P(blk["gd"]), P(xin), P(xin) if in_act else None, in_act,
                              P(gin), fused, done)
-            if blk["residual"]:
-                # the skip connection: the block input also gets the output's gradient
-                tr._t0("add", tr.stream)
-                L.of_add(P(gin), P(blk["gy"]), gin.numel(), P(gin), s)
-                tr._t1("add", tr.stream)
+                if skip is not None:   # a depthwise data gradient takes no residual
+                    tr._t0("add", tr.stream)
+                    L.of_add(P(gin), skip, gin.numel(), P(gin), s)
+                    tr._t1("add", tr.stream)
         # the stem is the first layer: no data gradient
         stem = self.stem
         if fused:

@@ -488,3 +488,20 @@ def test_linear_fwd_res_validation(lib):
     assert st(db, Y, None, Y, Ws) == L.OF_EINVAL
     # otherwise the usual checks apply
     assert st(d, Y + 4096, None, None) == L.OF_EINVAL        # y required
+
+
+def test_linear_bwd_data_res_validation(lib):
+    """of_linear_bwd_data_res: the residual gradient is required, 4-byte aligned,
+    and either dx itself or apart from it."""
+    W = _param(16 * 12)
+    d = _desc()                     # M 8, K 12: dx spans 384 bytes
+    DX = FAKE + 8192
+
+    def st(res, dx):
+        return _status(L.of_linear_bwd_data_res, d, FAKE, W, None, 0, res, dx, None, 0, None)
+
+    assert st(None, DX) == L.OF_EINVAL
+    assert st(DX + 4096 + 2, DX) == L.OF_EALIGN
+    assert st(DX + 64, DX) == L.OF_EINVAL     # overlaps dx, not in place
+    assert st(DX - 64, DX) == L.OF_EINVAL
+    assert st(DX + 4096, None) == L.OF_EINVAL   # dx required

@@ -129,3 +129,50 @@ def test_forward_residual_with_carried_update(env):
 
     for a, c in zip(run(True), run(False)):
         assert np.array_equal(_bits(a), _bits(c))
+
+
+# (M, N, K, ldx): ragged tails and scalar epilogues, a strided dX, split reductions
+DG_SHAPES = [(37, 70, 53, 53), (130, 96, 44, 49), (64, 4096, 1024, 1024), (401, 96, 576, 576),
+             (2048, 2048, 1024, 1024)]
+
+
+@pytest.mark.parametrize("M,N,K,ldx", DG_SHAPES)
+@pytest.mark.parametrize("kind", ["f32", "bf16"])
+@pytest.mark.parametrize("act", ["none", "relu", "gelu"])
+def test_data_gradient_residual_equals_data_gradient_then_add(env, M, N, K, ldx, kind, act):
+    """dX = (dZ W) * act'(prev) + R equals of_linear_bwd_data followed by of_add bit
+    for bit, in a separate buffer and in place."""
+    torch, L, dev = env
+    g = torch.Generator().manual_seed(M + 3 * N + K)
+    dz = (torch.randn((M, N), generator=g) * 1e-2).to(dev)
+    w = (torch.randn((N, K), generator=g) / K ** 0.5).to(dev)
+    prev = torch.randn((M, ldx), generator=g).to(dev)
+    r = torch.randn((M, ldx), generator=g).to(dev)
+    bf16 = kind == "bf16"
+    wb = w.to(torch.bfloat16) if bf16 else None
+    a = {"none": L.OF_ACT_NONE, "relu": L.OF_ACT_RELU, "gelu": L.OF_ACT_GELU}[act]
+    d = L.OfLinearDesc(M, N, K, ldx, 0, L.OF_BF16 if bf16 else L.OF_F32, L.OF_ACT_NONE, 0, 0)
+    Wp = L.OfParam(w.data_ptr(), None, None, wb.data_ptr() if bf16 else None, w.numel())
+    ws = _ws(torch, dev, L.of_linear_workspace_size(d, L.OF_LINEAR_BWD_DATA))
+    pp = prev.data_ptr() if a != L.OF_ACT_NONE else None
+
+    D0 = torch.full((M, ldx), float("nan"), device=dev)
+    L.of_linear_bwd_data(d, dz.data_ptr(), Wp, pp, a, D0.data_ptr(), ws.data_ptr(),
+                         ws.numel() * 4, 0)
+    S0 = torch.full((M, ldx), float("nan"), device=dev)
+    if ldx == K:
+        L.of_add(D0.data_ptr(), r.data_ptr(), M * K, S0.data_ptr(), 0)
+    else:
+        for i in range(M):
+            L.of_add(D0[i].data_ptr(), r[i].data_ptr(), K, S0[i].data_ptr(), 0)
+    D1 = torch.full((M, ldx), float("nan"), device=dev)
+    L.of_linear_bwd_data_res(d, dz.data_ptr(), Wp, pp, a, r.data_ptr(), D1.data_ptr(),
+                             ws.data_ptr(), ws.numel() * 4, 0)
+    Di = r.clone()
+    L.of_linear_bwd_data_res(d, dz.data_ptr(), Wp, pp, a, Di.data_ptr(), Di.data_ptr(),
+                             ws.data_ptr(), ws.numel() * 4, 0)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(D1[:, :K]), _bits(S0[:, :K]))
+    assert np.array_equal(_bits(Di[:, :K]), _bits(S0[:, :K]))
+    if ldx > K:
+        assert bool(torch.isnan(D1[:, K:]).all())
