@@ -271,7 +271,8 @@ struct CarryTensor {
 struct CarryArgs {
   CarryTensor t[OF_CARRY_MAX];
   OptK opt;
-  int z0;               // z-slices of the contraction itself; 0: nothing carried
+  int cz;               // leading z-slices that apply the update (dispatched first,
+                        // so they run beside the contraction); 0: nothing carried
 };
 
 struct EpiArgs {
@@ -298,7 +299,7 @@ struct EpiArgs {
   const float* gb;              // FF: pending bias gradient; BF: extra bias gradient
   int with_db;                  // WGRAD: db != NULL; WGRAD_BF: b.w != NULL
   OptK opt;
-  CarryArgs carry;              // FWD: a later operator's update (carry.z0 == 0: none)
+  CarryArgs carry;              // FWD: a later operator's update (carry.cz == 0: none)
 };
 
 size_t gemm_workspace_bytes(int kind, int P, int Q, int R, int conv = 0);

@@ -253,7 +253,7 @@ __global__ __launch_bounds__(T::NT) void gemm_bf16_kernel(GemmProblem pr, EpiArg
   __shared__ __attribute__((aligned(16))) unsigned char smem_raw[T::SMX];
   uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
   if constexpr (EPI == EPI_FWD) {
-    if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+    if ((int)blockIdx.z < ea.carry.cz) {
       carry_update<T::NT>(ea.carry);  // a later operator's update rides on this launch
       return;
     }
@@ -264,7 +264,7 @@ __global__ __launch_bounds__(T::NT) void gemm_bf16_kernel(GemmProblem pr, EpiArg
   int tx, ty;
   xcd_tile(tx, ty, pr.group);
   const int p0 = tx * T::BP, q0 = ty * T::BQ;
-  const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
+  const int split = (int)blockIdx.z - ea.carry.cz, S = (int)gridDim.z - ea.carry.cz;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
@@ -631,11 +631,11 @@ hipError_t gemm_bf16_launch(int kind, const GemmProblem& pr_in, const EpiArgs& e
   if ((pr.a_bf16 && kind != EPI_FWD) || pr.conv) return hipErrorInvalidValue;
   BCfg c = bselect(kind, pr.P, pr.Q, pr.R);
   EpiArgs ea = ea_in;
-  ea.carry.z0 = 0;
+  ea.carry.cz = 0;
   if (ea.carry.t[0].p.w) {
     if (kind != EPI_FWD) return hipErrorInvalidValue;  // only a forward carries an update
     c.cz = carry_slices(ea.carry, bntiles(c.tile, pr.P, pr.Q));
-    ea.carry.z0 = c.S;
+    ea.carry.cz = c.cz;
   }
   int vec_epi = 0;
   const int vec_ops = bvec_flags(pr, kind, ea, &vec_epi);

@@ -90,8 +90,8 @@ __device__ __forceinline__ void carry_update(const CarryArgs& c) {
   OptK o = c.opt;
   opt_prepare(o);
   const int64_t slice = (int64_t)gridDim.x * gridDim.y;
-  const int64_t u = ((int64_t)(blockIdx.z - c.z0) * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
-  const int64_t U = (int64_t)(gridDim.z - c.z0) * slice;
+  const int64_t u = ((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t U = (int64_t)c.cz * slice;
   // (unrolled: the tensors are indexed statically, so the arguments stay in
   // scalar registers instead of being copied to per-lane scratch)
 #pragma unroll

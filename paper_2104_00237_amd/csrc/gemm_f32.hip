@@ -333,7 +333,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   static_assert(EPI != EPI_FWD_FF || T::PAD == 4, "the fused forward stages W with a pad of 4");
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
   if constexpr (EPI == EPI_FWD) {
-    if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+    if ((int)blockIdx.z < ea.carry.cz) {
       carry_update(ea.carry);  // a later operator's update rides on this launch
       return;
     }
@@ -344,7 +344,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmProblem pr, EpiArgs ea, i
   int tx, ty;
   xcd_tile(tx, ty);
   const int p0 = tx * T::BP, q0 = ty * T::BQ;
-  const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
+  const int split = (int)blockIdx.z - ea.carry.cz, S = (int)gridDim.z - ea.carry.cz;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int nch = (rend - rbeg + T::BR - 1) / T::BR;
@@ -704,7 +704,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, Ep
   constexpr int KB = 16;                   // reduction elements per block
   __shared__ __attribute__((aligned(16))) float Cs[NW * 32 * 32];
   if constexpr (EPI == EPI_FWD) {
-    if (ea.carry.z0 && (int)blockIdx.z >= ea.carry.z0) {
+    if ((int)blockIdx.z < ea.carry.cz) {
       carry_update(ea.carry);  // a later operator's update rides on this launch
       return;
     }
@@ -714,7 +714,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_direct_kernel(GemmProblem pr, Ep
   int tx, ty;
   xcd_tile(tx, ty);
   const int p0 = tx * 32, q0 = ty * 32;
-  const int split = blockIdx.z, S = ea.carry.z0 ? ea.carry.z0 : (int)gridDim.z;
+  const int split = (int)blockIdx.z - ea.carry.cz, S = (int)gridDim.z - ea.carry.cz;
   const int rbeg = split * r_split;
   const int rend = min(pr.R, rbeg + r_split);
   const int np = pr.P - p0, nq = pr.Q - q0;
@@ -1176,11 +1176,11 @@ hipError_t gemm_launch(int kind, const GemmProblem& pr, const EpiArgs& ea_in, vo
   // ranges and workspace).
   if (kind == EPI_FWD_FF && c.tile == TI_128x128) c.tile = TI_128x64;
   EpiArgs ea = ea_in;
-  ea.carry.z0 = 0;
+  ea.carry.cz = 0;
   if (ea.carry.t[0].p.w) {
     if (kind != EPI_FWD) return hipErrorInvalidValue;  // only a forward carries an update
     c.cz = carry_slices(ea.carry, ntiles(c.tile, pr.P, pr.Q));
-    ea.carry.z0 = c.S;
+    ea.carry.cz = c.cz;
   }
   int vec_epi = 0;
   const int vec_ops = vec_flags(pr, kind, ea, &vec_epi);
