@@ -26,6 +26,7 @@ host, timed on a bounded sample of steps.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -351,7 +352,17 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     for t in range(max(warmup, 1)):
         x, y = batches[t % n]
         tr.step(x, y, ordering)
-    timer = KernelTimer(timer_classes) if timer_classes else None
+    # events for the bracketed launches are made before the timed region (one
+    # step's bracket count, measured on an extra untimed step, times the steps)
+    timer = None
+    if timer_classes:
+        count = KernelTimer(timer_classes)
+        tr.timer = count
+        x, y = batches[max(warmup, 1) % n]
+        tr.step(x, y, ordering)
+        tr.timer = None
+        per_step = sum(len(r) for r in count.records.values())
+        timer = KernelTimer(timer_classes, pool=min(2 * per_step * (steps + 1) + 16, 60000))
     if graph and timer is None:
         runs = [tr.capture(x, y, ordering) for x, y in batches]
         for t in range(n):          # each graph once before timing
@@ -362,13 +373,18 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(tr.stream)
-    t_host = time.perf_counter()
-    for t in range(steps):
-        runs[(warmup + t) % n]()
-    e1.record(tr.stream)
-    torch.cuda.synchronize()
-    host_s = time.perf_counter() - t_host
+    gc.collect()
+    gc.disable()    # no collector pauses on the host inside the timed region
+    try:
+        e0.record(tr.stream)
+        t_host = time.perf_counter()
+        for t in range(steps):
+            runs[(warmup + t) % n]()
+        e1.record(tr.stream)
+        torch.cuda.synchronize()
+        host_s = time.perf_counter() - t_host
+    finally:
+        gc.enable()
     ms = e0.elapsed_time(e1) / steps
     losses = tr.loss_history()
     tr.timer = None

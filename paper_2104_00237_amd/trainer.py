@@ -1559,31 +1559,43 @@ class KernelTimer:
     take its timestamp before the wait is satisfied, which would add the wait
     to the kernel's time."""
 
-    def __init__(self, classes):
+    def __init__(self, classes, pool=0):
+        """pool: events created (and recorded once, which creates the HIP
+        event) up front, so that timed steps do not create events: a host
+        stall inside the timed region lets the GPU drain its queue, and the
+        wait would be counted inside the bracket being timed."""
         self.classes = set(classes)
         self.records = {c: [] for c in self.classes}
         self._open = {}
+        self._pool = [torch.cuda.Event(enable_timing=True) for _ in range(pool)]
+        for e in self._pool:
+            e.record()
+        if pool:
+            torch.cuda.synchronize()
+
+    def _event(self):
+        return self._pool.pop() if self._pool else torch.cuda.Event(enable_timing=True)
 
     def wants(self, cls):
         return cls in self.classes
 
     def start(self, cls, stream, op=None):
         if cls in self.classes:
-            e = torch.cuda.Event(enable_timing=True)
+            e = self._event()
             e.record(stream)
             self._open[cls] = (e, op)
 
     def start_after(self, cls, stream, op, gate):
         """Start a launch on `stream` that waits for `gate` (a timing event)."""
         if cls in self.classes:
-            e = torch.cuda.Event(enable_timing=True)
+            e = self._event()
             e.record(stream)
             self._open[cls] = ((gate, e), op)
 
     def stop(self, cls, stream):
         if cls in self.classes:
             e0, op = self._open.pop(cls)
-            e1 = torch.cuda.Event(enable_timing=True)
+            e1 = self._event()
             e1.record(stream)
             self.records[cls].append((e0, e1, op))
 
