@@ -373,18 +373,14 @@ def time_ordering(torch, cfg, ordering, batches, warmup, steps, timer_classes=()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    gc.collect()
-    gc.disable()    # no collector pauses on the host inside the timed region
-    try:
-        e0.record(tr.stream)
-        t_host = time.perf_counter()
-        for t in range(steps):
-            runs[(warmup + t) % n]()
-        e1.record(tr.stream)
-        torch.cuda.synchronize()
-        host_s = time.perf_counter() - t_host
-    finally:
-        gc.enable()
+    gc.collect()    # a collection now rather than inside the timed region
+    e0.record(tr.stream)
+    t_host = time.perf_counter()
+    for t in range(steps):
+        runs[(warmup + t) % n]()
+    e1.record(tr.stream)
+    torch.cuda.synchronize()
+    host_s = time.perf_counter() - t_host
     ms = e0.elapsed_time(e1) / steps
     losses = tr.loss_history()
     tr.timer = None
